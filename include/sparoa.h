@@ -1,0 +1,271 @@
+/*
+ * sparoa.h -- C ABI of libsparoa.so, the MI355X (gfx950) hot path of SparOA
+ * (arXiv 2511.19457): per-operator input-activation sparsity, operator
+ * intensity, sparsity x intensity routing, and dense / zero-skipping /
+ * bandwidth-bound conv and FC kernels.
+ *
+ * General conventions
+ *   - Every function returns sparoa_status (SPAROA_OK = 0).  On failure a
+ *     thread-local message is available from sparoa_last_error().  No C++
+ *     exception crosses this boundary.
+ *   - Memory: the caller owns every buffer.  Device pointers (suffix _dev,
+ *     and every tensor argument of the device calls) point to memory of the
+ *     current HIP device.  The library never allocates device memory;
+ *     scratch memory comes from a caller workspace sized by the
+ *     *_workspace_size queries.
+ *   - Streams: device calls are asynchronous and stream-ordered on `stream`
+ *     (NULL = the null stream).  Only *_sync calls block.  Output counters
+ *     are initialised inside the call: no caller memset is needed.
+ *   - Layout: tensors are dense row-major.  Activations NHWC
+ *     ([n][h][w][c]); conv weights [c_out][k_h][k_w][c_in/groups];
+ *     FC activations [m][k]; FC weights [n][k] (output-feature major), or the
+ *     packed layout written by sparoa_fc_pack_weights for the bandwidth
+ *     paths.  Output dtype = input dtype; accumulation is fp32.
+ *   - Alignment: tensor pointers must be 16-byte aligned; a misaligned
+ *     pointer gives SPAROA_ERR_UNSUPPORTED (never a silent slow path).
+ *   - Threading: calls are reentrant; the only global state is the
+ *     thread-local error message.  Calls on different streams may overlap.
+ */
+#ifndef SPAROA_H
+#define SPAROA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPAROA_ABI_VERSION 1u
+
+typedef enum {
+  SPAROA_OK = 0,
+  SPAROA_ERR_INVALID_ARG = 1, /* null required pointer, bad shape, 0 elements, NaN threshold */
+  SPAROA_ERR_UNSUPPORTED = 2, /* valid but not implemented: dtype/path/shape/alignment combo */
+  SPAROA_ERR_WORKSPACE = 3,   /* workspace smaller than the *_workspace_size query */
+  SPAROA_ERR_HIP = 4          /* a HIP runtime call failed; message has hipGetErrorString */
+} sparoa_status;
+
+typedef enum { SPAROA_F32 = 0, SPAROA_F16 = 1, SPAROA_BF16 = 2 } sparoa_dtype;
+
+typedef enum { SPAROA_ACT_NONE = 0, SPAROA_ACT_RELU = 1, SPAROA_ACT_RELU6 = 2 } sparoa_act;
+
+/* bit 0 = skip zero blocks, bit 1 = bandwidth-bound kernel. */
+typedef enum {
+  SPAROA_PATH_DENSE_MFMA = 0,
+  SPAROA_PATH_SKIP_MFMA = 1,
+  SPAROA_PATH_DENSE_BW = 2,
+  SPAROA_PATH_SKIP_BW = 3
+} sparoa_path;
+
+typedef enum { SPAROA_ROUTE_BLOCK = 0, SPAROA_ROUTE_ELEMENT = 1 } sparoa_route_mode;
+
+/* 2-D convolution (cross-correlation).  x NHWC [n][h][w][c_in],
+ * w [c_out][kh][kw][c_in/groups], y NHWC [n][ho][wo][c_out] with
+ * ho = (h + 2 ph - dh (kh-1) - 1) / sh + 1 (likewise wo). */
+typedef struct {
+  int64_t n, c_in, h, w, c_out, kh, kw, sh, sw, ph, pw, dh, dw, groups;
+  sparoa_dtype dtype;
+  int has_bias;
+} sparoa_conv_desc;
+
+/* Fully connected y[m][n] = x[m][k] * w[n][k]^T (+ bias[n]). */
+typedef struct {
+  int64_t m, k, n;
+  sparoa_dtype dtype;
+  int has_bias;
+} sparoa_fc_desc;
+
+/* Sparsity statistics (Eq. 1).  zero_blocks/num_blocks are 0 when no block
+ * bitmap was requested. */
+typedef struct {
+  uint64_t zeros, numel, zero_blocks, num_blocks;
+} sparoa_counts;
+
+/* Operator work (Eq. 2): macs = multiply-accumulates, flops = 2 macs,
+ * bytes = compulsory traffic, intensity = flops / bytes (FLOP per byte). */
+typedef struct {
+  uint64_t macs, flops, bytes;
+  double intensity;
+} sparoa_intensity;
+
+/* Routing thresholds in natural units: sparsity in [0, 1], intensity in
+ * FLOP/byte.  mode selects block (default) or element sparsity. */
+typedef struct {
+  double sparsity_thr, intensity_thr;
+  int mode;
+} sparoa_thresholds;
+
+uint32_t sparoa_abi_version(void);
+const char *sparoa_status_string(sparoa_status s);
+/* Detail message of the last failing call on this thread ("" if none). */
+const char *sparoa_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Sparsity measurement (SparOA Section 3.1, Eq. 1: rho = zero fraction of an
+ * activation tensor; Section 2.1: zero activations may be skipped).
+ *
+ * x_dev is viewed as a row-major [rows x cols] matrix of `dtype`.  Writes
+ * counts_dev->zeros (elements whose magnitude bits are all clear: +0, -0),
+ * ->numel = rows*cols.  If mask_dev != NULL and block_rows, block_cols > 0,
+ * also writes the nonzero-block bitmap: blocks are block_rows x block_cols
+ * tiles (edge tiles clipped); block (bi, bj) has index
+ * bi*ceil(cols/block_cols) + bj and sets bit (idx & 31) of mask word idx >> 5
+ * iff it holds a nonzero element; unused high bits of the last word are 0;
+ * ->zero_blocks / ->num_blocks are filled.  mask_dev must hold
+ * sparoa_mask_words() words.  If per_sample_dev != NULL, rows are split into
+ * `samples` equal groups (rows % samples == 0, and when a mask is requested
+ * (rows/samples) % block_rows == 0) and per_sample_dev[s] = zeros of group s.
+ * Asynchronous on `stream`; all outputs are initialised by the call.
+ * Errors: INVALID_ARG for rows/cols <= 0, null x/counts, bad samples;
+ * UNSUPPORTED for a misaligned x.
+ * ---------------------------------------------------------------------- */
+sparoa_status sparoa_mask_words(int64_t rows, int64_t cols, int64_t block_rows,
+                                int64_t block_cols, int64_t *words);
+sparoa_status sparoa_measure_sparsity(const void *x_dev, sparoa_dtype dtype, int64_t rows,
+                                      int64_t cols, int64_t block_rows, int64_t block_cols,
+                                      int64_t samples, sparoa_counts *counts_dev,
+                                      uint32_t *mask_dev, uint64_t *per_sample_dev,
+                                      hipStream_t stream);
+/* Same, then copies the counts into *counts_host and waits for the stream.
+ * counts_dev is caller-provided device scratch of one sparoa_counts. */
+sparoa_status sparoa_measure_sparsity_sync(const void *x_dev, sparoa_dtype dtype, int64_t rows,
+                                           int64_t cols, int64_t block_rows, int64_t block_cols,
+                                           int64_t samples, sparoa_counts *counts_dev,
+                                           uint32_t *mask_dev, uint64_t *per_sample_dev,
+                                           sparoa_counts *counts_host, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Operator intensity (SparOA Section 3.1, Eq. 2: I = Kh Kw Cin Cout H W),
+ * read with H, W = output extents, times the batch, with Cin/groups:
+ *   macs  = n * ho * wo * c_out * (c_in/groups) * kh * kw
+ *   bytes = size(dtype) * (n c_in h w + c_out (c_in/groups) kh kw
+ *                          + n c_out ho wo + has_bias c_out)
+ * FC: macs = m k n, bytes = size * (m k + n k + m n + has_bias n).
+ * Host-only, pure.  Errors: INVALID_ARG for non-positive sizes, c_in or c_out
+ * not divisible by groups, an empty output, or uint64 overflow.
+ * ---------------------------------------------------------------------- */
+sparoa_status sparoa_op_intensity_conv(const sparoa_conv_desc *desc, sparoa_intensity *out);
+sparoa_status sparoa_op_intensity_fc(const sparoa_fc_desc *desc, sparoa_intensity *out);
+
+/* ------------------------------------------------------------------------
+ * Routing (SparOA Section 2.2: sparsity and intensity are independent axes
+ * giving four quadrants -- sparse/dense x heavy/light; Section 3 opening:
+ * fixed-threshold rule).  The CPU/GPU choice of the paper is remapped to
+ * kernel paths of one GPU:
+ *   skip bit      = rho >= sparsity_thr, rho = zero_blocks/num_blocks (BLOCK
+ *                   mode) or zeros/numel (ELEMENT mode), one double division;
+ *   bandwidth bit = is_depthwise || intensity < intensity_thr.
+ * counts is host memory.  Errors: INVALID_ARG for NaN or negative thresholds
+ * or intensity, num_blocks == 0 in BLOCK mode, numel == 0 in ELEMENT mode,
+ * counts larger than their totals, an unknown mode.
+ * ---------------------------------------------------------------------- */
+sparoa_status sparoa_route(const sparoa_counts *counts, const sparoa_intensity *intensity,
+                           int is_depthwise, const sparoa_thresholds *thr, sparoa_path *out);
+
+/* ------------------------------------------------------------------------
+ * Convolution (the operators of SparOA Sections 1 and 2.1; zero skipping of
+ * Section 2.1).  y = act(conv(x, w) + bias + residual), written in dtype (the
+ * residual joins before the activation, as in a ResNet bottleneck).
+ *   Paths: DENSE_MFMA / SKIP_MFMA : implicit-GEMM on MFMA (groups == 1);
+ *          DENSE_BW / SKIP_BW     : depthwise (groups == c_in == c_out) direct
+ *                                   kernel, or, for groups == 1, the
+ *                                   implicit GEMM with a tile shape that reads
+ *                                   each activation once.
+ *   Skip paths need `mask`: the bitmap of x written by
+ *   sparoa_measure_sparsity over the [n*h*w, c_in] view with the block shape
+ *   returned by sparoa_conv2d_skip_block (one pixel x 8 channels); a
+ *   work-group skips every (tile, K chunk) whose gathered input is zero:
+ *   those blocks are never loaded nor multiplied.  Needs c_in % 8 == 0
+ *   (else UNSUPPORTED).  Dense paths ignore mask.  The depthwise kernel reads
+ *   every input once and skips nothing.
+ *   bias [c_out] (if desc->has_bias), residual (NHWC, output shape) nullable.
+ *   executed_blocks_dev (nullable, skip paths): receives the number of
+ *   executed (row tile, tap, channel block) triples.
+ * Errors: INVALID_ARG for bad shapes, null x/w/y, a null mask on a skip path;
+ * UNSUPPORTED for grouped non-depthwise convs, unsupported dtype/path;
+ * WORKSPACE if ws_bytes is below sparoa_conv2d_workspace_size.
+ * ---------------------------------------------------------------------- */
+sparoa_status sparoa_conv2d_workspace_size(const sparoa_conv_desc *desc, sparoa_path path,
+                                           size_t *bytes);
+sparoa_status sparoa_conv2d_skip_block(const sparoa_conv_desc *desc, sparoa_path path,
+                                       int64_t *block_rows, int64_t *block_cols);
+/* Work tiling of the implicit-GEMM kernel: rows (output pixels) per tile and
+ * K values per chunk, the units executed_blocks_dev counts.  UNSUPPORTED for
+ * depthwise convs (not tiled). */
+sparoa_status sparoa_conv2d_tiling(const sparoa_conv_desc *desc, sparoa_path path,
+                                   int64_t *tile_rows, int64_t *kchunk);
+sparoa_status sparoa_conv2d(const sparoa_conv_desc *desc, sparoa_path path, const void *x,
+                            const void *w, const void *bias, const void *residual,
+                            sparoa_act act, const uint32_t *mask, void *y, void *workspace,
+                            size_t ws_bytes, uint64_t *executed_blocks_dev, hipStream_t stream);
+/* Fixed-path forms: dense = DENSE_MFMA for groups == 1, DENSE_BW for
+ * depthwise; zero_skip = SKIP_MFMA for groups == 1, SKIP_BW for depthwise. */
+sparoa_status sparoa_conv2d_dense(const sparoa_conv_desc *desc, const void *x, const void *w,
+                                  const void *bias, const void *residual, sparoa_act act,
+                                  void *y, void *workspace, size_t ws_bytes, hipStream_t stream);
+sparoa_status sparoa_conv2d_zero_skip(const sparoa_conv_desc *desc, const void *x,
+                                      const void *w, const void *bias, const void *residual,
+                                      sparoa_act act, const uint32_t *mask, void *y,
+                                      void *workspace, size_t ws_bytes,
+                                      uint64_t *executed_blocks_dev, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Fully connected (SparOA Sections 1 and 2.1).
+ * y = act(x w^T + bias + residual); residual [m][n] nullable.
+ *   Paths: DENSE_MFMA / SKIP_MFMA : tiled MFMA GEMM, w in [n][k];
+ *          DENSE_BW / SKIP_BW     : weight-streaming kernel for m <= 64,
+ *                                   w in the packed layout of
+ *                                   sparoa_fc_pack_weights (k-major [k][n]),
+ *                                   each weight byte read at most once.
+ *   Skip paths need `mask` of x measured over [m, k] with the block shape of
+ *   sparoa_fc_skip_block ((1, 8) for SKIP_MFMA, (m, 1) for SKIP_BW):
+ *   SKIP_MFMA skips (row tile, K chunk) pairs whose input block is zero;
+ *   SKIP_BW skips input columns that are zero in every row, and with them
+ *   their weight rows.
+ *   executed_blocks_dev (nullable, skip paths): executed (row tile, K block)
+ *   pairs (SKIP_MFMA) or nonzero columns (SKIP_BW).
+ * Errors as for sparoa_conv2d; UNSUPPORTED for m > 64 on a BW path.
+ * ---------------------------------------------------------------------- */
+/* Packed weights for the BW paths: 64-column panels, k-major inside a panel:
+ * packed[p][k][0..63] = w[64p + 0..63][k] (zero past n).  w_packed must hold
+ * sparoa_fc_packed_bytes() bytes and must not alias w_nk.  16-bit dtypes. */
+sparoa_status sparoa_fc_packed_bytes(const sparoa_fc_desc *desc, size_t *bytes);
+sparoa_status sparoa_fc_pack_weights(const sparoa_fc_desc *desc, const void *w_nk,
+                                     void *w_packed, hipStream_t stream);
+/* Work tiling: (tile_rows, kchunk) = the MFMA tile rows and K chunk on the
+ * MFMA paths, (m, 1) on the BW paths. */
+sparoa_status sparoa_fc_tiling(const sparoa_fc_desc *desc, sparoa_path path, int64_t *tile_rows,
+                               int64_t *kchunk);
+sparoa_status sparoa_fc_workspace_size(const sparoa_fc_desc *desc, sparoa_path path,
+                                       size_t *bytes);
+sparoa_status sparoa_fc_skip_block(const sparoa_fc_desc *desc, sparoa_path path,
+                                   int64_t *block_rows, int64_t *block_cols);
+sparoa_status sparoa_fc(const sparoa_fc_desc *desc, sparoa_path path, const void *x,
+                        const void *w_or_packed, const void *bias, const void *residual,
+                        sparoa_act act, const uint32_t *mask, void *y, void *workspace,
+                        size_t ws_bytes, uint64_t *executed_blocks_dev, hipStream_t stream);
+/* Fixed-path forms on the MFMA kernel (w in [n][k]). */
+sparoa_status sparoa_fc_dense(const sparoa_fc_desc *desc, const void *x, const void *w_nk,
+                              const void *bias, const void *residual, sparoa_act act, void *y,
+                              void *workspace, size_t ws_bytes, hipStream_t stream);
+sparoa_status sparoa_fc_zero_skip(const sparoa_fc_desc *desc, const void *x, const void *w_nk,
+                                  const void *bias, const void *residual, sparoa_act act,
+                                  const uint32_t *mask, void *y, void *workspace,
+                                  size_t ws_bytes, uint64_t *executed_blocks_dev,
+                                  hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Network glue (not routed): NHWC max pooling, window k, stride s, padding p.
+ * ---------------------------------------------------------------------- */
+sparoa_status sparoa_maxpool2d(const void *x, sparoa_dtype dtype, int64_t n, int64_t c,
+                               int64_t h, int64_t w, int64_t k, int64_t s, int64_t p, void *y,
+                               hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPAROA_H */

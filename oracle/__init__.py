@@ -65,8 +65,8 @@ def lib():
                                                _u32p, _i64, _i64, _dp, _dp, _u64p])
         L.or_conv2d_at.argtypes = ([_i64] * 14 + [ctypes.c_int, _vp, _vp, _vp, _vp, ctypes.c_int,
                                                   ctypes.POINTER(ctypes.c_int64), _i64, _dp, _dp])
-        L.or_fc.argtypes = [_i64] * 3 + [ctypes.c_int, _vp, _vp, _vp, ctypes.c_int, _u32p, _i64,
-                                         _i64, _dp, _dp]
+        L.or_fc.argtypes = [_i64] * 3 + [ctypes.c_int, _vp, _vp, _vp, _vp, ctypes.c_int, _u32p,
+                                         _i64, _i64, _dp, _dp]
         L.or_fc_executed_blocks.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _u64p]
         L.or_conv_executed_blocks.argtypes = [_vp, ctypes.c_int] + [_i64] * 14 + [_u64p]
         L.or_maxpool2d.argtypes = [_i64] * 7 + [ctypes.c_int, _vp, _dp]
@@ -178,8 +178,8 @@ def route(zeros, numel, zero_blocks, num_blocks, intensity, is_depthwise, sparsi
 
 def conv2d(x, w, n, cin, h, wd, cout, kh, kw, sh=1, sw=1, ph=0, pw=0, dh=1, dw=1, groups=1,
            bias=None, residual=None, act=ACT_NONE, skip_mask=None, skip_rows=0, skip_cols=0):
-    """Direct NHWC convolution.  Returns (y, a, macs) with y, a float64
-    [n, ho, wo, cout]."""
+    """Direct NHWC convolution, y = act(conv + bias + residual).  Returns
+    (y, a, macs) with y, a float64 [n, ho, wo, cout]."""
     xr, code = _bits(x)
     wr, wc = _bits(w)
     assert wc == code
@@ -219,14 +219,17 @@ def conv2d_at(x, w, idx, n, cin, h, wd, cout, kh, kw, sh=1, sw=1, ph=0, pw=0, dh
     return y, a
 
 
-def fc(x, w, m, k, n, bias=None, act=ACT_NONE, skip_mask=None, skip_rows=0, skip_cols=0):
-    """y[m][n] = act(bias + x w^T) in double.  w is [n][k].  Returns (y, a)."""
+def fc(x, w, m, k, n, bias=None, act=ACT_NONE, skip_mask=None, skip_rows=0, skip_cols=0,
+       residual=None):
+    """y[m][n] = act(bias + x w^T + residual) in double.  w is [n][k].
+    Returns (y, a)."""
     xr, code = _bits(x)
     wr, _ = _bits(w)
     br = _bits(bias)[0] if bias is not None else None
+    rr = _bits(residual)[0] if residual is not None else None
     y = np.zeros((m, n), dtype=np.float64)
     a = np.zeros_like(y)
-    rc = lib().or_fc(m, k, n, code, _ptr(xr), _ptr(wr), _ptr(br), act,
+    rc = lib().or_fc(m, k, n, code, _ptr(xr), _ptr(wr), _ptr(br), _ptr(rr), act,
                      None if skip_mask is None else
                      np.ascontiguousarray(skip_mask, dtype=np.uint32).ctypes.data_as(_u32p),
                      skip_rows, skip_cols, y.ctypes.data_as(_dp), a.ctypes.data_as(_dp))

@@ -300,7 +300,8 @@ static int mask_bit(const uint32_t *mask, int64_t idx) { return (mask[idx >> 5] 
  * 2-D convolution (cross-correlation, as in DNN frameworks).
  *   x : NHWC [n][h][w][cin]             w : [cout][kh][kw][cin/groups]
  *   bias : [cout] or NULL               residual : NHWC [n][ho][wo][cout] or NULL
- *   y = act(bias + sum x*w) + residual, evaluated in double.
+ *   y = act(bias + sum x*w + residual), evaluated in double (the residual
+ *   joins the sum before the activation, as in a ResNet bottleneck).
  *   y_out, a_out : [n][ho][wo][cout]; a_out = |bias| + sum |x*w| (+ |residual|),
  *   the scale of the rounding error of any summation order.
  * skip_mask (or NULL): bitmap over the [n*h*w, cin] view of x with
@@ -348,14 +349,13 @@ int or_conv2d(int64_t n, int64_t cin, int64_t h, int64_t w, int64_t cout, int64_
                 mag += fabs(p);
               }
             }
-          double v = act_apply(acc, act);
           int64_t o = ((in * ho_n + oh) * wo_n + ow) * cout + co;
           if (residual) {
             double rv = elem(residual, dt, o);
-            v += rv;
+            acc += rv;
             mag += fabs(rv);
           }
-          y_out[o] = v;
+          y_out[o] = act_apply(acc, act);
           if (a_out) a_out[o] = mag;
         }
     }
@@ -364,14 +364,15 @@ int or_conv2d(int64_t n, int64_t cin, int64_t h, int64_t w, int64_t cout, int64_
 }
 
 /*
- * Fully connected: y[m][j] = act(bias[j] + sum_k x[m][k] * w[j][k]).
- *   x : [m][k], w : [n][k] (output-feature major), y_out, a_out : [m][n].
+ * Fully connected: y[m][j] = act(bias[j] + sum_k x[m][k] * w[j][k] + residual[m][j]).
+ *   x : [m][k], w : [n][k] (output-feature major), residual : [m][n] or NULL,
+ *   y_out, a_out : [m][n].
  * skip_mask (or NULL): bitmap over the [m, k] view of x with skip_rows x
  * skip_cols blocks; terms whose x element lies in a zero block are skipped.
  */
 int or_fc(int64_t m, int64_t k, int64_t n, int dt, const void *x, const void *wt,
-          const void *bias, int act, const uint32_t *skip_mask, int64_t skip_rows,
-          int64_t skip_cols, double *y_out, double *a_out) {
+          const void *bias, const void *residual, int act, const uint32_t *skip_mask,
+          int64_t skip_rows, int64_t skip_cols, double *y_out, double *a_out) {
   if (!x || !wt || !y_out || !dt_ok(dt) || m <= 0 || k <= 0 || n <= 0) return OR_EINVAL;
   if (skip_mask && (skip_rows <= 0 || skip_cols <= 0)) return OR_EINVAL;
   int64_t nbc = skip_mask ? (k + skip_cols - 1) / skip_cols : 0;
@@ -385,6 +386,11 @@ int or_fc(int64_t m, int64_t k, int64_t n, int dt, const void *x, const void *wt
         double p = elem(x, dt, i * k + kk) * elem(wt, dt, j * k + kk);
         acc += p;
         mag += fabs(p);
+      }
+      if (residual) {
+        double rv = elem(residual, dt, i * n + j);
+        acc += rv;
+        mag += fabs(rv);
       }
       y_out[i * n + j] = act_apply(acc, act);
       if (a_out) a_out[i * n + j] = mag;
@@ -430,13 +436,12 @@ int or_conv2d_at(int64_t n, int64_t cin, int64_t h, int64_t w, int64_t cout, int
           mag += fabs(p);
         }
       }
-    double v = act_apply(acc, act);
     if (residual) {
       double rv = elem(residual, dt, o);
-      v += rv;
+      acc += rv;
       mag += fabs(rv);
     }
-    y_out[t] = v;
+    y_out[t] = act_apply(acc, act);
     if (a_out) a_out[t] = mag;
   }
   return OR_OK;

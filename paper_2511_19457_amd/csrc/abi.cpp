@@ -1,0 +1,449 @@
+// extern "C" entry points of libsparoa.so: argument validation, the host-side
+// intensity and routing functions, and dispatch to the HIP kernels.
+#include <cmath>
+#include <cstring>
+#include <string>
+
+#include "common.h"
+
+namespace sparoa {
+
+namespace {
+thread_local std::string g_last_error;
+
+bool mul_ok(uint64_t a, uint64_t b, uint64_t *r) { return !__builtin_mul_overflow(a, b, r); }
+bool add_ok(uint64_t a, uint64_t b, uint64_t *r) { return !__builtin_add_overflow(a, b, r); }
+
+bool dtype_ok(int d) { return d == SPAROA_F32 || d == SPAROA_F16 || d == SPAROA_BF16; }
+bool act_ok(int a) { return a == SPAROA_ACT_NONE || a == SPAROA_ACT_RELU || a == SPAROA_ACT_RELU6; }
+bool path_ok(int p) { return p >= SPAROA_PATH_DENSE_MFMA && p <= SPAROA_PATH_SKIP_BW; }
+
+int64_t out_extent(int64_t in, int64_t k, int64_t s, int64_t p, int64_t d) {
+  if (in <= 0 || k <= 0 || s <= 0 || p < 0 || d <= 0) return -1;
+  const int64_t span = in + 2 * p - d * (k - 1) - 1;
+  return span < 0 ? -1 : span / s + 1;
+}
+
+sparoa_status check_conv(const sparoa_conv_desc *d, int64_t *ho, int64_t *wo) {
+  if (!d) return fail(SPAROA_ERR_INVALID_ARG, "null conv descriptor");
+  if (!dtype_ok(d->dtype)) return fail(SPAROA_ERR_INVALID_ARG, "unknown dtype");
+  if (d->n <= 0 || d->c_in <= 0 || d->c_out <= 0 || d->groups <= 0 || d->c_in % d->groups ||
+      d->c_out % d->groups)
+    return fail(SPAROA_ERR_INVALID_ARG, "conv: bad batch/channel/group sizes");
+  *ho = out_extent(d->h, d->kh, d->sh, d->ph, d->dh);
+  *wo = out_extent(d->w, d->kw, d->sw, d->pw, d->dw);
+  if (*ho <= 0 || *wo <= 0) return fail(SPAROA_ERR_INVALID_ARG, "conv: empty output");
+  return SPAROA_OK;
+}
+
+sparoa_status check_fc(const sparoa_fc_desc *d) {
+  if (!d) return fail(SPAROA_ERR_INVALID_ARG, "null fc descriptor");
+  if (!dtype_ok(d->dtype)) return fail(SPAROA_ERR_INVALID_ARG, "unknown dtype");
+  if (d->m <= 0 || d->k <= 0 || d->n <= 0) return fail(SPAROA_ERR_INVALID_ARG, "fc: sizes must be > 0");
+  return SPAROA_OK;
+}
+
+bool is_depthwise(const sparoa_conv_desc &d) {
+  return d.groups > 1 && d.groups == d.c_in && d.groups == d.c_out;
+}
+
+// The 1x1 stride-1 unpadded convolution with the FC's shape.
+sparoa_conv_desc fc_as_conv(const sparoa_fc_desc &f) {
+  sparoa_conv_desc c;
+  c.n = f.m; c.c_in = f.k; c.h = 1; c.w = 1; c.c_out = f.n; c.kh = 1; c.kw = 1;
+  c.sh = 1; c.sw = 1; c.ph = 0; c.pw = 0; c.dh = 1; c.dw = 1; c.groups = 1;
+  c.dtype = f.dtype; c.has_bias = f.has_bias;
+  return c;
+}
+
+sparoa_status check_ptrs16(std::initializer_list<const void *> ps) {
+  for (const void *p : ps)
+    if (p && !aligned16(p)) return fail(SPAROA_ERR_UNSUPPORTED, "pointer not 16-byte aligned");
+  return SPAROA_OK;
+}
+}  // namespace
+
+sparoa_status fail(sparoa_status s, const std::string &msg) {
+  g_last_error = msg;
+  return s;
+}
+
+sparoa_status hip_fail(hipError_t e, const char *what) {
+  g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+  return SPAROA_ERR_HIP;
+}
+
+}  // namespace sparoa
+
+using namespace sparoa;
+
+extern "C" {
+
+uint32_t sparoa_abi_version(void) { return SPAROA_ABI_VERSION; }
+
+const char *sparoa_status_string(sparoa_status s) {
+  switch (s) {
+    case SPAROA_OK: return "ok";
+    case SPAROA_ERR_INVALID_ARG: return "invalid argument";
+    case SPAROA_ERR_UNSUPPORTED: return "unsupported";
+    case SPAROA_ERR_WORKSPACE: return "workspace too small";
+    case SPAROA_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char *sparoa_last_error(void) { return g_last_error.c_str(); }
+
+// ---------------------------------------------------------------- measure
+
+sparoa_status sparoa_mask_words(int64_t rows, int64_t cols, int64_t block_rows,
+                                int64_t block_cols, int64_t *words) {
+  g_last_error.clear();
+  if (!words || rows <= 0 || cols <= 0 || block_rows <= 0 || block_cols <= 0)
+    return fail(SPAROA_ERR_INVALID_ARG, "mask_words: sizes must be > 0");
+  uint64_t nb;
+  if (!mul_ok((uint64_t)cdiv(rows, block_rows), (uint64_t)cdiv(cols, block_cols), &nb) ||
+      nb > ((uint64_t)INT32_MAX) * 32u)
+    return fail(SPAROA_ERR_INVALID_ARG, "mask_words: too many blocks");
+  *words = (int64_t)((nb + 31) / 32);
+  return SPAROA_OK;
+}
+
+sparoa_status sparoa_measure_sparsity(const void *x_dev, sparoa_dtype dtype, int64_t rows,
+                                      int64_t cols, int64_t block_rows, int64_t block_cols,
+                                      int64_t samples, sparoa_counts *counts_dev,
+                                      uint32_t *mask_dev, uint64_t *per_sample_dev,
+                                      hipStream_t stream) {
+  g_last_error.clear();
+  if (!x_dev || !counts_dev) return fail(SPAROA_ERR_INVALID_ARG, "measure: null x or counts");
+  if (!dtype_ok(dtype)) return fail(SPAROA_ERR_INVALID_ARG, "measure: unknown dtype");
+  uint64_t numel;
+  if (rows <= 0 || cols <= 0 || !mul_ok((uint64_t)rows, (uint64_t)cols, &numel) ||
+      numel > (uint64_t)INT64_MAX / 4)
+    return fail(SPAROA_ERR_INVALID_ARG, "measure: rows and cols must be > 0");
+  if (mask_dev) {
+    int64_t words;
+    sparoa_status st = sparoa_mask_words(rows, cols, block_rows, block_cols, &words);
+    if (st != SPAROA_OK) return st;
+  }
+  if (per_sample_dev) {
+    if (samples <= 0 || rows % samples)
+      return fail(SPAROA_ERR_INVALID_ARG, "measure: rows must split into `samples` groups");
+    if (samples > 65535) return fail(SPAROA_ERR_UNSUPPORTED, "measure: more than 65535 samples");
+    if (mask_dev && (rows / samples) % block_rows)
+      return fail(SPAROA_ERR_INVALID_ARG, "measure: block rows straddle samples");
+  }
+  if (!aligned16(x_dev)) return fail(SPAROA_ERR_UNSUPPORTED, "measure: x not 16-byte aligned");
+  return launch_measure(x_dev, dtype, rows, cols, block_rows, block_cols, samples, counts_dev,
+                        mask_dev, per_sample_dev, stream);
+}
+
+sparoa_status sparoa_measure_sparsity_sync(const void *x_dev, sparoa_dtype dtype, int64_t rows,
+                                           int64_t cols, int64_t block_rows, int64_t block_cols,
+                                           int64_t samples, sparoa_counts *counts_dev,
+                                           uint32_t *mask_dev, uint64_t *per_sample_dev,
+                                           sparoa_counts *counts_host, hipStream_t stream) {
+  if (!counts_host) return fail(SPAROA_ERR_INVALID_ARG, "measure_sync: null host counts");
+  sparoa_status st = sparoa_measure_sparsity(x_dev, dtype, rows, cols, block_rows, block_cols,
+                                             samples, counts_dev, mask_dev, per_sample_dev,
+                                             stream);
+  if (st != SPAROA_OK) return st;
+  SPAROA_HIP_CHECK(hipMemcpyAsync(counts_host, counts_dev, sizeof(sparoa_counts),
+                                  hipMemcpyDeviceToHost, stream));
+  SPAROA_HIP_CHECK(hipStreamSynchronize(stream));
+  return SPAROA_OK;
+}
+
+// -------------------------------------------------------------- intensity
+
+sparoa_status sparoa_op_intensity_conv(const sparoa_conv_desc *d, sparoa_intensity *out) {
+  g_last_error.clear();
+  int64_t ho, wo;
+  sparoa_status st = check_conv(d, &ho, &wo);
+  if (st != SPAROA_OK) return st;
+  if (!out) return fail(SPAROA_ERR_INVALID_ARG, "null output");
+  const uint64_t sz = (uint64_t)elem_size(d->dtype);
+  uint64_t t, out_e, taps, macs, w_e, in_e, all, bytes;
+  bool ok = mul_ok((uint64_t)d->n, (uint64_t)ho, &t) && mul_ok(t, (uint64_t)wo, &t) &&
+            mul_ok(t, (uint64_t)d->c_out, &out_e) &&
+            mul_ok((uint64_t)(d->c_in / d->groups), (uint64_t)d->kh, &taps) &&
+            mul_ok(taps, (uint64_t)d->kw, &taps) && mul_ok(out_e, taps, &macs) &&
+            mul_ok((uint64_t)d->c_out, taps, &w_e) &&
+            mul_ok((uint64_t)d->n, (uint64_t)d->c_in, &t) && mul_ok(t, (uint64_t)d->h, &t) &&
+            mul_ok(t, (uint64_t)d->w, &in_e) && add_ok(in_e, w_e, &all) &&
+            add_ok(all, out_e, &all) &&
+            add_ok(all, d->has_bias ? (uint64_t)d->c_out : 0u, &all) && mul_ok(all, sz, &bytes) &&
+            macs <= UINT64_MAX / 2;
+  if (!ok) return fail(SPAROA_ERR_INVALID_ARG, "conv intensity: uint64 overflow");
+  out->macs = macs;
+  out->flops = 2 * macs;
+  out->bytes = bytes;
+  out->intensity = (double)out->flops / (double)bytes;
+  return SPAROA_OK;
+}
+
+sparoa_status sparoa_op_intensity_fc(const sparoa_fc_desc *d, sparoa_intensity *out) {
+  g_last_error.clear();
+  sparoa_status st = check_fc(d);
+  if (st != SPAROA_OK) return st;
+  if (!out) return fail(SPAROA_ERR_INVALID_ARG, "null output");
+  const uint64_t sz = (uint64_t)elem_size(d->dtype);
+  uint64_t x_e, macs, w_e, y_e, all, bytes;
+  bool ok = mul_ok((uint64_t)d->m, (uint64_t)d->k, &x_e) && mul_ok(x_e, (uint64_t)d->n, &macs) &&
+            mul_ok((uint64_t)d->n, (uint64_t)d->k, &w_e) &&
+            mul_ok((uint64_t)d->m, (uint64_t)d->n, &y_e) && add_ok(x_e, w_e, &all) &&
+            add_ok(all, y_e, &all) && add_ok(all, d->has_bias ? (uint64_t)d->n : 0u, &all) &&
+            mul_ok(all, sz, &bytes) && macs <= UINT64_MAX / 2;
+  if (!ok) return fail(SPAROA_ERR_INVALID_ARG, "fc intensity: uint64 overflow");
+  out->macs = macs;
+  out->flops = 2 * macs;
+  out->bytes = bytes;
+  out->intensity = (double)out->flops / (double)bytes;
+  return SPAROA_OK;
+}
+
+// ------------------------------------------------------------------ route
+
+sparoa_status sparoa_route(const sparoa_counts *c, const sparoa_intensity *in, int is_dw,
+                           const sparoa_thresholds *thr, sparoa_path *out) {
+  g_last_error.clear();
+  if (!c || !in || !thr || !out) return fail(SPAROA_ERR_INVALID_ARG, "route: null argument");
+  if (std::isnan(thr->sparsity_thr) || std::isnan(thr->intensity_thr) ||
+      std::isnan(in->intensity) || thr->sparsity_thr < 0 || thr->intensity_thr < 0 ||
+      in->intensity < 0)
+    return fail(SPAROA_ERR_INVALID_ARG, "route: NaN or negative threshold/intensity");
+  double rho;
+  if (thr->mode == SPAROA_ROUTE_BLOCK) {
+    if (c->num_blocks == 0 || c->zero_blocks > c->num_blocks)
+      return fail(SPAROA_ERR_INVALID_ARG, "route: block mode needs block counts");
+    rho = (double)c->zero_blocks / (double)c->num_blocks;
+  } else if (thr->mode == SPAROA_ROUTE_ELEMENT) {
+    if (c->numel == 0 || c->zeros > c->numel)
+      return fail(SPAROA_ERR_INVALID_ARG, "route: element mode needs numel > 0");
+    rho = (double)c->zeros / (double)c->numel;
+  } else {
+    return fail(SPAROA_ERR_INVALID_ARG, "route: unknown mode");
+  }
+  const int skip = rho >= thr->sparsity_thr ? 1 : 0;
+  const int bw = (is_dw || in->intensity < thr->intensity_thr) ? 1 : 0;
+  *out = (sparoa_path)(skip | (bw << 1));
+  return SPAROA_OK;
+}
+
+// ------------------------------------------------------------------- conv
+
+sparoa_status sparoa_conv2d_workspace_size(const sparoa_conv_desc *d, sparoa_path path,
+                                           size_t *bytes) {
+  g_last_error.clear();
+  int64_t ho, wo;
+  sparoa_status st = check_conv(d, &ho, &wo);
+  if (st != SPAROA_OK) return st;
+  if (!bytes || !path_ok(path)) return fail(SPAROA_ERR_INVALID_ARG, "workspace_size: bad argument");
+  *bytes = is_depthwise(*d) ? 0 : gemm_workspace(*d, path);
+  return SPAROA_OK;
+}
+
+sparoa_status sparoa_conv2d_skip_block(const sparoa_conv_desc *d, sparoa_path path,
+                                       int64_t *block_rows, int64_t *block_cols) {
+  g_last_error.clear();
+  int64_t ho, wo;
+  sparoa_status st = check_conv(d, &ho, &wo);
+  if (st != SPAROA_OK) return st;
+  if (!block_rows || !block_cols || !path_ok(path))
+    return fail(SPAROA_ERR_INVALID_ARG, "skip_block: bad argument");
+  if (is_depthwise(*d)) {
+    // The depthwise kernel reads every input once; its bitmap granularity
+    // is one pixel x 8 channels (routing statistics only).
+    *block_rows = 1;
+    *block_cols = 8;
+    return SPAROA_OK;
+  }
+  if (d->groups != 1) return fail(SPAROA_ERR_UNSUPPORTED, "grouped (non-depthwise) conv");
+  // The implicit-GEMM skip kernel reads one bit per (pixel, 8 channels).
+  *block_rows = 1;
+  *block_cols = 8;
+  return SPAROA_OK;
+}
+
+sparoa_status sparoa_conv2d_tiling(const sparoa_conv_desc *d, sparoa_path path,
+                                   int64_t *tile_rows, int64_t *kchunk) {
+  g_last_error.clear();
+  int64_t ho, wo;
+  sparoa_status st = check_conv(d, &ho, &wo);
+  if (st != SPAROA_OK) return st;
+  if (!tile_rows || !kchunk || !path_ok(path))
+    return fail(SPAROA_ERR_INVALID_ARG, "tiling: bad argument");
+  if (is_depthwise(*d)) return fail(SPAROA_ERR_UNSUPPORTED, "tiling: depthwise is not tiled");
+  if (d->groups != 1) return fail(SPAROA_ERR_UNSUPPORTED, "grouped (non-depthwise) conv");
+  GemmTileChoice t = gemm_choose(*d, path);
+  *tile_rows = t.bm;
+  *kchunk = t.kchunk;
+  return SPAROA_OK;
+}
+
+sparoa_status sparoa_conv2d(const sparoa_conv_desc *d, sparoa_path path, const void *x,
+                            const void *w, const void *bias, const void *residual,
+                            sparoa_act act, const uint32_t *mask, void *y, void *workspace,
+                            size_t ws_bytes, uint64_t *executed, hipStream_t stream) {
+  g_last_error.clear();
+  int64_t ho, wo;
+  sparoa_status st = check_conv(d, &ho, &wo);
+  if (st != SPAROA_OK) return st;
+  if (!x || !w || !y || !path_ok(path) || !act_ok(act))
+    return fail(SPAROA_ERR_INVALID_ARG, "conv2d: null x/w/y or bad path/act");
+  if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "conv2d: has_bias without bias");
+  const bool skip = (path & 1) != 0;
+  if (skip && !mask) return fail(SPAROA_ERR_INVALID_ARG, "conv2d: skip path needs a mask");
+  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace})) != SPAROA_OK) return st;
+  if (is_depthwise(*d)) {
+    if (!(path & 2)) return fail(SPAROA_ERR_UNSUPPORTED, "depthwise conv runs on the BW path");
+    if (executed && (st = launch_set_u64(executed, 0, stream)) != SPAROA_OK) return st;
+    return launch_depthwise(*d, x, w, d->has_bias ? bias : nullptr, residual, act, y, stream);
+  }
+  if (d->groups != 1) return fail(SPAROA_ERR_UNSUPPORTED, "grouped (non-depthwise) conv");
+  if (ws_bytes < gemm_workspace(*d, path))
+    return fail(SPAROA_ERR_WORKSPACE, "conv2d: workspace too small");
+  return launch_gemm_conv(*d, path, x, w, d->has_bias ? bias : nullptr, residual, act,
+                          skip ? mask : nullptr, y, workspace, ws_bytes, executed, stream);
+}
+
+sparoa_status sparoa_conv2d_dense(const sparoa_conv_desc *d, const void *x, const void *w,
+                                  const void *bias, const void *residual, sparoa_act act,
+                                  void *y, void *workspace, size_t ws_bytes, hipStream_t stream) {
+  const sparoa_path p =
+      (d && is_depthwise(*d)) ? SPAROA_PATH_DENSE_BW : SPAROA_PATH_DENSE_MFMA;
+  return sparoa_conv2d(d, p, x, w, bias, residual, act, nullptr, y, workspace, ws_bytes,
+                       nullptr, stream);
+}
+
+sparoa_status sparoa_conv2d_zero_skip(const sparoa_conv_desc *d, const void *x, const void *w,
+                                      const void *bias, const void *residual, sparoa_act act,
+                                      const uint32_t *mask, void *y, void *workspace,
+                                      size_t ws_bytes, uint64_t *executed, hipStream_t stream) {
+  const sparoa_path p = (d && is_depthwise(*d)) ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
+  return sparoa_conv2d(d, p, x, w, bias, residual, act, mask, y, workspace, ws_bytes, executed,
+                       stream);
+}
+
+// --------------------------------------------------------------------- fc
+
+sparoa_status sparoa_fc_pack_weights(const sparoa_fc_desc *d, const void *w_nk, void *w_packed,
+                                     hipStream_t stream) {
+  g_last_error.clear();
+  sparoa_status st = check_fc(d);
+  if (st != SPAROA_OK) return st;
+  if (!w_nk || !w_packed || w_nk == w_packed)
+    return fail(SPAROA_ERR_INVALID_ARG, "fc_pack_weights: null or aliased buffers");
+  if ((st = check_ptrs16({w_nk, w_packed})) != SPAROA_OK) return st;
+  return launch_fc_pack(*d, w_nk, w_packed, stream);
+}
+
+sparoa_status sparoa_fc_packed_bytes(const sparoa_fc_desc *d, size_t *bytes) {
+  g_last_error.clear();
+  sparoa_status st = check_fc(d);
+  if (st != SPAROA_OK) return st;
+  if (!bytes) return fail(SPAROA_ERR_INVALID_ARG, "packed_bytes: null output");
+  *bytes = fc_packed_bytes(*d);
+  return SPAROA_OK;
+}
+
+sparoa_status sparoa_fc_tiling(const sparoa_fc_desc *d, sparoa_path path, int64_t *tile_rows,
+                               int64_t *kchunk) {
+  g_last_error.clear();
+  sparoa_status st = check_fc(d);
+  if (st != SPAROA_OK) return st;
+  if (!tile_rows || !kchunk || !path_ok(path))
+    return fail(SPAROA_ERR_INVALID_ARG, "tiling: bad argument");
+  if (path & 2) {
+    *tile_rows = d->m;
+    *kchunk = 1;
+  } else {
+    GemmTileChoice t = gemm_choose(fc_as_conv(*d), path);
+    *tile_rows = t.bm;
+    *kchunk = t.kchunk;
+  }
+  return SPAROA_OK;
+}
+
+sparoa_status sparoa_fc_workspace_size(const sparoa_fc_desc *d, sparoa_path path, size_t *bytes) {
+  g_last_error.clear();
+  sparoa_status st = check_fc(d);
+  if (st != SPAROA_OK) return st;
+  if (!bytes || !path_ok(path)) return fail(SPAROA_ERR_INVALID_ARG, "workspace_size: bad argument");
+  *bytes = (path & 2) ? fc_bw_workspace(*d, path) : gemm_workspace(fc_as_conv(*d), path);
+  return SPAROA_OK;
+}
+
+sparoa_status sparoa_fc_skip_block(const sparoa_fc_desc *d, sparoa_path path,
+                                   int64_t *block_rows, int64_t *block_cols) {
+  g_last_error.clear();
+  sparoa_status st = check_fc(d);
+  if (st != SPAROA_OK) return st;
+  if (!block_rows || !block_cols || !path_ok(path))
+    return fail(SPAROA_ERR_INVALID_ARG, "skip_block: bad argument");
+  if (path & 2) {  // a column is skipped when it is zero in every row
+    *block_rows = d->m;
+    *block_cols = 1;
+  } else {  // the implicit-GEMM skip kernel reads one bit per (row, 8 columns)
+    *block_rows = 1;
+    *block_cols = 8;
+  }
+  return SPAROA_OK;
+}
+
+sparoa_status sparoa_fc(const sparoa_fc_desc *d, sparoa_path path, const void *x,
+                        const void *w, const void *bias, const void *residual, sparoa_act act,
+                        const uint32_t *mask, void *y, void *workspace, size_t ws_bytes,
+                        uint64_t *executed, hipStream_t stream) {
+  g_last_error.clear();
+  sparoa_status st = check_fc(d);
+  if (st != SPAROA_OK) return st;
+  if (!x || !w || !y || !path_ok(path) || !act_ok(act))
+    return fail(SPAROA_ERR_INVALID_ARG, "fc: null x/w/y or bad path/act");
+  if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "fc: has_bias without bias");
+  const bool skip = (path & 1) != 0;
+  if (skip && !mask) return fail(SPAROA_ERR_INVALID_ARG, "fc: skip path needs a mask");
+  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace})) != SPAROA_OK) return st;
+  if (path & 2) {
+    if (ws_bytes < fc_bw_workspace(*d, path))
+      return fail(SPAROA_ERR_WORKSPACE, "fc: workspace too small");
+    return launch_fc_bw(*d, path, x, w, d->has_bias ? bias : nullptr, residual, act,
+                        skip ? mask : nullptr, y, workspace, ws_bytes, executed, stream);
+  }
+  const sparoa_conv_desc c = fc_as_conv(*d);
+  if (ws_bytes < gemm_workspace(c, path)) return fail(SPAROA_ERR_WORKSPACE, "fc: workspace too small");
+  return launch_gemm_conv(c, path, x, w, d->has_bias ? bias : nullptr, residual, act,
+                          skip ? mask : nullptr, y, workspace, ws_bytes, executed, stream);
+}
+
+sparoa_status sparoa_fc_dense(const sparoa_fc_desc *d, const void *x, const void *w_nk,
+                              const void *bias, const void *residual, sparoa_act act, void *y,
+                              void *workspace, size_t ws_bytes, hipStream_t stream) {
+  return sparoa_fc(d, SPAROA_PATH_DENSE_MFMA, x, w_nk, bias, residual, act, nullptr, y, workspace,
+                   ws_bytes, nullptr, stream);
+}
+
+sparoa_status sparoa_fc_zero_skip(const sparoa_fc_desc *d, const void *x, const void *w_nk,
+                                  const void *bias, const void *residual, sparoa_act act,
+                                  const uint32_t *mask, void *y, void *workspace,
+                                  size_t ws_bytes, uint64_t *executed, hipStream_t stream) {
+  return sparoa_fc(d, SPAROA_PATH_SKIP_MFMA, x, w_nk, bias, residual, act, mask, y, workspace,
+                   ws_bytes, executed, stream);
+}
+
+// ------------------------------------------------------------------- glue
+
+sparoa_status sparoa_maxpool2d(const void *x, sparoa_dtype dtype, int64_t n, int64_t c,
+                               int64_t h, int64_t w, int64_t k, int64_t s, int64_t p, void *y,
+                               hipStream_t stream) {
+  g_last_error.clear();
+  if (!x || !y || !dtype_ok(dtype) || n <= 0 || c <= 0)
+    return fail(SPAROA_ERR_INVALID_ARG, "maxpool2d: bad argument");
+  if (out_extent(h, k, s, p, 1) <= 0 || out_extent(w, k, s, p, 1) <= 0 || p >= k)
+    return fail(SPAROA_ERR_INVALID_ARG, "maxpool2d: empty output or padding >= window");
+  sparoa_status st = check_ptrs16({x, y});
+  if (st != SPAROA_OK) return st;
+  return launch_maxpool(x, dtype, n, c, h, w, k, s, p, y, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,83 @@
+// Internal declarations shared by the HIP sources of libsparoa.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+
+#include "sparoa.h"
+
+namespace sparoa {
+
+// Thread-local error message plumbing (defined in abi.cpp).
+sparoa_status fail(sparoa_status s, const std::string &msg);
+sparoa_status hip_fail(hipError_t e, const char *what);
+
+#define SPAROA_HIP_CHECK(call)                                  \
+  do {                                                          \
+    hipError_t e_ = (call);                                     \
+    if (e_ != hipSuccess) return ::sparoa::hip_fail(e_, #call); \
+  } while (0)
+
+// Checks the launch of the kernel just enqueued.
+#define SPAROA_LAUNCH_CHECK(what)                               \
+  do {                                                          \
+    hipError_t e_ = hipGetLastError();                          \
+    if (e_ != hipSuccess) return ::sparoa::hip_fail(e_, what);  \
+  } while (0)
+
+inline int64_t elem_size(sparoa_dtype d) { return d == SPAROA_F32 ? 4 : 2; }
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// ---- launchers (validated arguments; defined in the .hip files) ---------
+
+sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64_t cols,
+                             int64_t block_rows, int64_t block_cols, int64_t samples,
+                             sparoa_counts *counts, uint32_t *mask, uint64_t *per_sample,
+                             hipStream_t stream);
+
+// Implicit-GEMM MFMA conv (groups == 1); FC runs through it as a 1x1 conv.
+struct GemmTileChoice {
+  int bm, bn;       // output tile rows (pixels) x cols (channels)
+  int kchunk;       // K elements per main-loop step == skip granularity (channels)
+  int split_k;      // number of K splits (1 = none)
+};
+GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path path);
+size_t gemm_workspace(const sparoa_conv_desc &d, sparoa_path path);
+sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, const void *x,
+                               const void *w, const void *bias, const void *residual,
+                               sparoa_act act, const uint32_t *mask, void *y, void *ws,
+                               size_t ws_bytes, uint64_t *executed, hipStream_t stream);
+
+// Sums split-K fp32 partials [split][M][N] in split order, adds bias and
+// residual, applies the activation, and writes y in dtype.
+sparoa_status launch_split_reduce(sparoa_dtype dt, const float *partial, int split, int64_t M,
+                                  int64_t N, const void *bias, const void *residual,
+                                  sparoa_act act, void *y, hipStream_t stream);
+
+// Writes v to *p on the stream with a one-lane kernel (no memset node).
+sparoa_status launch_set_u64(uint64_t *p, uint64_t v, hipStream_t stream);
+
+// Depthwise direct conv (groups == c_in == c_out).
+sparoa_status launch_depthwise(const sparoa_conv_desc &d, const void *x, const void *w,
+                               const void *bias, const void *residual, sparoa_act act, void *y,
+                               hipStream_t stream);
+
+// FC weight-streaming (bandwidth) kernel over k-major packed weights.
+size_t fc_packed_bytes(const sparoa_fc_desc &d);
+size_t fc_bw_workspace(const sparoa_fc_desc &d, sparoa_path path);
+sparoa_status launch_fc_pack(const sparoa_fc_desc &d, const void *w_nk, void *w_packed,
+                             hipStream_t stream);
+sparoa_status launch_fc_bw(const sparoa_fc_desc &d, sparoa_path path, const void *x,
+                           const void *w_packed, const void *bias, const void *residual,
+                           sparoa_act act,
+                           const uint32_t *mask, void *y, void *ws, size_t ws_bytes,
+                           uint64_t *executed, hipStream_t stream);
+
+sparoa_status launch_maxpool(const void *x, sparoa_dtype dt, int64_t n, int64_t c, int64_t h,
+                             int64_t w, int64_t k, int64_t s, int64_t p, void *y,
+                             hipStream_t stream);
+
+}  // namespace sparoa

@@ -1,0 +1,243 @@
+// Direct NHWC window kernels: depthwise convolution (the bandwidth path of
+// the light quadrant, SparOA Section 2.2 -- a 3x3 depthwise layer does
+// 9 MACs per input element, 1.8 - 4.5 FLOP/byte, far below the ridge point)
+// and max pooling (network glue).
+//
+// One lane owns V consecutive channels (one 16-byte vector) of a run of
+// kRun consecutive output pixels along a row.  The input columns it needs are
+// loaded once per kernel row and reused across the run from registers, the
+// per-channel weights stay in registers, accumulation is fp32.  Lanes of a
+// wave cover consecutive channel vectors, then consecutive pixels, so every
+// load and store is a coalesced 16-byte access; HBM sees each input and
+// output byte about once.
+#include "common.h"
+#include "dtype.h"
+
+namespace sparoa {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kRun = 4;          // output pixels per lane along w
+constexpr int kMaxTaps = 25;     // kernel windows up to 5 x 5 in registers
+
+struct DwArgs {
+  const char *x, *w, *bias, *residual;
+  char *y;
+  int64_t N, H, W, C, Ho, Wo;
+  int kh, kw, sh, sw, ph, pw, dh, dw;
+  int act;
+};
+
+template <int DT, int V>
+__device__ __forceinline__ void load_vec(const char *p, float *out) {
+  using E = Elem<DT>;
+  using raw = typename E::raw;
+  if constexpr (V * E::size == 16) {
+    const uint4 q = *reinterpret_cast<const uint4 *>(p);
+    raw e[V];
+    __builtin_memcpy(e, &q, 16);
+#pragma unroll
+    for (int i = 0; i < V; ++i) out[i] = E::to_f32(e[i]);
+  } else {
+    out[0] = E::to_f32(*reinterpret_cast<const raw *>(p));
+  }
+}
+
+template <int DT, int V>
+__device__ __forceinline__ void store_vec(char *p, const float *v) {
+  using E = Elem<DT>;
+  using raw = typename E::raw;
+  if constexpr (V * E::size == 16) {
+    raw e[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) e[i] = E::from_f32(v[i]);
+    uint4 q;
+    __builtin_memcpy(&q, e, 16);
+    *reinterpret_cast<uint4 *>(p) = q;
+  } else {
+    *reinterpret_cast<raw *>(p) = E::from_f32(v[0]);
+  }
+}
+
+// KH, KW > 0: compile-time window (registers only); 0: runtime window.
+template <int DT, int V, int KH, int KW>
+__global__ __launch_bounds__(kThreads) void depthwise_kernel(DwArgs a) {
+  using E = Elem<DT>;
+  using raw = typename E::raw;
+  constexpr int ESZ = E::size;
+  const int64_t cv = a.C / V;                       // channel vectors per pixel
+  const int64_t runs = (a.Wo + kRun - 1) / kRun;    // pixel runs per output row
+  const int64_t total = a.N * a.Ho * runs * cv;
+  const int kh = KH > 0 ? KH : a.kh, kw = KW > 0 ? KW : a.kw;
+  const int taps = kh * kw;
+  for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kThreads) {
+    const int64_t c0 = (i % cv) * V;
+    const int64_t run = (i / cv) % runs;
+    const int64_t oh = (i / cv / runs) % a.Ho;
+    const int64_t n = i / cv / runs / a.Ho;
+    const int64_t ow0 = run * kRun;
+
+    float wv[KH > 0 ? KH * KW : kMaxTaps][V];
+#pragma unroll
+    for (int t = 0; t < taps; ++t)
+#pragma unroll
+      for (int j = 0; j < V; ++j)
+        wv[t][j] = E::to_f32(reinterpret_cast<const raw *>(a.w)[(c0 + j) * taps + t]);
+
+    float acc[kRun][V];
+#pragma unroll
+    for (int r = 0; r < kRun; ++r)
+#pragma unroll
+      for (int j = 0; j < V; ++j)
+        acc[r][j] = a.bias ? E::to_f32(reinterpret_cast<const raw *>(a.bias)[c0 + j]) : 0.f;
+
+#pragma unroll
+    for (int r = 0; r < kh; ++r) {
+      const int64_t ih = oh * a.sh - a.ph + (int64_t)r * a.dh;
+      if (ih < 0 || ih >= a.H) continue;
+      const char *rowp = a.x + ((n * a.H + ih) * a.W) * a.C * ESZ + c0 * ESZ;
+#pragma unroll
+      for (int s = 0; s < kw; ++s) {
+        const float *wt = wv[r * kw + s];
+#pragma unroll
+        for (int q = 0; q < kRun; ++q) {
+          const int64_t ow = ow0 + q;
+          const int64_t iw = ow * a.sw - a.pw + (int64_t)s * a.dw;
+          if (ow >= a.Wo || iw < 0 || iw >= a.W) continue;
+          float xv[V];
+          load_vec<DT, V>(rowp + iw * a.C * ESZ, xv);
+#pragma unroll
+          for (int j = 0; j < V; ++j) acc[q][j] = fmaf(xv[j], wt[j], acc[q][j]);
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kRun; ++q) {
+      const int64_t ow = ow0 + q;
+      if (ow >= a.Wo) continue;
+      const int64_t o = ((n * a.Ho + oh) * a.Wo + ow) * a.C + c0;
+      if (a.residual) {
+        float rv[V];
+        load_vec<DT, V>(a.residual + o * ESZ, rv);
+#pragma unroll
+        for (int j = 0; j < V; ++j) acc[q][j] += rv[j];
+      }
+      float v[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) v[j] = apply_act(acc[q][j], a.act);
+      store_vec<DT, V>(a.y + o * ESZ, v);
+    }
+  }
+}
+
+template <int DT, int V>
+__global__ __launch_bounds__(kThreads) void maxpool_kernel(const char *x, char *y, int64_t N,
+                                                           int64_t C, int64_t H, int64_t W,
+                                                           int64_t Ho, int64_t Wo, int k, int s,
+                                                           int p) {
+  using E = Elem<DT>;
+  constexpr int ESZ = E::size;
+  const int64_t cv = C / V;
+  const int64_t total = N * Ho * Wo * cv;
+  for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kThreads) {
+    const int64_t c0 = (i % cv) * V, pix = i / cv;
+    const int64_t ow = pix % Wo, oh = (pix / Wo) % Ho, n = pix / Wo / Ho;
+    float best[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) best[j] = -INFINITY;
+    for (int r = 0; r < k; ++r) {
+      const int64_t ih = oh * s - p + r;
+      if (ih < 0 || ih >= H) continue;
+      for (int q = 0; q < k; ++q) {
+        const int64_t iw = ow * s - p + q;
+        if (iw < 0 || iw >= W) continue;
+        float v[V];
+        load_vec<DT, V>(x + (((n * H + ih) * W + iw) * C + c0) * ESZ, v);
+#pragma unroll
+        for (int j = 0; j < V; ++j) best[j] = v[j] > best[j] ? v[j] : best[j];
+      }
+    }
+    store_vec<DT, V>(y + (pix * C + c0) * ESZ, best);
+  }
+}
+
+template <int DT>
+sparoa_status dw_dispatch(const DwArgs &a, hipStream_t st) {
+  constexpr int VV = 16 / Elem<DT>::size;
+  const bool vec = a.C % VV == 0;
+  const int V = vec ? VV : 1;
+  const int64_t total = a.N * a.Ho * cdiv(a.Wo, kRun) * (a.C / V);
+  int64_t blocks = cdiv(total, kThreads);
+  if (blocks > 65536) blocks = 65536;
+  const bool k3 = a.kh == 3 && a.kw == 3;
+  if (vec && k3)
+    hipLaunchKernelGGL((depthwise_kernel<DT, VV, 3, 3>), dim3((unsigned)blocks), dim3(kThreads), 0, st, a);
+  else if (vec)
+    hipLaunchKernelGGL((depthwise_kernel<DT, VV, 0, 0>), dim3((unsigned)blocks), dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((depthwise_kernel<DT, 1, 0, 0>), dim3((unsigned)blocks), dim3(kThreads), 0, st, a);
+  SPAROA_LAUNCH_CHECK("depthwise_kernel");
+  return SPAROA_OK;
+}
+
+template <int DT>
+sparoa_status mp_dispatch(const void *x, void *y, int64_t n, int64_t c, int64_t h, int64_t w,
+                          int64_t ho, int64_t wo, int k, int s, int p, hipStream_t st) {
+  constexpr int VV = 16 / Elem<DT>::size;
+  const bool vec = c % VV == 0;
+  const int64_t total = n * ho * wo * (c / (vec ? VV : 1));
+  int64_t blocks = cdiv(total, kThreads);
+  if (blocks > 65536) blocks = 65536;
+  const char *xp = static_cast<const char *>(x);
+  char *yp = static_cast<char *>(y);
+  if (vec)
+    hipLaunchKernelGGL((maxpool_kernel<DT, VV>), dim3((unsigned)blocks), dim3(kThreads), 0, st, xp,
+                       yp, n, c, h, w, ho, wo, k, s, p);
+  else
+    hipLaunchKernelGGL((maxpool_kernel<DT, 1>), dim3((unsigned)blocks), dim3(kThreads), 0, st, xp,
+                       yp, n, c, h, w, ho, wo, k, s, p);
+  SPAROA_LAUNCH_CHECK("maxpool_kernel");
+  return SPAROA_OK;
+}
+
+}  // namespace
+
+sparoa_status launch_depthwise(const sparoa_conv_desc &d, const void *x, const void *w,
+                               const void *bias, const void *residual, sparoa_act act, void *y,
+                               hipStream_t stream) {
+  if (d.kh * d.kw > kMaxTaps) return fail(SPAROA_ERR_UNSUPPORTED, "depthwise window above 5x5");
+  DwArgs a;
+  a.x = static_cast<const char *>(x);
+  a.w = static_cast<const char *>(w);
+  a.bias = static_cast<const char *>(bias);
+  a.residual = static_cast<const char *>(residual);
+  a.y = static_cast<char *>(y);
+  a.N = d.n; a.H = d.h; a.W = d.w; a.C = d.c_in;
+  a.Ho = (d.h + 2 * d.ph - d.dh * (d.kh - 1) - 1) / d.sh + 1;
+  a.Wo = (d.w + 2 * d.pw - d.dw * (d.kw - 1) - 1) / d.sw + 1;
+  a.kh = (int)d.kh; a.kw = (int)d.kw; a.sh = (int)d.sh; a.sw = (int)d.sw;
+  a.ph = (int)d.ph; a.pw = (int)d.pw; a.dh = (int)d.dh; a.dw = (int)d.dw;
+  a.act = act;
+  switch (d.dtype) {
+    case SPAROA_BF16: return dw_dispatch<SPAROA_BF16>(a, stream);
+    case SPAROA_F16: return dw_dispatch<SPAROA_F16>(a, stream);
+    case SPAROA_F32: return dw_dispatch<SPAROA_F32>(a, stream);
+  }
+  return fail(SPAROA_ERR_INVALID_ARG, "depthwise: dtype");
+}
+
+sparoa_status launch_maxpool(const void *x, sparoa_dtype dt, int64_t n, int64_t c, int64_t h,
+                             int64_t w, int64_t k, int64_t s, int64_t p, void *y,
+                             hipStream_t stream) {
+  const int64_t ho = (h + 2 * p - k) / s + 1, wo = (w + 2 * p - k) / s + 1;
+  switch (dt) {
+    case SPAROA_BF16: return mp_dispatch<SPAROA_BF16>(x, y, n, c, h, w, ho, wo, (int)k, (int)s, (int)p, stream);
+    case SPAROA_F16: return mp_dispatch<SPAROA_F16>(x, y, n, c, h, w, ho, wo, (int)k, (int)s, (int)p, stream);
+    case SPAROA_F32: return mp_dispatch<SPAROA_F32>(x, y, n, c, h, w, ho, wo, (int)k, (int)s, (int)p, stream);
+  }
+  return fail(SPAROA_ERR_INVALID_ARG, "maxpool: dtype");
+}
+
+}  // namespace sparoa

@@ -1,0 +1,53 @@
+// Element types of the kernels: raw storage bits and fp32 conversions.
+#pragma once
+
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "sparoa.h"
+
+namespace sparoa {
+
+template <int DT>
+struct Elem;
+
+template <>
+struct Elem<SPAROA_F32> {
+  using raw = uint32_t;
+  static constexpr int size = 4;
+  __device__ static float to_f32(raw v) { return __uint_as_float(v); }
+  __device__ static raw from_f32(float v) { return __float_as_uint(v); }
+};
+
+template <>
+struct Elem<SPAROA_F16> {
+  using raw = uint16_t;
+  static constexpr int size = 2;
+  __device__ static float to_f32(raw v) { return __half2float(__ushort_as_half(v)); }
+  __device__ static raw from_f32(float v) { return __half_as_ushort(__float2half_rn(v)); }
+};
+
+template <>
+struct Elem<SPAROA_BF16> {
+  using raw = uint16_t;
+  static constexpr int size = 2;
+  // bfloat16 is the upper half of a binary32.
+  __device__ static float to_f32(raw v) { return __uint_as_float((uint32_t)v << 16); }
+  // Round to nearest, ties to even, on the 16 dropped bits; NaN stays a quiet NaN.
+  __device__ static raw from_f32(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (raw)((u >> 16) | 0x0040u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (raw)(u >> 16);
+  }
+};
+
+__device__ __forceinline__ float apply_act(float v, int act) {
+  if (act == SPAROA_ACT_RELU) return v > 0.f ? v : 0.f;
+  if (act == SPAROA_ACT_RELU6) return v > 0.f ? (v < 6.f ? v : 6.f) : 0.f;
+  return v;
+}
+
+}  // namespace sparoa

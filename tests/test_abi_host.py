@@ -1,0 +1,175 @@
+"""Host-side checks of libsparoa.so (no GPU needed): every declared symbol is
+exported, the host-only calls (intensity, routing) match the oracle bit for
+bit, and argument validation rejects bad calls before any device work."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2511_19457_amd import abi
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "sparoa.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    decl = r"^(?:sparoa_status|uint32_t|const char)\s+\*?(sparoa_[a-z0-9_]+)\("
+    return sorted(set(re.findall(decl, text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(abi._L, n), f"{n} declared in sparoa.h but not exported"
+    assert sorted(abi.EXPORTS) == names
+
+
+def test_abi_version_and_status_strings():
+    assert abi.sparoa_abi_version() == 1
+    assert abi.sparoa_status_string(0) == "ok"
+    assert abi.sparoa_status_string(3) == "workspace too small"
+
+
+def _odt(d):
+    return {abi.F32: oracle.F32, abi.F16: oracle.F16, abi.BF16: oracle.BF16}[d]
+
+
+def test_conv_intensity_matches_oracle():
+    g = np.random.default_rng(3)
+    for _ in range(500):
+        groups = int(g.choice([1, 1, 2, 4]))
+        args = dict(n=int(g.integers(1, 64)), c_in=groups * int(g.integers(1, 300)),
+                    h=int(g.integers(1, 300)), w=int(g.integers(1, 300)),
+                    c_out=groups * int(g.integers(1, 300)), kh=int(g.integers(1, 8)),
+                    kw=int(g.integers(1, 8)), sh=int(g.integers(1, 4)), sw=int(g.integers(1, 4)),
+                    ph=int(g.integers(0, 4)), pw=int(g.integers(0, 4)), dh=int(g.integers(1, 3)),
+                    dw=int(g.integers(1, 3)), groups=groups)
+        dt = int(g.integers(0, 3))
+        hb = int(g.integers(0, 2))
+        try:
+            ref = oracle.conv_intensity(*args.values(), dt=_odt(dt), has_bias=hb)
+        except ValueError:
+            with pytest.raises(abi.SparoaError):
+                abi.sparoa_op_intensity_conv(abi.conv_desc(**args, dtype=dt, has_bias=hb))
+            continue
+        got = abi.sparoa_op_intensity_conv(abi.conv_desc(**args, dtype=dt, has_bias=hb))
+        assert got == ref
+
+
+def test_fc_intensity_matches_oracle_and_overflow():
+    g = np.random.default_rng(4)
+    for _ in range(300):
+        m, k, n = (int(v) for v in g.integers(1, 10000, size=3))
+        dt = int(g.integers(0, 3))
+        assert abi.sparoa_op_intensity_fc(abi.fc_desc(m, k, n, dt)) == \
+            oracle.fc_intensity(m, k, n, _odt(dt))
+    with pytest.raises(abi.SparoaError) as e:
+        abi.sparoa_op_intensity_fc(abi.fc_desc(2**40, 2**20, 2**10))
+    assert e.value.status == 1
+
+
+def test_route_matches_oracle():
+    g = np.random.default_rng(5)
+    for _ in range(3000):
+        numel = int(g.integers(1, 10**9))
+        zeros = int(g.integers(0, numel + 1))
+        nb = int(g.integers(0, 1000))
+        zb = int(g.integers(0, nb + 1)) if nb else 0
+        inten = float(g.choice([g.uniform(0, 1000), 315.0, 20.0]))
+        s_thr = float(g.choice([g.uniform(0, 1), 0.5, zeros / numel]))
+        c_thr = float(g.choice([315.0, 20.0, inten]))
+        dw = int(g.integers(0, 2))
+        mode = int(g.integers(0, 2))
+        ref = oracle.route(zeros, numel, zb, nb, inten, dw, s_thr, c_thr, mode)
+        c = dict(zeros=zeros, numel=numel, zero_blocks=zb, num_blocks=nb)
+        i = dict(macs=0, flops=0, bytes=0, intensity=inten)
+        if ref < 0:
+            with pytest.raises(abi.SparoaError):
+                abi.sparoa_route(c, i, dw, s_thr, c_thr, mode)
+        else:
+            assert abi.sparoa_route(c, i, dw, s_thr, c_thr, mode) == ref
+
+
+def test_route_invalid_inputs():
+    c = dict(zeros=1, numel=2, zero_blocks=0, num_blocks=0)
+    i = dict(macs=0, flops=0, bytes=0, intensity=1.0)
+    for args in ((c, i, 0, float("nan"), 1.0, 1), (c, i, 0, 0.5, 1.0, 0), (c, i, 0, 0.5, 1.0, 9)):
+        with pytest.raises(abi.SparoaError) as e:
+            abi.sparoa_route(*args)
+        assert e.value.status == 1
+
+
+def test_mask_words():
+    assert abi.sparoa_mask_words(64, 4096, 16, 16) == (4 * 256 + 31) // 32
+    assert abi.sparoa_mask_words(3, 5, 2, 2) == 1
+    with pytest.raises(abi.SparoaError):
+        abi.sparoa_mask_words(0, 5, 2, 2)
+
+
+FAKE = 0x10000   # an aligned address never dereferenced: calls below fail validation first
+
+
+def test_validation_rejects_before_device_work():
+    d = abi.conv_desc(1, 64, 8, 8, 64, 3, 3, 1, 1, 1, 1)
+    # null x
+    with pytest.raises(abi.SparoaError) as e:
+        abi.sparoa_conv2d(d, abi.PATH_DENSE_MFMA, None, FAKE, None, None, 0, None, FAKE)
+    assert e.value.status == 1
+    # skip path without a mask
+    with pytest.raises(abi.SparoaError) as e:
+        abi.sparoa_conv2d(d, abi.PATH_SKIP_MFMA, FAKE, FAKE, None, None, 0, None, FAKE)
+    assert e.value.status == 1
+    # misaligned pointer
+    with pytest.raises(abi.SparoaError) as e:
+        abi.sparoa_conv2d(d, abi.PATH_DENSE_MFMA, FAKE + 2, FAKE, None, None, 0, None, FAKE)
+    assert e.value.status == 2
+    # grouped non-depthwise conv
+    g2 = abi.conv_desc(1, 64, 8, 8, 64, 3, 3, 1, 1, 1, 1, groups=2)
+    with pytest.raises(abi.SparoaError) as e:
+        abi.sparoa_conv2d(g2, abi.PATH_DENSE_MFMA, FAKE, FAKE, None, None, 0, None, FAKE)
+    assert e.value.status == 2
+    # empty output
+    with pytest.raises(abi.SparoaError) as e:
+        abi.sparoa_op_intensity_conv(abi.conv_desc(1, 4, 2, 2, 4, 5, 5))
+    assert e.value.status == 1
+    # has_bias without bias
+    with pytest.raises(abi.SparoaError) as e:
+        abi.sparoa_fc(abi.fc_desc(4, 64, 64, has_bias=1), 0, FAKE, FAKE, None, None, 0, None,
+                      FAKE)
+    assert e.value.status == 1
+    # BW FC with m > 64 is a valid request the kernel does not take
+    big = abi.fc_desc(65, 64, 64)
+    assert abi.sparoa_fc_skip_block(big, abi.PATH_SKIP_BW) == (65, 1)
+    # measurement: zero rows, samples not dividing rows, misaligned x
+    counts = FAKE
+    for args, status in (((FAKE, 0, 8, 0, 0, 0, counts), 1),
+                         ((FAKE, 6, 8, 0, 0, 4, counts, None, FAKE), 1),
+                         ((FAKE + 8, 6, 8, 0, 0, 0, counts), 2)):
+        with pytest.raises(abi.SparoaError) as e:
+            abi.sparoa_measure_sparsity(*args, dtype=abi.BF16)
+        assert e.value.status == status
+
+
+def test_workspace_too_small_is_reported():
+    # cfg1 conv needs split-K scratch; passing none must fail before launch
+    d = abi.conv_desc(1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, dtype=abi.F32)
+    need = abi.sparoa_conv2d_workspace_size(d, abi.PATH_DENSE_MFMA)
+    assert need > 0
+    with pytest.raises(abi.SparoaError) as e:
+        abi.sparoa_conv2d(d, abi.PATH_DENSE_MFMA, FAKE, FAKE, None, None, 0, None, FAKE)
+    assert e.value.status == 3
+
+
+def test_tiling_and_skip_block_queries():
+    d = abi.conv_desc(32, 256, 14, 14, 256, 3, 3, 1, 1, 1, 1)
+    assert abi.sparoa_conv2d_skip_block(d, abi.PATH_SKIP_MFMA) == (1, 8)
+    tr, kc = abi.sparoa_conv2d_tiling(d, abi.PATH_SKIP_MFMA)
+    assert tr in (64, 128) and kc == 32
+    f = abi.fc_desc(8, 4096, 4096)
+    assert abi.sparoa_fc_skip_block(f, abi.PATH_SKIP_BW) == (8, 1)
+    assert abi.sparoa_fc_tiling(f, abi.PATH_SKIP_BW) == (8, 1)
+    assert abi.sparoa_fc_packed_bytes(f) == 4096 * 4096 * 2
+    assert abi.sparoa_fc_packed_bytes(abi.fc_desc(1, 100, 65)) == 128 * 100 * 2

@@ -1,0 +1,152 @@
+"""GPU parity of the conv paths (implicit-GEMM MFMA dense / zero-skip,
+depthwise bandwidth kernel) and the max-pool glue against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests._util import RTOL, assert_close
+
+pytestmark = pytest.mark.gpu
+
+DT = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+
+
+def _abi():
+    from paper_2511_19457_amd import abi
+    return abi
+
+
+def run_conv(x, w, shape, path, bias=None, residual=None, act=0):
+    """x NHWC, w [co][kh][kw][ci/g] (CPU tensors).  Returns (y, executed, counts)."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, groups = shape
+    d = abi.conv_desc(n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, groups, x.dtype,
+                      has_bias=bias is not None)
+    ho = (h + 2 * ph - dh * (kh - 1) - 1) // sh + 1
+    wo = (wd + 2 * pw - dw * (kw - 1) - 1) // sw + 1
+    xd = x.to(dev)
+    br, bc = abi.sparoa_conv2d_skip_block(d, path)
+    counts = torch.zeros(4, dtype=torch.int64, device=dev)
+    mask = torch.zeros(abi.sparoa_mask_words(n * h * wd, cin, br, bc), dtype=torch.int32,
+                       device=dev)
+    c = abi.sparoa_measure_sparsity_sync(xd, n * h * wd, cin, br, bc, 0, counts, mask)
+    ws = torch.empty(max(16, abi.sparoa_conv2d_workspace_size(d, path)), dtype=torch.uint8,
+                     device=dev)
+    y = torch.full((n, ho, wo, cout), float("nan"), dtype=x.dtype, device=dev)
+    ex = torch.full((1,), -1, dtype=torch.int64, device=dev)
+    abi.sparoa_conv2d(d, path, xd, w.to(dev), None if bias is None else bias.to(dev),
+                      None if residual is None else residual.to(dev), act,
+                      mask if path & 1 else None, y, ws, ex if path & 1 else None)
+    torch.cuda.synchronize()
+    return y.cpu(), int(ex.item()), c
+
+
+def oracle_conv(x, w, shape, bias=None, residual=None, act=0):
+    n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, groups = shape
+    y, a, _ = oracle.conv2d(x, w, n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, groups,
+                            bias=bias, residual=residual, act=act)
+    return y, a
+
+
+GEMM_SHAPES = [
+    # n, cin, h, w, cout, kh, kw, sh, sw, ph, pw, dh, dw, groups
+    (1, 64, 14, 14, 64, 3, 3, 1, 1, 1, 1, 1, 1, 1),
+    (2, 32, 9, 11, 48, 3, 3, 2, 2, 1, 1, 1, 1, 1),
+    (1, 128, 7, 7, 200, 1, 1, 1, 1, 0, 0, 1, 1, 1),
+    (3, 24, 10, 10, 144, 1, 1, 1, 1, 0, 0, 1, 1, 1),   # MobileNetV2-like pointwise
+    (1, 3, 23, 23, 16, 7, 7, 2, 2, 3, 3, 1, 1, 1),     # stem: c_in % 8 != 0
+    (1, 16, 12, 12, 32, 3, 3, 1, 1, 2, 2, 2, 2, 1),    # dilation 2
+    (2, 256, 8, 8, 64, 1, 1, 2, 2, 0, 0, 1, 1, 1),     # strided projection
+]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
+@pytest.mark.parametrize("shape", GEMM_SHAPES)
+def test_conv_dense_vs_oracle(dt, shape):
+    seed = GEMM_SHAPES.index(shape) * 10 + list(DT).index(dt)
+    n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, g = shape
+    ho = (h + 2 * ph - dh * (kh - 1) - 1) // sh + 1
+    wo = (wd + 2 * pw - dw * (kw - 1) - 1) // sw + 1
+    x = synth.relu_normal((n, h, wd, cin), dt, seed)
+    w = synth.he_normal((cout, kh, kw, cin), kh * kw * cin, dt, seed + 1)
+    b = synth.normal((cout,), dt, seed + 2)
+    r = synth.normal((n, ho, wo, cout), dt, seed + 3)
+    y, _, _ = run_conv(x, w, shape, 0, bias=b, residual=r, act=1)
+    yr, ar = oracle_conv(x, w, shape, bias=b, residual=r, act=1)
+    assert_close(y, yr, ar, RTOL[DT[dt]], f"conv {shape} {dt}")
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+@pytest.mark.parametrize("rho", [0.0, 0.9, 0.999, 1.0])
+@pytest.mark.parametrize("shape", [GEMM_SHAPES[0], GEMM_SHAPES[2], GEMM_SHAPES[6],
+                                   (2, 64, 16, 16, 128, 3, 3, 1, 1, 1, 1, 1, 1, 1)])
+def test_conv_skip_equals_dense_and_oracle(dt, rho, shape):
+    n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, g = shape
+    x = synth.sparse_nhwc(n, h, wd, cin, rho, dt, int(rho * 1000) + cin)
+    w = synth.he_normal((cout, kh, kw, cin), kh * kw * cin, dt, cout)
+    yd, _, _ = run_conv(x, w, shape, 0, act=1)
+    ys, ex, _ = run_conv(x, w, shape, 1, act=1)
+    assert torch.equal(yd, ys)
+    yr, ar = oracle_conv(x, w, shape, act=1)
+    assert_close(ys, yr, ar, RTOL[DT[dt]], f"skip conv {shape}")
+    abi = _abi()
+    d = abi.conv_desc(n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, g, DT[dt])
+    tr, kc = abi.sparoa_conv2d_tiling(d, 1)
+    if cin % kc == 0:
+        assert ex == oracle.conv_executed_blocks(x, n, cin, h, wd, kh, kw, sh, sw, ph, pw, dh,
+                                                 dw, tr, kc)
+    if rho == 1.0:
+        assert ex == 0
+
+
+DW_SHAPES = [
+    (2, 32, 12, 12, 32, 3, 3, 1, 1, 1, 1, 1, 1, 32),
+    (1, 96, 15, 15, 96, 3, 3, 2, 2, 1, 1, 1, 1, 96),
+    (1, 144, 8, 9, 144, 3, 3, 1, 1, 1, 1, 1, 1, 144),
+    (1, 12, 7, 7, 12, 5, 5, 1, 1, 2, 2, 1, 1, 12),     # runtime-window kernel
+    (1, 5, 6, 6, 5, 3, 3, 1, 1, 1, 1, 1, 1, 5),        # channels % 8 != 0
+]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
+@pytest.mark.parametrize("shape", DW_SHAPES)
+def test_depthwise_vs_oracle(dt, shape):
+    n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, g = shape
+    ho = (h + 2 * ph - dh * (kh - 1) - 1) // sh + 1
+    wo = (wd + 2 * pw - dw * (kw - 1) - 1) // sw + 1
+    seed = DW_SHAPES.index(shape) * 7
+    x = synth.relu_normal((n, h, wd, cin), dt, seed)
+    w = synth.he_normal((cout, kh, kw, 1), kh * kw, dt, seed + 1)
+    b = synth.normal((cout,), dt, seed + 2)
+    r = synth.normal((n, ho, wo, cout), dt, seed + 3)
+    for path in (2, 3):
+        y, _, _ = run_conv(x, w, shape, path, bias=b, residual=r, act=2)
+        yr, ar = oracle_conv(x, w, shape, bias=b, residual=r, act=2)
+        assert_close(y, yr, ar, RTOL[DT[dt]], f"depthwise {shape} {dt}")
+
+
+def test_config1_full():
+    """Single 3x3 conv 64 -> 64 at 56 x 56, fp32, ReLU(N(0,1)) input."""
+    shape = (1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, 1, 1, 1)
+    x = synth.relu_normal((1, 56, 56, 64), "f32", synth.seed_for(1, 0))
+    w = synth.he_normal((64, 3, 3, 64), 576, "f32", synth.seed_for(1, 1))
+    b = torch.zeros(64)
+    y, _, c = run_conv(x, w, shape, 0, bias=b)
+    yr, ar = oracle_conv(x, w, shape, bias=b)
+    assert_close(y, yr, ar, 1e-5, "config 1")
+    ref = oracle.measure(x, 3136, 64)
+    assert c["zeros"] == ref["zeros"]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
+def test_maxpool_vs_oracle(dt):
+    abi = _abi()
+    x = synth.normal((2, 17, 18, 64), dt, 123)
+    y = torch.empty(2, 9, 9, 64, dtype=DT[dt], device="cuda")
+    abi.sparoa_maxpool2d(x.cuda(), 2, 64, 17, 18, 3, 2, 1, y)
+    torch.cuda.synchronize()
+    ref = oracle.maxpool2d(x, 2, 64, 17, 18)
+    assert np.array_equal(y.float().cpu().numpy().astype(np.float64), ref)

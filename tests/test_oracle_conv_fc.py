@@ -19,12 +19,12 @@ def _torch_conv(x, w, n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, group
     wt = _f64(w).permute(0, 3, 1, 2)                 # [co][kh][kw][ci] -> [co][ci][kh][kw]
     y = F.conv2d(xt, wt, None if bias is None else _f64(bias), stride=(sh, sw),
                  padding=(ph, pw), dilation=(dh, dw), groups=groups).permute(0, 2, 3, 1)
+    if residual is not None:
+        y = y + _f64(residual)
     if act == oracle.ACT_RELU:
         y = torch.relu(y)
     elif act == oracle.ACT_RELU6:
         y = torch.clamp(y, 0, 6)
-    if residual is not None:
-        y = y + _f64(residual)
     return y.numpy()
 
 
@@ -87,8 +87,9 @@ def test_fc_vs_numpy_matmul(dt):
     x = synth.normal((m, k), dt, 21)
     w = synth.normal((n, k), dt, 22)
     b = synth.normal((n,), dt, 23)
-    y, a = oracle.fc(x, w, m, k, n, bias=b)
-    ref = _f64(x).numpy() @ _f64(w).numpy().T + _f64(b).numpy()
+    r = synth.normal((m, n), dt, 24)
+    y, a = oracle.fc(x, w, m, k, n, bias=b, residual=r, act=oracle.ACT_RELU)
+    ref = np.maximum(_f64(x).numpy() @ _f64(w).numpy().T + _f64(b).numpy() + _f64(r).numpy(), 0)
     assert np.all(np.abs(y - ref) <= 1e-13 * a)
 
 
