@@ -1,0 +1,310 @@
+#!/usr/bin/env python3
+"""Benchmark of the SparOA hot path on one MI355X: the FC/GEMM sparsity sweep.
+
+Workload (one "step"): 24 FC operators y = x w^T, x [m, 4096], w [4096, 4096]
+bf16 ~ N(0, 1/4096), m in {1, 8, 64}, activation sparsity rho in
+{0, 0.5, 0.8, 0.95}, zeros placed i.i.d. or as 16 x 16 blocks, nonzeros
+|N(0, 1)|.  Every operator has its own weight matrix (24 x 32 MiB, more than
+the 256 MB Infinity Cache holds), so weights stream from HBM.  Per operator
+the step runs the whole path: intensity from the shape (host), sparsity
+measurement (GPU) with the counts read back, routing (host), and the routed
+FC kernel.  Inputs are resident in HBM before timing starts.
+
+value = dense-equivalent TFLOP/s of the step: sum over operators of
+2 m k n divided by the step time (skipped work counts as done).
+
+Prints one JSON line on stdout.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("dense-equiv TFLOP/s & HBM GB/s vs activation sparsity; per-model latency @1 GPU")
+HBM_PEAK_GBS = 8000.0
+M_LIST = (1, 8, 64)
+RHO_LIST = (0.0, 0.5, 0.8, 0.95)
+PATTERNS = ("iid", "block")
+K = N = 4096
+INTENSITY_THR = 315.0   # bf16 ridge point of MI355X: 2.5 PFLOP/s / 8 TB/s (datasheet)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--cpu-seconds", type=float, default=20.0,
+                   help="bound on the oracle CPU-baseline sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--sparsity-thr", type=float, default=None,
+                   help="routing threshold; default: calibrated from forced-path timings")
+    p.add_argument("--cases-out", default=None, help="write the per-case table (JSON) here")
+    return p.parse_args()
+
+
+def case_list():
+    out = []
+    for m in M_LIST:
+        for rho in RHO_LIST:
+            for pat in PATTERNS:
+                out.append((m, rho, pat))
+    return out
+
+
+def source_digest():
+    h = hashlib.sha256()
+    for f in ("fc_bw.hip", "measure.hip"):
+        with open(os.path.join(ROOT, "paper_2511_19457_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(digest):
+    """HBM traffic per FC launch measured by rocprofv3 counters, if taken on
+    the current kernel source (profiles/fc_bw_kernel_fc_sweep_traffic.json)."""
+    path = os.path.join(ROOT, "profiles", "fc_bw_kernel_fc_sweep_traffic.json")
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_digest") != digest:
+        return None
+    return t.get("bytes_per_launch")
+
+
+class Case:
+    pass
+
+
+def build_cases(abi, torch, synth, dev):
+    cases = []
+    for idx, (m, rho, pat) in enumerate(case_list()):
+        c = Case()
+        c.idx, c.m, c.rho, c.pattern = idx, m, rho, pat
+        c.seed_x = synth.seed_for(2, idx)
+        c.seed_w = synth.seed_for(2, 50 + idx)
+        c.x_cpu = synth.sparse_matrix(m, K, rho, pat, "bf16", c.seed_x)
+        c.desc = abi.fc_desc(m, K, N, abi.BF16)
+        c.x = c.x_cpu.to(dev)
+        w = synth.normal((N, K), "bf16", c.seed_w, std=1.0 / 64.0).to(dev)
+        c.wp = torch.empty(abi.sparoa_fc_packed_bytes(c.desc) // 2, dtype=torch.bfloat16,
+                           device=dev)
+        abi.sparoa_fc_pack_weights(c.desc, w, c.wp)
+        c.w = w                      # [n][k] for the MFMA paths
+        c.inten = abi.sparoa_op_intensity_fc(c.desc)
+        fam_skip = abi.PATH_SKIP_BW if c.inten["intensity"] < INTENSITY_THR else abi.PATH_SKIP_MFMA
+        c.br, c.bc = abi.sparoa_fc_skip_block(c.desc, fam_skip)
+        c.counts = torch.zeros(4, dtype=torch.int64, device=dev)
+        c.mask = torch.zeros(abi.sparoa_mask_words(m, K, c.br, c.bc), dtype=torch.int32,
+                             device=dev)
+        ws = max(abi.sparoa_fc_workspace_size(c.desc, p) for p in range(4))
+        c.ws = torch.zeros(max(16, ws), dtype=torch.uint8, device=dev)
+        c.y = torch.empty(m, N, dtype=torch.bfloat16, device=dev)
+        cases.append(c)
+    torch.cuda.synchronize()
+    for c in cases:   # only the packed copy is needed by the bandwidth paths
+        if c.inten["intensity"] < INTENSITY_THR:
+            c.w = None
+    torch.cuda.empty_cache()
+    return cases
+
+
+def run_case(abi, c, s_thr, ev=None):
+    """One operator through the whole path; returns the routed path."""
+    counts = abi.sparoa_measure_sparsity_sync(c.x, c.m, K, c.br, c.bc, 0, c.counts, c.mask)
+    path = abi.sparoa_route(counts, c.inten, 0, s_thr, INTENSITY_THR)
+    w = c.wp if path & 2 else c.w
+    if ev is not None:
+        ev[0].record()
+    abi.sparoa_fc(c.desc, path, c.x, w, None, None, abi.ACT_NONE, c.mask if path & 1 else None,
+                  c.y, c.ws)
+    if ev is not None:
+        ev[1].record()
+    c.counts_host = counts
+    return path
+
+
+def forced_times(abi, torch, c, paths, reps=20):
+    """Median duration (us) of the FC kernel on each forced path (HIP events)."""
+    out = {}
+    abi.sparoa_measure_sparsity_sync(c.x, c.m, K, c.br, c.bc, 0, c.counts, c.mask)
+    for p in paths:
+        w = c.wp if p & 2 else c.w
+        if w is None:
+            continue
+        ts = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            abi.sparoa_fc(c.desc, p, c.x, w, None, None, abi.ACT_NONE, c.mask if p & 1 else None,
+                          c.y, c.ws)
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3)
+        ts.sort()
+        out[p] = ts[len(ts) // 2]
+    return out
+
+
+def alg_bytes(c, path, nonzero_cols):
+    """Algorithmic HBM bytes of one FC launch: x, y and the weight rows the
+    path must read (all of them, or only the nonzero input columns')."""
+    rows = nonzero_cols if path & 1 else K
+    return 2 * (c.m * K + c.m * N) + 2 * rows * N
+
+
+def cpu_baseline_timed(cases, budget_s):
+    """The oracle (C, double precision, OpenMP) on a bounded sample of the
+    same sweep: measure + route + FC per operator, in case order, until the
+    time budget is spent (weight generation excluded); returns the
+    dense-equivalent flops done and the time taken."""
+    import oracle
+    import synth
+    flops, elapsed, done = 0, 0.0, []
+    for c in cases:
+        w_cpu = synth.normal((N, K), "bf16", c.seed_w, std=1.0 / 64.0)   # not timed
+        t1 = time.perf_counter()
+        st = oracle.measure(c.x_cpu, c.m, K, c.m, 1)
+        path = oracle.route(st["zeros"], st["numel"], st["zero_blocks"], st["num_blocks"],
+                            c.inten["intensity"], 0, 0.5, INTENSITY_THR)
+        oracle.fc(c.x_cpu, w_cpu, c.m, K, N,
+                  skip_mask=st["mask"] if path & 1 else None, skip_rows=c.m, skip_cols=1)
+        elapsed += time.perf_counter() - t1
+        flops += 2 * c.m * K * N
+        done.append(f"m{c.m}/rho{c.rho}/{c.pattern}")
+        if elapsed > budget_s:
+            break
+    return flops, elapsed, done
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
+              "(the hot path shards by batch with no exchange; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    import synth
+    from paper_2511_19457_amd import abi
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    print("bench: building 24 FC operators (packing weights)", file=sys.stderr, flush=True)
+    cases = build_cases(abi, torch, synth, dev)
+
+    # Forced-path timings per case (untimed phase): the sparsity sweep of the
+    # metric, and the data the routing threshold is calibrated from.
+    print("bench: forced-path sweep", file=sys.stderr, flush=True)
+    for c in cases:
+        c.forced = forced_times(abi, torch, c, (abi.PATH_DENSE_BW, abi.PATH_SKIP_BW))
+        st = c.counts.cpu().tolist()
+        c.rho_e = st[0] / st[1]
+        c.rho_b = st[2] / st[3]
+    if args.sparsity_thr is None:
+        # smallest block sparsity above which the skip path wins in every case
+        pts = sorted((c.rho_b, c.forced[abi.PATH_SKIP_BW] < c.forced[abi.PATH_DENSE_BW])
+                     for c in cases)
+        s_thr = 1.0
+        for rb, wins in reversed(pts):
+            if not wins:
+                break
+            s_thr = rb
+        s_thr = max(s_thr, 1e-9)
+    else:
+        s_thr = args.sparsity_thr
+
+    print(f"bench: warmup {args.warmup} steps, sparsity threshold {s_thr:.4g}", file=sys.stderr,
+          flush=True)
+    for _ in range(args.warmup):
+        for c in cases:
+            run_case(abi, c, s_thr)
+    torch.cuda.synchronize()
+
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in cases] for _ in range(args.steps)]
+    paths = [None] * len(cases)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        for i, c in enumerate(cases):
+            paths[i] = run_case(abi, c, s_thr, evs[s][i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    step_s = (t1 - t0) / args.steps
+    print(f"bench: timed {args.steps} steps, {step_s * 1e3:.3f} ms/step", file=sys.stderr,
+          flush=True)
+
+    flops_step = sum(2 * c.m * K * N for c in cases)
+    value = flops_step / step_s / 1e12
+
+    # live kernel durations of the routed FC launches (HIP events on the
+    # stream the library launches on)
+    kern_us = [sum(evs[s][i][0].elapsed_time(evs[s][i][1]) for s in range(args.steps)) * 1e3 /
+               args.steps for i in range(len(cases))]
+    table = []
+    tot_bytes = 0
+    for i, c in enumerate(cases):
+        nz_cols = c.counts_host["num_blocks"] - c.counts_host["zero_blocks"]
+        b = alg_bytes(c, paths[i], nz_cols)
+        tot_bytes += b
+        table.append(dict(
+            m=c.m, rho=c.rho, pattern=c.pattern, rho_e=round(c.rho_e, 4),
+            rho_b=round(c.rho_b, 4), path=abi.PATH_NAMES[paths[i]], us=round(kern_us[i], 2),
+            alg_bytes=b, gbps=round(b / kern_us[i] / 1e3, 1),
+            dense_equiv_tflops=round(2 * c.m * K * N / kern_us[i] / 1e6, 2),
+            dense_bw_us=round(c.forced[abi.PATH_DENSE_BW], 2),
+            skip_bw_us=round(c.forced[abi.PATH_SKIP_BW], 2)))
+    launches = len(cases)
+    achieved = tot_bytes / launches / (sum(kern_us) / launches * 1e-6) / 1e9
+    digest = source_digest()
+    traffic = load_traffic(digest)
+    roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
+                    kernel="fc_bw_kernel", alg_bytes_per_launch=int(tot_bytes / launches),
+                    source_digest=digest)
+    measure_bytes = sum(2 * c.m * K for c in cases)
+
+    line = dict(
+        metric=METRIC, value=round(value, 3), unit="TFLOP/s", n_gpus=1, steps=args.steps,
+        warmup=args.warmup, ms_per_step=round(step_s * 1e3, 4), higher_is_better=True,
+        scaling="weak", vs_baseline=None, dtype="bf16", data="synthetic",
+        config=dict(workload="fc_sweep: 24 FC operators, x [m,4096] (m in 1,8,64; sparsity "
+                             "0/0.5/0.8/0.95 i.i.d. or 16x16 blocks) x w [4096,4096] bf16, "
+                             "one weight matrix per operator; measure+route+execute each",
+                    global_batch=sum(M_LIST) * len(RHO_LIST) * len(PATTERNS),
+                    sparsity_thr=s_thr, intensity_thr=INTENSITY_THR, route_mode="block"),
+        hbm_gbps_step=round((tot_bytes + measure_bytes) / step_s / 1e9, 1),
+        roofline=roofline,
+        sweep=table,
+    )
+    if not args.no_cpu_baseline:
+        print("bench: oracle CPU baseline", file=sys.stderr, flush=True)
+        flops, elapsed, done = cpu_baseline_timed(cases, args.cpu_seconds)
+        cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        line["cpu_baseline"] = dict(
+            value=round(flops / elapsed / 1e12, 6), unit="TFLOP/s", cores=cores, kind="oracle",
+            sample=f"first {len(done)} of 24 sweep operators in case order "
+                   f"({done[0]} .. {done[-1]}): oracle measure + route + FC in double, "
+                   f"{elapsed:.1f} s")
+    else:
+        line["cpu_baseline"] = None
+    if args.cases_out:
+        with open(args.cases_out, "w") as f:
+            json.dump(table, f, indent=1)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

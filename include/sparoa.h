@@ -216,10 +216,11 @@ sparoa_status sparoa_conv2d_zero_skip(const sparoa_conv_desc *desc, const void *
  * Fully connected (SparOA Sections 1 and 2.1).
  * y = act(x w^T + bias + residual); residual [m][n] nullable.
  *   Paths: DENSE_MFMA / SKIP_MFMA : tiled MFMA GEMM, w in [n][k];
- *          DENSE_BW / SKIP_BW     : weight-streaming kernel for m <= 64,
- *                                   w in the packed layout of
- *                                   sparoa_fc_pack_weights (k-major [k][n]),
- *                                   each weight byte read at most once.
+ *          DENSE_BW / SKIP_BW     : weight-streaming kernel for m <= 64 and
+ *                                   k <= 16384, 16-bit dtypes, w in the
+ *                                   packed layout of sparoa_fc_pack_weights,
+ *                                   each weight byte read at most once; no
+ *                                   workspace.
  *   Skip paths need `mask` of x measured over [m, k] with the block shape of
  *   sparoa_fc_skip_block ((1, 8) for SKIP_MFMA, (m, 1) for SKIP_BW):
  *   SKIP_MFMA skips (row tile, K chunk) pairs whose input block is zero;
@@ -229,8 +230,8 @@ sparoa_status sparoa_conv2d_zero_skip(const sparoa_conv_desc *desc, const void *
  *   pairs (SKIP_MFMA) or nonzero columns (SKIP_BW).
  * Errors as for sparoa_conv2d; UNSUPPORTED for m > 64 on a BW path.
  * ---------------------------------------------------------------------- */
-/* Packed weights for the BW paths: 64-column panels, k-major inside a panel:
- * packed[p][k][0..63] = w[64p + 0..63][k] (zero past n).  w_packed must hold
+/* Packed weights for the BW paths: 16-column panels, k-major inside a panel:
+ * packed[p][k][0..15] = w[16p + 0..15][k] (zero past n).  w_packed must hold
  * sparoa_fc_packed_bytes() bytes and must not alias w_nk.  16-bit dtypes. */
 sparoa_status sparoa_fc_packed_bytes(const sparoa_fc_desc *desc, size_t *bytes);
 sparoa_status sparoa_fc_pack_weights(const sparoa_fc_desc *desc, const void *w_nk,

@@ -2,11 +2,11 @@
 // bitmap and per-sample zero counts of an activation tensor, in one coalesced
 // pass over HBM.
 //
-// Work item = (block row, group of V consecutive columns).  A lane loads the
-// V elements of its group (one 16-byte load for V = 16 / element size) in
-// every row of its block row, tests the raw magnitude bits (+0 and -0 are
-// zero; subnormals, NaN and Inf are not; no float compare, so FTZ/DAZ cannot
-// matter) and keeps a V-bit "nonzero seen" flag.  Consecutive lanes hold
+// Work item = (block row, chunk of up to 4 of its rows, group of V consecutive
+// columns).  A lane loads the V elements of its group (one 16-byte load for
+// V = 16 / element size) in each row of its chunk, tests the raw magnitude
+// bits (+0 and -0 are zero; subnormals, NaN and Inf are not; no float
+// compare, so FTZ/DAZ cannot matter) and keeps a V-bit "nonzero seen" flag.  Consecutive lanes hold
 // consecutive items, so a wave covers a contiguous run of bitmap bits: the
 // wave ORs its bits per bitmap word across lanes (shuffles) and one lane per
 // word issues the atomicOr.  The old word returned by atomicOr tells which
@@ -19,7 +19,8 @@ namespace sparoa {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;  // items per lane in flight
+constexpr int kUnroll = 4;    // items per lane in flight
+constexpr int kRowChunk = 4;  // rows of one block handled by one lane
 
 __global__ void measure_init(sparoa_counts *counts, uint64_t numel, uint64_t nb, uint32_t *mask,
                              int64_t words, uint64_t *per_sample, int64_t samples) {
@@ -107,60 +108,63 @@ __device__ __forceinline__ uint32_t nonzero_bits(const char *p) {
 
 // grid = (x: work-groups per sample, y: samples).  Sample s covers rows
 // [s*rs, s*rs + rs); its block rows are numbered s*nbr_s + local index.
+// Work item = (block row, chunk of kRowChunk rows inside it, column group):
+// chunks of one block OR their flags into the same bitmap bits, so tall
+// blocks still spread over many lanes.  The kUnroll item slots of a lane are
+// a grid-width apart, keeping each wave on a contiguous run of items.
 template <int ESZ, int V>
 __global__ __launch_bounds__(kThreads) void measure_main(
     const char *__restrict__ x, int64_t cols, int64_t rs, int64_t br, int64_t bc, int64_t nbc,
-    int64_t nbr_s, int64_t gpr, uint32_t *__restrict__ mask, sparoa_counts *counts,
+    int64_t nbr_s, int64_t cpb, int64_t gpr, uint32_t *__restrict__ mask, sparoa_counts *counts,
     uint64_t *per_sample) {
   const int64_t s = blockIdx.y;
-  const int64_t items = nbr_s * gpr;
+  const int64_t per_block = cpb * gpr;
+  const int64_t items = nbr_s * per_block;
   const int64_t row_bytes = cols * ESZ;
+  const int64_t slot = (int64_t)gridDim.x * kThreads;
   uint64_t zeros = 0;
   uint32_t newly = 0;
-  for (int64_t base = (int64_t)blockIdx.x * kThreads * kUnroll; base < items;
-       base += (int64_t)gridDim.x * kThreads * kUnroll) {
+  for (int64_t base = (int64_t)blockIdx.x * kThreads; base < items;
+       base += slot * kUnroll) {
     uint32_t nz[kUnroll];
-    bool valid[kUnroll];
+    int64_t bitpos[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int64_t item = base + u * kThreads + threadIdx.x;
-      valid[u] = item < items;
+      const int64_t item = base + u * slot + threadIdx.x;
       nz[u] = 0;
-      if (valid[u]) {
-        const int64_t bi = item / gpr, g = item - bi * gpr;
-        const int64_t r0 = s * rs + bi * br;
-        const int64_t r1 = min(r0 + br, s * rs + rs);
+      bitpos[u] = -1;
+      if (item < items) {
+        const int64_t bi = item / per_block, rem = item - bi * per_block;
+        const int64_t rc = rem / gpr, g = rem - rc * gpr;
+        const int64_t blk0 = s * rs + bi * br;
+        const int64_t r0 = blk0 + rc * kRowChunk;
+        const int64_t r1 = min(min(r0 + kRowChunk, blk0 + br), s * rs + rs);
         const char *p = x + r0 * row_bytes + g * V * ESZ;
-#pragma unroll 4
+#pragma unroll
         for (int64_t r = r0; r < r1; ++r, p += row_bytes) {
           const uint32_t b = nonzero_bits<ESZ, V>(p);
           zeros += V - __popc(b);
           nz[u] |= b;
         }
+        bitpos[u] = (s * nbr_s + bi) * nbc + (g * V) / bc;
       }
     }
     if (mask) {
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
-        const int64_t item = base + u * kThreads + threadIdx.x;
         int word = 0;
         uint32_t lo = 0, hi = 0;
-        if (valid[u]) {
-          const int64_t bi = item / gpr, g = item - bi * gpr;
-          const int64_t row_base = (s * nbr_s + bi) * nbc;
+        if (bitpos[u] >= 0) {
           uint32_t lbits;
-          int64_t b0;
           if (V == 1 || bc % V == 0) {  // the V columns lie in one block
-            b0 = row_base + (g * V) / bc;
             lbits = nz[u] != 0u;
           } else {  // V % bc == 0: V / bc blocks per lane
-            b0 = row_base + (g * V) / bc;
             lbits = 0;
             const uint32_t bm = (1u << bc) - 1u;
             for (int j = 0; j < V / bc; ++j) lbits |= ((nz[u] >> (j * bc)) & bm ? 1u : 0u) << j;
           }
-          word = (int)(b0 >> 5);
-          const uint64_t sh = (uint64_t)lbits << (b0 & 31);
+          word = (int)(bitpos[u] >> 5);
+          const uint64_t sh = (uint64_t)lbits << (bitpos[u] & 31);
           lo = (uint32_t)sh;
           hi = (uint32_t)(sh >> 32);
         }
@@ -182,11 +186,11 @@ __global__ __launch_bounds__(kThreads) void measure_main(
 
 template <int ESZ, int V>
 void launch_main(dim3 grid, hipStream_t st, const void *x, int64_t cols, int64_t rs, int64_t br,
-                 int64_t bc, int64_t nbc, int64_t nbr_s, uint32_t *mask, sparoa_counts *counts,
-                 uint64_t *per_sample) {
+                 int64_t bc, int64_t nbc, int64_t nbr_s, int64_t cpb, uint32_t *mask,
+                 sparoa_counts *counts, uint64_t *per_sample) {
   hipLaunchKernelGGL((measure_main<ESZ, V>), grid, dim3(kThreads), 0, st,
-                     static_cast<const char *>(x), cols, rs, br, bc, nbc, nbr_s, cols / V, mask,
-                     counts, per_sample);
+                     static_cast<const char *>(x), cols, rs, br, bc, nbc, nbr_s, cpb, cols / V,
+                     mask, counts, per_sample);
 }
 
 }  // namespace
@@ -218,22 +222,23 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
 
   const bool vec = cols % vw == 0 && (!want_mask || bc % vw == 0 || vw % bc == 0);
   const int V = vec ? vw : 1;
-  const int64_t items_s = nbr_s * (cols / V);
-  int64_t gx = cdiv(items_s, (int64_t)kThreads * kUnroll);
+  const int64_t cpb = cdiv(br < rs ? br : rs, kRowChunk);   // row chunks per block row
+  const int64_t items_s = nbr_s * cpb * (cols / V);
+  int64_t gx = cdiv(items_s, (int64_t)kThreads);
   const int64_t cap = cdiv(2048, S);
   if (gx > cap) gx = cap;
   if (gx < 1) gx = 1;
   dim3 grid((unsigned)gx, (unsigned)S);
   if (esz == 2) {
     if (vec)
-      launch_main<2, 8>(grid, stream, x, cols, rs, br, bc, nbc, nbr_s, mask, counts, per_sample);
+      launch_main<2, 8>(grid, stream, x, cols, rs, br, bc, nbc, nbr_s, cpb, mask, counts, per_sample);
     else
-      launch_main<2, 1>(grid, stream, x, cols, rs, br, bc, nbc, nbr_s, mask, counts, per_sample);
+      launch_main<2, 1>(grid, stream, x, cols, rs, br, bc, nbc, nbr_s, cpb, mask, counts, per_sample);
   } else {
     if (vec)
-      launch_main<4, 4>(grid, stream, x, cols, rs, br, bc, nbc, nbr_s, mask, counts, per_sample);
+      launch_main<4, 4>(grid, stream, x, cols, rs, br, bc, nbc, nbr_s, cpb, mask, counts, per_sample);
     else
-      launch_main<4, 1>(grid, stream, x, cols, rs, br, bc, nbc, nbr_s, mask, counts, per_sample);
+      launch_main<4, 1>(grid, stream, x, cols, rs, br, bc, nbc, nbr_s, cpb, mask, counts, per_sample);
   }
   SPAROA_LAUNCH_CHECK("measure_main");
   return SPAROA_OK;

@@ -1,0 +1,154 @@
+"""Per-layer driver: measure -> route -> execute over a layer stack.
+
+For every conv/FC layer (SparOA Section 3.1 features, Section 2.2 quadrants,
+Section 5 online execution on one device):
+  1. intensity from the shape (host, Eq. 2);
+  2. the kernel family the intensity selects (bandwidth when light or
+     depthwise, MFMA otherwise) fixes the skip granularity of its zero-skip
+     kernel; the input activation is measured at that granularity on the GPU
+     (Eq. 1) and the four counts are read back -- the one host/device
+     synchronisation per layer;
+  3. sparoa_route picks one of the four paths;
+  4. the routed kernel runs with the fused epilogue (bias, residual,
+     activation), producing the next layer's input.
+Max pooling is glue and is not routed.  All computation is in libsparoa.so;
+this module only allocates buffers (PyTorch) and sequences the C calls.
+"""
+import time
+from dataclasses import dataclass
+
+import torch
+
+from . import abi
+from .stacks import Layer, input_shape, output_shape
+
+
+@dataclass
+class LayerRecord:
+    name: str
+    kind: str
+    rho_e: float = 0.0
+    rho_b: float = 0.0
+    intensity: float = 0.0
+    macs: int = 0
+    bytes: int = 0
+    path: int = -1
+    us: float = 0.0
+
+
+class Engine:
+    """Holds weights and per-layer buffers of one stack on one device."""
+
+    def __init__(self, layers, dtype, device, seed=0, sparsity_thr=0.5, intensity_thr=315.0,
+                 mode=abi.ROUTE_BLOCK, weights=None):
+        import synth
+        self.layers = layers
+        self.dtype = dtype
+        self.dev = torch.device(device)
+        self.s_thr, self.c_thr, self.mode = sparsity_thr, intensity_thr, mode
+        self.st = []
+        self.acts = [None] * (len(layers) + 1)
+        for i, L in enumerate(layers):
+            st = {}
+            if L.kind != "maxpool":
+                s = L.shape
+                if L.kind == "conv":
+                    d = abi.conv_desc(s["n"], s["cin"], s["h"], s["w"], s["cout"], s["kh"],
+                                      s["kw"], s["sh"], s["sw"], s["ph"], s["pw"], 1, 1,
+                                      s["groups"], dtype)
+                    st["inten"] = abi.sparoa_op_intensity_conv(d)
+                    wshape = (s["cout"], s["kh"], s["kw"], s["cin"] // s["groups"])
+                    fan_in = s["kh"] * s["kw"] * s["cin"] // s["groups"]
+                    st["rows"], st["cols"] = s["n"] * s["h"] * s["w"], s["cin"]
+                    fam = abi.PATH_DENSE_BW if (L.depthwise or st["inten"]["intensity"] <
+                                                self.c_thr) else abi.PATH_DENSE_MFMA
+                    st["br"], st["bc"] = abi.sparoa_conv2d_skip_block(d, fam | 1)
+                    ws = max(abi.sparoa_conv2d_workspace_size(d, p) for p in range(4))
+                else:
+                    d = abi.fc_desc(s["m"], s["k"], s["n"], dtype)
+                    st["inten"] = abi.sparoa_op_intensity_fc(d)
+                    wshape = (s["n"], s["k"])
+                    fan_in = s["k"]
+                    st["rows"], st["cols"] = s["m"], s["k"]
+                    fam = abi.PATH_DENSE_BW if st["inten"]["intensity"] < self.c_thr \
+                        else abi.PATH_DENSE_MFMA
+                    st["br"], st["bc"] = abi.sparoa_fc_skip_block(d, fam | 1)
+                    ws = max(abi.sparoa_fc_workspace_size(d, p) for p in (fam, fam | 1))
+                st["desc"], st["family"] = d, fam
+                if weights is not None:
+                    w = weights[i].to(self.dev)
+                else:
+                    w = synth.he_normal(wshape, fan_in, dtype, seed + 1000 + i).to(self.dev)
+                st["w"] = w
+                if L.kind == "fc" and fam & 2:
+                    wp = torch.empty(abi.sparoa_fc_packed_bytes(d) // w.element_size(),
+                                     dtype=dtype, device=self.dev)
+                    abi.sparoa_fc_pack_weights(d, w, wp)
+                    st["wp"] = wp
+                st["counts"] = torch.zeros(4, dtype=torch.int64, device=self.dev)
+                st["mask"] = torch.zeros(
+                    abi.sparoa_mask_words(st["rows"], st["cols"], st["br"], st["bc"]),
+                    dtype=torch.int32, device=self.dev)
+                st["ws"] = torch.zeros(max(16, ws), dtype=torch.uint8, device=self.dev)
+            self.acts[i + 1] = torch.empty(output_shape(L), dtype=dtype, device=self.dev)
+            self.st.append(st)
+        torch.cuda.synchronize(self.dev)
+
+    def weights_cpu(self):
+        return [st.get("w").cpu() if "w" in st else None for st in self.st]
+
+    def run_layer(self, i, force_path=None):
+        """Runs layer i on the activations already in place; returns its record."""
+        L, st = self.layers[i], self.st[i]
+        x = self.acts[L.src]
+        y = self.acts[i + 1]
+        rec = LayerRecord(L.name, L.kind)
+        if L.kind == "maxpool":
+            s = L.shape
+            abi.sparoa_maxpool2d(x, s["n"], s["c"], s["h"], s["w"], s["k"], s["s"], s["p"], y)
+            return rec
+        c = abi.sparoa_measure_sparsity_sync(x, st["rows"], st["cols"], st["br"], st["bc"], 0,
+                                             st["counts"], st["mask"])
+        inten = st["inten"]
+        path = abi.sparoa_route(c, inten, int(L.depthwise), self.s_thr, self.c_thr, self.mode)
+        if force_path is not None:
+            path = force_path
+        res = self.acts[L.res] if L.res is not None else None
+        mask = st["mask"] if path & 1 else None
+        if L.kind == "conv":
+            abi.sparoa_conv2d(st["desc"], path, x, st["w"], None, res, L.act, mask, y, st["ws"])
+        else:
+            w = st["wp"] if (path & 2) else st["w"]
+            abi.sparoa_fc(st["desc"], path, x, w, None, res, L.act, mask, y, st["ws"])
+        rec.rho_e = c["zeros"] / c["numel"]
+        rec.rho_b = c["zero_blocks"] / c["num_blocks"] if c["num_blocks"] else 0.0
+        rec.intensity, rec.macs, rec.bytes = inten["intensity"], inten["macs"], inten["bytes"]
+        rec.path = path
+        rec.counts = c
+        return rec
+
+    def run(self, x, timed=False):
+        """Full stack on input x (device tensor of the input shape); returns
+        (output, records, wall seconds)."""
+        assert tuple(x.shape) == input_shape(self.layers) and x.dtype == self.dtype
+        self.acts[0] = x
+        recs = []
+        torch.cuda.synchronize(self.dev)
+        t0 = time.perf_counter()
+        for i in range(len(self.layers)):
+            if timed:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+            r = self.run_layer(i)
+            if timed:
+                e1.record()
+                r._ev = (e0, e1)
+            recs.append(r)
+        torch.cuda.synchronize(self.dev)
+        wall = time.perf_counter() - t0
+        if timed:
+            for r in recs:
+                r.us = r._ev[0].elapsed_time(r._ev[1]) * 1e3
+                del r._ev
+        return self.acts[len(self.layers)], recs, wall

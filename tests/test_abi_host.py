@@ -172,4 +172,4 @@ def test_tiling_and_skip_block_queries():
     assert abi.sparoa_fc_skip_block(f, abi.PATH_SKIP_BW) == (8, 1)
     assert abi.sparoa_fc_tiling(f, abi.PATH_SKIP_BW) == (8, 1)
     assert abi.sparoa_fc_packed_bytes(f) == 4096 * 4096 * 2
-    assert abi.sparoa_fc_packed_bytes(abi.fc_desc(1, 100, 65)) == 128 * 100 * 2
+    assert abi.sparoa_fc_packed_bytes(abi.fc_desc(1, 100, 65)) == 80 * 100 * 2   # 16-column panels

@@ -40,7 +40,7 @@ def run_fc(x, w, bias, act, path, wp=None, residual=None):
         wt = wp
     else:
         wt = w.to(dev)
-    ws = torch.empty(max(16, abi.sparoa_fc_workspace_size(d, path)), dtype=torch.uint8,
+    ws = torch.zeros(max(16, abi.sparoa_fc_workspace_size(d, path)), dtype=torch.uint8,
                      device=dev)
     y = torch.full((m, n), float("nan"), dtype=x.dtype, device=dev)
     ex = torch.full((1,), -1, dtype=torch.int64, device=dev)
