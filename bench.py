@@ -7,8 +7,10 @@ bf16 ~ N(0, 1/4096), m in {1, 8, 64}, activation sparsity rho in
 |N(0, 1)|.  Every operator has its own weight matrix (24 x 32 MiB, more than
 the 256 MB Infinity Cache holds), so weights stream from HBM.  Per operator
 the step runs the whole path: intensity from the shape (host), sparsity
-measurement (GPU) with the counts read back, routing (host), and the routed
-FC kernel.  Inputs are resident in HBM before timing starts.
+measurement (GPU), routing, and the routed FC kernel.  Routing runs inside
+the FC kernel from the counts in device memory, the 24 operators issued by
+one native call (default), or on the host after reading the counts back,
+one Python call per kernel (--route host).  Inputs are resident in HBM before timing starts.
 
 value = dense-equivalent TFLOP/s of the step: sum over operators of
 2 m k n divided by the step time (skipped work counts as done).
@@ -45,6 +47,10 @@ def parse():
     p.add_argument("--sparsity-thr", type=float, default=None,
                    help="routing threshold; default: calibrated from forced-path timings")
     p.add_argument("--cases-out", default=None, help="write the per-case table (JSON) here")
+    p.add_argument("--route", choices=("device", "host"), default="device",
+                   help="device: the kernel takes the skip decision from the counts in device "
+                        "memory (no host round trip); host: counts read back, sparoa_route on "
+                        "the host, then the fixed-path call")
     return p.parse_args()
 
 
@@ -107,6 +113,7 @@ def build_cases(abi, torch, synth, dev):
         ws = max(abi.sparoa_fc_workspace_size(c.desc, p) for p in range(4))
         c.ws = torch.zeros(max(16, ws), dtype=torch.uint8, device=dev)
         c.y = torch.empty(m, N, dtype=torch.bfloat16, device=dev)
+        c.path_dev = torch.zeros(1, dtype=torch.int32, device=dev)
         cases.append(c)
     torch.cuda.synchronize()
     for c in cases:   # only the packed copy is needed by the bandwidth paths
@@ -114,6 +121,19 @@ def build_cases(abi, torch, synth, dev):
             c.w = None
     torch.cuda.empty_cache()
     return cases
+
+
+def run_case_device(abi, c, s_thr, ev=None):
+    """One operator through the whole path with device-side routing: no host
+    synchronisation; the path taken is left in c.path_dev."""
+    abi.sparoa_measure_sparsity(c.x, c.m, K, c.br, c.bc, 0, c.counts, c.mask)
+    if ev is not None:
+        ev[0].record()
+    abi.sparoa_fc_routed(c.desc, s_thr, INTENSITY_THR, abi.ROUTE_BLOCK, c.counts, c.x, c.w, c.wp,
+                         None, None, abi.ACT_NONE, c.mask, c.y, c.ws, c.path_dev)
+    if ev is not None:
+        ev[1].record()
+    return None
 
 
 def run_case(abi, c, s_thr, ev=None):
@@ -227,21 +247,44 @@ def main():
 
     print(f"bench: warmup {args.warmup} steps, sparsity threshold {s_thr:.4g}", file=sys.stderr,
           flush=True)
+    step_fn = run_case_device if args.route == "device" else run_case
+    # device routing: the whole step is one native call (sparoa_fc_ops_run)
+    op_array = abi.fc_op_array([
+        abi.fc_op(c.desc, c.x, c.w, c.wp, None, None, abi.ACT_NONE, c.counts, c.mask, c.y, c.ws,
+                  c.path_dev) for c in cases])
     for _ in range(args.warmup):
-        for c in cases:
-            run_case(abi, c, s_thr)
+        if args.route == "device":
+            abi.sparoa_fc_ops_run(op_array, s_thr, INTENSITY_THR)
+        else:
+            for c in cases:
+                step_fn(abi, c, s_thr)
     torch.cuda.synchronize()
 
     evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             for _ in cases] for _ in range(args.steps)]
+    for step_evs in evs:          # create the events before handing them to the library
+        for e0, e1 in step_evs:
+            e0.record()
+            e1.record()
+    flat = [[e for pair in step_evs for e in pair] for step_evs in evs]
     paths = [None] * len(cases)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
-        for i, c in enumerate(cases):
-            paths[i] = run_case(abi, c, s_thr, evs[s][i])
+        if args.route == "device":
+            abi.sparoa_fc_ops_run(op_array, s_thr, INTENSITY_THR, events=flat[s])
+        else:
+            for i, c in enumerate(cases):
+                paths[i] = step_fn(abi, c, s_thr, evs[s][i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    if args.route == "device":
+        for i, c in enumerate(cases):
+            paths[i] = int(c.path_dev.item())
+            c.counts_host = dict(zip(("zeros", "numel", "zero_blocks", "num_blocks"),
+                                     c.counts.cpu().tolist()))
+            # the device decision must be the host rule's on the same counts
+            assert paths[i] == abi.sparoa_route(c.counts_host, c.inten, 0, s_thr, INTENSITY_THR)
     step_s = (t1 - t0) / args.steps
     print(f"bench: timed {args.steps} steps, {step_s * 1e3:.3f} ms/step", file=sys.stderr,
           flush=True)
@@ -284,7 +327,8 @@ def main():
                              "0/0.5/0.8/0.95 i.i.d. or 16x16 blocks) x w [4096,4096] bf16, "
                              "one weight matrix per operator; measure+route+execute each",
                     global_batch=sum(M_LIST) * len(RHO_LIST) * len(PATTERNS),
-                    sparsity_thr=s_thr, intensity_thr=INTENSITY_THR, route_mode="block"),
+                    sparsity_thr=s_thr, intensity_thr=INTENSITY_THR, route_mode="block",
+                    routing=args.route),
         hbm_gbps_step=round((tot_bytes + measure_bytes) / step_s / 1e9, 1),
         roofline=roofline,
         sweep=table,

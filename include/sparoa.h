@@ -178,8 +178,8 @@ sparoa_status sparoa_route(const sparoa_counts *counts, const sparoa_intensity *
  *   sparoa_measure_sparsity over the [n*h*w, c_in] view with the block shape
  *   returned by sparoa_conv2d_skip_block (one pixel x 8 channels); a
  *   work-group skips every (tile, K chunk) whose gathered input is zero:
- *   those blocks are never loaded nor multiplied.  Needs c_in % 8 == 0
- *   (else UNSUPPORTED).  Dense paths ignore mask.  The depthwise kernel reads
+ *   those blocks are never loaded nor multiplied.  UNSUPPORTED above
+ *   K = 65536 (the routed form then runs dense).  Dense paths ignore mask.  The depthwise kernel reads
  *   every input once and skips nothing.
  *   bias [c_out] (if desc->has_bias), residual (NHWC, output shape) nullable.
  *   executed_blocks_dev (nullable, skip paths): receives the number of
@@ -216,13 +216,17 @@ sparoa_status sparoa_conv2d_zero_skip(const sparoa_conv_desc *desc, const void *
  * Fully connected (SparOA Sections 1 and 2.1).
  * y = act(x w^T + bias + residual); residual [m][n] nullable.
  *   Paths: DENSE_MFMA / SKIP_MFMA : tiled MFMA GEMM, w in [n][k];
- *          DENSE_BW / SKIP_BW     : weight-streaming kernel for m <= 64 and
- *                                   k <= 16384, 16-bit dtypes, w in the
- *                                   packed layout of sparoa_fc_pack_weights,
- *                                   each weight byte read at most once; no
- *                                   workspace.
+ *          DENSE_BW / SKIP_BW     : weight-streaming kernel for 16-bit
+ *                                   dtypes, m <= 64 and k <= 16384, w in
+ *                                   the packed layout of
+ *                                   sparoa_fc_pack_weights, each weight byte
+ *                                   read at most once, no workspace; any
+ *                                   other FC on a BW path runs the implicit
+ *                                   GEMM on w[n][k] (sparoa_fc_uses_packed
+ *                                   tells which layout a call takes).
  *   Skip paths need `mask` of x measured over [m, k] with the block shape of
- *   sparoa_fc_skip_block ((1, 8) for SKIP_MFMA, (m, 1) for SKIP_BW):
+ *   sparoa_fc_skip_block ((1, 8) for the implicit GEMM, (m, 1) for the
+ *   weight-streaming kernel):
  *   SKIP_MFMA skips (row tile, K chunk) pairs whose input block is zero;
  *   SKIP_BW skips input columns that are zero in every row, and with them
  *   their weight rows.
@@ -236,8 +240,11 @@ sparoa_status sparoa_conv2d_zero_skip(const sparoa_conv_desc *desc, const void *
 sparoa_status sparoa_fc_packed_bytes(const sparoa_fc_desc *desc, size_t *bytes);
 sparoa_status sparoa_fc_pack_weights(const sparoa_fc_desc *desc, const void *w_nk,
                                      void *w_packed, hipStream_t stream);
-/* Work tiling: (tile_rows, kchunk) = the MFMA tile rows and K chunk on the
- * MFMA paths, (m, 1) on the BW paths. */
+/* *packed = 1 when the call on `path` takes the packed weight layout (the
+ * weight-streaming kernel), 0 when it takes w[n][k]. */
+sparoa_status sparoa_fc_uses_packed(const sparoa_fc_desc *desc, sparoa_path path, int *packed);
+/* Work tiling: (tile_rows, kchunk) = the implicit-GEMM tile rows and K chunk,
+ * or (m, 1) for the weight-streaming kernel. */
 sparoa_status sparoa_fc_tiling(const sparoa_fc_desc *desc, sparoa_path path, int64_t *tile_rows,
                                int64_t *kchunk);
 sparoa_status sparoa_fc_workspace_size(const sparoa_fc_desc *desc, sparoa_path path,
@@ -257,6 +264,63 @@ sparoa_status sparoa_fc_zero_skip(const sparoa_fc_desc *desc, const void *x, con
                                   const uint32_t *mask, void *y, void *workspace,
                                   size_t ws_bytes, uint64_t *executed_blocks_dev,
                                   hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Device-side routing: the one-GPU form of the paper's asynchronous engine
+ * (SparOA Section 5.1 -- execution proceeds without waiting on the host).
+ * The bandwidth bit depends on shapes only and is computed on the host from
+ * the operator's intensity (Eq. 2) and thr; the skip bit is decided inside
+ * the kernel from counts_dev (left in device memory by
+ * sparoa_measure_sparsity on the same stream) with the arithmetic of
+ * sparoa_route, so the path equals sparoa_route's on the same counts.  No
+ * host synchronisation between measurement and execution.
+ *   mask: bitmap of x at the block shape of the family's skip path
+ *         (sparoa_*_skip_block with SKIP_MFMA or SKIP_BW); required.
+ *   FC: w_nk is used on the MFMA family, w_packed on the BW family; the
+ *       other may be NULL.
+ *   path_dev (nullable): receives the path taken (a uint32 sparoa_path).
+ *   Counts with num_blocks == 0 (BLOCK mode) or numel == 0 (ELEMENT mode)
+ *   select the dense path.  Depthwise convs always run the direct kernel;
+ *   path_dev still records the decision.
+ * Errors: those of sparoa_route (host-checkable thresholds) and of the
+ * fixed-path calls.
+ * ---------------------------------------------------------------------- */
+sparoa_status sparoa_conv2d_routed(const sparoa_conv_desc *desc, const sparoa_thresholds *thr,
+                                   const sparoa_counts *counts_dev, const void *x, const void *w,
+                                   const void *bias, const void *residual, sparoa_act act,
+                                   const uint32_t *mask, void *y, void *workspace,
+                                   size_t ws_bytes, uint32_t *path_dev, hipStream_t stream);
+sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_thresholds *thr,
+                               const sparoa_counts *counts_dev, const void *x, const void *w_nk,
+                               const void *w_packed, const void *bias, const void *residual,
+                               sparoa_act act, const uint32_t *mask, void *y, void *workspace,
+                               size_t ws_bytes, uint32_t *path_dev, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Native executor of independent FC operators: for each op in order,
+ * measure x at the skip granularity of the family its intensity selects,
+ * then run the device-routed FC -- the whole measure -> route -> execute path
+ * with one host call per batch (host launch cost instead of one Python call
+ * per kernel).  Per op: counts (one sparoa_counts) and mask (sparoa_mask_words
+ * words for that granularity) are device scratch; path (nullable) receives
+ * the path taken; w_nk / w_packed as for sparoa_fc_routed.
+ * events (nullable): 2n hipEvent_t; events[2i] / events[2i+1] are recorded
+ * on `stream` right before / after op i's FC kernel.
+ * Stops at the first failing op and returns its status.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+  sparoa_fc_desc desc;
+  const void *x, *w_nk, *w_packed, *bias, *residual;
+  sparoa_act act;
+  sparoa_counts *counts;
+  uint32_t *mask;
+  void *y;
+  void *workspace;
+  size_t ws_bytes;
+  uint32_t *path;
+} sparoa_fc_op;
+sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr,
+                                hipEvent_t *events, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Network glue (not routed): NHWC max pooling, window k, stride s, padding p.

@@ -29,7 +29,8 @@ EXPORTS = [
     "sparoa_conv2d_skip_block", "sparoa_conv2d_tiling", "sparoa_conv2d", "sparoa_conv2d_dense",
     "sparoa_conv2d_zero_skip", "sparoa_fc_packed_bytes", "sparoa_fc_pack_weights",
     "sparoa_fc_tiling", "sparoa_fc_workspace_size", "sparoa_fc_skip_block", "sparoa_fc",
-    "sparoa_fc_dense", "sparoa_fc_zero_skip", "sparoa_maxpool2d",
+    "sparoa_fc_dense", "sparoa_fc_zero_skip", "sparoa_maxpool2d", "sparoa_conv2d_routed",
+    "sparoa_fc_routed", "sparoa_fc_uses_packed", "sparoa_fc_ops_run",
 ]
 
 
@@ -65,6 +66,15 @@ class Intensity(ctypes.Structure):
 
     def as_dict(self):
         return dict(macs=self.macs, flops=self.flops, bytes=self.bytes, intensity=self.intensity)
+
+
+class FcOp(ctypes.Structure):
+    _fields_ = [("desc", FcDesc), ("x", ctypes.c_void_p), ("w_nk", ctypes.c_void_p),
+                ("w_packed", ctypes.c_void_p), ("bias", ctypes.c_void_p),
+                ("residual", ctypes.c_void_p), ("act", ctypes.c_int),
+                ("counts", ctypes.c_void_p), ("mask", ctypes.c_void_p), ("y", ctypes.c_void_p),
+                ("workspace", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t),
+                ("path", ctypes.c_void_p)]
 
 
 class Thresholds(ctypes.Structure):
@@ -106,6 +116,8 @@ def _load():
         "sparoa_fc_tiling": (ctypes.c_int, [P(FcDesc), ctypes.c_int, P(i64), P(i64)]),
         "sparoa_fc_workspace_size": (ctypes.c_int, [P(FcDesc), ctypes.c_int, P(sz)]),
         "sparoa_fc_skip_block": (ctypes.c_int, [P(FcDesc), ctypes.c_int, P(i64), P(i64)]),
+        "sparoa_fc_uses_packed": (ctypes.c_int, [P(FcDesc), ctypes.c_int, P(ctypes.c_int)]),
+        "sparoa_fc_ops_run": (ctypes.c_int, [P(FcOp), i64, P(Thresholds), P(vp), vp]),
         "sparoa_fc": (ctypes.c_int, [P(FcDesc), ctypes.c_int, vp, vp, vp, vp, ctypes.c_int, vp,
                                      vp, vp, sz, vp, vp]),
         "sparoa_fc_dense": (ctypes.c_int, [P(FcDesc), vp, vp, vp, vp, ctypes.c_int, vp, vp, sz,
@@ -114,6 +126,10 @@ def _load():
                                                vp, sz, vp, vp]),
         "sparoa_maxpool2d": (ctypes.c_int, [vp, ctypes.c_int, i64, i64, i64, i64, i64, i64, i64,
                                             vp, vp]),
+        "sparoa_conv2d_routed": (ctypes.c_int, [P(ConvDesc), P(Thresholds), vp, vp, vp, vp, vp,
+                                                ctypes.c_int, vp, vp, vp, sz, vp, vp]),
+        "sparoa_fc_routed": (ctypes.c_int, [P(FcDesc), P(Thresholds), vp, vp, vp, vp, vp, vp,
+                                            ctypes.c_int, vp, vp, vp, sz, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -324,3 +340,51 @@ def sparoa_fc_zero_skip(desc, x, w, bias, residual, act, mask, y, workspace=None
 def sparoa_maxpool2d(x, n, c, h, w, k, s, p, y, stream=None):
     _check(_L.sparoa_maxpool2d(_ptr(x), dtype_code(x), n, c, h, w, k, s, p, _ptr(y),
                                _stream(stream)))
+
+
+def sparoa_conv2d_routed(desc, sparsity_thr, intensity_thr, mode, counts, x, w, bias, residual,
+                         act, mask, y, workspace=None, path=None, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    t = Thresholds(sparsity_thr, intensity_thr, mode)
+    _check(_L.sparoa_conv2d_routed(ctypes.byref(desc), ctypes.byref(t), _ptr(counts), _ptr(x),
+                                   _ptr(w), _ptr(bias), _ptr(residual), act, _ptr(mask), _ptr(y),
+                                   _ptr(workspace), ws_bytes, _ptr(path), _stream(stream)))
+
+
+def sparoa_fc_routed(desc, sparsity_thr, intensity_thr, mode, counts, x, w_nk, w_packed, bias,
+                     residual, act, mask, y, workspace=None, path=None, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    t = Thresholds(sparsity_thr, intensity_thr, mode)
+    _check(_L.sparoa_fc_routed(ctypes.byref(desc), ctypes.byref(t), _ptr(counts), _ptr(x),
+                               _ptr(w_nk), _ptr(w_packed), _ptr(bias), _ptr(residual), act,
+                               _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes, _ptr(path),
+                               _stream(stream)))
+
+
+def sparoa_fc_uses_packed(desc, path):
+    v = ctypes.c_int()
+    _check(_L.sparoa_fc_uses_packed(ctypes.byref(desc), path, ctypes.byref(v)))
+    return bool(v.value)
+
+
+def fc_op(desc, x, w_nk, w_packed, bias, residual, act, counts, mask, y, workspace=None,
+          path=None):
+    """One entry of a sparoa_fc_ops_run batch (pointers captured now)."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    return FcOp(desc, _ptr(x), _ptr(w_nk), _ptr(w_packed), _ptr(bias), _ptr(residual), act,
+                _ptr(counts), _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes, _ptr(path))
+
+
+def fc_op_array(ops):
+    return (FcOp * len(ops))(*ops)
+
+
+def sparoa_fc_ops_run(op_array, sparsity_thr, intensity_thr, mode=ROUTE_BLOCK, events=None,
+                      stream=None):
+    """Runs a batch built by fc_op_array.  events: flat list of 2n recorded
+    torch.cuda.Event objects (or None)."""
+    t = Thresholds(sparsity_thr, intensity_thr, mode)
+    ev = None
+    if events is not None:
+        ev = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+    _check(_L.sparoa_fc_ops_run(op_array, len(op_array), ctypes.byref(t), ev, _stream(stream)))

@@ -354,7 +354,7 @@ sparoa_status sparoa_fc_tiling(const sparoa_fc_desc *d, sparoa_path path, int64_
   if (st != SPAROA_OK) return st;
   if (!tile_rows || !kchunk || !path_ok(path))
     return fail(SPAROA_ERR_INVALID_ARG, "tiling: bad argument");
-  if (path & 2) {
+  if ((path & 2) && fc_bw_streams(*d)) {
     *tile_rows = d->m;
     *kchunk = 1;
   } else {
@@ -370,7 +370,17 @@ sparoa_status sparoa_fc_workspace_size(const sparoa_fc_desc *d, sparoa_path path
   sparoa_status st = check_fc(d);
   if (st != SPAROA_OK) return st;
   if (!bytes || !path_ok(path)) return fail(SPAROA_ERR_INVALID_ARG, "workspace_size: bad argument");
-  *bytes = (path & 2) ? fc_bw_workspace(*d, path) : gemm_workspace(fc_as_conv(*d), path);
+  *bytes = ((path & 2) && fc_bw_streams(*d)) ? fc_bw_workspace(*d, path)
+                                              : gemm_workspace(fc_as_conv(*d), path);
+  return SPAROA_OK;
+}
+
+sparoa_status sparoa_fc_uses_packed(const sparoa_fc_desc *d, sparoa_path path, int *packed) {
+  g_last_error.clear();
+  sparoa_status st = check_fc(d);
+  if (st != SPAROA_OK) return st;
+  if (!packed || !path_ok(path)) return fail(SPAROA_ERR_INVALID_ARG, "uses_packed: bad argument");
+  *packed = ((path & 2) && fc_bw_streams(*d)) ? 1 : 0;
   return SPAROA_OK;
 }
 
@@ -381,7 +391,7 @@ sparoa_status sparoa_fc_skip_block(const sparoa_fc_desc *d, sparoa_path path,
   if (st != SPAROA_OK) return st;
   if (!block_rows || !block_cols || !path_ok(path))
     return fail(SPAROA_ERR_INVALID_ARG, "skip_block: bad argument");
-  if (path & 2) {  // a column is skipped when it is zero in every row
+  if ((path & 2) && fc_bw_streams(*d)) {  // a column is skipped when it is zero in every row
     *block_rows = d->m;
     *block_cols = 1;
   } else {  // the implicit-GEMM skip kernel reads one bit per (row, 8 columns)
@@ -404,7 +414,7 @@ sparoa_status sparoa_fc(const sparoa_fc_desc *d, sparoa_path path, const void *x
   const bool skip = (path & 1) != 0;
   if (skip && !mask) return fail(SPAROA_ERR_INVALID_ARG, "fc: skip path needs a mask");
   if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace})) != SPAROA_OK) return st;
-  if (path & 2) {
+  if ((path & 2) && fc_bw_streams(*d)) {
     if (ws_bytes < fc_bw_workspace(*d, path))
       return fail(SPAROA_ERR_WORKSPACE, "fc: workspace too small");
     return launch_fc_bw(*d, path, x, w, d->has_bias ? bias : nullptr, residual, act,
@@ -429,6 +439,105 @@ sparoa_status sparoa_fc_zero_skip(const sparoa_fc_desc *d, const void *x, const 
                                   size_t ws_bytes, uint64_t *executed, hipStream_t stream) {
   return sparoa_fc(d, SPAROA_PATH_SKIP_MFMA, x, w_nk, bias, residual, act, mask, y, workspace,
                    ws_bytes, executed, stream);
+}
+
+// -------------------------------------------------------- device routing
+
+namespace {
+sparoa_status check_thr(const sparoa_thresholds *thr) {
+  if (!thr) return fail(SPAROA_ERR_INVALID_ARG, "routed: null thresholds");
+  if (std::isnan(thr->sparsity_thr) || std::isnan(thr->intensity_thr) || thr->sparsity_thr < 0 ||
+      thr->intensity_thr < 0)
+    return fail(SPAROA_ERR_INVALID_ARG, "routed: NaN or negative threshold");
+  if (thr->mode != SPAROA_ROUTE_BLOCK && thr->mode != SPAROA_ROUTE_ELEMENT)
+    return fail(SPAROA_ERR_INVALID_ARG, "routed: unknown mode");
+  return SPAROA_OK;
+}
+}  // namespace
+
+sparoa_status sparoa_conv2d_routed(const sparoa_conv_desc *d, const sparoa_thresholds *thr,
+                                   const sparoa_counts *counts_dev, const void *x, const void *w,
+                                   const void *bias, const void *residual, sparoa_act act,
+                                   const uint32_t *mask, void *y, void *workspace,
+                                   size_t ws_bytes, uint32_t *path_dev, hipStream_t stream) {
+  g_last_error.clear();
+  sparoa_intensity in;
+  sparoa_status st = sparoa_op_intensity_conv(d, &in);
+  if (st != SPAROA_OK) return st;
+  if ((st = check_thr(thr)) != SPAROA_OK) return st;
+  if (!counts_dev || !x || !w || !y || !mask || !act_ok(act))
+    return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed: null counts/x/w/mask/y or bad act");
+  if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed: has_bias without bias");
+  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace})) != SPAROA_OK) return st;
+  const bool dw = is_depthwise(*d);
+  const int bw = (dw || in.intensity < thr->intensity_thr) ? 1 : 0;
+  const DeviceRoute r{counts_dev, thr->sparsity_thr, thr->mode, bw, path_dev};
+  if (dw) return launch_depthwise(*d, x, w, d->has_bias ? bias : nullptr, residual, act, y, stream, &r);
+  if (d->groups != 1) return fail(SPAROA_ERR_UNSUPPORTED, "grouped (non-depthwise) conv");
+  const sparoa_path p = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
+  if (ws_bytes < gemm_workspace(*d, p)) return fail(SPAROA_ERR_WORKSPACE, "conv2d_routed: workspace too small");
+  // without a skip kernel for this shape the dense kernel runs and records a dense path
+  const bool can_skip = gemm_skip_supported(*d);
+  return launch_gemm_conv(*d, p, x, w, d->has_bias ? bias : nullptr, residual, act,
+                          can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r);
+}
+
+sparoa_status sparoa_fc_routed(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
+                               const sparoa_counts *counts_dev, const void *x, const void *w_nk,
+                               const void *w_packed, const void *bias, const void *residual,
+                               sparoa_act act, const uint32_t *mask, void *y, void *workspace,
+                               size_t ws_bytes, uint32_t *path_dev, hipStream_t stream) {
+  g_last_error.clear();
+  sparoa_intensity in;
+  sparoa_status st = sparoa_op_intensity_fc(d, &in);
+  if (st != SPAROA_OK) return st;
+  if ((st = check_thr(thr)) != SPAROA_OK) return st;
+  const int bw = in.intensity < thr->intensity_thr ? 1 : 0;
+  const bool streams = bw && fc_bw_streams(*d);
+  const void *w = streams ? w_packed : w_nk;
+  if (!counts_dev || !x || !w || !y || !mask || !act_ok(act))
+    return fail(SPAROA_ERR_INVALID_ARG, "fc_routed: null counts/x/weights/mask/y or bad act");
+  if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "fc_routed: has_bias without bias");
+  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace})) != SPAROA_OK) return st;
+  const DeviceRoute r{counts_dev, thr->sparsity_thr, thr->mode, bw, path_dev};
+  if (streams)
+    return launch_fc_bw(*d, SPAROA_PATH_SKIP_BW, x, w, d->has_bias ? bias : nullptr, residual, act,
+                        mask, y, workspace, ws_bytes, nullptr, stream, &r);
+  const sparoa_conv_desc c = fc_as_conv(*d);
+  const sparoa_path p = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
+  if (ws_bytes < gemm_workspace(c, p)) return fail(SPAROA_ERR_WORKSPACE, "fc_routed: workspace too small");
+  const bool can_skip = gemm_skip_supported(c);
+  return launch_gemm_conv(c, p, x, w, d->has_bias ? bias : nullptr, residual, act,
+                          can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r);
+}
+
+// ---------------------------------------------------------------- executor
+
+sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr,
+                                hipEvent_t *events, hipStream_t stream) {
+  g_last_error.clear();
+  if (!ops || n < 0) return fail(SPAROA_ERR_INVALID_ARG, "fc_ops_run: null ops or n < 0");
+  sparoa_status st = check_thr(thr);
+  if (st != SPAROA_OK) return st;
+  for (int64_t i = 0; i < n; ++i) {
+    const sparoa_fc_op &o = ops[i];
+    sparoa_intensity in;
+    if ((st = sparoa_op_intensity_fc(&o.desc, &in)) != SPAROA_OK) return st;
+    const sparoa_path fam =
+        in.intensity < thr->intensity_thr ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
+    int64_t br, bc;
+    if ((st = sparoa_fc_skip_block(&o.desc, fam, &br, &bc)) != SPAROA_OK) return st;
+    if ((st = sparoa_measure_sparsity(o.x, o.desc.dtype, o.desc.m, o.desc.k, br, bc, 0, o.counts,
+                                      o.mask, nullptr, stream)) != SPAROA_OK)
+      return st;
+    if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i], stream));
+    if ((st = sparoa_fc_routed(&o.desc, thr, o.counts, o.x, o.w_nk, o.w_packed, o.bias,
+                               o.residual, o.act, o.mask, o.y, o.workspace, o.ws_bytes, o.path,
+                               stream)) != SPAROA_OK)
+      return st;
+    if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i + 1], stream));
+  }
+  return SPAROA_OK;
 }
 
 // ------------------------------------------------------------------- glue

@@ -31,6 +31,33 @@ inline int64_t elem_size(sparoa_dtype d) { return d == SPAROA_F32 ? 4 : 2; }
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Device-side routing: the skip decision is taken inside the kernel from the
+// counts the measurement kernel left in device memory (no host round trip);
+// the bandwidth bit depends on shapes only and is fixed by the host.
+struct DeviceRoute {
+  const sparoa_counts *counts;  // nullptr: the host already chose the path
+  double sparsity_thr;
+  int mode;
+  int bw_bit;
+  uint32_t *path_out;  // nullable: receives the path taken
+};
+
+#ifdef __HIPCC__
+// Same arithmetic as sparoa_route: one double division, >= comparison.
+__device__ __forceinline__ bool device_route_skip(const DeviceRoute &r) {
+  const sparoa_counts c = *r.counts;
+  double rho;
+  if (r.mode == SPAROA_ROUTE_BLOCK) {
+    if (c.num_blocks == 0 || c.zero_blocks > c.num_blocks) return false;
+    rho = (double)c.zero_blocks / (double)c.num_blocks;
+  } else {
+    if (c.numel == 0 || c.zeros > c.numel) return false;
+    rho = (double)c.zeros / (double)c.numel;
+  }
+  return rho >= r.sparsity_thr;
+}
+#endif
+
 // ---- launchers (validated arguments; defined in the .hip files) ---------
 
 sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64_t cols,
@@ -45,11 +72,13 @@ struct GemmTileChoice {
   int split_k;      // number of K splits (1 = none)
 };
 GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path path);
+bool gemm_skip_supported(const sparoa_conv_desc &d);
 size_t gemm_workspace(const sparoa_conv_desc &d, sparoa_path path);
 sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, const void *x,
                                const void *w, const void *bias, const void *residual,
                                sparoa_act act, const uint32_t *mask, void *y, void *ws,
-                               size_t ws_bytes, uint64_t *executed, hipStream_t stream);
+                               size_t ws_bytes, uint64_t *executed, hipStream_t stream,
+                               const DeviceRoute *route = nullptr);
 
 // Sums split-K fp32 partials [split][M][N] in split order, adds bias and
 // residual, applies the activation, and writes y in dtype.
@@ -63,10 +92,13 @@ sparoa_status launch_set_u64(uint64_t *p, uint64_t v, hipStream_t stream);
 // Depthwise direct conv (groups == c_in == c_out).
 sparoa_status launch_depthwise(const sparoa_conv_desc &d, const void *x, const void *w,
                                const void *bias, const void *residual, sparoa_act act, void *y,
-                               hipStream_t stream);
+                               hipStream_t stream, const DeviceRoute *route = nullptr);
 
 // FC weight-streaming (bandwidth) kernel over k-major packed weights.
 size_t fc_packed_bytes(const sparoa_fc_desc &d);
+// The weight-streaming kernel takes 16-bit FCs with m <= 64 and k <= 16384;
+// every other bandwidth-path FC runs the implicit GEMM on w[n][k].
+bool fc_bw_streams(const sparoa_fc_desc &d);
 size_t fc_bw_workspace(const sparoa_fc_desc &d, sparoa_path path);
 sparoa_status launch_fc_pack(const sparoa_fc_desc &d, const void *w_nk, void *w_packed,
                              hipStream_t stream);
@@ -74,7 +106,8 @@ sparoa_status launch_fc_bw(const sparoa_fc_desc &d, sparoa_path path, const void
                            const void *w_packed, const void *bias, const void *residual,
                            sparoa_act act,
                            const uint32_t *mask, void *y, void *ws, size_t ws_bytes,
-                           uint64_t *executed, hipStream_t stream);
+                           uint64_t *executed, hipStream_t stream,
+                           const DeviceRoute *route = nullptr);
 
 sparoa_status launch_maxpool(const void *x, sparoa_dtype dt, int64_t n, int64_t c, int64_t h,
                              int64_t w, int64_t k, int64_t s, int64_t p, void *y,

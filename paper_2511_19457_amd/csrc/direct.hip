@@ -26,6 +26,7 @@ struct DwArgs {
   int64_t N, H, W, C, Ho, Wo;
   int kh, kw, sh, sw, ph, pw, dh, dw;
   int act;
+  DeviceRoute route;
 };
 
 template <int DT, int V>
@@ -70,6 +71,8 @@ __global__ __launch_bounds__(kThreads) void depthwise_kernel(DwArgs a) {
   const int64_t total = a.N * a.Ho * runs * cv;
   const int kh = KH > 0 ? KH : a.kh, kw = KW > 0 ? KW : a.kw;
   const int taps = kh * kw;
+  if (a.route.counts && a.route.path_out && blockIdx.x == 0 && threadIdx.x == 0)
+    *a.route.path_out = (device_route_skip(a.route) ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
   for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < total;
        i += (int64_t)gridDim.x * kThreads) {
     const int64_t c0 = (i % cv) * V;
@@ -206,7 +209,7 @@ sparoa_status mp_dispatch(const void *x, void *y, int64_t n, int64_t c, int64_t 
 
 sparoa_status launch_depthwise(const sparoa_conv_desc &d, const void *x, const void *w,
                                const void *bias, const void *residual, sparoa_act act, void *y,
-                               hipStream_t stream) {
+                               hipStream_t stream, const DeviceRoute *route) {
   if (d.kh * d.kw > kMaxTaps) return fail(SPAROA_ERR_UNSUPPORTED, "depthwise window above 5x5");
   DwArgs a;
   a.x = static_cast<const char *>(x);
@@ -220,6 +223,7 @@ sparoa_status launch_depthwise(const sparoa_conv_desc &d, const void *x, const v
   a.kh = (int)d.kh; a.kw = (int)d.kw; a.sh = (int)d.sh; a.sw = (int)d.sw;
   a.ph = (int)d.ph; a.pw = (int)d.pw; a.dh = (int)d.dh; a.dw = (int)d.dw;
   a.act = act;
+  a.route = route ? *route : DeviceRoute{nullptr, 0.0, 0, 0, nullptr};
   switch (d.dtype) {
     case SPAROA_BF16: return dw_dispatch<SPAROA_BF16>(a, stream);
     case SPAROA_F16: return dw_dispatch<SPAROA_F16>(a, stream);

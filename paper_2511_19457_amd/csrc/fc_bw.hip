@@ -10,11 +10,14 @@
 // skip variant drops it from the stream (skip granularity: one column).
 //
 // One work-group streams one panel over all of K (no cross-work-group
-// reduction, no device-scope fences).  Its 8 waves split K into contiguous
-// slices.  A wave walks its slice -- all of it, or, in the skip variant, the
-// nonzero columns listed from the column bitmap by ballot + popcount -- in
-// chunks of 32 entries, keeping 4 chunks of weight rows (16-byte loads, two
-// lanes per row) and input values in flight in registers.  Each chunk goes
+// reduction, no device-scope fences).  Its waves (16 for m <= 32, else 8)
+// split K into contiguous slices.  A wave walks its slice -- all of it, or,
+// in the skip variant, the nonzero columns listed from the column bitmap by a
+// popcount prefix sum -- in chunks of 32 entries, keeping 4 to 8 chunks of
+// weight rows (16-byte loads, two lanes per row) and input values
+// in flight in registers.  Dense input rows are read with 16-byte loads; the
+// skip variant gathers input pairs spread over all lanes (one 4-byte load
+// when the pair's columns are adjacent).  Each chunk goes
 // through a wave-private LDS tile (weights transposed on the way in) into
 // v_mfma_f32_16x16x32 over all m (padded to 16) and the panel's 16 columns.
 // The waves' fp32 partials are added in wave order through LDS
@@ -25,13 +28,17 @@
 namespace sparoa {
 namespace {
 
-constexpr int kWaves = 8;
-constexpr int kThreads = 64 * kWaves;
 constexpr int kPanel = 16;          // output columns per panel / work-group
 constexpr int kCh = 32;             // entries per chunk = one MFMA k-step
-constexpr int kDepth = 4;           // chunks in flight per wave
-constexpr int kMaxSlice = 2048;     // K values per wave (K <= 16384)
+constexpr int kMaxWaveK = 1024;     // K values per wave slice
 constexpr int kRowB = (kCh + 8) * 2;  // LDS row stride in bytes (80: conflict-free b128 reads)
+
+// Waves per work-group and chunks in flight per wave for MT row tiles.
+template <int MT>
+struct Shape {
+  static constexpr int waves = MT <= 2 ? 16 : 8;
+  static constexpr int depth = MT == 1 ? 8 : (MT == 2 ? 5 : 4);  // within the VGPR budget
+};
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
@@ -47,6 +54,8 @@ struct FcBwArgs {
   unsigned long long *executed;
   int64_t M, K, N, slice;
   int act;
+  int xvec;
+  DeviceRoute route;
 };
 
 // LDS of one wave: transposed weight tile [16 cols][32 entries], input tile
@@ -55,19 +64,22 @@ template <int MT, bool SKIP>
 struct WaveLds {
   char wt[kPanel * kRowB];
   char xs[MT * 16 * kRowB];
-  unsigned short list[SKIP ? kMaxSlice : 8];
+  unsigned short list[SKIP ? kMaxWaveK : 8];
 };
 
 template <int DT, int MT, bool SKIP, bool XVEC>
-__global__ __launch_bounds__(kThreads) void fc_bw_kernel(FcBwArgs a) {
+__global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_kernel(FcBwArgs a) {
+  constexpr int NW = Shape<MT>::waves;
+  constexpr int kDepth = Shape<MT>::depth;
+  constexpr int kThreads = 64 * NW;
   using E = Elem<DT>;
   using raw = typename E::raw;
   static_assert(E::size == 2, "16-bit types only");
   using Lds = WaveLds<MT, SKIP>;
   // gfx950 addresses 160 KB of LDS per work-group
-  static_assert(sizeof(Lds) * kWaves <= 160 * 1024, "LDS budget");
-  static_assert(sizeof(Lds) * kWaves >= kWaves * MT * 16 * kPanel * 4, "reduction space");
-  __shared__ __attribute__((aligned(16))) char lds_raw[sizeof(Lds) * kWaves];
+  static_assert(sizeof(Lds) * NW <= 160 * 1024, "LDS budget");
+  static_assert(sizeof(Lds) * NW >= NW * MT * 16 * kPanel * 4, "reduction space");
+  __shared__ __attribute__((aligned(16))) char lds_raw[sizeof(Lds) * NW];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   Lds &L = reinterpret_cast<Lds *>(lds_raw)[wave];
@@ -77,15 +89,39 @@ __global__ __launch_bounds__(kThreads) void fc_bw_kernel(FcBwArgs a) {
   const char *wpanel = a.wp + p * a.K * kPanel * 2;
 
   int count = ke > kb ? (int)(ke - kb) : 0;
+  bool use_list = SKIP;
   if constexpr (SKIP) {
-    int total = 0;
-    for (int64_t base = kb; base < ke; base += 64) {
-      const int64_t k = base + lane;
-      const bool nz = k < ke && ((a.mask[k >> 5] >> (k & 31)) & 1u);
-      const uint64_t bal = __ballot(nz);
-      if (nz) L.list[total + __popcll(bal & ((1ull << lane) - 1ull))] = (unsigned short)(k - kb);
-      total += __popcll(bal);
+    if (a.route.counts) {
+      use_list = device_route_skip(a.route);
+      if (a.route.path_out && p == 0 && tid == 0)
+        *a.route.path_out = (use_list ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
     }
+  }
+  if (SKIP && use_list) {
+    // The slice's bitmap words (at most 32: one per lane) are loaded at once;
+    // an exclusive prefix sum of their popcounts gives each lane its place
+    // in the list, then each lane writes the offsets of its set bits.
+    const int nw = (count + 31) / 32;
+    uint32_t wv = 0;
+    if (lane < nw) {
+      wv = a.mask[(kb >> 5) + lane];
+      const int tail = count - 32 * lane;
+      if (tail < 32) wv &= (1u << tail) - 1u;
+    }
+    const int cnt = __popc(wv);
+    int incl = cnt;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    int pos = incl - cnt;
+    while (wv) {
+      const int b = __ffs(wv) - 1;
+      L.list[pos++] = (unsigned short)(32 * lane + b);
+      wv &= wv - 1u;
+    }
+    const int total = __shfl(incl, 63, 64);
     count = total;
     if (a.executed && p == 0 && lane == 0 && total)
       atomicAdd(a.executed, (unsigned long long)total);
@@ -95,29 +131,33 @@ __global__ __launch_bounds__(kThreads) void fc_bw_kernel(FcBwArgs a) {
   // entry -> column k (or -1 past the end of the wave's list)
   auto entry_k = [&](int e) -> int64_t {
     if (e >= count) return -1;
-    if constexpr (SKIP) return kb + (int64_t)L.list[e];
+    if (SKIP && use_list) return kb + (int64_t)L.list[e];
     return kb + e;
   };
-
-  // Register staging of one chunk: weight row e = lane / 2, half lane % 2;
-  // input vectors (row m, 8 entries) v = lane + 64 j.
+  // Register staging of one chunk: weight row e = lane / 2, half lane % 2.
+  // Input, vector form: (row m, 8 entries) per v = lane + 64 j, one 16-byte
+  // load when the 8 columns are contiguous (dense order);
+  // pair form (skip order): (row m, entries 2q, 2q + 1) per v = lane + 64 j,
+  // one 4-byte load when the two columns are adjacent, else two gathers.
+  // Both forms use the same 4 * MT registers.
+  const bool vecform = !SKIP || !use_list;
+  const bool xvec = XVEC || (SKIP && a.xvec);  // rows 16-byte aligned
   struct Stage {
     uint4 w;
-    uint4 x[MT];
+    uint32_t xr[4 * MT];
   };
   auto load = [&](int c, Stage &s) {
-    const int e = c * kCh + (lane >> 1);
-    const int64_t k = entry_k(e);
+    const int64_t k = entry_k(c * kCh + (lane >> 1));
     s.w = k >= 0 ? *reinterpret_cast<const uint4 *>(wpanel + (k * kPanel + 8 * (lane & 1)) * 2)
                  : make_uint4(0, 0, 0, 0);
+    if (vecform) {
 #pragma unroll
-    for (int j = 0; j < MT; ++j) {
-      const int v = lane + 64 * j;
-      const int m = v >> 2, e0 = c * kCh + 8 * (v & 3);
-      uint4 q = make_uint4(0, 0, 0, 0);
-      if (m < a.M) {
-        if constexpr (XVEC) {
-          if (e0 + 8 <= count) {
+      for (int j = 0; j < MT; ++j) {
+        const int v = lane + 64 * j;
+        const int m = v >> 2, e0 = c * kCh + 8 * (v & 3);
+        uint4 q = make_uint4(0, 0, 0, 0);
+        if (m < a.M) {
+          if (xvec && e0 + 8 <= count) {
             q = *reinterpret_cast<const uint4 *>(a.x + (m * a.K + kb + e0) * 2);
           } else {
             raw t[8];
@@ -127,17 +167,27 @@ __global__ __launch_bounds__(kThreads) void fc_bw_kernel(FcBwArgs a) {
                                     : (raw)0;
             __builtin_memcpy(&q, t, 16);
           }
-        } else {
-          raw t[8];
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const int64_t k = entry_k(e0 + i);
-            t[i] = k >= 0 ? reinterpret_cast<const raw *>(a.x)[m * a.K + k] : (raw)0;
-          }
-          __builtin_memcpy(&q, t, 16);
         }
+        __builtin_memcpy(&s.xr[4 * j], &q, 16);
       }
-      s.x[j] = q;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4 * MT; ++j) {
+        const int v = lane + 64 * j;
+        const int m = v >> 4, e0 = c * kCh + 2 * (v & 15);
+        uint32_t pr = 0;
+        if (m < a.M) {
+          const int64_t k0 = entry_k(e0), k1 = entry_k(e0 + 1);
+          const raw *xr = reinterpret_cast<const raw *>(a.x) + m * a.K;
+          if (k0 >= 0 && k1 == k0 + 1 && ((m * a.K + k0) & 1) == 0) {  // 4-byte aligned pair
+            pr = *reinterpret_cast<const uint32_t *>(xr + k0);
+          } else {
+            const uint32_t lo = k0 >= 0 ? xr[k0] : 0u, hi = k1 >= 0 ? xr[k1] : 0u;
+            pr = lo | (hi << 16);
+          }
+        }
+        s.xr[j] = pr;
+      }
     }
   };
   auto stash = [&](const Stage &s) {
@@ -147,10 +197,20 @@ __global__ __launch_bounds__(kThreads) void fc_bw_kernel(FcBwArgs a) {
     __builtin_memcpy(h, &s.w, 16);
 #pragma unroll
     for (int i = 0; i < 8; ++i) *reinterpret_cast<raw *>(&L.wt[(c0 + i) * kRowB + 2 * e]) = h[i];
+    if (vecform) {
 #pragma unroll
-    for (int j = 0; j < MT; ++j) {
-      const int v = lane + 64 * j;
-      *reinterpret_cast<uint4 *>(&L.xs[(v >> 2) * kRowB + 16 * (v & 3)]) = s.x[j];
+      for (int j = 0; j < MT; ++j) {
+        const int v = lane + 64 * j;
+        uint4 q;
+        __builtin_memcpy(&q, &s.xr[4 * j], 16);
+        *reinterpret_cast<uint4 *>(&L.xs[(v >> 2) * kRowB + 16 * (v & 3)]) = q;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4 * MT; ++j) {
+        const int v = lane + 64 * j;
+        *reinterpret_cast<uint32_t *>(&L.xs[(v >> 4) * kRowB + 4 * (v & 15)]) = s.xr[j];
+      }
     }
   };
 
@@ -203,7 +263,7 @@ __global__ __launch_bounds__(kThreads) void fc_bw_kernel(FcBwArgs a) {
     if (row >= a.M || col >= a.N) continue;
     float o = 0.f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) o += red[w * MT * 16 * kPanel + e];
+    for (int w = 0; w < NW; ++w) o += red[w * MT * 16 * kPanel + e];
     if (a.bias) o += E::to_f32(reinterpret_cast<const raw *>(a.bias)[col]);
     if (a.residual) o += E::to_f32(reinterpret_cast<const raw *>(a.residual)[row * a.N + col]);
     reinterpret_cast<raw *>(a.y)[row * a.N + col] = E::from_f32(apply_act(o, a.act));
@@ -230,13 +290,19 @@ __global__ void fc_pack_kernel(const raw *__restrict__ w, raw *__restrict__ wp, 
   }
 }
 
+template <int DT, int MT, bool SKIP, bool XVEC>
+void launch_one(dim3 grid, hipStream_t st, const FcBwArgs &a) {
+  hipLaunchKernelGGL((fc_bw_kernel<DT, MT, SKIP, XVEC>), grid, dim3(64 * Shape<MT>::waves), 0, st,
+                     a);
+}
+
 template <int DT, bool SKIP, bool XVEC>
 bool launch_mt(int mt, dim3 grid, hipStream_t st, const FcBwArgs &a) {
   switch (mt) {
-    case 1: hipLaunchKernelGGL((fc_bw_kernel<DT, 1, SKIP, XVEC>), grid, dim3(kThreads), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((fc_bw_kernel<DT, 2, SKIP, XVEC>), grid, dim3(kThreads), 0, st, a); break;
-    case 3: hipLaunchKernelGGL((fc_bw_kernel<DT, 3, SKIP, XVEC>), grid, dim3(kThreads), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((fc_bw_kernel<DT, 4, SKIP, XVEC>), grid, dim3(kThreads), 0, st, a); break;
+    case 1: launch_one<DT, 1, SKIP, XVEC>(grid, st, a); break;
+    case 2: launch_one<DT, 2, SKIP, XVEC>(grid, st, a); break;
+    case 3: launch_one<DT, 3, SKIP, XVEC>(grid, st, a); break;
+    case 4: launch_one<DT, 4, SKIP, XVEC>(grid, st, a); break;
     default: return false;
   }
   return true;
@@ -249,7 +315,17 @@ bool launch_dt(int mt, bool skip, bool xvec, dim3 grid, hipStream_t st, const Fc
               : launch_mt<DT, false, false>(mt, grid, st, a);
 }
 
+int waves_for(int64_t m) { return m <= 32 ? Shape<1>::waves : Shape<3>::waves; }
+
+int64_t slice_for(const sparoa_fc_desc &d) {
+  return cdiv(cdiv(d.k, waves_for(d.m)), 64) * 64;
+}
+
 }  // namespace
+
+bool fc_bw_streams(const sparoa_fc_desc &d) {
+  return d.dtype != SPAROA_F32 && d.m <= 64 && slice_for(d) <= kMaxWaveK;
+}
 
 size_t fc_packed_bytes(const sparoa_fc_desc &d) {
   return (size_t)cdiv(d.n, kPanel) * kPanel * (size_t)d.k * (size_t)elem_size(d.dtype);
@@ -274,11 +350,9 @@ sparoa_status launch_fc_pack(const sparoa_fc_desc &d, const void *w_nk, void *w_
 sparoa_status launch_fc_bw(const sparoa_fc_desc &d, sparoa_path, const void *x,
                            const void *w_packed, const void *bias, const void *residual,
                            sparoa_act act, const uint32_t *mask, void *y, void *, size_t,
-                           uint64_t *executed, hipStream_t stream) {
-  if (d.dtype == SPAROA_F32) return fail(SPAROA_ERR_UNSUPPORTED, "fc bandwidth path: fp32");
-  if (d.m > 64) return fail(SPAROA_ERR_UNSUPPORTED, "fc bandwidth path: m > 64");
-  const int64_t slice = cdiv(cdiv(d.k, kWaves), 64) * 64;
-  if (slice > kMaxSlice) return fail(SPAROA_ERR_UNSUPPORTED, "fc bandwidth path: k > 16384");
+                           uint64_t *executed, hipStream_t stream, const DeviceRoute *route) {
+  if (!fc_bw_streams(d))
+    return fail(SPAROA_ERR_UNSUPPORTED, "weight-streaming FC: needs 16-bit, m <= 64, k <= 16384");
   const bool skip = mask != nullptr;
   FcBwArgs a;
   a.x = static_cast<const char *>(x);
@@ -288,8 +362,9 @@ sparoa_status launch_fc_bw(const sparoa_fc_desc &d, sparoa_path, const void *x,
   a.y = static_cast<char *>(y);
   a.mask = mask;
   a.executed = reinterpret_cast<unsigned long long *>(skip ? executed : nullptr);
-  a.M = d.m; a.K = d.k; a.N = d.n; a.slice = slice;
+  a.M = d.m; a.K = d.k; a.N = d.n; a.slice = slice_for(d);
   a.act = act;
+  a.route = route ? *route : DeviceRoute{nullptr, 0.0, 0, 0, nullptr};
   if (a.executed) {
     sparoa_status st = launch_set_u64(executed, 0, stream);
     if (st != SPAROA_OK) return st;
@@ -297,6 +372,7 @@ sparoa_status launch_fc_bw(const sparoa_fc_desc &d, sparoa_path, const void *x,
   const int mt = (int)cdiv(d.m, 16);
   // dense x rows are read as 16-byte vectors: needs every row 16-byte aligned
   const bool xvec = d.k % 8 == 0;
+  a.xvec = xvec ? 1 : 0;
   dim3 grid((unsigned)cdiv(d.n, kPanel));
   const bool ok = d.dtype == SPAROA_BF16 ? launch_dt<SPAROA_BF16>(mt, skip, xvec, grid, stream, a)
                                          : launch_dt<SPAROA_F16>(mt, skip, xvec, grid, stream, a);

@@ -57,6 +57,7 @@ struct GemmArgs {
   int64_t nchunks, chunks_per_split;
   int act;
   int split;
+  DeviceRoute route;
 };
 
 template <int DT>
@@ -147,9 +148,21 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
 
   // ---- chunk list (skip variant) -------------------------------------------
   int64_t count = c_end - c_begin;
+  bool use_list = SKIP;
   if constexpr (SKIP) {
-    const int cpg = (int)(a.Cin / 8);  // bitmap blocks per pixel
-    const int kv_words = (int)((a.K / 8 + 31) / 32);
+    if (a.route.counts) {
+      use_list = device_route_skip(a.route);
+      if (a.route.path_out && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && tid == 0)
+        *a.route.path_out = (use_list ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+    }
+  }
+  if constexpr (!SKIP) {
+    if (a.route.path_out && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && tid == 0)
+      *a.route.path_out = (uint32_t)a.route.bw_bit << 1;
+  }
+  if (SKIP && use_list) {
+    const int cpg = (int)((a.Cin + 7) / 8);  // bitmap blocks per pixel
+    const int kv_words = (int)((a.taps * cpg + 31) / 32);
     for (int i = tid; i < kv_words; i += kThreads) nzvec[i] = 0u;
     __syncthreads();
     for (int64_t p = tid; p < (int64_t)BM * a.taps; p += kThreads) {
@@ -174,9 +187,16 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
         const int64_t j = base + lane;
         bool nz = false;
         if (j < c_end) {
-          const int64_t v0 = j * (kBK / 8);  // first 8-wide K slice of the chunk
-          const int64_t v1 = min(v0 + kBK / 8, a.K / 8);
-          for (int64_t v = v0; v < v1; ++v) nz |= (nzvec[v >> 5] >> (v & 31)) & 1u;
+          // walk the chunk's k range one (tap, 8-channel block) run at a time
+          uint32_t k = (uint32_t)(j * kBK);
+          const uint32_t kend = (uint32_t)min(j * kBK + kBK, a.K);
+          while (k < kend) {
+            const uint32_t tap = k / cin, c = k - tap * cin;
+            const uint32_t bit = tap * (uint32_t)cpg + c / 8;
+            nz |= (nzvec[bit >> 5] >> (bit & 31)) & 1u;
+            const uint32_t cnext = (c / 8 + 1) * 8;
+            k = tap * cin + (cnext < cin ? cnext : cin);
+          }
         }
         const uint64_t bal = __ballot(nz);
         const int before = __popcll(bal & ((1ull << lane) - 1ull));
@@ -269,7 +289,9 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto chunk_at = [&](int64_t i) -> int64_t { return SKIP ? (int64_t)list[i] : c_begin + i; };
+  auto chunk_at = [&](int64_t i) -> int64_t {
+    return (SKIP && use_list) ? (int64_t)list[i] : c_begin + i;
+  };
 
   const int g = lane >> 4, rl = lane & 15;
   if (count > 0) {
@@ -366,7 +388,8 @@ bool dispatch(int bm, int bn, bool vec, bool skip, dim3 grid, hipStream_t st, co
   if (vec)
     return skip ? dispatch_tile<DT, true, true>(bm, bn, grid, st, a)
                 : dispatch_tile<DT, true, false>(bm, bn, grid, st, a);
-  return dispatch_tile<DT, false, false>(bm, bn, grid, st, a);
+  return skip ? dispatch_tile<DT, false, true>(bm, bn, grid, st, a)
+              : dispatch_tile<DT, false, false>(bm, bn, grid, st, a);
 }
 
 struct Shape {
@@ -419,6 +442,12 @@ sparoa_status launch_split_reduce(sparoa_dtype dt, const float *partial, int spl
   return SPAROA_OK;
 }
 
+bool gemm_skip_supported(const sparoa_conv_desc &d) {
+  const Shape s = shape_of(d);
+  const int64_t bits = d.kh * d.kw * cdiv(d.c_in, 8);
+  return cdiv(s.K, kBK) <= kMaxChunks && bits <= (int64_t)kMaxVecWords * 32;
+}
+
 GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path) {
   const Shape s = shape_of(d);
   GemmTileChoice t;
@@ -455,17 +484,16 @@ size_t gemm_workspace(const sparoa_conv_desc &d, sparoa_path path) {
 sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, const void *x,
                                const void *w, const void *bias, const void *residual,
                                sparoa_act act, const uint32_t *mask, void *y, void *ws,
-                               size_t ws_bytes, uint64_t *executed, hipStream_t stream) {
+                               size_t ws_bytes, uint64_t *executed, hipStream_t stream,
+                               const DeviceRoute *route) {
   const Shape s = shape_of(d);
   const GemmTileChoice t = gemm_choose(d, path);
   const int epv = d.dtype == SPAROA_F32 ? 4 : 8;
   const bool vec = d.c_in % epv == 0;
   const bool skip = mask != nullptr;
-  if (skip && (d.c_in % 8 != 0 || !vec))
-    return fail(SPAROA_ERR_UNSUPPORTED, "zero-skip conv needs c_in % 8 == 0");
   const int64_t nchunks = cdiv(s.K, kBK);
-  if (skip && nchunks > kMaxChunks)
-    return fail(SPAROA_ERR_UNSUPPORTED, "zero-skip conv: K above 65536");
+  if (skip && !gemm_skip_supported(d))
+    return fail(SPAROA_ERR_UNSUPPORTED, "zero-skip conv: K above the skip kernel's 65536");
   if (s.M > INT32_MAX || s.N > INT32_MAX) return fail(SPAROA_ERR_UNSUPPORTED, "GEMM too large");
 
   GemmArgs a;
@@ -485,6 +513,7 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   a.split = t.split_k;
   a.chunks_per_split = cdiv(nchunks, t.split_k);
   a.act = act;
+  a.route = route ? *route : DeviceRoute{nullptr, 0.0, 0, 0, nullptr};
   const int64_t gz = cdiv(nchunks, a.chunks_per_split);
   a.split = (int)gz;
   if (gz > 1 && ws_bytes < (size_t)gz * s.M * s.N * sizeof(float))

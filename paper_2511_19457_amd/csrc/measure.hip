@@ -184,6 +184,177 @@ __global__ __launch_bounds__(kThreads) void measure_main(
   }
 }
 
+// One bitmap bit per lane (block = 1 row x V columns, V = elements per
+// 16-byte vector): item index == block index, so the 64 items of a wave slot
+// are two whole bitmap words.  The wave ballots its bits and two lanes store
+// the words: no atomics, and the bitmap needs no clearing.  The grid's slots
+// start at multiples of 64 items, which keeps the words aligned.
+template <int ESZ, int V>
+__global__ __launch_bounds__(kThreads) void measure_lanebit(const char *__restrict__ x,
+                                                            int64_t items, int64_t words,
+                                                            uint32_t *__restrict__ mask,
+                                                            sparoa_counts *counts) {
+  const int lane = threadIdx.x & 63;
+  const int64_t slot = (int64_t)gridDim.x * kThreads;
+  uint64_t zeros = 0, nonzero = 0;
+  for (int64_t base = (int64_t)blockIdx.x * kThreads; base < items; base += slot * kUnroll) {
+    uint32_t nz[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t item = base + u * slot + threadIdx.x;
+      nz[u] = 0;
+      if (item < items) {
+        nz[u] = nonzero_bits<ESZ, V>(x + item * 16);
+        zeros += V - __popc(nz[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint64_t bal = __ballot(nz[u] != 0u);
+      const int64_t w0 = (base + u * slot + (threadIdx.x & ~63)) >> 5;
+      if (lane == 0 && w0 < words) mask[w0] = (uint32_t)bal;
+      if (lane == 32 && w0 + 1 < words) mask[w0 + 1] = (uint32_t)(bal >> 32);
+      nonzero += lane == 0 ? (uint64_t)__popcll(bal) : 0ull;
+    }
+  }
+  const uint64_t wz = wave_sum(zeros), wn = wave_sum(nonzero);
+  if (lane == 0) {
+    if (wz) atomicAdd((unsigned long long *)&counts->zeros, (unsigned long long)wz);
+    if (wn) atomicAdd((unsigned long long *)&counts->zero_blocks, (unsigned long long)(0ull - wn));
+  }
+}
+
+// Column strips: a single block row covering all rows, one column per block
+// (the "column is zero in every row" bitmap).  A work-group owns 64 column
+// groups (64 V columns = 2 V whole bitmap words); its 4 waves take every
+// 4th row of the strip, their flags are ORed in LDS, and wave 0 assembles and
+// stores the words: no atomics, no clearing.
+template <int ESZ, int V>
+__global__ __launch_bounds__(kThreads) void measure_strips(const char *__restrict__ x,
+                                                           int64_t rows, int64_t cols,
+                                                           int64_t words,
+                                                           uint32_t *__restrict__ mask,
+                                                           sparoa_counts *counts) {
+  static_assert(32 % V == 0, "lanes per word");
+  __shared__ uint32_t flags[kThreads];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t gpr = cols / V;
+  const int64_t g = (int64_t)blockIdx.x * 64 + lane;
+  const int64_t row_bytes = cols * ESZ;
+  uint64_t zeros = 0;
+  uint32_t nz = 0;
+  if (g < gpr) {
+    const char *p = x + g * V * ESZ;
+    int64_t r = wave;
+    for (; r + 12 < rows; r += 16) {  // four rows of this wave in flight
+      const uint32_t b0 = nonzero_bits<ESZ, V>(p + r * row_bytes);
+      const uint32_t b1 = nonzero_bits<ESZ, V>(p + (r + 4) * row_bytes);
+      const uint32_t b2 = nonzero_bits<ESZ, V>(p + (r + 8) * row_bytes);
+      const uint32_t b3 = nonzero_bits<ESZ, V>(p + (r + 12) * row_bytes);
+      zeros += 4 * V - __popc(b0) - __popc(b1) - __popc(b2) - __popc(b3);
+      nz |= b0 | b1 | b2 | b3;
+    }
+    for (; r < rows; r += 4) {
+      const uint32_t b = nonzero_bits<ESZ, V>(p + r * row_bytes);
+      zeros += V - __popc(b);
+      nz |= b;
+    }
+  }
+  flags[threadIdx.x] = nz;
+  __syncthreads();
+  uint64_t nonzero = 0;
+  if (wave == 0) {
+    const uint32_t f = flags[lane] | flags[64 + lane] | flags[128 + lane] | flags[192 + lane];
+    constexpr int kLanesPerWord = 32 / V;
+    uint32_t word = 0;
+#pragma unroll
+    for (int j = 0; j < kLanesPerWord; ++j) word |= __shfl(f, (lane & ~(kLanesPerWord - 1)) + j, 64) << (j * V);
+    const int64_t w = ((int64_t)blockIdx.x * 64 + lane) / kLanesPerWord;
+    if (lane % kLanesPerWord == 0 && w < words) {
+      mask[w] = word;
+      nonzero = __popc(word);
+    }
+  }
+  const uint64_t wz = wave_sum(zeros), wn = wave_sum(nonzero);
+  if (lane == 0) {
+    if (wz) atomicAdd((unsigned long long *)&counts->zeros, (unsigned long long)wz);
+    if (wn) atomicAdd((unsigned long long *)&counts->zero_blocks, (unsigned long long)(0ull - wn));
+  }
+}
+
+// Column strips that fit one work-group (at most 16 x 64 column groups): 16
+// waves in ceil(groups / 64) sets, the waves of a set taking interleaved
+// rows; flags and counts combine in LDS and the work-group writes the bitmap
+// and all four counts itself -- one launch, no atomics, no clearing.
+template <int ESZ, int V>
+__global__ __launch_bounds__(1024) void measure_strips_wg(const char *__restrict__ x, int64_t rows,
+                                                           int64_t cols, int64_t words,
+                                                           uint32_t *__restrict__ mask,
+                                                           sparoa_counts *counts) {
+  static_assert(32 % V == 0, "lanes per word");
+  __shared__ uint32_t flags[16][64];
+  __shared__ unsigned long long zsum[16], nzsum[16];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t gpr = cols / V;
+  const int sets = (int)((gpr + 63) / 64);
+  const int wps = 16 / sets;  // waves per set
+  const int set = wave / wps, sub = wave - set * wps;
+  const int64_t g = (int64_t)set * 64 + lane;
+  const int64_t row_bytes = cols * ESZ;
+  uint64_t zeros = 0;
+  uint32_t nz = 0;
+  if (set < sets && g < gpr) {
+    const char *p = x + g * V * ESZ;
+    int64_t r = sub;
+    for (; r + 3 * wps < rows; r += 4 * wps) {  // four rows in flight
+      const uint32_t b0 = nonzero_bits<ESZ, V>(p + r * row_bytes);
+      const uint32_t b1 = nonzero_bits<ESZ, V>(p + (r + wps) * row_bytes);
+      const uint32_t b2 = nonzero_bits<ESZ, V>(p + (r + 2 * wps) * row_bytes);
+      const uint32_t b3 = nonzero_bits<ESZ, V>(p + (r + 3 * wps) * row_bytes);
+      zeros += 4 * V - __popc(b0) - __popc(b1) - __popc(b2) - __popc(b3);
+      nz |= b0 | b1 | b2 | b3;
+    }
+    for (; r < rows; r += wps) {
+      const uint32_t b = nonzero_bits<ESZ, V>(p + r * row_bytes);
+      zeros += V - __popc(b);
+      nz |= b;
+    }
+  }
+  flags[wave][lane] = nz;
+  const uint64_t wz = wave_sum(zeros);
+  if (lane == 0) zsum[wave] = wz;
+  __syncthreads();
+  uint64_t nonzero = 0;
+  if (set < sets && sub == 0) {
+    uint32_t f = 0;
+    for (int i = 0; i < wps; ++i) f |= flags[wave + i][lane];
+    constexpr int kLanesPerWord = 32 / V;
+    uint32_t word = 0;
+#pragma unroll
+    for (int j = 0; j < kLanesPerWord; ++j)
+      word |= __shfl(f, (lane & ~(kLanesPerWord - 1)) + j, 64) << (j * V);
+    const int64_t w = ((int64_t)set * 64 + lane) / kLanesPerWord;
+    if (lane % kLanesPerWord == 0 && w < words) {
+      mask[w] = word;
+      nonzero = __popc(word);
+    }
+  }
+  const uint64_t wn = wave_sum(nonzero);
+  if (lane == 0) nzsum[wave] = wn;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long z = 0, n = 0;
+    for (int i = 0; i < 16; ++i) {
+      z += zsum[i];
+      n += nzsum[i];
+    }
+    counts->zeros = z;
+    counts->numel = (uint64_t)(rows * cols);
+    counts->zero_blocks = (uint64_t)cols - n;
+    counts->num_blocks = (uint64_t)cols;
+  }
+}
+
 template <int ESZ, int V>
 void launch_main(dim3 grid, hipStream_t st, const void *x, int64_t cols, int64_t rs, int64_t br,
                  int64_t bc, int64_t nbc, int64_t nbr_s, int64_t cpb, uint32_t *mask,
@@ -211,16 +382,57 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
   const int64_t nb = want_mask ? cdiv(rows, br) * nbc : 0;
   const int64_t words = want_mask ? cdiv(nb, 32) : 0;
 
+  const bool vec = cols % vw == 0 && (!want_mask || bc % vw == 0 || vw % bc == 0);
+  // fast paths that own whole bitmap words (no atomics, no clearing)
+  const bool lanebit = want_mask && vec && br == 1 && bc == vw && !per_sample;
+  const bool strips = want_mask && vec && bc == 1 && !per_sample && br >= rows;
+
+  if (strips && cols / vw <= 16 * 64) {  // one work-group measures it all
+    if (esz == 2)
+      hipLaunchKernelGGL((measure_strips_wg<2, 8>), dim3(1), dim3(1024), 0, stream,
+                         static_cast<const char *>(x), rows, cols, words, mask, counts);
+    else
+      hipLaunchKernelGGL((measure_strips_wg<4, 4>), dim3(1), dim3(1024), 0, stream,
+                         static_cast<const char *>(x), rows, cols, words, mask, counts);
+    SPAROA_LAUNCH_CHECK("measure_strips_wg");
+    return SPAROA_OK;
+  }
+
   {
-    const int64_t work = words > S ? words : S;
+    const int64_t zw = (lanebit || strips) ? 0 : words;   // words to clear
+    const int64_t work = zw > S ? zw : S;
     const int64_t g = work < 1 ? 1 : (cdiv(work, 256) < 1024 ? cdiv(work, 256) : 1024);
     hipLaunchKernelGGL(measure_init, dim3((unsigned)g), dim3(256), 0, stream, counts,
-                       (uint64_t)(rows * cols), (uint64_t)nb, mask, words, per_sample,
+                       (uint64_t)(rows * cols), (uint64_t)nb, mask, zw, per_sample,
                        per_sample ? S : 0);
     SPAROA_LAUNCH_CHECK("measure_init");
   }
 
-  const bool vec = cols % vw == 0 && (!want_mask || bc % vw == 0 || vw % bc == 0);
+  if (lanebit) {
+    const int64_t items = rows * (cols / vw);
+    int64_t gx = cdiv(items, (int64_t)kThreads);
+    if (gx > 2048) gx = 2048;
+    if (esz == 2)
+      hipLaunchKernelGGL((measure_lanebit<2, 8>), dim3((unsigned)gx), dim3(kThreads), 0, stream,
+                         static_cast<const char *>(x), items, words, mask, counts);
+    else
+      hipLaunchKernelGGL((measure_lanebit<4, 4>), dim3((unsigned)gx), dim3(kThreads), 0, stream,
+                         static_cast<const char *>(x), items, words, mask, counts);
+    SPAROA_LAUNCH_CHECK("measure_lanebit");
+    return SPAROA_OK;
+  }
+  if (strips) {
+    const int64_t gx = cdiv(cols / vw, 64);
+    if (esz == 2)
+      hipLaunchKernelGGL((measure_strips<2, 8>), dim3((unsigned)gx), dim3(kThreads), 0, stream,
+                         static_cast<const char *>(x), rows, cols, words, mask, counts);
+    else
+      hipLaunchKernelGGL((measure_strips<4, 4>), dim3((unsigned)gx), dim3(kThreads), 0, stream,
+                         static_cast<const char *>(x), rows, cols, words, mask, counts);
+    SPAROA_LAUNCH_CHECK("measure_strips");
+    return SPAROA_OK;
+  }
+
   const int V = vec ? vw : 1;
   const int64_t cpb = cdiv(br < rs ? br : rs, kRowChunk);   // row chunks per block row
   const int64_t items_s = nbr_s * cpb * (cols / V);

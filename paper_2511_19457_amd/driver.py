@@ -13,6 +13,11 @@ Section 5 online execution on one device):
      activation), producing the next layer's input.
 Max pooling is glue and is not routed.  All computation is in libsparoa.so;
 this module only allocates buffers (PyTorch) and sequences the C calls.
+
+With ``routed=True`` steps 2-4 run without the host round trip: the counts
+stay in device memory and the routed kernels take the skip decision
+themselves (same arithmetic as sparoa_route); counts and paths are read back
+once, after the whole stack.
 """
 import time
 from dataclasses import dataclass
@@ -80,7 +85,7 @@ class Engine:
                 else:
                     w = synth.he_normal(wshape, fan_in, dtype, seed + 1000 + i).to(self.dev)
                 st["w"] = w
-                if L.kind == "fc" and fam & 2:
+                if L.kind == "fc" and abi.sparoa_fc_uses_packed(d, fam):
                     wp = torch.empty(abi.sparoa_fc_packed_bytes(d) // w.element_size(),
                                      dtype=dtype, device=self.dev)
                     abi.sparoa_fc_pack_weights(d, w, wp)
@@ -90,6 +95,7 @@ class Engine:
                     abi.sparoa_mask_words(st["rows"], st["cols"], st["br"], st["bc"]),
                     dtype=torch.int32, device=self.dev)
                 st["ws"] = torch.zeros(max(16, ws), dtype=torch.uint8, device=self.dev)
+                st["path"] = torch.zeros(1, dtype=torch.int32, device=self.dev)
             self.acts[i + 1] = torch.empty(output_shape(L), dtype=dtype, device=self.dev)
             self.st.append(st)
         torch.cuda.synchronize(self.dev)
@@ -118,7 +124,7 @@ class Engine:
         if L.kind == "conv":
             abi.sparoa_conv2d(st["desc"], path, x, st["w"], None, res, L.act, mask, y, st["ws"])
         else:
-            w = st["wp"] if (path & 2) else st["w"]
+            w = st["wp"] if "wp" in st and (path & 2) else st["w"]
             abi.sparoa_fc(st["desc"], path, x, w, None, res, L.act, mask, y, st["ws"])
         rec.rho_e = c["zeros"] / c["numel"]
         rec.rho_b = c["zero_blocks"] / c["num_blocks"] if c["num_blocks"] else 0.0
@@ -127,12 +133,52 @@ class Engine:
         rec.counts = c
         return rec
 
-    def run(self, x, timed=False):
+    def run_layer_routed(self, i):
+        """Runs layer i with device-side routing (no host synchronisation)."""
+        L, st = self.layers[i], self.st[i]
+        x = self.acts[L.src]
+        y = self.acts[i + 1]
+        if L.kind == "maxpool":
+            s = L.shape
+            abi.sparoa_maxpool2d(x, s["n"], s["c"], s["h"], s["w"], s["k"], s["s"], s["p"], y)
+            return
+        abi.sparoa_measure_sparsity(x, st["rows"], st["cols"], st["br"], st["bc"], 0,
+                                    st["counts"], st["mask"])
+        res = self.acts[L.res] if L.res is not None else None
+        if L.kind == "conv":
+            abi.sparoa_conv2d_routed(st["desc"], self.s_thr, self.c_thr, self.mode, st["counts"],
+                                     x, st["w"], None, res, L.act, st["mask"], y, st["ws"],
+                                     st["path"])
+        else:
+            abi.sparoa_fc_routed(st["desc"], self.s_thr, self.c_thr, self.mode, st["counts"], x,
+                                 st["w"], st.get("wp"), None, res, L.act, st["mask"], y, st["ws"],
+                                 st["path"])
+
+    def records_from_device(self):
+        """Counts and paths of the last routed run, read back after the fact."""
+        recs = []
+        for L, st in zip(self.layers, self.st):
+            rec = LayerRecord(L.name, L.kind)
+            if L.kind != "maxpool":
+                c = dict(zip(("zeros", "numel", "zero_blocks", "num_blocks"),
+                             st["counts"].cpu().tolist()))
+                rec.counts = c
+                rec.rho_e = c["zeros"] / c["numel"]
+                rec.rho_b = c["zero_blocks"] / c["num_blocks"] if c["num_blocks"] else 0.0
+                inten = st["inten"]
+                rec.intensity, rec.macs, rec.bytes = (inten["intensity"], inten["macs"],
+                                                      inten["bytes"])
+                rec.path = int(st["path"].item())
+            recs.append(rec)
+        return recs
+
+    def run(self, x, timed=False, routed=False):
         """Full stack on input x (device tensor of the input shape); returns
         (output, records, wall seconds)."""
         assert tuple(x.shape) == input_shape(self.layers) and x.dtype == self.dtype
         self.acts[0] = x
         recs = []
+        evs = []
         torch.cuda.synchronize(self.dev)
         t0 = time.perf_counter()
         for i in range(len(self.layers)):
@@ -140,13 +186,19 @@ class Engine:
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record()
-            r = self.run_layer(i)
+            if routed:
+                self.run_layer_routed(i)
+            else:
+                recs.append(self.run_layer(i))
             if timed:
                 e1.record()
-                r._ev = (e0, e1)
-            recs.append(r)
+                evs.append((e0, e1))
         torch.cuda.synchronize(self.dev)
         wall = time.perf_counter() - t0
+        if routed:
+            recs = self.records_from_device()
+        for r, ev in zip(recs, evs):
+            r._ev = ev
         if timed:
             for r in recs:
                 r.us = r._ev[0].elapsed_time(r._ev[1]) * 1e3

@@ -140,9 +140,16 @@ def test_validation_rejects_before_device_work():
         abi.sparoa_fc(abi.fc_desc(4, 64, 64, has_bias=1), 0, FAKE, FAKE, None, None, 0, None,
                       FAKE)
     assert e.value.status == 1
-    # BW FC with m > 64 is a valid request the kernel does not take
+    # a BW FC the weight-streaming kernel cannot take (m > 64, or fp32) runs
+    # the implicit GEMM on w[n][k], with that kernel's bitmap granularity
     big = abi.fc_desc(65, 64, 64)
-    assert abi.sparoa_fc_skip_block(big, abi.PATH_SKIP_BW) == (65, 1)
+    assert abi.sparoa_fc_skip_block(big, abi.PATH_SKIP_BW) == (1, 8)
+    assert not abi.sparoa_fc_uses_packed(big, abi.PATH_SKIP_BW)
+    small = abi.fc_desc(64, 64, 64)
+    assert abi.sparoa_fc_skip_block(small, abi.PATH_SKIP_BW) == (64, 1)
+    assert abi.sparoa_fc_uses_packed(small, abi.PATH_DENSE_BW)
+    assert not abi.sparoa_fc_uses_packed(small, abi.PATH_DENSE_MFMA)
+    assert not abi.sparoa_fc_uses_packed(abi.fc_desc(8, 64, 64, abi.F32), abi.PATH_DENSE_BW)
     # measurement: zero rows, samples not dividing rows, misaligned x
     counts = FAKE
     for args, status in (((FAKE, 0, 8, 0, 0, 0, counts), 1),

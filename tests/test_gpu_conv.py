@@ -82,7 +82,8 @@ def test_conv_dense_vs_oracle(dt, shape):
 @pytest.mark.parametrize("dt", ["bf16", "f16"])
 @pytest.mark.parametrize("rho", [0.0, 0.9, 0.999, 1.0])
 @pytest.mark.parametrize("shape", [GEMM_SHAPES[0], GEMM_SHAPES[2], GEMM_SHAPES[6],
-                                   (2, 64, 16, 16, 128, 3, 3, 1, 1, 1, 1, 1, 1, 1)])
+                                   (2, 64, 16, 16, 128, 3, 3, 1, 1, 1, 1, 1, 1, 1),
+                                   GEMM_SHAPES[3], GEMM_SHAPES[4], GEMM_SHAPES[5]])
 def test_conv_skip_equals_dense_and_oracle(dt, rho, shape):
     n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, g = shape
     x = synth.sparse_nhwc(n, h, wd, cin, rho, dt, int(rho * 1000) + cin)

@@ -32,7 +32,7 @@ def run_fc(x, w, bias, act, path, wp=None, residual=None):
     br, bc = abi.sparoa_fc_skip_block(d, path)
     mask = torch.zeros(abi.sparoa_mask_words(m, k, br, bc), dtype=torch.int32, device=dev)
     c = abi.sparoa_measure_sparsity_sync(xd, m, k, br, bc, 0, counts, mask)
-    if path & 2:
+    if abi.sparoa_fc_uses_packed(d, path):
         if wp is None:
             wp = torch.empty(abi.sparoa_fc_packed_bytes(d) // x.element_size(), dtype=x.dtype,
                              device=dev)
@@ -52,7 +52,7 @@ def run_fc(x, w, bias, act, path, wp=None, residual=None):
 
 
 SHAPES = [(1, 256, 64), (8, 512, 192), (16, 640, 100), (33, 96, 70), (64, 1024, 256),
-          (5, 1000, 64), (64, 4096, 128)]
+          (5, 1000, 64), (64, 4096, 128), (65, 256, 64), (96, 520, 130)]
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f16"])
@@ -79,7 +79,7 @@ def test_fc_fp32_mfma(shape):
     m, k, n = shape
     x = synth.sparse_matrix(m, k, 0.5, "iid", "f32", 500 + m)
     w = synth.normal((n, k), "f32", 501 + m, std=k ** -0.5)
-    for path in (0, 1):
+    for path in (0, 1, 2, 3):      # fp32 bandwidth paths run the implicit GEMM
         y, _, _, _ = run_fc(x, w, None, 0, path)
         yr, ar = oracle.fc(x, w, m, k, n)
         assert_close(y, yr, ar, RTOL[torch.float32], f"fc f32 {shape} path {path}")

@@ -1,0 +1,159 @@
+"""Device-side routing: the path a kernel takes from the counts in device
+memory must equal sparoa_route's (and the oracle's) on the same counts, and
+its output must equal the fixed-path output bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _abi():
+    from paper_2511_19457_amd import abi
+    return abi
+
+
+def _measure(abi, x, rows, cols, br, bc):
+    dev = x.device
+    counts = torch.zeros(4, dtype=torch.int64, device=dev)
+    mask = torch.zeros(abi.sparoa_mask_words(rows, cols, br, bc), dtype=torch.int32, device=dev)
+    abi.sparoa_measure_sparsity(x, rows, cols, br, bc, 0, counts, mask)
+    return counts, mask
+
+
+FC_CASES = [(1, 4096, 1024, "iid", 0.9), (8, 2048, 512, "block", 0.8), (64, 1024, 256, "block", 0.9),
+            (16, 512, 80, "iid", 0.3), (256, 768, 512, "block", 0.95), (300, 512, 200, "iid", 0.5)]
+
+
+@pytest.mark.parametrize("case", FC_CASES)
+@pytest.mark.parametrize("thr_kind", ["below", "tie", "above"])
+def test_fc_routed_matches_host_route_and_fixed_path(case, thr_kind):
+    abi = _abi()
+    m, k, n, pattern, rho = case
+    dev = torch.device("cuda")
+    x = synth.sparse_matrix(m, k, rho, pattern, "bf16", FC_CASES.index(case))
+    w = synth.normal((n, k), "bf16", 99, std=k ** -0.5)
+    d = abi.fc_desc(m, k, n, abi.BF16)
+    inten = abi.sparoa_op_intensity_fc(d)
+    fam = abi.PATH_SKIP_BW if inten["intensity"] < 315.0 else abi.PATH_SKIP_MFMA
+    br, bc = abi.sparoa_fc_skip_block(d, fam)
+    ref = oracle.measure(x, m, k, br, bc)
+    rho_b = ref["zero_blocks"] / ref["num_blocks"]
+    s_thr = {"below": rho_b / 2, "tie": rho_b, "above": min(1.0, rho_b + 0.01)}[thr_kind]
+    if thr_kind == "above" and rho_b >= 1.0:
+        pytest.skip("nothing above a fully sparse input")
+    want = oracle.route(ref["zeros"], ref["numel"], ref["zero_blocks"], ref["num_blocks"],
+                        inten["intensity"], 0, s_thr, 315.0)
+    xd, wd = x.to(dev), w.to(dev)
+    wp = torch.empty(abi.sparoa_fc_packed_bytes(d) // 2, dtype=torch.bfloat16, device=dev)
+    abi.sparoa_fc_pack_weights(d, wd, wp)
+    ws = torch.zeros(max(16, max(abi.sparoa_fc_workspace_size(d, p) for p in range(4))),
+                     dtype=torch.uint8, device=dev)
+    counts, mask = _measure(abi, xd, m, k, br, bc)
+    y = torch.full((m, n), float("nan"), dtype=torch.bfloat16, device=dev)
+    path = torch.full((1,), -1, dtype=torch.int32, device=dev)
+    abi.sparoa_fc_routed(d, s_thr, 315.0, abi.ROUTE_BLOCK, counts, xd, wd, wp, None, None,
+                         abi.ACT_RELU, mask, y, ws, path)
+    torch.cuda.synchronize()
+    assert int(path.item()) == want
+    host = abi.sparoa_route(dict(zip(("zeros", "numel", "zero_blocks", "num_blocks"),
+                                     counts.cpu().tolist())), inten, 0, s_thr, 315.0)
+    assert host == want
+    y2 = torch.full((m, n), float("nan"), dtype=torch.bfloat16, device=dev)
+    abi.sparoa_fc(d, want, xd, wp if abi.sparoa_fc_uses_packed(d, want) else wd, None, None,
+                  abi.ACT_RELU,
+                  mask if want & 1 else None, y2, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+
+
+CONV_CASES = [(2, 64, 14, 14, 64, 3, 3, 1, 1, 1, 1, 1), (1, 32, 20, 20, 192, 1, 1, 1, 1, 0, 0, 1),
+              (2, 96, 12, 12, 96, 3, 3, 2, 2, 1, 1, 96)]
+
+
+@pytest.mark.parametrize("case", CONV_CASES)
+@pytest.mark.parametrize("rho", [0.2, 0.999])
+def test_conv_routed_matches_host_route_and_fixed_path(case, rho):
+    abi = _abi()
+    n, cin, h, w, cout, kh, kw, sh, sw, ph, pw, g = case
+    dev = torch.device("cuda")
+    d = abi.conv_desc(n, cin, h, w, cout, kh, kw, sh, sw, ph, pw, 1, 1, g, abi.F16)
+    x = synth.sparse_nhwc(n, h, w, cin, rho, "f16", int(rho * 100) + cin)
+    wt = synth.he_normal((cout, kh, kw, cin // g), kh * kw * cin // g, "f16", 7)
+    inten = abi.sparoa_op_intensity_conv(d)
+    dwise = g > 1
+    fam = abi.PATH_SKIP_BW if (dwise or inten["intensity"] < 315.0) else abi.PATH_SKIP_MFMA
+    br, bc = abi.sparoa_conv2d_skip_block(d, fam)
+    ref = oracle.measure(x, n * h * w, cin, br, bc)
+    s_thr = 0.5
+    want = oracle.route(ref["zeros"], ref["numel"], ref["zero_blocks"], ref["num_blocks"],
+                        inten["intensity"], int(dwise), s_thr, 315.0)
+    xd, wd = x.to(dev), wt.to(dev)
+    counts, mask = _measure(abi, xd, n * h * w, cin, br, bc)
+    ws = torch.zeros(max(16, max(abi.sparoa_conv2d_workspace_size(d, p) for p in range(4))),
+                     dtype=torch.uint8, device=dev)
+    ho = (h + 2 * ph - kh) // sh + 1
+    wo = (w + 2 * pw - kw) // sw + 1
+    y = torch.full((n, ho, wo, cout), float("nan"), dtype=torch.float16, device=dev)
+    path = torch.full((1,), -1, dtype=torch.int32, device=dev)
+    abi.sparoa_conv2d_routed(d, s_thr, 315.0, abi.ROUTE_BLOCK, counts, xd, wd, None, None,
+                             abi.ACT_RELU, mask, y, ws, path)
+    torch.cuda.synchronize()
+    assert int(path.item()) == want
+    y2 = torch.full_like(y, float("nan"))
+    abi.sparoa_conv2d(d, want, xd, wd, None, None, abi.ACT_RELU, mask if want & 1 else None, y2,
+                      ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+
+
+def test_fc_ops_run_equals_per_op_routed_calls():
+    """The native batch executor runs measure + routed FC per op: paths and
+    outputs equal the per-op calls, counts equal the oracle's."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    specs = [(1, 2048, 512, "iid", 0.95), (8, 1024, 256, "block", 0.9), (64, 512, 128, "iid", 0.5),
+             (200, 512, 256, "block", 0.9), (16, 300, 70, "iid", 0.0)]
+    ops, bufs = [], []
+    for i, (m, k, n, pat, rho) in enumerate(specs):
+        d = abi.fc_desc(m, k, n, abi.F16)
+        x = synth.sparse_matrix(m, k, rho, pat, "f16", 300 + i).to(dev)
+        w = synth.normal((n, k), "f16", 400 + i, std=k ** -0.5).to(dev)
+        wp = torch.empty(abi.sparoa_fc_packed_bytes(d) // 2, dtype=torch.float16, device=dev)
+        abi.sparoa_fc_pack_weights(d, w, wp)
+        inten = abi.sparoa_op_intensity_fc(d)
+        fam = abi.PATH_SKIP_BW if inten["intensity"] < 315.0 else abi.PATH_SKIP_MFMA
+        br, bc = abi.sparoa_fc_skip_block(d, fam)
+        b = dict(d=d, x=x, w=w, wp=wp, br=br, bc=bc,
+                 counts=torch.zeros(4, dtype=torch.int64, device=dev),
+                 mask=torch.zeros(abi.sparoa_mask_words(m, k, br, bc), dtype=torch.int32,
+                                  device=dev),
+                 y=torch.full((m, n), float("nan"), dtype=torch.float16, device=dev),
+                 ws=torch.zeros(max(16, max(abi.sparoa_fc_workspace_size(d, p) for p in range(4))),
+                                dtype=torch.uint8, device=dev),
+                 path=torch.full((1,), -1, dtype=torch.int32, device=dev))
+        bufs.append(b)
+        ops.append(abi.fc_op(d, x, w, wp, None, None, abi.ACT_RELU, b["counts"], b["mask"], b["y"],
+                             b["ws"], b["path"]))
+    arr = abi.fc_op_array(ops)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * len(ops))]
+    for e in evs:
+        e.record()
+    abi.sparoa_fc_ops_run(arr, 0.5, 315.0, abi.ROUTE_BLOCK, events=evs)
+    torch.cuda.synchronize()
+    for i, b in enumerate(bufs):
+        m, k = b["x"].shape
+        ref = oracle.measure(b["x"].cpu(), m, k, b["br"], b["bc"])
+        c = b["counts"].cpu().tolist()
+        assert c == [ref["zeros"], ref["numel"], ref["zero_blocks"], ref["num_blocks"]]
+        y2 = torch.full_like(b["y"], float("nan"))
+        p2 = torch.full((1,), -1, dtype=torch.int32, device=dev)
+        abi.sparoa_fc_routed(b["d"], 0.5, 315.0, abi.ROUTE_BLOCK, b["counts"], b["x"], b["w"],
+                             b["wp"], None, None, abi.ACT_RELU, b["mask"], y2, b["ws"], p2)
+        torch.cuda.synchronize()
+        assert int(p2.item()) == int(b["path"].item())
+        assert torch.equal(y2, b["y"])
+        assert evs[2 * i].elapsed_time(evs[2 * i + 1]) > 0

@@ -100,3 +100,29 @@ def test_stack_full_size(stack, batch):
     else:
         layers, dt, seed = stacks.ffn(), torch.float16, synth.seed_for(5, 12)
     _run_stack(layers, dt, seed, 128)
+
+
+@pytest.mark.parametrize("stack", ["resnet50", "mobilenet_v2", "ffn"])
+def test_device_routing_equals_host_routing(stack):
+    """Device-side routing takes the same path as the host route on every
+    layer and produces bit-identical activations."""
+    from paper_2511_19457_amd import stacks
+    from paper_2511_19457_amd.driver import Engine
+    from paper_2511_19457_amd.stacks import input_shape
+    if stack == "resnet50":
+        layers, dt = stacks.resnet50(1), torch.bfloat16
+    elif stack == "mobilenet_v2":
+        layers, dt = stacks.mobilenet_v2(2), torch.float16
+    else:
+        layers, dt = stacks.ffn(2048, 768, 3072, 2), torch.float16
+    for thr in (0.05, 0.5):
+        eng = Engine(layers, dt, "cuda", seed=11, sparsity_thr=thr)
+        x = synth.normal(input_shape(layers), dt, 12).cuda()
+        y_host, rec_host, _ = eng.run(x)
+        y_host = y_host.clone()
+        acts_host = [a.clone() for a in eng.acts[1:]]
+        y_dev, rec_dev, _ = eng.run(x, routed=True)
+        assert [r.path for r in rec_dev] == [r.path for r in rec_host]
+        for a, b in zip(acts_host, eng.acts[1:]):
+            assert torch.equal(a, b)
+        assert torch.equal(y_host, y_dev)
