@@ -116,10 +116,6 @@ def build_cases(abi, torch, synth, dev):
         c.path_dev = torch.zeros(1, dtype=torch.int32, device=dev)
         cases.append(c)
     torch.cuda.synchronize()
-    for c in cases:   # only the packed copy is needed by the bandwidth paths
-        if c.inten["intensity"] < INTENSITY_THR:
-            c.w = None
-    torch.cuda.empty_cache()
     return cases
 
 
@@ -151,27 +147,44 @@ def run_case(abi, c, s_thr, ev=None):
     return path
 
 
-def forced_times(abi, torch, c, paths, reps=20):
-    """Median duration (us) of the FC kernel on each forced path (HIP events)."""
+def forced_times(abi, torch, c, paths, reps=20, rounds=3):
+    """Duration (us) of the FC kernel on each forced path: `reps` back-to-back
+    launches between one pair of HIP events, best of `rounds` (the weights
+    stay cache-resident here, so these read low next to the cold step)."""
     out = {}
     abi.sparoa_measure_sparsity_sync(c.x, c.m, K, c.br, c.bc, 0, c.counts, c.mask)
     for p in paths:
-        w = c.wp if p & 2 else c.w
+        w = c.wp if abi.sparoa_fc_uses_packed(c.desc, p) else c.w
         if w is None:
             continue
-        ts = []
-        for _ in range(reps):
+        best = None
+        for _ in range(rounds):
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record()
-            abi.sparoa_fc(c.desc, p, c.x, w, None, None, abi.ACT_NONE, c.mask if p & 1 else None,
-                          c.y, c.ws)
+            for _ in range(reps):
+                abi.sparoa_fc(c.desc, p, c.x, w, None, None, abi.ACT_NONE,
+                              c.mask if p & 1 else None, c.y, c.ws)
             e1.record()
             e1.synchronize()
-            ts.append(e0.elapsed_time(e1) * 1e3)
-        ts.sort()
-        out[p] = ts[len(ts) // 2]
+            t = e0.elapsed_time(e1) * 1e3 / reps
+            best = t if best is None else min(best, t)
+        out[p] = best
     return out
+
+
+def routed_time(abi, torch, c, s_thr, reps=20):
+    """Duration (us) of the device-routed FC call of one operator, `reps`
+    launches back to back between one pair of HIP events."""
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        abi.sparoa_fc_routed(c.desc, s_thr, INTENSITY_THR, abi.ROUTE_BLOCK, c.counts, c.x, c.w,
+                             c.wp, None, None, abi.ACT_NONE, c.mask, c.y, c.ws, c.path_dev)
+    e1.record()
+    e1.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / reps
 
 
 def alg_bytes(c, path, nonzero_cols):
@@ -228,7 +241,8 @@ def main():
     # metric, and the data the routing threshold is calibrated from.
     print("bench: forced-path sweep", file=sys.stderr, flush=True)
     for c in cases:
-        c.forced = forced_times(abi, torch, c, (abi.PATH_DENSE_BW, abi.PATH_SKIP_BW))
+        c.forced = forced_times(abi, torch, c, (abi.PATH_DENSE_BW, abi.PATH_SKIP_BW,
+                                                abi.PATH_DENSE_MFMA))
         st = c.counts.cpu().tolist()
         c.rho_e = st[0] / st[1]
         c.rho_b = st[2] / st[3]
@@ -260,22 +274,30 @@ def main():
                 step_fn(abi, c, s_thr)
     torch.cuda.synchronize()
 
+    # device routing: operator i+1's measurement on a side stream overlaps
+    # operator i's routed FC on the main stream (one event per operator);
+    # one pair of timing events brackets each step's FC phase
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()                      # default priority
+    ready = [torch.cuda.Event() for _ in cases]
+    phase = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(args.steps)]
     evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-            for _ in cases] for _ in range(args.steps)]
-    for step_evs in evs:          # create the events before handing them to the library
-        for e0, e1 in step_evs:
-            e0.record()
-            e1.record()
-    flat = [[e for pair in step_evs for e in pair] for step_evs in evs]
+            for _ in cases] for _ in range(args.steps)] if args.route == "host" else None
+    for e in ready + [e for pr in phase for e in pr]:   # create them before the library uses them
+        e.record()
     paths = [None] * len(cases)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
         if args.route == "device":
-            abi.sparoa_fc_ops_run(op_array, s_thr, INTENSITY_THR, events=flat[s])
+            abi.sparoa_fc_ops_run2(op_array, s_thr, INTENSITY_THR, ready=ready,
+                                   timing=list(phase[s]), measure_stream=side, exec_stream=main)
         else:
+            phase[s][0].record()
             for i, c in enumerate(cases):
                 paths[i] = step_fn(abi, c, s_thr, evs[s][i])
+            phase[s][1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     if args.route == "device":
@@ -292,10 +314,16 @@ def main():
     flops_step = sum(2 * c.m * K * N for c in cases)
     value = flops_step / step_s / 1e12
 
-    # live kernel durations of the routed FC launches (HIP events on the
-    # stream the library launches on)
-    kern_us = [sum(evs[s][i][0].elapsed_time(evs[s][i][1]) for s in range(args.steps)) * 1e3 /
-               args.steps for i in range(len(cases))]
+    # live duration of the FC phase: 24 routed FC launches back to back on the
+    # stream the library launches on, bracketed by HIP events, every step
+    phase_us = sum(a.elapsed_time(b) for a, b in phase) * 1e3 / args.steps
+    if args.route == "host":
+        for i, c in enumerate(cases):
+            c.routed_us = sum(evs[s][i][0].elapsed_time(evs[s][i][1])
+                              for s in range(args.steps)) * 1e3 / args.steps
+    else:
+        for i, c in enumerate(cases):   # per-operator view: same routed call, warm, back to back
+            c.routed_us = routed_time(abi, torch, c, s_thr)
     table = []
     tot_bytes = 0
     for i, c in enumerate(cases):
@@ -304,18 +332,21 @@ def main():
         tot_bytes += b
         table.append(dict(
             m=c.m, rho=c.rho, pattern=c.pattern, rho_e=round(c.rho_e, 4),
-            rho_b=round(c.rho_b, 4), path=abi.PATH_NAMES[paths[i]], us=round(kern_us[i], 2),
-            alg_bytes=b, gbps=round(b / kern_us[i] / 1e3, 1),
-            dense_equiv_tflops=round(2 * c.m * K * N / kern_us[i] / 1e6, 2),
+            rho_b=round(c.rho_b, 4), path=abi.PATH_NAMES[paths[i]], alg_bytes=b,
+            us=round(c.routed_us, 2), gbps=round(b / c.routed_us / 1e3, 1),
+            dense_equiv_tflops=round(2 * c.m * K * N / c.routed_us / 1e6, 2),
             dense_bw_us=round(c.forced[abi.PATH_DENSE_BW], 2),
-            skip_bw_us=round(c.forced[abi.PATH_SKIP_BW], 2)))
+            skip_bw_us=round(c.forced[abi.PATH_SKIP_BW], 2),
+            dense_mfma_us=round(c.forced[abi.PATH_DENSE_MFMA], 2)))
     launches = len(cases)
-    achieved = tot_bytes / launches / (sum(kern_us) / launches * 1e-6) / 1e9
+    achieved = tot_bytes / (phase_us * 1e-6) / 1e9
     digest = source_digest()
     traffic = load_traffic(digest)
     roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
                     kernel="fc_bw_kernel", alg_bytes_per_launch=int(tot_bytes / launches),
+                    avg_launch_us=round(phase_us / launches, 3),
+                    timing="HIP events around each step's FC phase (24 launches), timed steps",
                     source_digest=digest)
     measure_bytes = sum(2 * c.m * K for c in cases)
 

@@ -321,6 +321,18 @@ typedef struct {
 } sparoa_fc_op;
 sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr,
                                 hipEvent_t *events, hipStream_t stream);
+/* The same path on two streams: op i's measurement is issued on
+ * measure_stream and recorded in ready[i] (n events, required); op i's
+ * device-routed FC is issued on exec_stream after a wait on ready[i].  Issue
+ * interleaves (measure i+1 is issued right after FC i), so the measurement
+ * of the next op (a short, latency-bound pass) runs while the current FC
+ * streams its weights.  measure_stream first waits for exec_stream's earlier
+ * work, so buffers of a previous batch are not overwritten early.
+ * timing (2 events, nullable): recorded on exec_stream right before the first
+ * FC kernel and right after the last one. */
+sparoa_status sparoa_fc_ops_run2(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr,
+                                 hipEvent_t *ready, hipEvent_t *timing,
+                                 hipStream_t measure_stream, hipStream_t exec_stream);
 
 /* ------------------------------------------------------------------------
  * Network glue (not routed): NHWC max pooling, window k, stride s, padding p.

@@ -513,30 +513,69 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *d, const sparoa_thresholds 
 
 // ---------------------------------------------------------------- executor
 
+namespace {
+sparoa_status measure_op(const sparoa_fc_op &o, const sparoa_thresholds *thr,
+                         hipStream_t stream) {
+  sparoa_intensity in;
+  sparoa_status st = sparoa_op_intensity_fc(&o.desc, &in);
+  if (st != SPAROA_OK) return st;
+  const sparoa_path fam =
+      in.intensity < thr->intensity_thr ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
+  int64_t br, bc;
+  if ((st = sparoa_fc_skip_block(&o.desc, fam, &br, &bc)) != SPAROA_OK) return st;
+  return sparoa_measure_sparsity(o.x, o.desc.dtype, o.desc.m, o.desc.k, br, bc, 0, o.counts,
+                                 o.mask, nullptr, stream);
+}
+
+sparoa_status execute_op(const sparoa_fc_op &o, const sparoa_thresholds *thr,
+                         hipStream_t stream) {
+  return sparoa_fc_routed(&o.desc, thr, o.counts, o.x, o.w_nk, o.w_packed, o.bias, o.residual,
+                          o.act, o.mask, o.y, o.workspace, o.ws_bytes, o.path, stream);
+}
+
+sparoa_status check_ops(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr) {
+  if (!ops || n < 0) return fail(SPAROA_ERR_INVALID_ARG, "fc_ops: null ops or n < 0");
+  return check_thr(thr);
+}
+}  // namespace
+
 sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr,
                                 hipEvent_t *events, hipStream_t stream) {
   g_last_error.clear();
-  if (!ops || n < 0) return fail(SPAROA_ERR_INVALID_ARG, "fc_ops_run: null ops or n < 0");
-  sparoa_status st = check_thr(thr);
+  sparoa_status st = check_ops(ops, n, thr);
   if (st != SPAROA_OK) return st;
   for (int64_t i = 0; i < n; ++i) {
-    const sparoa_fc_op &o = ops[i];
-    sparoa_intensity in;
-    if ((st = sparoa_op_intensity_fc(&o.desc, &in)) != SPAROA_OK) return st;
-    const sparoa_path fam =
-        in.intensity < thr->intensity_thr ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
-    int64_t br, bc;
-    if ((st = sparoa_fc_skip_block(&o.desc, fam, &br, &bc)) != SPAROA_OK) return st;
-    if ((st = sparoa_measure_sparsity(o.x, o.desc.dtype, o.desc.m, o.desc.k, br, bc, 0, o.counts,
-                                      o.mask, nullptr, stream)) != SPAROA_OK)
-      return st;
+    if ((st = measure_op(ops[i], thr, stream)) != SPAROA_OK) return st;
     if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i], stream));
-    if ((st = sparoa_fc_routed(&o.desc, thr, o.counts, o.x, o.w_nk, o.w_packed, o.bias,
-                               o.residual, o.act, o.mask, o.y, o.workspace, o.ws_bytes, o.path,
-                               stream)) != SPAROA_OK)
-      return st;
+    if ((st = execute_op(ops[i], thr, stream)) != SPAROA_OK) return st;
     if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i + 1], stream));
   }
+  return SPAROA_OK;
+}
+
+sparoa_status sparoa_fc_ops_run2(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr,
+                                 hipEvent_t *ready, hipEvent_t *timing,
+                                 hipStream_t measure_stream, hipStream_t exec_stream) {
+  g_last_error.clear();
+  sparoa_status st = check_ops(ops, n, thr);
+  if (st != SPAROA_OK) return st;
+  if (!ready && n > 0) return fail(SPAROA_ERR_INVALID_ARG, "fc_ops_run2: null ready events");
+  if (n == 0) return SPAROA_OK;
+  // measure_stream must not overwrite counts/masks an earlier FC still reads
+  SPAROA_HIP_CHECK(hipEventRecord(ready[0], exec_stream));
+  SPAROA_HIP_CHECK(hipStreamWaitEvent(measure_stream, ready[0], 0));
+  if ((st = measure_op(ops[0], thr, measure_stream)) != SPAROA_OK) return st;
+  SPAROA_HIP_CHECK(hipEventRecord(ready[0], measure_stream));
+  for (int64_t i = 0; i < n; ++i) {
+    SPAROA_HIP_CHECK(hipStreamWaitEvent(exec_stream, ready[i], 0));
+    if (timing && i == 0) SPAROA_HIP_CHECK(hipEventRecord(timing[0], exec_stream));
+    if ((st = execute_op(ops[i], thr, exec_stream)) != SPAROA_OK) return st;
+    if (i + 1 < n) {
+      if ((st = measure_op(ops[i + 1], thr, measure_stream)) != SPAROA_OK) return st;
+      SPAROA_HIP_CHECK(hipEventRecord(ready[i + 1], measure_stream));
+    }
+  }
+  if (timing) SPAROA_HIP_CHECK(hipEventRecord(timing[1], exec_stream));
   return SPAROA_OK;
 }
 

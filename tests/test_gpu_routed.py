@@ -157,3 +157,47 @@ def test_fc_ops_run_equals_per_op_routed_calls():
         assert int(p2.item()) == int(b["path"].item())
         assert torch.equal(y2, b["y"])
         assert evs[2 * i].elapsed_time(evs[2 * i + 1]) > 0
+
+
+def test_fc_ops_two_streams_equal_interleaved_run():
+    """Measurement on a side stream overlapping execution on the main stream
+    gives the same paths and outputs as the one-stream executor."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    ops, bufs = [], []
+    for i, (m, rho, pat) in enumerate([(1, 0.95, "iid"), (8, 0.9, "block"), (64, 0.9, "block"),
+                                       (8, 0.0, "iid")]):
+        k, n = 2048, 512
+        d = abi.fc_desc(m, k, n, abi.BF16)
+        b = dict(x=synth.sparse_matrix(m, k, rho, pat, "bf16", 500 + i).to(dev),
+                 w=synth.normal((n, k), "bf16", 600 + i, std=k ** -0.5).to(dev),
+                 wp=torch.empty(abi.sparoa_fc_packed_bytes(d) // 2, dtype=torch.bfloat16,
+                                device=dev),
+                 counts=torch.zeros(4, dtype=torch.int64, device=dev),
+                 mask=torch.zeros(abi.sparoa_mask_words(m, k, m, 1), dtype=torch.int32, device=dev),
+                 y=torch.zeros(m, n, dtype=torch.bfloat16, device=dev),
+                 path=torch.zeros(1, dtype=torch.int32, device=dev))
+        abi.sparoa_fc_pack_weights(d, b["w"], b["wp"])
+        bufs.append(b)          # keeps every buffer alive while the op structs point at it
+        ops.append(abi.fc_op(d, b["x"], b["w"], b["wp"], None, None, abi.ACT_NONE, b["counts"],
+                             b["mask"], b["y"], None, b["path"]))
+    arr = abi.fc_op_array(ops)
+    abi.sparoa_fc_ops_run(arr, 0.5, 315.0)
+    torch.cuda.synchronize()
+    ref = [(b["y"].clone(), int(b["path"].item())) for b in bufs]
+    for b in bufs:
+        b["y"].zero_()
+        b["path"].fill_(-1)
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    ready = [torch.cuda.Event() for _ in ops]
+    timing = [torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+    for e in ready + timing:
+        e.record()
+    for _ in range(3):
+        abi.sparoa_fc_ops_run2(arr, 0.5, 315.0, ready=ready, timing=timing, measure_stream=side,
+                               exec_stream=main)
+    torch.cuda.synchronize()
+    for b, (y, p) in zip(bufs, ref):
+        assert torch.equal(b["y"], y) and int(b["path"].item()) == p
+    assert timing[0].elapsed_time(timing[1]) > 0
