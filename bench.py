@@ -7,10 +7,13 @@ bf16 ~ N(0, 1/4096), m in {1, 8, 64}, activation sparsity rho in
 |N(0, 1)|.  Every operator has its own weight matrix (24 x 32 MiB, more than
 the 256 MB Infinity Cache holds), so weights stream from HBM.  Per operator
 the step runs the whole path: intensity from the shape (host), sparsity
-measurement (GPU), routing, and the routed FC kernel.  Routing runs inside
-the FC kernel from the counts in device memory, the 24 operators issued by
-one native call (default), or on the host after reading the counts back,
-one Python call per kernel (--route host).  Inputs are resident in HBM before timing starts.
+measurement (GPU), routing, and the routed FC kernel.  Default (--mode graph):
+the 24 operators are issued by one native executor call (sparoa_fc_ops_run),
+captured once in a HIP graph; each FC kernel measures its own input and takes
+the route decision itself, so a step is one graph launch of 24 kernels.
+--mode eager issues the same executor call every step; --mode host reads the
+counts back and routes on the host, one Python call per kernel.  Inputs are
+resident in HBM before timing starts.
 
 value = dense-equivalent TFLOP/s of the step: sum over operators of
 2 m k n divided by the step time (skipped work counts as done).
@@ -47,10 +50,13 @@ def parse():
     p.add_argument("--sparsity-thr", type=float, default=None,
                    help="routing threshold; default: calibrated from forced-path timings")
     p.add_argument("--cases-out", default=None, help="write the per-case table (JSON) here")
-    p.add_argument("--route", choices=("device", "host"), default="device",
-                   help="device: the kernel takes the skip decision from the counts in device "
-                        "memory (no host round trip); host: counts read back, sparoa_route on "
-                        "the host, then the fixed-path call")
+    p.add_argument("--no-sweep", action="store_true",
+                   help="skip the forced-path and per-operator timings (needs --sparsity-thr): "
+                        "only the step kernels run, e.g. under a profiler")
+    p.add_argument("--mode", choices=("graph", "eager", "host"), default="graph",
+                   help="graph: the executor call captured in a HIP graph, one replay per step; "
+                        "eager: the executor call every step; host: counts read back, "
+                        "sparoa_route on the host, then the fixed-path call")
     return p.parse_args()
 
 
@@ -119,19 +125,6 @@ def build_cases(abi, torch, synth, dev):
     return cases
 
 
-def run_case_device(abi, c, s_thr, ev=None):
-    """One operator through the whole path with device-side routing: no host
-    synchronisation; the path taken is left in c.path_dev."""
-    abi.sparoa_measure_sparsity(c.x, c.m, K, c.br, c.bc, 0, c.counts, c.mask)
-    if ev is not None:
-        ev[0].record()
-    abi.sparoa_fc_routed(c.desc, s_thr, INTENSITY_THR, abi.ROUTE_BLOCK, c.counts, c.x, c.w, c.wp,
-                         None, None, abi.ACT_NONE, c.mask, c.y, c.ws, c.path_dev)
-    if ev is not None:
-        ev[1].record()
-    return None
-
-
 def run_case(abi, c, s_thr, ev=None):
     """One operator through the whole path; returns the routed path."""
     counts = abi.sparoa_measure_sparsity_sync(c.x, c.m, K, c.br, c.bc, 0, c.counts, c.mask)
@@ -173,15 +166,16 @@ def forced_times(abi, torch, c, paths, reps=20, rounds=3):
     return out
 
 
-def routed_time(abi, torch, c, s_thr, reps=20):
-    """Duration (us) of the device-routed FC call of one operator, `reps`
-    launches back to back between one pair of HIP events."""
+def path_time(abi, torch, c, s_thr, reps=20):
+    """Duration (us) of one operator's whole path (sparoa_fc_measured:
+    measure, route and FC), `reps` calls back to back between one pair of
+    HIP events."""
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(reps):
-        abi.sparoa_fc_routed(c.desc, s_thr, INTENSITY_THR, abi.ROUTE_BLOCK, c.counts, c.x, c.w,
-                             c.wp, None, None, abi.ACT_NONE, c.mask, c.y, c.ws, c.path_dev)
+        abi.sparoa_fc_measured(c.desc, s_thr, INTENSITY_THR, abi.ROUTE_BLOCK, c.x, c.w, c.wp,
+                               None, None, abi.ACT_NONE, c.counts, c.mask, c.y, c.ws, c.path_dev)
     e1.record()
     e1.synchronize()
     return e0.elapsed_time(e1) * 1e3 / reps
@@ -239,17 +233,21 @@ def main():
 
     # Forced-path timings per case (untimed phase): the sparsity sweep of the
     # metric, and the data the routing threshold is calibrated from.
-    print("bench: forced-path sweep", file=sys.stderr, flush=True)
+    if args.no_sweep and args.sparsity_thr is None:
+        print("bench.py: --no-sweep needs --sparsity-thr", file=sys.stderr)
+        sys.exit(2)
+    if not args.no_sweep:
+        print("bench: forced-path sweep", file=sys.stderr, flush=True)
     for c in cases:
-        c.forced = forced_times(abi, torch, c, (abi.PATH_DENSE_BW, abi.PATH_SKIP_BW,
-                                                abi.PATH_DENSE_MFMA))
-        st = c.counts.cpu().tolist()
-        c.rho_e = st[0] / st[1]
-        c.rho_b = st[2] / st[3]
+        c.forced = {} if args.no_sweep else forced_times(
+            abi, torch, c, (abi.PATH_DENSE_BW, abi.PATH_SKIP_BW, abi.PATH_DENSE_MFMA))
     if args.sparsity_thr is None:
         # smallest block sparsity above which the skip path wins in every case
-        pts = sorted((c.rho_b, c.forced[abi.PATH_SKIP_BW] < c.forced[abi.PATH_DENSE_BW])
-                     for c in cases)
+        pts = []
+        for c in cases:     # forced_times left the counts at the skip block in c.counts
+            st = c.counts.cpu().tolist()
+            pts.append((st[2] / st[3], c.forced[abi.PATH_SKIP_BW] < c.forced[abi.PATH_DENSE_BW]))
+        pts.sort()
         s_thr = 1.0
         for rb, wins in reversed(pts):
             if not wins:
@@ -261,94 +259,101 @@ def main():
 
     print(f"bench: warmup {args.warmup} steps, sparsity threshold {s_thr:.4g}", file=sys.stderr,
           flush=True)
-    step_fn = run_case_device if args.route == "device" else run_case
-    # device routing: the whole step is one native call (sparoa_fc_ops_run)
+    # the executor's batch: one sparoa_fc_measured per operator
     op_array = abi.fc_op_array([
         abi.fc_op(c.desc, c.x, c.w, c.wp, None, None, abi.ACT_NONE, c.counts, c.mask, c.y, c.ws,
                   c.path_dev) for c in cases])
-    for _ in range(args.warmup):
-        if args.route == "device":
-            abi.sparoa_fc_ops_run(op_array, s_thr, INTENSITY_THR)
+
+    def executor_step():
+        abi.sparoa_fc_ops_run(op_array, s_thr, INTENSITY_THR)
+
+    # eager reference outputs: the graph replays must reproduce them
+    executor_step()
+    torch.cuda.synchronize()
+    y_ref = [c.y.clone() for c in cases]
+    graph = None
+    if args.mode == "graph":
+        cap = torch.cuda.Stream()                   # default priority
+        cap.wait_stream(torch.cuda.current_stream())
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(cap):
+            with torch.cuda.graph(graph):
+                executor_step()
+        torch.cuda.synchronize()
+
+    def step():
+        if args.mode == "graph":
+            graph.replay()
+        elif args.mode == "eager":
+            executor_step()
         else:
             for c in cases:
-                step_fn(abi, c, s_thr)
+                run_case(abi, c, s_thr)
+
+    for _ in range(args.warmup):
+        step()
     torch.cuda.synchronize()
 
-    # device routing: operator i+1's measurement on a side stream overlaps
-    # operator i's routed FC on the main stream (one event per operator);
-    # one pair of timing events brackets each step's FC phase
-    main = torch.cuda.current_stream()
-    side = torch.cuda.Stream()                      # default priority
-    ready = [torch.cuda.Event() for _ in cases]
-    phase = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-             for _ in range(args.steps)]
-    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-            for _ in cases] for _ in range(args.steps)] if args.route == "host" else None
-    for e in ready + [e for pr in phase for e in pr]:   # create them before the library uses them
-        e.record()
-    paths = [None] * len(cases)
+    # one pair of HIP events brackets every step on the stream it runs on
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
-        if args.route == "device":
-            abi.sparoa_fc_ops_run2(op_array, s_thr, INTENSITY_THR, ready=ready,
-                                   timing=list(phase[s]), measure_stream=side, exec_stream=main)
-        else:
-            phase[s][0].record()
-            for i, c in enumerate(cases):
-                paths[i] = step_fn(abi, c, s_thr, evs[s][i])
-            phase[s][1].record()
+        ev[s][0].record()
+        step()
+        ev[s][1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    if args.route == "device":
-        for i, c in enumerate(cases):
-            paths[i] = int(c.path_dev.item())
-            c.counts_host = dict(zip(("zeros", "numel", "zero_blocks", "num_blocks"),
-                                     c.counts.cpu().tolist()))
-            # the device decision must be the host rule's on the same counts
-            assert paths[i] == abi.sparoa_route(c.counts_host, c.inten, 0, s_thr, INTENSITY_THR)
+    paths = [int(c.path_dev.item()) for c in cases] if args.mode != "host" else \
+        [run_case(abi, c, s_thr) for c in cases]
+    torch.cuda.synchronize()
+    for i, c in enumerate(cases):
+        c.counts_host = dict(zip(("zeros", "numel", "zero_blocks", "num_blocks"),
+                                 c.counts.cpu().tolist()))
+        # the device decision must be the host rule's on the same counts
+        assert paths[i] == abi.sparoa_route(c.counts_host, c.inten, 0, s_thr, INTENSITY_THR)
+        assert torch.equal(c.y, y_ref[i]), f"operator {i}: step output differs from eager run"
     step_s = (t1 - t0) / args.steps
     print(f"bench: timed {args.steps} steps, {step_s * 1e3:.3f} ms/step", file=sys.stderr,
           flush=True)
 
     flops_step = sum(2 * c.m * K * N for c in cases)
     value = flops_step / step_s / 1e12
-
-    # live duration of the FC phase: 24 routed FC launches back to back on the
-    # stream the library launches on, bracketed by HIP events, every step
-    phase_us = sum(a.elapsed_time(b) for a, b in phase) * 1e3 / args.steps
-    if args.route == "host":
-        for i, c in enumerate(cases):
-            c.routed_us = sum(evs[s][i][0].elapsed_time(evs[s][i][1])
-                              for s in range(args.steps)) * 1e3 / args.steps
-    else:
-        for i, c in enumerate(cases):   # per-operator view: same routed call, warm, back to back
-            c.routed_us = routed_time(abi, torch, c, s_thr)
+    # GPU time of a step from its events: 24 kernel launches back to back
+    step_gpu_us = sum(a.elapsed_time(b) for a, b in ev) * 1e3 / args.steps
+    for c in cases:   # per-operator view: the whole path of one operator, back to back
+        c.path_us = None if args.no_sweep else path_time(abi, torch, c, s_thr)
     table = []
     tot_bytes = 0
     for i, c in enumerate(cases):
-        nz_cols = c.counts_host["num_blocks"] - c.counts_host["zero_blocks"]
+        ch = c.counts_host
+        nz_cols = ch["num_blocks"] - ch["zero_blocks"]
         b = alg_bytes(c, paths[i], nz_cols)
         tot_bytes += b
-        table.append(dict(
-            m=c.m, rho=c.rho, pattern=c.pattern, rho_e=round(c.rho_e, 4),
-            rho_b=round(c.rho_b, 4), path=abi.PATH_NAMES[paths[i]], alg_bytes=b,
-            us=round(c.routed_us, 2), gbps=round(b / c.routed_us / 1e3, 1),
-            dense_equiv_tflops=round(2 * c.m * K * N / c.routed_us / 1e6, 2),
-            dense_bw_us=round(c.forced[abi.PATH_DENSE_BW], 2),
-            skip_bw_us=round(c.forced[abi.PATH_SKIP_BW], 2),
-            dense_mfma_us=round(c.forced[abi.PATH_DENSE_MFMA], 2)))
+        row = dict(m=c.m, rho=c.rho, pattern=c.pattern, rho_e=round(ch["zeros"] / ch["numel"], 4),
+                   rho_b=round(ch["zero_blocks"] / ch["num_blocks"], 4),
+                   path=abi.PATH_NAMES[paths[i]], alg_bytes=b)
+        if c.path_us is not None:
+            row.update(us=round(c.path_us, 2), gbps=round(b / c.path_us / 1e3, 1),
+                       dense_equiv_tflops=round(2 * c.m * K * N / c.path_us / 1e6, 2))
+        for p, name in ((abi.PATH_DENSE_BW, "dense_bw_us"), (abi.PATH_SKIP_BW, "skip_bw_us"),
+                        (abi.PATH_DENSE_MFMA, "dense_mfma_us")):
+            if p in c.forced:
+                row[name] = round(c.forced[p], 2)
+        table.append(row)
     launches = len(cases)
-    achieved = tot_bytes / (phase_us * 1e-6) / 1e9
+    achieved = tot_bytes / (step_gpu_us * 1e-6) / 1e9
     digest = source_digest()
     traffic = load_traffic(digest)
     roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
-                    kernel="fc_bw_kernel", alg_bytes_per_launch=int(tot_bytes / launches),
-                    avg_launch_us=round(phase_us / launches, 3),
-                    timing="HIP events around each step's FC phase (24 launches), timed steps",
+                    kernel="fc_bw_kernel (self-measuring)",
+                    alg_bytes_per_launch=int(tot_bytes / launches),
+                    avg_launch_us=round(step_gpu_us / launches, 3),
+                    timing="HIP events around every timed step (24 launches, gaps between "
+                           "launches included)",
                     source_digest=digest)
-    measure_bytes = sum(2 * c.m * K for c in cases)
 
     line = dict(
         metric=METRIC, value=round(value, 3), unit="TFLOP/s", n_gpus=1, steps=args.steps,
@@ -359,8 +364,9 @@ def main():
                              "one weight matrix per operator; measure+route+execute each",
                     global_batch=sum(M_LIST) * len(RHO_LIST) * len(PATTERNS),
                     sparsity_thr=s_thr, intensity_thr=INTENSITY_THR, route_mode="block",
-                    routing=args.route),
-        hbm_gbps_step=round((tot_bytes + measure_bytes) / step_s / 1e9, 1),
+                    issue=args.mode),
+        hbm_gbps_step=round(tot_bytes / step_s / 1e9, 1),
+        step_gpu_us=round(step_gpu_us, 2),
         roofline=roofline,
         sweep=table,
     )

@@ -297,15 +297,38 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
                                size_t ws_bytes, uint32_t *path_dev, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * The whole path of one FC operator -- measure, route, execute (SparOA
+ * Section 3.1 sparsity feature, Eq. 1; Section 2.2 quadrant routing) -- in
+ * one call and no host round trip.
+ *   x is measured at the skip granularity of the family that the FC's
+ *   intensity (Eq. 2) selects: counts_dev and mask_dev receive exactly what
+ *   sparoa_measure_sparsity gives at sparoa_fc_skip_block(desc, family|skip)
+ *   (mask_dev: sparoa_mask_words(...) words, caller-owned); the device-routed
+ *   FC then runs as in sparoa_fc_routed.  When the weight-streaming kernel
+ *   serves the FC and k % 8 == 0, the FC kernel measures its own input and
+ *   the call is one kernel launch; otherwise it is the measurement kernel
+ *   followed by the routed kernel on the same stream.
+ *   Other arguments as for sparoa_fc_routed.
+ * Errors: those of sparoa_measure_sparsity and sparoa_fc_routed.
+ * ---------------------------------------------------------------------- */
+sparoa_status sparoa_fc_measured(const sparoa_fc_desc *desc, const sparoa_thresholds *thr,
+                                 const void *x, const void *w_nk, const void *w_packed,
+                                 const void *bias, const void *residual, sparoa_act act,
+                                 sparoa_counts *counts_dev, uint32_t *mask_dev, void *y,
+                                 void *workspace, size_t ws_bytes, uint32_t *path_dev,
+                                 hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Native executor of independent FC operators: for each op in order,
- * measure x at the skip granularity of the family its intensity selects,
- * then run the device-routed FC -- the whole measure -> route -> execute path
- * with one host call per batch (host launch cost instead of one Python call
- * per kernel).  Per op: counts (one sparoa_counts) and mask (sparoa_mask_words
- * words for that granularity) are device scratch; path (nullable) receives
- * the path taken; w_nk / w_packed as for sparoa_fc_routed.
+ * sparoa_fc_measured -- the whole measure -> route -> execute path with one
+ * host call per batch (host launch cost instead of one Python call per
+ * kernel).  Issues no memset, copy or synchronisation, and no event unless
+ * events are given, so a caller may capture it in a HIP graph.  Per op:
+ * counts (one sparoa_counts) and mask (sparoa_mask_words words for that
+ * granularity) are device scratch; path (nullable) receives the path taken;
+ * w_nk / w_packed as for sparoa_fc_routed.
  * events (nullable): 2n hipEvent_t; events[2i] / events[2i+1] are recorded
- * on `stream` right before / after op i's FC kernel.
+ * on `stream` right before op i's first kernel / after its last kernel.
  * Stops at the first failing op and returns its status.
  * ---------------------------------------------------------------------- */
 typedef struct {
@@ -321,18 +344,7 @@ typedef struct {
 } sparoa_fc_op;
 sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr,
                                 hipEvent_t *events, hipStream_t stream);
-/* The same path on two streams: op i's measurement is issued on
- * measure_stream and recorded in ready[i] (n events, required); op i's
- * device-routed FC is issued on exec_stream after a wait on ready[i].  Issue
- * interleaves (measure i+1 is issued right after FC i), so the measurement
- * of the next op (a short, latency-bound pass) runs while the current FC
- * streams its weights.  measure_stream first waits for exec_stream's earlier
- * work, so buffers of a previous batch are not overwritten early.
- * timing (2 events, nullable): recorded on exec_stream right before the first
- * FC kernel and right after the last one. */
-sparoa_status sparoa_fc_ops_run2(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr,
-                                 hipEvent_t *ready, hipEvent_t *timing,
-                                 hipStream_t measure_stream, hipStream_t exec_stream);
+
 
 /* ------------------------------------------------------------------------
  * Network glue (not routed): NHWC max pooling, window k, stride s, padding p.

@@ -30,7 +30,8 @@ EXPORTS = [
     "sparoa_conv2d_zero_skip", "sparoa_fc_packed_bytes", "sparoa_fc_pack_weights",
     "sparoa_fc_tiling", "sparoa_fc_workspace_size", "sparoa_fc_skip_block", "sparoa_fc",
     "sparoa_fc_dense", "sparoa_fc_zero_skip", "sparoa_maxpool2d", "sparoa_conv2d_routed",
-    "sparoa_fc_routed", "sparoa_fc_uses_packed", "sparoa_fc_ops_run", "sparoa_fc_ops_run2",
+    "sparoa_fc_routed", "sparoa_fc_uses_packed", "sparoa_fc_ops_run",
+    "sparoa_fc_measured",
 ]
 
 
@@ -118,7 +119,8 @@ def _load():
         "sparoa_fc_skip_block": (ctypes.c_int, [P(FcDesc), ctypes.c_int, P(i64), P(i64)]),
         "sparoa_fc_uses_packed": (ctypes.c_int, [P(FcDesc), ctypes.c_int, P(ctypes.c_int)]),
         "sparoa_fc_ops_run": (ctypes.c_int, [P(FcOp), i64, P(Thresholds), P(vp), vp]),
-        "sparoa_fc_ops_run2": (ctypes.c_int, [P(FcOp), i64, P(Thresholds), P(vp), P(vp), vp, vp]),
+        "sparoa_fc_measured": (ctypes.c_int, [P(FcDesc), P(Thresholds), vp, vp, vp, vp, vp,
+                                              ctypes.c_int, vp, vp, vp, vp, sz, vp, vp]),
         "sparoa_fc": (ctypes.c_int, [P(FcDesc), ctypes.c_int, vp, vp, vp, vp, ctypes.c_int, vp,
                                      vp, vp, sz, vp, vp]),
         "sparoa_fc_dense": (ctypes.c_int, [P(FcDesc), vp, vp, vp, vp, ctypes.c_int, vp, vp, sz,
@@ -362,6 +364,17 @@ def sparoa_fc_routed(desc, sparsity_thr, intensity_thr, mode, counts, x, w_nk, w
                                _stream(stream)))
 
 
+def sparoa_fc_measured(desc, sparsity_thr, intensity_thr, mode, x, w_nk, w_packed, bias, residual,
+                       act, counts, mask, y, workspace=None, path=None, stream=None):
+    """Measure -> route -> execute of one FC (see sparoa.h)."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    t = Thresholds(sparsity_thr, intensity_thr, mode)
+    _check(_L.sparoa_fc_measured(ctypes.byref(desc), ctypes.byref(t), _ptr(x), _ptr(w_nk),
+                                 _ptr(w_packed), _ptr(bias), _ptr(residual), act, _ptr(counts),
+                                 _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes, _ptr(path),
+                                 _stream(stream)))
+
+
 def sparoa_fc_uses_packed(desc, path):
     v = ctypes.c_int()
     _check(_L.sparoa_fc_uses_packed(ctypes.byref(desc), path, ctypes.byref(v)))
@@ -389,15 +402,3 @@ def sparoa_fc_ops_run(op_array, sparsity_thr, intensity_thr, mode=ROUTE_BLOCK, e
     if events is not None:
         ev = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
     _check(_L.sparoa_fc_ops_run(op_array, len(op_array), ctypes.byref(t), ev, _stream(stream)))
-
-
-def _events(evs):
-    return None if evs is None else (ctypes.c_void_p * len(evs))(*[e.cuda_event for e in evs])
-
-
-def sparoa_fc_ops_run2(op_array, sparsity_thr, intensity_thr, mode=ROUTE_BLOCK, ready=None,
-                       timing=None, measure_stream=None, exec_stream=None):
-    """Two-stream form of sparoa_fc_ops_run (see sparoa.h); ready: n events."""
-    t = Thresholds(sparsity_thr, intensity_thr, mode)
-    _check(_L.sparoa_fc_ops_run2(op_array, len(op_array), ctypes.byref(t), _events(ready),
-                                 _events(timing), _stream(measure_stream), _stream(exec_stream)))

@@ -511,28 +511,41 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *d, const sparoa_thresholds 
                           can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r);
 }
 
+sparoa_status sparoa_fc_measured(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
+                                 const void *x, const void *w_nk, const void *w_packed,
+                                 const void *bias, const void *residual, sparoa_act act,
+                                 sparoa_counts *counts_dev, uint32_t *mask_dev, void *y,
+                                 void *workspace, size_t ws_bytes, uint32_t *path_dev,
+                                 hipStream_t stream) {
+  g_last_error.clear();
+  sparoa_intensity in;
+  sparoa_status st = sparoa_op_intensity_fc(d, &in);
+  if (st != SPAROA_OK) return st;
+  if ((st = check_thr(thr)) != SPAROA_OK) return st;
+  const int bw = in.intensity < thr->intensity_thr ? 1 : 0;
+  if (bw && fc_bw_self_measures(*d)) {
+    if (!counts_dev || !x || !w_packed || !y || !mask_dev || !act_ok(act))
+      return fail(SPAROA_ERR_INVALID_ARG, "fc_measured: null counts/x/w_packed/mask/y or bad act");
+    if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "fc_measured: has_bias without bias");
+    if ((st = check_ptrs16({x, w_packed, bias, residual, y, mask_dev, counts_dev})) != SPAROA_OK)
+      return st;
+    const DeviceRoute r{nullptr, thr->sparsity_thr, thr->mode, bw, path_dev};
+    return launch_fc_bw_measured(*d, x, w_packed, d->has_bias ? bias : nullptr, residual, act,
+                                 counts_dev, mask_dev, y, stream, r);
+  }
+  int64_t br, bc;
+  const sparoa_path fam = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
+  if ((st = sparoa_fc_skip_block(d, fam, &br, &bc)) != SPAROA_OK) return st;
+  if ((st = sparoa_measure_sparsity(x, d->dtype, d->m, d->k, br, bc, 0, counts_dev, mask_dev,
+                                    nullptr, stream)) != SPAROA_OK)
+    return st;
+  return sparoa_fc_routed(d, thr, counts_dev, x, w_nk, w_packed, bias, residual, act, mask_dev, y,
+                          workspace, ws_bytes, path_dev, stream);
+}
+
 // ---------------------------------------------------------------- executor
 
 namespace {
-sparoa_status measure_op(const sparoa_fc_op &o, const sparoa_thresholds *thr,
-                         hipStream_t stream) {
-  sparoa_intensity in;
-  sparoa_status st = sparoa_op_intensity_fc(&o.desc, &in);
-  if (st != SPAROA_OK) return st;
-  const sparoa_path fam =
-      in.intensity < thr->intensity_thr ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
-  int64_t br, bc;
-  if ((st = sparoa_fc_skip_block(&o.desc, fam, &br, &bc)) != SPAROA_OK) return st;
-  return sparoa_measure_sparsity(o.x, o.desc.dtype, o.desc.m, o.desc.k, br, bc, 0, o.counts,
-                                 o.mask, nullptr, stream);
-}
-
-sparoa_status execute_op(const sparoa_fc_op &o, const sparoa_thresholds *thr,
-                         hipStream_t stream) {
-  return sparoa_fc_routed(&o.desc, thr, o.counts, o.x, o.w_nk, o.w_packed, o.bias, o.residual,
-                          o.act, o.mask, o.y, o.workspace, o.ws_bytes, o.path, stream);
-}
-
 sparoa_status check_ops(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr) {
   if (!ops || n < 0) return fail(SPAROA_ERR_INVALID_ARG, "fc_ops: null ops or n < 0");
   return check_thr(thr);
@@ -545,37 +558,14 @@ sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa
   sparoa_status st = check_ops(ops, n, thr);
   if (st != SPAROA_OK) return st;
   for (int64_t i = 0; i < n; ++i) {
-    if ((st = measure_op(ops[i], thr, stream)) != SPAROA_OK) return st;
+    const sparoa_fc_op &o = ops[i];
     if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i], stream));
-    if ((st = execute_op(ops[i], thr, stream)) != SPAROA_OK) return st;
+    if ((st = sparoa_fc_measured(&o.desc, thr, o.x, o.w_nk, o.w_packed, o.bias, o.residual, o.act,
+                                 o.counts, o.mask, o.y, o.workspace, o.ws_bytes, o.path,
+                                 stream)) != SPAROA_OK)
+      return st;
     if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i + 1], stream));
   }
-  return SPAROA_OK;
-}
-
-sparoa_status sparoa_fc_ops_run2(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr,
-                                 hipEvent_t *ready, hipEvent_t *timing,
-                                 hipStream_t measure_stream, hipStream_t exec_stream) {
-  g_last_error.clear();
-  sparoa_status st = check_ops(ops, n, thr);
-  if (st != SPAROA_OK) return st;
-  if (!ready && n > 0) return fail(SPAROA_ERR_INVALID_ARG, "fc_ops_run2: null ready events");
-  if (n == 0) return SPAROA_OK;
-  // measure_stream must not overwrite counts/masks an earlier FC still reads
-  SPAROA_HIP_CHECK(hipEventRecord(ready[0], exec_stream));
-  SPAROA_HIP_CHECK(hipStreamWaitEvent(measure_stream, ready[0], 0));
-  if ((st = measure_op(ops[0], thr, measure_stream)) != SPAROA_OK) return st;
-  SPAROA_HIP_CHECK(hipEventRecord(ready[0], measure_stream));
-  for (int64_t i = 0; i < n; ++i) {
-    SPAROA_HIP_CHECK(hipStreamWaitEvent(exec_stream, ready[i], 0));
-    if (timing && i == 0) SPAROA_HIP_CHECK(hipEventRecord(timing[0], exec_stream));
-    if ((st = execute_op(ops[i], thr, exec_stream)) != SPAROA_OK) return st;
-    if (i + 1 < n) {
-      if ((st = measure_op(ops[i + 1], thr, measure_stream)) != SPAROA_OK) return st;
-      SPAROA_HIP_CHECK(hipEventRecord(ready[i + 1], measure_stream));
-    }
-  }
-  if (timing) SPAROA_HIP_CHECK(hipEventRecord(timing[1], exec_stream));
   return SPAROA_OK;
 }
 

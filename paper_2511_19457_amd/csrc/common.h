@@ -44,17 +44,19 @@ struct DeviceRoute {
 
 #ifdef __HIPCC__
 // Same arithmetic as sparoa_route: one double division, >= comparison.
-__device__ __forceinline__ bool device_route_skip(const DeviceRoute &r) {
-  const sparoa_counts c = *r.counts;
+__device__ __forceinline__ bool route_skip_counts(const sparoa_counts &c, double thr, int mode) {
   double rho;
-  if (r.mode == SPAROA_ROUTE_BLOCK) {
+  if (mode == SPAROA_ROUTE_BLOCK) {
     if (c.num_blocks == 0 || c.zero_blocks > c.num_blocks) return false;
     rho = (double)c.zero_blocks / (double)c.num_blocks;
   } else {
     if (c.numel == 0 || c.zeros > c.numel) return false;
     rho = (double)c.zeros / (double)c.numel;
   }
-  return rho >= r.sparsity_thr;
+  return rho >= thr;
+}
+__device__ __forceinline__ bool device_route_skip(const DeviceRoute &r) {
+  return route_skip_counts(*r.counts, r.sparsity_thr, r.mode);
 }
 #endif
 
@@ -108,6 +110,16 @@ sparoa_status launch_fc_bw(const sparoa_fc_desc &d, sparoa_path path, const void
                            const uint32_t *mask, void *y, void *ws, size_t ws_bytes,
                            uint64_t *executed, hipStream_t stream,
                            const DeviceRoute *route = nullptr);
+// The weight-streaming kernel can also measure its own input (zero count and
+// the column bitmap at block (m, 1)) before routing: needs k % 8 == 0.
+bool fc_bw_self_measures(const sparoa_fc_desc &d);
+// Measures x into counts/mask (what sparoa_measure_sparsity gives at block
+// (m, 1)), takes the skip decision from those counts and runs the FC, in one
+// launch.  route->counts is ignored; its thresholds, bw bit and path_out apply.
+sparoa_status launch_fc_bw_measured(const sparoa_fc_desc &d, const void *x, const void *w_packed,
+                                    const void *bias, const void *residual, sparoa_act act,
+                                    sparoa_counts *counts, uint32_t *mask, void *y,
+                                    hipStream_t stream, const DeviceRoute &route);
 
 sparoa_status launch_maxpool(const void *x, sparoa_dtype dt, int64_t n, int64_t c, int64_t h,
                              int64_t w, int64_t k, int64_t s, int64_t p, void *y,

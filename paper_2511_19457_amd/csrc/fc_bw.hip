@@ -22,6 +22,13 @@
 // v_mfma_f32_16x16x32 over all m (padded to 16) and the panel's 16 columns.
 // The waves' fp32 partials are added in wave order through LDS
 // (deterministic), then bias, residual, activation and the cast to dtype.
+//
+// Self-measuring form (measure -> route -> execute in one launch): every
+// work-group reads all of x anyway, so before streaming it counts the zeros
+// of x and builds the column bitmap in LDS (16-byte loads, a lane per group
+// of 8 columns over all rows), takes the route decision from those counts
+// with the same arithmetic as the host route, and uses the LDS bitmap for its
+// column list; work-group 0 also stores the counts, the bitmap and the path.
 #include "common.h"
 #include "dtype.h"
 
@@ -56,7 +63,11 @@ struct FcBwArgs {
   int act;
   int xvec;
   DeviceRoute route;
+  sparoa_counts *mcounts;  // self-measuring form: outputs of the measurement
+  uint32_t *mmask;
 };
+
+constexpr int kMaxColWords = kMaxWaveK * 16 / 32;  // bitmap words for the largest K
 
 // LDS of one wave: transposed weight tile [16 cols][32 entries], input tile
 // [16*MT rows][32 entries], and the wave's list of columns.
@@ -67,8 +78,9 @@ struct WaveLds {
   unsigned short list[SKIP ? kMaxWaveK : 8];
 };
 
-template <int DT, int MT, bool SKIP, bool XVEC>
+template <int DT, int MT, bool SKIP, bool XVEC, bool MEASURE = false>
 __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_kernel(FcBwArgs a) {
+  static_assert(!MEASURE || SKIP, "the self-measuring form may skip");
   constexpr int NW = Shape<MT>::waves;
   constexpr int kDepth = Shape<MT>::depth;
   constexpr int kThreads = 64 * NW;
@@ -90,8 +102,85 @@ __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_kernel(FcBwArgs a
 
   int count = ke > kb ? (int)(ke - kb) : 0;
   bool use_list = SKIP;
+  const uint32_t *colbits = a.mask;
   if constexpr (SKIP) {
-    if (a.route.counts) {
+    __shared__ uint32_t mbits[MEASURE ? kMaxColWords : 1];
+    if constexpr (MEASURE) {
+      // Thread t owns column groups t, t + kThreads, ... (8 columns = one
+      // bitmap byte; K % 8 == 0): it ORs the group's nonzero flags over all
+      // rows (kMR row loads in flight), counts zeros, and stores the byte;
+      // bytes past K up to the last whole word are stored as 0.  The waves'
+      // sums meet in LDS: one barrier.
+      constexpr int kMR = MT == 1 ? 8 : (MT == 2 ? 16 : 32);
+      __shared__ unsigned wsum[NW][2];
+      const int ng = (int)(a.K / 8);
+      const int nbytes = 4 * (int)((a.K + 31) / 32);
+      unsigned zeros = 0, ones = 0;
+      for (int g = tid; g < nbytes; g += kThreads) {
+        uint32_t nzb = 0;
+        if (g < ng) {
+          const char *px = a.x + (int64_t)g * 16;
+          for (int m0 = 0; m0 < a.M; m0 += kMR) {
+            // unconditional loads (rows past M re-read row M - 1 and are
+            // masked below), so all kMR stay in flight
+            uint4 q[kMR];
+#pragma unroll
+            for (int u = 0; u < kMR; ++u) {
+              const int64_t r = min((int64_t)(m0 + u), a.M - 1);
+              q[u] = *reinterpret_cast<const uint4 *>(px + r * a.K * 2);
+            }
+#pragma unroll
+            for (int u = 0; u < kMR; ++u) {
+              const uint32_t wv[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+              uint32_t b = 0;
+#pragma unroll
+              for (int h = 0; h < 4; ++h) {
+                b |= ((wv[h] & 0x7FFFu) != 0u ? 1u : 0u) << (2 * h);
+                b |= ((wv[h] & 0x7FFF0000u) != 0u ? 1u : 0u) << (2 * h + 1);
+              }
+              const bool valid = m0 + u < a.M;
+              zeros += valid ? 8u - (unsigned)__popc(b) : 0u;
+              nzb |= valid ? b : 0u;
+            }
+          }
+          ones += (unsigned)__popc(nzb);
+        }
+        reinterpret_cast<unsigned char *>(mbits)[g] = (unsigned char)nzb;
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        zeros += __shfl_xor(zeros, o, 64);
+        ones += __shfl_xor(ones, o, 64);
+      }
+      if (lane == 0) {
+        wsum[wave][0] = zeros;
+        wsum[wave][1] = ones;
+      }
+      __syncthreads();
+      zeros = 0;
+      ones = 0;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        zeros += wsum[w][0];
+        ones += wsum[w][1];
+      }
+      const int nwords = nbytes / 4;
+      sparoa_counts c;
+      c.zeros = zeros;
+      c.numel = (uint64_t)a.M * (uint64_t)a.K;
+      c.zero_blocks = (uint64_t)a.K - ones;
+      c.num_blocks = (uint64_t)a.K;
+      use_list = route_skip_counts(c, a.route.sparsity_thr, a.route.mode);
+      if (p == 0) {
+        for (int i = tid; i < nwords; i += kThreads) a.mmask[i] = mbits[i];
+        if (tid == 0) {
+          *a.mcounts = c;
+          if (a.route.path_out)
+            *a.route.path_out = (use_list ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+        }
+      }
+      colbits = mbits;
+    } else if (a.route.counts) {
       use_list = device_route_skip(a.route);
       if (a.route.path_out && p == 0 && tid == 0)
         *a.route.path_out = (use_list ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
@@ -104,7 +193,7 @@ __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_kernel(FcBwArgs a
     const int nw = (count + 31) / 32;
     uint32_t wv = 0;
     if (lane < nw) {
-      wv = a.mask[(kb >> 5) + lane];
+      wv = colbits[(kb >> 5) + lane];
       const int tail = count - 32 * lane;
       if (tail < 32) wv &= (1u << tail) - 1u;
     }
@@ -290,19 +379,19 @@ __global__ void fc_pack_kernel(const raw *__restrict__ w, raw *__restrict__ wp, 
   }
 }
 
-template <int DT, int MT, bool SKIP, bool XVEC>
+template <int DT, int MT, bool SKIP, bool XVEC, bool MEASURE>
 void launch_one(dim3 grid, hipStream_t st, const FcBwArgs &a) {
-  hipLaunchKernelGGL((fc_bw_kernel<DT, MT, SKIP, XVEC>), grid, dim3(64 * Shape<MT>::waves), 0, st,
-                     a);
+  hipLaunchKernelGGL((fc_bw_kernel<DT, MT, SKIP, XVEC, MEASURE>), grid,
+                     dim3(64 * Shape<MT>::waves), 0, st, a);
 }
 
-template <int DT, bool SKIP, bool XVEC>
+template <int DT, bool SKIP, bool XVEC, bool MEASURE = false>
 bool launch_mt(int mt, dim3 grid, hipStream_t st, const FcBwArgs &a) {
   switch (mt) {
-    case 1: launch_one<DT, 1, SKIP, XVEC>(grid, st, a); break;
-    case 2: launch_one<DT, 2, SKIP, XVEC>(grid, st, a); break;
-    case 3: launch_one<DT, 3, SKIP, XVEC>(grid, st, a); break;
-    case 4: launch_one<DT, 4, SKIP, XVEC>(grid, st, a); break;
+    case 1: launch_one<DT, 1, SKIP, XVEC, MEASURE>(grid, st, a); break;
+    case 2: launch_one<DT, 2, SKIP, XVEC, MEASURE>(grid, st, a); break;
+    case 3: launch_one<DT, 3, SKIP, XVEC, MEASURE>(grid, st, a); break;
+    case 4: launch_one<DT, 4, SKIP, XVEC, MEASURE>(grid, st, a); break;
     default: return false;
   }
   return true;
@@ -365,6 +454,8 @@ sparoa_status launch_fc_bw(const sparoa_fc_desc &d, sparoa_path, const void *x,
   a.M = d.m; a.K = d.k; a.N = d.n; a.slice = slice_for(d);
   a.act = act;
   a.route = route ? *route : DeviceRoute{nullptr, 0.0, 0, 0, nullptr};
+  a.mcounts = nullptr;
+  a.mmask = nullptr;
   if (a.executed) {
     sparoa_status st = launch_set_u64(executed, 0, stream);
     if (st != SPAROA_OK) return st;
@@ -378,6 +469,39 @@ sparoa_status launch_fc_bw(const sparoa_fc_desc &d, sparoa_path, const void *x,
                                          : launch_dt<SPAROA_F16>(mt, skip, xvec, grid, stream, a);
   if (!ok) return fail(SPAROA_ERR_UNSUPPORTED, "fc bandwidth path: m");
   SPAROA_LAUNCH_CHECK("fc_bw_kernel");
+  return SPAROA_OK;
+}
+
+bool fc_bw_self_measures(const sparoa_fc_desc &d) { return fc_bw_streams(d) && d.k % 8 == 0; }
+
+sparoa_status launch_fc_bw_measured(const sparoa_fc_desc &d, const void *x, const void *w_packed,
+                                    const void *bias, const void *residual, sparoa_act act,
+                                    sparoa_counts *counts, uint32_t *mask, void *y,
+                                    hipStream_t stream, const DeviceRoute &route) {
+  if (!fc_bw_self_measures(d))
+    return fail(SPAROA_ERR_UNSUPPORTED, "self-measuring FC: needs the streaming kernel and k % 8 == 0");
+  FcBwArgs a;
+  a.x = static_cast<const char *>(x);
+  a.wp = static_cast<const char *>(w_packed);
+  a.bias = static_cast<const char *>(bias);
+  a.residual = static_cast<const char *>(residual);
+  a.y = static_cast<char *>(y);
+  a.mask = nullptr;
+  a.executed = nullptr;
+  a.M = d.m; a.K = d.k; a.N = d.n; a.slice = slice_for(d);
+  a.act = act;
+  a.xvec = 1;
+  a.route = route;
+  a.route.counts = nullptr;
+  a.mcounts = counts;
+  a.mmask = mask;
+  const int mt = (int)cdiv(d.m, 16);
+  dim3 grid((unsigned)cdiv(d.n, kPanel));
+  const bool ok = d.dtype == SPAROA_BF16
+                      ? launch_mt<SPAROA_BF16, true, false, true>(mt, grid, stream, a)
+                      : launch_mt<SPAROA_F16, true, false, true>(mt, grid, stream, a);
+  if (!ok) return fail(SPAROA_ERR_UNSUPPORTED, "fc bandwidth path: m");
+  SPAROA_LAUNCH_CHECK("fc_bw_kernel (self-measuring)");
   return SPAROA_OK;
 }
 

@@ -13,6 +13,10 @@
 // bits were newly set, so each nonzero block is counted exactly once and the
 // zero-block count needs no second pass.  Integer sums are order-independent,
 // so every output is deterministic.
+//
+// Counts leave a work-group through one atomic per counter: atomics on one
+// address serialise device-wide (~10 ns each on MI355X), so grids stay at a
+// few hundred work-groups that loop over the tensor.
 #include "common.h"
 
 namespace sparoa {
@@ -46,6 +50,35 @@ __device__ __forceinline__ uint64_t wave_sum(uint64_t v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
+}
+
+// Adds the work-group's zero count and nonzero-block count to the totals
+// (and the zero count to a per-sample slot): the waves' sums meet in LDS and
+// one lane issues one atomic per counter.  Every thread must call it.
+template <int NT>
+__device__ __forceinline__ void wg_commit(uint64_t zeros, uint64_t nonzero, sparoa_counts *counts,
+                                          uint64_t *sample_zeros) {
+  __shared__ unsigned long long part[2][NT / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t wz = wave_sum(zeros), wn = wave_sum(nonzero);
+  if (lane == 0) {
+    part[0][wave] = wz;
+    part[1][wave] = wn;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long z = 0, n = 0;
+#pragma unroll
+    for (int i = 0; i < NT / 64; ++i) {
+      z += part[0][i];
+      n += part[1][i];
+    }
+    if (z) {
+      atomicAdd((unsigned long long *)&counts->zeros, z);
+      if (sample_zeros) atomicAdd((unsigned long long *)sample_zeros, z);
+    }
+    if (n) atomicAdd((unsigned long long *)&counts->zero_blocks, 0ull - n);
+  }
 }
 
 // ORs (word, bits) pairs of the lanes into the bitmap, one atomic per distinct
@@ -173,15 +206,7 @@ __global__ __launch_bounds__(kThreads) void measure_main(
       }
     }
   }
-  const uint64_t wz = wave_sum(zeros);
-  const uint64_t wn = wave_sum((uint64_t)newly);
-  if ((threadIdx.x & 63) == 0) {
-    if (wz) {
-      atomicAdd((unsigned long long *)&counts->zeros, (unsigned long long)wz);
-      if (per_sample) atomicAdd((unsigned long long *)(per_sample + s), (unsigned long long)wz);
-    }
-    if (wn) atomicAdd((unsigned long long *)&counts->zero_blocks, (unsigned long long)(0ull - wn));
-  }
+  wg_commit<kThreads>(zeros, (uint64_t)newly, counts, per_sample ? per_sample + s : nullptr);
 }
 
 // One bitmap bit per lane (block = 1 row x V columns, V = elements per
@@ -189,27 +214,35 @@ __global__ __launch_bounds__(kThreads) void measure_main(
 // are two whole bitmap words.  The wave ballots its bits and two lanes store
 // the words: no atomics, and the bitmap needs no clearing.  The grid's slots
 // start at multiples of 64 items, which keeps the words aligned.
+constexpr int kLanebitThreads = 1024;  // one work-group per CU, 16 waves
+constexpr int kLanebitUnroll = 4;
+
 template <int ESZ, int V>
-__global__ __launch_bounds__(kThreads) void measure_lanebit(const char *__restrict__ x,
-                                                            int64_t items, int64_t words,
-                                                            uint32_t *__restrict__ mask,
-                                                            sparoa_counts *counts) {
+__global__ __launch_bounds__(kLanebitThreads) void measure_lanebit(const char *__restrict__ x,
+                                                                   int64_t items, int64_t words,
+                                                                   uint32_t *__restrict__ mask,
+                                                                   sparoa_counts *counts) {
+  constexpr int NT = kLanebitThreads;
   const int lane = threadIdx.x & 63;
-  const int64_t slot = (int64_t)gridDim.x * kThreads;
+  const int64_t slot = (int64_t)gridDim.x * NT;
   uint64_t zeros = 0, nonzero = 0;
-  for (int64_t base = (int64_t)blockIdx.x * kThreads; base < items; base += slot * kUnroll) {
-    uint32_t nz[kUnroll];
+  for (int64_t base = (int64_t)blockIdx.x * NT; base < items; base += slot * kLanebitUnroll) {
+    // unconditional loads (items past the end re-read the last item and are
+    // masked), so all kLanebitUnroll stay in flight
+    uint32_t nz[kLanebitUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
+    for (int u = 0; u < kLanebitUnroll; ++u) {
       const int64_t item = base + u * slot + threadIdx.x;
-      nz[u] = 0;
-      if (item < items) {
-        nz[u] = nonzero_bits<ESZ, V>(x + item * 16);
-        zeros += V - __popc(nz[u]);
-      }
+      nz[u] = nonzero_bits<ESZ, V>(x + min(item, items - 1) * 16);
     }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
+    for (int u = 0; u < kLanebitUnroll; ++u) {
+      const bool valid = base + u * slot + threadIdx.x < items;
+      nz[u] = valid ? nz[u] : 0u;
+      zeros += valid ? (uint64_t)(V - __popc(nz[u])) : 0ull;
+    }
+#pragma unroll
+    for (int u = 0; u < kLanebitUnroll; ++u) {
       const uint64_t bal = __ballot(nz[u] != 0u);
       const int64_t w0 = (base + u * slot + (threadIdx.x & ~63)) >> 5;
       if (lane == 0 && w0 < words) mask[w0] = (uint32_t)bal;
@@ -217,11 +250,7 @@ __global__ __launch_bounds__(kThreads) void measure_lanebit(const char *__restri
       nonzero += lane == 0 ? (uint64_t)__popcll(bal) : 0ull;
     }
   }
-  const uint64_t wz = wave_sum(zeros), wn = wave_sum(nonzero);
-  if (lane == 0) {
-    if (wz) atomicAdd((unsigned long long *)&counts->zeros, (unsigned long long)wz);
-    if (wn) atomicAdd((unsigned long long *)&counts->zero_blocks, (unsigned long long)(0ull - wn));
-  }
+  wg_commit<NT>(zeros, nonzero, counts, nullptr);
 }
 
 // Column strips: a single block row covering all rows, one column per block
@@ -275,11 +304,7 @@ __global__ __launch_bounds__(kThreads) void measure_strips(const char *__restric
       nonzero = __popc(word);
     }
   }
-  const uint64_t wz = wave_sum(zeros), wn = wave_sum(nonzero);
-  if (lane == 0) {
-    if (wz) atomicAdd((unsigned long long *)&counts->zeros, (unsigned long long)wz);
-    if (wn) atomicAdd((unsigned long long *)&counts->zero_blocks, (unsigned long long)(0ull - wn));
-  }
+  wg_commit<kThreads>(zeros, nonzero, counts, nullptr);
 }
 
 // Column strips that fit one work-group (at most 16 x 64 column groups): 16
@@ -410,14 +435,14 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
 
   if (lanebit) {
     const int64_t items = rows * (cols / vw);
-    int64_t gx = cdiv(items, (int64_t)kThreads);
-    if (gx > 2048) gx = 2048;
+    int64_t gx = cdiv(items, (int64_t)kLanebitThreads);
+    if (gx > 256) gx = 256;
     if (esz == 2)
-      hipLaunchKernelGGL((measure_lanebit<2, 8>), dim3((unsigned)gx), dim3(kThreads), 0, stream,
-                         static_cast<const char *>(x), items, words, mask, counts);
+      hipLaunchKernelGGL((measure_lanebit<2, 8>), dim3((unsigned)gx), dim3(kLanebitThreads), 0,
+                         stream, static_cast<const char *>(x), items, words, mask, counts);
     else
-      hipLaunchKernelGGL((measure_lanebit<4, 4>), dim3((unsigned)gx), dim3(kThreads), 0, stream,
-                         static_cast<const char *>(x), items, words, mask, counts);
+      hipLaunchKernelGGL((measure_lanebit<4, 4>), dim3((unsigned)gx), dim3(kLanebitThreads), 0,
+                         stream, static_cast<const char *>(x), items, words, mask, counts);
     SPAROA_LAUNCH_CHECK("measure_lanebit");
     return SPAROA_OK;
   }
@@ -437,7 +462,7 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
   const int64_t cpb = cdiv(br < rs ? br : rs, kRowChunk);   // row chunks per block row
   const int64_t items_s = nbr_s * cpb * (cols / V);
   int64_t gx = cdiv(items_s, (int64_t)kThreads);
-  const int64_t cap = cdiv(2048, S);
+  const int64_t cap = cdiv(512, S);
   if (gx > cap) gx = cap;
   if (gx < 1) gx = 1;
   dim3 grid((unsigned)gx, (unsigned)S);

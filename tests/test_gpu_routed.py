@@ -110,6 +110,59 @@ def test_conv_routed_matches_host_route_and_fixed_path(case, rho):
     assert torch.equal(y, y2)
 
 
+MEASURED_CASES = [(1, 4096, 512, "iid", 0.9), (8, 2048, 256, "block", 0.8),
+                  (16, 1024, 100, "iid", 0.97), (33, 520, 64, "block", 0.9),
+                  (64, 1024, 128, "block", 0.95), (5, 300, 48, "iid", 0.9),
+                  (96, 512, 256, "block", 0.9), (4, 4096, 4096, "iid", 0.0)]
+
+
+@pytest.mark.parametrize("case", MEASURED_CASES)
+@pytest.mark.parametrize("mode,thr_kind", [("block", "below"), ("block", "tie"),
+                                           ("block", "above"), ("element", "tie")])
+def test_fc_measured_equals_measure_then_routed(case, mode, thr_kind):
+    """sparoa_fc_measured (the FC kernel measuring its own input where it
+    can) gives the oracle's counts, bitmap and route bit for bit, and the
+    output of the fixed path it chose."""
+    abi = _abi()
+    m, k, n, pattern, rho = case
+    dev = torch.device("cuda")
+    dt = "f16" if m % 2 else "bf16"
+    tdt = torch.float16 if dt == "f16" else torch.bfloat16
+    x = synth.sparse_matrix(m, k, rho, pattern, dt, 700 + MEASURED_CASES.index(case))
+    w = synth.normal((n, k), dt, 98, std=k ** -0.5)
+    d = abi.fc_desc(m, k, n, abi.F16 if dt == "f16" else abi.BF16)
+    inten = abi.sparoa_op_intensity_fc(d)
+    fam = abi.PATH_SKIP_BW if inten["intensity"] < 315.0 else abi.PATH_SKIP_MFMA
+    br, bc = abi.sparoa_fc_skip_block(d, fam)
+    ref = oracle.measure(x, m, k, br, bc)
+    mcode = abi.ROUTE_BLOCK if mode == "block" else abi.ROUTE_ELEMENT
+    r = (ref["zero_blocks"] / ref["num_blocks"]) if mode == "block" else ref["zeros"] / ref["numel"]
+    s_thr = {"below": r / 2, "tie": r, "above": min(1.0, r + 0.01)}[thr_kind]
+    want = oracle.route(ref["zeros"], ref["numel"], ref["zero_blocks"], ref["num_blocks"],
+                        inten["intensity"], 0, s_thr, 315.0, mcode)
+    xd, wd = x.to(dev), w.to(dev)
+    wp = torch.empty(abi.sparoa_fc_packed_bytes(d) // 2, dtype=tdt, device=dev)
+    abi.sparoa_fc_pack_weights(d, wd, wp)
+    ws = torch.zeros(max(16, max(abi.sparoa_fc_workspace_size(d, p) for p in range(4))),
+                     dtype=torch.uint8, device=dev)
+    counts = torch.full((4,), -1, dtype=torch.int64, device=dev)
+    mask = torch.full((abi.sparoa_mask_words(m, k, br, bc),), -1, dtype=torch.int32, device=dev)
+    y = torch.full((m, n), float("nan"), dtype=tdt, device=dev)
+    path = torch.full((1,), -1, dtype=torch.int32, device=dev)
+    abi.sparoa_fc_measured(d, s_thr, 315.0, mcode, xd, wd, wp, None, None, abi.ACT_RELU, counts,
+                           mask, y, ws, path)
+    torch.cuda.synchronize()
+    assert counts.cpu().tolist() == [ref["zeros"], ref["numel"], ref["zero_blocks"],
+                                     ref["num_blocks"]]
+    assert np.array_equal(mask.cpu().numpy().view(np.uint32), ref["mask"])
+    assert int(path.item()) == want
+    y2 = torch.full_like(y, float("nan"))
+    wf = wp if abi.sparoa_fc_uses_packed(d, want) else wd
+    abi.sparoa_fc(d, want, xd, wf, None, None, abi.ACT_RELU, mask if want & 1 else None, y2, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+
+
 def test_fc_ops_run_equals_per_op_routed_calls():
     """The native batch executor runs measure + routed FC per op: paths and
     outputs equal the per-op calls, counts equal the oracle's."""
@@ -149,6 +202,7 @@ def test_fc_ops_run_equals_per_op_routed_calls():
         ref = oracle.measure(b["x"].cpu(), m, k, b["br"], b["bc"])
         c = b["counts"].cpu().tolist()
         assert c == [ref["zeros"], ref["numel"], ref["zero_blocks"], ref["num_blocks"]]
+        assert np.array_equal(b["mask"].cpu().numpy().view(np.uint32), ref["mask"])
         y2 = torch.full_like(b["y"], float("nan"))
         p2 = torch.full((1,), -1, dtype=torch.int32, device=dev)
         abi.sparoa_fc_routed(b["d"], 0.5, 315.0, abi.ROUTE_BLOCK, b["counts"], b["x"], b["w"],
@@ -159,45 +213,59 @@ def test_fc_ops_run_equals_per_op_routed_calls():
         assert evs[2 * i].elapsed_time(evs[2 * i + 1]) > 0
 
 
-def test_fc_ops_two_streams_equal_interleaved_run():
-    """Measurement on a side stream overlapping execution on the main stream
-    gives the same paths and outputs as the one-stream executor."""
+def test_fc_ops_run_in_a_hip_graph_equals_eager():
+    """The executor captured in a HIP graph: every replay (with eager work and
+    synchronisations in between) gives the eager run's counts, paths and
+    outputs."""
     abi = _abi()
     dev = torch.device("cuda")
     ops, bufs = [], []
     for i, (m, rho, pat) in enumerate([(1, 0.95, "iid"), (8, 0.9, "block"), (64, 0.9, "block"),
-                                       (8, 0.0, "iid")]):
+                                       (8, 0.0, "iid"), (96, 0.9, "block")]):
         k, n = 2048, 512
         d = abi.fc_desc(m, k, n, abi.BF16)
+        inten = abi.sparoa_op_intensity_fc(d)
+        fam = abi.PATH_SKIP_BW if inten["intensity"] < 315.0 else abi.PATH_SKIP_MFMA
+        br, bc = abi.sparoa_fc_skip_block(d, fam)
         b = dict(x=synth.sparse_matrix(m, k, rho, pat, "bf16", 500 + i).to(dev),
                  w=synth.normal((n, k), "bf16", 600 + i, std=k ** -0.5).to(dev),
                  wp=torch.empty(abi.sparoa_fc_packed_bytes(d) // 2, dtype=torch.bfloat16,
                                 device=dev),
                  counts=torch.zeros(4, dtype=torch.int64, device=dev),
-                 mask=torch.zeros(abi.sparoa_mask_words(m, k, m, 1), dtype=torch.int32, device=dev),
+                 mask=torch.zeros(abi.sparoa_mask_words(m, k, br, bc), dtype=torch.int32,
+                                  device=dev),
                  y=torch.zeros(m, n, dtype=torch.bfloat16, device=dev),
+                 ws=torch.zeros(max(16, max(abi.sparoa_fc_workspace_size(d, p) for p in range(4))),
+                                dtype=torch.uint8, device=dev),
                  path=torch.zeros(1, dtype=torch.int32, device=dev))
         abi.sparoa_fc_pack_weights(d, b["w"], b["wp"])
         bufs.append(b)          # keeps every buffer alive while the op structs point at it
         ops.append(abi.fc_op(d, b["x"], b["w"], b["wp"], None, None, abi.ACT_NONE, b["counts"],
-                             b["mask"], b["y"], None, b["path"]))
+                             b["mask"], b["y"], b["ws"], b["path"]))
     arr = abi.fc_op_array(ops)
     abi.sparoa_fc_ops_run(arr, 0.5, 315.0)
     torch.cuda.synchronize()
-    ref = [(b["y"].clone(), int(b["path"].item())) for b in bufs]
-    for b in bufs:
-        b["y"].zero_()
-        b["path"].fill_(-1)
-    main = torch.cuda.current_stream()
+    ref = [(b["y"].clone(), int(b["path"].item()), b["counts"].clone(), b["mask"].clone())
+           for b in bufs]
     side = torch.cuda.Stream()
-    ready = [torch.cuda.Event() for _ in ops]
-    timing = [torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-    for e in ready + timing:
-        e.record()
-    for _ in range(3):
-        abi.sparoa_fc_ops_run2(arr, 0.5, 315.0, ready=ready, timing=timing, measure_stream=side,
-                               exec_stream=main)
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g):
+            abi.sparoa_fc_ops_run(arr, 0.5, 315.0)
     torch.cuda.synchronize()
-    for b, (y, p) in zip(bufs, ref):
-        assert torch.equal(b["y"], y) and int(b["path"].item()) == p
-    assert timing[0].elapsed_time(timing[1]) > 0
+    scratch = torch.ones(1 << 20, device=dev)
+    for rep in range(3):
+        for b in bufs:                      # eager work between replays
+            b["y"].zero_()
+            b["path"].fill_(-1)
+            b["counts"].fill_(-1)
+            b["mask"].fill_(-1)
+        scratch.mul_(2.0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for b, (y, p, c, mk) in zip(bufs, ref):
+            assert torch.equal(b["y"], y), rep
+            assert int(b["path"].item()) == p, rep
+            assert torch.equal(b["counts"], c) and torch.equal(b["mask"], mk), rep
