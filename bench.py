@@ -50,6 +50,9 @@ def parse():
     p.add_argument("--sparsity-thr", type=float, default=None,
                    help="routing threshold; default: calibrated from forced-path timings")
     p.add_argument("--cases-out", default=None, help="write the per-case table (JSON) here")
+    p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                   help="only run 5 plain device-to-device copies of MIB MiB and exit (the "
+                        "reference kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     p.add_argument("--no-sweep", action="store_true",
                    help="skip the forced-path and per-operator timings (needs --sparsity-thr): "
                         "only the step kernels run, e.g. under a profiler")
@@ -96,16 +99,27 @@ class Case:
 
 
 def build_cases(abi, torch, synth, dev):
+    from concurrent.futures import ThreadPoolExecutor
+    specs = list(enumerate(case_list()))
+
+    def draw(spec):     # host-side seeded draws (numpy releases the GIL)
+        idx, (m, rho, pat) = spec
+        return (synth.sparse_matrix(m, K, rho, pat, "bf16", synth.seed_for(2, idx)),
+                synth.normal((N, K), "bf16", synth.seed_for(2, 50 + idx), std=1.0 / 64.0))
+
+    with ThreadPoolExecutor(max_workers=8) as pool:
+        drawn = list(pool.map(draw, specs))
     cases = []
-    for idx, (m, rho, pat) in enumerate(case_list()):
+    for (idx, (m, rho, pat)), (x_cpu, w_cpu) in zip(specs, drawn):
         c = Case()
         c.idx, c.m, c.rho, c.pattern = idx, m, rho, pat
         c.seed_x = synth.seed_for(2, idx)
         c.seed_w = synth.seed_for(2, 50 + idx)
-        c.x_cpu = synth.sparse_matrix(m, K, rho, pat, "bf16", c.seed_x)
+        c.x_cpu = x_cpu
         c.desc = abi.fc_desc(m, K, N, abi.BF16)
         c.x = c.x_cpu.to(dev)
-        w = synth.normal((N, K), "bf16", c.seed_w, std=1.0 / 64.0).to(dev)
+        w = w_cpu.to(dev)
+        del w_cpu
         c.wp = torch.empty(abi.sparoa_fc_packed_bytes(c.desc) // 2, dtype=torch.bfloat16,
                            device=dev)
         abi.sparoa_fc_pack_weights(c.desc, w, c.wp)
@@ -223,11 +237,19 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
-    import synth
-    from paper_2511_19457_amd import abi
-
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps(dict(copy_probe_bytes=n, copies=5)), flush=True)
+        return
+    import synth
+    from paper_2511_19457_amd import abi
     print("bench: building 24 FC operators (packing weights)", file=sys.stderr, flush=True)
     cases = build_cases(abi, torch, synth, dev)
 

@@ -134,6 +134,117 @@ __global__ __launch_bounds__(kThreads) void depthwise_kernel(DwArgs a) {
   }
 }
 
+// 3x3 depthwise, padding 1, stride S in both directions, 16-byte channel
+// vectors.  An item is (n, oh, run of kRun3 output pixels, channel vector);
+// the grid stride is a multiple of the channel-vector count, so a thread
+// keeps one channel vector for its whole life and loads its 9 x V weights
+// once (nine 16-byte loads: w[c][3][3] is contiguous over the V channels).
+// Per item, the 3 x NC input vectors the run needs are loaded unconditionally
+// (clamped addresses, zeroed outside the image) so they are all in flight
+// at once; each is decoded once and feeds every (output, tap) pair that
+// uses it.
+constexpr int kRun3 = 4;
+
+template <int DT, int S>
+__global__ __launch_bounds__(kThreads) void dw3x3_kernel(DwArgs a) {
+  using E = Elem<DT>;
+  using raw = typename E::raw;
+  constexpr int ESZ = E::size;
+  constexpr int V = 16 / ESZ;
+  constexpr int R = kRun3;
+  constexpr int NC = (R - 1) * S + 3;  // input columns per kernel row
+  const int64_t cv = a.C / V;
+  const int64_t runs = (a.Wo + R - 1) / R;
+  const int64_t total = a.N * a.Ho * runs * cv;
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  if (a.route.counts && a.route.path_out && blockIdx.x == 0 && threadIdx.x == 0)
+    *a.route.path_out = (device_route_skip(a.route) ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+  int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x;
+  if (i >= total) return;
+  const int64_t c0 = (i % cv) * V;
+  float wv[9][V];
+  {
+    raw we[9 * V];
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const uint4 q = *reinterpret_cast<const uint4 *>(a.w + (c0 * 9 + t * V) * ESZ);
+      __builtin_memcpy(&we[t * V], &q, 16);
+    }
+#pragma unroll
+    for (int j = 0; j < V; ++j)
+#pragma unroll
+      for (int t = 0; t < 9; ++t) wv[t][j] = E::to_f32(we[j * 9 + t]);
+  }
+  float bv[V];
+#pragma unroll
+  for (int j = 0; j < V; ++j)
+    bv[j] = a.bias ? E::to_f32(reinterpret_cast<const raw *>(a.bias)[c0 + j]) : 0.f;
+  const int H = (int)a.H, W = (int)a.W;
+  for (; i < total; i += stride) {
+    const int64_t rest = i / cv;
+    const int run = (int)(rest % runs);
+    const int64_t rest2 = rest / runs;
+    const int oh = (int)(rest2 % a.Ho);
+    const int64_t n = rest2 / a.Ho;
+    const int ow0 = run * R;
+    const int ih0 = oh * S - 1, iw0 = ow0 * S - 1;
+    uint4 xin[3][NC];
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+      const int ih = ih0 + r;
+      const bool rv = ih >= 0 && ih < H;
+      const int ihc = min(max(ih, 0), H - 1);
+      const char *rowp = a.x + (((n * H + ihc) * W) * a.C + c0) * ESZ;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int iw = iw0 + c;
+        const bool v = rv && iw >= 0 && iw < W;
+        const int iwc = min(max(iw, 0), W - 1);
+        const uint4 q = *reinterpret_cast<const uint4 *>(rowp + (int64_t)iwc * a.C * ESZ);
+        xin[r][c] = v ? q : make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+    float acc[R][V];
+#pragma unroll
+    for (int q = 0; q < R; ++q)
+#pragma unroll
+      for (int j = 0; j < V; ++j) acc[q][j] = bv[j];
+#pragma unroll
+    for (int r = 0; r < 3; ++r)
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        raw e[V];
+        __builtin_memcpy(e, &xin[r][c], 16);
+        float xv[V];
+#pragma unroll
+        for (int j = 0; j < V; ++j) xv[j] = E::to_f32(e[j]);
+#pragma unroll
+        for (int q = 0; q < R; ++q) {
+          const int s = c - q * S;  // tap column that reads input column c for output q
+          if (s < 0 || s > 2) continue;
+#pragma unroll
+          for (int j = 0; j < V; ++j) acc[q][j] = fmaf(xv[j], wv[r * 3 + s][j], acc[q][j]);
+        }
+      }
+#pragma unroll
+    for (int q = 0; q < R; ++q) {
+      const int ow = ow0 + q;
+      if (ow >= a.Wo) continue;
+      const int64_t o = ((n * a.Ho + oh) * a.Wo + ow) * a.C + c0;
+      if (a.residual) {
+        float rv[V];
+        load_vec<DT, V>(a.residual + o * ESZ, rv);
+#pragma unroll
+        for (int j = 0; j < V; ++j) acc[q][j] += rv[j];
+      }
+      float v[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) v[j] = apply_act(acc[q][j], a.act);
+      store_vec<DT, V>(a.y + o * ESZ, v);
+    }
+  }
+}
+
 template <int DT, int V>
 __global__ __launch_bounds__(kThreads) void maxpool_kernel(const char *x, char *y, int64_t N,
                                                            int64_t C, int64_t H, int64_t W,
@@ -175,6 +286,25 @@ sparoa_status dw_dispatch(const DwArgs &a, hipStream_t st) {
   int64_t blocks = cdiv(total, kThreads);
   if (blocks > 65536) blocks = 65536;
   const bool k3 = a.kh == 3 && a.kw == 3;
+  const bool fast3 = vec && k3 && a.ph == 1 && a.pw == 1 && a.dh == 1 && a.dw == 1 &&
+                     a.sh == a.sw && (a.sh == 1 || a.sh == 2);
+  if (fast3) {
+    // the grid stride must be a multiple of the channel-vector count
+    const int64_t cv = a.C / VV;
+    int64_t g = 256, c = cv;
+    while (c) { const int64_t t = g % c; g = c; c = t; }  // gcd(256, cv)
+    const int64_t q = cv / g;
+    const int64_t items = a.N * a.Ho * cdiv(a.Wo, kRun3) * cv;
+    int64_t nb = cdiv(items, kThreads);
+    if (nb > 4096) nb = 4096;
+    nb = cdiv(nb, q) * q;
+    if (a.sh == 1)
+      hipLaunchKernelGGL((dw3x3_kernel<DT, 1>), dim3((unsigned)nb), dim3(kThreads), 0, st, a);
+    else
+      hipLaunchKernelGGL((dw3x3_kernel<DT, 2>), dim3((unsigned)nb), dim3(kThreads), 0, st, a);
+    SPAROA_LAUNCH_CHECK("dw3x3_kernel");
+    return SPAROA_OK;
+  }
   if (vec && k3)
     hipLaunchKernelGGL((depthwise_kernel<DT, VV, 3, 3>), dim3((unsigned)blocks), dim3(kThreads), 0, st, a);
   else if (vec)

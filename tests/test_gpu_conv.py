@@ -109,6 +109,9 @@ DW_SHAPES = [
     (1, 144, 8, 9, 144, 3, 3, 1, 1, 1, 1, 1, 1, 144),
     (1, 12, 7, 7, 12, 5, 5, 1, 1, 2, 2, 1, 1, 12),     # runtime-window kernel
     (1, 5, 6, 6, 5, 3, 3, 1, 1, 1, 1, 1, 1, 5),        # channels % 8 != 0
+    (3, 24, 14, 13, 24, 3, 3, 2, 2, 1, 1, 1, 1, 24),   # stride 2, ragged pixel runs
+    (2, 16, 5, 3, 16, 3, 3, 1, 1, 1, 1, 1, 1, 16),     # row narrower than a run
+    (1, 40, 9, 9, 40, 3, 3, 1, 1, 1, 1, 2, 2, 40),     # dilation 2: general kernel
 ]
 
 
