@@ -69,6 +69,7 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
 
 // Implicit-GEMM MFMA conv (groups == 1); FC runs through it as a 1x1 conv.
 struct GemmTileChoice {
+  int cfg;          // 0: general kernel; else a tile of the 64-channel-chunk kernel
   int bm, bn;       // output tile rows (pixels) x cols (channels)
   int kchunk;       // K elements per main-loop step == skip granularity (channels)
   int split_k;      // number of K splits (1 = none)

@@ -35,13 +35,8 @@ struct Elem<SPAROA_BF16> {
   static constexpr int size = 2;
   // bfloat16 is the upper half of a binary32.
   __device__ static float to_f32(raw v) { return __uint_as_float((uint32_t)v << 16); }
-  // Round to nearest, ties to even, on the 16 dropped bits; NaN stays a quiet NaN.
-  __device__ static raw from_f32(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (raw)((u >> 16) | 0x0040u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (raw)(u >> 16);
-  }
+  // Round to nearest, ties to even (gfx950 converts in hardware: v_cvt_pk_bf16_f32).
+  __device__ static raw from_f32(float f) { return __builtin_bit_cast(raw, (__bf16)f); }
 };
 
 __device__ __forceinline__ float apply_act(float v, int act) {

@@ -42,6 +42,7 @@ constexpr int kMaxVecWords = kMaxChunks * kBK / 8 / 32;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 struct GemmArgs {
   const char *x;
@@ -55,6 +56,8 @@ struct GemmArgs {
   int64_t M, N, K;
   int64_t H, W, Cin, Ho, Wo, Kw, sh, sw, ph, pw, dh, dw, taps;
   int64_t nchunks, chunks_per_split;
+  int64_t x_bytes, w_bytes;  // buffer-descriptor ranges (second-generation kernel)
+  float inv_wo, inv_ho;      // 1 / Wo, 1 / Ho rounded once on the host (float divmod)
   int act;
   int split;
   DeviceRoute route;
@@ -84,6 +87,23 @@ __device__ __forceinline__ f32x4 mfma_chunk(const char *a_row, const char *b_row
     return acc;
   }
 }
+
+__device__ __forceinline__ int64_t cdiv_dev(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// q = n / d, r = n % d for 0 <= n < 2^24 and 0 < d < 2^24: the float
+// quotient is within one of the true one, then one integer correction.
+__device__ __forceinline__ void divmod_small(int n, int d, float inv_d, int &q, int &r) {
+  q = (int)((float)n * inv_d);
+  r = n - q * d;
+  if (r < 0) {
+    --q;
+    r += d;
+  } else if (r >= d) {
+    ++q;
+    r -= d;
+  }
+}
+
 
 // Reads n <= 32 bits starting at bit `pos` of a bitmap.
 __device__ __forceinline__ uint32_t read_bits(const uint32_t *m, int64_t pos, int n) {
@@ -361,6 +381,387 @@ __global__ __launch_bounds__(256) void split_reduce(const float *__restrict__ pa
   }
 }
 
+// ---------------------------------------------------------------------------
+// Second-generation implicit GEMM for the common case: 16-bit data, groups 1,
+// C_in % 64 == 0.  A K chunk is 64 channels of one tap, so the tap and
+// channel offset of a chunk are work-group-uniform scalars (no per-vector
+// division), and a thread's gathered pixels only move by the tap offset.
+// Work-group = 256 threads = WGM x WGN waves; a wave owns WTM x WTN MFMA
+// 16x16 blocks (up to 128 x 64 outputs), which sets the LDS bytes read per
+// MFMA.  Chunks are staged global -> registers -> LDS (row stride 144 B:
+// conflict-free 16-byte reads and writes), double-buffered, one barrier per
+// 64-wide chunk (two MFMA k-steps).  Gathers are branch-free (out-of-image
+// taps read a valid address and are zeroed) so all of a thread's loads are
+// in flight together.  Tiles are ordered so that each XCD works on a
+// contiguous range of output rows (neighbouring tiles share input halos in
+// that XCD's L2).  The skip form walks only the (tap, 64-channel) chunks in
+// which some gathered pixel of the tile is nonzero, in dense order, so its
+// output equals the dense form's bit for bit.
+constexpr int kBK2 = 64;
+constexpr int kMaxChunks2 = 1024;          // K <= 65536 on the skip path
+// Word 3 of a raw buffer descriptor on gfx9-family GPUs (32-bit data format;
+// untyped dword loads ignore the rest).
+constexpr int kBufDword3 = 0x00020000;
+
+template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
+__global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
+  constexpr int BKC = 32 * KS;         // channels per chunk (KS MFMA k-steps)
+  constexpr int ROW = BKC * 2 + 32;    // LDS row stride, bytes: +32 is free of bank conflicts
+                                       // for the 16-byte writes and MFMA-operand reads on gfx950
+  constexpr int VPR = BKC / 8;         // 16-byte vectors per chunk row
+  using E = Elem<DT>;
+  static_assert(E::size == 2, "16-bit types");
+  static_assert(WGM * WGN == 4, "four waves");
+  constexpr int BM = WGM * 16 * WTM, BN = WGN * 16 * WTN;
+  constexpr int AV = BM * VPR / kThreads;  // 16-byte A vectors per thread per chunk
+  constexpr int BV = BN * VPR / kThreads;
+  constexpr int RPU = kThreads / VPR;       // rows covered by one vector slot u
+  static_assert(AV >= 1 && BV >= 1, "tile too small");
+
+  __shared__ __attribute__((aligned(16))) char smem[2][(BM + BN) * ROW];
+  __shared__ unsigned short list[SKIP ? kMaxChunks2 : 1];
+  __shared__ uint32_t nzvec[SKIP ? kMaxVecWords : 1];
+  __shared__ int list_len;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  // XCD-aware order on a 1-D grid: work-groups are dealt round-robin to the 8
+  // XCDs, so XCD i gets the i-th contiguous range of tile ids, and a tile id
+  // walks (split, row tile, column tile) with the column tiles innermost: the
+  // tiles that gather the same input rows run together in one XCD's L2.
+  const int64_t ntm = cdiv_dev(a.M, BM), ntn = cdiv_dev(a.N, BN);
+  int64_t tile;
+  {
+    const int64_t total = (int64_t)gridDim.x, L = blockIdx.x;
+    const int64_t q = total >> 3, r = total & 7, xcd = L & 7, k = L >> 3;
+    tile = xcd < r ? xcd * (q + 1) + k : r * (q + 1) + (xcd - r) * q + k;
+  }
+  const int64_t zsplit = tile / (ntm * ntn);
+  const int64_t rest = tile - zsplit * ntm * ntn;
+  const int64_t m0 = (rest / ntn) * BM, n0 = (rest % ntn) * BN;
+  const bool first_tile = tile == 0;
+  const bool first_col = rest % ntn == 0;
+  const int64_t c_begin = zsplit * a.chunks_per_split;
+  const int64_t c_end = min(c_begin + a.chunks_per_split, a.nchunks);
+  const int cpt = (int)(a.Cin / BKC);   // chunks per tap
+  const int cg = tid % VPR;             // this thread's 16-byte column of a chunk row
+  const int rr = tid / VPR;             // this thread's first chunk row
+
+  // ---- gathered pixels of this thread's A rows (fixed over the K loop).
+  // Loads go through buffer descriptors: a 32-bit byte offset per lane, and
+  // an offset past the end (taps in the padding) reads 0 without touching
+  // memory.  vt[u] has bit t set when tap t of row u lies inside the image.
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc((void *)a.x, (short)0, (int)a.x_bytes, kBufDword3);
+  const __amdgpu_buffer_rsrc_t wr =
+      __builtin_amdgcn_make_buffer_rsrc((void *)a.w, (short)0, (int)a.w_bytes, kBufDword3);
+  int a_offb[AV];      // byte offset of (n, h0, w0, channel cg*8)
+  uint32_t vrow[AV], vcol[AV];  // bit r / s: kernel row r / column s lies inside the image
+  const int H = (int)a.H, W = (int)a.W, Ho = (int)a.Ho, Wo = (int)a.Wo, Cin = (int)a.Cin;
+  const int kw = (int)a.Kw, dh = (int)a.dh, dw = (int)a.dw;
+  const float inv_wo = a.inv_wo, inv_ho = a.inv_ho;
+#pragma unroll
+  for (int u = 0; u < AV; ++u) {
+    const int m = (int)m0 + rr + RPU * u;
+    const int mm = m < (int)a.M ? m : 0;
+    int t1, ow, nn, oh;
+    divmod_small(mm, Wo, inv_wo, t1, ow);
+    divmod_small(t1, Ho, inv_ho, nn, oh);
+    const int h0 = oh * (int)a.sh - (int)a.ph, w0 = ow * (int)a.sw - (int)a.pw;
+    a_offb[u] = (((nn * H + h0) * W + w0) * Cin + cg * 8) * 2;
+    uint32_t rb_ = 0, cb_ = 0;
+    for (int r = 0; r < (int)a.taps / kw; ++r) {
+      const int ih = h0 + r * dh;
+      rb_ |= (ih >= 0 && ih < H ? 1u : 0u) << r;
+    }
+    for (int sx = 0; sx < kw; ++sx) {
+      const int iw = w0 + sx * dw;
+      cb_ |= (iw >= 0 && iw < W ? 1u : 0u) << sx;
+    }
+    vrow[u] = rb_;
+    vcol[u] = cb_;
+  }
+  int b_offb[BV];
+#pragma unroll
+  for (int u = 0; u < BV; ++u) {
+    const int jn = (int)n0 + rr + RPU * u;
+    b_offb[u] = ((jn < (int)a.N ? jn : 0) * (int)a.K + cg * 8) * 2;
+  }
+
+  // ---- skip list ---------------------------------------------------------
+  int64_t count = c_end - c_begin;
+  bool use_list = SKIP;
+  if constexpr (SKIP) {
+    if (a.route.counts) {
+      use_list = device_route_skip(a.route);
+      if (a.route.path_out && first_tile && tid == 0)
+        *a.route.path_out = (use_list ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+    }
+  }
+  if constexpr (!SKIP) {
+    if (a.route.path_out && first_tile && tid == 0)
+      *a.route.path_out = (uint32_t)a.route.bw_bit << 1;
+  }
+  if (SKIP && use_list) {
+    const int cpg = (int)(a.Cin / 8);  // bitmap blocks per pixel
+    const int kv_words = (int)((a.taps * cpg + 31) / 32);
+    for (int i = tid; i < kv_words; i += kThreads) nzvec[i] = 0u;
+    __syncthreads();
+    for (int64_t p = tid; p < (int64_t)BM * a.taps; p += kThreads) {
+      const int r_in = (int)(p / a.taps);
+      const int tap = (int)(p - (int64_t)r_in * a.taps);
+      const int64_t m = m0 + r_in;
+      if (m >= a.M) continue;
+      const int64_t ow = m % a.Wo, oh = (m / a.Wo) % a.Ho, nn = m / (a.Wo * a.Ho);
+      const int64_t r = tap / a.Kw, sx = tap - r * a.Kw;
+      const int64_t ih = oh * a.sh - a.ph + r * a.dh, iw = ow * a.sw - a.pw + sx * a.dw;
+      if (ih < 0 || ih >= a.H || iw < 0 || iw >= a.W) continue;
+      const int64_t pix = (nn * a.H + ih) * a.W + iw;
+      for (int b = 0; b < cpg; b += 32) {
+        const int nb = min(32, cpg - b);
+        lds_or_bits(nzvec, tap * cpg + b, read_bits(a.mask, pix * cpg + b, nb), nb);
+      }
+    }
+    __syncthreads();
+    if (wave == 0) {
+      int total = 0;
+      for (int64_t base = c_begin; base < c_end; base += 64) {
+        const int64_t j = base + lane;
+        bool nz = false;
+        if (j < c_end) {
+          // chunk j = channels [BKC cb, BKC cb + BKC) of tap t: BKC / 8
+          // bitmap bits starting at a multiple of BKC / 8 (cpg is one too),
+          // so they lie inside one 32-bit word
+          const int t = (int)(j / cpt), cb = (int)(j - (int64_t)t * cpt);
+          const int pos = t * cpg + (BKC / 8) * cb;
+          constexpr uint32_t kBits = BKC / 8 >= 32 ? 0xFFFFFFFFu : ((1u << (BKC / 8)) - 1u);
+          nz = ((nzvec[pos >> 5] >> (pos & 31)) & kBits) != 0u;
+        }
+        const uint64_t bal = __ballot(nz);
+        const int before = __popcll(bal & ((1ull << lane) - 1ull));
+        if (nz) list[total + before] = (unsigned short)j;
+        total += __popcll(bal);
+      }
+      if (lane == 0) {
+        list_len = total;
+        if (a.executed && first_col && total)
+          atomicAdd(a.executed, (unsigned long long)total);
+      }
+    }
+    __syncthreads();
+    count = list_len;
+  }
+  auto chunk_at = [&](int i) __attribute__((always_inline)) -> int {
+    return (SKIP && use_list) ? (int)list[i] : (int)c_begin + i;
+  };
+
+  // ---- staging: a ring of PF chunks in registers, two chunks in LDS --------
+  u32x4 ra[PF][AV], rb[PF][BV];  // native vectors: no struct copies, stays in VGPRs
+  auto load_chunk = [&](int j, u32x4 (&ra_s)[AV], u32x4 (&rb_s)[BV])
+                        __attribute__((always_inline)) {
+    const int t = j / cpt, cb = j - t * cpt;
+    const int r = t / kw, sx = t - r * kw;
+    const int tap_offb = ((r * dh * W + sx * dw) * Cin + cb * BKC) * 2;
+#pragma unroll
+    for (int u = 0; u < AV; ++u) {
+      const bool in_img = (vrow[u] >> r) & (vcol[u] >> sx) & 1u;
+      const int off = in_img ? a_offb[u] + tap_offb : (int)0x80000000;
+      ra_s[u] = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < BV; ++u)
+      rb_s[u] = __builtin_amdgcn_raw_buffer_load_b128(wr, b_offb[u], j * (BKC * 2), 0);
+  };
+  auto store_chunk = [&](int buf, const u32x4 (&ra_s)[AV], const u32x4 (&rb_s)[BV])
+                         __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < AV; ++u)
+      *reinterpret_cast<u32x4 *>(&smem[buf][(rr + RPU * u) * ROW + cg * 16]) = ra_s[u];
+#pragma unroll
+    for (int u = 0; u < BV; ++u)
+      *reinterpret_cast<u32x4 *>(&smem[buf][(BM + rr + RPU * u) * ROW + cg * 16]) =
+          rb_s[u];
+  };
+
+  f32x4 acc[WTM][WTN];
+#pragma unroll
+  for (int i = 0; i < WTM; ++i)
+#pragma unroll
+    for (int j = 0; j < WTN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int g = lane >> 4, rl = lane & 15;
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    const char *As = &smem[buf][(wm * WTM * 16 + rl) * ROW + 16 * g];
+    const char *Bs = &smem[buf][(BM + wn * WTN * 16 + rl) * ROW + 16 * g];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      u32x4 af[WTM], bfr[WTN];
+#pragma unroll
+      for (int tm = 0; tm < WTM; ++tm)
+        af[tm] = *reinterpret_cast<const u32x4 *>(As + tm * 16 * ROW + 64 * ks);
+#pragma unroll
+      for (int tn = 0; tn < WTN; ++tn)
+        bfr[tn] = *reinterpret_cast<const u32x4 *>(Bs + tn * 16 * ROW + 64 * ks);
+#pragma unroll
+      for (int tm = 0; tm < WTM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < WTN; ++tn) {
+          if constexpr (DT == SPAROA_BF16)
+            acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, af[tm]), __builtin_bit_cast(bf16x8, bfr[tn]),
+                acc[tm][tn], 0, 0, 0);
+          else
+            acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                __builtin_bit_cast(f16x8, af[tm]), __builtin_bit_cast(f16x8, bfr[tn]),
+                acc[tm][tn], 0, 0, 0);
+        }
+    }
+  };
+  // Chunk i lives in register slot i % PF until it is stored to LDS buffer
+  // i & 1 (one iteration ahead of its use); the slot is then refilled with
+  // chunk i + PF, so PF chunks of loads are always in flight.  The loop body
+  // is written out once per slot so every slot index is a constant and the
+  // ring stays in registers.
+  static_assert(PF >= 2 && PF <= 4, "register ring depth");
+  const int n = (int)count;
+  if (n > 0) {
+    // chunk 0 alone first (every work-group starts at once: a deep prologue
+    // would queue each one's first chunk behind all the others' prefetch)
+    load_chunk(chunk_at(0), ra[0], rb[0]);
+    store_chunk(0, ra[0], rb[0]);
+    load_chunk(chunk_at(min(1, n - 1)), ra[1], rb[1]);
+    if constexpr (PF > 2) load_chunk(chunk_at(min(2, n - 1)), ra[PF > 2 ? 2 : 0], rb[PF > 2 ? 2 : 0]);
+    if constexpr (PF > 3) load_chunk(chunk_at(min(3, n - 1)), ra[PF > 3 ? 3 : 0], rb[PF > 3 ? 3 : 0]);
+    load_chunk(chunk_at(min(PF, n - 1)), ra[0], rb[0]);
+    __syncthreads();
+  // Steady state: groups of PF straight-line steps (no branch inside a step,
+  // so the compiler's load counters stay exact and PF chunks stay in flight);
+  // the refill past the end re-reads the last chunk.  The last group runs
+  // the guarded form.
+#define SPAROA_IG_STEP(D, GUARD)                                                   \
+  {                                                                                \
+    constexpr int sn = ((D) + 1) % PF;                                             \
+    const int i = i0 + (D);                                                        \
+    if (!(GUARD) || i < n) {                                                       \
+      compute(i & 1);                                                              \
+      if (!(GUARD) || i + 1 < n) store_chunk((i + 1) & 1, ra[sn], rb[sn]); \
+      load_chunk(chunk_at(min(i + 1 + PF, n - 1)), ra[sn], rb[sn]);       \
+      __syncthreads();                                                             \
+    }                                                                              \
+  }
+    int i0 = 0;
+    for (; i0 + PF < n; i0 += PF) {
+      SPAROA_IG_STEP(0, false)
+      SPAROA_IG_STEP(1, false)
+      if constexpr (PF > 2) SPAROA_IG_STEP(2, false)
+      if constexpr (PF > 3) SPAROA_IG_STEP(3, false)
+    }
+    for (; i0 < n; i0 += PF) {
+      SPAROA_IG_STEP(0, true)
+      SPAROA_IG_STEP(1, true)
+      if constexpr (PF > 2) SPAROA_IG_STEP(2, true)
+      if constexpr (PF > 3) SPAROA_IG_STEP(3, true)
+    }
+#undef SPAROA_IG_STEP
+  }
+
+  // ---- epilogue: the fp32 tile goes through LDS (a lane holds rows
+  // 4*(lane/16) + v, column lane % 16 of each MFMA block), then each thread
+  // finishes 8 consecutive columns of a row: bias and residual as 16-byte
+  // loads, one 16-byte store.
+  using raw = typename E::raw;
+  constexpr int CS = BN + 4;  // fp32 row stride of the staged tile
+  static_assert(BM * CS * 4 <= (int)sizeof(smem), "staged tile fits the LDS buffers");
+  float *ct = reinterpret_cast<float *>(&smem[0][0]);
+  __syncthreads();
+#pragma unroll
+  for (int tm = 0; tm < WTM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < WTN; ++tn)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        ct[(wm * WTM * 16 + tm * 16 + 4 * g + v) * CS + wn * WTN * 16 + tn * 16 + rl] =
+            acc[tm][tn][v];
+  __syncthreads();
+  constexpr int C8 = BN / 8;
+  const bool vec_n = a.N % 8 == 0;
+  for (int q = tid; q < BM * C8; q += kThreads) {
+    const int r = q / C8, c = (q % C8) * 8;
+    const int64_t row = m0 + r, col = n0 + c;
+    if (row >= a.M || col >= a.N) continue;
+    float o[8];
+    {
+      const float4 lo = *reinterpret_cast<const float4 *>(&ct[r * CS + c]);
+      const float4 hi = *reinterpret_cast<const float4 *>(&ct[r * CS + c + 4]);
+      o[0] = lo.x; o[1] = lo.y; o[2] = lo.z; o[3] = lo.w;
+      o[4] = hi.x; o[5] = hi.y; o[6] = hi.z; o[7] = hi.w;
+    }
+    const int ne = (int)min((int64_t)8, a.N - col);
+    if (a.split > 1) {
+      float *dst = a.partial + (zsplit * a.M + row) * a.N + col;
+      if (vec_n) {
+        *reinterpret_cast<float4 *>(dst) = make_float4(o[0], o[1], o[2], o[3]);
+        *reinterpret_cast<float4 *>(dst + 4) = make_float4(o[4], o[5], o[6], o[7]);
+      } else {
+        for (int e = 0; e < ne; ++e) dst[e] = o[e];
+      }
+      continue;
+    }
+    raw *dst = reinterpret_cast<raw *>(a.y) + row * a.N + col;
+    if (vec_n) {
+      raw bv[8], rv[8], out[8];
+      if (a.bias) {
+        const uint4 q4 = *reinterpret_cast<const uint4 *>(reinterpret_cast<const raw *>(a.bias) + col);
+        __builtin_memcpy(bv, &q4, 16);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] += E::to_f32(bv[e]);
+      }
+      if (a.residual) {
+        const uint4 q4 = *reinterpret_cast<const uint4 *>(
+            reinterpret_cast<const raw *>(a.residual) + row * a.N + col);
+        __builtin_memcpy(rv, &q4, 16);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] += E::to_f32(rv[e]);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) out[e] = E::from_f32(apply_act(o[e], a.act));
+      uint4 q4;
+      __builtin_memcpy(&q4, out, 16);
+      *reinterpret_cast<uint4 *>(dst) = q4;
+    } else {
+      for (int e = 0; e < ne; ++e) {
+        float v = o[e];
+        if (a.bias) v += E::to_f32(reinterpret_cast<const raw *>(a.bias)[col + e]);
+        if (a.residual) v += E::to_f32(reinterpret_cast<const raw *>(a.residual)[row * a.N + col + e]);
+        dst[e] = E::from_f32(apply_act(v, a.act));
+      }
+    }
+  }
+}
+
+template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
+void launch_ig(dim3 grid, hipStream_t st, const GemmArgs &a) {
+  hipLaunchKernelGGL((igemm_kernel<DT, WGM, WGN, WTM, WTN, PF, KS, SKIP>), grid, dim3(kThreads),
+                     0, st, a);
+}
+
+// Tile configurations of the second-generation kernel (BM x BN) and the
+// chunks each keeps in flight in registers.
+enum IgCfg { kIg128x128 = 1, kIg128x64, kIg64x64 };
+
+// 64-channel chunks: two MFMA k-steps per barrier (four measured slower:
+// more LDS and registers per work-group for the same latency per step).
+template <int DT, bool SKIP>
+bool dispatch_ig(int cfg, int kchunk, dim3 grid, hipStream_t st, const GemmArgs &a) {
+  if (kchunk != kBK2) return false;
+  switch (cfg) {
+    case kIg128x128: launch_ig<DT, 2, 2, 4, 4, 3, 2, SKIP>(grid, st, a); return true;
+    case kIg128x64: launch_ig<DT, 2, 2, 4, 2, 4, 2, SKIP>(grid, st, a); return true;
+    case kIg64x64: launch_ig<DT, 2, 2, 2, 2, 4, 2, SKIP>(grid, st, a); return true;
+  }
+  return false;
+}
+
 __global__ void set_u64(unsigned long long *p, unsigned long long v) { *p = v; }
 
 template <int DT, int TM, int TN, bool VEC, bool SKIP>
@@ -442,15 +843,58 @@ sparoa_status launch_split_reduce(sparoa_dtype dt, const float *partial, int spl
   return SPAROA_OK;
 }
 
+namespace {
+// The second-generation kernel takes 16-bit convs whose channel count is a
+// multiple of its 64-wide K chunk.
+bool ig_eligible(const sparoa_conv_desc &d) {
+  // 32-bit byte offsets into x and w; pixel indices below 2^24 (float divmod)
+  if (d.n * d.h * d.w * d.c_in >= ((int64_t)1 << 30)) return false;
+  if (shape_of(d).M >= ((int64_t)1 << 24) || d.kw > 32 || d.kh > 32) return false;
+  if (d.c_out * d.kh * d.kw * d.c_in >= ((int64_t)1 << 30)) return false;
+  return d.dtype != SPAROA_F32 && d.groups == 1 && d.c_in % kBK2 == 0 &&
+         cdiv(d.kh * d.kw * d.c_in, kBK2) <= kMaxChunks2 &&
+         d.kh * d.kw * (d.c_in / 8) <= (int64_t)kMaxVecWords * 32;
+}
+
+// Tile of the second-generation kernel: the largest tile that still gives
+// every CU a work-group, else the smallest with split-K.
+GemmTileChoice ig_choose(const Shape &s, int64_t c_in) {
+  auto tiles = [&](int bm, int bn) { return cdiv(s.M, bm) * cdiv(s.N, bn); };
+  GemmTileChoice t;
+  t.kchunk = kBK2;
+  (void)c_in;
+  if (s.N <= 64) {
+    if (tiles(128, 64) >= 240) { t.cfg = kIg128x64; t.bm = 128; t.bn = 64; }
+    else { t.cfg = kIg64x64; t.bm = 64; t.bn = 64; }
+  } else if (tiles(128, 128) >= 240) { t.cfg = kIg128x128; t.bm = 128; t.bn = 128; }
+  else if (tiles(128, 64) >= 240) { t.cfg = kIg128x64; t.bm = 128; t.bn = 64; }
+  else { t.cfg = kIg64x64; t.bm = 64; t.bn = 64; }
+  const int64_t tl = tiles(t.bm, t.bn), nchunks = cdiv(s.K, t.kchunk);
+  int64_t split = 1;
+  if (tl < 192) {
+    split = cdiv(512, tl);
+    if (split > 8) split = 8;
+    if (split > nchunks / 4) split = nchunks / 4;
+    if (split < 1) split = 1;
+  }
+  t.split_k = (int)split;
+  return t;
+}
+}  // namespace
+
 bool gemm_skip_supported(const sparoa_conv_desc &d) {
   const Shape s = shape_of(d);
+  if (ig_eligible(d)) return true;
   const int64_t bits = d.kh * d.kw * cdiv(d.c_in, 8);
   return cdiv(s.K, kBK) <= kMaxChunks && bits <= (int64_t)kMaxVecWords * 32;
 }
 
+
 GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path) {
   const Shape s = shape_of(d);
+  if (ig_eligible(d)) return ig_choose(s, d.c_in);
   GemmTileChoice t;
+  t.cfg = 0;
   t.kchunk = kBK;
   if (d.dtype == SPAROA_F32) {
     t.bm = 64;
@@ -491,7 +935,7 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   const int epv = d.dtype == SPAROA_F32 ? 4 : 8;
   const bool vec = d.c_in % epv == 0;
   const bool skip = mask != nullptr;
-  const int64_t nchunks = cdiv(s.K, kBK);
+  const int64_t nchunks = cdiv(s.K, t.kchunk);
   if (skip && !gemm_skip_supported(d))
     return fail(SPAROA_ERR_UNSUPPORTED, "zero-skip conv: K above the skip kernel's 65536");
   if (s.M > INT32_MAX || s.N > INT32_MAX) return fail(SPAROA_ERR_UNSUPPORTED, "GEMM too large");
@@ -509,6 +953,10 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   a.H = d.h; a.W = d.w; a.Cin = d.c_in; a.Ho = s.ho; a.Wo = s.wo; a.Kw = d.kw;
   a.sh = d.sh; a.sw = d.sw; a.ph = d.ph; a.pw = d.pw; a.dh = d.dh; a.dw = d.dw;
   a.taps = d.kh * d.kw;
+  a.x_bytes = d.n * d.h * d.w * d.c_in * elem_size(d.dtype);
+  a.w_bytes = s.N * s.K * elem_size(d.dtype);
+  a.inv_wo = 1.0f / (float)s.wo;
+  a.inv_ho = 1.0f / (float)s.ho;
   a.nchunks = nchunks;
   a.split = t.split_k;
   a.chunks_per_split = cdiv(nchunks, t.split_k);
@@ -525,8 +973,21 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
     SPAROA_LAUNCH_CHECK("set_u64");
   }
   dim3 grid((unsigned)cdiv(s.M, t.bm), (unsigned)cdiv(s.N, t.bn), (unsigned)gz);
+  if (t.cfg) grid = dim3((unsigned)(cdiv(s.M, t.bm) * cdiv(s.N, t.bn) * gz));
   bool ok = false;
-  switch (d.dtype) {
+  if (t.cfg) {
+    switch (d.dtype) {
+      case SPAROA_BF16:
+        ok = skip ? dispatch_ig<SPAROA_BF16, true>(t.cfg, t.kchunk, grid, stream, a)
+                  : dispatch_ig<SPAROA_BF16, false>(t.cfg, t.kchunk, grid, stream, a);
+        break;
+      case SPAROA_F16:
+        ok = skip ? dispatch_ig<SPAROA_F16, true>(t.cfg, t.kchunk, grid, stream, a)
+                  : dispatch_ig<SPAROA_F16, false>(t.cfg, t.kchunk, grid, stream, a);
+        break;
+      default: break;
+    }
+  } else switch (d.dtype) {
     case SPAROA_BF16: ok = dispatch<SPAROA_BF16>(t.bm, t.bn, vec, skip, grid, stream, a); break;
     case SPAROA_F16: ok = dispatch<SPAROA_F16>(t.bm, t.bn, vec, skip, grid, stream, a); break;
     case SPAROA_F32: ok = dispatch<SPAROA_F32>(t.bm, t.bn, vec, skip, grid, stream, a); break;

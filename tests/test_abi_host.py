@@ -174,7 +174,12 @@ def test_tiling_and_skip_block_queries():
     d = abi.conv_desc(32, 256, 14, 14, 256, 3, 3, 1, 1, 1, 1)
     assert abi.sparoa_conv2d_skip_block(d, abi.PATH_SKIP_MFMA) == (1, 8)
     tr, kc = abi.sparoa_conv2d_tiling(d, abi.PATH_SKIP_MFMA)
-    assert tr in (64, 128) and kc == 32
+    assert tr in (64, 128, 256) and kc == 64          # channels % 64 == 0: 64-wide chunks
+    d24 = abi.conv_desc(2, 24, 14, 14, 144, 1, 1)
+    tr, kc = abi.sparoa_conv2d_tiling(d24, abi.PATH_SKIP_MFMA)
+    assert tr in (64, 128) and kc == 32               # general kernel: 32-wide chunks
+    d32 = abi.conv_desc(1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, dtype=abi.F32)
+    assert abi.sparoa_conv2d_tiling(d32, abi.PATH_DENSE_MFMA)[1] == 32
     f = abi.fc_desc(8, 4096, 4096)
     assert abi.sparoa_fc_skip_block(f, abi.PATH_SKIP_BW) == (8, 1)
     assert abi.sparoa_fc_tiling(f, abi.PATH_SKIP_BW) == (8, 1)

@@ -6,7 +6,7 @@ import torch
 
 import oracle
 import synth
-from tests._util import RTOL, assert_close
+from tests._util import RTOL, SUBNORMAL_STEP, assert_close
 
 pytestmark = pytest.mark.gpu
 
@@ -154,3 +154,54 @@ def test_maxpool_vs_oracle(dt):
     torch.cuda.synchronize()
     ref = oracle.maxpool2d(x, 2, 64, 17, 18)
     assert np.array_equal(y.float().cpu().numpy().astype(np.float64), ref)
+
+
+# Shapes that make the tile chooser pick each tile of the 64-channel-chunk
+# kernel (expected tile rows in the last field).
+IG_SHAPES = [
+    ((2, 64, 64, 64, 1024, 1, 1, 1, 1, 0, 0, 1, 1, 1), 128),   # 128 x 128
+    ((1, 64, 64, 64, 1000, 1, 1, 1, 1, 0, 0, 1, 1, 1), 128),   # 128 x 128, ragged N
+    ((4, 64, 128, 128, 64, 3, 3, 1, 1, 1, 1, 1, 1, 1), 128),   # 128 x 64, N = 64
+    ((2, 64, 127, 129, 64, 3, 3, 1, 1, 1, 1, 1, 1, 1), 128),   # 128 x 64, ragged M
+    ((1, 128, 32, 64, 1024, 1, 1, 1, 1, 0, 0, 1, 1, 1), 128),  # 128 x 64, wide N
+    ((2, 128, 9, 9, 96, 3, 3, 2, 2, 1, 1, 1, 1, 1), 64),       # 64 x 64, split-K
+    ((1, 192, 7, 7, 36, 3, 3, 1, 1, 1, 1, 1, 1, 1), 64),       # 64 x 64, N % 8 != 0
+]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+@pytest.mark.parametrize("case", IG_SHAPES)
+def test_chunk64_tiles_vs_oracle_and_skip(dt, case):
+    """Every tile of the 64-channel-chunk kernel: sampled outputs against the
+    oracle (bias, residual, ReLU), and the skip path equal to the dense path
+    bit for bit on an input whose second image and first 64 channels are
+    zero (whole chunks skipped)."""
+    shape, rows = case
+    abi = _abi()
+    n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, g = shape
+    d = abi.conv_desc(n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, g, DT[dt])
+    assert abi.sparoa_conv2d_tiling(d, 0) == (rows, 64)
+    ho = (h + 2 * ph - dh * (kh - 1) - 1) // sh + 1
+    wo = (wd + 2 * pw - dw * (kw - 1) - 1) // sw + 1
+    seed = 900 + IG_SHAPES.index(case)
+    x = synth.relu_normal((n, h, wd, cin), dt, seed)
+    if n > 1:
+        x[1:] = 0
+    if cin >= 128:
+        x[..., :64] = 0
+    w = synth.he_normal((cout, kh, kw, cin), kh * kw * cin, dt, seed + 1)
+    b = synth.normal((cout,), dt, seed + 2)
+    r = synth.normal((n, ho, wo, cout), dt, seed + 3)
+    yd, _, _ = run_conv(x, w, shape, 0, bias=b, residual=r, act=1)
+    ys, ex, _ = run_conv(x, w, shape, 1, bias=b, residual=r, act=1)
+    assert torch.equal(yd, ys)
+    total = yd.numel()
+    rng = np.random.default_rng(seed)
+    idx = np.unique(np.concatenate([rng.integers(0, total, size=3000), [0, total - 1]]))
+    yr, ar = oracle.conv2d_at(x, w, idx, n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, g,
+                              bias=b, residual=r, act=1)
+    yg = yd.reshape(-1)[idx].float().numpy().astype(np.float64)
+    bound = RTOL[DT[dt]] * ar + SUBNORMAL_STEP[DT[dt]]
+    assert np.all(np.abs(yg - yr) <= bound), float(np.max(np.abs(yg - yr) - bound))
+    full = oracle.conv_executed_blocks(x, n, cin, h, wd, kh, kw, sh, sw, ph, pw, dh, dw, rows, 64)
+    assert ex == full
