@@ -27,6 +27,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -47,14 +49,17 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=20.0,
                    help="bound on the oracle CPU-baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--sparsity-thr", type=float, default=None,
-                   help="routing threshold; default: calibrated from forced-path timings")
+    p.add_argument("--thresholds", default=None,
+                   help='JSON {m: [sparsity_thr, intensity_thr]}; default: calibrated from the '
+                        'cold forced-path timings')
     p.add_argument("--cases-out", default=None, help="write the per-case table (JSON) here")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only run 5 plain device-to-device copies of MIB MiB and exit (the "
                         "reference kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
+    p.add_argument("--no-models", action="store_true",
+                   help="skip the per-model latency runs (ResNet-50, MobileNetV2, FFN stacks)")
     p.add_argument("--no-sweep", action="store_true",
-                   help="skip the forced-path and per-operator timings (needs --sparsity-thr): "
+                   help="skip the forced-path and per-operator timings (needs --thresholds): "
                         "only the step kernels run, e.g. under a profiler")
     p.add_argument("--mode", choices=("graph", "eager", "host"), default="graph",
                    help="graph: the executor call captured in a HIP graph, one replay per step; "
@@ -74,24 +79,27 @@ def case_list():
 
 def source_digest():
     h = hashlib.sha256()
-    for f in ("fc_bw.hip", "measure.hip"):
+    for f in ("fc_bw.hip", "measure.hip", "gemm.hip"):
         with open(os.path.join(ROOT, "paper_2511_19457_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def load_traffic(digest):
-    """HBM traffic per FC launch measured by rocprofv3 counters, if taken on
-    the current kernel source (profiles/fc_bw_kernel_fc_sweep_traffic.json)."""
-    path = os.path.join(ROOT, "profiles", "fc_bw_kernel_fc_sweep_traffic.json")
+def load_traffic(digest, family, alg_per_launch):
+    """HBM traffic per operator of one kernel family measured by rocprofv3
+    counters (profiles/fc_sweep_traffic.json), if taken on the current kernel
+    sources and on the same operators and paths (same algorithmic bytes per
+    operator)."""
+    path = os.path.join(ROOT, "profiles", "fc_sweep_traffic.json")
     try:
         with open(path) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("source_digest") != digest:
+    fam = t.get("families", {}).get(family, {})
+    if t.get("source_digest") != digest or fam.get("alg_bytes_per_launch") != alg_per_launch:
         return None
-    return t.get("bytes_per_launch")
+    return fam.get("bytes_per_launch")
 
 
 class Case:
@@ -125,11 +133,12 @@ def build_cases(abi, torch, synth, dev):
         abi.sparoa_fc_pack_weights(c.desc, w, c.wp)
         c.w = w                      # [n][k] for the MFMA paths
         c.inten = abi.sparoa_op_intensity_fc(c.desc)
-        fam_skip = abi.PATH_SKIP_BW if c.inten["intensity"] < INTENSITY_THR else abi.PATH_SKIP_MFMA
-        c.br, c.bc = abi.sparoa_fc_skip_block(c.desc, fam_skip)
+        # skip granularity of each kernel family; the mask fits either
+        c.block = {fam: abi.sparoa_fc_skip_block(c.desc, fam | 1)
+                   for fam in (abi.PATH_DENSE_BW, abi.PATH_DENSE_MFMA)}
         c.counts = torch.zeros(4, dtype=torch.int64, device=dev)
-        c.mask = torch.zeros(abi.sparoa_mask_words(m, K, c.br, c.bc), dtype=torch.int32,
-                             device=dev)
+        c.mask = torch.zeros(max(abi.sparoa_mask_words(m, K, br, bc) for br, bc in c.block.values()),
+                             dtype=torch.int32, device=dev)
         ws = max(abi.sparoa_fc_workspace_size(c.desc, p) for p in range(4))
         c.ws = torch.zeros(max(16, ws), dtype=torch.uint8, device=dev)
         c.y = torch.empty(m, N, dtype=torch.bfloat16, device=dev)
@@ -139,67 +148,171 @@ def build_cases(abi, torch, synth, dev):
     return cases
 
 
-def run_case(abi, c, s_thr, ev=None):
-    """One operator through the whole path; returns the routed path."""
-    counts = abi.sparoa_measure_sparsity_sync(c.x, c.m, K, c.br, c.bc, 0, c.counts, c.mask)
-    path = abi.sparoa_route(counts, c.inten, 0, s_thr, INTENSITY_THR)
-    w = c.wp if path & 2 else c.w
-    if ev is not None:
-        ev[0].record()
+def family(c):
+    """Kernel family the operator's intensity threshold selects."""
+    return abi_mod().PATH_DENSE_BW if c.inten["intensity"] < c.c_thr else abi_mod().PATH_DENSE_MFMA
+
+
+def abi_mod():
+    from paper_2511_19457_amd import abi
+    return abi
+
+
+def run_case(abi, c):
+    """One operator through the whole path with the host route (counts read
+    back, sparoa_route, fixed-path call); returns the routed path."""
+    br, bc = c.block[family(c)]
+    counts = abi.sparoa_measure_sparsity_sync(c.x, c.m, K, br, bc, 0, c.counts, c.mask)
+    path = abi.sparoa_route(counts, c.inten, 0, c.s_thr, c.c_thr)
+    w = c.wp if abi.sparoa_fc_uses_packed(c.desc, path) else c.w
     abi.sparoa_fc(c.desc, path, c.x, w, None, None, abi.ACT_NONE, c.mask if path & 1 else None,
                   c.y, c.ws)
-    if ev is not None:
-        ev[1].record()
     c.counts_host = counts
     return path
 
 
-def forced_times(abi, torch, c, paths, reps=20, rounds=3):
-    """Duration (us) of the FC kernel on each forced path: `reps` back-to-back
-    launches between one pair of HIP events, best of `rounds` (the weights
-    stay cache-resident here, so these read low next to the cold step)."""
-    out = {}
-    abi.sparoa_measure_sparsity_sync(c.x, c.m, K, c.br, c.bc, 0, c.counts, c.mask)
+def forced_times(abi, torch, cases, paths, rounds=3):
+    """Duration (us) of the FC kernel of every case on each forced path, with
+    cold weights: one launch per case in case order (each case streams its
+    own 32 MiB of weights, so the 24 cases overflow the Infinity Cache), a
+    pair of HIP events around each launch, best of `rounds`."""
+    for c in cases:
+        c.forced = {}
+        c.rho_b = {}
     for p in paths:
-        w = c.wp if abi.sparoa_fc_uses_packed(c.desc, p) else c.w
-        if w is None:
-            continue
-        best = None
+        fam = p & 2
+        for c in cases:     # the mask at this family's skip granularity (untimed)
+            br, bc = c.block[fam]
+            st = abi.sparoa_measure_sparsity_sync(c.x, c.m, K, br, bc, 0, c.counts, c.mask)
+            c.rho_b[fam] = st["zero_blocks"] / st["num_blocks"]
+        best = [None] * len(cases)
         for _ in range(rounds):
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in cases]
+            for c, (e0, e1) in zip(cases, ev):
+                w = c.wp if abi.sparoa_fc_uses_packed(c.desc, p) else c.w
+                e0.record()
+                abi.sparoa_fc(c.desc, p, c.x, w, None, None, abi.ACT_NONE,
+                              c.mask if p & 1 else None, c.y, c.ws)
+                e1.record()
+            torch.cuda.synchronize()
+            for i, (e0, e1) in enumerate(ev):
+                t = e0.elapsed_time(e1) * 1e3
+                best[i] = t if best[i] is None else min(best[i], t)
+        for c, t in zip(cases, best):
+            c.forced[p] = t
+
+
+def path_times(abi, torch, cases, rounds=3):
+    """Duration (us) of each operator's whole path (sparoa_fc_measured:
+    measure, route and FC) with cold weights: one call per case in case
+    order between a pair of HIP events, best of `rounds`."""
+    best = [None] * len(cases)
+    for _ in range(rounds):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in cases]
+        for c, (e0, e1) in zip(cases, ev):
+            e0.record()
+            abi.sparoa_fc_measured(c.desc, c.s_thr, c.c_thr, abi.ROUTE_BLOCK, c.x, c.w, c.wp,
+                                   None, None, abi.ACT_NONE, c.counts, c.mask, c.y, c.ws,
+                                   c.path_dev)
+            e1.record()
+        torch.cuda.synchronize()
+        for i, (e0, e1) in enumerate(ev):
+            t = e0.elapsed_time(e1) * 1e3
+            best[i] = t if best[i] is None else min(best[i], t)
+    for c, t in zip(cases, best):
+        c.path_us = t
+
+
+def alg_bytes(c, path, mask_host):
+    """Algorithmic HBM bytes of one operator's FC: x, y and the weight rows the
+    path must read.  Bandwidth skip path: the rows of input columns that are
+    nonzero in some row (mask at block (m, 1)).  MFMA skip path: the 64-row
+    channel chunks in which some row of the (single, m <= 64) row tile is
+    nonzero (mask at block (1, 8)).  Dense paths: all K rows."""
+    rows = K
+    if path & 1:
+        bits = np.unpackbits(mask_host.view(np.uint8), bitorder="little")
+        if path & 2:
+            rows = int(bits[:K].sum())
+        else:
+            per_row = bits[:c.m * (K // 8)].reshape(c.m, K // 8).any(axis=0)
+            rows = int(per_row.reshape(K // 64, 8).any(axis=1).sum()) * 64
+    return 2 * (c.m * K + c.m * N) + 2 * rows * N
+
+
+def model_latencies(abi, torch, synth, reps=10):
+    """Per-model latency at one GPU: the whole stack (measure, device-side
+    route, execute, glue per layer) captured once in a HIP graph and replayed;
+    HIP events around each replay, median over `reps`.  Weights He-normal,
+    inputs N(0, 1) (seeded)."""
+    from paper_2511_19457_amd import stacks
+    from paper_2511_19457_amd.driver import Engine
+    out = {}
+    specs = [("resnet50_b1_bf16", stacks.resnet50(1), torch.bfloat16),
+             ("resnet50_b8_bf16", stacks.resnet50(8), torch.bfloat16),
+             ("resnet50_b32_bf16", stacks.resnet50(32), torch.bfloat16),
+             ("mobilenet_v2_b32_fp16", stacks.mobilenet_v2(32), torch.float16),
+             ("ffn12_2048x768_fp16", stacks.ffn(), torch.float16)]
+    for name, layers, dt in specs:
+        eng = Engine(layers, dt, "cuda", seed=synth.seed_for(3, 0), sparsity_thr=0.5)
+        x = synth.normal(stacks.input_shape(layers), dt, synth.seed_for(3, 1)).cuda()
+        eng.forward_routed(x)                       # warm-up, eager
+        torch.cuda.synchronize()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(cap):
+            with torch.cuda.graph(g):
+                eng.forward_routed(x)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record()
-            for _ in range(reps):
-                abi.sparoa_fc(c.desc, p, c.x, w, None, None, abi.ACT_NONE,
-                              c.mask if p & 1 else None, c.y, c.ws)
+            g.replay()
             e1.record()
             e1.synchronize()
-            t = e0.elapsed_time(e1) * 1e3 / reps
-            best = t if best is None else min(best, t)
-        out[p] = best
+            ts.append(e0.elapsed_time(e1))
+        ts.sort()
+        flops = sum(2 * eng.st[i]["inten"]["macs"] for i, L in enumerate(layers)
+                    if L.kind != "maxpool")
+        ms = ts[len(ts) // 2]
+        out[name] = dict(ms=round(ms, 3), dense_equiv_tflops=round(flops / (ms * 1e-3) / 1e12, 2),
+                         layers=len(layers))
+        print(f"bench: model {name}: {ms:.3f} ms", file=sys.stderr, flush=True)
+        del g, eng, x
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
     return out
 
 
-def path_time(abi, torch, c, s_thr, reps=20):
-    """Duration (us) of one operator's whole path (sparoa_fc_measured:
-    measure, route and FC), `reps` calls back to back between one pair of
-    HIP events."""
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        abi.sparoa_fc_measured(c.desc, s_thr, INTENSITY_THR, abi.ROUTE_BLOCK, c.x, c.w, c.wp,
-                               None, None, abi.ACT_NONE, c.counts, c.mask, c.y, c.ws, c.path_dev)
-    e1.record()
-    e1.synchronize()
-    return e0.elapsed_time(e1) * 1e3 / reps
-
-
-def alg_bytes(c, path, nonzero_cols):
-    """Algorithmic HBM bytes of one FC launch: x, y and the weight rows the
-    path must read (all of them, or only the nonzero input columns')."""
-    rows = nonzero_cols if path & 1 else K
-    return 2 * (c.m * K + c.m * N) + 2 * rows * N
+def calibrate(abi, cases):
+    """Thresholds per operator class (m), from the cold forced-path timings:
+    the kernel family whose dense path is faster (intensity threshold: the
+    class's own intensity when the MFMA family wins, the bf16 ridge point
+    otherwise), and the smallest block sparsity at or above which that
+    family's skip path beats its dense path in every case of the class (1.0
+    when it never does)."""
+    out = {}
+    for m in M_LIST:
+        cs = [c for c in cases if c.m == m]
+        bw = sum(c.forced[abi.PATH_DENSE_BW] for c in cs)
+        mf = sum(c.forced[abi.PATH_DENSE_MFMA] for c in cs)
+        fam = abi.PATH_DENSE_MFMA if mf < bw else abi.PATH_DENSE_BW
+        c_thr = cs[0].inten["intensity"] if fam == abi.PATH_DENSE_MFMA else INTENSITY_THR
+        pts = sorted((c.rho_b[fam], c.forced[fam | 1] < c.forced[fam]) for c in cs)
+        s_thr = 1.0
+        for rb, wins in reversed(pts):
+            if not wins:
+                break
+            s_thr = rb
+        out[m] = (max(s_thr, 1e-9), c_thr)
+    return out
 
 
 def cpu_baseline_timed(cases, budget_s):
@@ -213,11 +326,12 @@ def cpu_baseline_timed(cases, budget_s):
     for c in cases:
         w_cpu = synth.normal((N, K), "bf16", c.seed_w, std=1.0 / 64.0)   # not timed
         t1 = time.perf_counter()
-        st = oracle.measure(c.x_cpu, c.m, K, c.m, 1)
+        br, bc = c.block[family(c)]
+        st = oracle.measure(c.x_cpu, c.m, K, br, bc)
         path = oracle.route(st["zeros"], st["numel"], st["zero_blocks"], st["num_blocks"],
-                            c.inten["intensity"], 0, 0.5, INTENSITY_THR)
+                            c.inten["intensity"], 0, c.s_thr, c.c_thr)
         oracle.fc(c.x_cpu, w_cpu, c.m, K, N,
-                  skip_mask=st["mask"] if path & 1 else None, skip_rows=c.m, skip_cols=1)
+                  skip_mask=st["mask"] if path & 1 else None, skip_rows=br, skip_cols=bc)
         elapsed += time.perf_counter() - t1
         flops += 2 * c.m * K * N
         done.append(f"m{c.m}/rho{c.rho}/{c.pattern}")
@@ -253,55 +367,51 @@ def main():
     print("bench: building 24 FC operators (packing weights)", file=sys.stderr, flush=True)
     cases = build_cases(abi, torch, synth, dev)
 
-    # Forced-path timings per case (untimed phase): the sparsity sweep of the
-    # metric, and the data the routing threshold is calibrated from.
-    if args.no_sweep and args.sparsity_thr is None:
-        print("bench.py: --no-sweep needs --sparsity-thr", file=sys.stderr)
+    # Forced-path timings per case (untimed phase, cold weights): the sparsity
+    # sweep of the metric, and the data the thresholds are calibrated from.
+    paths_swept = (abi.PATH_DENSE_BW, abi.PATH_SKIP_BW, abi.PATH_DENSE_MFMA, abi.PATH_SKIP_MFMA)
+    if args.thresholds is None and args.no_sweep:
+        print("bench.py: --no-sweep needs --thresholds", file=sys.stderr)
         sys.exit(2)
-    if not args.no_sweep:
-        print("bench: forced-path sweep", file=sys.stderr, flush=True)
-    for c in cases:
-        c.forced = {} if args.no_sweep else forced_times(
-            abi, torch, c, (abi.PATH_DENSE_BW, abi.PATH_SKIP_BW, abi.PATH_DENSE_MFMA))
-    if args.sparsity_thr is None:
-        # smallest block sparsity above which the skip path wins in every case
-        pts = []
-        for c in cases:     # forced_times left the counts at the skip block in c.counts
-            st = c.counts.cpu().tolist()
-            pts.append((st[2] / st[3], c.forced[abi.PATH_SKIP_BW] < c.forced[abi.PATH_DENSE_BW]))
-        pts.sort()
-        s_thr = 1.0
-        for rb, wins in reversed(pts):
-            if not wins:
-                break
-            s_thr = rb
-        s_thr = max(s_thr, 1e-9)
+    if args.no_sweep:
+        for c in cases:
+            c.forced, c.rho_b = {}, {}
     else:
-        s_thr = args.sparsity_thr
+        print("bench: forced-path sweep", file=sys.stderr, flush=True)
+        forced_times(abi, torch, cases, paths_swept)
+    thresholds = calibrate(abi, cases) if args.thresholds is None else \
+        {int(k): tuple(v) for k, v in json.loads(args.thresholds).items()}
+    for c in cases:
+        c.s_thr, c.c_thr = thresholds[c.m]
+    print(f"bench: warmup {args.warmup} steps, thresholds per m (sparsity, intensity): "
+          f"{thresholds}", file=sys.stderr, flush=True)
 
-    print(f"bench: warmup {args.warmup} steps, sparsity threshold {s_thr:.4g}", file=sys.stderr,
-          flush=True)
-    # the executor's batch: one sparoa_fc_measured per operator
-    op_array = abi.fc_op_array([
-        abi.fc_op(c.desc, c.x, c.w, c.wp, None, None, abi.ACT_NONE, c.counts, c.mask, c.y, c.ws,
-                  c.path_dev) for c in cases])
+    # the executor's batch: one sparoa_fc_measured per operator, own thresholds
+    def batch(sel):
+        return abi.fc_op_array([
+            abi.fc_op(c.desc, c.x, c.w, c.wp, None, None, abi.ACT_NONE, c.counts, c.mask, c.y,
+                      c.ws, c.path_dev, (c.s_thr, c.c_thr, abi.ROUTE_BLOCK)) for c in sel])
+    op_array = batch(cases)
 
     def executor_step():
-        abi.sparoa_fc_ops_run(op_array, s_thr, INTENSITY_THR)
+        abi.sparoa_fc_ops_run(op_array)
 
     # eager reference outputs: the graph replays must reproduce them
     executor_step()
     torch.cuda.synchronize()
     y_ref = [c.y.clone() for c in cases]
-    graph = None
-    if args.mode == "graph":
+
+    def capture(fn):
         cap = torch.cuda.Stream()                   # default priority
         cap.wait_stream(torch.cuda.current_stream())
-        graph = torch.cuda.CUDAGraph()
+        g = torch.cuda.CUDAGraph()
         with torch.cuda.stream(cap):
-            with torch.cuda.graph(graph):
-                executor_step()
+            with torch.cuda.graph(g):
+                fn()
         torch.cuda.synchronize()
+        return g
+
+    graph = capture(executor_step) if args.mode == "graph" else None
 
     def step():
         if args.mode == "graph":
@@ -310,7 +420,7 @@ def main():
             executor_step()
         else:
             for c in cases:
-                run_case(abi, c, s_thr)
+                run_case(abi, c)
 
     for _ in range(args.warmup):
         step()
@@ -328,13 +438,15 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     paths = [int(c.path_dev.item()) for c in cases] if args.mode != "host" else \
-        [run_case(abi, c, s_thr) for c in cases]
+        [run_case(abi, c) for c in cases]
     torch.cuda.synchronize()
+    masks = []
     for i, c in enumerate(cases):
         c.counts_host = dict(zip(("zeros", "numel", "zero_blocks", "num_blocks"),
                                  c.counts.cpu().tolist()))
+        masks.append(c.mask.cpu().numpy())
         # the device decision must be the host rule's on the same counts
-        assert paths[i] == abi.sparoa_route(c.counts_host, c.inten, 0, s_thr, INTENSITY_THR)
+        assert paths[i] == abi.sparoa_route(c.counts_host, c.inten, 0, c.s_thr, c.c_thr)
         assert torch.equal(c.y, y_ref[i]), f"operator {i}: step output differs from eager run"
     step_s = (t1 - t0) / args.steps
     print(f"bench: timed {args.steps} steps, {step_s * 1e3:.3f} ms/step", file=sys.stderr,
@@ -342,40 +454,72 @@ def main():
 
     flops_step = sum(2 * c.m * K * N for c in cases)
     value = flops_step / step_s / 1e12
-    # GPU time of a step from its events: 24 kernel launches back to back
     step_gpu_us = sum(a.elapsed_time(b) for a, b in ev) * 1e3 / args.steps
-    for c in cases:   # per-operator view: the whole path of one operator, back to back
-        c.path_us = None if args.no_sweep else path_time(abi, torch, c, s_thr)
+    if args.no_sweep:
+        for c in cases:
+            c.path_us = None
+    else:           # per-operator view: the whole path of one operator, cold weights
+        path_times(abi, torch, cases)
     table = []
-    tot_bytes = 0
     for i, c in enumerate(cases):
         ch = c.counts_host
-        nz_cols = ch["num_blocks"] - ch["zero_blocks"]
-        b = alg_bytes(c, paths[i], nz_cols)
-        tot_bytes += b
+        c.alg = alg_bytes(c, paths[i], masks[i])
         row = dict(m=c.m, rho=c.rho, pattern=c.pattern, rho_e=round(ch["zeros"] / ch["numel"], 4),
                    rho_b=round(ch["zero_blocks"] / ch["num_blocks"], 4),
-                   path=abi.PATH_NAMES[paths[i]], alg_bytes=b)
+                   path=abi.PATH_NAMES[paths[i]], alg_bytes=c.alg)
         if c.path_us is not None:
-            row.update(us=round(c.path_us, 2), gbps=round(b / c.path_us / 1e3, 1),
+            row.update(us=round(c.path_us, 2), gbps=round(c.alg / c.path_us / 1e3, 1),
                        dense_equiv_tflops=round(2 * c.m * K * N / c.path_us / 1e6, 2))
-        for p, name in ((abi.PATH_DENSE_BW, "dense_bw_us"), (abi.PATH_SKIP_BW, "skip_bw_us"),
-                        (abi.PATH_DENSE_MFMA, "dense_mfma_us")):
+        for p in paths_swept:
             if p in c.forced:
-                row[name] = round(c.forced[p], 2)
+                row[abi.PATH_NAMES[p] + "_us"] = round(c.forced[p], 2)
         table.append(row)
-    launches = len(cases)
-    achieved = tot_bytes / (step_gpu_us * 1e-6) / 1e9
+    tot_bytes = sum(c.alg for c in cases)
+
+    # Roofline of each kernel family's launches: the step's operators of one
+    # family replayed as their own HIP graph, events around every replay.
+    fam_rows = {}
+    for fam in (abi.PATH_DENSE_BW, abi.PATH_DENSE_MFMA):
+        sel = [c for c in cases if family(c) == fam]
+        if not sel:
+            continue
+        arr = batch(sel)
+        g = capture(lambda: abi.sparoa_fc_ops_run(arr))
+        g.replay()
+        torch.cuda.synchronize()
+        reps = max(10, args.steps)
+        evf = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(reps)]
+        for e0, e1 in evf:
+            e0.record()
+            g.replay()
+            e1.record()
+        torch.cuda.synchronize()
+        us = sum(a.elapsed_time(b) for a, b in evf) * 1e3 / reps
+        fam_rows[fam] = (sel, us)
+    dominant = max(fam_rows, key=lambda f: fam_rows[f][1])
     digest = source_digest()
-    traffic = load_traffic(digest)
-    roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
-                    kernel="fc_bw_kernel (self-measuring)",
-                    alg_bytes_per_launch=int(tot_bytes / launches),
-                    avg_launch_us=round(step_gpu_us / launches, 3),
-                    timing="HIP events around every timed step (24 launches, gaps between "
-                           "launches included)",
+
+    def roofline_of(fam):
+        sel, us = fam_rows[fam]
+        nb = sum(c.alg for c in sel)
+        achieved = nb / (us * 1e-6) / 1e9
+        per_launch = int(nb / len(sel))
+        if fam == abi.PATH_DENSE_BW:
+            kernel = "fc_bw_kernel (self-measuring; one launch per operator)"
+        else:
+            kernel = "igemm_kernel (one measurement, GEMM and split-K reduction launch per operator)"
+        traffic = load_traffic(digest, abi.PATH_NAMES[fam], per_launch)
+        return dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic, kernel=kernel,
+                    operators=len(sel), alg_bytes_per_launch=per_launch,
+                    avg_launch_us=round(us / len(sel), 3),
+                    timing="this family's operators of the step replayed as one HIP graph, HIP "
+                           "events around every replay (gaps between launches included)",
                     source_digest=digest)
+
+    roofline = roofline_of(dominant)
+    others = {abi.PATH_NAMES[f]: roofline_of(f) for f in fam_rows if f != dominant}
 
     line = dict(
         metric=METRIC, value=round(value, 3), unit="TFLOP/s", n_gpus=1, steps=args.steps,
@@ -385,13 +529,16 @@ def main():
                              "0/0.5/0.8/0.95 i.i.d. or 16x16 blocks) x w [4096,4096] bf16, "
                              "one weight matrix per operator; measure+route+execute each",
                     global_batch=sum(M_LIST) * len(RHO_LIST) * len(PATTERNS),
-                    sparsity_thr=s_thr, intensity_thr=INTENSITY_THR, route_mode="block",
-                    issue=args.mode),
+                    thresholds_per_m={str(k): v for k, v in thresholds.items()},
+                    route_mode="block", issue=args.mode),
         hbm_gbps_step=round(tot_bytes / step_s / 1e9, 1),
         step_gpu_us=round(step_gpu_us, 2),
         roofline=roofline,
+        roofline_other_families=others,
         sweep=table,
     )
+    if not args.no_models:
+        line["models"] = model_latencies(abi, torch, synth)
     if not args.no_cpu_baseline:
         print("bench: oracle CPU baseline", file=sys.stderr, flush=True)
         flops, elapsed, done = cpu_baseline_timed(cases, args.cpu_seconds)

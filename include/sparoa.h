@@ -326,7 +326,9 @@ sparoa_status sparoa_fc_measured(const sparoa_fc_desc *desc, const sparoa_thresh
  * events are given, so a caller may capture it in a HIP graph.  Per op:
  * counts (one sparoa_counts) and mask (sparoa_mask_words words for that
  * granularity) are device scratch; path (nullable) receives the path taken;
- * w_nk / w_packed as for sparoa_fc_routed.
+ * w_nk / w_packed as for sparoa_fc_routed; thr holds the op's own
+ * thresholds (the paper's predictor emits a threshold pair per operator,
+ * Section 3, Eq. 5), used when the call's thr argument is NULL.
  * events (nullable): 2n hipEvent_t; events[2i] / events[2i+1] are recorded
  * on `stream` right before op i's first kernel / after its last kernel.
  * Stops at the first failing op and returns its status.
@@ -341,7 +343,9 @@ typedef struct {
   void *workspace;
   size_t ws_bytes;
   uint32_t *path;
+  sparoa_thresholds thr;
 } sparoa_fc_op;
+/* thr: thresholds for every op, or NULL to use each op's own. */
 sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr,
                                 hipEvent_t *events, hipStream_t stream);
 

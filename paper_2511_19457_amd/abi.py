@@ -69,18 +69,18 @@ class Intensity(ctypes.Structure):
         return dict(macs=self.macs, flops=self.flops, bytes=self.bytes, intensity=self.intensity)
 
 
+class Thresholds(ctypes.Structure):
+    _fields_ = [("sparsity_thr", ctypes.c_double), ("intensity_thr", ctypes.c_double),
+                ("mode", ctypes.c_int)]
+
+
 class FcOp(ctypes.Structure):
     _fields_ = [("desc", FcDesc), ("x", ctypes.c_void_p), ("w_nk", ctypes.c_void_p),
                 ("w_packed", ctypes.c_void_p), ("bias", ctypes.c_void_p),
                 ("residual", ctypes.c_void_p), ("act", ctypes.c_int),
                 ("counts", ctypes.c_void_p), ("mask", ctypes.c_void_p), ("y", ctypes.c_void_p),
                 ("workspace", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t),
-                ("path", ctypes.c_void_p)]
-
-
-class Thresholds(ctypes.Structure):
-    _fields_ = [("sparsity_thr", ctypes.c_double), ("intensity_thr", ctypes.c_double),
-                ("mode", ctypes.c_int)]
+                ("path", ctypes.c_void_p), ("thr", Thresholds)]
 
 
 def _load():
@@ -382,23 +382,27 @@ def sparoa_fc_uses_packed(desc, path):
 
 
 def fc_op(desc, x, w_nk, w_packed, bias, residual, act, counts, mask, y, workspace=None,
-          path=None):
-    """One entry of a sparoa_fc_ops_run batch (pointers captured now)."""
+          path=None, thresholds=None):
+    """One entry of a sparoa_fc_ops_run batch (pointers captured now).
+    thresholds: (sparsity_thr, intensity_thr, mode) of this op, used when the
+    batch call passes no thresholds of its own."""
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    t = Thresholds(*(thresholds or (0.5, 315.0, ROUTE_BLOCK)))
     return FcOp(desc, _ptr(x), _ptr(w_nk), _ptr(w_packed), _ptr(bias), _ptr(residual), act,
-                _ptr(counts), _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes, _ptr(path))
+                _ptr(counts), _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes, _ptr(path), t)
 
 
 def fc_op_array(ops):
     return (FcOp * len(ops))(*ops)
 
 
-def sparoa_fc_ops_run(op_array, sparsity_thr, intensity_thr, mode=ROUTE_BLOCK, events=None,
-                      stream=None):
-    """Runs a batch built by fc_op_array.  events: flat list of 2n recorded
-    torch.cuda.Event objects (or None)."""
-    t = Thresholds(sparsity_thr, intensity_thr, mode)
+def sparoa_fc_ops_run(op_array, sparsity_thr=None, intensity_thr=None, mode=ROUTE_BLOCK,
+                      events=None, stream=None):
+    """Runs a batch built by fc_op_array with the given thresholds, or with
+    each op's own when sparsity_thr is None.  events: flat list of 2n
+    recorded torch.cuda.Event objects (or None)."""
+    t = None if sparsity_thr is None else ctypes.byref(Thresholds(sparsity_thr, intensity_thr, mode))
     ev = None
     if events is not None:
         ev = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
-    _check(_L.sparoa_fc_ops_run(op_array, len(op_array), ctypes.byref(t), ev, _stream(stream)))
+    _check(_L.sparoa_fc_ops_run(op_array, len(op_array), t, ev, _stream(stream)))

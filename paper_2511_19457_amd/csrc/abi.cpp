@@ -548,7 +548,12 @@ sparoa_status sparoa_fc_measured(const sparoa_fc_desc *d, const sparoa_threshold
 namespace {
 sparoa_status check_ops(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr) {
   if (!ops || n < 0) return fail(SPAROA_ERR_INVALID_ARG, "fc_ops: null ops or n < 0");
-  return check_thr(thr);
+  if (thr) return check_thr(thr);
+  for (int64_t i = 0; i < n; ++i) {
+    sparoa_status st = check_thr(&ops[i].thr);
+    if (st != SPAROA_OK) return st;
+  }
+  return SPAROA_OK;
 }
 }  // namespace
 
@@ -560,7 +565,8 @@ sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa
   for (int64_t i = 0; i < n; ++i) {
     const sparoa_fc_op &o = ops[i];
     if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i], stream));
-    if ((st = sparoa_fc_measured(&o.desc, thr, o.x, o.w_nk, o.w_packed, o.bias, o.residual, o.act,
+    if ((st = sparoa_fc_measured(&o.desc, thr ? thr : &o.thr, o.x, o.w_nk, o.w_packed, o.bias,
+                                 o.residual, o.act,
                                  o.counts, o.mask, o.y, o.workspace, o.ws_bytes, o.path,
                                  stream)) != SPAROA_OK)
       return st;

@@ -154,6 +154,15 @@ class Engine:
                                  st["w"], st.get("wp"), None, res, L.act, st["mask"], y, st["ws"],
                                  st["path"])
 
+    def forward_routed(self, x):
+        """The whole stack with device-side routing and no host synchronisation
+        (stream-ordered; safe to capture in a HIP graph).  Returns the output
+        activation tensor."""
+        self.acts[0] = x
+        for i in range(len(self.layers)):
+            self.run_layer_routed(i)
+        return self.acts[len(self.layers)]
+
     def records_from_device(self):
         """Counts and paths of the last routed run, read back after the fact."""
         recs = []

@@ -269,3 +269,52 @@ def test_fc_ops_run_in_a_hip_graph_equals_eager():
             assert torch.equal(b["y"], y), rep
             assert int(b["path"].item()) == p, rep
             assert torch.equal(b["counts"], c) and torch.equal(b["mask"], mk), rep
+
+
+def test_fc_ops_run_uses_each_ops_own_thresholds():
+    """With no batch thresholds, every op routes with its own (sparsity,
+    intensity) pair: the path equals the host rule on that op's counts, and
+    an intensity threshold at the op's own intensity sends it to the MFMA
+    family (measured at that family's granularity)."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    ops, bufs = [], []
+    specs = [(8, 0.9, "block", (0.5, 315.0)), (8, 0.9, "block", (0.99, 315.0)),
+             (64, 0.9, "block", (0.5, None)), (1, 0.95, "iid", (0.2, 315.0))]
+    for i, (m, rho, pat, (s_thr, c_thr)) in enumerate(specs):
+        k, n = 1024, 256
+        d = abi.fc_desc(m, k, n, abi.BF16)
+        inten = abi.sparoa_op_intensity_fc(d)
+        c_thr = inten["intensity"] if c_thr is None else c_thr
+        words = max(abi.sparoa_mask_words(m, k, *abi.sparoa_fc_skip_block(d, f))
+                    for f in (abi.PATH_SKIP_BW, abi.PATH_SKIP_MFMA))
+        b = dict(d=d, x=synth.sparse_matrix(m, k, rho, pat, "bf16", 800 + i).to(dev),
+                 w=synth.normal((n, k), "bf16", 810 + i, std=k ** -0.5).to(dev),
+                 wp=torch.empty(abi.sparoa_fc_packed_bytes(d) // 2, dtype=torch.bfloat16,
+                                device=dev),
+                 counts=torch.zeros(4, dtype=torch.int64, device=dev),
+                 mask=torch.zeros(words, dtype=torch.int32, device=dev),
+                 y=torch.zeros(m, n, dtype=torch.bfloat16, device=dev),
+                 ws=torch.zeros(max(16, max(abi.sparoa_fc_workspace_size(d, p) for p in range(4))),
+                                dtype=torch.uint8, device=dev),
+                 path=torch.full((1,), -1, dtype=torch.int32, device=dev), thr=(s_thr, c_thr),
+                 inten=inten)
+        abi.sparoa_fc_pack_weights(d, b["w"], b["wp"])
+        bufs.append(b)
+        ops.append(abi.fc_op(d, b["x"], b["w"], b["wp"], None, None, abi.ACT_NONE, b["counts"],
+                             b["mask"], b["y"], b["ws"], b["path"],
+                             (s_thr, c_thr, abi.ROUTE_BLOCK)))
+    arr = abi.fc_op_array(ops)
+    abi.sparoa_fc_ops_run(arr)
+    torch.cuda.synchronize()
+    for b in bufs:
+        m, k = b["x"].shape
+        fam = abi.PATH_SKIP_BW if b["inten"]["intensity"] < b["thr"][1] else abi.PATH_SKIP_MFMA
+        ref = oracle.measure(b["x"].cpu(), m, k, *abi.sparoa_fc_skip_block(b["d"], fam))
+        assert b["counts"].cpu().tolist() == [ref["zeros"], ref["numel"], ref["zero_blocks"],
+                                              ref["num_blocks"]]
+        want = oracle.route(ref["zeros"], ref["numel"], ref["zero_blocks"], ref["num_blocks"],
+                            b["inten"]["intensity"], 0, b["thr"][0], b["thr"][1])
+        assert int(b["path"].item()) == want
+    assert int(bufs[2]["path"].item()) & 2 == 0          # m = 64 sent to the MFMA family
+    assert int(bufs[0]["path"].item()) != int(bufs[1]["path"].item())
