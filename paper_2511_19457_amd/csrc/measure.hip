@@ -253,6 +253,58 @@ __global__ __launch_bounds__(kLanebitThreads) void measure_lanebit(const char *_
   wg_commit<NT>(zeros, nonzero, counts, nullptr);
 }
 
+// The lanebit layout measured by one work-group that also writes all four
+// counts (no init launch, no atomics): for small tensors, where two launches
+// cost more than the pass.  Each wave reduces its slots in registers; the
+// waves' sums meet in LDS.
+template <int ESZ, int V>
+__global__ __launch_bounds__(1024) void measure_lanebit_wg(const char *__restrict__ x,
+                                                          int64_t items, int64_t words,
+                                                          uint32_t *__restrict__ mask,
+                                                          sparoa_counts *counts) {
+  constexpr int NT = 1024, U = 8;
+  __shared__ unsigned long long part[2][NT / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint64_t zeros = 0, nonzero = 0;
+  for (int64_t base = 0; base < items; base += (int64_t)NT * U) {
+    uint32_t nz[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {  // unconditional loads, masked past the end
+      const int64_t item = base + u * NT + threadIdx.x;
+      nz[u] = nonzero_bits<ESZ, V>(x + min(item, items - 1) * 16);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t w0 = (base + u * NT + (threadIdx.x & ~63)) >> 5;
+      const bool valid = base + u * NT + threadIdx.x < items;
+      const uint32_t b = valid ? nz[u] : 0u;
+      zeros += valid ? (uint64_t)(V - __popc(b)) : 0ull;
+      const uint64_t bal = __ballot(b != 0u);
+      if (lane == 0 && w0 < words) mask[w0] = (uint32_t)bal;
+      if (lane == 32 && w0 + 1 < words) mask[w0 + 1] = (uint32_t)(bal >> 32);
+      nonzero += lane == 0 ? (uint64_t)__popcll(bal) : 0ull;
+    }
+  }
+  const uint64_t wz = wave_sum(zeros), wn = wave_sum(nonzero);
+  if (lane == 0) {
+    part[0][wave] = wz;
+    part[1][wave] = wn;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long z = 0, n = 0;
+#pragma unroll
+    for (int i = 0; i < NT / 64; ++i) {
+      z += part[0][i];
+      n += part[1][i];
+    }
+    counts->zeros = z;
+    counts->numel = (uint64_t)items * V;
+    counts->zero_blocks = (uint64_t)items - n;
+    counts->num_blocks = (uint64_t)items;
+  }
+}
+
 // Column strips: a single block row covering all rows, one column per block
 // (the "column is zero in every row" bitmap).  A work-group owns 64 column
 // groups (64 V columns = 2 V whole bitmap words); its 4 waves take every
@@ -412,6 +464,17 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
   const bool lanebit = want_mask && vec && br == 1 && bc == vw && !per_sample;
   const bool strips = want_mask && vec && bc == 1 && !per_sample && br >= rows;
 
+  if (lanebit && rows * (cols / vw) <= 4096) {  // one work-group measures it all
+    const int64_t items = rows * (cols / vw);
+    if (esz == 2)
+      hipLaunchKernelGGL((measure_lanebit_wg<2, 8>), dim3(1), dim3(1024), 0, stream,
+                         static_cast<const char *>(x), items, words, mask, counts);
+    else
+      hipLaunchKernelGGL((measure_lanebit_wg<4, 4>), dim3(1), dim3(1024), 0, stream,
+                         static_cast<const char *>(x), items, words, mask, counts);
+    SPAROA_LAUNCH_CHECK("measure_lanebit_wg");
+    return SPAROA_OK;
+  }
   if (strips && cols / vw <= 16 * 64) {  // one work-group measures it all
     if (esz == 2)
       hipLaunchKernelGGL((measure_strips_wg<2, 8>), dim3(1), dim3(1024), 0, stream,
