@@ -134,24 +134,45 @@ __global__ __launch_bounds__(kThreads) void depthwise_kernel(DwArgs a) {
   }
 }
 
+// Division by a run-time constant through a multiply-high (Granlund and
+// Montgomery, 1994): for 0 <= n < 2^31 and 1 <= d < 2^31,
+// n / d == (umulhi(n, m) + n) >> l with l = ceil(log2 d) and
+// m = floor(2^32 (2^l - d) / d) + 1.
+struct FastDiv {
+  uint32_t d, m, l;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;
+  const uint64_t m = ((1ull << 32) * ((1ull << l) - d)) / d + 1;
+  return FastDiv{d, (uint32_t)m, l};
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv &f) {
+  return (__umulhi(n, f.m) + n) >> f.l;
+}
+
 // 3x3 depthwise, padding 1, stride S in both directions, 16-byte channel
-// vectors.  An item is (n, oh, run of kRun3 output pixels, channel vector);
+// vectors.  An item is (n, oh, run of run3<S>() output pixels, channel vector);
 // the grid stride is a multiple of the channel-vector count, so a thread
 // keeps one channel vector for its whole life and loads its 9 x V weights
 // once (nine 16-byte loads: w[c][3][3] is contiguous over the V channels).
 // Per item, the 3 x NC input vectors the run needs are loaded unconditionally
 // (clamped addresses, zeroed outside the image) so they are all in flight
 // at once; each is decoded once and feeds every (output, tap) pair that
-// uses it.
-constexpr int kRun3 = 4;
+// uses it.  Run length: 4 outputs over 6 input columns at stride 1; 2 outputs
+// over 5 columns at stride 2 (more lanes in flight, measured faster there).
+template <int S>
+constexpr int run3() { return S == 1 ? 4 : 2; }
 
 template <int DT, int S>
-__global__ __launch_bounds__(kThreads) void dw3x3_kernel(DwArgs a) {
+__global__ __launch_bounds__(kThreads) void dw3x3_kernel(DwArgs a, FastDiv fcv, FastDiv fruns, FastDiv fho) {
   using E = Elem<DT>;
   using raw = typename E::raw;
   constexpr int ESZ = E::size;
   constexpr int V = 16 / ESZ;
-  constexpr int R = kRun3;
+  constexpr int R = run3<S>();
   constexpr int NC = (R - 1) * S + 3;  // input columns per kernel row
   const int64_t cv = a.C / V;
   const int64_t runs = (a.Wo + R - 1) / R;
@@ -161,7 +182,7 @@ __global__ __launch_bounds__(kThreads) void dw3x3_kernel(DwArgs a) {
     *a.route.path_out = (device_route_skip(a.route) ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
   int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x;
   if (i >= total) return;
-  const int64_t c0 = (i % cv) * V;
+  const int64_t c0 = (int64_t)((uint32_t)i - fdiv((uint32_t)i, fcv) * (uint32_t)cv) * V;
   float wv[9][V];
   {
     raw we[9 * V];
@@ -176,16 +197,20 @@ __global__ __launch_bounds__(kThreads) void dw3x3_kernel(DwArgs a) {
       for (int t = 0; t < 9; ++t) wv[t][j] = E::to_f32(we[j * 9 + t]);
   }
   float bv[V];
+  if (a.bias) {
+    load_vec<DT, V>(a.bias + c0 * ESZ, bv);
+  } else {
 #pragma unroll
-  for (int j = 0; j < V; ++j)
-    bv[j] = a.bias ? E::to_f32(reinterpret_cast<const raw *>(a.bias)[c0 + j]) : 0.f;
+    for (int j = 0; j < V; ++j) bv[j] = 0.f;
+  }
   const int H = (int)a.H, W = (int)a.W;
   for (; i < total; i += stride) {
-    const int64_t rest = i / cv;
-    const int run = (int)(rest % runs);
-    const int64_t rest2 = rest / runs;
-    const int oh = (int)(rest2 % a.Ho);
-    const int64_t n = rest2 / a.Ho;
+    const uint32_t rest = fdiv((uint32_t)i, fcv);
+    const uint32_t rest2 = fdiv(rest, fruns);
+    const int run = (int)(rest - rest2 * (uint32_t)runs);
+    const uint32_t n32 = fdiv(rest2, fho);
+    const int oh = (int)(rest2 - n32 * (uint32_t)a.Ho);
+    const int64_t n = n32;
     const int ow0 = run * R;
     const int ih0 = oh * S - 1, iw0 = ow0 * S - 1;
     uint4 xin[3][NC];
@@ -288,20 +313,24 @@ sparoa_status dw_dispatch(const DwArgs &a, hipStream_t st) {
   const bool k3 = a.kh == 3 && a.kw == 3;
   const bool fast3 = vec && k3 && a.ph == 1 && a.pw == 1 && a.dh == 1 && a.dw == 1 &&
                      a.sh == a.sw && (a.sh == 1 || a.sh == 2);
-  if (fast3) {
+  const int64_t cv = a.C / VV;
+  const int64_t runs = cdiv(a.Wo, a.sh == 1 ? run3<1>() : run3<2>());
+  const int64_t items = a.N * a.Ho * runs * cv;
+  // item indices and the grid stride stay below 2^31 (32-bit divisions)
+  if (fast3 && items < (1ll << 30)) {
     // the grid stride must be a multiple of the channel-vector count
-    const int64_t cv = a.C / VV;
     int64_t g = 256, c = cv;
     while (c) { const int64_t t = g % c; g = c; c = t; }  // gcd(256, cv)
     const int64_t q = cv / g;
-    const int64_t items = a.N * a.Ho * cdiv(a.Wo, kRun3) * cv;
     int64_t nb = cdiv(items, kThreads);
     if (nb > 4096) nb = 4096;
     nb = cdiv(nb, q) * q;
+    const FastDiv fcv = make_fastdiv((uint32_t)cv), fruns = make_fastdiv((uint32_t)runs),
+                  fho = make_fastdiv((uint32_t)a.Ho);
     if (a.sh == 1)
-      hipLaunchKernelGGL((dw3x3_kernel<DT, 1>), dim3((unsigned)nb), dim3(kThreads), 0, st, a);
+      hipLaunchKernelGGL((dw3x3_kernel<DT, 1>), dim3((unsigned)nb), dim3(kThreads), 0, st, a, fcv, fruns, fho);
     else
-      hipLaunchKernelGGL((dw3x3_kernel<DT, 2>), dim3((unsigned)nb), dim3(kThreads), 0, st, a);
+      hipLaunchKernelGGL((dw3x3_kernel<DT, 2>), dim3((unsigned)nb), dim3(kThreads), 0, st, a, fcv, fruns, fho);
     SPAROA_LAUNCH_CHECK("dw3x3_kernel");
     return SPAROA_OK;
   }

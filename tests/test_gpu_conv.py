@@ -132,6 +132,21 @@ def test_depthwise_vs_oracle(dt, shape):
         assert_close(y, yr, ar, RTOL[DT[dt]], f"depthwise {shape} {dt}")
 
 
+@pytest.mark.parametrize("stride", [1, 2])
+def test_depthwise_grid_stride_loop(stride):
+    """More lane items than the grid holds (over 2^20): lanes loop over items;
+    the first and last images are checked against the oracle."""
+    n, c, hw = 160 * stride, 16, 128
+    shape = (n, c, hw, hw, c, 3, 3, stride, stride, 1, 1, 1, 1, c)
+    x = synth.relu_normal((n, hw, hw, c), "bf16", 91 + stride)
+    w = synth.he_normal((c, 3, 3, 1), 9, "bf16", 93)
+    y, _, _ = run_conv(x, w, shape, 2, act=1)
+    for sel in (slice(0, 2), slice(n - 2, n)):
+        sub = (2,) + shape[1:]
+        yr, ar = oracle_conv(x[sel].contiguous(), w, sub, act=1)
+        assert_close(y[sel], yr, ar, RTOL[torch.bfloat16], f"depthwise loop s{stride} {sel}")
+
+
 def test_config1_full():
     """Single 3x3 conv 64 -> 64 at 56 x 56, fp32, ReLU(N(0,1)) input."""
     shape = (1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, 1, 1, 1)
