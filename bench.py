@@ -61,6 +61,10 @@ def parse():
     p.add_argument("--no-sweep", action="store_true",
                    help="skip the forced-path and per-operator timings (needs --thresholds): "
                         "only the step kernels run, e.g. under a profiler")
+    p.add_argument("--profile-summary", default=None, metavar="DIR",
+                   help="no GPU: turn the rocprofv3 outputs under DIR (prof_bench/, "
+                        "pmc_{bench,copy}_{FETCH,WRITE}_SIZE/ and their .log files) into "
+                        "profiles/fc_sweep_step_kernels.md and profiles/fc_sweep_traffic.json")
     p.add_argument("--mode", choices=("graph", "eager", "host"), default="graph",
                    help="graph: the executor call captured in a HIP graph, one replay per step; "
                         "eager: the executor call every step; host: counts read back, "
@@ -100,6 +104,113 @@ def load_traffic(digest, family, alg_per_launch):
     if t.get("source_digest") != digest or fam.get("alg_bytes_per_launch") != alg_per_launch:
         return None
     return fam.get("bytes_per_launch")
+
+
+# ---------------------------------------------------------------------------
+# rocprofv3 summaries (host only).  The commands below are run from /tmp on the
+# GPU machine with REPO the repository root; THR is the thresholds JSON the
+# step runs with (--thresholds), so the profiled step is the timed one.
+PROFILE_COMMANDS = {
+    "trace": "rocprofv3 --kernel-trace --stats -d $REPO/gpurun_out/prof_bench -o bench -- "
+             "python3 $REPO/bench.py --steps 20 --warmup 3 --no-cpu-baseline --no-sweep "
+             "--no-models --thresholds \"$THR\"",
+    "pmc_bench": "rocprofv3 --pmc {C} --output-format csv -d $REPO/gpurun_out/pmc_bench_{C} -o pmc "
+                 "-- python3 $REPO/bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-sweep "
+                 "--no-models --thresholds \"$THR\"",
+    "pmc_copy": "rocprofv3 --pmc {C} --output-format csv -d $REPO/gpurun_out/pmc_copy_{C} -o pmc "
+                "-- python3 $REPO/bench.py --copy-probe {MIB}",
+}
+
+
+def _bench_line(log_path):
+    with open(log_path) as f:
+        for line in reversed(f.read().splitlines()):
+            if line.startswith("{") and '"metric"' in line:
+                return json.loads(line)
+    raise ValueError(f"no bench JSON line in {log_path}")
+
+
+def _short(name):
+    return name.replace("sparoa::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+
+
+def profile_summary(d, copy_mib):
+    """Writes the two profile summaries from rocprofv3 outputs under d."""
+    import csv
+    import glob
+    import sqlite3
+    from collections import defaultdict
+
+    # kernel trace of the timed step
+    line = _bench_line(os.path.join(d, "prof_bench.log"))
+    thr = json.dumps(line["config"]["thresholds_per_m"])
+    db = sorted(glob.glob(os.path.join(d, "prof_bench", "**", "*.db"), recursive=True))[0]
+    rows = sqlite3.connect(db).execute("select name, start, end from kernels").fetchall()
+    agg = defaultdict(list)
+    for name, t0, t1 in rows:
+        agg[_short(name)].append((t1 - t0) / 1e3)
+    tot = sum(sum(v) for v in agg.values())
+    out = [f"# FC sweep step: kernel trace ({line['ms_per_step']} ms/step in this run)", "",
+           "Command (from /tmp on the GPU machine, REPO = repository root):", "", "```",
+           "THR='" + thr + "'", PROFILE_COMMANDS["trace"], "```", "",
+           f"Kernel dispatches: {len(rows)}; total kernel time {tot / 1e3:.2f} ms (all phases "
+           "of the run: eager reference, warm-up, timed steps, per-family replays).", "",
+           "| kernel | calls | total ms | avg us | min us | max us | % |", "|---|---|---|---|---|---|---|"]
+    for k, v in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
+        out.append(f"| `{k}` | {len(v)} | {sum(v) / 1e3:.3f} | {sum(v) / len(v):.2f} | "
+                   f"{min(v):.2f} | {max(v):.2f} | {100 * sum(v) / tot:.1f} |")
+    out += ["", "bench.py's own figures in the same run (HIP events, per-family graph replays):", ""]
+    for fam, r in [("dominant", line["roofline"])] + list(line.get("roofline_other_families", {}).items()):
+        out.append(f"- {fam}: `{r['kernel']}`, {r['operators']} operators, avg {r['avg_launch_us']} us "
+                   f"per operator, {r['achieved']} GB/s algorithmic")
+    with open(os.path.join(ROOT, "profiles", "fc_sweep_step_kernels.md"), "w") as f:
+        f.write("\n".join(out) + "\n")
+
+    # HBM traffic per operator of each family, counters scaled by a plain copy
+    def counters(sub):
+        with open(os.path.join(d, sub, "pmc_counter_collection.csv")) as f:
+            return [(r["Kernel_Name"], float(r["Counter_Value"])) for r in csv.DictReader(f)]
+
+    pline = _bench_line(os.path.join(d, "pmc_bench_FETCH_SIZE.log"))
+    fams = {pline["roofline"]["kernel"]: pline["roofline"]}
+    fams.update({r["kernel"]: r for r in pline.get("roofline_other_families", {}).values()})
+    res = dict(workload="FC sweep step (24 operators), thresholds per m: " + thr,
+               source_digest=pline["roofline"]["source_digest"],   # sources the counters ran on
+               scale_reading="a plain device-to-device copy of known size reads FETCH_SIZE and "
+                             "WRITE_SIZE; each counter is scaled by known bytes / measured",
+               families={}, commands=[])
+    scale = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        cp = sorted(v for n, v in counters(f"pmc_copy_{c}") if "copyBuffer" in n)[-5:]
+        scale[c] = copy_mib * 1024.0 / (sum(cp) / len(cp))
+        res[f"copy_{c.lower()}_kib"] = round(sum(cp) / len(cp), 3)
+        res[f"scale_{c.lower()}"] = round(scale[c], 4)
+    per = {c: counters(f"pmc_bench_{c}") for c in ("FETCH_SIZE", "WRITE_SIZE")}
+    for kernel, r in fams.items():
+        mfma = "igemm" in kernel
+        name = "dense_mfma" if mfma else "dense_bw"
+        kib = {}
+        for c, rows_c in per.items():
+            if mfma:   # one operator = measure_init + measure_lanebit + igemm + split_reduce
+                ops = sum(1 for n, _ in rows_c if "igemm_kernel<" in n)
+                tot_c = sum(v for n, v in rows_c if any(k in n for k in (
+                    "measure_init", "measure_lanebit<", "igemm_kernel<", "split_reduce<")))
+            else:      # one operator = one self-measuring fc_bw_kernel launch
+                sel = [v for n, v in rows_c if "fc_bw_kernel<" in n and _short(n).endswith("true>")]
+                ops, tot_c = len(sel), sum(sel)
+            kib[c] = (tot_c / max(ops, 1), ops)
+        res["families"][name] = dict(
+            kernel=kernel, operators=r["operators"], alg_bytes_per_launch=r["alg_bytes_per_launch"],
+            bytes_per_launch=int(sum(kib[c][0] * 1024 * scale[c] for c in kib)),
+            fetch_kib_per_launch=round(kib["FETCH_SIZE"][0], 3),
+            write_kib_per_launch=round(kib["WRITE_SIZE"][0], 3),
+            launches_counted=kib["FETCH_SIZE"][1])
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        res["commands"].append("THR='" + thr + "' " + PROFILE_COMMANDS["pmc_bench"].format(C=c))
+        res["commands"].append(PROFILE_COMMANDS["pmc_copy"].format(C=c, MIB=copy_mib))
+    with open(os.path.join(ROOT, "profiles", "fc_sweep_traffic.json"), "w") as f:
+        json.dump(res, f, indent=1)
+    print(json.dumps(res["families"], indent=1))
 
 
 class Case:
@@ -172,28 +283,31 @@ def run_case(abi, c):
 
 
 def forced_times(abi, torch, cases, paths, rounds=3):
-    """Duration (us) of the FC kernel of every case on each forced path, with
-    cold weights: one launch per case in case order (each case streams its
-    own 32 MiB of weights, so the 24 cases overflow the Infinity Cache), a
-    pair of HIP events around each launch, best of `rounds`."""
+    """Duration (us) of every case's whole path (sparoa_fc_measured: measure,
+    route, execute) with the route forced onto each path by its thresholds
+    (intensity threshold 0 or 1e30 picks the family, sparsity threshold 0 or 2
+    the skip bit), so a family is charged the measurement it needs (the
+    streaming kernel measures inside its one launch; the GEMM family measures
+    in a launch of its own).  Cold weights: one call per case in case order
+    (each case streams its own 32 MiB of weights, so the 24 cases overflow the
+    Infinity Cache), a pair of HIP events around each call, best of `rounds`.
+    Also records each case's block sparsity at each family's granularity."""
     for c in cases:
         c.forced = {}
         c.rho_b = {}
     for p in paths:
         fam = p & 2
-        for c in cases:     # the mask at this family's skip granularity (untimed)
-            br, bc = c.block[fam]
-            st = abi.sparoa_measure_sparsity_sync(c.x, c.m, K, br, bc, 0, c.counts, c.mask)
-            c.rho_b[fam] = st["zero_blocks"] / st["num_blocks"]
+        s_thr = 0.0 if p & 1 else 2.0
+        c_thr = 1e30 if fam else 0.0
         best = [None] * len(cases)
         for _ in range(rounds):
             ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                   for _ in cases]
             for c, (e0, e1) in zip(cases, ev):
-                w = c.wp if abi.sparoa_fc_uses_packed(c.desc, p) else c.w
                 e0.record()
-                abi.sparoa_fc(c.desc, p, c.x, w, None, None, abi.ACT_NONE,
-                              c.mask if p & 1 else None, c.y, c.ws)
+                abi.sparoa_fc_measured(c.desc, s_thr, c_thr, abi.ROUTE_BLOCK, c.x, c.w, c.wp,
+                                       None, None, abi.ACT_NONE, c.counts, c.mask, c.y, c.ws,
+                                       c.path_dev)
                 e1.record()
             torch.cuda.synchronize()
             for i, (e0, e1) in enumerate(ev):
@@ -201,6 +315,9 @@ def forced_times(abi, torch, cases, paths, rounds=3):
                 best[i] = t if best[i] is None else min(best[i], t)
         for c, t in zip(cases, best):
             c.forced[p] = t
+            assert int(c.path_dev.item()) == p, "forced thresholds must force the path"
+            z, _, zb, nb = c.counts.cpu().tolist()
+            c.rho_b[fam] = zb / nb
 
 
 def path_times(abi, torch, cases, rounds=3):
@@ -292,8 +409,8 @@ def model_latencies(abi, torch, synth, reps=10):
 
 
 def calibrate(abi, cases):
-    """Thresholds per operator class (m), from the cold forced-path timings:
-    the kernel family whose dense path is faster (intensity threshold: the
+    """Thresholds per operator class (m), from the cold forced-path timings of
+    the whole path: the kernel family whose dense path is faster (intensity threshold: the
     class's own intensity when the MFMA family wins, the bf16 ridge point
     otherwise), and the smallest block sparsity at or above which that
     family's skip path beats its dense path in every case of the class (1.0
@@ -342,6 +459,9 @@ def cpu_baseline_timed(cases, budget_s):
 
 def main():
     args = parse()
+    if args.profile_summary:
+        profile_summary(args.profile_summary, args.copy_probe or 256)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
               "(the hot path shards by batch with no exchange; see the design notes)",
@@ -470,9 +590,9 @@ def main():
         if c.path_us is not None:
             row.update(us=round(c.path_us, 2), gbps=round(c.alg / c.path_us / 1e3, 1),
                        dense_equiv_tflops=round(2 * c.m * K * N / c.path_us / 1e6, 2))
-        for p in paths_swept:
+        for p in paths_swept:   # whole path (measure, route, execute) forced onto p
             if p in c.forced:
-                row[abi.PATH_NAMES[p] + "_us"] = round(c.forced[p], 2)
+                row[abi.PATH_NAMES[p] + "_path_us"] = round(c.forced[p], 2)
         table.append(row)
     tot_bytes = sum(c.alg for c in cases)
 

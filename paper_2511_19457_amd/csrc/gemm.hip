@@ -870,7 +870,9 @@ GemmTileChoice ig_choose(const Shape &s, int64_t c_in) {
   const int64_t tl = tiles(t.bm, t.bn), nchunks = cdiv(s.K, t.kchunk);
   int64_t split = 1;
   if (tl < 192) {
-    split = cdiv(512, tl);
+    // about one work-group per CU: more splits cost more partial traffic than
+    // they gain (FC 64 x 4096 x 4096: split 4 15.1 us, split 8 17.8 us)
+    split = cdiv(256, tl);
     if (split > 8) split = 8;
     if (split > nchunks / 4) split = nchunks / 4;
     if (split < 1) split = 1;

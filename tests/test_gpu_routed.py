@@ -163,6 +163,58 @@ def test_fc_measured_equals_measure_then_routed(case, mode, thr_kind):
     assert torch.equal(y, y2)
 
 
+@pytest.mark.parametrize("m,k,n", [(96, 512, 256), (200, 16384, 64)])
+def test_fc_measured_gemm_family_consecutive_calls(m, k, n):
+    """GEMM-family FC (measurement launch, then the routed GEMM): the
+    oracle's counts, bitmap and route on consecutive calls that share one
+    workspace and one set of count/bitmap buffers -- over several measuring
+    work-groups (m=96) and past their grid cap, with lanes looping (m=200)."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    d = abi.fc_desc(m, k, n, abi.BF16)
+    br, bc = abi.sparoa_fc_skip_block(d, abi.PATH_SKIP_MFMA)
+    w = synth.normal((n, k), "bf16", 5, std=k ** -0.5).to(dev)
+    ws = torch.zeros(max(abi.sparoa_fc_workspace_size(d, p) for p in range(4)), dtype=torch.uint8,
+                     device=dev)
+    counts = torch.zeros(4, dtype=torch.int64, device=dev)
+    mask = torch.zeros(abi.sparoa_mask_words(m, k, br, bc), dtype=torch.int32, device=dev)
+    y = torch.empty(m, n, dtype=torch.bfloat16, device=dev)
+    path = torch.zeros(1, dtype=torch.int32, device=dev)
+    for call, (rho, pattern) in enumerate([(0.7, "block"), (0.3, "iid"), (0.95, "block")]):
+        x = synth.sparse_matrix(m, k, rho, pattern, "bf16", 900 + call)
+        ref = oracle.measure(x, m, k, br, bc)
+        abi.sparoa_fc_measured(d, 0.5, 0.0, abi.ROUTE_BLOCK, x.to(dev), w, None, None, None,
+                               abi.ACT_NONE, counts, mask, y, ws, path)
+        torch.cuda.synchronize()
+        assert counts.cpu().tolist() == [ref["zeros"], ref["numel"], ref["zero_blocks"],
+                                         ref["num_blocks"]], f"call {call}"
+        assert np.array_equal(mask.cpu().numpy().view(np.uint32), ref["mask"]), f"call {call}"
+        assert int(path.item()) == (1 if ref["zero_blocks"] / ref["num_blocks"] >= 0.5 else 0)
+
+
+def test_fc_measured_without_split_k_needs_no_workspace():
+    """An FC whose GEMM has no split-K runs the whole path with a token
+    workspace, and measures exactly."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    m, k, n = 4096, 256, 512
+    d = abi.fc_desc(m, k, n, abi.BF16)
+    br, bc = abi.sparoa_fc_skip_block(d, abi.PATH_SKIP_MFMA)
+    x = synth.sparse_matrix(m, k, 0.6, "block", "bf16", 950)
+    w = synth.normal((n, k), "bf16", 951, std=k ** -0.5)
+    ref = oracle.measure(x, m, k, br, bc)
+    ws = torch.zeros(64, dtype=torch.uint8, device=dev)
+    counts = torch.full((4,), -1, dtype=torch.int64, device=dev)
+    mask = torch.full((abi.sparoa_mask_words(m, k, br, bc),), -1, dtype=torch.int32, device=dev)
+    y = torch.empty(m, n, dtype=torch.bfloat16, device=dev)
+    abi.sparoa_fc_measured(d, 0.5, 0.0, abi.ROUTE_BLOCK, x.to(dev), w.to(dev), None, None, None,
+                           abi.ACT_NONE, counts, mask, y, ws, None)
+    torch.cuda.synchronize()
+    assert counts.cpu().tolist() == [ref["zeros"], ref["numel"], ref["zero_blocks"],
+                                     ref["num_blocks"]]
+    assert np.array_equal(mask.cpu().numpy().view(np.uint32), ref["mask"])
+
+
 def test_fc_ops_run_equals_per_op_routed_calls():
     """The native batch executor runs measure + routed FC per op: paths and
     outputs equal the per-op calls, counts equal the oracle's."""
