@@ -191,10 +191,10 @@ def profile_summary(d, copy_mib):
         name = "dense_mfma" if mfma else "dense_bw"
         kib = {}
         for c, rows_c in per.items():
-            if mfma:   # one operator = measure_init + measure_lanebit + igemm + split_reduce
-                ops = sum(1 for n, _ in rows_c if "igemm_kernel<" in n)
+            if mfma:   # per operator: its GEMM and its share of the grouped measurement
+                ops = sum(1 for n, _ in rows_c if "igemm_kernel<" in n)    # and reduction
                 tot_c = sum(v for n, v in rows_c if any(k in n for k in (
-                    "measure_init", "measure_lanebit<", "igemm_kernel<", "split_reduce<")))
+                    "measure_init", "measure_lanebit", "igemm_kernel<", "split_reduce")))
             else:      # one operator = one self-measuring fc_bw_kernel launch
                 sel = [v for n, v in rows_c if "fc_bw_kernel<" in n and _short(n).endswith("true>")]
                 ops, tot_c = len(sel), sum(sel)
@@ -628,7 +628,8 @@ def main():
         if fam == abi.PATH_DENSE_BW:
             kernel = "fc_bw_kernel (self-measuring; one launch per operator)"
         else:
-            kernel = "igemm_kernel (one measurement, GEMM and split-K reduction launch per operator)"
+            kernel = ("igemm_kernel (per operator; the family's measurements and split-K "
+                      "reductions run as grouped launches)")
         traffic = load_traffic(digest, abi.PATH_NAMES[fam], per_launch)
         return dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic, kernel=kernel,

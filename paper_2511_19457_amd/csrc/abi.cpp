@@ -3,6 +3,7 @@
 #include <cmath>
 #include <cstring>
 #include <string>
+#include <vector>
 
 #include "common.h"
 
@@ -61,6 +62,32 @@ sparoa_status check_ptrs16(std::initializer_list<const void *> ps) {
     if (p && !aligned16(p)) return fail(SPAROA_ERR_UNSUPPORTED, "pointer not 16-byte aligned");
   return SPAROA_OK;
 }
+
+sparoa_status check_measure(const void *x_dev, sparoa_dtype dtype, int64_t rows, int64_t cols,
+                            int64_t block_rows, int64_t block_cols, int64_t samples,
+                            const sparoa_counts *counts_dev, const uint32_t *mask_dev,
+                            const uint64_t *per_sample_dev) {
+  if (!x_dev || !counts_dev) return fail(SPAROA_ERR_INVALID_ARG, "measure: null x or counts");
+  if (!dtype_ok(dtype)) return fail(SPAROA_ERR_INVALID_ARG, "measure: unknown dtype");
+  uint64_t numel;
+  if (rows <= 0 || cols <= 0 || !mul_ok((uint64_t)rows, (uint64_t)cols, &numel) ||
+      numel > (uint64_t)INT64_MAX / 4)
+    return fail(SPAROA_ERR_INVALID_ARG, "measure: rows and cols must be > 0");
+  if (mask_dev) {
+    int64_t words;
+    sparoa_status st = sparoa_mask_words(rows, cols, block_rows, block_cols, &words);
+    if (st != SPAROA_OK) return st;
+  }
+  if (per_sample_dev) {
+    if (samples <= 0 || rows % samples)
+      return fail(SPAROA_ERR_INVALID_ARG, "measure: rows must split into `samples` groups");
+    if (samples > 65535) return fail(SPAROA_ERR_UNSUPPORTED, "measure: more than 65535 samples");
+    if (mask_dev && (rows / samples) % block_rows)
+      return fail(SPAROA_ERR_INVALID_ARG, "measure: block rows straddle samples");
+  }
+  if (!aligned16(x_dev)) return fail(SPAROA_ERR_UNSUPPORTED, "measure: x not 16-byte aligned");
+  return SPAROA_OK;
+}
 }  // namespace
 
 sparoa_status fail(sparoa_status s, const std::string &msg) {
@@ -115,25 +142,9 @@ sparoa_status sparoa_measure_sparsity(const void *x_dev, sparoa_dtype dtype, int
                                       uint32_t *mask_dev, uint64_t *per_sample_dev,
                                       hipStream_t stream) {
   g_last_error.clear();
-  if (!x_dev || !counts_dev) return fail(SPAROA_ERR_INVALID_ARG, "measure: null x or counts");
-  if (!dtype_ok(dtype)) return fail(SPAROA_ERR_INVALID_ARG, "measure: unknown dtype");
-  uint64_t numel;
-  if (rows <= 0 || cols <= 0 || !mul_ok((uint64_t)rows, (uint64_t)cols, &numel) ||
-      numel > (uint64_t)INT64_MAX / 4)
-    return fail(SPAROA_ERR_INVALID_ARG, "measure: rows and cols must be > 0");
-  if (mask_dev) {
-    int64_t words;
-    sparoa_status st = sparoa_mask_words(rows, cols, block_rows, block_cols, &words);
-    if (st != SPAROA_OK) return st;
-  }
-  if (per_sample_dev) {
-    if (samples <= 0 || rows % samples)
-      return fail(SPAROA_ERR_INVALID_ARG, "measure: rows must split into `samples` groups");
-    if (samples > 65535) return fail(SPAROA_ERR_UNSUPPORTED, "measure: more than 65535 samples");
-    if (mask_dev && (rows / samples) % block_rows)
-      return fail(SPAROA_ERR_INVALID_ARG, "measure: block rows straddle samples");
-  }
-  if (!aligned16(x_dev)) return fail(SPAROA_ERR_UNSUPPORTED, "measure: x not 16-byte aligned");
+  sparoa_status st = check_measure(x_dev, dtype, rows, cols, block_rows, block_cols, samples,
+                                   counts_dev, mask_dev, per_sample_dev);
+  if (st != SPAROA_OK) return st;
   return launch_measure(x_dev, dtype, rows, cols, block_rows, block_cols, samples, counts_dev,
                         mask_dev, per_sample_dev, stream);
 }
@@ -482,12 +493,17 @@ sparoa_status sparoa_conv2d_routed(const sparoa_conv_desc *d, const sparoa_thres
                           can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r);
 }
 
-sparoa_status sparoa_fc_routed(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
-                               const sparoa_counts *counts_dev, const void *x, const void *w_nk,
-                               const void *w_packed, const void *bias, const void *residual,
-                               sparoa_act act, const uint32_t *mask, void *y, void *workspace,
-                               size_t ws_bytes, uint32_t *path_dev, hipStream_t stream) {
-  g_last_error.clear();
+}  // extern "C"
+
+namespace {
+// The routed FC (see sparoa_fc_routed); defer as for launch_gemm_conv.
+sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
+                             const sparoa_counts *counts_dev, const void *x, const void *w_nk,
+                             const void *w_packed, const void *bias, const void *residual,
+                             sparoa_act act, const uint32_t *mask, void *y, void *workspace,
+                             size_t ws_bytes, uint32_t *path_dev, hipStream_t stream,
+                             SplitReduceJob *defer) {
+  if (defer) defer->split = 0;
   sparoa_intensity in;
   sparoa_status st = sparoa_op_intensity_fc(d, &in);
   if (st != SPAROA_OK) return st;
@@ -508,7 +524,52 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *d, const sparoa_thresholds 
   if (ws_bytes < gemm_workspace(c, p)) return fail(SPAROA_ERR_WORKSPACE, "fc_routed: workspace too small");
   const bool can_skip = gemm_skip_supported(c);
   return launch_gemm_conv(c, p, x, w, d->has_bias ? bias : nullptr, residual, act,
-                          can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r);
+                          can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r,
+                          defer);
+}
+
+// How sparoa_fc_measured runs one FC: the self-measuring streaming kernel
+// (one launch), or a lanebit-layout measurement that an executor may group
+// with others, or the standalone measurement; then the routed kernel.
+struct FcPlan {
+  bool self_measures;
+  MeasureJob measure;
+};
+
+sparoa_status fc_measured_plan(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
+                               const void *x, const void *w_packed, const void *bias,
+                               const void *residual, sparoa_act act, sparoa_counts *counts_dev,
+                               uint32_t *mask_dev, void *y, FcPlan *p) {
+  sparoa_intensity in;
+  sparoa_status st = sparoa_op_intensity_fc(d, &in);
+  if (st != SPAROA_OK) return st;
+  if ((st = check_thr(thr)) != SPAROA_OK) return st;
+  const int bw = in.intensity < thr->intensity_thr ? 1 : 0;
+  p->self_measures = bw && fc_bw_self_measures(*d);
+  if (p->self_measures) {
+    if (!counts_dev || !x || !w_packed || !y || !mask_dev || !act_ok(act))
+      return fail(SPAROA_ERR_INVALID_ARG, "fc_measured: null counts/x/w_packed/mask/y or bad act");
+    if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "fc_measured: has_bias without bias");
+    return check_ptrs16({x, w_packed, bias, residual, y, mask_dev, counts_dev});
+  }
+  int64_t br, bc;
+  const sparoa_path fam = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
+  if ((st = sparoa_fc_skip_block(d, fam, &br, &bc)) != SPAROA_OK) return st;
+  p->measure = MeasureJob{x, d->dtype, d->m, d->k, br, bc, counts_dev, mask_dev};
+  return check_measure(x, d->dtype, d->m, d->k, br, bc, 0, counts_dev, mask_dev, nullptr);
+}
+}  // namespace
+
+extern "C" {
+
+sparoa_status sparoa_fc_routed(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
+                               const sparoa_counts *counts_dev, const void *x, const void *w_nk,
+                               const void *w_packed, const void *bias, const void *residual,
+                               sparoa_act act, const uint32_t *mask, void *y, void *workspace,
+                               size_t ws_bytes, uint32_t *path_dev, hipStream_t stream) {
+  g_last_error.clear();
+  return fc_routed_impl(d, thr, counts_dev, x, w_nk, w_packed, bias, residual, act, mask, y,
+                        workspace, ws_bytes, path_dev, stream, nullptr);
 }
 
 sparoa_status sparoa_fc_measured(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
@@ -518,34 +579,51 @@ sparoa_status sparoa_fc_measured(const sparoa_fc_desc *d, const sparoa_threshold
                                  void *workspace, size_t ws_bytes, uint32_t *path_dev,
                                  hipStream_t stream) {
   g_last_error.clear();
-  sparoa_intensity in;
-  sparoa_status st = sparoa_op_intensity_fc(d, &in);
+  FcPlan p;
+  sparoa_status st = fc_measured_plan(d, thr, x, w_packed, bias, residual, act, counts_dev,
+                                      mask_dev, y, &p);
   if (st != SPAROA_OK) return st;
-  if ((st = check_thr(thr)) != SPAROA_OK) return st;
-  const int bw = in.intensity < thr->intensity_thr ? 1 : 0;
-  if (bw && fc_bw_self_measures(*d)) {
-    if (!counts_dev || !x || !w_packed || !y || !mask_dev || !act_ok(act))
-      return fail(SPAROA_ERR_INVALID_ARG, "fc_measured: null counts/x/w_packed/mask/y or bad act");
-    if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "fc_measured: has_bias without bias");
-    if ((st = check_ptrs16({x, w_packed, bias, residual, y, mask_dev, counts_dev})) != SPAROA_OK)
-      return st;
+  if (p.self_measures) {
+    const int bw = 1;
     const DeviceRoute r{nullptr, thr->sparsity_thr, thr->mode, bw, path_dev};
     return launch_fc_bw_measured(*d, x, w_packed, d->has_bias ? bias : nullptr, residual, act,
                                  counts_dev, mask_dev, y, stream, r);
   }
-  int64_t br, bc;
-  const sparoa_path fam = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
-  if ((st = sparoa_fc_skip_block(d, fam, &br, &bc)) != SPAROA_OK) return st;
-  if ((st = sparoa_measure_sparsity(x, d->dtype, d->m, d->k, br, bc, 0, counts_dev, mask_dev,
-                                    nullptr, stream)) != SPAROA_OK)
+  const MeasureJob &m = p.measure;
+  if ((st = launch_measure(m.x, m.dt, m.rows, m.cols, m.block_rows, m.block_cols, 0, m.counts,
+                           m.mask, nullptr, stream)) != SPAROA_OK)
     return st;
-  return sparoa_fc_routed(d, thr, counts_dev, x, w_nk, w_packed, bias, residual, act, mask_dev, y,
-                          workspace, ws_bytes, path_dev, stream);
+  return fc_routed_impl(d, thr, counts_dev, x, w_nk, w_packed, bias, residual, act, mask_dev, y,
+                        workspace, ws_bytes, path_dev, stream, nullptr);
 }
 
 // ---------------------------------------------------------------- executor
 
 namespace {
+// True when some op reads memory that some op writes (an output feeding
+// another op's input): then the ops must run strictly one after another.
+bool ops_chained(const sparoa_fc_op *ops, int64_t n) {
+  auto range = [](const void *p, int64_t bytes) {
+    const uintptr_t b = reinterpret_cast<uintptr_t>(p);
+    return std::make_pair(b, b + (uintptr_t)(p ? bytes : 0));
+  };
+  auto overlap = [](std::pair<uintptr_t, uintptr_t> a, std::pair<uintptr_t, uintptr_t> b) {
+    return a.first < b.second && b.first < a.second;
+  };
+  for (int64_t j = 0; j < n; ++j) {
+    const sparoa_fc_desc &dj = ops[j].desc;
+    const int64_t e = elem_size(dj.dtype);
+    const auto xj = range(ops[j].x, dj.m * dj.k * e), rj = range(ops[j].residual, dj.m * dj.n * e);
+    for (int64_t i = 0; i < n; ++i) {
+      if (i == j) continue;
+      const sparoa_fc_desc &di = ops[i].desc;
+      const auto yi = range(ops[i].y, di.m * di.n * elem_size(di.dtype));
+      if (overlap(xj, yi) || overlap(rj, yi)) return true;
+    }
+  }
+  return false;
+}
+
 sparoa_status check_ops(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr) {
   if (!ops || n < 0) return fail(SPAROA_ERR_INVALID_ARG, "fc_ops: null ops or n < 0");
   if (thr) return check_thr(thr);
@@ -562,15 +640,81 @@ sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa
   g_last_error.clear();
   sparoa_status st = check_ops(ops, n, thr);
   if (st != SPAROA_OK) return st;
+  if (events || ops_chained(ops, n)) {  // op by op (each bracketed by its events, if given)
+    for (int64_t i = 0; i < n; ++i) {
+      const sparoa_fc_op &o = ops[i];
+      if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i], stream));
+      if ((st = sparoa_fc_measured(&o.desc, thr ? thr : &o.thr, o.x, o.w_nk, o.w_packed, o.bias,
+                                   o.residual, o.act, o.counts, o.mask, o.y, o.workspace,
+                                   o.ws_bytes, o.path, stream)) != SPAROA_OK)
+        return st;
+      if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i + 1], stream));
+    }
+    return SPAROA_OK;
+  }
+  // Batched: every op is validated first; the measurements of the ops that
+  // measure in a launch of their own run grouped (counter init and
+  // measurement: two launches per kGroupMax ops of one element size); then
+  // each op's FC kernel in op order; then the split-K reductions, grouped
+  // per dtype.  Same kernels and arithmetic as op-by-op calls, fewer launches.
+  std::vector<FcPlan> plan((size_t)n);
   for (int64_t i = 0; i < n; ++i) {
     const sparoa_fc_op &o = ops[i];
-    if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i], stream));
-    if ((st = sparoa_fc_measured(&o.desc, thr ? thr : &o.thr, o.x, o.w_nk, o.w_packed, o.bias,
-                                 o.residual, o.act,
-                                 o.counts, o.mask, o.y, o.workspace, o.ws_bytes, o.path,
-                                 stream)) != SPAROA_OK)
+    if ((st = fc_measured_plan(&o.desc, thr ? thr : &o.thr, o.x, o.w_packed, o.bias, o.residual,
+                               o.act, o.counts, o.mask, o.y, &plan[i])) != SPAROA_OK)
       return st;
-    if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i + 1], stream));
+  }
+  for (int esz : {2, 4}) {
+    std::vector<MeasureJob> group;
+    for (int64_t i = 0; i < n; ++i) {
+      const MeasureJob &m = plan[i].measure;
+      if (plan[i].self_measures || elem_size(m.dt) != esz) continue;
+      if (!measure_groupable(m)) {
+        if ((st = launch_measure(m.x, m.dt, m.rows, m.cols, m.block_rows, m.block_cols, 0,
+                                 m.counts, m.mask, nullptr, stream)) != SPAROA_OK)
+          return st;
+        continue;
+      }
+      group.push_back(m);
+      if ((int)group.size() == kGroupMax) {
+        if ((st = launch_measure_group(group.data(), kGroupMax, stream)) != SPAROA_OK) return st;
+        group.clear();
+      }
+    }
+    if (!group.empty() &&
+        (st = launch_measure_group(group.data(), (int)group.size(), stream)) != SPAROA_OK)
+      return st;
+  }
+  std::vector<SplitReduceJob> reduces;
+  for (int64_t i = 0; i < n; ++i) {
+    const sparoa_fc_op &o = ops[i];
+    const sparoa_thresholds *t = thr ? thr : &o.thr;
+    if (plan[i].self_measures) {
+      const DeviceRoute r{nullptr, t->sparsity_thr, t->mode, 1, o.path};
+      st = launch_fc_bw_measured(o.desc, o.x, o.w_packed, o.desc.has_bias ? o.bias : nullptr,
+                                 o.residual, o.act, o.counts, o.mask, o.y, stream, r);
+    } else {
+      SplitReduceJob job;
+      st = fc_routed_impl(&o.desc, t, o.counts, o.x, o.w_nk, o.w_packed, o.bias, o.residual,
+                          o.act, o.mask, o.y, o.workspace, o.ws_bytes, o.path, stream, &job);
+      if (st == SPAROA_OK && job.split > 1) reduces.push_back(job);
+    }
+    if (st != SPAROA_OK) return st;
+  }
+  for (sparoa_dtype dt : {SPAROA_F32, SPAROA_F16, SPAROA_BF16}) {
+    std::vector<SplitReduceJob> group;
+    for (const SplitReduceJob &j : reduces) {
+      if (j.dt != dt) continue;
+      group.push_back(j);
+      if ((int)group.size() == kGroupMax) {
+        if ((st = launch_split_reduce_group(group.data(), kGroupMax, stream)) != SPAROA_OK)
+          return st;
+        group.clear();
+      }
+    }
+    if (!group.empty() &&
+        (st = launch_split_reduce_group(group.data(), (int)group.size(), stream)) != SPAROA_OK)
+      return st;
   }
   return SPAROA_OK;
 }

@@ -67,6 +67,36 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
                              sparoa_counts *counts, uint32_t *mask, uint64_t *per_sample,
                              hipStream_t stream);
 
+constexpr int kGroupMax = 16;  // jobs per grouped launch
+
+// Several measurements in the lanebit layout (block 1 x one 16-byte vector,
+// a mask given), all of one element size, in two launches (counter init,
+// measurement) for up to kGroupMax tensors.
+struct MeasureJob {
+  const void *x;
+  sparoa_dtype dt;
+  int64_t rows, cols, block_rows, block_cols;
+  sparoa_counts *counts;
+  uint32_t *mask;
+};
+bool measure_groupable(const MeasureJob &j);
+sparoa_status launch_measure_group(const MeasureJob *jobs, int n, hipStream_t stream);
+
+// Sums split-K fp32 partials [split][M][N] in split order, adds bias and
+// residual, applies the activation, and writes y in dtype.
+struct SplitReduceJob {
+  sparoa_dtype dt;
+  const float *partial;
+  int split;          // 0: nothing to reduce
+  int64_t M, N;
+  const void *bias, *residual;
+  sparoa_act act;
+  void *y;
+};
+sparoa_status launch_split_reduce(const SplitReduceJob &job, hipStream_t stream);
+// Several reductions of one dtype in one launch (n <= kGroupMax).
+sparoa_status launch_split_reduce_group(const SplitReduceJob *jobs, int n, hipStream_t stream);
+
 // Implicit-GEMM MFMA conv (groups == 1); FC runs through it as a 1x1 conv.
 struct GemmTileChoice {
   int cfg;          // 0: general kernel; else a tile of the 64-channel-chunk kernel
@@ -81,13 +111,10 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
                                const void *w, const void *bias, const void *residual,
                                sparoa_act act, const uint32_t *mask, void *y, void *ws,
                                size_t ws_bytes, uint64_t *executed, hipStream_t stream,
-                               const DeviceRoute *route = nullptr);
-
-// Sums split-K fp32 partials [split][M][N] in split order, adds bias and
-// residual, applies the activation, and writes y in dtype.
-sparoa_status launch_split_reduce(sparoa_dtype dt, const float *partial, int split, int64_t M,
-                                  int64_t N, const void *bias, const void *residual,
-                                  sparoa_act act, void *y, hipStream_t stream);
+                               const DeviceRoute *route = nullptr,
+                               SplitReduceJob *defer = nullptr);
+// defer: when non-null, a split-K reduction is described there (split > 1)
+// instead of launched; split = 0 when the GEMM needs none.
 
 // Writes v to *p on the stream with a one-lane kernel (no memset node).
 sparoa_status launch_set_u64(uint64_t *p, uint64_t v, hipStream_t stream);

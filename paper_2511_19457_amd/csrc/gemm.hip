@@ -363,21 +363,84 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
 }
 
 // Sums the K-split partials in split order, adds bias and residual, then
-// applies the activation.
+// applies the activation.  Grouped form: up to kGroupMax reductions of one
+// dtype in one launch, work-groups dealt to the jobs in proportion to their
+// size.  A thread finishes 8 consecutive outputs (16-byte partial, bias and
+// residual loads, one 16-byte store) when N % 8 == 0, else one.
+struct ReduceGroup {
+  int n;
+  int wg_begin[kGroupMax + 1];
+  const float *partial[kGroupMax];
+  int split[kGroupMax];
+  int64_t M[kGroupMax], N[kGroupMax];
+  const char *bias[kGroupMax], *residual[kGroupMax];
+  int act[kGroupMax];
+  char *y[kGroupMax];
+};
+
 template <int DT>
-__global__ __launch_bounds__(256) void split_reduce(const float *__restrict__ partial, int split,
-                                                    int64_t M, int64_t N, const char *bias,
-                                                    const char *residual, int act, char *y) {
+__global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
   using E = Elem<DT>;
-  const int64_t total = M * N;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    float o = 0.f;
-    for (int z = 0; z < split; ++z) o += partial[z * total + i];
-    const int64_t col = i % N;
-    if (bias) o += E::to_f32(reinterpret_cast<const typename E::raw *>(bias)[col]);
-    if (residual) o += E::to_f32(reinterpret_cast<const typename E::raw *>(residual)[i]);
-    reinterpret_cast<typename E::raw *>(y)[i] = E::from_f32(apply_act(o, act));
+  using raw = typename E::raw;
+  int j = 0;
+  while (j + 1 < g.n && (int)blockIdx.x >= g.wg_begin[j + 1]) ++j;
+  const int64_t b0 = blockIdx.x - g.wg_begin[j], nb = g.wg_begin[j + 1] - g.wg_begin[j];
+  const int64_t M = g.M[j], N = g.N[j], total = M * N;
+  const float *partial = g.partial[j];
+  const int split = g.split[j], act = g.act[j];
+  const raw *bias = reinterpret_cast<const raw *>(g.bias[j]);
+  const raw *res = reinterpret_cast<const raw *>(g.residual[j]);
+  raw *y = reinterpret_cast<raw *>(g.y[j]);
+  if (N % 8 == 0) {
+    for (int64_t v = b0 * 256 + threadIdx.x; v < total / 8; v += nb * 256) {
+      const int64_t i = v * 8, col = i % N;
+      float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      for (int z = 0; z < split; ++z) {
+        const float4 lo = *reinterpret_cast<const float4 *>(partial + z * total + i);
+        const float4 hi = *reinterpret_cast<const float4 *>(partial + z * total + i + 4);
+        o[0] += lo.x; o[1] += lo.y; o[2] += lo.z; o[3] += lo.w;
+        o[4] += hi.x; o[5] += hi.y; o[6] += hi.z; o[7] += hi.w;
+      }
+      raw t[8];
+      if (bias) {
+        if constexpr (E::size == 2) {
+          const uint4 q = *reinterpret_cast<const uint4 *>(bias + col);
+          __builtin_memcpy(t, &q, 16);
+        } else {
+          for (int e = 0; e < 8; ++e) t[e] = bias[col + e];
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] += E::to_f32(t[e]);
+      }
+      if (res) {
+        if constexpr (E::size == 2) {
+          const uint4 q = *reinterpret_cast<const uint4 *>(res + i);
+          __builtin_memcpy(t, &q, 16);
+        } else {
+          for (int e = 0; e < 8; ++e) t[e] = res[i + e];
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] += E::to_f32(t[e]);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t[e] = E::from_f32(apply_act(o[e], act));
+      if constexpr (E::size == 2) {
+        uint4 q;
+        __builtin_memcpy(&q, t, 16);
+        *reinterpret_cast<uint4 *>(y + i) = q;
+      } else {
+        for (int e = 0; e < 8; ++e) y[i + e] = t[e];
+      }
+    }
+  } else {
+    for (int64_t i = b0 * 256 + threadIdx.x; i < total; i += nb * 256) {
+      float o = 0.f;
+      for (int z = 0; z < split; ++z) o += partial[z * total + i];
+      const int64_t col = i % N;
+      if (bias) o += E::to_f32(bias[col]);
+      if (res) o += E::to_f32(res[i]);
+      y[i] = E::from_f32(apply_act(o, act));
+    }
   }
 }
 
@@ -815,31 +878,47 @@ sparoa_status launch_set_u64(uint64_t *p, uint64_t v, hipStream_t stream) {
   return SPAROA_OK;
 }
 
-sparoa_status launch_split_reduce(sparoa_dtype dt, const float *partial, int split, int64_t M,
-                                  int64_t N, const void *bias, const void *residual,
-                                  sparoa_act act, void *y, hipStream_t stream) {
-  const int64_t total = M * N;
-  int64_t blocks = cdiv(total, 256);
-  if (blocks > 4096) blocks = 4096;
-  const char *b = static_cast<const char *>(bias);
-  const char *r = static_cast<const char *>(residual);
-  char *o = static_cast<char *>(y);
-  switch (dt) {
+sparoa_status launch_split_reduce_group(const SplitReduceJob *jobs, int n, hipStream_t stream) {
+  if (n < 1 || n > kGroupMax) return fail(SPAROA_ERR_INVALID_ARG, "split reduce: group size");
+  ReduceGroup g;
+  g.n = n;
+  int64_t wg = 0;
+  for (int j = 0; j < n; ++j) {
+    const SplitReduceJob &r = jobs[j];
+    if (r.dt != jobs[0].dt) return fail(SPAROA_ERR_INVALID_ARG, "split reduce: mixed dtypes");
+    // 16-byte vectors need N % 8 == 0 and 16-byte aligned rows of bias / residual / y
+    const int64_t items = r.N % 8 == 0 ? r.M * r.N / 8 : r.M * r.N;
+    int64_t blocks = cdiv(items, 256);
+    if (blocks > 2048) blocks = 2048;
+    g.wg_begin[j] = (int)wg;
+    g.partial[j] = r.partial;
+    g.split[j] = r.split;
+    g.M[j] = r.M;
+    g.N[j] = r.N;
+    g.bias[j] = static_cast<const char *>(r.bias);
+    g.residual[j] = static_cast<const char *>(r.residual);
+    g.act[j] = (int)r.act;
+    g.y[j] = static_cast<char *>(r.y);
+    wg += blocks;
+  }
+  g.wg_begin[n] = (int)wg;
+  switch (jobs[0].dt) {
     case SPAROA_BF16:
-      hipLaunchKernelGGL(split_reduce<SPAROA_BF16>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                         partial, split, M, N, b, r, (int)act, o);
+      hipLaunchKernelGGL(split_reduce_group<SPAROA_BF16>, dim3((unsigned)wg), dim3(256), 0, stream, g);
       break;
     case SPAROA_F16:
-      hipLaunchKernelGGL(split_reduce<SPAROA_F16>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                         partial, split, M, N, b, r, (int)act, o);
+      hipLaunchKernelGGL(split_reduce_group<SPAROA_F16>, dim3((unsigned)wg), dim3(256), 0, stream, g);
       break;
     case SPAROA_F32:
-      hipLaunchKernelGGL(split_reduce<SPAROA_F32>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                         partial, split, M, N, b, r, (int)act, o);
+      hipLaunchKernelGGL(split_reduce_group<SPAROA_F32>, dim3((unsigned)wg), dim3(256), 0, stream, g);
       break;
   }
-  SPAROA_LAUNCH_CHECK("split_reduce");
+  SPAROA_LAUNCH_CHECK("split_reduce_group");
   return SPAROA_OK;
+}
+
+sparoa_status launch_split_reduce(const SplitReduceJob &job, hipStream_t stream) {
+  return launch_split_reduce_group(&job, 1, stream);
 }
 
 namespace {
@@ -929,7 +1008,7 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
                                const void *w, const void *bias, const void *residual,
                                sparoa_act act, const uint32_t *mask, void *y, void *ws,
                                size_t ws_bytes, uint64_t *executed, hipStream_t stream,
-                               const DeviceRoute *route) {
+                               const DeviceRoute *route, SplitReduceJob *defer) {
   const Shape s = shape_of(d);
   const GemmTileChoice t = gemm_choose(d, path);
   const int epv = d.dtype == SPAROA_F32 ? 4 : 8;
@@ -994,9 +1073,13 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   }
   if (!ok) return fail(SPAROA_ERR_UNSUPPORTED, "GEMM tile shape");
   SPAROA_LAUNCH_CHECK("gemm_kernel");
-  if (gz > 1)
-    return launch_split_reduce(d.dtype, a.partial, a.split, s.M, s.N, bias, residual, act, y,
-                               stream);
+  const SplitReduceJob job{d.dtype, a.partial, gz > 1 ? (int)gz : 0, s.M, s.N, bias, residual,
+                           act, y};
+  if (defer) {
+    *defer = job;
+    return SPAROA_OK;
+  }
+  if (gz > 1) return launch_split_reduce(job, stream);
   return SPAROA_OK;
 }
 

@@ -217,16 +217,16 @@ __global__ __launch_bounds__(kThreads) void measure_main(
 constexpr int kLanebitThreads = 1024;  // one work-group per CU, 16 waves
 constexpr int kLanebitUnroll = 4;
 
+// Work-group `bid` of `nblk` measuring one tensor.
 template <int ESZ, int V>
-__global__ __launch_bounds__(kLanebitThreads) void measure_lanebit(const char *__restrict__ x,
-                                                                   int64_t items, int64_t words,
-                                                                   uint32_t *__restrict__ mask,
-                                                                   sparoa_counts *counts) {
+__device__ __forceinline__ void lanebit_pass(const char *__restrict__ x, int64_t items,
+                                             int64_t words, uint32_t *__restrict__ mask,
+                                             sparoa_counts *counts, int64_t bid, int64_t nblk) {
   constexpr int NT = kLanebitThreads;
   const int lane = threadIdx.x & 63;
-  const int64_t slot = (int64_t)gridDim.x * NT;
+  const int64_t slot = nblk * NT;
   uint64_t zeros = 0, nonzero = 0;
-  for (int64_t base = (int64_t)blockIdx.x * NT; base < items; base += slot * kLanebitUnroll) {
+  for (int64_t base = bid * NT; base < items; base += slot * kLanebitUnroll) {
     // unconditional loads (items past the end re-read the last item and are
     // masked), so all kLanebitUnroll stay in flight
     uint32_t nz[kLanebitUnroll];
@@ -251,6 +251,44 @@ __global__ __launch_bounds__(kLanebitThreads) void measure_lanebit(const char *_
     }
   }
   wg_commit<NT>(zeros, nonzero, counts, nullptr);
+}
+
+template <int ESZ, int V>
+__global__ __launch_bounds__(kLanebitThreads) void measure_lanebit(const char *__restrict__ x,
+                                                                   int64_t items, int64_t words,
+                                                                   uint32_t *__restrict__ mask,
+                                                                   sparoa_counts *counts) {
+  lanebit_pass<ESZ, V>(x, items, words, mask, counts, blockIdx.x, gridDim.x);
+}
+
+// Several tensors of one element size in the lanebit layout, one launch:
+// work-groups are dealt to the tensors in proportion to their size.
+struct LanebitGroup {
+  int n;
+  int wg_begin[kGroupMax + 1];
+  const char *x[kGroupMax];
+  int64_t items[kGroupMax];
+  uint32_t *mask[kGroupMax];
+  sparoa_counts *counts[kGroupMax];
+};
+
+template <int V>
+__global__ void measure_init_group(LanebitGroup g) {
+  const int j = threadIdx.x;
+  if (j < g.n) {
+    g.counts[j]->zeros = 0;
+    g.counts[j]->numel = (uint64_t)g.items[j] * V;
+    g.counts[j]->zero_blocks = (uint64_t)g.items[j];  // nonzero blocks are subtracted
+    g.counts[j]->num_blocks = (uint64_t)g.items[j];
+  }
+}
+
+template <int ESZ, int V>
+__global__ __launch_bounds__(kLanebitThreads) void measure_lanebit_group(LanebitGroup g) {
+  int j = 0;
+  while (j + 1 < g.n && (int)blockIdx.x >= g.wg_begin[j + 1]) ++j;
+  lanebit_pass<ESZ, V>(g.x[j], g.items[j], (g.items[j] + 31) / 32, g.mask[j], g.counts[j],
+                       blockIdx.x - g.wg_begin[j], g.wg_begin[j + 1] - g.wg_begin[j]);
 }
 
 // The lanebit layout measured by one work-group that also writes all four
@@ -442,6 +480,47 @@ void launch_main(dim3 grid, hipStream_t st, const void *x, int64_t cols, int64_t
 }
 
 }  // namespace
+
+bool measure_groupable(const MeasureJob &j) {
+  const int vw = 16 / (int)elem_size(j.dt);
+  return j.mask && j.cols % vw == 0 && j.block_rows == 1 && j.block_cols == vw;
+}
+
+sparoa_status launch_measure_group(const MeasureJob *jobs, int n, hipStream_t stream) {
+  if (n < 1 || n > kGroupMax) return fail(SPAROA_ERR_INVALID_ARG, "measure group: size");
+  const int esz = (int)elem_size(jobs[0].dt);
+  LanebitGroup g;
+  g.n = n;
+  int64_t wg = 0;
+  for (int j = 0; j < n; ++j) {
+    const MeasureJob &m = jobs[j];
+    if (!measure_groupable(m) || (int)elem_size(m.dt) != esz)
+      return fail(SPAROA_ERR_INVALID_ARG, "measure group: layout or element size");
+    g.wg_begin[j] = (int)wg;
+    g.x[j] = static_cast<const char *>(m.x);
+    g.items[j] = m.rows * (m.cols / (16 / esz));
+    g.mask[j] = m.mask;
+    g.counts[j] = m.counts;
+    int64_t b = cdiv(g.items[j], (int64_t)kLanebitThreads);
+    if (b > 256) b = 256;
+    if (b < 1) b = 1;
+    wg += b;
+  }
+  g.wg_begin[n] = (int)wg;
+  if (esz == 2) {
+    hipLaunchKernelGGL(measure_init_group<8>, dim3(1), dim3(64), 0, stream, g);
+    SPAROA_LAUNCH_CHECK("measure_init_group");
+    hipLaunchKernelGGL((measure_lanebit_group<2, 8>), dim3((unsigned)wg), dim3(kLanebitThreads), 0,
+                       stream, g);
+  } else {
+    hipLaunchKernelGGL(measure_init_group<4>, dim3(1), dim3(64), 0, stream, g);
+    SPAROA_LAUNCH_CHECK("measure_init_group");
+    hipLaunchKernelGGL((measure_lanebit_group<4, 4>), dim3((unsigned)wg), dim3(kLanebitThreads), 0,
+                       stream, g);
+  }
+  SPAROA_LAUNCH_CHECK("measure_lanebit_group");
+  return SPAROA_OK;
+}
 
 sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64_t cols,
                              int64_t block_rows, int64_t block_cols, int64_t samples,

@@ -185,3 +185,21 @@ def test_tiling_and_skip_block_queries():
     assert abi.sparoa_fc_tiling(f, abi.PATH_SKIP_BW) == (8, 1)
     assert abi.sparoa_fc_packed_bytes(f) == 4096 * 4096 * 2
     assert abi.sparoa_fc_packed_bytes(abi.fc_desc(1, 100, 65)) == 80 * 100 * 2   # 16-column panels
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"),
+                    reason="host-only check: the fake device pointers must never reach a GPU")
+def test_executor_chained_batch_without_events_fails_cleanly_without_a_gpu():
+    """Regression: a chained batch (op 1 reads op 0's output) with no events
+    takes the op-by-op route; with no GPU present it must report the HIP
+    error of its first launch, not dereference the missing event array."""
+    d = abi.fc_desc(128, 256, 256, abi.BF16)
+    y0 = 0x200000000
+    t = abi.Thresholds(0.5, 315.0, abi.ROUTE_BLOCK)
+    ops = [abi.FcOp(d, 0x100000000, 0x110000000, 0x120000000, None, None, abi.ACT_RELU,
+                    0x130000000, 0x140000000, y0, 0x150000000, 1 << 20, 0x160000000, t),
+           abi.FcOp(d, y0, 0x170000000, 0x180000000, None, None, abi.ACT_RELU, 0x190000000,
+                    0x1a0000000, 0x1b0000000, 0x1c0000000, 1 << 20, 0x1d0000000, t)]
+    arr = (abi.FcOp * 2)(*ops)
+    st = abi._L.sparoa_fc_ops_run(arr, 2, None, None, None)
+    assert st == 4, abi._L.sparoa_last_error()

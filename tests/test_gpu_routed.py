@@ -265,6 +265,82 @@ def test_fc_ops_run_equals_per_op_routed_calls():
         assert evs[2 * i].elapsed_time(evs[2 * i + 1]) > 0
 
 
+def _batch_op(abi, dev, d, x, seed, thr=None, residual=None):
+    m, k, n = d.m, d.k, d.n
+    tdt = torch.float16 if d.dtype == abi.F16 else torch.bfloat16
+    w = synth.normal((n, k), "f16" if d.dtype == abi.F16 else "bf16", seed, std=k ** -0.5).to(dev)
+    wp = torch.empty(abi.sparoa_fc_packed_bytes(d) // 2, dtype=tdt, device=dev)
+    abi.sparoa_fc_pack_weights(d, w, wp)
+    fam = abi.PATH_SKIP_BW if abi.sparoa_op_intensity_fc(d)["intensity"] < (thr or (0.5, 315.0))[1] \
+        else abi.PATH_SKIP_MFMA
+    br, bc = abi.sparoa_fc_skip_block(d, fam)
+    return dict(d=d, x=x, w=w, wp=wp, br=br, bc=bc, res=residual,
+                thr=thr or (0.5, 315.0),
+                counts=torch.zeros(4, dtype=torch.int64, device=dev),
+                mask=torch.zeros(abi.sparoa_mask_words(m, k, br, bc), dtype=torch.int32, device=dev),
+                y=torch.full((m, n), float("nan"), dtype=tdt, device=dev),
+                ws=torch.zeros(max(16, max(abi.sparoa_fc_workspace_size(d, p) for p in range(4))),
+                               dtype=torch.uint8, device=dev),
+                path=torch.full((1,), -1, dtype=torch.int32, device=dev))
+
+
+def test_fc_ops_run_batched_equals_op_by_op():
+    """The batched executor (grouped measurements and split-K reductions,
+    here 20 GEMM-family ops in two dtypes next to streaming ops, so groups
+    fill and spill over 16) gives every op the counts, bitmap, path and
+    output bits of op-by-op sparoa_fc_measured calls; a chained pair (an
+    op's output is the next op's input) is detected and run in order."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    bufs = []
+    for i in range(24):
+        if i % 6 == 0:      # streaming, self-measuring
+            m, k, n, dt = 8, 1024, 256, abi.BF16
+        else:               # GEMM family (m > 64), split-K
+            m, k, n, dt = 96 + 8 * (i % 3), 1024, 128, (abi.F16 if i % 2 else abi.BF16)
+        d = abi.fc_desc(m, k, n, dt)
+        x = synth.sparse_matrix(m, k, 0.3 + 0.02 * i, "block" if i % 4 else "iid",
+                                "f16" if dt == abi.F16 else "bf16", 600 + i).to(dev)
+        # intensity threshold 0 puts the m > 64 ops on the MFMA family
+        bufs.append(_batch_op(abi, dev, d, x, 700 + i,
+                              thr=(0.25 + 0.02 * i, 315.0 if i % 6 == 0 else 0.0)))
+    ops = [abi.fc_op(b["d"], b["x"], b["w"], b["wp"], None, b["res"], abi.ACT_RELU, b["counts"],
+                     b["mask"], b["y"], b["ws"], b["path"], (b["thr"][0], b["thr"][1], abi.ROUTE_BLOCK))
+           for b in bufs]
+    abi.sparoa_fc_ops_run(abi.fc_op_array(ops))
+    torch.cuda.synchronize()
+    for i, b in enumerate(bufs):
+        c2 = torch.zeros_like(b["counts"])
+        k2 = torch.zeros_like(b["mask"])
+        y2 = torch.full_like(b["y"], float("nan"))
+        p2 = torch.full((1,), -1, dtype=torch.int32, device=dev)
+        abi.sparoa_fc_measured(b["d"], b["thr"][0], b["thr"][1], abi.ROUTE_BLOCK, b["x"], b["w"],
+                               b["wp"], None, b["res"], abi.ACT_RELU, c2, k2, y2, b["ws"], p2)
+        torch.cuda.synchronize()
+        assert torch.equal(c2, b["counts"]), f"op {i}"
+        assert torch.equal(k2, b["mask"]), f"op {i}"
+        assert int(p2.item()) == int(b["path"].item()), f"op {i}"
+        assert torch.equal(y2, b["y"]), f"op {i}"
+    # a chain: op 1 reads op 0's output (same shape in and out)
+    d = abi.fc_desc(128, 256, 256, abi.BF16)
+    x0 = synth.sparse_matrix(128, 256, 0.5, "block", "bf16", 620).to(dev)
+    b0 = _batch_op(abi, dev, d, x0, 720)
+    b1 = _batch_op(abi, dev, d, b0["y"], 721)
+    ops = [abi.fc_op(b["d"], b["x"], b["w"], b["wp"], None, None, abi.ACT_RELU, b["counts"],
+                     b["mask"], b["y"], b["ws"], b["path"]) for b in (b0, b1)]
+    abi.sparoa_fc_ops_run(abi.fc_op_array(ops), 0.5, 315.0, abi.ROUTE_BLOCK)
+    torch.cuda.synchronize()
+    y_chain = b1["y"].clone()
+    ref = oracle.measure(b0["y"].cpu(), 128, 256, b1["br"], b1["bc"])
+    assert b1["counts"].cpu().tolist() == [ref["zeros"], ref["numel"], ref["zero_blocks"],
+                                           ref["num_blocks"]]
+    y2 = torch.full_like(y_chain, float("nan"))
+    abi.sparoa_fc_measured(d, 0.5, 315.0, abi.ROUTE_BLOCK, b0["y"], b1["w"], b1["wp"], None, None,
+                           abi.ACT_RELU, b1["counts"], b1["mask"], y2, b1["ws"], b1["path"])
+    torch.cuda.synchronize()
+    assert torch.equal(y2, y_chain)
+
+
 def test_fc_ops_run_in_a_hip_graph_equals_eager():
     """The executor captured in a HIP graph: every replay (with eager work and
     synchronisations in between) gives the eager run's counts, paths and
