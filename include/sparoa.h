@@ -297,6 +297,42 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
                                size_t ws_bytes, uint32_t *path_dev, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Routed conv / FC that also measures its own output, the next layer's input
+ * (the sparsity feature of Eq. 1 is taken on a layer's output activation,
+ * SparOA Section 3.1; here the producer emits it instead of a separate pass).
+ *   y_counts, y_mask (device, required): afterwards they hold exactly what
+ *   sparoa_measure_sparsity(y, dtype, rows, cols, 1, 8, 0, ...) gives, with
+ *   rows = n*Ho*Wo, cols = c_out (FC: rows = m, cols = n) -- the block shape
+ *   every conv and MFMA-family FC consumer skips at.  y_mask holds
+ *   sparoa_mask_words(rows, cols, 1, 8) words and needs no clearing.
+ *   y_counts must hold {0, rows*cols, nb, nb} on entry, nb = rows*ceil(cols/8):
+ *   the fused form adds into it (a caller resets all of a network's counters
+ *   with one copy from a template before each pass).
+ *   Fused into the GEMM epilogue (or its split-K reduction) when the 16-bit
+ *   64-channel-chunk implicit GEMM serves the layer and cols % 64 == 0: no
+ *   launch of its own and no second read of y; otherwise the standalone
+ *   measurement of y runs after the layer (and overwrites y_counts).
+ *   Other arguments as for sparoa_conv2d_routed / sparoa_fc_routed.
+ * Errors: theirs, and INVALID_ARG for a null y_counts or y_mask.
+ * ---------------------------------------------------------------------- */
+sparoa_status sparoa_conv2d_routed_measured(const sparoa_conv_desc *desc,
+                                            const sparoa_thresholds *thr,
+                                            const sparoa_counts *counts_dev, const void *x,
+                                            const void *w, const void *bias, const void *residual,
+                                            sparoa_act act, const uint32_t *mask, void *y,
+                                            void *workspace, size_t ws_bytes, uint32_t *path_dev,
+                                            sparoa_counts *y_counts, uint32_t *y_mask,
+                                            hipStream_t stream);
+sparoa_status sparoa_fc_routed_measured(const sparoa_fc_desc *desc, const sparoa_thresholds *thr,
+                                        const sparoa_counts *counts_dev, const void *x,
+                                        const void *w_nk, const void *w_packed, const void *bias,
+                                        const void *residual, sparoa_act act,
+                                        const uint32_t *mask, void *y, void *workspace,
+                                        size_t ws_bytes, uint32_t *path_dev,
+                                        sparoa_counts *y_counts, uint32_t *y_mask,
+                                        hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * The whole path of one FC operator -- measure, route, execute (SparOA
  * Section 3.1 sparsity feature, Eq. 1; Section 2.2 quadrant routing) -- in
  * one call and no host round trip.

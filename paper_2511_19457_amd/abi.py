@@ -31,7 +31,7 @@ EXPORTS = [
     "sparoa_fc_tiling", "sparoa_fc_workspace_size", "sparoa_fc_skip_block", "sparoa_fc",
     "sparoa_fc_dense", "sparoa_fc_zero_skip", "sparoa_maxpool2d", "sparoa_conv2d_routed",
     "sparoa_fc_routed", "sparoa_fc_uses_packed", "sparoa_fc_ops_run",
-    "sparoa_fc_measured",
+    "sparoa_fc_measured", "sparoa_conv2d_routed_measured", "sparoa_fc_routed_measured",
 ]
 
 
@@ -133,6 +133,12 @@ def _load():
                                                 ctypes.c_int, vp, vp, vp, sz, vp, vp]),
         "sparoa_fc_routed": (ctypes.c_int, [P(FcDesc), P(Thresholds), vp, vp, vp, vp, vp, vp,
                                             ctypes.c_int, vp, vp, vp, sz, vp, vp]),
+        "sparoa_conv2d_routed_measured": (ctypes.c_int, [P(ConvDesc), P(Thresholds), vp, vp, vp,
+                                                         vp, vp, ctypes.c_int, vp, vp, vp, sz, vp,
+                                                         vp, vp, vp]),
+        "sparoa_fc_routed_measured": (ctypes.c_int, [P(FcDesc), P(Thresholds), vp, vp, vp, vp, vp,
+                                                     vp, ctypes.c_int, vp, vp, vp, sz, vp, vp, vp,
+                                                     vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -362,6 +368,30 @@ def sparoa_fc_routed(desc, sparsity_thr, intensity_thr, mode, counts, x, w_nk, w
                                _ptr(w_nk), _ptr(w_packed), _ptr(bias), _ptr(residual), act,
                                _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes, _ptr(path),
                                _stream(stream)))
+
+
+def sparoa_conv2d_routed_measured(desc, sparsity_thr, intensity_thr, mode, counts, x, w, bias,
+                                  residual, act, mask, y, y_counts, y_mask, workspace=None,
+                                  path=None, stream=None):
+    """sparoa_conv2d_routed that also measures y into y_counts / y_mask."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    t = Thresholds(sparsity_thr, intensity_thr, mode)
+    _check(_L.sparoa_conv2d_routed_measured(
+        ctypes.byref(desc), ctypes.byref(t), _ptr(counts), _ptr(x), _ptr(w), _ptr(bias),
+        _ptr(residual), act, _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes, _ptr(path),
+        _ptr(y_counts), _ptr(y_mask), _stream(stream)))
+
+
+def sparoa_fc_routed_measured(desc, sparsity_thr, intensity_thr, mode, counts, x, w_nk, w_packed,
+                              bias, residual, act, mask, y, y_counts, y_mask, workspace=None,
+                              path=None, stream=None):
+    """sparoa_fc_routed that also measures y into y_counts / y_mask."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    t = Thresholds(sparsity_thr, intensity_thr, mode)
+    _check(_L.sparoa_fc_routed_measured(
+        ctypes.byref(desc), ctypes.byref(t), _ptr(counts), _ptr(x), _ptr(w_nk), _ptr(w_packed),
+        _ptr(bias), _ptr(residual), act, _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes,
+        _ptr(path), _ptr(y_counts), _ptr(y_mask), _stream(stream)))
 
 
 def sparoa_fc_measured(desc, sparsity_thr, intensity_thr, mode, x, w_nk, w_packed, bias, residual,

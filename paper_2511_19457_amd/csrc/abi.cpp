@@ -466,12 +466,18 @@ sparoa_status check_thr(const sparoa_thresholds *thr) {
 }
 }  // namespace
 
-sparoa_status sparoa_conv2d_routed(const sparoa_conv_desc *d, const sparoa_thresholds *thr,
-                                   const sparoa_counts *counts_dev, const void *x, const void *w,
-                                   const void *bias, const void *residual, sparoa_act act,
-                                   const uint32_t *mask, void *y, void *workspace,
-                                   size_t ws_bytes, uint32_t *path_dev, hipStream_t stream) {
-  g_last_error.clear();
+}  // extern "C"
+
+namespace {
+// The routed conv (see sparoa_conv2d_routed).  With y_counts / y_mask
+// non-null it also measures y at block (1, 8) over [N*Ho*Wo, C_out]: in the
+// GEMM's epilogue where that is fused, else by a standalone pass after it.
+sparoa_status conv_routed_impl(const sparoa_conv_desc *d, const sparoa_thresholds *thr,
+                               const sparoa_counts *counts_dev, const void *x, const void *w,
+                               const void *bias, const void *residual, sparoa_act act,
+                               const uint32_t *mask, void *y, void *workspace, size_t ws_bytes,
+                               uint32_t *path_dev, sparoa_counts *y_counts, uint32_t *y_mask,
+                               hipStream_t stream) {
   sparoa_intensity in;
   sparoa_status st = sparoa_op_intensity_conv(d, &in);
   if (st != SPAROA_OK) return st;
@@ -479,19 +485,74 @@ sparoa_status sparoa_conv2d_routed(const sparoa_conv_desc *d, const sparoa_thres
   if (!counts_dev || !x || !w || !y || !mask || !act_ok(act))
     return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed: null counts/x/w/mask/y or bad act");
   if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed: has_bias without bias");
-  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace})) != SPAROA_OK) return st;
+  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace, y_counts, y_mask})) != SPAROA_OK)
+    return st;
+  const bool measure_y = y_counts != nullptr;
+  if (measure_y != (y_mask != nullptr))
+    return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed_measured: null y_counts or y_mask");
   const bool dw = is_depthwise(*d);
   const int bw = (dw || in.intensity < thr->intensity_thr) ? 1 : 0;
   const DeviceRoute r{counts_dev, thr->sparsity_thr, thr->mode, bw, path_dev};
-  if (dw) return launch_depthwise(*d, x, w, d->has_bias ? bias : nullptr, residual, act, y, stream, &r);
+  int64_t ho = 0, wo = 0;
+  if ((st = check_conv(d, &ho, &wo)) != SPAROA_OK) return st;
+  const int64_t rows = d->n * ho * wo, cols = d->c_out;
+  auto measure_after = [&]() {
+    return measure_y ? launch_measure(y, d->dtype, rows, cols, 1, 8, 0, y_counts, y_mask, nullptr,
+                                      stream)
+                     : SPAROA_OK;
+  };
+  if (dw) {
+    if ((st = launch_depthwise(*d, x, w, d->has_bias ? bias : nullptr, residual, act, y, stream,
+                               &r)) != SPAROA_OK)
+      return st;
+    return measure_after();
+  }
   if (d->groups != 1) return fail(SPAROA_ERR_UNSUPPORTED, "grouped (non-depthwise) conv");
   const sparoa_path p = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
   if (ws_bytes < gemm_workspace(*d, p)) return fail(SPAROA_ERR_WORKSPACE, "conv2d_routed: workspace too small");
   // without a skip kernel for this shape the dense kernel runs and records a dense path
   const bool can_skip = gemm_skip_supported(*d);
-  return launch_gemm_conv(*d, p, x, w, d->has_bias ? bias : nullptr, residual, act,
-                          can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r);
+  if (measure_y && gemm_fuses_out_measure(*d, p)) {   // y_counts arrives initialised
+    const OutMeasure om{y_counts, y_mask};
+    return launch_gemm_conv(*d, p, x, w, d->has_bias ? bias : nullptr, residual, act,
+                            can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r,
+                            nullptr, &om);
+  }
+  if ((st = launch_gemm_conv(*d, p, x, w, d->has_bias ? bias : nullptr, residual, act,
+                             can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream,
+                             &r)) != SPAROA_OK)
+    return st;
+  return measure_after();
 }
+}  // namespace
+
+extern "C" {
+
+sparoa_status sparoa_conv2d_routed(const sparoa_conv_desc *d, const sparoa_thresholds *thr,
+                                   const sparoa_counts *counts_dev, const void *x, const void *w,
+                                   const void *bias, const void *residual, sparoa_act act,
+                                   const uint32_t *mask, void *y, void *workspace,
+                                   size_t ws_bytes, uint32_t *path_dev, hipStream_t stream) {
+  g_last_error.clear();
+  return conv_routed_impl(d, thr, counts_dev, x, w, bias, residual, act, mask, y, workspace,
+                          ws_bytes, path_dev, nullptr, nullptr, stream);
+}
+
+sparoa_status sparoa_conv2d_routed_measured(const sparoa_conv_desc *d,
+                                            const sparoa_thresholds *thr,
+                                            const sparoa_counts *counts_dev, const void *x,
+                                            const void *w, const void *bias, const void *residual,
+                                            sparoa_act act, const uint32_t *mask, void *y,
+                                            void *workspace, size_t ws_bytes, uint32_t *path_dev,
+                                            sparoa_counts *y_counts, uint32_t *y_mask,
+                                            hipStream_t stream) {
+  g_last_error.clear();
+  if (!y_counts || !y_mask)
+    return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed_measured: null y_counts or y_mask");
+  return conv_routed_impl(d, thr, counts_dev, x, w, bias, residual, act, mask, y, workspace,
+                          ws_bytes, path_dev, y_counts, y_mask, stream);
+}
+
 
 }  // extern "C"
 
@@ -502,7 +563,8 @@ sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *t
                              const void *w_packed, const void *bias, const void *residual,
                              sparoa_act act, const uint32_t *mask, void *y, void *workspace,
                              size_t ws_bytes, uint32_t *path_dev, hipStream_t stream,
-                             SplitReduceJob *defer) {
+                             SplitReduceJob *defer, sparoa_counts *y_counts = nullptr,
+                             uint32_t *y_mask = nullptr) {
   if (defer) defer->split = 0;
   sparoa_intensity in;
   sparoa_status st = sparoa_op_intensity_fc(d, &in);
@@ -514,18 +576,40 @@ sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *t
   if (!counts_dev || !x || !w || !y || !mask || !act_ok(act))
     return fail(SPAROA_ERR_INVALID_ARG, "fc_routed: null counts/x/weights/mask/y or bad act");
   if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "fc_routed: has_bias without bias");
-  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace})) != SPAROA_OK) return st;
+  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace, y_counts, y_mask})) != SPAROA_OK)
+    return st;
+  const bool measure_y = y_counts != nullptr;
+  if (measure_y != (y_mask != nullptr))
+    return fail(SPAROA_ERR_INVALID_ARG, "fc_routed_measured: null y_counts or y_mask");
+  auto measure_after = [&]() {
+    return measure_y ? launch_measure(y, d->dtype, d->m, d->n, 1, 8, 0, y_counts, y_mask, nullptr,
+                                      stream)
+                     : SPAROA_OK;
+  };
   const DeviceRoute r{counts_dev, thr->sparsity_thr, thr->mode, bw, path_dev};
-  if (streams)
-    return launch_fc_bw(*d, SPAROA_PATH_SKIP_BW, x, w, d->has_bias ? bias : nullptr, residual, act,
-                        mask, y, workspace, ws_bytes, nullptr, stream, &r);
+  if (streams) {
+    if ((st = launch_fc_bw(*d, SPAROA_PATH_SKIP_BW, x, w, d->has_bias ? bias : nullptr, residual,
+                           act, mask, y, workspace, ws_bytes, nullptr, stream, &r)) != SPAROA_OK)
+      return st;
+    return measure_after();
+  }
   const sparoa_conv_desc c = fc_as_conv(*d);
   const sparoa_path p = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
   if (ws_bytes < gemm_workspace(c, p)) return fail(SPAROA_ERR_WORKSPACE, "fc_routed: workspace too small");
   const bool can_skip = gemm_skip_supported(c);
-  return launch_gemm_conv(c, p, x, w, d->has_bias ? bias : nullptr, residual, act,
-                          can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r,
-                          defer);
+  if (measure_y && gemm_fuses_out_measure(c, p)) {   // y_counts arrives initialised
+    const OutMeasure om{y_counts, y_mask};
+    return launch_gemm_conv(c, p, x, w, d->has_bias ? bias : nullptr, residual, act,
+                            can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r,
+                            defer, &om);
+  }
+  if ((st = launch_gemm_conv(c, p, x, w, d->has_bias ? bias : nullptr, residual, act,
+                             can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream,
+                             &r, defer)) != SPAROA_OK)
+    return st;
+  if (measure_y && defer && defer->split > 1)   // the caller reduces later: cannot measure y now
+    return fail(SPAROA_ERR_UNSUPPORTED, "fc_routed_measured: deferred reduction");
+  return measure_after();
 }
 
 // How sparoa_fc_measured runs one FC: the self-measuring streaming kernel
@@ -570,6 +654,21 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *d, const sparoa_thresholds 
   g_last_error.clear();
   return fc_routed_impl(d, thr, counts_dev, x, w_nk, w_packed, bias, residual, act, mask, y,
                         workspace, ws_bytes, path_dev, stream, nullptr);
+}
+
+sparoa_status sparoa_fc_routed_measured(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
+                                        const sparoa_counts *counts_dev, const void *x,
+                                        const void *w_nk, const void *w_packed, const void *bias,
+                                        const void *residual, sparoa_act act,
+                                        const uint32_t *mask, void *y, void *workspace,
+                                        size_t ws_bytes, uint32_t *path_dev,
+                                        sparoa_counts *y_counts, uint32_t *y_mask,
+                                        hipStream_t stream) {
+  g_last_error.clear();
+  if (!y_counts || !y_mask)
+    return fail(SPAROA_ERR_INVALID_ARG, "fc_routed_measured: null y_counts or y_mask");
+  return fc_routed_impl(d, thr, counts_dev, x, w_nk, w_packed, bias, residual, act, mask, y,
+                        workspace, ws_bytes, path_dev, stream, nullptr, y_counts, y_mask);
 }
 
 sparoa_status sparoa_fc_measured(const sparoa_fc_desc *d, const sparoa_thresholds *thr,

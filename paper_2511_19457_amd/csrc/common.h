@@ -92,10 +92,22 @@ struct SplitReduceJob {
   const void *bias, *residual;
   sparoa_act act;
   void *y;
+  sparoa_counts *om_counts;  // non-null: measure y (see OutMeasure)
+  uint32_t *om_mask;
 };
 sparoa_status launch_split_reduce(const SplitReduceJob &job, hipStream_t stream);
 // Several reductions of one dtype in one launch (n <= kGroupMax).
 sparoa_status launch_split_reduce_group(const SplitReduceJob *jobs, int n, hipStream_t stream);
+
+// Measurement of a producer's output in its own epilogue (the next layer's
+// input): counts and the bitmap at block (1 row, 8 channels) of y viewed as
+// [M = N*Ho*Wo, C_out] -- exactly what launch_measure gives for that view.
+// counts must hold {0, numel, nb, nb} before the producer runs (the caller
+// resets them); the bitmap needs no clearing.
+struct OutMeasure {
+  sparoa_counts *counts;
+  uint32_t *mask;
+};
 
 // Implicit-GEMM MFMA conv (groups == 1); FC runs through it as a 1x1 conv.
 struct GemmTileChoice {
@@ -112,9 +124,13 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
                                sparoa_act act, const uint32_t *mask, void *y, void *ws,
                                size_t ws_bytes, uint64_t *executed, hipStream_t stream,
                                const DeviceRoute *route = nullptr,
-                               SplitReduceJob *defer = nullptr);
+                               SplitReduceJob *defer = nullptr,
+                               const OutMeasure *om = nullptr);
 // defer: when non-null, a split-K reduction is described there (split > 1)
 // instead of launched; split = 0 when the GEMM needs none.
+// om: measure y in the epilogue (or in the split-K reduction); only when
+// gemm_fuses_out_measure(d, path) -- otherwise the call fails.
+bool gemm_fuses_out_measure(const sparoa_conv_desc &d, sparoa_path path);
 
 // Writes v to *p on the stream with a one-lane kernel (no memset node).
 sparoa_status launch_set_u64(uint64_t *p, uint64_t v, hipStream_t stream);

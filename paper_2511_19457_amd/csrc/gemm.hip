@@ -61,6 +61,8 @@ struct GemmArgs {
   int act;
   int split;
   DeviceRoute route;
+  sparoa_counts *om_counts;  // non-null: the epilogue measures y (OutMeasure)
+  uint32_t *om_mask;
 };
 
 template <int DT>
@@ -362,6 +364,32 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
       }
 }
 
+// Adds a work-group's zero count and nonzero-block count into counts (one
+// atomic per counter per work-group; zero_blocks starts at nb).
+__device__ __forceinline__ void om_commit(uint32_t zeros, uint32_t nz, sparoa_counts *counts) {
+  __shared__ uint32_t part[2][16];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    zeros += __shfl_xor(zeros, o, 64);
+    nz += __shfl_xor(nz, o, 64);
+  }
+  if (lane == 0) {
+    part[0][wave] = zeros;
+    part[1][wave] = nz;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long z = 0, n = 0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) {
+      z += part[0][i];
+      n += part[1][i];
+    }
+    if (z) atomicAdd((unsigned long long *)&counts->zeros, z);
+    if (n) atomicAdd((unsigned long long *)&counts->zero_blocks, 0ull - n);
+  }
+}
+
 // Sums the K-split partials in split order, adds bias and residual, then
 // applies the activation.  Grouped form: up to kGroupMax reductions of one
 // dtype in one launch, work-groups dealt to the jobs in proportion to their
@@ -376,6 +404,8 @@ struct ReduceGroup {
   const char *bias[kGroupMax], *residual[kGroupMax];
   int act[kGroupMax];
   char *y[kGroupMax];
+  sparoa_counts *om_counts[kGroupMax];  // non-null: measure y (16-bit, N % 8 == 0)
+  uint32_t *om_mask[kGroupMax];
 };
 
 template <int DT>
@@ -391,6 +421,13 @@ __global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
   const raw *bias = reinterpret_cast<const raw *>(g.bias[j]);
   const raw *res = reinterpret_cast<const raw *>(g.residual[j]);
   raw *y = reinterpret_cast<raw *>(g.y[j]);
+  // output measurement: vector v = block v at (1 row, 8 channels); a wave's
+  // 64 consecutive vectors are two whole bitmap words (as in measure_lanebit)
+  sparoa_counts *om = E::size == 2 ? g.om_counts[j] : nullptr;
+  uint32_t *om_mask = g.om_mask[j];
+  const int lane = threadIdx.x & 63;
+  const int64_t om_words = (total / 8 + 31) / 32;
+  uint32_t om_zeros = 0, om_nz = 0;
   if (N % 8 == 0) {
     for (int64_t v = b0 * 256 + threadIdx.x; v < total / 8; v += nb * 256) {
       const int64_t i = v * 8, col = i % N;
@@ -428,10 +465,25 @@ __global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
         uint4 q;
         __builtin_memcpy(&q, t, 16);
         *reinterpret_cast<uint4 *>(y + i) = q;
+        if (om) {
+          uint32_t nzb = 0;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const bool z = (t[e] & 0x7FFFu) == 0u;
+            om_zeros += z ? 1u : 0u;
+            nzb |= z ? 0u : 1u;
+          }
+          om_nz += nzb;
+          const uint64_t bal = __ballot(nzb != 0u);
+          const int64_t w0 = (v - lane) >> 5;
+          if (lane == 0 && w0 < om_words) om_mask[w0] = (uint32_t)bal;
+          if (lane == 32 && w0 + 1 < om_words) om_mask[w0 + 1] = (uint32_t)(bal >> 32);
+        }
       } else {
         for (int e = 0; e < 8; ++e) y[i + e] = t[e];
       }
     }
+    if (om) om_commit(om_zeros, om_nz, om);
   } else {
     for (int64_t i = b0 * 256 + threadIdx.x; i < total; i += nb * 256) {
       float o = 0.f;
@@ -748,9 +800,58 @@ __global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
   __syncthreads();
   constexpr int C8 = BN / 8;
   const bool vec_n = a.N % 8 == 0;
+  // Output measurement (host: no split, N % 64 == 0, BN == 64): the 8 lanes
+  // of a tile row hold one bitmap byte (8 channel blocks of 8); every lane
+  // stays in the loop for the ballot.
+  const bool om = BN == 64 && a.om_counts != nullptr;
+  uint32_t om_zeros = 0, om_nz = 0;
   for (int q = tid; q < BM * C8; q += kThreads) {
     const int r = q / C8, c = (q % C8) * 8;
     const int64_t row = m0 + r, col = n0 + c;
+    if (om) {
+      const bool valid = row < a.M;
+      uint32_t nzb = 0;
+      if (valid) {
+        float o[8];
+        const float4 lo = *reinterpret_cast<const float4 *>(&ct[r * CS + c]);
+        const float4 hi = *reinterpret_cast<const float4 *>(&ct[r * CS + c + 4]);
+        o[0] = lo.x; o[1] = lo.y; o[2] = lo.z; o[3] = lo.w;
+        o[4] = hi.x; o[5] = hi.y; o[6] = hi.z; o[7] = hi.w;
+        raw t[8], out[8];
+        if (a.bias) {
+          const uint4 q4 = *reinterpret_cast<const uint4 *>(reinterpret_cast<const raw *>(a.bias) + col);
+          __builtin_memcpy(t, &q4, 16);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] += E::to_f32(t[e]);
+        }
+        if (a.residual) {
+          const uint4 q4 = *reinterpret_cast<const uint4 *>(
+              reinterpret_cast<const raw *>(a.residual) + row * a.N + col);
+          __builtin_memcpy(t, &q4, 16);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] += E::to_f32(t[e]);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          out[e] = E::from_f32(apply_act(o[e], a.act));
+          const bool z = (out[e] & 0x7FFFu) == 0u;
+          om_zeros += z ? 1u : 0u;
+          nzb |= z ? 0u : 1u;
+        }
+        uint4 q4;
+        __builtin_memcpy(&q4, out, 16);
+        *reinterpret_cast<uint4 *>(reinterpret_cast<raw *>(a.y) + row * a.N + col) = q4;
+      }
+      om_nz += nzb;
+      const uint64_t bal = __ballot(nzb != 0u);
+      // rows past M still clear their byte when it lies inside the bitmap's
+      // last word (bits past the last block are 0)
+      const int64_t byte = row * (a.N / 64) + n0 / 64;
+      const int64_t mbytes = 4 * ((a.M * (a.N / 8) + 31) / 32);
+      if ((lane & 7) == 0 && (valid || byte < mbytes))
+        reinterpret_cast<uint8_t *>(a.om_mask)[byte] = valid ? (uint8_t)(bal >> (lane & ~7)) : 0;
+      continue;
+    }
     if (row >= a.M || col >= a.N) continue;
     float o[8];
     {
@@ -800,6 +901,7 @@ __global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
       }
     }
   }
+  if (om) om_commit(om_zeros, om_nz, a.om_counts);
 }
 
 template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
@@ -899,6 +1001,10 @@ sparoa_status launch_split_reduce_group(const SplitReduceJob *jobs, int n, hipSt
     g.residual[j] = static_cast<const char *>(r.residual);
     g.act[j] = (int)r.act;
     g.y[j] = static_cast<char *>(r.y);
+    g.om_counts[j] = r.om_counts;
+    g.om_mask[j] = r.om_mask;
+    if (r.om_counts && (elem_size(r.dt) != 2 || r.N % 8 != 0))
+      return fail(SPAROA_ERR_UNSUPPORTED, "split reduce: output measurement needs 16-bit, N % 8 == 0");
     wg += blocks;
   }
   g.wg_begin[n] = (int)wg;
@@ -997,6 +1103,12 @@ GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path) {
   return t;
 }
 
+bool gemm_fuses_out_measure(const sparoa_conv_desc &d, sparoa_path path) {
+  // the second-generation kernel (64-column tiles) writes whole bitmap bytes
+  // when C_out % 64 == 0; its split-K reduction measures 16-byte vectors
+  return gemm_choose(d, path).cfg != 0 && d.c_out % 64 == 0 && elem_size(d.dtype) == 2;
+}
+
 size_t gemm_workspace(const sparoa_conv_desc &d, sparoa_path path) {
   const GemmTileChoice t = gemm_choose(d, path);
   if (t.split_k <= 1) return 0;
@@ -1008,9 +1120,12 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
                                const void *w, const void *bias, const void *residual,
                                sparoa_act act, const uint32_t *mask, void *y, void *ws,
                                size_t ws_bytes, uint64_t *executed, hipStream_t stream,
-                               const DeviceRoute *route, SplitReduceJob *defer) {
+                               const DeviceRoute *route, SplitReduceJob *defer,
+                               const OutMeasure *om) {
   const Shape s = shape_of(d);
   const GemmTileChoice t = gemm_choose(d, path);
+  if (om && !gemm_fuses_out_measure(d, path))
+    return fail(SPAROA_ERR_UNSUPPORTED, "GEMM: no fused output measurement for this shape");
   const int epv = d.dtype == SPAROA_F32 ? 4 : 8;
   const bool vec = d.c_in % epv == 0;
   const bool skip = mask != nullptr;
@@ -1043,6 +1158,9 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   a.route = route ? *route : DeviceRoute{nullptr, 0.0, 0, 0, nullptr};
   const int64_t gz = cdiv(nchunks, a.chunks_per_split);
   a.split = (int)gz;
+  // the epilogue measures y when it writes y; with split-K the reduction does
+  a.om_counts = om && gz == 1 ? om->counts : nullptr;
+  a.om_mask = om && gz == 1 ? om->mask : nullptr;
   if (gz > 1 && ws_bytes < (size_t)gz * s.M * s.N * sizeof(float))
     return fail(SPAROA_ERR_WORKSPACE, "GEMM split-K workspace too small");
 
@@ -1074,7 +1192,8 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   if (!ok) return fail(SPAROA_ERR_UNSUPPORTED, "GEMM tile shape");
   SPAROA_LAUNCH_CHECK("gemm_kernel");
   const SplitReduceJob job{d.dtype, a.partial, gz > 1 ? (int)gz : 0, s.M, s.N, bias, residual,
-                           act, y};
+                           act, y, om && gz > 1 ? om->counts : nullptr,
+                           om && gz > 1 ? om->mask : nullptr};
   if (defer) {
     *defer = job;
     return SPAROA_OK;

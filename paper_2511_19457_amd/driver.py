@@ -16,8 +16,10 @@ this module only allocates buffers (PyTorch) and sequences the C calls.
 
 With ``routed=True`` steps 2-4 run without the host round trip: the counts
 stay in device memory and the routed kernels take the skip decision
-themselves (same arithmetic as sparoa_route); counts and paths are read back
-once, after the whole stack.
+themselves (same arithmetic as sparoa_route); a conv/FC whose output feeds a
+conv/FC measures that output in its own epilogue (sparoa_*_routed_measured),
+so those consumers skip their measurement pass; counts and paths are read
+back once, after the whole stack.
 """
 import time
 from dataclasses import dataclass
@@ -98,7 +100,37 @@ class Engine:
                 st["path"] = torch.zeros(1, dtype=torch.int32, device=self.dev)
             self.acts[i + 1] = torch.empty(output_shape(L), dtype=dtype, device=self.dev)
             self.st.append(st)
+        # Activations a conv/FC produces and some consumer measures at block
+        # (1, 8): in routed mode the producer measures them in its epilogue
+        # (sparoa_*_routed_measured) and those consumers skip their own pass.
+        # Their counters live in one tensor, reset from a template before
+        # each routed pass (one kernel for the whole network).
+        self.tmeas = {}
+        meas = []
+        for i, L in enumerate(layers):
+            if L.kind == "maxpool":
+                continue
+            t = i + 1
+            if any(layers[k].src == t and layers[k].kind != "maxpool" and
+                   (self.st[k]["br"], self.st[k]["bc"]) == (1, 8) for k in range(len(layers))):
+                shp = output_shape(L)
+                rows = 1
+                for v in shp[:-1]:
+                    rows *= v
+                nb = rows * -(-shp[-1] // 8)
+                meas.append((t, [0, rows * shp[-1], nb, nb], abi.sparoa_mask_words(rows, shp[-1], 1, 8)))
+        self.tm_template = torch.tensor([m[1] for m in meas] or [[0, 0, 0, 0]], dtype=torch.int64,
+                                        device=self.dev)
+        self.tm_counts = torch.zeros_like(self.tm_template)
+        for j, (t, _, words) in enumerate(meas):
+            self.tmeas[t] = dict(counts=self.tm_counts[j],
+                                 mask=torch.zeros(words, dtype=torch.int32, device=self.dev))
         torch.cuda.synchronize(self.dev)
+
+    def reset_out_counts(self):
+        """Initial values of the fused output measurements (a kernel, not a
+        memset or copy node, so a captured graph replays it safely)."""
+        torch.mul(self.tm_template, 1, out=self.tm_counts)
 
     def weights_cpu(self):
         return [st.get("w").cpu() if "w" in st else None for st in self.st]
@@ -134,7 +166,11 @@ class Engine:
         return rec
 
     def run_layer_routed(self, i):
-        """Runs layer i with device-side routing (no host synchronisation)."""
+        """Runs layer i with device-side routing (no host synchronisation).
+        Its input counts and bitmap come from the producer's fused
+        measurement when there is one at this layer's block shape, else from
+        a measurement pass; its own output is measured in its epilogue when a
+        consumer needs it."""
         L, st = self.layers[i], self.st[i]
         x = self.acts[L.src]
         y = self.acts[i + 1]
@@ -142,16 +178,31 @@ class Engine:
             s = L.shape
             abi.sparoa_maxpool2d(x, s["n"], s["c"], s["h"], s["w"], s["k"], s["s"], s["p"], y)
             return
-        abi.sparoa_measure_sparsity(x, st["rows"], st["cols"], st["br"], st["bc"], 0,
-                                    st["counts"], st["mask"])
-        res = self.acts[L.res] if L.res is not None else None
-        if L.kind == "conv":
-            abi.sparoa_conv2d_routed(st["desc"], self.s_thr, self.c_thr, self.mode, st["counts"],
-                                     x, st["w"], None, res, L.act, st["mask"], y, st["ws"],
-                                     st["path"])
+        src = self.tmeas.get(L.src) if (st["br"], st["bc"]) == (1, 8) else None
+        if src is not None:
+            counts, mask = src["counts"], src["mask"]
         else:
-            abi.sparoa_fc_routed(st["desc"], self.s_thr, self.c_thr, self.mode, st["counts"], x,
-                                 st["w"], st.get("wp"), None, res, L.act, st["mask"], y, st["ws"],
+            counts, mask = st["counts"], st["mask"]
+            abi.sparoa_measure_sparsity(x, st["rows"], st["cols"], st["br"], st["bc"], 0, counts,
+                                        mask)
+        st["used"] = (counts, mask)
+        res = self.acts[L.res] if L.res is not None else None
+        out = self.tmeas.get(i + 1)
+        if L.kind == "conv":
+            if out is not None:
+                abi.sparoa_conv2d_routed_measured(st["desc"], self.s_thr, self.c_thr, self.mode,
+                                                  counts, x, st["w"], None, res, L.act, mask, y,
+                                                  out["counts"], out["mask"], st["ws"], st["path"])
+            else:
+                abi.sparoa_conv2d_routed(st["desc"], self.s_thr, self.c_thr, self.mode, counts, x,
+                                         st["w"], None, res, L.act, mask, y, st["ws"], st["path"])
+        elif out is not None:
+            abi.sparoa_fc_routed_measured(st["desc"], self.s_thr, self.c_thr, self.mode, counts, x,
+                                          st["w"], st.get("wp"), None, res, L.act, mask, y,
+                                          out["counts"], out["mask"], st["ws"], st["path"])
+        else:
+            abi.sparoa_fc_routed(st["desc"], self.s_thr, self.c_thr, self.mode, counts, x,
+                                 st["w"], st.get("wp"), None, res, L.act, mask, y, st["ws"],
                                  st["path"])
 
     def forward_routed(self, x):
@@ -159,6 +210,7 @@ class Engine:
         (stream-ordered; safe to capture in a HIP graph).  Returns the output
         activation tensor."""
         self.acts[0] = x
+        self.reset_out_counts()
         for i in range(len(self.layers)):
             self.run_layer_routed(i)
         return self.acts[len(self.layers)]
@@ -170,7 +222,7 @@ class Engine:
             rec = LayerRecord(L.name, L.kind)
             if L.kind != "maxpool":
                 c = dict(zip(("zeros", "numel", "zero_blocks", "num_blocks"),
-                             st["counts"].cpu().tolist()))
+                             st.get("used", (st["counts"],))[0].cpu().tolist()))
                 rec.counts = c
                 rec.rho_e = c["zeros"] / c["numel"]
                 rec.rho_b = c["zero_blocks"] / c["num_blocks"] if c["num_blocks"] else 0.0
@@ -190,6 +242,8 @@ class Engine:
         evs = []
         torch.cuda.synchronize(self.dev)
         t0 = time.perf_counter()
+        if routed:
+            self.reset_out_counts()
         for i in range(len(self.layers)):
             if timed:
                 e0 = torch.cuda.Event(enable_timing=True)

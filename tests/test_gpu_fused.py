@@ -1,0 +1,137 @@
+"""Output measurement fused into the producer (a layer measuring its own
+output, the next layer's input): the counts and bitmap must equal the
+oracle's measurement of the output bit for bit, and the output must equal
+the unfused routed call's bit for bit -- on the fused epilogue, on the fused
+split-K reduction, and on the fallbacks (a standalone pass after the layer)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _abi():
+    from paper_2511_19457_amd import abi
+    return abi
+
+
+def _fresh_counts(rows, cols, dev):
+    """y_counts as the measured calls expect them on entry: {0, numel, nb, nb}."""
+    nb = rows * -(-cols // 8)
+    return torch.tensor([0, rows * cols, nb, nb], dtype=torch.int64, device=dev)
+
+
+def _check_y_measurement(abi, y, rows, cols, y_counts, y_mask, what):
+    ref = oracle.measure(y.cpu(), rows, cols, 1, 8)
+    assert y_counts.cpu().tolist() == [ref["zeros"], ref["numel"], ref["zero_blocks"],
+                                       ref["num_blocks"]], what
+    assert np.array_equal(y_mask.cpu().numpy().view(np.uint32), ref["mask"]), what
+
+
+CONV_CASES = [
+    # n, cin, h, w, cout, k, s, dtype; comment: which form runs
+    (8, 64, 32, 32, 128, 3, 1, "bf16"),    # fused epilogue, 64 x 64 tiles, no split
+    (4, 64, 32, 32, 64, 1, 1, "f16"),      # fused epilogue, 128 x 64 tiles
+    (1, 128, 14, 14, 128, 3, 1, "bf16"),   # split-K: fused reduction
+    (3, 64, 15, 13, 64, 3, 2, "f16"),      # ragged rows, split-K
+    (15, 64, 29, 31, 64, 3, 1, "bf16"),    # ragged rows in the last tile, no split
+    (2, 64, 16, 16, 96, 1, 1, "bf16"),     # c_out % 64 != 0: standalone pass
+    (2, 32, 16, 16, 64, 3, 1, "bf16"),     # c_in % 64 != 0 (first-generation GEMM): standalone
+    (2, 64, 16, 16, 64, 3, 1, "f32"),      # fp32: standalone pass
+]
+
+
+@pytest.mark.parametrize("case", CONV_CASES)
+def test_conv_routed_measured(case):
+    abi = _abi()
+    dev = torch.device("cuda")
+    n, cin, h, w, cout, k, s, dt = case
+    tdt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[dt]
+    p = k // 2
+    d = abi.conv_desc(n, cin, h, w, cout, k, k, s, s, p, p, 1, 1, 1, tdt, has_bias=True)
+    ho, wo = (h + 2 * p - k) // s + 1, (w + 2 * p - k) // s + 1
+    seed = 1100 + CONV_CASES.index(case) * 5
+    x = synth.relu_normal((n, h, w, cin), dt, seed).to(dev)
+    wt = synth.he_normal((cout, k, k, cin), k * k * cin, dt, seed + 1).to(dev)
+    b = synth.normal((cout,), dt, seed + 2).to(dev)
+    r = synth.normal((n, ho, wo, cout), dt, seed + 3).to(dev)
+    counts = torch.zeros(4, dtype=torch.int64, device=dev)
+    mask = torch.zeros(abi.sparoa_mask_words(n * h * w, cin, 1, 8), dtype=torch.int32, device=dev)
+    abi.sparoa_measure_sparsity(x, n * h * w, cin, 1, 8, 0, counts, mask)
+    ws = torch.zeros(max(16, max(abi.sparoa_conv2d_workspace_size(d, q) for q in range(4))),
+                     dtype=torch.uint8, device=dev)
+    rows, cols = n * ho * wo, cout
+    for s_thr in (0.0, 2.0):       # skip and dense routes
+        y = torch.full((n, ho, wo, cout), float("nan"), dtype=tdt, device=dev)
+        y_counts = _fresh_counts(rows, cols, dev)
+        y_mask = torch.full((abi.sparoa_mask_words(rows, cols, 1, 8),), -1, dtype=torch.int32,
+                            device=dev)
+        path = torch.full((1,), -1, dtype=torch.int32, device=dev)
+        abi.sparoa_conv2d_routed_measured(d, s_thr, 0.0, abi.ROUTE_BLOCK, counts, x, wt, b, r,
+                                          abi.ACT_RELU, mask, y, y_counts, y_mask, ws, path)
+        y2 = torch.full_like(y, float("nan"))
+        p2 = torch.full((1,), -1, dtype=torch.int32, device=dev)
+        abi.sparoa_conv2d_routed(d, s_thr, 0.0, abi.ROUTE_BLOCK, counts, x, wt, b, r,
+                                 abi.ACT_RELU, mask, y2, ws, p2)
+        torch.cuda.synchronize()
+        assert int(path.item()) == int(p2.item())
+        assert torch.equal(y, y2), f"{case} s_thr {s_thr}"
+        _check_y_measurement(abi, y, rows, cols, y_counts, y_mask, f"{case} s_thr {s_thr}")
+
+
+FC_CASES = [
+    # m, k, n, dtype, intensity threshold (0: MFMA family)
+    (256, 768, 3072, "f16", 0.0),     # fused epilogue
+    (64, 4096, 4096, "bf16", 0.0),    # split-K: fused reduction
+    (100, 512, 256, "bf16", 0.0),     # ragged rows, split-K
+    (8, 1024, 512, "bf16", 315.0),    # weight-streaming FC: standalone pass
+]
+
+
+@pytest.mark.parametrize("case", FC_CASES)
+def test_fc_routed_measured(case):
+    abi = _abi()
+    dev = torch.device("cuda")
+    m, k, n, dt, c_thr = case
+    tdt = torch.float16 if dt == "f16" else torch.bfloat16
+    d = abi.fc_desc(m, k, n, abi.F16 if dt == "f16" else abi.BF16)
+    seed = 1200 + FC_CASES.index(case) * 5
+    x = synth.sparse_matrix(m, k, 0.5, "block", dt, seed).to(dev)
+    w = synth.normal((n, k), dt, seed + 1, std=k ** -0.5).to(dev)
+    wp = torch.empty(abi.sparoa_fc_packed_bytes(d) // 2, dtype=tdt, device=dev)
+    abi.sparoa_fc_pack_weights(d, w, wp)
+    fam = abi.PATH_SKIP_BW if abi.sparoa_op_intensity_fc(d)["intensity"] < c_thr \
+        else abi.PATH_SKIP_MFMA
+    br, bc = abi.sparoa_fc_skip_block(d, fam)
+    counts = torch.zeros(4, dtype=torch.int64, device=dev)
+    mask = torch.zeros(abi.sparoa_mask_words(m, k, br, bc), dtype=torch.int32, device=dev)
+    abi.sparoa_measure_sparsity(x, m, k, br, bc, 0, counts, mask)
+    ws = torch.zeros(max(16, max(abi.sparoa_fc_workspace_size(d, q) for q in range(4))),
+                     dtype=torch.uint8, device=dev)
+    y = torch.full((m, n), float("nan"), dtype=tdt, device=dev)
+    y_counts = _fresh_counts(m, n, dev)
+    y_mask = torch.full((abi.sparoa_mask_words(m, n, 1, 8),), -1, dtype=torch.int32, device=dev)
+    abi.sparoa_fc_routed_measured(d, 0.5, c_thr, abi.ROUTE_BLOCK, counts, x, w, wp, None, None,
+                                  abi.ACT_RELU, mask, y, y_counts, y_mask, ws)
+    y2 = torch.full_like(y, float("nan"))
+    abi.sparoa_fc_routed(d, 0.5, c_thr, abi.ROUTE_BLOCK, counts, x, w, wp, None, None,
+                         abi.ACT_RELU, mask, y2, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+    _check_y_measurement(abi, y, m, n, y_counts, y_mask, str(case))
+
+
+def test_measured_calls_reject_missing_outputs():
+    abi = _abi()
+    dev = torch.device("cuda")
+    d = abi.fc_desc(64, 256, 128, abi.BF16)
+    t = torch.zeros(64, 256, dtype=torch.bfloat16, device=dev)
+    counts = torch.zeros(4, dtype=torch.int64, device=dev)
+    mask = torch.zeros(64, dtype=torch.int32, device=dev)
+    y = torch.empty(64, 128, dtype=torch.bfloat16, device=dev)
+    with pytest.raises(abi.SparoaError):
+        abi.sparoa_fc_routed_measured(d, 0.5, 0.0, abi.ROUTE_BLOCK, counts, t, t, None, None, None,
+                                      abi.ACT_NONE, mask, y, None, mask)

@@ -121,8 +121,16 @@ def test_device_routing_equals_host_routing(stack):
         y_host, rec_host, _ = eng.run(x)
         y_host = y_host.clone()
         acts_host = [a.clone() for a in eng.acts[1:]]
+        masks_host = [st["mask"].clone() if "mask" in st else None for st in eng.st]
         y_dev, rec_dev, _ = eng.run(x, routed=True)
         assert [r.path for r in rec_dev] == [r.path for r in rec_host]
         for a, b in zip(acts_host, eng.acts[1:]):
             assert torch.equal(a, b)
         assert torch.equal(y_host, y_dev)
+        # the producers' fused measurements equal the consumers' own passes
+        for i, (rh, rd) in enumerate(zip(rec_host, rec_dev)):
+            if masks_host[i] is None:
+                continue
+            assert rd.counts == rh.counts, (stack, thr, i)
+            assert torch.equal(eng.st[i]["used"][1], masks_host[i]), (stack, thr, i)
+        assert eng.tmeas, "some layer measures its output in its epilogue"
