@@ -65,6 +65,10 @@ def parse():
                    help="no GPU: turn the rocprofv3 outputs under DIR (prof_bench/, "
                         "pmc_{bench,copy}_{FETCH,WRITE}_SIZE/ and their .log files) into "
                         "profiles/fc_sweep_step_kernels.md and profiles/fc_sweep_traffic.json")
+    p.add_argument("--crossover", action="store_true",
+                   help="f2 sweep instead of the benchmark: whole-path time of every forced "
+                        "path at block sparsity 0 .. 0.99 (step 0.05) for each m and zero "
+                        "pattern; prints one JSON line with the skip/dense crossovers")
     p.add_argument("--mode", choices=("graph", "eager", "host"), default="graph",
                    help="graph: the executor call captured in a HIP graph, one replay per step; "
                         "eager: the executor call every step; host: counts read back, "
@@ -359,6 +363,72 @@ def alg_bytes(c, path, mask_host):
     return 2 * (c.m * K + c.m * N) + 2 * rows * N
 
 
+def crossover_sweep(abi, torch, synth, dev, n_w=12):
+    """f2: the sparsity at which each family's skip path starts to beat its
+    dense path, per operator class.  x [m, 4096] at rho = 0, 0.05, .., 0.95,
+    0.99 (i.i.d. or 16 x 16 block zeros), w [4096, 4096] bf16 from a pool of
+    n_w matrices used in turn (cold: the pool exceeds the Infinity Cache).
+    Each point: the whole path (sparoa_fc_measured) forced onto each of the
+    four paths, median of one call per pool matrix."""
+    rhos = [round(0.05 * i, 2) for i in range(20)] + [0.99]
+    ws_nk, ws_p = [], []
+    d0 = abi.fc_desc(1, K, N, abi.BF16)
+    for i in range(n_w):
+        w = synth.normal((N, K), "bf16", synth.seed_for(6, 900 + i), std=1.0 / 64.0).to(dev)
+        wp = torch.empty(abi.sparoa_fc_packed_bytes(d0) // 2, dtype=torch.bfloat16, device=dev)
+        abi.sparoa_fc_pack_weights(d0, w, wp)
+        ws_nk.append(w)
+        ws_p.append(wp)
+    out = {}
+    for m in M_LIST:
+        d = abi.fc_desc(m, K, N, abi.BF16)
+        blocks = {fam: abi.sparoa_fc_skip_block(d, fam | 1)
+                  for fam in (abi.PATH_DENSE_BW, abi.PATH_DENSE_MFMA)}
+        counts = torch.zeros(4, dtype=torch.int64, device=dev)
+        mask = torch.zeros(max(abi.sparoa_mask_words(m, K, br, bc) for br, bc in blocks.values()),
+                           dtype=torch.int32, device=dev)
+        ws = torch.zeros(max(16, max(abi.sparoa_fc_workspace_size(d, p) for p in range(4))),
+                         dtype=torch.uint8, device=dev)
+        y = torch.empty(m, N, dtype=torch.bfloat16, device=dev)
+        path = torch.zeros(1, dtype=torch.int32, device=dev)
+        for pat in PATTERNS:
+            rows = []
+            for j, rho in enumerate(rhos):
+                x = synth.sparse_matrix(m, K, rho, pat, "bf16",
+                                        synth.seed_for(6, 100 * m + 10 * j + len(pat))).to(dev)
+                row = dict(rho=rho)
+                for p in (abi.PATH_DENSE_BW, abi.PATH_SKIP_BW, abi.PATH_DENSE_MFMA,
+                          abi.PATH_SKIP_MFMA):
+                    s_thr, c_thr = (0.0 if p & 1 else 2.0), (1e30 if p & 2 else 0.0)
+                    ev = [(torch.cuda.Event(enable_timing=True),
+                           torch.cuda.Event(enable_timing=True)) for _ in range(n_w)]
+                    for i, (e0, e1) in enumerate(ev):
+                        e0.record()
+                        abi.sparoa_fc_measured(d, s_thr, c_thr, abi.ROUTE_BLOCK, x, ws_nk[i],
+                                               ws_p[i], None, None, abi.ACT_NONE, counts, mask, y,
+                                               ws, path)
+                        e1.record()
+                    torch.cuda.synchronize()
+                    ts = sorted(e0.elapsed_time(e1) * 1e3 for e0, e1 in ev)
+                    row[abi.PATH_NAMES[p] + "_us"] = round(ts[len(ts) // 2], 2)
+                    z, _, zb, nb = counts.cpu().tolist()
+                    row["rho_b_" + ("bw" if p & 2 else "mfma")] = round(zb / nb, 4)
+                rows.append(row)
+            cross = {}
+            for fam, tag in ((abi.PATH_DENSE_BW, "bw"), (abi.PATH_DENSE_MFMA, "mfma")):
+                dn, sk = abi.PATH_NAMES[fam] + "_us", abi.PATH_NAMES[fam | 1] + "_us"
+                c = None           # smallest block sparsity from which skip always wins
+                for r in reversed(sorted(rows, key=lambda r: r["rho_b_" + tag])):
+                    if r[sk] < r[dn]:
+                        c = r["rho_b_" + tag]
+                    else:
+                        break
+                cross[tag] = c
+            out[f"m{m}_{pat}"] = dict(crossover_rho_b=cross, points=rows)
+            print(f"bench: crossover m={m} {pat}: {cross}", file=sys.stderr, flush=True)
+    return out
+
+
 def model_latencies(abi, torch, synth, reps=10):
     """Per-model latency at one GPU: the whole stack (measure, device-side
     route, execute, glue per layer) captured once in a HIP graph and replayed;
@@ -484,6 +554,11 @@ def main():
         return
     import synth
     from paper_2511_19457_amd import abi
+    if args.crossover:
+        print(json.dumps(dict(sweep="f2 crossover", workload="x [m,4096] x w [4096,4096] bf16, "
+                              "whole path forced per path", data="synthetic",
+                              results=crossover_sweep(abi, torch, synth, dev))), flush=True)
+        return
     print("bench: building 24 FC operators (packing weights)", file=sys.stderr, flush=True)
     cases = build_cases(abi, torch, synth, dev)
 
