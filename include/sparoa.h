@@ -333,6 +333,39 @@ sparoa_status sparoa_fc_routed_measured(const sparoa_fc_desc *desc, const sparoa
                                         hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Split execution of one operator over the zero-skip and dense paths: the
+ * on-device reading of the paper's operator split (Algorithm 1 divides an
+ * operator's work between two processors by a ratio; here its rows are
+ * divided between two kernel paths by their own sparsity).  Every row tile of
+ * the skip-capable implicit GEMM (tile rows: sparoa_conv2d_tiling with
+ * SKIP_MFMA) takes its own route: the skip path iff
+ *     (double)sum(sample_zeros[s0..s1]) / (double)((s1-s0+1) * sample_numel)
+ *         >= sparsity_thr,
+ * where s0..s1 are the input samples the tile's output rows come from (conv:
+ * rows_per_sample = Ho*Wo, sample_numel = H*W*C_in; FC: one sample per row,
+ * sample_numel = k).  The output equals the dense path's bit for bit (a
+ * skipped chunk is all zeros).
+ *   sample_zeros_dev / row_zeros_dev: per-sample zero counts of x
+ *     (sparoa_measure_sparsity with samples = n, or = m for an FC).
+ *   mask: bitmap of x at block (1, 8).
+ *   executed_blocks_dev (nullable): executed (row tile, tap, 64-channel
+ *     chunk) triples, every chunk counting on a dense tile.
+ * Errors: UNSUPPORTED unless the 16-bit, C_in % 64 == 0, groups 1 implicit
+ * GEMM serves the layer; INVALID_ARG for null pointers or a NaN / negative
+ * threshold; WORKSPACE as for sparoa_conv2d.
+ * ---------------------------------------------------------------------- */
+sparoa_status sparoa_conv2d_split(const sparoa_conv_desc *desc, double sparsity_thr,
+                                  const uint64_t *sample_zeros_dev, const void *x, const void *w,
+                                  const void *bias, const void *residual, sparoa_act act,
+                                  const uint32_t *mask, void *y, void *workspace, size_t ws_bytes,
+                                  uint64_t *executed_blocks_dev, hipStream_t stream);
+sparoa_status sparoa_fc_split(const sparoa_fc_desc *desc, double sparsity_thr,
+                              const uint64_t *row_zeros_dev, const void *x, const void *w_nk,
+                              const void *bias, const void *residual, sparoa_act act,
+                              const uint32_t *mask, void *y, void *workspace, size_t ws_bytes,
+                              uint64_t *executed_blocks_dev, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * The whole path of one FC operator -- measure, route, execute (SparOA
  * Section 3.1 sparsity feature, Eq. 1; Section 2.2 quadrant routing) -- in
  * one call and no host round trip.

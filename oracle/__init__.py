@@ -69,6 +69,8 @@ def lib():
                                          _i64, _i64, _dp, _dp]
         L.or_fc_executed_blocks.argtypes = [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _u64p]
         L.or_conv_executed_blocks.argtypes = [_vp, ctypes.c_int] + [_i64] * 14 + [_u64p]
+        L.or_conv_split_executed_blocks.argtypes = ([_vp, ctypes.c_int] + [_i64] * 14 +
+                                                    [ctypes.c_double, _u64p])
         L.or_maxpool2d.argtypes = [_i64] * 7 + [ctypes.c_int, _vp, _dp]
         _lib = L
     return _lib
@@ -251,6 +253,17 @@ def conv_executed_blocks(x, n, cin, h, w, kh, kw, sh, sw, ph, pw, dh, dw, tile_r
     _check(lib().or_conv_executed_blocks(_ptr(xr), code, n, cin, h, w, kh, kw, sh, sw, ph, pw,
                                          dh, dw, tile_rows, block_c, ctypes.byref(out)),
            "conv_executed_blocks")
+    return out.value
+
+
+def conv_split_executed_blocks(x, n, cin, h, w, kh, kw, sh, sw, ph, pw, dh, dw, tile_rows,
+                               block_c, sparsity_thr):
+    """Executed triples when each row tile is routed on its own (split execution)."""
+    xr, code = _bits(x)
+    out = ctypes.c_uint64()
+    _check(lib().or_conv_split_executed_blocks(_ptr(xr), code, n, cin, h, w, kh, kw, sh, sw, ph,
+                                               pw, dh, dw, tile_rows, block_c, sparsity_thr,
+                                               ctypes.byref(out)), "conv_split_executed_blocks")
     return out.value
 
 

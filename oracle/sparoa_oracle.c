@@ -511,6 +511,65 @@ int or_conv_executed_blocks(const void *x, int dt, int64_t n, int64_t cin, int64
   return OR_OK;
 }
 
+/*
+ * Split execution of one convolution over the skipping and the dense path
+ * (the operator split of Algorithm 1, read on one GPU as a split of the
+ * operator's row tiles between two kernel paths): the executed (tile, tap,
+ * channel block) triples when every tile of tile_rows output pixels is routed
+ * on its own.  A tile whose pixels come from input samples s0..s1 skips iff
+ *     zeros(x[s0..s1]) / ((s1 - s0 + 1) * h * w * cin) >= sparsity_thr
+ * (one double division; zeros counted element by element over the whole
+ * samples) and then executes its nonzero triples as above; otherwise it
+ * executes all kh * kw * ceil(cin / block_c) of them.  An FC is the case
+ * h = w = kh = kw = 1 with one sample per row.
+ */
+int or_conv_split_executed_blocks(const void *x, int dt, int64_t n, int64_t cin, int64_t h,
+                                  int64_t w, int64_t kh, int64_t kw, int64_t sh, int64_t sw,
+                                  int64_t ph, int64_t pw, int64_t dh, int64_t dw,
+                                  int64_t tile_rows, int64_t block_c, double sparsity_thr,
+                                  uint64_t *out) {
+  if (!x || !out || !dt_ok(dt) || n <= 0 || cin <= 0 || tile_rows <= 0 || block_c <= 0 ||
+      !(sparsity_thr >= 0))
+    return OR_EINVAL;
+  int64_t ho_n = or_out_dim(h, kh, sh, ph, dh), wo_n = or_out_dim(w, kw, sw, pw, dw);
+  if (ho_n <= 0 || wo_n <= 0) return OR_EINVAL;
+  const int64_t rows = n * ho_n * wo_n, per = ho_n * wo_n, snum = h * w * cin;
+  uint64_t *sz = (uint64_t *)calloc((size_t)n, sizeof(uint64_t));
+  if (!sz) return OR_EINVAL;
+  for (int64_t s = 0; s < n; ++s)
+    for (int64_t e = 0; e < snum; ++e)
+      if (elem_is_zero(x, dt, s * snum + e)) ++sz[s];
+  const uint64_t all = (uint64_t)(kh * kw) * (uint64_t)((cin + block_c - 1) / block_c);
+  uint64_t cnt = 0;
+  for (int64_t t0 = 0; t0 < rows; t0 += tile_rows) {
+    const int64_t t1 = (t0 + tile_rows < rows ? t0 + tile_rows : rows) - 1;
+    const int64_t s0 = t0 / per, s1 = t1 / per;
+    uint64_t z = 0;
+    for (int64_t s = s0; s <= s1; ++s) z += sz[s];
+    const double rho = (double)z / (double)((uint64_t)(s1 - s0 + 1) * (uint64_t)snum);
+    if (!(rho >= sparsity_thr)) {
+      cnt += all;
+      continue;
+    }
+    for (int64_t r = 0; r < kh; ++r)
+      for (int64_t q = 0; q < kw; ++q)
+        for (int64_t c0 = 0; c0 < cin; c0 += block_c) {
+          int nz = 0;
+          for (int64_t p = t0; p <= t1 && !nz; ++p) {
+            int64_t ow = p % wo_n, oh = (p / wo_n) % ho_n, in = p / wo_n / ho_n;
+            int64_t ih = oh * sh - ph + r * dh, iw = ow * sw - pw + q * dw;
+            if (ih < 0 || ih >= h || iw < 0 || iw >= w) continue;
+            for (int64_t c = c0; c < cin && c < c0 + block_c; ++c)
+              if (!elem_is_zero(x, dt, ((in * h + ih) * w + iw) * cin + c)) nz = 1;
+          }
+          cnt += (uint64_t)nz;
+        }
+  }
+  free(sz);
+  *out = cnt;
+  return OR_OK;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Glue: max pooling (not routed).                                            */
 /* ------------------------------------------------------------------------ */

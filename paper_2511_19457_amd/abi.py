@@ -32,6 +32,7 @@ EXPORTS = [
     "sparoa_fc_dense", "sparoa_fc_zero_skip", "sparoa_maxpool2d", "sparoa_conv2d_routed",
     "sparoa_fc_routed", "sparoa_fc_uses_packed", "sparoa_fc_ops_run",
     "sparoa_fc_measured", "sparoa_conv2d_routed_measured", "sparoa_fc_routed_measured",
+    "sparoa_conv2d_split", "sparoa_fc_split",
 ]
 
 
@@ -133,6 +134,10 @@ def _load():
                                                 ctypes.c_int, vp, vp, vp, sz, vp, vp]),
         "sparoa_fc_routed": (ctypes.c_int, [P(FcDesc), P(Thresholds), vp, vp, vp, vp, vp, vp,
                                             ctypes.c_int, vp, vp, vp, sz, vp, vp]),
+        "sparoa_conv2d_split": (ctypes.c_int, [P(ConvDesc), ctypes.c_double, vp, vp, vp, vp, vp,
+                                               ctypes.c_int, vp, vp, vp, sz, vp, vp]),
+        "sparoa_fc_split": (ctypes.c_int, [P(FcDesc), ctypes.c_double, vp, vp, vp, vp, vp,
+                                           ctypes.c_int, vp, vp, vp, sz, vp, vp]),
         "sparoa_conv2d_routed_measured": (ctypes.c_int, [P(ConvDesc), P(Thresholds), vp, vp, vp,
                                                          vp, vp, ctypes.c_int, vp, vp, vp, sz, vp,
                                                          vp, vp, vp]),
@@ -392,6 +397,24 @@ def sparoa_fc_routed_measured(desc, sparsity_thr, intensity_thr, mode, counts, x
         ctypes.byref(desc), ctypes.byref(t), _ptr(counts), _ptr(x), _ptr(w_nk), _ptr(w_packed),
         _ptr(bias), _ptr(residual), act, _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes,
         _ptr(path), _ptr(y_counts), _ptr(y_mask), _stream(stream)))
+
+
+def sparoa_conv2d_split(desc, sparsity_thr, sample_zeros, x, w, bias, residual, act, mask, y,
+                        workspace=None, executed=None, stream=None):
+    """One conv split over the skip and dense paths by row tile (see sparoa.h)."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_L.sparoa_conv2d_split(ctypes.byref(desc), sparsity_thr, _ptr(sample_zeros), _ptr(x),
+                                  _ptr(w), _ptr(bias), _ptr(residual), act, _ptr(mask), _ptr(y),
+                                  _ptr(workspace), ws_bytes, _ptr(executed), _stream(stream)))
+
+
+def sparoa_fc_split(desc, sparsity_thr, row_zeros, x, w_nk, bias, residual, act, mask, y,
+                    workspace=None, executed=None, stream=None):
+    """One FC split over the skip and dense paths by row tile (see sparoa.h)."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_L.sparoa_fc_split(ctypes.byref(desc), sparsity_thr, _ptr(row_zeros), _ptr(x),
+                              _ptr(w_nk), _ptr(bias), _ptr(residual), act, _ptr(mask), _ptr(y),
+                              _ptr(workspace), ws_bytes, _ptr(executed), _stream(stream)))
 
 
 def sparoa_fc_measured(desc, sparsity_thr, intensity_thr, mode, x, w_nk, w_packed, bias, residual,

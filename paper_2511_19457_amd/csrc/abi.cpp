@@ -696,6 +696,64 @@ sparoa_status sparoa_fc_measured(const sparoa_fc_desc *d, const sparoa_threshold
                         workspace, ws_bytes, path_dev, stream, nullptr);
 }
 
+// ------------------------------------------------------- split execution
+
+}  // extern "C"
+
+namespace {
+sparoa_status split_impl(const sparoa_conv_desc &c, double sparsity_thr,
+                         const uint64_t *sample_zeros, const void *x, const void *w,
+                         const void *bias, const void *residual, sparoa_act act,
+                         const uint32_t *mask, void *y, void *workspace, size_t ws_bytes,
+                         uint64_t *executed, hipStream_t stream) {
+  int64_t ho, wo;
+  sparoa_status st = check_conv(&c, &ho, &wo);
+  if (st != SPAROA_OK) return st;
+  if (!sample_zeros || !x || !w || !y || !mask || !act_ok(act))
+    return fail(SPAROA_ERR_INVALID_ARG, "split: null sample_zeros/x/w/mask/y or bad act");
+  if (std::isnan(sparsity_thr) || sparsity_thr < 0)
+    return fail(SPAROA_ERR_INVALID_ARG, "split: NaN or negative threshold");
+  if (c.has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "split: has_bias without bias");
+  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace})) != SPAROA_OK) return st;
+  if (is_depthwise(c) || c.groups != 1 || gemm_choose(c, SPAROA_PATH_SKIP_MFMA).cfg == 0)
+    return fail(SPAROA_ERR_UNSUPPORTED,
+                "split: needs the 16-bit, C_in % 64 == 0 implicit GEMM (groups 1)");
+  if (ws_bytes < gemm_workspace(c, SPAROA_PATH_SKIP_MFMA))
+    return fail(SPAROA_ERR_WORKSPACE, "split: workspace too small");
+  DeviceRoute r{nullptr, sparsity_thr, SPAROA_ROUTE_ELEMENT, 0, nullptr};
+  r.sample_zeros = reinterpret_cast<const unsigned long long *>(sample_zeros);
+  r.rows_per_sample = ho * wo;
+  r.sample_numel = c.h * c.w * c.c_in;
+  return launch_gemm_conv(c, SPAROA_PATH_SKIP_MFMA, x, w, c.has_bias ? bias : nullptr, residual,
+                          act, mask, y, workspace, ws_bytes, executed, stream, &r);
+}
+}  // namespace
+
+extern "C" {
+
+sparoa_status sparoa_conv2d_split(const sparoa_conv_desc *d, double sparsity_thr,
+                                  const uint64_t *sample_zeros_dev, const void *x, const void *w,
+                                  const void *bias, const void *residual, sparoa_act act,
+                                  const uint32_t *mask, void *y, void *workspace, size_t ws_bytes,
+                                  uint64_t *executed_blocks_dev, hipStream_t stream) {
+  g_last_error.clear();
+  if (!d) return fail(SPAROA_ERR_INVALID_ARG, "split: null desc");
+  return split_impl(*d, sparsity_thr, sample_zeros_dev, x, w, bias, residual, act, mask, y,
+                    workspace, ws_bytes, executed_blocks_dev, stream);
+}
+
+sparoa_status sparoa_fc_split(const sparoa_fc_desc *d, double sparsity_thr,
+                              const uint64_t *row_zeros_dev, const void *x, const void *w_nk,
+                              const void *bias, const void *residual, sparoa_act act,
+                              const uint32_t *mask, void *y, void *workspace, size_t ws_bytes,
+                              uint64_t *executed_blocks_dev, hipStream_t stream) {
+  g_last_error.clear();
+  sparoa_status st = check_fc(d);
+  if (st != SPAROA_OK) return st;
+  return split_impl(fc_as_conv(*d), sparsity_thr, row_zeros_dev, x, w_nk, bias, residual, act,
+                    mask, y, workspace, ws_bytes, executed_blocks_dev, stream);
+}
+
 // ---------------------------------------------------------------- executor
 
 namespace {

@@ -40,6 +40,13 @@ struct DeviceRoute {
   int mode;
   int bw_bit;
   uint32_t *path_out;  // nullable: receives the path taken
+  // Split execution (one operator over both paths): when non-null, every row
+  // tile of the skip-capable GEMM takes its own route -- the skip path iff
+  // the zero fraction of the input samples its output rows come from is at
+  // least sparsity_thr.  sample_zeros[s] = zeros of input sample s, which
+  // holds sample_numel elements and yields rows_per_sample output rows.
+  const unsigned long long *sample_zeros = nullptr;
+  int64_t rows_per_sample = 0, sample_numel = 0;
 };
 
 #ifdef __HIPCC__

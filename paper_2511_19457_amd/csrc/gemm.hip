@@ -607,7 +607,19 @@ __global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
   int64_t count = c_end - c_begin;
   bool use_list = SKIP;
   if constexpr (SKIP) {
-    if (a.route.counts) {
+    if (a.route.sample_zeros) {
+      // split execution: this tile's own route, from the zero counts of the
+      // samples its rows come from (one double division, >=, as sparoa_route)
+      const int64_t last = min(m0 + BM, a.M) - 1;
+      const int64_t s0 = m0 / a.route.rows_per_sample, s1 = last / a.route.rows_per_sample;
+      unsigned long long z = 0;
+      for (int64_t q = s0; q <= s1; ++q) z += a.route.sample_zeros[q];
+      const double n = (double)((unsigned long long)(s1 - s0 + 1) *
+                                (unsigned long long)a.route.sample_numel);
+      use_list = (double)z / n >= a.route.sparsity_thr;
+      if (!use_list && a.executed && first_col && tid == 0 && count)
+        atomicAdd(a.executed, (unsigned long long)count);  // a dense tile runs every chunk
+    } else if (a.route.counts) {
       use_list = device_route_skip(a.route);
       if (a.route.path_out && first_tile && tid == 0)
         *a.route.path_out = (use_list ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);

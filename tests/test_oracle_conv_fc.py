@@ -164,6 +164,35 @@ def test_conv_executed_blocks_extremes_and_hand_example():
     assert oracle.conv_executed_blocks(x, n, c, h, w, 3, 3, 1, 1, 1, 1, 1, 1, 4, 4) == 4
 
 
+def test_conv_split_executed_blocks_pins():
+    """Split execution (each row tile routed on its own): threshold 0 routes
+    every tile to the skip path (= conv_executed_blocks), a threshold above 1
+    routes every tile to the dense path (tiles x taps x channel blocks), and a
+    hand example fixes the per-tile rule, including tiles that straddle
+    samples (whose zero fraction is taken over their whole samples)."""
+    x = synth.sparse_matrix(2 * 6 * 7, 16, 0.7, "block", "f32", 31).reshape(2, 6, 7, 16)
+    args = (2, 16, 6, 7, 3, 3, 1, 1, 1, 1, 1, 1)
+    for tr, bc in ((8, 8), (16, 16), (13, 8)):
+        skip_all = oracle.conv_executed_blocks(x, *args, tr, bc)
+        assert oracle.conv_split_executed_blocks(x, *args, tr, bc, 0.0) == skip_all
+        tiles = -(-2 * 6 * 7 // tr)
+        assert oracle.conv_split_executed_blocks(x, *args, tr, bc, 2.0) == tiles * 9 * (16 // bc)
+    # 1x1 conv, 3 samples of 5 x 5 pixels, 128 channels, blocks of 64: sample 0
+    # all zero; sample 1 zero in channels 0-63 only (zero fraction 0.5);
+    # sample 2 all zero.  Tiles of 16 rows: t0 = s0, t1 = s0|s1, t2 = s1,
+    # t3 = s1|s2, t4 = s2 (zero fractions 1, 0.75, 0.5, 0.75, 1).  A skipping
+    # tile that holds sample-1 rows executes 1 block; a dense tile 2; an
+    # all-zero skipping tile 0.
+    x = torch.zeros(3, 5, 5, 128)
+    x[1, :, :, 64:] = 1.0
+    a1 = (3, 128, 5, 5, 1, 1, 1, 1, 0, 0, 1, 1, 16, 64)
+    assert oracle.conv_split_executed_blocks(x, *a1, 0.4) == 0 + 1 + 1 + 1 + 0
+    assert oracle.conv_split_executed_blocks(x, *a1, 0.5) == 0 + 1 + 1 + 1 + 0
+    assert oracle.conv_split_executed_blocks(x, *a1, 0.6) == 0 + 1 + 2 + 1 + 0
+    assert oracle.conv_split_executed_blocks(x, *a1, 0.8) == 0 + 2 + 2 + 2 + 0
+    assert oracle.conv_split_executed_blocks(x, *a1, 1.01) == 2 * 5
+
+
 def test_conv_at_matches_full():
     n, h, w, cin, cout = 2, 5, 6, 8, 6
     x = synth.normal((n, h, w, cin), "f16", 61)
