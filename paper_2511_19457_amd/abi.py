@@ -32,7 +32,7 @@ EXPORTS = [
     "sparoa_fc_dense", "sparoa_fc_zero_skip", "sparoa_maxpool2d", "sparoa_conv2d_routed",
     "sparoa_fc_routed", "sparoa_fc_uses_packed", "sparoa_fc_ops_run",
     "sparoa_fc_measured", "sparoa_conv2d_routed_measured", "sparoa_fc_routed_measured",
-    "sparoa_conv2d_split", "sparoa_fc_split",
+    "sparoa_conv2d_split", "sparoa_fc_split", "sparoa_measure_sparsity_preset",
 ]
 
 
@@ -134,6 +134,8 @@ def _load():
                                                 ctypes.c_int, vp, vp, vp, sz, vp, vp]),
         "sparoa_fc_routed": (ctypes.c_int, [P(FcDesc), P(Thresholds), vp, vp, vp, vp, vp, vp,
                                             ctypes.c_int, vp, vp, vp, sz, vp, vp]),
+        "sparoa_measure_sparsity_preset": (ctypes.c_int, [vp, ctypes.c_int, i64, i64, i64, i64,
+                                                          vp, vp, vp]),
         "sparoa_conv2d_split": (ctypes.c_int, [P(ConvDesc), ctypes.c_double, vp, vp, vp, vp, vp,
                                                ctypes.c_int, vp, vp, vp, sz, vp, vp]),
         "sparoa_fc_split": (ctypes.c_int, [P(FcDesc), ctypes.c_double, vp, vp, vp, vp, vp,
@@ -226,6 +228,14 @@ def sparoa_measure_sparsity(x, rows, cols, block_rows, block_cols, samples, coun
     _check(_L.sparoa_measure_sparsity(
         _ptr(x), dtype_code(x) if dtype is None else dtype, rows, cols, block_rows, block_cols,
         samples, _ptr(counts), _ptr(mask), _ptr(per_sample), _stream(stream)))
+
+
+def sparoa_measure_sparsity_preset(x, rows, cols, block_rows, block_cols, counts, mask,
+                                   stream=None, dtype=None):
+    """Measurement into counters already set to {0, numel, nb, nb} (see sparoa.h)."""
+    _check(_L.sparoa_measure_sparsity_preset(
+        _ptr(x), dtype_code(x) if dtype is None else dtype, rows, cols, block_rows, block_cols,
+        _ptr(counts), _ptr(mask), _stream(stream)))
 
 
 def sparoa_measure_sparsity_sync(x, rows, cols, block_rows, block_cols, samples, counts,

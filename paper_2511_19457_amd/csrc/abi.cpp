@@ -149,6 +149,18 @@ sparoa_status sparoa_measure_sparsity(const void *x_dev, sparoa_dtype dtype, int
                         mask_dev, per_sample_dev, stream);
 }
 
+sparoa_status sparoa_measure_sparsity_preset(const void *x_dev, sparoa_dtype dtype, int64_t rows,
+                                             int64_t cols, int64_t block_rows,
+                                             int64_t block_cols, sparoa_counts *counts_dev,
+                                             uint32_t *mask_dev, hipStream_t stream) {
+  g_last_error.clear();
+  sparoa_status st = check_measure(x_dev, dtype, rows, cols, block_rows, block_cols, 0,
+                                   counts_dev, mask_dev, nullptr);
+  if (st != SPAROA_OK) return st;
+  return launch_measure(x_dev, dtype, rows, cols, block_rows, block_cols, 0, counts_dev,
+                        mask_dev, nullptr, stream, true);
+}
+
 sparoa_status sparoa_measure_sparsity_sync(const void *x_dev, sparoa_dtype dtype, int64_t rows,
                                            int64_t cols, int64_t block_rows, int64_t block_cols,
                                            int64_t samples, sparoa_counts *counts_dev,

@@ -525,7 +525,7 @@ sparoa_status launch_measure_group(const MeasureJob *jobs, int n, hipStream_t st
 sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64_t cols,
                              int64_t block_rows, int64_t block_cols, int64_t samples,
                              sparoa_counts *counts, uint32_t *mask, uint64_t *per_sample,
-                             hipStream_t stream) {
+                             hipStream_t stream, bool preset) {
   const int esz = (int)elem_size(dt);
   const int vw = 16 / esz;
   const bool want_mask = mask != nullptr;
@@ -565,7 +565,8 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
     return SPAROA_OK;
   }
 
-  {
+  // counters the caller already set and no bitmap to clear: no init launch
+  if (!(preset && (lanebit || strips))) {
     const int64_t zw = (lanebit || strips) ? 0 : words;   // words to clear
     const int64_t work = zw > S ? zw : S;
     const int64_t g = work < 1 ? 1 : (cdiv(work, 256) < 1024 ? cdiv(work, 256) : 1024);

@@ -119,18 +119,37 @@ class Engine:
                     rows *= v
                 nb = rows * -(-shp[-1] // 8)
                 meas.append((t, [0, rows * shp[-1], nb, nb], abi.sparoa_mask_words(rows, shp[-1], 1, 8)))
-        self.tm_template = torch.tensor([m[1] for m in meas] or [[0, 0, 0, 0]], dtype=torch.int64,
-                                        device=self.dev)
-        self.tm_counts = torch.zeros_like(self.tm_template)
+        # Every counter of a routed pass -- each layer's own input measurement
+        # (rows 0 .. L-1) and the fused output measurements -- starts from its
+        # preset {0, numel, nb, nb}: one reset kernel per pass, and the
+        # measurement passes need no init launch of their own.
+        tmpl = []
+        for i, L in enumerate(layers):
+            st = self.st[i]
+            if L.kind == "maxpool":
+                tmpl.append([0, 0, 0, 0])
+                continue
+            nb = -(-st["rows"] // st["br"]) * -(-st["cols"] // st["bc"])
+            tmpl.append([0, st["rows"] * st["cols"], nb, nb])
+        tmpl += [m[1] for m in meas]
+        # one 128-byte line per counter: a kernel's atomics into its output
+        # counters never share a line with the input counters other
+        # work-groups of the same kernel read
+        pad = [row + [0] * 12 for row in tmpl]
+        self.ctr_template = torch.tensor(pad, dtype=torch.int64, device=self.dev)
+        self.ctr = torch.zeros_like(self.ctr_template)
+        for i, L in enumerate(layers):
+            if L.kind != "maxpool":
+                self.st[i]["counts"] = self.ctr[i, :4]
         for j, (t, _, words) in enumerate(meas):
-            self.tmeas[t] = dict(counts=self.tm_counts[j],
+            self.tmeas[t] = dict(counts=self.ctr[len(layers) + j, :4],
                                  mask=torch.zeros(words, dtype=torch.int32, device=self.dev))
         torch.cuda.synchronize(self.dev)
 
-    def reset_out_counts(self):
-        """Initial values of the fused output measurements (a kernel, not a
+    def reset_counters(self):
+        """Preset values of every counter of a routed pass (a kernel, not a
         memset or copy node, so a captured graph replays it safely)."""
-        torch.mul(self.tm_template, 1, out=self.tm_counts)
+        torch.mul(self.ctr_template, 1, out=self.ctr)
 
     def weights_cpu(self):
         return [st.get("w").cpu() if "w" in st else None for st in self.st]
@@ -183,8 +202,8 @@ class Engine:
             counts, mask = src["counts"], src["mask"]
         else:
             counts, mask = st["counts"], st["mask"]
-            abi.sparoa_measure_sparsity(x, st["rows"], st["cols"], st["br"], st["bc"], 0, counts,
-                                        mask)
+            abi.sparoa_measure_sparsity_preset(x, st["rows"], st["cols"], st["br"], st["bc"],
+                                               counts, mask)
         st["used"] = (counts, mask)
         res = self.acts[L.res] if L.res is not None else None
         out = self.tmeas.get(i + 1)
@@ -210,7 +229,7 @@ class Engine:
         (stream-ordered; safe to capture in a HIP graph).  Returns the output
         activation tensor."""
         self.acts[0] = x
-        self.reset_out_counts()
+        self.reset_counters()
         for i in range(len(self.layers)):
             self.run_layer_routed(i)
         return self.acts[len(self.layers)]
@@ -243,7 +262,7 @@ class Engine:
         torch.cuda.synchronize(self.dev)
         t0 = time.perf_counter()
         if routed:
-            self.reset_out_counts()
+            self.reset_counters()
         for i in range(len(self.layers)):
             if timed:
                 e0 = torch.cuda.Event(enable_timing=True)

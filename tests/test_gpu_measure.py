@@ -109,3 +109,33 @@ def test_measure_full_size(shape, dt, blk):
     cols = shape[-1]
     samples = shape[0] if len(shape) == 4 else 0
     _check(x, rows, cols, blk[0], blk[1], samples)
+
+
+@pytest.mark.parametrize("rows,cols,br,bc,dt", [
+    (3136, 64, 1, 8, "bf16"),         # 1 x one 16-byte vector: one launch
+    (100352, 96, 1, 8, "f16"),        # same, grid-stride over many work-groups
+    (40, 2048, 1, 4, "f32"),          # fp32 vector
+    (8, 4096, 8, 1, "bf16"),          # whole-column strips
+    (37, 100, 2, 4, "bf16"),          # other blocks: initialises everything itself
+])
+def test_measure_preset_counters(rows, cols, br, bc, dt):
+    """sparoa_measure_sparsity_preset: with counters preset to
+    {0, numel, nb, nb} it gives the oracle's counts and bitmap; block shapes
+    that need their bitmap cleared ignore the preset (garbage in, exact out)."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    x = synth.sparse_matrix(rows, cols, 0.7, "block", dt, rows + cols)
+    ref = oracle.measure(x, rows, cols, br, bc)
+    nb = -(-rows // br) * -(-cols // bc)
+    lanebit_or_strips = (br == 1 and bc * torch.tensor([], dtype=DT[dt]).element_size() == 16) or \
+        (bc == 1 and br >= rows)
+    preset = [0, rows * cols, nb, nb] if lanebit_or_strips else [7, 7, 7, 7]
+    for _ in range(2):    # twice: the second call starts from the preset again
+        counts = torch.tensor(preset, dtype=torch.int64, device=dev)
+        mask = torch.full((abi.sparoa_mask_words(rows, cols, br, bc),), -1, dtype=torch.int32,
+                          device=dev)
+        abi.sparoa_measure_sparsity_preset(x.to(dev), rows, cols, br, bc, counts, mask)
+        torch.cuda.synchronize()
+        assert counts.cpu().tolist() == [ref["zeros"], ref["numel"], ref["zero_blocks"],
+                                         ref["num_blocks"]]
+        assert np.array_equal(mask_np(mask), ref["mask"])
