@@ -9,8 +9,10 @@ the 256 MB Infinity Cache holds), so weights stream from HBM.  Per operator
 the step runs the whole path: intensity from the shape (host), sparsity
 measurement (GPU), routing, and the routed FC kernel.  Default (--mode graph):
 the 24 operators are issued by one native executor call (sparoa_fc_ops_run),
-captured once in a HIP graph; each FC kernel measures its own input and takes
-the route decision itself, so a step is one graph launch of 24 kernels.
+captured once in a HIP graph.  The weight-streaming FCs measure their own
+input and take the route decision themselves, all of them in one grouped
+launch; the implicit-GEMM FCs run a grouped measurement, one GEMM each
+(device-side route) and a grouped split-K reduction.
 --mode eager issues the same executor call every step; --mode host reads the
 counts back and routes on the host, one Python call per kernel.  Inputs are
 resident in HBM before timing starts.
@@ -165,8 +167,9 @@ def profile_summary(d, copy_mib):
                    f"{min(v):.2f} | {max(v):.2f} | {100 * sum(v) / tot:.1f} |")
     out += ["", "bench.py's own figures in the same run (HIP events, per-family graph replays):", ""]
     for fam, r in [("dominant", line["roofline"])] + list(line.get("roofline_other_families", {}).items()):
-        out.append(f"- {fam}: `{r['kernel']}`, {r['operators']} operators, avg {r['avg_launch_us']} us "
-                   f"per operator, {r['achieved']} GB/s algorithmic")
+        out.append(f"- {fam}: `{r['kernel']}`, {r['operators']} operators in {r['launches']} "
+                   f"launches, avg {r['avg_launch_us']} us per launch, {r['achieved']} GB/s "
+                   "algorithmic")
     with open(os.path.join(ROOT, "profiles", "fc_sweep_step_kernels.md"), "w") as f:
         f.write("\n".join(out) + "\n")
 
@@ -199,8 +202,8 @@ def profile_summary(d, copy_mib):
                 ops = sum(1 for n, _ in rows_c if "igemm_kernel<" in n)    # and reduction
                 tot_c = sum(v for n, v in rows_c if any(k in n for k in (
                     "measure_init", "measure_lanebit", "igemm_kernel<", "split_reduce")))
-            else:      # one operator = one self-measuring fc_bw_kernel launch
-                sel = [v for n, v in rows_c if "fc_bw_kernel<" in n and _short(n).endswith("true>")]
+            else:      # one launch = one grouped self-measuring streaming-FC dispatch
+                sel = [v for n, v in rows_c if "fc_bw_measured_group<" in n]
                 ops, tot_c = len(sel), sum(sel)
             kib[c] = (tot_c / max(ops, 1), ops)
         res["families"][name] = dict(
@@ -322,6 +325,43 @@ def forced_times(abi, torch, cases, paths, rounds=3):
             assert int(c.path_dev.item()) == p, "forced thresholds must force the path"
             z, _, zb, nb = c.counts.cpu().tolist()
             c.rho_b[fam] = zb / nb
+
+
+def family_batch_times(abi, torch, cases, reps=10):
+    """Per operator class (m) and kernel family: duration (us) of the class's
+    operators issued as one executor batch (sparoa_fc_ops_run, captured in a
+    HIP graph, as the step issues them) with the family forced on every
+    operator (intensity threshold 1e30 or 0, dense paths).  Median of `reps`
+    replays between HIP events; weights stay cold across the classes' 8 x 32
+    MiB."""
+    out = {}
+    for m in M_LIST:
+        cs = [c for c in cases if c.m == m]
+        for fam, c_thr in ((abi.PATH_DENSE_BW, 1e30), (abi.PATH_DENSE_MFMA, 0.0)):
+            arr = abi.fc_op_array([
+                abi.fc_op(c.desc, c.x, c.w, c.wp, None, None, abi.ACT_NONE, c.counts, c.mask,
+                          c.y, c.ws, c.path_dev, (2.0, c_thr, abi.ROUTE_BLOCK)) for c in cs])
+            cap = torch.cuda.Stream()
+            cap.wait_stream(torch.cuda.current_stream())
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(cap):
+                with torch.cuda.graph(g):
+                    abi.sparoa_fc_ops_run(arr)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert all(int(c.path_dev.item()) == fam for c in cs), "forced family"
+            ts = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                g.replay()
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e3)
+            out[(m, fam)] = sorted(ts)[reps // 2]
+            del g
+    return out
 
 
 def path_times(abi, torch, cases, rounds=3):
@@ -478,18 +518,23 @@ def model_latencies(abi, torch, synth, reps=10):
     return out
 
 
-def calibrate(abi, cases):
-    """Thresholds per operator class (m), from the cold forced-path timings of
-    the whole path: the kernel family whose dense path is faster (intensity threshold: the
-    class's own intensity when the MFMA family wins, the bf16 ridge point
-    otherwise), and the smallest block sparsity at or above which that
-    family's skip path beats its dense path in every case of the class (1.0
-    when it never does)."""
+def calibrate(abi, cases, batch=None):
+    """Thresholds per operator class (m): the kernel family whose dense path
+    is faster -- over the class's operators issued as one executor batch when
+    `batch` (family_batch_times) is given, else summed over the cold
+    single-operator forced-path timings -- (intensity threshold: the class's
+    own intensity when the MFMA family wins, the bf16 ridge point otherwise),
+    and the smallest block sparsity at or above which that family's skip path
+    beats its dense path in every case of the class (1.0 when it never
+    does)."""
     out = {}
     for m in M_LIST:
         cs = [c for c in cases if c.m == m]
-        bw = sum(c.forced[abi.PATH_DENSE_BW] for c in cs)
-        mf = sum(c.forced[abi.PATH_DENSE_MFMA] for c in cs)
+        if batch is not None:
+            bw, mf = batch[(m, abi.PATH_DENSE_BW)], batch[(m, abi.PATH_DENSE_MFMA)]
+        else:
+            bw = sum(c.forced[abi.PATH_DENSE_BW] for c in cs)
+            mf = sum(c.forced[abi.PATH_DENSE_MFMA] for c in cs)
         fam = abi.PATH_DENSE_MFMA if mf < bw else abi.PATH_DENSE_BW
         c_thr = cs[0].inten["intensity"] if fam == abi.PATH_DENSE_MFMA else INTENSITY_THR
         pts = sorted((c.rho_b[fam], c.forced[fam | 1] < c.forced[fam]) for c in cs)
@@ -568,13 +613,15 @@ def main():
     if args.thresholds is None and args.no_sweep:
         print("bench.py: --no-sweep needs --thresholds", file=sys.stderr)
         sys.exit(2)
+    batch_times = None
     if args.no_sweep:
         for c in cases:
             c.forced, c.rho_b = {}, {}
     else:
         print("bench: forced-path sweep", file=sys.stderr, flush=True)
         forced_times(abi, torch, cases, paths_swept)
-    thresholds = calibrate(abi, cases) if args.thresholds is None else \
+        batch_times = family_batch_times(abi, torch, cases)
+    thresholds = calibrate(abi, cases, batch_times) if args.thresholds is None else \
         {int(k): tuple(v) for k, v in json.loads(args.thresholds).items()}
     for c in cases:
         c.s_thr, c.c_thr = thresholds[c.m]
@@ -699,17 +746,24 @@ def main():
         sel, us = fam_rows[fam]
         nb = sum(c.alg for c in sel)
         achieved = nb / (us * 1e-6) / 1e9
-        per_launch = int(nb / len(sel))
         if fam == abi.PATH_DENSE_BW:
-            kernel = "fc_bw_kernel (self-measuring; one launch per operator)"
+            # one grouped launch per 16 operators of one dtype and row-tile count
+            keys = {}
+            for c in sel:
+                keys[(c.desc.dtype, -(-c.m // 16))] = keys.get((c.desc.dtype, -(-c.m // 16)), 0) + 1
+            launches = sum(-(-v // 16) for v in keys.values())
+            kernel = ("fc_bw_measured_group (self-measuring weight-streaming FC; the family's "
+                      "operators in grouped launches of up to 16)")
         else:
+            launches = len(sel)
             kernel = ("igemm_kernel (per operator; the family's measurements and split-K "
                       "reductions run as grouped launches)")
+        per_launch = int(nb / launches)
         traffic = load_traffic(digest, abi.PATH_NAMES[fam], per_launch)
         return dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic, kernel=kernel,
-                    operators=len(sel), alg_bytes_per_launch=per_launch,
-                    avg_launch_us=round(us / len(sel), 3),
+                    operators=len(sel), launches=launches, alg_bytes_per_launch=per_launch,
+                    avg_launch_us=round(us / launches, 3),
                     timing="this family's operators of the step replayed as one HIP graph, HIP "
                            "events around every replay (gaps between launches included)",
                     source_digest=digest)
@@ -731,6 +785,8 @@ def main():
         step_gpu_us=round(step_gpu_us, 2),
         roofline=roofline,
         roofline_other_families=others,
+        family_batch_us=None if batch_times is None else {
+            f"m={m} {abi.PATH_NAMES[f]}": round(t, 2) for (m, f), t in batch_times.items()},
         sweep=table,
     )
     if not args.no_models:

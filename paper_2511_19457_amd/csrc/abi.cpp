@@ -1,5 +1,6 @@
 // extern "C" entry points of libsparoa.so: argument validation, the host-side
 // intensity and routing functions, and dispatch to the HIP kernels.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -823,9 +824,11 @@ sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa
   }
   // Batched: every op is validated first; the measurements of the ops that
   // measure in a launch of their own run grouped (counter init and
-  // measurement: two launches per kGroupMax ops of one element size); then
-  // each op's FC kernel in op order; then the split-K reductions, grouped
-  // per dtype.  Same kernels and arithmetic as op-by-op calls, fewer launches.
+  // measurement: two launches per kGroupMax ops of one element size); the
+  // self-measuring streaming FCs run grouped (one launch per kGroupMax ops of
+  // one dtype and row-tile count); then each other op's FC kernel in op
+  // order; then the split-K reductions, grouped per dtype.  Same arithmetic
+  // as op-by-op calls, fewer launches.
   std::vector<FcPlan> plan((size_t)n);
   for (int64_t i = 0; i < n; ++i) {
     const sparoa_fc_op &o = ops[i];
@@ -854,21 +857,44 @@ sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa
         (st = launch_measure_group(group.data(), (int)group.size(), stream)) != SPAROA_OK)
       return st;
   }
+  // Self-measuring streaming FCs run as grouped launches, one per key (dtype
+  // and row tiles) and kGroupMax ops, in op order within a group.
+  std::vector<int> keys;
+  for (int64_t i = 0; i < n; ++i) {
+    if (!plan[i].self_measures) continue;
+    const int k = fc_bw_group_key(ops[i].desc);
+    if (std::find(keys.begin(), keys.end(), k) == keys.end()) keys.push_back(k);
+  }
+  for (int key : keys) {
+    std::vector<FcBwJob> group;
+    for (int64_t i = 0; i < n; ++i) {
+      const sparoa_fc_op &o = ops[i];
+      if (!plan[i].self_measures || fc_bw_group_key(o.desc) != key) continue;
+      const sparoa_thresholds *t = thr ? thr : &o.thr;
+      group.push_back(FcBwJob{o.desc, o.x, o.w_packed, o.desc.has_bias ? o.bias : nullptr,
+                              o.residual, o.act, o.counts, o.mask, o.y,
+                              DeviceRoute{nullptr, t->sparsity_thr, t->mode, 1, o.path}});
+      if ((int)group.size() == kGroupMax) {
+        if ((st = launch_fc_bw_measured_group(group.data(), kGroupMax, stream)) != SPAROA_OK)
+          return st;
+        group.clear();
+      }
+    }
+    if (!group.empty() &&
+        (st = launch_fc_bw_measured_group(group.data(), (int)group.size(), stream)) != SPAROA_OK)
+      return st;
+  }
   std::vector<SplitReduceJob> reduces;
   for (int64_t i = 0; i < n; ++i) {
     const sparoa_fc_op &o = ops[i];
     const sparoa_thresholds *t = thr ? thr : &o.thr;
-    if (plan[i].self_measures) {
-      const DeviceRoute r{nullptr, t->sparsity_thr, t->mode, 1, o.path};
-      st = launch_fc_bw_measured(o.desc, o.x, o.w_packed, o.desc.has_bias ? o.bias : nullptr,
-                                 o.residual, o.act, o.counts, o.mask, o.y, stream, r);
-    } else {
-      SplitReduceJob job;
-      st = fc_routed_impl(&o.desc, t, o.counts, o.x, o.w_nk, o.w_packed, o.bias, o.residual,
-                          o.act, o.mask, o.y, o.workspace, o.ws_bytes, o.path, stream, &job);
-      if (st == SPAROA_OK && job.split > 1) reduces.push_back(job);
-    }
-    if (st != SPAROA_OK) return st;
+    if (plan[i].self_measures) continue;
+    SplitReduceJob job;
+    if ((st = fc_routed_impl(&o.desc, t, o.counts, o.x, o.w_nk, o.w_packed, o.bias, o.residual,
+                             o.act, o.mask, o.y, o.workspace, o.ws_bytes, o.path, stream,
+                             &job)) != SPAROA_OK)
+      return st;
+    if (job.split > 1) reduces.push_back(job);
   }
   for (sparoa_dtype dt : {SPAROA_F32, SPAROA_F16, SPAROA_BF16}) {
     std::vector<SplitReduceJob> group;

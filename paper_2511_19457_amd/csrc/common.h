@@ -31,6 +31,11 @@ inline int64_t elem_size(sparoa_dtype d) { return d == SPAROA_F32 ? 4 : 2; }
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Word 3 of a raw buffer descriptor on gfx9-family GPUs (32-bit data format;
+// untyped loads ignore the rest).  Buffer loads at an offset past the
+// descriptor's size return zero without a memory access.
+constexpr int kBufDword3 = 0x00020000;
+
 // Device-side routing: the skip decision is taken inside the kernel from the
 // counts the measurement kernel left in device memory (no host round trip);
 // the bandwidth bit depends on shapes only and is fixed by the host.
@@ -174,6 +179,23 @@ sparoa_status launch_fc_bw_measured(const sparoa_fc_desc &d, const void *x, cons
                                     const void *bias, const void *residual, sparoa_act act,
                                     sparoa_counts *counts, uint32_t *mask, void *y,
                                     hipStream_t stream, const DeviceRoute &route);
+
+// One self-measuring streaming FC of a grouped launch (route.counts unused).
+struct FcBwJob {
+  sparoa_fc_desc d;
+  const void *x, *w_packed, *bias, *residual;
+  sparoa_act act;
+  sparoa_counts *counts;
+  uint32_t *mask;
+  void *y;
+  DeviceRoute route;
+};
+// FCs with equal keys (>= 0) can share a grouped launch; -1: not self-measuring.
+int fc_bw_group_key(const sparoa_fc_desc &d);
+// Up to kGroupMax independent self-measuring FCs (no FC reads another's
+// output) of one key in one launch; per FC, the same arithmetic and outputs
+// as launch_fc_bw_measured.
+sparoa_status launch_fc_bw_measured_group(const FcBwJob *jobs, int n, hipStream_t stream);
 
 sparoa_status launch_maxpool(const void *x, sparoa_dtype dt, int64_t n, int64_t c, int64_t h,
                              int64_t w, int64_t k, int64_t s, int64_t p, void *y,

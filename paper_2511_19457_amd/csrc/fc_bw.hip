@@ -32,6 +32,9 @@
 #include "common.h"
 #include "dtype.h"
 
+#include <algorithm>
+#include <type_traits>
+
 namespace sparoa {
 namespace {
 
@@ -44,7 +47,10 @@ constexpr int kRowB = (kCh + 8) * 2;  // LDS row stride in bytes (80: conflict-f
 template <int MT>
 struct Shape {
   static constexpr int waves = MT <= 2 ? 16 : 8;
-  static constexpr int depth = MT == 1 ? 8 : (MT == 2 ? 5 : 4);  // within the VGPR budget
+  // ring depth (chunks in flight), dense and skip order, within the VGPR
+  // budget without spills (a skip-order chunk holds twice the input registers)
+  static constexpr int depth = MT == 1 ? 8 : 4;
+  static constexpr int list_depth = MT == 1 ? 6 : (MT == 4 ? 2 : 3);
 };
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -61,7 +67,6 @@ struct FcBwArgs {
   unsigned long long *executed;
   int64_t M, K, N, slice;
   int act;
-  int xvec;
   DeviceRoute route;
   sparoa_counts *mcounts;  // self-measuring form: outputs of the measurement
   uint32_t *mmask;
@@ -69,278 +74,359 @@ struct FcBwArgs {
 
 constexpr int kMaxColWords = kMaxWaveK * 16 / 32;  // bitmap words for the largest K
 
-// LDS of one wave: transposed weight tile [16 cols][32 entries], input tile
-// [16*MT rows][32 entries], and the wave's list of columns.
-template <int MT, bool SKIP>
-struct WaveLds {
+// LDS of one wave: transposed weight tile [16 cols][32 entries] and input
+// tile [16*MT rows][32 entries] of the chunk in flight to the MFMA.
+template <int MT>
+struct WaveTiles {
   char wt[kPanel * kRowB];
   char xs[MT * 16 * kRowB];
-  unsigned short list[SKIP ? kMaxWaveK : 8];
 };
 
+// ---- pieces shared by the single-operator and the grouped kernels --------
+
+// Measurement of x by one work-group of NW waves (the self-measuring forms):
+// zero count and the column bitmap at block (m, 1) into mbits (LDS), the
+// route decision from those counts with the host route's arithmetic.  When
+// store, the counts, the bitmap and the path also go to a.mcounts / a.mmask /
+// path_out.  Thread t owns column groups t, t + 64 NW, ... (8 columns = one
+// bitmap byte; K % 8 == 0): it ORs the group's nonzero flags over all rows
+// (kMR row loads in flight), counts zeros, and stores the byte; bytes past K
+// up to the last whole word are stored as 0.  The waves' sums meet in LDS.
+// Returns the skip decision (the same in every lane).
+template <int MT, int NW>
+__device__ __forceinline__ bool fc_measure_route(const FcBwArgs &a, bool store, uint32_t *mbits) {
+  constexpr int kThreads = 64 * NW;
+  constexpr int kMR = MT == 1 ? 8 : (MT == 2 ? 16 : 32);
+  __shared__ unsigned wsum[NW][2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ng = (int)(a.K / 8);
+  const int nbytes = 4 * (int)((a.K + 31) / 32);
+  unsigned zeros = 0, ones = 0;
+  for (int g = tid; g < nbytes; g += kThreads) {
+    uint32_t nzb = 0;
+    if (g < ng) {
+      const char *px = a.x + (int64_t)g * 16;
+      for (int m0 = 0; m0 < a.M; m0 += kMR) {
+        // unconditional loads (rows past M re-read row M - 1 and are masked
+        // below), so all kMR stay in flight
+        uint4 q[kMR];
+#pragma unroll
+        for (int u = 0; u < kMR; ++u) {
+          const int64_t r = min((int64_t)(m0 + u), a.M - 1);
+          q[u] = *reinterpret_cast<const uint4 *>(px + r * a.K * 2);
+        }
+#pragma unroll
+        for (int u = 0; u < kMR; ++u) {
+          const uint32_t wv[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+          uint32_t b = 0;
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            b |= ((wv[h] & 0x7FFFu) != 0u ? 1u : 0u) << (2 * h);
+            b |= ((wv[h] & 0x7FFF0000u) != 0u ? 1u : 0u) << (2 * h + 1);
+          }
+          const bool valid = m0 + u < a.M;
+          zeros += valid ? 8u - (unsigned)__popc(b) : 0u;
+          nzb |= valid ? b : 0u;
+        }
+      }
+      ones += (unsigned)__popc(nzb);
+    }
+    reinterpret_cast<unsigned char *>(mbits)[g] = (unsigned char)nzb;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    zeros += __shfl_xor(zeros, o, 64);
+    ones += __shfl_xor(ones, o, 64);
+  }
+  if (lane == 0) {
+    wsum[wave][0] = zeros;
+    wsum[wave][1] = ones;
+  }
+  __syncthreads();
+  zeros = 0;
+  ones = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    zeros += wsum[w][0];
+    ones += wsum[w][1];
+  }
+  sparoa_counts c;
+  c.zeros = zeros;
+  c.numel = (uint64_t)a.M * (uint64_t)a.K;
+  c.zero_blocks = (uint64_t)a.K - ones;
+  c.num_blocks = (uint64_t)a.K;
+  const bool skip = __builtin_amdgcn_readfirstlane(
+                        route_skip_counts(c, a.route.sparsity_thr, a.route.mode) ? 1 : 0) != 0;
+  if (store) {
+    for (int i = tid; i < nbytes / 4; i += kThreads) a.mmask[i] = mbits[i];
+    if (tid == 0) {
+      *a.mcounts = c;
+      if (a.route.path_out)
+        *a.route.path_out = (skip ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+    }
+  }
+  return skip;
+}
+
+// List of the nonzero columns of slice [kb, kb + count) (offsets from kb, in
+// order) built by one wave from the column bitmap: the slice's bitmap words
+// (at most 32: one per lane) are loaded at once, an exclusive prefix sum of
+// their popcounts gives each lane its place, then each lane writes the
+// offsets of its set bits.  Returns the list length (the same in every lane).
+__device__ __forceinline__ int fc_build_list(const uint32_t *colbits, int64_t kb, int count,
+                                             unsigned short *list, int lane) {
+  const int nw = (count + 31) / 32;
+  uint32_t wv = 0;
+  if (lane < nw) {
+    wv = colbits[(kb >> 5) + lane];
+    const int tail = count - 32 * lane;
+    if (tail < 32) wv &= (1u << tail) - 1u;
+  }
+  const int cnt = __popc(wv);
+  int incl = cnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += t;
+  }
+  int pos = incl - cnt;
+  while (wv) {
+    const int b = __ffs(wv) - 1;
+    list[pos++] = (unsigned short)(32 * lane + b);
+    wv &= wv - 1u;
+  }
+  return __builtin_amdgcn_readfirstlane(__shfl(incl, 63, 64));
+}
+
+// Register staging of one chunk: weight row e = lane / 2, half lane % 2;
+// the input as 4 * MT pairs (dense order: packed), or in skip order as
+// 8 * MT 16-bit gathers, each in a register of its own (two loads into the
+// halves of one register would make the second wait for the first).
+template <int MT, bool LIST>
+struct Stage {
+  uint4 w;
+  uint32_t xr[LIST ? 8 * MT : 4 * MT];
+};
+
+// Entry e of a slice walk -> column k, or -1 past its end.  LIST: the skip
+// order (list of nonzero columns of the slice), else dense order.
+// Branch-free: the list read is clamped and the result selected.
+template <bool LIST>
+__device__ __forceinline__ int fc_entry_k(const unsigned short *list, int kb, int count, int e) {
+  int k;
+  if constexpr (LIST) k = kb + (int)list[max(0, min(e, count - 1))];
+  else k = kb + e;
+  return e < count ? k : -1;
+}
+
+constexpr int kOob = (int)0x80000000;  // a buffer offset past every descriptor's size
+
+// Loads chunk c of the slice [kb, kb + count) of one 16-column panel (wrs:
+// its k-major weights).  Input, dense order: (row m, 8 entries) per
+// v = lane + 64 j, one 16-byte load (rows 16-byte aligned: XVEC) or eight
+// 2-byte loads; skip order: (row m, entries 2q, 2q + 1) per v = lane + 64 j,
+// two 2-byte gathers.  Both forms use the same 4 * MT registers.  Every load
+// is a buffer load issued unconditionally: an entry past the end, a row past
+// M or a ring slot past the last chunk (live false) reads zero from an
+// out-of-range offset without touching memory, so the compiler's load
+// counters stay exact and the ring stays in flight.
+template <int DT, int MT, bool LIST, bool XVEC>
+__device__ __forceinline__ void fc_load_chunk(Stage<MT, LIST> &s, __amdgpu_buffer_rsrc_t wrs,
+                                              __amdgpu_buffer_rsrc_t xrs, int Mi, int Ki, int kb,
+                                              int count, const unsigned short *list, int c,
+                                              bool live, int lane) {
+  using raw = typename Elem<DT>::raw;
+  const int k = fc_entry_k<LIST>(list, kb, count, c * kCh + (lane >> 1));
+  s.w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+      wrs, live && k >= 0 ? (k * kPanel + 8 * (lane & 1)) * 2 : kOob, 0, 0));
+  if constexpr (!LIST) {
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      const int v = lane + 64 * j;
+      const int m = v >> 2, e0 = c * kCh + 8 * (v & 3);
+      const int row = (m * Ki + kb + e0) * 2;
+      uint4 q;
+      if constexpr (XVEC) {  // count % 8 == 0: e0 < count covers all 8 entries
+        q = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+            xrs, live && m < Mi && e0 < count ? row : kOob, 0, 0));
+      } else {
+        raw t[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          t[i] = __builtin_bit_cast(raw, __builtin_amdgcn_raw_buffer_load_b16(
+              xrs, live && m < Mi && e0 + i < count ? row + 2 * i : kOob, 0, 0));
+        __builtin_memcpy(&q, t, 16);
+      }
+      __builtin_memcpy(&s.xr[4 * j], &q, 16);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4 * MT; ++j) {
+      const int v = lane + 64 * j;
+      const int m = v >> 4, e0 = c * kCh + 2 * (v & 15);
+      const int k0 = fc_entry_k<true>(list, kb, count, e0);
+      const int k1 = fc_entry_k<true>(list, kb, count, e0 + 1);
+      const bool ok = live && m < Mi;
+      s.xr[2 * j] = __builtin_bit_cast(uint16_t, __builtin_amdgcn_raw_buffer_load_b16(
+          xrs, ok && k0 >= 0 ? (m * Ki + k0) * 2 : kOob, 0, 0));
+      s.xr[2 * j + 1] = __builtin_bit_cast(uint16_t, __builtin_amdgcn_raw_buffer_load_b16(
+          xrs, ok && k1 >= 0 ? (m * Ki + k1) * 2 : kOob, 0, 0));
+    }
+  }
+}
+
+// One staged chunk through the wave's LDS tiles (weights transposed on the
+// way in) into v_mfma_f32_16x16x32 over all m (padded to 16) and the
+// panel's 16 columns.  LDS operations of one wave execute in order: the
+// tile written here is the one read back, and the reads finish before the
+// next chunk's writes.
+template <int DT, int MT, bool LIST>
+__device__ __forceinline__ void fc_mma_chunk(const Stage<MT, LIST> &s, WaveTiles<MT> &T,
+                                             f32x4 (&acc)[MT], int lane) {
+  using raw = typename Elem<DT>::raw;
+  const int e = lane >> 1, c0 = 8 * (lane & 1);
+  raw h[8];
+  __builtin_memcpy(h, &s.w, 16);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) *reinterpret_cast<raw *>(&T.wt[(c0 + i) * kRowB + 2 * e]) = h[i];
+  if constexpr (!LIST) {
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      const int v = lane + 64 * j;
+      uint4 q;
+      __builtin_memcpy(&q, &s.xr[4 * j], 16);
+      *reinterpret_cast<uint4 *>(&T.xs[(v >> 2) * kRowB + 16 * (v & 3)]) = q;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4 * MT; ++j) {
+      const int v = lane + 64 * j;
+      *reinterpret_cast<uint32_t *>(&T.xs[(v >> 4) * kRowB + 4 * (v & 15)]) =
+          s.xr[2 * j] | (s.xr[2 * j + 1] << 16);
+    }
+  }
+  const int g = lane >> 4, rl = lane & 15;
+  const char *brow = &T.wt[rl * kRowB + 16 * g];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const char *arow = &T.xs[(mt * 16 + rl) * kRowB + 16 * g];
+    if constexpr (DT == SPAROA_BF16)
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8 *>(arow),
+                                                        *reinterpret_cast<const bf16x8 *>(brow),
+                                                        acc[mt], 0, 0, 0);
+    else
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(*reinterpret_cast<const f16x8 *>(arow),
+                                                       *reinterpret_cast<const f16x8 *>(brow),
+                                                       acc[mt], 0, 0, 0);
+  }
+}
+
+// Output element (row, col) from its fp32 sum: bias, residual, activation,
+// cast (the same order in both kernels).
+template <int DT>
+__device__ __forceinline__ void fc_store(const FcBwArgs &a, int64_t row, int64_t col, float o) {
+  using E = Elem<DT>;
+  using raw = typename E::raw;
+  if (a.bias) o += E::to_f32(reinterpret_cast<const raw *>(a.bias)[col]);
+  if (a.residual) o += E::to_f32(reinterpret_cast<const raw *>(a.residual)[row * a.N + col]);
+  reinterpret_cast<raw *>(a.y)[row * a.N + col] = E::from_f32(apply_act(o, a.act));
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t fc_panel_rsrc(const FcBwArgs &a, int64_t p) {
+  return __builtin_amdgcn_make_buffer_rsrc((void *)(a.wp + p * a.K * kPanel * 2), (short)0,
+                                           (int)(a.K * kPanel * 2), kBufDword3);
+}
+
+// ---- single operator: one work-group per panel ----------------------------
+// Wave w walks K slice w ([w * slice, (w + 1) * slice) ∩ [0, K)); the waves'
+// fp32 partials meet in LDS and are added in wave order (deterministic).
 template <int DT, int MT, bool SKIP, bool XVEC, bool MEASURE = false>
 __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_kernel(FcBwArgs a) {
   static_assert(!MEASURE || SKIP, "the self-measuring form may skip");
   constexpr int NW = Shape<MT>::waves;
   constexpr int kDepth = Shape<MT>::depth;
   constexpr int kThreads = 64 * NW;
-  using E = Elem<DT>;
-  using raw = typename E::raw;
-  static_assert(E::size == 2, "16-bit types only");
-  using Lds = WaveLds<MT, SKIP>;
+  static_assert(Elem<DT>::size == 2, "16-bit types only");
+  __shared__ WaveTiles<MT> tiles[NW];
+  __shared__ unsigned short lists[SKIP ? NW : 1][SKIP ? kMaxWaveK : 1];
+  __shared__ float red[NW * MT * 16 * kPanel];  // [wave][16*MT][16] partials
+  __shared__ uint32_t mbits[MEASURE ? kMaxColWords : 1];
   // gfx950 addresses 160 KB of LDS per work-group
-  static_assert(sizeof(Lds) * NW <= 160 * 1024, "LDS budget");
-  static_assert(sizeof(Lds) * NW >= NW * MT * 16 * kPanel * 4, "reduction space");
-  __shared__ __attribute__((aligned(16))) char lds_raw[sizeof(Lds) * NW];
+  static_assert(sizeof(tiles) + sizeof(lists) + sizeof(red) + sizeof(mbits) <= 160 * 1024,
+                "LDS budget");
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  Lds &L = reinterpret_cast<Lds *>(lds_raw)[wave];
+  // wave, count, use_list: the same in every lane of a wave; readfirstlane
+  // tells the compiler, so descriptors and loop bounds live in scalar
+  // registers (no per-lane loops around buffer loads, no divergent branches)
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int64_t p = blockIdx.x;
-  const int64_t kb = (int64_t)wave * a.slice;
-  const int64_t ke = min(kb + a.slice, a.K);
-  const char *wpanel = a.wp + p * a.K * kPanel * 2;
-
-  int count = ke > kb ? (int)(ke - kb) : 0;
+  const int kb = (int)(wave * a.slice);
+  int count = (int)max((int64_t)0, min(a.slice, a.K - kb));
   bool use_list = SKIP;
   const uint32_t *colbits = a.mask;
-  if constexpr (SKIP) {
-    __shared__ uint32_t mbits[MEASURE ? kMaxColWords : 1];
-    if constexpr (MEASURE) {
-      // Thread t owns column groups t, t + kThreads, ... (8 columns = one
-      // bitmap byte; K % 8 == 0): it ORs the group's nonzero flags over all
-      // rows (kMR row loads in flight), counts zeros, and stores the byte;
-      // bytes past K up to the last whole word are stored as 0.  The waves'
-      // sums meet in LDS: one barrier.
-      constexpr int kMR = MT == 1 ? 8 : (MT == 2 ? 16 : 32);
-      __shared__ unsigned wsum[NW][2];
-      const int ng = (int)(a.K / 8);
-      const int nbytes = 4 * (int)((a.K + 31) / 32);
-      unsigned zeros = 0, ones = 0;
-      for (int g = tid; g < nbytes; g += kThreads) {
-        uint32_t nzb = 0;
-        if (g < ng) {
-          const char *px = a.x + (int64_t)g * 16;
-          for (int m0 = 0; m0 < a.M; m0 += kMR) {
-            // unconditional loads (rows past M re-read row M - 1 and are
-            // masked below), so all kMR stay in flight
-            uint4 q[kMR];
-#pragma unroll
-            for (int u = 0; u < kMR; ++u) {
-              const int64_t r = min((int64_t)(m0 + u), a.M - 1);
-              q[u] = *reinterpret_cast<const uint4 *>(px + r * a.K * 2);
-            }
-#pragma unroll
-            for (int u = 0; u < kMR; ++u) {
-              const uint32_t wv[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
-              uint32_t b = 0;
-#pragma unroll
-              for (int h = 0; h < 4; ++h) {
-                b |= ((wv[h] & 0x7FFFu) != 0u ? 1u : 0u) << (2 * h);
-                b |= ((wv[h] & 0x7FFF0000u) != 0u ? 1u : 0u) << (2 * h + 1);
-              }
-              const bool valid = m0 + u < a.M;
-              zeros += valid ? 8u - (unsigned)__popc(b) : 0u;
-              nzb |= valid ? b : 0u;
-            }
-          }
-          ones += (unsigned)__popc(nzb);
-        }
-        reinterpret_cast<unsigned char *>(mbits)[g] = (unsigned char)nzb;
-      }
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        zeros += __shfl_xor(zeros, o, 64);
-        ones += __shfl_xor(ones, o, 64);
-      }
-      if (lane == 0) {
-        wsum[wave][0] = zeros;
-        wsum[wave][1] = ones;
-      }
-      __syncthreads();
-      zeros = 0;
-      ones = 0;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        zeros += wsum[w][0];
-        ones += wsum[w][1];
-      }
-      const int nwords = nbytes / 4;
-      sparoa_counts c;
-      c.zeros = zeros;
-      c.numel = (uint64_t)a.M * (uint64_t)a.K;
-      c.zero_blocks = (uint64_t)a.K - ones;
-      c.num_blocks = (uint64_t)a.K;
-      use_list = route_skip_counts(c, a.route.sparsity_thr, a.route.mode);
-      if (p == 0) {
-        for (int i = tid; i < nwords; i += kThreads) a.mmask[i] = mbits[i];
-        if (tid == 0) {
-          *a.mcounts = c;
-          if (a.route.path_out)
-            *a.route.path_out = (use_list ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
-        }
-      }
-      colbits = mbits;
-    } else if (a.route.counts) {
+  if constexpr (MEASURE) {
+    use_list = fc_measure_route<MT, NW>(a, p == 0, mbits);
+    colbits = mbits;
+  } else if constexpr (SKIP) {
+    if (a.route.counts) {
       use_list = device_route_skip(a.route);
       if (a.route.path_out && p == 0 && tid == 0)
         *a.route.path_out = (use_list ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
     }
   }
+  const unsigned short *list = lists[SKIP ? wave : 0];
   if (SKIP && use_list) {
-    // The slice's bitmap words (at most 32: one per lane) are loaded at once;
-    // an exclusive prefix sum of their popcounts gives each lane its place
-    // in the list, then each lane writes the offsets of its set bits.
-    const int nw = (count + 31) / 32;
-    uint32_t wv = 0;
-    if (lane < nw) {
-      wv = colbits[(kb >> 5) + lane];
-      const int tail = count - 32 * lane;
-      if (tail < 32) wv &= (1u << tail) - 1u;
-    }
-    const int cnt = __popc(wv);
-    int incl = cnt;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int t = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += t;
-    }
-    int pos = incl - cnt;
-    while (wv) {
-      const int b = __ffs(wv) - 1;
-      L.list[pos++] = (unsigned short)(32 * lane + b);
-      wv &= wv - 1u;
-    }
-    const int total = __shfl(incl, 63, 64);
-    count = total;
-    if (a.executed && p == 0 && lane == 0 && total)
-      atomicAdd(a.executed, (unsigned long long)total);
+    count = fc_build_list(colbits, kb, count, lists[wave], lane);
+    if (a.executed && p == 0 && lane == 0 && count)
+      atomicAdd(a.executed, (unsigned long long)count);
   }
+  // Chunk c sits in register slot c % D (the ring depth); ring slots past the last chunk
+  // load nothing.
   const int nch = (count + kCh - 1) / kCh;
-
-  // entry -> column k (or -1 past the end of the wave's list)
-  auto entry_k = [&](int e) -> int64_t {
-    if (e >= count) return -1;
-    if (SKIP && use_list) return kb + (int64_t)L.list[e];
-    return kb + e;
-  };
-  // Register staging of one chunk: weight row e = lane / 2, half lane % 2.
-  // Input, vector form: (row m, 8 entries) per v = lane + 64 j, one 16-byte
-  // load when the 8 columns are contiguous (dense order);
-  // pair form (skip order): (row m, entries 2q, 2q + 1) per v = lane + 64 j,
-  // one 4-byte load when the two columns are adjacent, else two gathers.
-  // Both forms use the same 4 * MT registers.
-  const bool vecform = !SKIP || !use_list;
-  const bool xvec = XVEC || (SKIP && a.xvec);  // rows 16-byte aligned
-  struct Stage {
-    uint4 w;
-    uint32_t xr[4 * MT];
-  };
-  auto load = [&](int c, Stage &s) {
-    const int64_t k = entry_k(c * kCh + (lane >> 1));
-    s.w = k >= 0 ? *reinterpret_cast<const uint4 *>(wpanel + (k * kPanel + 8 * (lane & 1)) * 2)
-                 : make_uint4(0, 0, 0, 0);
-    if (vecform) {
-#pragma unroll
-      for (int j = 0; j < MT; ++j) {
-        const int v = lane + 64 * j;
-        const int m = v >> 2, e0 = c * kCh + 8 * (v & 3);
-        uint4 q = make_uint4(0, 0, 0, 0);
-        if (m < a.M) {
-          if (xvec && e0 + 8 <= count) {
-            q = *reinterpret_cast<const uint4 *>(a.x + (m * a.K + kb + e0) * 2);
-          } else {
-            raw t[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-              t[i] = e0 + i < count ? reinterpret_cast<const raw *>(a.x)[m * a.K + kb + e0 + i]
-                                    : (raw)0;
-            __builtin_memcpy(&q, t, 16);
-          }
-        }
-        __builtin_memcpy(&s.xr[4 * j], &q, 16);
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4 * MT; ++j) {
-        const int v = lane + 64 * j;
-        const int m = v >> 4, e0 = c * kCh + 2 * (v & 15);
-        uint32_t pr = 0;
-        if (m < a.M) {
-          const int64_t k0 = entry_k(e0), k1 = entry_k(e0 + 1);
-          const raw *xr = reinterpret_cast<const raw *>(a.x) + m * a.K;
-          if (k0 >= 0 && k1 == k0 + 1 && ((m * a.K + k0) & 1) == 0) {  // 4-byte aligned pair
-            pr = *reinterpret_cast<const uint32_t *>(xr + k0);
-          } else {
-            const uint32_t lo = k0 >= 0 ? xr[k0] : 0u, hi = k1 >= 0 ? xr[k1] : 0u;
-            pr = lo | (hi << 16);
-          }
-        }
-        s.xr[j] = pr;
-      }
-    }
-  };
-  auto stash = [&](const Stage &s) {
-    // weights: lane holds columns 8h..8h+7 of entry e; write them transposed
-    const int e = lane >> 1, c0 = 8 * (lane & 1);
-    raw h[8];
-    __builtin_memcpy(h, &s.w, 16);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) *reinterpret_cast<raw *>(&L.wt[(c0 + i) * kRowB + 2 * e]) = h[i];
-    if (vecform) {
-#pragma unroll
-      for (int j = 0; j < MT; ++j) {
-        const int v = lane + 64 * j;
-        uint4 q;
-        __builtin_memcpy(&q, &s.xr[4 * j], 16);
-        *reinterpret_cast<uint4 *>(&L.xs[(v >> 2) * kRowB + 16 * (v & 3)]) = q;
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4 * MT; ++j) {
-        const int v = lane + 64 * j;
-        *reinterpret_cast<uint32_t *>(&L.xs[(v >> 4) * kRowB + 4 * (v & 15)]) = s.xr[j];
-      }
-    }
-  };
-
+  const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)a.x, (short)0, (int)(a.M * a.K * 2), kBufDword3);
+  const __amdgpu_buffer_rsrc_t wrs = fc_panel_rsrc(a, p);
+  const int Mi = (int)a.M, Ki = (int)a.K;
   f32x4 acc[MT];
 #pragma unroll
   for (int i = 0; i < MT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int g = lane >> 4, rl = lane & 15;
 
-  Stage st[kDepth];
+  // the walk, with the order (dense or skip list) fixed outside the loop
+  auto run = [&](auto list_tag) __attribute__((always_inline)) {
+    constexpr bool LIST = decltype(list_tag)::value;
+    constexpr int D = LIST ? Shape<MT>::list_depth : kDepth;
+    Stage<MT, LIST> st[D];
 #pragma unroll
-  for (int j = 0; j < kDepth; ++j)
-    if (j < nch) load(j, st[j]);
-  for (int c0 = 0; c0 < nch; c0 += kDepth) {
+    for (int j = 0; j < D; ++j) {
+      fc_load_chunk<DT, MT, LIST, XVEC>(st[j], wrs, xrs, Mi, Ki, kb, count, list, j, j < nch,
+                                        lane);
+      __builtin_amdgcn_sched_barrier(0);  // slot order, as in the steady state
+    }
+    // steady state: straight-line groups of D chunks; then the last
+    // (partial) group, whose chunks are all loaded already
+    int c0 = 0;
+    for (; c0 + D <= nch; c0 += D) {
 #pragma unroll
-    for (int j = 0; j < kDepth; ++j) {
-      const int c = c0 + j;
-      if (c < nch) {
-        // LDS operations of one wave execute in order: the tile written here
-        // is the one read below, and the reads finish before the next write.
-        stash(st[j]);
-        const char *brow = &L.wt[rl * kRowB + 16 * g];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const char *arow = &L.xs[(mt * 16 + rl) * kRowB + 16 * g];
-          if constexpr (DT == SPAROA_BF16)
-            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                *reinterpret_cast<const bf16x8 *>(arow), *reinterpret_cast<const bf16x8 *>(brow),
-                acc[mt], 0, 0, 0);
-          else
-            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                *reinterpret_cast<const f16x8 *>(arow), *reinterpret_cast<const f16x8 *>(brow),
-                acc[mt], 0, 0, 0);
-        }
-        if (c + kDepth < nch) load(c + kDepth, st[j]);
+      for (int j = 0; j < D; ++j) {
+        fc_mma_chunk<DT, MT, LIST>(st[j], tiles[wave], acc, lane);
+        const int cn = c0 + j + D;
+        fc_load_chunk<DT, MT, LIST, XVEC>(st[j], wrs, xrs, Mi, Ki, kb, count, list, cn, cn < nch,
+                                          lane);
+        // keep the steps in order: hoisting later steps' LDS staging would
+        // wait for all the ring's chunks at once and drain it
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
-  }
+#pragma unroll
+    for (int j = 0; j < D; ++j)
+      if (c0 + j < nch) fc_mma_chunk<DT, MT, LIST>(st[j], tiles[wave], acc, lane);
+  };
+  if (SKIP && use_list) run(std::true_type{});
+  else run(std::false_type{});
 
-  // Cross-wave reduction in wave order through LDS (reuses the tiles).
   __syncthreads();
-  float *red = reinterpret_cast<float *>(lds_raw);  // [wave][16*MT][16]
+  const int g = lane >> 4, rl = lane & 15;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -353,10 +439,153 @@ __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_kernel(FcBwArgs a
     float o = 0.f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) o += red[w * MT * 16 * kPanel + e];
-    if (a.bias) o += E::to_f32(reinterpret_cast<const raw *>(a.bias)[col]);
-    if (a.residual) o += E::to_f32(reinterpret_cast<const raw *>(a.residual)[row * a.N + col]);
-    reinterpret_cast<raw *>(a.y)[row * a.N + col] = E::from_f32(apply_act(o, a.act));
+    fc_store<DT>(a, row, col, o);
   }
+}
+
+// ---- several operators in one launch: one wave per panel ------------------
+// The G_j = start[j + 1] - start[j] work-groups of FC j each take NW
+// consecutive panels, one per wave.  A wave walks every K slice of the
+// single-operator kernel in slice order (the same chunks, lists and MFMA
+// sequence), keeps each slice's partial apart and adds it to its sum at the
+// slice's end: the sums are those of the single-operator kernel bit for bit,
+// and the stream needs no barrier, so every wave keeps its ring in flight.
+// The work-group measures x once, and its waves build the slice lists
+// together (wave s: slice s).
+struct FcBwGroup {
+  FcBwArgs op[kGroupMax];
+  int start[kGroupMax + 1];
+  int n;
+};
+static_assert(sizeof(FcBwGroup) <= 4096, "kernel argument space");
+
+// A copy of v held in scalar registers: v is the same in every lane, but the
+// compiler cannot see that for a kernel-argument entry picked by a computed
+// index (it would wrap each buffer load in a loop over distinct descriptors).
+template <typename T>
+__device__ __forceinline__ T uniform_copy(const T &v) {
+  static_assert(sizeof(T) % 4 == 0, "whole dwords");
+  uint32_t w[sizeof(T) / 4];
+  __builtin_memcpy(w, &v, sizeof(T));
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 4); ++i) w[i] = __builtin_amdgcn_readfirstlane(w[i]);
+  T out;
+  __builtin_memcpy(&out, w, sizeof(T));
+  return out;
+}
+
+template <int DT, int MT>
+__global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_measured_group(FcBwGroup grp) {
+  constexpr int NW = Shape<MT>::waves;
+  constexpr int kDepth = Shape<MT>::depth;
+  __shared__ WaveTiles<MT> tiles[NW];
+  __shared__ unsigned short lists[NW][kMaxWaveK];
+  __shared__ int slice_count[NW];
+  __shared__ uint32_t mbits[kMaxColWords];
+  static_assert(sizeof(tiles) + sizeof(lists) + sizeof(mbits) <= 160 * 1024, "LDS budget");
+
+  int j = 0;
+  while (j + 1 < grp.n && (int)blockIdx.x >= grp.start[j + 1]) ++j;
+  const FcBwArgs a = uniform_copy(grp.op[j]);
+  const int wg = (int)blockIdx.x - grp.start[j];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  const bool use_list = fc_measure_route<MT, NW>(a, wg == 0, mbits);
+  const int nslices = (int)((a.K + a.slice - 1) / a.slice);  // <= NW
+  if (wave < nslices) {
+    const int kb = (int)(wave * a.slice);
+    int count = (int)min(a.slice, a.K - kb);
+    if (use_list) count = fc_build_list(mbits, kb, count, lists[wave], lane);
+    if (lane == 0) slice_count[wave] = count;
+  }
+  __syncthreads();  // the last barrier: waves past the last panel may leave now
+
+  const int64_t p = (int64_t)wg * NW + wave;
+  if (p >= (a.N + kPanel - 1) / kPanel) return;
+  const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)a.x, (short)0, (int)(a.M * a.K * 2), kBufDword3);
+  const __amdgpu_buffer_rsrc_t wrs = fc_panel_rsrc(a, p);
+  const int Mi = (int)a.M, Ki = (int)a.K, slice = (int)a.slice;
+
+  // The walk: every slice in slice order, each as nchu chunks (the most any
+  // slice has; chunks past a slice's entries load nothing and add zeros, so
+  // the slice partials are those of the single-operator kernel).  Entry i =
+  // chunk i % nchu of slice i / nchu, tracked by branch-free scalar cursors,
+  // so the steady-state loop is straight-line code (exact load counters, the
+  // ring stays in flight).  The ring slot of entry i is i % D (ring depth); slots
+  // past the end load nothing.
+  int nchu = 0;
+  for (int s = 0; s < nslices; ++s)
+    nchu = max(nchu, __builtin_amdgcn_readfirstlane((slice_count[s] + kCh - 1) / kCh));
+  const int total = nslices * nchu;
+  f32x4 acc[MT], sum[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) acc[i] = sum[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto run = [&](auto list_tag) __attribute__((always_inline)) {
+    constexpr bool LIST = decltype(list_tag)::value;
+    int ls = 0, lc = 0;  // load cursor: slice, chunk
+    auto load_at = [&](Stage<MT, LIST> &st, int i) __attribute__((always_inline)) {
+      const int sl = min(ls, nslices - 1);
+      fc_load_chunk<DT, MT, LIST, true>(st, wrs, xrs, Mi, Ki, sl * slice, slice_count[sl],
+                                        lists[sl], lc, i < total, lane);
+      const bool wrap = ++lc == nchu;
+      ls += wrap ? 1 : 0;
+      lc = wrap ? 0 : lc;
+    };
+    int cc = 0;  // compute cursor: chunk within the slice
+    // entry computed: at a slice's end its partial joins the sum (selects,
+    // no branch)
+    auto step = [&](const Stage<MT, LIST> &st) __attribute__((always_inline)) {
+      fc_mma_chunk<DT, MT, LIST>(st, tiles[wave], acc, lane);
+      const bool end = ++cc == nchu;
+      cc = end ? 0 : cc;
+#pragma unroll
+      for (int r = 0; r < MT; ++r) {
+        const f32x4 t = sum[r] + acc[r];
+        sum[r] = end ? t : sum[r];
+        acc[r] = end ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[r];
+      }
+    };
+    constexpr int D = LIST ? Shape<MT>::list_depth : kDepth;
+    Stage<MT, LIST> st[D];
+#pragma unroll
+    for (int q = 0; q < D; ++q) {
+      load_at(st[q], q);
+      __builtin_amdgcn_sched_barrier(0);  // slot order, as in the steady state
+    }
+    // steady state: straight-line groups of D entries; then the last
+    // (partial) group, whose entries are all loaded already
+    int i0 = 0;
+    for (; i0 + D <= total; i0 += D) {
+#pragma unroll
+      for (int q = 0; q < D; ++q) {
+        step(st[q]);
+        load_at(st[q], i0 + q + D);
+        // keep the steps in order: hoisting later steps' LDS staging would
+        // wait for all the ring's chunks at once and drain it
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < D; ++q)
+      if (i0 + q < total) step(st[q]);
+  };
+  if (total > 0) {
+    if (use_list) run(std::true_type{});
+    else run(std::false_type{});
+  }
+
+  const int g = lane >> 4, rl = lane & 15;
+  const int64_t col = p * kPanel + rl;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t row = mt * 16 + 4 * g + v;
+      if (row < a.M && col < a.N) fc_store<DT>(a, row, col, sum[mt][v]);
+    }
 }
 
 // Packs w[n][k] into 16-column k-major panels, zero-filled past n.
@@ -399,7 +628,9 @@ bool launch_mt(int mt, dim3 grid, hipStream_t st, const FcBwArgs &a) {
 
 template <int DT>
 bool launch_dt(int mt, bool skip, bool xvec, dim3 grid, hipStream_t st, const FcBwArgs &a) {
-  if (skip) return launch_mt<DT, true, false>(mt, grid, st, a);
+  if (skip)
+    return xvec ? launch_mt<DT, true, true>(mt, grid, st, a)
+                : launch_mt<DT, true, false>(mt, grid, st, a);
   return xvec ? launch_mt<DT, false, true>(mt, grid, st, a)
               : launch_mt<DT, false, false>(mt, grid, st, a);
 }
@@ -463,7 +694,6 @@ sparoa_status launch_fc_bw(const sparoa_fc_desc &d, sparoa_path, const void *x,
   const int mt = (int)cdiv(d.m, 16);
   // dense x rows are read as 16-byte vectors: needs every row 16-byte aligned
   const bool xvec = d.k % 8 == 0;
-  a.xvec = xvec ? 1 : 0;
   dim3 grid((unsigned)cdiv(d.n, kPanel));
   const bool ok = d.dtype == SPAROA_BF16 ? launch_dt<SPAROA_BF16>(mt, skip, xvec, grid, stream, a)
                                          : launch_dt<SPAROA_F16>(mt, skip, xvec, grid, stream, a);
@@ -490,7 +720,6 @@ sparoa_status launch_fc_bw_measured(const sparoa_fc_desc &d, const void *x, cons
   a.executed = nullptr;
   a.M = d.m; a.K = d.k; a.N = d.n; a.slice = slice_for(d);
   a.act = act;
-  a.xvec = 1;
   a.route = route;
   a.route.counts = nullptr;
   a.mcounts = counts;
@@ -498,10 +727,65 @@ sparoa_status launch_fc_bw_measured(const sparoa_fc_desc &d, const void *x, cons
   const int mt = (int)cdiv(d.m, 16);
   dim3 grid((unsigned)cdiv(d.n, kPanel));
   const bool ok = d.dtype == SPAROA_BF16
-                      ? launch_mt<SPAROA_BF16, true, false, true>(mt, grid, stream, a)
-                      : launch_mt<SPAROA_F16, true, false, true>(mt, grid, stream, a);
+                      ? launch_mt<SPAROA_BF16, true, true, true>(mt, grid, stream, a)
+                      : launch_mt<SPAROA_F16, true, true, true>(mt, grid, stream, a);
   if (!ok) return fail(SPAROA_ERR_UNSUPPORTED, "fc bandwidth path: m");
   SPAROA_LAUNCH_CHECK("fc_bw_kernel (self-measuring)");
+  return SPAROA_OK;
+}
+
+int fc_bw_group_key(const sparoa_fc_desc &d) {
+  return fc_bw_self_measures(d) ? (int)d.dtype * 8 + (int)cdiv(d.m, 16) : -1;
+}
+
+sparoa_status launch_fc_bw_measured_group(const FcBwJob *jobs, int n, hipStream_t stream) {
+  if (n < 1 || n > kGroupMax) return fail(SPAROA_ERR_INVALID_ARG, "fc group: size");
+  const int key = fc_bw_group_key(jobs[0].d);
+  FcBwGroup g;
+  g.n = n;
+  int64_t wg = 0;
+  for (int j = 0; j < n; ++j) {
+    const FcBwJob &o = jobs[j];
+    if (fc_bw_group_key(o.d) != key || key < 0)
+      return fail(SPAROA_ERR_INVALID_ARG, "fc group: mixed dtype or row tiles");
+    FcBwArgs &a = g.op[j];
+    a.x = static_cast<const char *>(o.x);
+    a.wp = static_cast<const char *>(o.w_packed);
+    a.bias = static_cast<const char *>(o.bias);
+    a.residual = static_cast<const char *>(o.residual);
+    a.y = static_cast<char *>(o.y);
+    a.mask = nullptr;
+    a.executed = nullptr;
+    a.M = o.d.m; a.K = o.d.k; a.N = o.d.n; a.slice = slice_for(o.d);
+    a.act = o.act;
+    a.route = o.route;
+    a.route.counts = nullptr;
+    a.mcounts = o.counts;
+    a.mmask = o.mask;
+    g.start[j] = (int)wg;
+    wg += cdiv(cdiv(o.d.n, kPanel), (int64_t)waves_for(o.d.m));  // a wave per panel
+    if (wg > (int64_t)1 << 30) return fail(SPAROA_ERR_UNSUPPORTED, "fc group: too many panels");
+  }
+  g.start[n] = (int)wg;
+  const int mt = (int)cdiv(jobs[0].d.m, 16);
+  const dim3 grid((unsigned)wg), block(64 * waves_for(jobs[0].d.m));
+  const bool bf = jobs[0].d.dtype == SPAROA_BF16;
+  switch (mt) {
+#define SPAROA_FCG(MT)                                                                   \
+  case MT:                                                                               \
+    if (bf)                                                                              \
+      hipLaunchKernelGGL((fc_bw_measured_group<SPAROA_BF16, MT>), grid, block, 0, stream, g); \
+    else                                                                                 \
+      hipLaunchKernelGGL((fc_bw_measured_group<SPAROA_F16, MT>), grid, block, 0, stream, g);  \
+    break;
+    SPAROA_FCG(1)
+    SPAROA_FCG(2)
+    SPAROA_FCG(3)
+    SPAROA_FCG(4)
+#undef SPAROA_FCG
+    default: return fail(SPAROA_ERR_UNSUPPORTED, "fc group: m");
+  }
+  SPAROA_LAUNCH_CHECK("fc_bw_measured_group");
   return SPAROA_OK;
 }
 

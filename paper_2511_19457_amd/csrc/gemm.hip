@@ -514,9 +514,6 @@ __global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
 // output equals the dense form's bit for bit.
 constexpr int kBK2 = 64;
 constexpr int kMaxChunks2 = 1024;          // K <= 65536 on the skip path
-// Word 3 of a raw buffer descriptor on gfx9-family GPUs (32-bit data format;
-// untyped dword loads ignore the rest).
-constexpr int kBufDword3 = 0x00020000;
 
 template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
 __global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {

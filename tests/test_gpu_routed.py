@@ -341,6 +341,54 @@ def test_fc_ops_run_batched_equals_op_by_op():
     assert torch.equal(y2, y_chain)
 
 
+def test_fc_ops_run_grouped_streaming_equals_op_by_op():
+    """Self-measuring streaming FCs run as grouped launches (one per dtype and
+    row-tile count, at most 16 ops each): 22 ops in 5 groups, m from 1 to 64
+    (ragged), bias and residual on some, skip and dense routes -- counts,
+    bitmap, path and output bits equal op-by-op calls; counts equal the
+    oracle's."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    specs = []
+    for i in range(18):                 # one key (bf16, one row tile): groups of 16 + 2
+        specs.append((1 + (i % 3) * 7, 1024 + 256 * (i % 2), 64 + 16 * (i % 5), abi.BF16))
+    specs += [(20, 512, 96, abi.BF16), (33, 768, 128, abi.F16), (64, 1024, 160, abi.F16),
+              (5, 2048, 48, abi.F16)]
+    bufs = []
+    for i, (m, k, n, dt) in enumerate(specs):
+        d = abi.fc_desc(m, k, n, dt, has_bias=(i % 4 == 1))
+        sd = "f16" if dt == abi.F16 else "bf16"
+        x = synth.sparse_matrix(m, k, (0.0, 0.5, 0.8, 0.95)[i % 4], "block" if i % 2 else "iid",
+                                sd, 800 + i).to(dev)
+        res = synth.normal((m, n), sd, 850 + i).to(dev) if i % 3 == 2 else None
+        b = _batch_op(abi, dev, d, x, 900 + i, thr=(0.1 + 0.05 * i, 315.0), residual=res)
+        b["bias"] = synth.normal((n,), sd, 950 + i).to(dev) if d.has_bias else None
+        bufs.append(b)
+    ops = [abi.fc_op(b["d"], b["x"], b["w"], b["wp"], b["bias"], b["res"], abi.ACT_RELU,
+                     b["counts"], b["mask"], b["y"], b["ws"], b["path"],
+                     (b["thr"][0], b["thr"][1], abi.ROUTE_BLOCK)) for b in bufs]
+    abi.sparoa_fc_ops_run(abi.fc_op_array(ops))
+    torch.cuda.synchronize()
+    seen = set()
+    for i, b in enumerate(bufs):
+        m, k = b["x"].shape
+        ref = oracle.measure(b["x"].cpu(), m, k, b["br"], b["bc"])
+        assert b["counts"].cpu().tolist() == [ref["zeros"], ref["numel"], ref["zero_blocks"],
+                                              ref["num_blocks"]], f"op {i}"
+        assert np.array_equal(b["mask"].cpu().numpy().view(np.uint32), ref["mask"]), f"op {i}"
+        c2 = torch.zeros_like(b["counts"])
+        k2 = torch.zeros_like(b["mask"])
+        y2 = torch.full_like(b["y"], float("nan"))
+        p2 = torch.full((1,), -1, dtype=torch.int32, device=dev)
+        abi.sparoa_fc_measured(b["d"], b["thr"][0], b["thr"][1], abi.ROUTE_BLOCK, b["x"], b["w"],
+                               b["wp"], b["bias"], b["res"], abi.ACT_RELU, c2, k2, y2, b["ws"], p2)
+        torch.cuda.synchronize()
+        assert int(p2.item()) == int(b["path"].item()), f"op {i}"
+        assert torch.equal(y2, b["y"]), f"op {i}"
+        seen.add(int(p2.item()))
+    assert seen == {abi.PATH_DENSE_BW, abi.PATH_SKIP_BW}
+
+
 def test_fc_ops_run_in_a_hip_graph_equals_eager():
     """The executor captured in a HIP graph: every replay (with eager work and
     synchronisations in between) gives the eager run's counts, paths and
