@@ -747,10 +747,10 @@ def main():
         nb = sum(c.alg for c in sel)
         achieved = nb / (us * 1e-6) / 1e9
         if fam == abi.PATH_DENSE_BW:
-            # one grouped launch per 16 operators of one dtype and row-tile count
+            # one grouped launch per 16 operators of one dtype
             keys = {}
             for c in sel:
-                keys[(c.desc.dtype, -(-c.m // 16))] = keys.get((c.desc.dtype, -(-c.m // 16)), 0) + 1
+                keys[c.desc.dtype] = keys.get(c.desc.dtype, 0) + 1
             launches = sum(-(-v // 16) for v in keys.values())
             kernel = ("fc_bw_measured_group (self-measuring weight-streaming FC; the family's "
                       "operators in grouped launches of up to 16)")

@@ -412,11 +412,13 @@ sparoa_status sparoa_fc_measured(const sparoa_fc_desc *desc, const sparoa_thresh
  * events (nullable): 2n hipEvent_t; events[2i] / events[2i+1] are recorded
  * on `stream` right before op i's first kernel / after its last kernel, and
  * the ops run one after another.  Without events the batch is validated
- * first and its launches are grouped: the ops that measure in a launch of
- * their own are measured together (two launches per 16 ops), then every
- * op's FC kernel runs in op order, then their split-K reductions run
- * together (one launch per 16 ops of a dtype); results are those of
- * op-by-op calls.  Ops whose inputs (x, residual) overlap another op's
+ * first and its launches are grouped: the self-measuring weight-streaming
+ * FCs (16-bit, m <= 64, k % 8 == 0, bandwidth route) run as one launch per
+ * 16 ops of a dtype and 16-row-tile count; the ops that measure in a launch
+ * of their own are measured together (two launches per 16 ops), then their
+ * FC kernels run in op order, then their split-K reductions run together
+ * (one launch per 16 ops of a dtype); results are those of op-by-op calls,
+ * bit for bit.  Ops whose inputs (x, residual) overlap another op's
  * output run op by op instead.
  * Stops at the first failing op and returns its status (a batch that fails
  * validation launches nothing).

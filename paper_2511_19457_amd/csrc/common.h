@@ -190,7 +190,8 @@ struct FcBwJob {
   void *y;
   DeviceRoute route;
 };
-// FCs with equal keys (>= 0) can share a grouped launch; -1: not self-measuring.
+// FCs with equal keys (>= 0: dtype and 16-row tiles) can share a grouped
+// launch; -1: not self-measuring.
 int fc_bw_group_key(const sparoa_fc_desc &d);
 // Up to kGroupMax independent self-measuring FCs (no FC reads another's
 // output) of one key in one launch; per FC, the same arithmetic and outputs

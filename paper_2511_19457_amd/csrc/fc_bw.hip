@@ -56,6 +56,7 @@ struct Shape {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 struct FcBwArgs {
   const char *x;
@@ -80,6 +81,12 @@ template <int MT>
 struct WaveTiles {
   char wt[kPanel * kRowB];
   char xs[MT * 16 * kRowB];
+};
+
+// LDS of one wave in the grouped kernel: the transposed weight tile only (the
+// input is staged per work-group).
+struct WeightTile {
+  char wt[kPanel * kRowB];
 };
 
 // ---- pieces shared by the single-operator and the grouped kernels --------
@@ -168,6 +175,94 @@ __device__ __forceinline__ bool fc_measure_route(const FcBwArgs &a, bool store, 
   return skip;
 }
 
+// The same measurement and route for any m, rows split over threads (the
+// grouped kernel, where m reaches 64): tpg threads per column group (a power
+// of two, tpg * groups <= 64 NW, tpg <= m), each ORs its rows' nonzero flags
+// into the group's bitmap byte with an LDS atomic and counts their zeros;
+// the nonzero-column count is taken from the finished bitmap.
+template <int NW>
+__device__ __forceinline__ bool fc_measure_route_rows(const FcBwArgs &a, bool store,
+                                                      uint32_t *mbits) {
+  constexpr int kThreads = 64 * NW;
+  constexpr int kMR = 8;
+  __shared__ unsigned wsum[NW][2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int M = (int)a.M;
+  const int ng = (int)(a.K / 8);
+  const int nwords = (int)((a.K + 31) / 32);
+  for (int i = tid; i < nwords; i += kThreads) mbits[i] = 0u;
+  __syncthreads();
+  int lt = 0;  // log2 of tpg
+  while ((2 << lt) * ng <= kThreads && (2 << lt) <= M) ++lt;
+  const int tpg = 1 << lt;
+  unsigned zeros = 0;
+  for (int t = tid; t < ng * tpg; t += kThreads) {
+    const int g = t >> lt, ph = t & (tpg - 1);
+    const char *px = a.x + (int64_t)g * 16;
+    uint32_t nzb = 0;
+    for (int m0 = ph * kMR; m0 < M; m0 += tpg * kMR) {
+      // unconditional loads (rows past M re-read row M - 1 and are masked
+      // below), so all kMR stay in flight
+      uint4 q[kMR];
+#pragma unroll
+      for (int u = 0; u < kMR; ++u) {
+        const int64_t r = min(m0 + u, M - 1);
+        q[u] = *reinterpret_cast<const uint4 *>(px + r * a.K * 2);
+      }
+#pragma unroll
+      for (int u = 0; u < kMR; ++u) {
+        const uint32_t wv[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+        uint32_t b = 0;
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          b |= ((wv[h] & 0x7FFFu) != 0u ? 1u : 0u) << (2 * h);
+          b |= ((wv[h] & 0x7FFF0000u) != 0u ? 1u : 0u) << (2 * h + 1);
+        }
+        const bool valid = m0 + u < M;
+        zeros += valid ? 8u - (unsigned)__popc(b) : 0u;
+        nzb |= valid ? b : 0u;
+      }
+    }
+    if (nzb) atomicOr(&mbits[g >> 2], nzb << (8 * (g & 3)));
+  }
+  __syncthreads();
+  unsigned ones = 0;
+  for (int i = tid; i < nwords; i += kThreads) ones += (unsigned)__popc(mbits[i]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    zeros += __shfl_xor(zeros, o, 64);
+    ones += __shfl_xor(ones, o, 64);
+  }
+  if (lane == 0) {
+    wsum[wave][0] = zeros;
+    wsum[wave][1] = ones;
+  }
+  __syncthreads();
+  zeros = 0;
+  ones = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    zeros += wsum[w][0];
+    ones += wsum[w][1];
+  }
+  sparoa_counts c;
+  c.zeros = zeros;
+  c.numel = (uint64_t)a.M * (uint64_t)a.K;
+  c.zero_blocks = (uint64_t)a.K - ones;
+  c.num_blocks = (uint64_t)a.K;
+  const bool skip = __builtin_amdgcn_readfirstlane(
+                        route_skip_counts(c, a.route.sparsity_thr, a.route.mode) ? 1 : 0) != 0;
+  if (store) {
+    for (int i = tid; i < nwords; i += kThreads) a.mmask[i] = mbits[i];
+    if (tid == 0) {
+      *a.mcounts = c;
+      if (a.route.path_out)
+        *a.route.path_out = (skip ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+    }
+  }
+  return skip;
+}
+
 // List of the nonzero columns of slice [kb, kb + count) (offsets from kb, in
 // order) built by one wave from the column bitmap: the slice's bitmap words
 // (at most 32: one per lane) are loaded at once, an exclusive prefix sum of
@@ -232,7 +327,8 @@ constexpr int kOob = (int)0x80000000;  // a buffer offset past every descriptor'
 // counters stay exact and the ring stays in flight.
 template <int DT, int MT, bool LIST, bool XVEC>
 __device__ __forceinline__ void fc_load_chunk(Stage<MT, LIST> &s, __amdgpu_buffer_rsrc_t wrs,
-                                              __amdgpu_buffer_rsrc_t xrs, int Mi, int Ki, int kb,
+                                              __amdgpu_buffer_rsrc_t xrs, int r0, int Mi, int Ki,
+                                              int kb,
                                               int count, const unsigned short *list, int c,
                                               bool live, int lane) {
   using raw = typename Elem<DT>::raw;
@@ -243,7 +339,7 @@ __device__ __forceinline__ void fc_load_chunk(Stage<MT, LIST> &s, __amdgpu_buffe
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
       const int v = lane + 64 * j;
-      const int m = v >> 2, e0 = c * kCh + 8 * (v & 3);
+      const int m = r0 + (v >> 2), e0 = c * kCh + 8 * (v & 3);
       const int row = (m * Ki + kb + e0) * 2;
       uint4 q;
       if constexpr (XVEC) {  // count % 8 == 0: e0 < count covers all 8 entries
@@ -263,7 +359,7 @@ __device__ __forceinline__ void fc_load_chunk(Stage<MT, LIST> &s, __amdgpu_buffe
 #pragma unroll
     for (int j = 0; j < 4 * MT; ++j) {
       const int v = lane + 64 * j;
-      const int m = v >> 4, e0 = c * kCh + 2 * (v & 15);
+      const int m = r0 + (v >> 4), e0 = c * kCh + 2 * (v & 15);
       const int k0 = fc_entry_k<true>(list, kb, count, e0);
       const int k1 = fc_entry_k<true>(list, kb, count, e0 + 1);
       const bool ok = live && m < Mi;
@@ -399,7 +495,7 @@ __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_kernel(FcBwArgs a
     Stage<MT, LIST> st[D];
 #pragma unroll
     for (int j = 0; j < D; ++j) {
-      fc_load_chunk<DT, MT, LIST, XVEC>(st[j], wrs, xrs, Mi, Ki, kb, count, list, j, j < nch,
+      fc_load_chunk<DT, MT, LIST, XVEC>(st[j], wrs, xrs, 0, Mi, Ki, kb, count, list, j, j < nch,
                                         lane);
       __builtin_amdgcn_sched_barrier(0);  // slot order, as in the steady state
     }
@@ -411,7 +507,7 @@ __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_kernel(FcBwArgs a
       for (int j = 0; j < D; ++j) {
         fc_mma_chunk<DT, MT, LIST>(st[j], tiles[wave], acc, lane);
         const int cn = c0 + j + D;
-        fc_load_chunk<DT, MT, LIST, XVEC>(st[j], wrs, xrs, Mi, Ki, kb, count, list, cn, cn < nch,
+        fc_load_chunk<DT, MT, LIST, XVEC>(st[j], wrs, xrs, 0, Mi, Ki, kb, count, list, cn, cn < nch,
                                           lane);
         // keep the steps in order: hoisting later steps' LDS staging would
         // wait for all the ring's chunks at once and drain it
@@ -443,15 +539,18 @@ __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_kernel(FcBwArgs a
   }
 }
 
-// ---- several operators in one launch: one wave per panel ------------------
-// The G_j = start[j + 1] - start[j] work-groups of FC j each take NW
+// ---- several operators in one launch --------------------------------------
+// The G_j = start[j + 1] - start[j] work-groups of FC j each take 16
 // consecutive panels, one per wave.  A wave walks every K slice of the
 // single-operator kernel in slice order (the same chunks, lists and MFMA
 // sequence), keeps each slice's partial apart and adds it to its sum at the
-// slice's end: the sums are those of the single-operator kernel bit for bit,
-// and the stream needs no barrier, so every wave keeps its ring in flight.
+// slice's end: the sums are those of the single-operator kernel bit for bit.
 // The work-group measures x once, and its waves build the slice lists
-// together (wave s: slice s).
+// together (wave s: slice s).  The input is staged once per work-group, SC
+// chunks at a time, in double-buffered LDS that all 16 waves read their MFMA
+// A operands from (x is read from L2 once per work-group, not once per
+// wave); the weights stream through a per-wave register ring that runs on
+// across the stage barriers.
 struct FcBwGroup {
   FcBwArgs op[kGroupMax];
   int start[kGroupMax + 1];
@@ -474,15 +573,42 @@ __device__ __forceinline__ T uniform_copy(const T &v) {
   return out;
 }
 
+
+// Waves (= panels) per work-group: 8, so that two work-groups share a CU
+// and the dispatcher rebalances as work-groups of skipped (short) operators
+// finish; chunks per x stage SC >= ring depth D, so that waiting for a
+// stage's x loads (issued SC chunks earlier) leaves the ring in flight.
+// Dense order stages 8 chunks and keeps 8 in flight; skip order, whose
+// gathers take a register per 2-byte value, 4 and 4 for m > 16.
+template <int MT, bool LIST = false>
+struct GroupShape {
+  static constexpr int NW = 8;
+  static constexpr int SC = LIST && MT > 1 ? 4 : 8;            // chunks per x stage
+  static constexpr int D = SC;                                 // weight ring depth (chunks)
+  static constexpr int U = SC;                                 // steps per loop iteration
+  static constexpr int XROW = SC * kCh * 2 + 16;               // LDS bytes per staged x row
+  static constexpr int XVEC = MT * 16 * SC * 4;                // 16-byte vectors per stage
+  static constexpr int XVAL = MT * 16 * SC * kCh;              // 2-byte values per stage
+  static constexpr int NXVEC = (XVEC + 64 * NW - 1) / (64 * NW);  // per thread
+  static constexpr int NXV = (XVAL + 64 * NW - 1) / (64 * NW);    // per thread
+};
+
 template <int DT, int MT>
-__global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_measured_group(FcBwGroup grp) {
-  constexpr int NW = Shape<MT>::waves;
-  constexpr int kDepth = Shape<MT>::depth;
-  __shared__ WaveTiles<MT> tiles[NW];
-  __shared__ unsigned short lists[NW][kMaxWaveK];
-  __shared__ int slice_count[NW];
+__global__ __launch_bounds__(64 * GroupShape<MT>::NW) void fc_bw_measured_group(FcBwGroup grp) {
+  constexpr int NW = GroupShape<MT>::NW;
+  constexpr int kThreads = 64 * NW;
+  constexpr int XROWMAX = GroupShape<MT>::XROW;  // the dense stage is the larger
+  using raw = typename Elem<DT>::raw;
+  __shared__ WeightTile wtiles[NW];  // each wave's transposed weight chunk
+  __shared__ __attribute__((aligned(16))) char xst[2][MT * 16 * XROWMAX];
+  constexpr int kMaxSlices = Shape<1>::waves;  // K slices of the single-operator kernel
+  __shared__ unsigned short lists[kMaxSlices][kMaxWaveK];
+  __shared__ int slice_count[kMaxSlices];
   __shared__ uint32_t mbits[kMaxColWords];
-  static_assert(sizeof(tiles) + sizeof(lists) + sizeof(mbits) <= 160 * 1024, "LDS budget");
+  // m <= 32: two work-groups per CU; larger m holds one (registers bound it)
+  static_assert(sizeof(wtiles) + sizeof(xst) + sizeof(lists) + sizeof(mbits) <=
+                    (MT <= 2 ? 80 : 160) * 1024,
+                "LDS budget");
 
   int j = 0;
   while (j + 1 < grp.n && (int)blockIdx.x >= grp.start[j + 1]) ++j;
@@ -491,33 +617,32 @@ __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_measured_group(Fc
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  const bool use_list = fc_measure_route<MT, NW>(a, wg == 0, mbits);
-  const int nslices = (int)((a.K + a.slice - 1) / a.slice);  // <= NW
-  if (wave < nslices) {
-    const int kb = (int)(wave * a.slice);
+  const bool use_list = fc_measure_route_rows<NW>(a, wg == 0, mbits);
+  const int nslices = (int)((a.K + a.slice - 1) / a.slice);  // <= kMaxSlices
+  for (int sl = wave; sl < nslices; sl += NW) {
+    const int kb = (int)(sl * a.slice);
     int count = (int)min(a.slice, a.K - kb);
-    if (use_list) count = fc_build_list(mbits, kb, count, lists[wave], lane);
-    if (lane == 0) slice_count[wave] = count;
+    if (use_list) count = fc_build_list(mbits, kb, count, lists[sl], lane);
+    if (lane == 0) slice_count[sl] = count;
   }
-  __syncthreads();  // the last barrier: waves past the last panel may leave now
+  __syncthreads();
 
+  // this wave's panel; waves past the last one still stage x and meet the
+  // barriers, but load no weights and store nothing
   const int64_t p = (int64_t)wg * NW + wave;
-  if (p >= (a.N + kPanel - 1) / kPanel) return;
+  const bool pvalid = p < (a.N + kPanel - 1) / kPanel;
   const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.x, (short)0, (int)(a.M * a.K * 2), kBufDword3);
-  const __amdgpu_buffer_rsrc_t wrs = fc_panel_rsrc(a, p);
+  const __amdgpu_buffer_rsrc_t wrs = fc_panel_rsrc(a, pvalid ? p : 0);
   const int Mi = (int)a.M, Ki = (int)a.K, slice = (int)a.slice;
 
   // The walk: every slice in slice order, each as nchu chunks (the most any
   // slice has; chunks past a slice's entries load nothing and add zeros, so
-  // the slice partials are those of the single-operator kernel).  Entry i =
-  // chunk i % nchu of slice i / nchu, tracked by branch-free scalar cursors,
-  // so the steady-state loop is straight-line code (exact load counters, the
-  // ring stays in flight).  The ring slot of entry i is i % D (ring depth); slots
-  // past the end load nothing.
+  // the slice partials are those of the single-operator kernel).  Chunk i =
+  // chunk i % nchu of slice i / nchu; x stage t holds chunks [t SC, t SC + SC).
   int nchu = 0;
-  for (int s = 0; s < nslices; ++s)
-    nchu = max(nchu, __builtin_amdgcn_readfirstlane((slice_count[s] + kCh - 1) / kCh));
+  for (int sl = 0; sl < nslices; ++sl)
+    nchu = max(nchu, __builtin_amdgcn_readfirstlane((slice_count[sl] + kCh - 1) / kCh));
   const int total = nslices * nchu;
   f32x4 acc[MT], sum[MT];
 #pragma unroll
@@ -525,20 +650,105 @@ __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_measured_group(Fc
 
   auto run = [&](auto list_tag) __attribute__((always_inline)) {
     constexpr bool LIST = decltype(list_tag)::value;
-    int ls = 0, lc = 0;  // load cursor: slice, chunk
-    auto load_at = [&](Stage<MT, LIST> &st, int i) __attribute__((always_inline)) {
-      const int sl = min(ls, nslices - 1);
-      fc_load_chunk<DT, MT, LIST, true>(st, wrs, xrs, Mi, Ki, sl * slice, slice_count[sl],
-                                        lists[sl], lc, i < total, lane);
-      const bool wrap = ++lc == nchu;
-      ls += wrap ? 1 : 0;
-      lc = wrap ? 0 : lc;
+    using GS = GroupShape<MT, LIST>;
+    constexpr int SC = GS::SC, D = GS::D, U = GS::U, XROW = GS::XROW;
+    constexpr int NXVEC = GS::NXVEC;  // staged 16-byte x vectors per thread (dense order)
+    constexpr int NXV = GS::NXV;      // staged 2-byte x values per thread (skip order)
+    static_assert(U % SC == 0 && U % D == 0 && SC >= D, "whole stages and ring cycles");
+    static_assert((LIST ? GS::XVAL : GS::XVEC) % kThreads == 0,
+                  "every thread stages whole vectors / values");
+    // Column of entry e of chunk i (-1 past the slice's entries or the walk).
+    // Everything is computed unconditionally and selected (a short-circuit
+    // here becomes a branch inside the ring, which drains it).
+    auto column = [&](int i, int e) __attribute__((always_inline)) -> int {
+      const int ic = min(i, total - 1);
+      const int sl = ic / nchu, c = ic - sl * nchu;
+      const int cnt = slice_count[sl];
+      const int ee = c * kCh + e;
+      int k;
+      if constexpr (LIST) k = sl * slice + (int)lists[sl][max(0, min(ee, cnt - 1))];
+      else k = sl * slice + ee;
+      const bool ok = (i < total) & (ee < cnt);
+      return ok ? k : -1;
     };
-    int cc = 0;  // compute cursor: chunk within the slice
-    // entry computed: at a slice's end its partial joins the sum (selects,
-    // no branch)
-    auto step = [&](const Stage<MT, LIST> &st) __attribute__((always_inline)) {
-      fc_mma_chunk<DT, MT, LIST>(st, tiles[wave], acc, lane);
+    // x stage t -> registers: dense, NXVEC 16-byte vectors (row, 8 entries)
+    // per thread; skip order, NXV 2-byte gathers per thread.
+    uint4 xv[NXVEC];
+    uint32_t xh[NXV];
+    auto stage_load = [&](int t) __attribute__((always_inline)) {
+      // rows past M read row M - 1: their outputs are never stored, and an
+      // MFMA output row depends on its own A row only (no per-lane test
+      // here, which the compiler would turn into a branch in the ring)
+      if constexpr (!LIST) {
+#pragma unroll
+        for (int u = 0; u < NXVEC; ++u) {
+          const int v = tid + kThreads * u;
+          const int r = v / (SC * 4), eg = v - r * (SC * 4);
+          const int k = column(t * SC + (eg >> 2), 8 * (eg & 3));
+          xv[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+              xrs, k >= 0 ? (min(r, Mi - 1) * Ki + k) * 2 : kOob, 0, 0));
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < NXV; ++u) {
+          const int v = tid + kThreads * u;
+          const int r = v / (SC * kCh), ev = v - r * (SC * kCh);
+          const int k = column(t * SC + ev / kCh, ev % kCh);
+          xh[u] = __builtin_bit_cast(uint16_t, __builtin_amdgcn_raw_buffer_load_b16(
+              xrs, k >= 0 ? (min(r, Mi - 1) * Ki + k) * 2 : kOob, 0, 0));
+        }
+      }
+    };
+    auto stage_store = [&](int t) __attribute__((always_inline)) {
+      char *buf = xst[t & 1];
+      if constexpr (!LIST) {
+#pragma unroll
+        for (int u = 0; u < NXVEC; ++u) {
+          const int v = tid + kThreads * u;
+          const int r = v / (SC * 4), eg = v - r * (SC * 4);
+          *reinterpret_cast<uint4 *>(&buf[r * XROW + 16 * eg]) = xv[u];
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < NXV; ++u) {
+          const int v = tid + kThreads * u;
+          const int r = v / (SC * kCh), ev = v - r * (SC * kCh);
+          *reinterpret_cast<raw *>(&buf[r * XROW + 2 * ev]) = (raw)xh[u];
+        }
+      }
+    };
+    // weight ring: chunk i's 32 entries, lane = (entry lane / 2, half lane % 2)
+    auto wload = [&](uint4 &w, int i) __attribute__((always_inline)) {
+      const int k = column(i, lane >> 1);
+      w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+          wrs, pvalid && k >= 0 ? (k * kPanel + 8 * (lane & 1)) * 2 : kOob, 0, 0));
+    };
+    int cc = 0;  // chunks done in the current slice
+    auto step = [&](const uint4 &w, int i) __attribute__((always_inline)) {
+      // weights transposed into the wave's tile, then MT MFMAs whose A
+      // operands come straight from the staged x
+      WeightTile &T = wtiles[wave];
+      const int e = lane >> 1, c0 = 8 * (lane & 1);
+      raw h[8];
+      __builtin_memcpy(h, &w, 16);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) *reinterpret_cast<raw *>(&T.wt[(c0 + q) * kRowB + 2 * e]) = h[q];
+      const int g = lane >> 4, rl = lane & 15;
+      const u32x4 bq = *reinterpret_cast<const u32x4 *>(&T.wt[rl * kRowB + 16 * g]);
+      const char *xa = &xst[(i / SC) & 1][rl * XROW + ((i % SC) * kCh + 8 * g) * 2];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const u32x4 aq = *reinterpret_cast<const u32x4 *>(xa + mt * 16 * XROW);
+        if constexpr (DT == SPAROA_BF16)
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, aq),
+                                                            __builtin_bit_cast(bf16x8, bq),
+                                                            acc[mt], 0, 0, 0);
+        else
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, aq),
+                                                           __builtin_bit_cast(f16x8, bq),
+                                                           acc[mt], 0, 0, 0);
+      }
+      // at a slice's end its partial joins the sum (selects, no branch)
       const bool end = ++cc == nchu;
       cc = end ? 0 : cc;
 #pragma unroll
@@ -548,35 +758,36 @@ __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_measured_group(Fc
         acc[r] = end ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[r];
       }
     };
-    constexpr int D = LIST ? Shape<MT>::list_depth : kDepth;
-    Stage<MT, LIST> st[D];
+
+    uint4 ring[D];
+    stage_load(0);
+    stage_store(0);
 #pragma unroll
     for (int q = 0; q < D; ++q) {
-      load_at(st[q], q);
-      __builtin_amdgcn_sched_barrier(0);  // slot order, as in the steady state
+      wload(ring[q], q);
+      __builtin_amdgcn_sched_barrier(0);  // slot order, as in the loop
     }
-    // steady state: straight-line groups of D entries; then the last
-    // (partial) group, whose entries are all loaded already
-    int i0 = 0;
-    for (; i0 + D <= total; i0 += D) {
+    __syncthreads();
+    const int iters = (total + U - 1) / U;  // loop iterations of U steps
+    for (int it = 0; it < iters; ++it) {
 #pragma unroll
-      for (int q = 0; q < D; ++q) {
-        step(st[q]);
-        load_at(st[q], i0 + q + D);
-        // keep the steps in order: hoisting later steps' LDS staging would
-        // wait for all the ring's chunks at once and drain it
-        __builtin_amdgcn_sched_barrier(0);
+      for (int q = 0; q < U; ++q) {
+        const int i = it * U + q;
+        if (q % SC == 0) stage_load(i / SC + 1);  // the next stage, during this one
+        step(ring[q % D], i);
+        wload(ring[q % D], i + D);
+        if (q % SC == SC - 1) {
+          stage_store(i / SC + 1);
+          __syncthreads();  // next stage staged; this stage's readers done
+        }
+        __builtin_amdgcn_sched_barrier(0);  // keep the steps in order
       }
     }
-#pragma unroll
-    for (int q = 0; q < D; ++q)
-      if (i0 + q < total) step(st[q]);
   };
-  if (total > 0) {
-    if (use_list) run(std::true_type{});
-    else run(std::false_type{});
-  }
+  if (use_list) run(std::true_type{});
+  else run(std::false_type{});
 
+  if (!pvalid) return;
   const int g = lane >> 4, rl = lane & 15;
   const int64_t col = p * kPanel + rl;
 #pragma unroll
@@ -747,7 +958,7 @@ sparoa_status launch_fc_bw_measured_group(const FcBwJob *jobs, int n, hipStream_
   for (int j = 0; j < n; ++j) {
     const FcBwJob &o = jobs[j];
     if (fc_bw_group_key(o.d) != key || key < 0)
-      return fail(SPAROA_ERR_INVALID_ARG, "fc group: mixed dtype or row tiles");
+      return fail(SPAROA_ERR_INVALID_ARG, "fc group: mixed dtypes or row tiles");
     FcBwArgs &a = g.op[j];
     a.x = static_cast<const char *>(o.x);
     a.wp = static_cast<const char *>(o.w_packed);
@@ -763,19 +974,18 @@ sparoa_status launch_fc_bw_measured_group(const FcBwJob *jobs, int n, hipStream_
     a.mcounts = o.counts;
     a.mmask = o.mask;
     g.start[j] = (int)wg;
-    wg += cdiv(cdiv(o.d.n, kPanel), (int64_t)waves_for(o.d.m));  // a wave per panel
+    wg += cdiv(cdiv(o.d.n, kPanel), (int64_t)GroupShape<1>::NW);  // a wave per panel
     if (wg > (int64_t)1 << 30) return fail(SPAROA_ERR_UNSUPPORTED, "fc group: too many panels");
   }
   g.start[n] = (int)wg;
-  const int mt = (int)cdiv(jobs[0].d.m, 16);
-  const dim3 grid((unsigned)wg), block(64 * waves_for(jobs[0].d.m));
+  const dim3 grid((unsigned)wg), block(64 * GroupShape<1>::NW);
   const bool bf = jobs[0].d.dtype == SPAROA_BF16;
-  switch (mt) {
-#define SPAROA_FCG(MT)                                                                   \
-  case MT:                                                                               \
-    if (bf)                                                                              \
+  switch ((int)cdiv(jobs[0].d.m, 16)) {
+#define SPAROA_FCG(MT)                                                                        \
+  case MT:                                                                                    \
+    if (bf)                                                                                   \
       hipLaunchKernelGGL((fc_bw_measured_group<SPAROA_BF16, MT>), grid, block, 0, stream, g); \
-    else                                                                                 \
+    else                                                                                      \
       hipLaunchKernelGGL((fc_bw_measured_group<SPAROA_F16, MT>), grid, block, 0, stream, g);  \
     break;
     SPAROA_FCG(1)

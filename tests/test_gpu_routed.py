@@ -342,11 +342,11 @@ def test_fc_ops_run_batched_equals_op_by_op():
 
 
 def test_fc_ops_run_grouped_streaming_equals_op_by_op():
-    """Self-measuring streaming FCs run as grouped launches (one per dtype and
-    row-tile count, at most 16 ops each): 22 ops in 5 groups, m from 1 to 64
-    (ragged), bias and residual on some, skip and dense routes -- counts,
-    bitmap, path and output bits equal op-by-op calls; counts equal the
-    oracle's."""
+    """Self-measuring streaming FCs run as grouped launches (one per dtype,
+    at most 16 ops each): 22 ops in 3 launches, m from 1 to 64 (ragged, up to
+    four 16-row tiles), bias and residual on some, skip and dense routes --
+    counts, bitmap, path and output bits equal op-by-op calls; counts equal
+    the oracle's."""
     abi = _abi()
     dev = torch.device("cuda")
     specs = []
