@@ -245,9 +245,14 @@ sparoa_status sparoa_conv2d_zero_skip(const sparoa_conv_desc *desc, const void *
  *   pairs (SKIP_MFMA) or nonzero columns (SKIP_BW).
  * Errors as for sparoa_conv2d; UNSUPPORTED for m > 64 on a BW path.
  * ---------------------------------------------------------------------- */
-/* Packed weights for the BW paths: 16-column panels, k-major inside a panel:
- * packed[p][k][0..15] = w[16p + 0..15][k] (zero past n).  w_packed must hold
- * sparoa_fc_packed_bytes() bytes and must not alias w_nk.  16-bit dtypes. */
+/* Packed weights for the BW paths, 16-column panels in two layouts, one
+ * after the other: the skip layout, k-major inside a panel,
+ * S[p][k][0..15] = w[16p + 0..15][k] (zero past n; the skip path streams
+ * the rows of nonzero input columns), then the dense layout, per 32-k chunk
+ * column-major, D[p][c][j][0..31] = w[16p + j][32c + 0..31] (zero past n and
+ * k; the dense path loads MFMA operands from it as they are).  Each path
+ * reads one layout.  w_packed must hold sparoa_fc_packed_bytes() bytes and
+ * must not alias w_nk.  16-bit dtypes. */
 sparoa_status sparoa_fc_packed_bytes(const sparoa_fc_desc *desc, size_t *bytes);
 sparoa_status sparoa_fc_pack_weights(const sparoa_fc_desc *desc, const void *w_nk,
                                      void *w_packed, hipStream_t stream);

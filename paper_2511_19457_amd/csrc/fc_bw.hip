@@ -3,11 +3,15 @@
 // 2.1).  At m <= 64 an FC has intensity <= ~62 FLOP/byte, far below the
 // MI355X ridge point, so its time is the time to stream the weights once.
 //
-// Weights are packed once (sparoa_fc_pack_weights) into 16-column panels,
-// k-major inside a panel: Wp[p][k][0..15] = w[16p + 0..15][k] (zero past n).
-// A panel is one contiguous stream of k rows of 32 bytes; an input column k
-// that is zero in all m rows owns exactly one such row per panel, so the
-// skip variant drops it from the stream (skip granularity: one column).
+// Weights are packed once (sparoa_fc_pack_weights) into 16-column panels in
+// two layouts.  Skip layout, k-major inside a panel: S[p][k][0..15] =
+// w[16p + 0..15][k] (zero past n): a panel is one contiguous stream of k rows
+// of 32 bytes, and an input column k that is zero in all m rows owns exactly
+// one such row per panel, so the skip variant drops it from the stream (skip
+// granularity: one column).  Dense layout, per 32-k chunk column-major:
+// D[p][c][j][0..31] = w[16p + j][32c + 0..31] (zero past n and k): the 16
+// bytes a lane loads are its MFMA B operand as they are (8 consecutive k of
+// one column), so the dense order needs no transpose through LDS.
 //
 // One work-group streams one panel over all of K (no cross-work-group
 // reduction, no device-scope fences).  Its waves (16 for m <= 32, else 8)
@@ -60,7 +64,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 struct FcBwArgs {
   const char *x;
-  const char *wp;
+  const char *wp;  // skip layout
+  const char *wd;  // dense layout
   const char *bias;
   const char *residual;
   char *y;
@@ -332,9 +337,15 @@ __device__ __forceinline__ void fc_load_chunk(Stage<MT, LIST> &s, __amdgpu_buffe
                                               int count, const unsigned short *list, int c,
                                               bool live, int lane) {
   using raw = typename Elem<DT>::raw;
-  const int k = fc_entry_k<LIST>(list, kb, count, c * kCh + (lane >> 1));
-  s.w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-      wrs, live && k >= 0 ? (k * kPanel + 8 * (lane & 1)) * 2 : kOob, 0, 0));
+  if constexpr (LIST) {  // skip layout (wrs): row k, half lane % 2, transposed later
+    const int k = fc_entry_k<LIST>(list, kb, count, c * kCh + (lane >> 1));
+    s.w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+        wrs, live && k >= 0 ? (k * kPanel + 8 * (lane & 1)) * 2 : kOob, 0, 0));
+  } else {  // dense layout (wrs): the B operand, column lane % 16, k 8 (lane / 16) + 0..7
+    s.w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+        wrs, live && c * kCh < count ? (((kb >> 5) + c) * 16 + (lane & 15)) * 64 + 16 * (lane >> 4)
+                                      : kOob, 0, 0));
+  }
   if constexpr (!LIST) {
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
@@ -380,11 +391,13 @@ template <int DT, int MT, bool LIST>
 __device__ __forceinline__ void fc_mma_chunk(const Stage<MT, LIST> &s, WaveTiles<MT> &T,
                                              f32x4 (&acc)[MT], int lane) {
   using raw = typename Elem<DT>::raw;
-  const int e = lane >> 1, c0 = 8 * (lane & 1);
-  raw h[8];
-  __builtin_memcpy(h, &s.w, 16);
+  if constexpr (LIST) {  // skip layout: weights transposed through the wave's tile
+    const int e = lane >> 1, c0 = 8 * (lane & 1);
+    raw h[8];
+    __builtin_memcpy(h, &s.w, 16);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) *reinterpret_cast<raw *>(&T.wt[(c0 + i) * kRowB + 2 * e]) = h[i];
+    for (int i = 0; i < 8; ++i) *reinterpret_cast<raw *>(&T.wt[(c0 + i) * kRowB + 2 * e]) = h[i];
+  }
   if constexpr (!LIST) {
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
@@ -402,17 +415,19 @@ __device__ __forceinline__ void fc_mma_chunk(const Stage<MT, LIST> &s, WaveTiles
     }
   }
   const int g = lane >> 4, rl = lane & 15;
-  const char *brow = &T.wt[rl * kRowB + 16 * g];
+  u32x4 bq;
+  if constexpr (LIST) bq = *reinterpret_cast<const u32x4 *>(&T.wt[rl * kRowB + 16 * g]);
+  else bq = __builtin_bit_cast(u32x4, s.w);  // dense layout: already the B operand
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    const char *arow = &T.xs[(mt * 16 + rl) * kRowB + 16 * g];
+    const u32x4 aq = *reinterpret_cast<const u32x4 *>(&T.xs[(mt * 16 + rl) * kRowB + 16 * g]);
     if constexpr (DT == SPAROA_BF16)
-      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8 *>(arow),
-                                                        *reinterpret_cast<const bf16x8 *>(brow),
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, aq),
+                                                        __builtin_bit_cast(bf16x8, bq),
                                                         acc[mt], 0, 0, 0);
     else
-      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(*reinterpret_cast<const f16x8 *>(arow),
-                                                       *reinterpret_cast<const f16x8 *>(brow),
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, aq),
+                                                       __builtin_bit_cast(f16x8, bq),
                                                        acc[mt], 0, 0, 0);
   }
 }
@@ -428,9 +443,15 @@ __device__ __forceinline__ void fc_store(const FcBwArgs &a, int64_t row, int64_t
   reinterpret_cast<raw *>(a.y)[row * a.N + col] = E::from_f32(apply_act(o, a.act));
 }
 
+// Panel p's weights in the skip layout (LIST) or the dense layout.
+template <bool LIST>
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t fc_panel_rsrc(const FcBwArgs &a, int64_t p) {
-  return __builtin_amdgcn_make_buffer_rsrc((void *)(a.wp + p * a.K * kPanel * 2), (short)0,
-                                           (int)(a.K * kPanel * 2), kBufDword3);
+  if constexpr (LIST)
+    return __builtin_amdgcn_make_buffer_rsrc((void *)(a.wp + p * a.K * kPanel * 2), (short)0,
+                                             (int)(a.K * kPanel * 2), kBufDword3);
+  const int64_t bytes = (a.K + kCh - 1) / kCh * kPanel * kCh * 2;
+  return __builtin_amdgcn_make_buffer_rsrc((void *)(a.wd + p * bytes), (short)0, (int)bytes,
+                                           kBufDword3);
 }
 
 // ---- single operator: one work-group per panel ----------------------------
@@ -482,7 +503,6 @@ __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_kernel(FcBwArgs a
   const int nch = (count + kCh - 1) / kCh;
   const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.x, (short)0, (int)(a.M * a.K * 2), kBufDword3);
-  const __amdgpu_buffer_rsrc_t wrs = fc_panel_rsrc(a, p);
   const int Mi = (int)a.M, Ki = (int)a.K;
   f32x4 acc[MT];
 #pragma unroll
@@ -492,6 +512,7 @@ __global__ __launch_bounds__(64 * Shape<MT>::waves) void fc_bw_kernel(FcBwArgs a
   auto run = [&](auto list_tag) __attribute__((always_inline)) {
     constexpr bool LIST = decltype(list_tag)::value;
     constexpr int D = LIST ? Shape<MT>::list_depth : kDepth;
+    const __amdgpu_buffer_rsrc_t wrs = fc_panel_rsrc<LIST>(a, p);
     Stage<MT, LIST> st[D];
 #pragma unroll
     for (int j = 0; j < D; ++j) {
@@ -633,7 +654,6 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW) void fc_bw_measured_group(
   const bool pvalid = p < (a.N + kPanel - 1) / kPanel;
   const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
       (void *)a.x, (short)0, (int)(a.M * a.K * 2), kBufDword3);
-  const __amdgpu_buffer_rsrc_t wrs = fc_panel_rsrc(a, pvalid ? p : 0);
   const int Mi = (int)a.M, Ki = (int)a.K, slice = (int)a.slice;
 
   // The walk: every slice in slice order, each as nchu chunks (the most any
@@ -652,6 +672,7 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW) void fc_bw_measured_group(
     constexpr bool LIST = decltype(list_tag)::value;
     using GS = GroupShape<MT, LIST>;
     constexpr int SC = GS::SC, D = GS::D, U = GS::U, XROW = GS::XROW;
+    const __amdgpu_buffer_rsrc_t wrs = fc_panel_rsrc<LIST>(a, pvalid ? p : 0);
     constexpr int NXVEC = GS::NXVEC;  // staged 16-byte x vectors per thread (dense order)
     constexpr int NXV = GS::NXV;      // staged 2-byte x values per thread (skip order)
     static_assert(U % SC == 0 && U % D == 0 && SC >= D, "whole stages and ring cycles");
@@ -717,24 +738,38 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW) void fc_bw_measured_group(
         }
       }
     };
-    // weight ring: chunk i's 32 entries, lane = (entry lane / 2, half lane % 2)
+    // weight ring: chunk i's 32 entries; skip layout: lane = (entry lane / 2,
+    // half lane % 2); dense layout: the B operand (column lane % 16, entries
+    // 8 (lane / 16) + 0..7) of the slice's k chunk
     auto wload = [&](uint4 &w, int i) __attribute__((always_inline)) {
-      const int k = column(i, lane >> 1);
-      w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-          wrs, pvalid && k >= 0 ? (k * kPanel + 8 * (lane & 1)) * 2 : kOob, 0, 0));
+      int off;
+      if constexpr (LIST) {
+        const int k = column(i, lane >> 1);
+        off = pvalid && k >= 0 ? (k * kPanel + 8 * (lane & 1)) * 2 : kOob;
+      } else {
+        const int k = column(i, 0);  // the chunk's first column, -1 past the walk
+        off = pvalid && k >= 0 ? ((k >> 5) * 16 + (lane & 15)) * 64 + 16 * (lane >> 4) : kOob;
+      }
+      w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wrs, off, 0, 0));
     };
     int cc = 0;  // chunks done in the current slice
     auto step = [&](const uint4 &w, int i) __attribute__((always_inline)) {
       // weights transposed into the wave's tile, then MT MFMAs whose A
       // operands come straight from the staged x
-      WeightTile &T = wtiles[wave];
-      const int e = lane >> 1, c0 = 8 * (lane & 1);
-      raw h[8];
-      __builtin_memcpy(h, &w, 16);
-#pragma unroll
-      for (int q = 0; q < 8; ++q) *reinterpret_cast<raw *>(&T.wt[(c0 + q) * kRowB + 2 * e]) = h[q];
       const int g = lane >> 4, rl = lane & 15;
-      const u32x4 bq = *reinterpret_cast<const u32x4 *>(&T.wt[rl * kRowB + 16 * g]);
+      u32x4 bq;
+      if constexpr (LIST) {
+        WeightTile &T = wtiles[wave];
+        const int e = lane >> 1, c0 = 8 * (lane & 1);
+        raw h[8];
+        __builtin_memcpy(h, &w, 16);
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          *reinterpret_cast<raw *>(&T.wt[(c0 + q) * kRowB + 2 * e]) = h[q];
+        bq = *reinterpret_cast<const u32x4 *>(&T.wt[rl * kRowB + 16 * g]);
+      } else {
+        bq = __builtin_bit_cast(u32x4, w);  // dense layout: already the B operand
+      }
       const char *xa = &xst[(i / SC) & 1][rl * XROW + ((i % SC) * kCh + 8 * g) * 2];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
@@ -819,6 +854,24 @@ __global__ void fc_pack_kernel(const raw *__restrict__ w, raw *__restrict__ wp, 
   }
 }
 
+// Packs w[n][k] into the dense layout: vector v = (panel, chunk, column j,
+// group g) holds w[16 panel + j][32 chunk + 8 g + 0..7], zero past n and k.
+__global__ void fc_pack_dense_kernel(const uint16_t *__restrict__ w, uint16_t *__restrict__ wd,
+                                     int64_t K, int64_t N, int64_t chunks, int64_t vecs) {
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < vecs;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t g = v & 3, j = (v >> 2) % kPanel, pc = (v >> 2) / kPanel;
+    const int64_t c = pc % chunks, p = pc / chunks;
+    const int64_t n = p * kPanel + j, k0 = c * kCh + 8 * g;
+    uint16_t t[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) t[i] = n < N && k0 + i < K ? w[n * K + k0 + i] : (uint16_t)0;
+    uint4 out;
+    __builtin_memcpy(&out, t, 16);
+    *reinterpret_cast<uint4 *>(wd + 8 * v) = out;
+  }
+}
+
 template <int DT, int MT, bool SKIP, bool XVEC, bool MEASURE>
 void launch_one(dim3 grid, hipStream_t st, const FcBwArgs &a) {
   hipLaunchKernelGGL((fc_bw_kernel<DT, MT, SKIP, XVEC, MEASURE>), grid,
@@ -858,8 +911,15 @@ bool fc_bw_streams(const sparoa_fc_desc &d) {
   return d.dtype != SPAROA_F32 && d.m <= 64 && slice_for(d) <= kMaxWaveK;
 }
 
-size_t fc_packed_bytes(const sparoa_fc_desc &d) {
+// Skip layout, then the dense layout (k rounded up to whole 32-k chunks).
+size_t fc_skip_layout_bytes(const sparoa_fc_desc &d) {
   return (size_t)cdiv(d.n, kPanel) * kPanel * (size_t)d.k * (size_t)elem_size(d.dtype);
+}
+
+size_t fc_packed_bytes(const sparoa_fc_desc &d) {
+  return fc_skip_layout_bytes(d) +
+         (size_t)cdiv(d.n, kPanel) * kPanel * (size_t)(cdiv(d.k, kCh) * kCh) *
+             (size_t)elem_size(d.dtype);
 }
 
 size_t fc_bw_workspace(const sparoa_fc_desc &, sparoa_path) { return 0; }
@@ -875,6 +935,15 @@ sparoa_status launch_fc_pack(const sparoa_fc_desc &d, const void *w_nk, void *w_
                      static_cast<const uint16_t *>(w_nk), static_cast<uint16_t *>(w_packed), d.k,
                      d.n, panels);
   SPAROA_LAUNCH_CHECK("fc_pack_kernel");
+  const int64_t chunks = cdiv(d.k, kCh);
+  const int64_t vecs = panels * chunks * kPanel * 4;  // 16-byte vectors of the dense layout
+  blocks = std::min<int64_t>(cdiv(vecs, 256), 8192);
+  hipLaunchKernelGGL(fc_pack_dense_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                     static_cast<const uint16_t *>(w_nk),
+                     reinterpret_cast<uint16_t *>(static_cast<char *>(w_packed) +
+                                                  fc_skip_layout_bytes(d)),
+                     d.k, d.n, chunks, vecs);
+  SPAROA_LAUNCH_CHECK("fc_pack_dense_kernel");
   return SPAROA_OK;
 }
 
@@ -888,6 +957,7 @@ sparoa_status launch_fc_bw(const sparoa_fc_desc &d, sparoa_path, const void *x,
   FcBwArgs a;
   a.x = static_cast<const char *>(x);
   a.wp = static_cast<const char *>(w_packed);
+  a.wd = static_cast<const char *>(w_packed) + fc_skip_layout_bytes(d);
   a.bias = static_cast<const char *>(bias);
   a.residual = static_cast<const char *>(residual);
   a.y = static_cast<char *>(y);
@@ -924,6 +994,7 @@ sparoa_status launch_fc_bw_measured(const sparoa_fc_desc &d, const void *x, cons
   FcBwArgs a;
   a.x = static_cast<const char *>(x);
   a.wp = static_cast<const char *>(w_packed);
+  a.wd = static_cast<const char *>(w_packed) + fc_skip_layout_bytes(d);
   a.bias = static_cast<const char *>(bias);
   a.residual = static_cast<const char *>(residual);
   a.y = static_cast<char *>(y);
@@ -962,6 +1033,7 @@ sparoa_status launch_fc_bw_measured_group(const FcBwJob *jobs, int n, hipStream_
     FcBwArgs &a = g.op[j];
     a.x = static_cast<const char *>(o.x);
     a.wp = static_cast<const char *>(o.w_packed);
+    a.wd = static_cast<const char *>(o.w_packed) + fc_skip_layout_bytes(o.d);
     a.bias = static_cast<const char *>(o.bias);
     a.residual = static_cast<const char *>(o.residual);
     a.y = static_cast<char *>(o.y);

@@ -183,8 +183,9 @@ def test_tiling_and_skip_block_queries():
     f = abi.fc_desc(8, 4096, 4096)
     assert abi.sparoa_fc_skip_block(f, abi.PATH_SKIP_BW) == (8, 1)
     assert abi.sparoa_fc_tiling(f, abi.PATH_SKIP_BW) == (8, 1)
-    assert abi.sparoa_fc_packed_bytes(f) == 4096 * 4096 * 2
-    assert abi.sparoa_fc_packed_bytes(abi.fc_desc(1, 100, 65)) == 80 * 100 * 2   # 16-column panels
+    # two layouts of 16-column panels: k-major, then 32-k chunks (k rounded up)
+    assert abi.sparoa_fc_packed_bytes(f) == 2 * 4096 * 4096 * 2
+    assert abi.sparoa_fc_packed_bytes(abi.fc_desc(1, 100, 65)) == 80 * 100 * 2 + 80 * 128 * 2
 
 
 @pytest.mark.skipif(os.path.exists("/dev/kfd"),
