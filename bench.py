@@ -290,7 +290,7 @@ def run_case(abi, c):
     return path
 
 
-def forced_times(abi, torch, cases, paths, rounds=3):
+def forced_times(abi, torch, cases, paths, rounds=5):
     """Duration (us) of every case's whole path (sparoa_fc_measured: measure,
     route, execute) with the route forced onto each path by its thresholds
     (intensity threshold 0 or 1e30 picks the family, sparsity threshold 0 or 2
@@ -298,7 +298,8 @@ def forced_times(abi, torch, cases, paths, rounds=3):
     streaming kernel measures inside its one launch; the GEMM family measures
     in a launch of its own).  Cold weights: one call per case in case order
     (each case streams its own 32 MiB of weights, so the 24 cases overflow the
-    Infinity Cache), a pair of HIP events around each call, best of `rounds`.
+    Infinity Cache), a pair of HIP events around each call, best of `rounds`
+    (five: a single slow sample of one case would move a class's threshold).
     Also records each case's block sparsity at each family's granularity."""
     for c in cases:
         c.forced = {}

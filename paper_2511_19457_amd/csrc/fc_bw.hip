@@ -622,7 +622,7 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW) void fc_bw_measured_group(
   using raw = typename Elem<DT>::raw;
   __shared__ WeightTile wtiles[NW];  // each wave's transposed weight chunk
   __shared__ __attribute__((aligned(16))) char xst[2][MT * 16 * XROWMAX];
-  constexpr int kMaxSlices = Shape<1>::waves;  // K slices of the single-operator kernel
+  constexpr int kMaxSlices = Shape<MT>::waves;  // K slices of the single-operator kernel
   __shared__ unsigned short lists[kMaxSlices][kMaxWaveK];
   __shared__ int slice_count[kMaxSlices];
   __shared__ uint32_t mbits[kMaxColWords];
