@@ -599,12 +599,14 @@ __device__ __forceinline__ T uniform_copy(const T &v) {
 // and the dispatcher rebalances as work-groups of skipped (short) operators
 // finish; chunks per x stage SC >= ring depth D, so that waiting for a
 // stage's x loads (issued SC chunks earlier) leaves the ring in flight.
-// Dense order stages 8 chunks and keeps 8 in flight; skip order, whose
-// gathers take a register per 2-byte value, 4 and 4 for m > 16.
+// Chunks per x stage SC = chunks in flight D: dense order 8 (4 for m > 48,
+// whose staged rows take the room); skip order, whose gathers take a
+// register per 2-byte value, 8, 4 for m > 16, 2 for m > 48 -- so that every
+// form fits two work-groups per CU (128 VGPRs, 80 KB of LDS).
 template <int MT, bool LIST = false>
 struct GroupShape {
   static constexpr int NW = 8;
-  static constexpr int SC = LIST && MT > 1 ? 4 : 8;            // chunks per x stage
+  static constexpr int SC = LIST ? (MT == 1 ? 8 : (MT == 4 ? 2 : 4)) : (MT == 4 ? 4 : 8);
   static constexpr int D = SC;                                 // weight ring depth (chunks)
   static constexpr int U = SC;                                 // steps per loop iteration
   static constexpr int XROW = SC * kCh * 2 + 16;               // LDS bytes per staged x row
@@ -614,8 +616,9 @@ struct GroupShape {
   static constexpr int NXV = (XVAL + 64 * NW - 1) / (64 * NW);    // per thread
 };
 
+// (at least four waves per SIMD: two work-groups per CU)
 template <int DT, int MT>
-__global__ __launch_bounds__(64 * GroupShape<MT>::NW) void fc_bw_measured_group(FcBwGroup grp) {
+__global__ __launch_bounds__(64 * GroupShape<MT>::NW, 4) void fc_bw_measured_group(FcBwGroup grp) {
   constexpr int NW = GroupShape<MT>::NW;
   constexpr int kThreads = 64 * NW;
   constexpr int XROWMAX = GroupShape<MT>::XROW;  // the dense stage is the larger
