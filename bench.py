@@ -107,10 +107,14 @@ def load_traffic(digest, family, alg_per_launch):
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    fam = t.get("families", {}).get(family, {})
-    if t.get("source_digest") != digest or fam.get("alg_bytes_per_launch") != alg_per_launch:
+    if t.get("source_digest") != digest:
         return None
-    return fam.get("bytes_per_launch")
+    # one entry per routing outcome profiled (calibration may route a
+    # borderline class either way from run to run)
+    for fam in t.get("families", {}).get(family, []):
+        if fam.get("alg_bytes_per_launch") == alg_per_launch:
+            return fam.get("bytes_per_launch")
+    return None
 
 
 # ---------------------------------------------------------------------------
@@ -182,11 +186,22 @@ def profile_summary(d, copy_mib):
     pline = _bench_line(os.path.join(d, "pmc_bench_FETCH_SIZE.log"))
     fams = {pline["roofline"]["kernel"]: pline["roofline"]}
     fams.update({r["kernel"]: r for r in pline.get("roofline_other_families", {}).values()})
-    res = dict(workload="FC sweep step (24 operators), thresholds per m: " + thr,
+    res = dict(workload="FC sweep step (24 operators)",
                source_digest=pline["roofline"]["source_digest"],   # sources the counters ran on
                scale_reading="a plain device-to-device copy of known size reads FETCH_SIZE and "
                              "WRITE_SIZE; each counter is scaled by known bytes / measured",
                families={}, commands=[])
+    out_path = os.path.join(ROOT, "profiles", "fc_sweep_traffic.json")
+    try:      # keep the entries of other routing outcomes taken on the same sources
+        with open(out_path) as f:
+            old = json.load(f)
+        if old.get("source_digest") == res["source_digest"]:
+            res["families"] = {k: [e for e in v if e.get("thresholds") != thr]
+                               for k, v in old.get("families", {}).items()
+                               if isinstance(v, list)}
+            res["commands"] = old.get("commands", [])
+    except (OSError, ValueError):
+        pass
     scale = {}
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
         cp = sorted(v for n, v in counters(f"pmc_copy_{c}") if "copyBuffer" in n)[-5:]
@@ -207,16 +222,19 @@ def profile_summary(d, copy_mib):
                 sel = [v for n, v in rows_c if "fc_bw_measured_group<" in n]
                 ops, tot_c = len(sel), sum(sel)
             kib[c] = (tot_c / max(ops, 1), ops)
-        res["families"][name] = dict(
+        res["families"].setdefault(name, []).append(dict(
+            thresholds=thr,
             kernel=kernel, operators=r["operators"], alg_bytes_per_launch=r["alg_bytes_per_launch"],
             bytes_per_launch=int(sum(kib[c][0] * 1024 * scale[c] for c in kib)),
             fetch_kib_per_launch=round(kib["FETCH_SIZE"][0], 3),
             write_kib_per_launch=round(kib["WRITE_SIZE"][0], 3),
-            launches_counted=kib["FETCH_SIZE"][1])
+            launches_counted=kib["FETCH_SIZE"][1]))
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
-        res["commands"].append("THR='" + thr + "' " + PROFILE_COMMANDS["pmc_bench"].format(C=c))
-        res["commands"].append(PROFILE_COMMANDS["pmc_copy"].format(C=c, MIB=copy_mib))
-    with open(os.path.join(ROOT, "profiles", "fc_sweep_traffic.json"), "w") as f:
+        for cmd in ("THR='" + thr + "' " + PROFILE_COMMANDS["pmc_bench"].format(C=c),
+                    PROFILE_COMMANDS["pmc_copy"].format(C=c, MIB=copy_mib)):
+            if cmd not in res["commands"]:
+                res["commands"].append(cmd)
+    with open(out_path, "w") as f:
         json.dump(res, f, indent=1)
     print(json.dumps(res["families"], indent=1))
 
