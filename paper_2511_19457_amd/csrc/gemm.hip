@@ -501,10 +501,10 @@ __global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
 // C_in % 64 == 0.  A K chunk is 64 channels of one tap, so the tap and
 // channel offset of a chunk are work-group-uniform scalars (no per-vector
 // division), and a thread's gathered pixels only move by the tap offset.
-// Work-group = 256 threads = WGM x WGN waves; a wave owns WTM x WTN MFMA
-// 16x16 blocks, which sets the LDS bytes read per MFMA.  Chunks are staged
-// global -> registers -> LDS (row stride 160 B: conflict-free 16-byte reads
-// and writes), double-buffered, one barrier per
+// Work-group = WGM x WGN waves; a wave owns WTM x WTN MFMA 16x16 blocks,
+// which sets the LDS bytes read per MFMA.  Chunks are staged global ->
+// registers -> LDS (swizzled 128-byte rows: conflict-free 16-byte reads and
+// writes), double-buffered, one barrier per
 // 64-wide chunk (two MFMA k-steps).  Gathers are branch-free (out-of-image
 // taps read a valid address and are zeroed) so all of a thread's loads are
 // in flight together.  Tiles are ordered so that each XCD works on a
@@ -516,21 +516,33 @@ constexpr int kBK2 = 64;
 constexpr int kMaxChunks2 = 1024;          // K <= 65536 on the skip path
 
 template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
-__global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
+__global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
+  constexpr int NT = 64 * WGM * WGN;   // threads per work-group
   constexpr int BKC = 32 * KS;         // channels per chunk (KS MFMA k-steps)
-  constexpr int ROW = BKC * 2 + 32;    // LDS row stride, bytes: +32 is free of bank conflicts
-                                       // for the 16-byte writes and MFMA-operand reads on gfx950
+  // LDS rows of 128 bytes with 16-byte vector v of row r stored at slot
+  // v ^ (r & 7): the vectors of one column in any 8 consecutive rows sit in
+  // distinct banks, so the 16-byte writes and MFMA-operand reads are free of
+  // bank conflicts without padding (measured as fast as 160-byte padded rows
+  // and 20 % smaller).
+  constexpr int ROW = BKC * 2;
   constexpr int VPR = BKC / 8;         // 16-byte vectors per chunk row
   using E = Elem<DT>;
   static_assert(E::size == 2, "16-bit types");
-  static_assert(WGM * WGN == 4, "four waves");
+  static_assert(VPR == 8, "swizzle of 8-vector rows");
   constexpr int BM = WGM * 16 * WTM, BN = WGN * 16 * WTN;
-  constexpr int AV = BM * VPR / kThreads;  // 16-byte A vectors per thread per chunk
-  constexpr int BV = BN * VPR / kThreads;
-  constexpr int RPU = kThreads / VPR;       // rows covered by one vector slot u
+  constexpr int AV = BM * VPR / NT;  // 16-byte A vectors per thread per chunk
+  constexpr int BV = BN * VPR / NT;
+  constexpr int RPU = NT / VPR;       // rows covered by one vector slot u
   static_assert(AV >= 1 && BV >= 1, "tile too small");
+  static_assert(RPU % 8 == 0, "a thread's rows agree mod 8");
+  constexpr int CS = BN + 4;  // fp32 row stride of the epilogue's staged tile
+  constexpr int STAGE = 2 * (BM + BN) * ROW;
+  constexpr int SMEM = STAGE > BM * CS * 4 ? STAGE : BM * CS * 4;
 
-  __shared__ __attribute__((aligned(16))) char smem[2][(BM + BN) * ROW];
+  __shared__ __attribute__((aligned(16))) char smem_raw[SMEM];
+  auto stage = [&](int buf) __attribute__((always_inline)) -> char * {
+    return smem_raw + buf * ((BM + BN) * ROW);
+  };
   __shared__ unsigned short list[SKIP ? kMaxChunks2 : 1];
   __shared__ uint32_t nzvec[SKIP ? kMaxVecWords : 1];
   __shared__ int list_len;
@@ -629,9 +641,9 @@ __global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
   if (SKIP && use_list) {
     const int cpg = (int)(a.Cin / 8);  // bitmap blocks per pixel
     const int kv_words = (int)((a.taps * cpg + 31) / 32);
-    for (int i = tid; i < kv_words; i += kThreads) nzvec[i] = 0u;
+    for (int i = tid; i < kv_words; i += NT) nzvec[i] = 0u;
     __syncthreads();
-    for (int64_t p = tid; p < (int64_t)BM * a.taps; p += kThreads) {
+    for (int64_t p = tid; p < (int64_t)BM * a.taps; p += NT) {
       const int r_in = (int)(p / a.taps);
       const int tap = (int)(p - (int64_t)r_in * a.taps);
       const int64_t m = m0 + r_in;
@@ -696,15 +708,17 @@ __global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
     for (int u = 0; u < BV; ++u)
       rb_s[u] = __builtin_amdgcn_raw_buffer_load_b128(wr, b_offb[u], j * (BKC * 2), 0);
   };
+  // every row a thread stores is rr mod 8 (RPU and BM are multiples of 8)
+  const int st_col = 16 * (cg ^ (rr & 7));
   auto store_chunk = [&](int buf, const u32x4 (&ra_s)[AV], const u32x4 (&rb_s)[BV])
                          __attribute__((always_inline)) {
+    char *s = stage(buf);
 #pragma unroll
     for (int u = 0; u < AV; ++u)
-      *reinterpret_cast<u32x4 *>(&smem[buf][(rr + RPU * u) * ROW + cg * 16]) = ra_s[u];
+      *reinterpret_cast<u32x4 *>(s + (rr + RPU * u) * ROW + st_col) = ra_s[u];
 #pragma unroll
     for (int u = 0; u < BV; ++u)
-      *reinterpret_cast<u32x4 *>(&smem[buf][(BM + rr + RPU * u) * ROW + cg * 16]) =
-          rb_s[u];
+      *reinterpret_cast<u32x4 *>(s + (BM + rr + RPU * u) * ROW + st_col) = rb_s[u];
   };
 
   f32x4 acc[WTM][WTN];
@@ -714,18 +728,22 @@ __global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
     for (int j = 0; j < WTN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int g = lane >> 4, rl = lane & 15;
+  // operand rows of a lane are rl mod 16, so their swizzle is rl & 7
+  int ks_col[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) ks_col[ks] = 16 * ((4 * ks + g) ^ (rl & 7));
   auto compute = [&](int buf) __attribute__((always_inline)) {
-    const char *As = &smem[buf][(wm * WTM * 16 + rl) * ROW + 16 * g];
-    const char *Bs = &smem[buf][(BM + wn * WTN * 16 + rl) * ROW + 16 * g];
+    const char *As = stage(buf) + (wm * WTM * 16 + rl) * ROW;
+    const char *Bs = stage(buf) + (BM + wn * WTN * 16 + rl) * ROW;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       u32x4 af[WTM], bfr[WTN];
 #pragma unroll
       for (int tm = 0; tm < WTM; ++tm)
-        af[tm] = *reinterpret_cast<const u32x4 *>(As + tm * 16 * ROW + 64 * ks);
+        af[tm] = *reinterpret_cast<const u32x4 *>(As + tm * 16 * ROW + ks_col[ks]);
 #pragma unroll
       for (int tn = 0; tn < WTN; ++tn)
-        bfr[tn] = *reinterpret_cast<const u32x4 *>(Bs + tn * 16 * ROW + 64 * ks);
+        bfr[tn] = *reinterpret_cast<const u32x4 *>(Bs + tn * 16 * ROW + ks_col[ks]);
 #pragma unroll
       for (int tm = 0; tm < WTM; ++tm)
 #pragma unroll
@@ -794,9 +812,7 @@ __global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
   // finishes 8 consecutive columns of a row: bias and residual as 16-byte
   // loads, one 16-byte store.
   using raw = typename E::raw;
-  constexpr int CS = BN + 4;  // fp32 row stride of the staged tile
-  static_assert(BM * CS * 4 <= (int)sizeof(smem), "staged tile fits the LDS buffers");
-  float *ct = reinterpret_cast<float *>(&smem[0][0]);
+  float *ct = reinterpret_cast<float *>(smem_raw);
   __syncthreads();
 #pragma unroll
   for (int tm = 0; tm < WTM; ++tm)
@@ -809,12 +825,12 @@ __global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
   __syncthreads();
   constexpr int C8 = BN / 8;
   const bool vec_n = a.N % 8 == 0;
-  // Output measurement (host: no split, N % 64 == 0, BN == 64): the 8 lanes
-  // of a tile row hold one bitmap byte (8 channel blocks of 8); every lane
-  // stays in the loop for the ballot.
-  const bool om = BN == 64 && a.om_counts != nullptr;
+  // Output measurement (host: no split, N % 64 == 0, and N % BN == 0 for
+  // wider tiles): each 8 consecutive lanes of a tile row hold one bitmap byte
+  // (8 channel blocks of 8); every lane stays in the loop for the ballot.
+  const bool om = BN % 64 == 0 && a.om_counts != nullptr;
   uint32_t om_zeros = 0, om_nz = 0;
-  for (int q = tid; q < BM * C8; q += kThreads) {
+  for (int q = tid; q < BM * C8; q += NT) {
     const int r = q / C8, c = (q % C8) * 8;
     const int64_t row = m0 + r, col = n0 + c;
     if (om) {
@@ -855,7 +871,7 @@ __global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
       const uint64_t bal = __ballot(nzb != 0u);
       // rows past M still clear their byte when it lies inside the bitmap's
       // last word (bits past the last block are 0)
-      const int64_t byte = row * (a.N / 64) + n0 / 64;
+      const int64_t byte = row * (a.N / 64) + col / 64;
       const int64_t mbytes = 4 * ((a.M * (a.N / 8) + 31) / 32);
       if ((lane & 7) == 0 && (valid || byte < mbytes))
         reinterpret_cast<uint8_t *>(a.om_mask)[byte] = valid ? (uint8_t)(bal >> (lane & ~7)) : 0;
@@ -915,13 +931,13 @@ __global__ __launch_bounds__(kThreads) void igemm_kernel(GemmArgs a) {
 
 template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
 void launch_ig(dim3 grid, hipStream_t st, const GemmArgs &a) {
-  hipLaunchKernelGGL((igemm_kernel<DT, WGM, WGN, WTM, WTN, PF, KS, SKIP>), grid, dim3(kThreads),
-                     0, st, a);
+  hipLaunchKernelGGL((igemm_kernel<DT, WGM, WGN, WTM, WTN, PF, KS, SKIP>), grid,
+                     dim3(64 * WGM * WGN), 0, st, a);
 }
 
 // Tile configurations of the second-generation kernel (BM x BN) and the
 // chunks each keeps in flight in registers.
-enum IgCfg { kIg128x64 = 1, kIg64x64 };
+enum IgCfg { kIg128x64 = 1, kIg64x64, kIg128x128 };
 
 // 64-channel chunks: two MFMA k-steps per barrier (four measured slower:
 // more LDS and registers per work-group for the same latency per step).
@@ -931,6 +947,7 @@ bool dispatch_ig(int cfg, int kchunk, dim3 grid, hipStream_t st, const GemmArgs 
   switch (cfg) {
     case kIg128x64: launch_ig<DT, 2, 2, 4, 2, 4, 2, SKIP>(grid, st, a); return true;
     case kIg64x64: launch_ig<DT, 2, 2, 2, 2, 4, 2, SKIP>(grid, st, a); return true;
+    case kIg128x128: launch_ig<DT, 2, 2, 4, 4, 3, 2, SKIP>(grid, st, a); return true;
   }
   return false;
 }
@@ -1059,7 +1076,12 @@ GemmTileChoice ig_choose(const Shape &s, int64_t c_in) {
   // 128 x 64 (waves of 64 x 32, two work-groups per CU) wherever it fills
   // the chip: it beat 128 x 128 (one work-group per CU) by 10 - 25% on 3x3
   // convs at N = 32 (638 vs 506 TFLOP/s at 256 channels, 56 x 56)
-  if (tiles(128, 64) >= 240) { t.cfg = kIg128x64; t.bm = 128; t.bn = 64; }
+  // 128 x 128 (waves of 64 x 64: half the LDS reads per MFMA, two
+  // work-groups per CU) where it still gives each CU several tiles: 19-23 %
+  // faster on 3x3 convs with 256-512 channels at 56 x 56, N = 32; with fewer
+  // tiles the chip runs part-empty and 128 x 64 wins
+  if (s.N % 128 == 0 && tiles(128, 128) >= 384) { t.cfg = kIg128x128; t.bm = 128; t.bn = 128; }
+  else if (tiles(128, 64) >= 240) { t.cfg = kIg128x64; t.bm = 128; t.bn = 64; }
   else { t.cfg = kIg64x64; t.bm = 64; t.bn = 64; }
   const int64_t tl = tiles(t.bm, t.bn), nchunks = cdiv(s.K, t.kchunk);
   int64_t split = 1;

@@ -38,6 +38,7 @@ CONV_CASES = [
     (1, 128, 14, 14, 128, 3, 1, "bf16"),   # split-K: fused reduction
     (3, 64, 15, 13, 64, 3, 2, "f16"),      # ragged rows, split-K
     (15, 64, 29, 31, 64, 3, 1, "bf16"),    # ragged rows in the last tile, no split
+    (13, 64, 59, 61, 256, 3, 1, "bf16"),   # 128 x 128 tiles, ragged rows, no split
     (2, 64, 16, 16, 96, 1, 1, "bf16"),     # c_out % 64 != 0: standalone pass
     (2, 32, 16, 16, 64, 3, 1, "bf16"),     # c_in % 64 != 0 (first-generation GEMM): standalone
     (2, 64, 16, 16, 64, 3, 1, "f32"),      # fp32: standalone pass
@@ -85,6 +86,7 @@ def test_conv_routed_measured(case):
 FC_CASES = [
     # m, k, n, dtype, intensity threshold (0: MFMA family)
     (256, 768, 3072, "f16", 0.0),     # fused epilogue
+    (2048, 768, 3072, "f16", 0.0),    # fused epilogue, 128 x 128 tiles
     (64, 4096, 4096, "bf16", 0.0),    # split-K: fused reduction
     (100, 512, 256, "bf16", 0.0),     # ragged rows, split-K
     (8, 1024, 512, "bf16", 315.0),    # weight-streaming FC: standalone pass
