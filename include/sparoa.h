@@ -129,19 +129,21 @@ sparoa_status sparoa_measure_sparsity(const void *x_dev, sparoa_dtype dtype, int
                                       int64_t samples, sparoa_counts *counts_dev,
                                       uint32_t *mask_dev, uint64_t *per_sample_dev,
                                       hipStream_t stream);
-/* Same, then copies the counts into *counts_host and waits for the stream.
- * counts_dev is caller-provided device scratch of one sparoa_counts. */
 /* The same measurement (no per-sample counts) into counters the caller has
  * already set to {0, rows*cols, nb, nb} (nb = ceil(rows/block_rows) *
  * ceil(cols/block_cols); a caller resets many counters with one copy): for
  * the block shapes whose bitmap needs no clearing -- 1 row x one 16-byte
- * vector, or whole columns (block_rows >= rows, block_cols == 1) -- the
- * call is then one launch instead of two.  Other block shapes initialise
- * everything as sparoa_measure_sparsity does.  Errors as there. */
+ * vector, 1 row x block_cols >= cols for rows narrower than 16 bytes, or
+ * whole columns (block_rows >= rows, block_cols == 1) -- the call is then
+ * one launch instead of two.  Other block shapes initialise everything as
+ * sparoa_measure_sparsity does.  Errors as there. */
 sparoa_status sparoa_measure_sparsity_preset(const void *x_dev, sparoa_dtype dtype, int64_t rows,
                                              int64_t cols, int64_t block_rows,
                                              int64_t block_cols, sparoa_counts *counts_dev,
                                              uint32_t *mask_dev, hipStream_t stream);
+/* Same as sparoa_measure_sparsity, then copies the counts into *counts_host
+ * and waits for the stream.  counts_dev is caller-provided device scratch of
+ * one sparoa_counts. */
 sparoa_status sparoa_measure_sparsity_sync(const void *x_dev, sparoa_dtype dtype, int64_t rows,
                                            int64_t cols, int64_t block_rows, int64_t block_cols,
                                            int64_t samples, sparoa_counts *counts_dev,

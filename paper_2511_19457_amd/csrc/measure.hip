@@ -261,6 +261,65 @@ __global__ __launch_bounds__(kLanebitThreads) void measure_lanebit(const char *_
   lanebit_pass<ESZ, V>(x, items, words, mask, counts, blockIdx.x, gridDim.x);
 }
 
+// One bitmap bit per row (block = 1 row x block_cols >= cols) for rows
+// narrower than one 16-byte vector, e.g. a 3-channel image in NHWC: a lane
+// owns 8 consecutive rows, i.e. 8 * cols contiguous elements starting at a
+// multiple of 16 bytes (cols * ESZ / 2 vectors), so a wave owns 512 rows =
+// 16 whole bitmap words: no atomics on the bitmap and no clearing.  The one
+// lane whose rows run past the end reads its elements one at a time (the
+// tensor's byte size need not be a multiple of 16).
+template <int ESZ>
+__global__ __launch_bounds__(kLanebitThreads) void measure_rowbit(const char *__restrict__ x,
+                                                                  int64_t rows, int cols,
+                                                                  int64_t words,
+                                                                  uint32_t *__restrict__ mask,
+                                                                  sparoa_counts *counts) {
+  constexpr int EPV = 16 / ESZ;  // elements per 16-byte vector
+  const int lane = threadIdx.x & 63;
+  const int nv = cols * ESZ / 2;  // vectors per 8 rows
+  const int64_t groups = (rows + 7) / 8;
+  const int64_t numel = rows * cols;
+  const int64_t stride = (int64_t)gridDim.x * kLanebitThreads;
+  uint64_t zeros = 0, nonzero = 0;
+  // wave-uniform loop: a wave's 64 groups start at a multiple of 64
+  for (int64_t base = (int64_t)blockIdx.x * kLanebitThreads + (threadIdx.x & ~63);
+       base < groups; base += stride) {
+    const int64_t gi = base + lane;
+    const int64_t e0 = gi * 8 * cols;
+    uint32_t rowbits = 0;
+    if (gi < groups) {
+      int r = 0, k = 0;  // row within the group, column within the row
+      if (e0 + 8 * cols <= numel) {
+        const char *p = x + e0 * ESZ;
+        for (int v = 0; v < nv; ++v) {
+          const uint32_t nzv = nonzero_bits<ESZ, EPV>(p + 16 * v);
+          zeros += (uint64_t)(EPV - __popc(nzv));
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) {
+            rowbits |= ((nzv >> e) & 1u) << r;
+            if (++k == cols) { k = 0; ++r; }
+          }
+        }
+      } else {
+        for (int64_t e = e0; e < numel; ++e) {
+          const uint32_t nz = nonzero_bits<ESZ, 1>(x + e * ESZ);
+          zeros += 1u - nz;
+          rowbits |= nz << r;
+          if (++k == cols) { k = 0; ++r; }
+        }
+      }
+    }
+    nonzero += (uint64_t)__popc(rowbits);
+    // lanes 4q .. 4q + 3 hold the 32 rows of bitmap word base / 4 + q
+    const uint32_t word = rowbits | (__shfl_down(rowbits, 1, 64) << 8) |
+                          (__shfl_down(rowbits, 2, 64) << 16) |
+                          (__shfl_down(rowbits, 3, 64) << 24);
+    const int64_t w = base / 4 + lane / 4;
+    if ((lane & 3) == 0 && w < words) mask[w] = word;
+  }
+  wg_commit<kLanebitThreads>(zeros, nonzero, counts, nullptr);
+}
+
 // Several tensors of one element size in the lanebit layout, one launch:
 // work-groups are dealt to the tensors in proportion to their size.
 struct LanebitGroup {
@@ -542,6 +601,7 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
   // fast paths that own whole bitmap words (no atomics, no clearing)
   const bool lanebit = want_mask && vec && br == 1 && bc == vw && !per_sample;
   const bool strips = want_mask && vec && bc == 1 && !per_sample && br >= rows;
+  const bool rowbit = want_mask && br == 1 && bc >= cols && cols * esz < 16 && !per_sample;
 
   if (lanebit && rows * (cols / vw) <= 4096) {  // one work-group measures it all
     const int64_t items = rows * (cols / vw);
@@ -566,8 +626,8 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
   }
 
   // counters the caller already set and no bitmap to clear: no init launch
-  if (!(preset && (lanebit || strips))) {
-    const int64_t zw = (lanebit || strips) ? 0 : words;   // words to clear
+  if (!(preset && (lanebit || strips || rowbit))) {
+    const int64_t zw = (lanebit || strips || rowbit) ? 0 : words;   // words to clear
     const int64_t work = zw > S ? zw : S;
     const int64_t g = work < 1 ? 1 : (cdiv(work, 256) < 1024 ? cdiv(work, 256) : 1024);
     hipLaunchKernelGGL(measure_init, dim3((unsigned)g), dim3(256), 0, stream, counts,
@@ -587,6 +647,18 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
       hipLaunchKernelGGL((measure_lanebit<4, 4>), dim3((unsigned)gx), dim3(kLanebitThreads), 0,
                          stream, static_cast<const char *>(x), items, words, mask, counts);
     SPAROA_LAUNCH_CHECK("measure_lanebit");
+    return SPAROA_OK;
+  }
+  if (rowbit) {
+    int64_t gx = cdiv(cdiv(rows, 8), (int64_t)kLanebitThreads);
+    if (gx > 256) gx = 256;
+    if (esz == 2)
+      hipLaunchKernelGGL(measure_rowbit<2>, dim3((unsigned)gx), dim3(kLanebitThreads), 0, stream,
+                         static_cast<const char *>(x), rows, (int)cols, words, mask, counts);
+    else
+      hipLaunchKernelGGL(measure_rowbit<4>, dim3((unsigned)gx), dim3(kLanebitThreads), 0, stream,
+                         static_cast<const char *>(x), rows, (int)cols, words, mask, counts);
+    SPAROA_LAUNCH_CHECK("measure_rowbit");
     return SPAROA_OK;
   }
   if (strips) {

@@ -51,6 +51,9 @@ CASES = [
     (37, 1000, 16, 16, 0), (3136, 64, 1, 8, 0), (4 * 49, 256, 1, 8, 4), (100, 24, 1, 8, 4),
     (50, 3, 1, 8, 5), (7, 13, 2, 3, 0), (33, 96, 3, 2, 0), (1000, 40, 7, 4, 0),
     (256, 512, 16, 32, 2), (5, 8, 100, 100, 0), (300, 128, 0, 0, 3),
+    # rows narrower than 16 bytes, one block per row (one bit per row)
+    (1001, 3, 1, 8, 0), (777, 1, 1, 4, 0), (3000, 7, 1, 8, 0), (4099, 3, 1, 3, 0),
+    (2100001, 3, 1, 8, 0),
 ]
 
 
@@ -102,6 +105,7 @@ def test_measure_reuses_buffers_and_reinitialises():
     ((32, 56, 56, 256), "bf16", (1, 8)),       # ResNet-50 stage-2 activation, batch 32
     ((32, 112, 112, 96), "f16", (1, 8)),       # MobileNetV2 largest depthwise input
     ((2048, 3072), "f16", (1, 8)),             # FFN second-FC input
+    ((32, 224, 224, 3), "bf16", (1, 8)),       # ResNet-50 stem input (3 channels)
 ])
 def test_measure_full_size(shape, dt, blk):
     x = synth.relu_normal(shape, dt, seed=synth.seed_for(3, 90))
@@ -117,6 +121,8 @@ def test_measure_full_size(shape, dt, blk):
     (40, 2048, 1, 4, "f32"),          # fp32 vector
     (8, 4096, 8, 1, "bf16"),          # whole-column strips
     (37, 100, 2, 4, "bf16"),          # other blocks: initialises everything itself
+    (1001, 3, 1, 8, "bf16"),          # rows narrower than 16 bytes, one bit per row
+    (1001, 3, 1, 8, "f32"),
 ])
 def test_measure_preset_counters(rows, cols, br, bc, dt):
     """sparoa_measure_sparsity_preset: with counters preset to
@@ -127,9 +133,10 @@ def test_measure_preset_counters(rows, cols, br, bc, dt):
     x = synth.sparse_matrix(rows, cols, 0.7, "block", dt, rows + cols)
     ref = oracle.measure(x, rows, cols, br, bc)
     nb = -(-rows // br) * -(-cols // bc)
-    lanebit_or_strips = (br == 1 and bc * torch.tensor([], dtype=DT[dt]).element_size() == 16) or \
-        (bc == 1 and br >= rows)
-    preset = [0, rows * cols, nb, nb] if lanebit_or_strips else [7, 7, 7, 7]
+    esz = torch.tensor([], dtype=DT[dt]).element_size()
+    owns_words = (br == 1 and bc * esz == 16) or (bc == 1 and br >= rows) or \
+        (br == 1 and bc >= cols and cols * esz < 16)
+    preset = [0, rows * cols, nb, nb] if owns_words else [7, 7, 7, 7]
     for _ in range(2):    # twice: the second call starts from the preset again
         counts = torch.tensor(preset, dtype=torch.int64, device=dev)
         mask = torch.full((abi.sparoa_mask_words(rows, cols, br, bc),), -1, dtype=torch.int32,
