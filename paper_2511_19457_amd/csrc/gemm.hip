@@ -28,6 +28,8 @@
 // are those of the dense variant, and a skipped chunk would only have added
 // exact zeros, the skip output equals the dense output bit for bit (for
 // finite weights).
+#include <atomic>
+
 #include "common.h"
 #include "dtype.h"
 
@@ -515,7 +517,7 @@ __global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
 constexpr int kBK2 = 64;
 constexpr int kMaxChunks2 = 1024;          // K <= 65536 on the skip path
 
-template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
+template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP, bool PT>
 __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   constexpr int NT = 64 * WGM * WGN;   // threads per work-group
   constexpr int BKC = 32 * KS;         // channels per chunk (KS MFMA k-steps)
@@ -553,11 +555,19 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   // XCDs, so XCD i gets the i-th contiguous range of tile ids, and a tile id
   // walks (split, row tile, column tile) with the column tiles innermost: the
   // tiles that gather the same input rows run together in one XCD's L2.
+  // PT: a grid smaller than the tile count (a multiple of 8, so a
+  // work-group's virtual ids keep its XCD) walks the tiles persistently, and
+  // a launch that measures its output commits its counts once per work-group
+  // instead of once per tile (same-address atomics serialise device-wide).
+  // Otherwise the grid has one work-group per tile.
   const int64_t ntm = cdiv_dev(a.M, BM), ntn = cdiv_dev(a.N, BN);
+  const int64_t ntiles = ntm * ntn * a.split;
+  const bool om = BN % 64 == 0 && a.om_counts != nullptr;
+  // one tile; returns its output's zero count and nonzero-block count
+  auto tile_body = [&](const int64_t vid) __attribute__((always_inline)) -> uint2 {
   int64_t tile;
   {
-    const int64_t total = (int64_t)gridDim.x, L = blockIdx.x;
-    const int64_t q = total >> 3, r = total & 7, xcd = L & 7, k = L >> 3;
+    const int64_t q = ntiles >> 3, r = ntiles & 7, xcd = vid & 7, k = vid >> 3;
     tile = xcd < r ? xcd * (q + 1) + k : r * (q + 1) + (xcd - r) * q + k;
   }
   const int64_t zsplit = tile / (ntm * ntn);
@@ -687,9 +697,6 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
     __syncthreads();
     count = list_len;
   }
-  auto chunk_at = [&](int i) __attribute__((always_inline)) -> int {
-    return (SKIP && use_list) ? (int)list[i] : (int)c_begin + i;
-  };
 
   // ---- staging: a ring of PF chunks in registers, two chunks in LDS --------
   u32x4 ra[PF][AV], rb[PF][BV];  // native vectors: no struct copies, stays in VGPRs
@@ -766,6 +773,9 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   // ring stays in registers.
   static_assert(PF >= 2 && PF <= 4, "register ring depth");
   const int n = (int)count;
+  auto chunk_at = [&](int i) __attribute__((always_inline)) -> int {
+    return (SKIP && use_list) ? (int)list[i] : (int)c_begin + i;
+  };
   if (n > 0) {
     // chunk 0 alone first (every work-group starts at once: a deep prologue
     // would queue each one's first chunk behind all the others' prefetch)
@@ -828,7 +838,6 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   // Output measurement (host: no split, N % 64 == 0, and N % BN == 0 for
   // wider tiles): each 8 consecutive lanes of a tile row hold one bitmap byte
   // (8 channel blocks of 8); every lane stays in the loop for the ballot.
-  const bool om = BN % 64 == 0 && a.om_counts != nullptr;
   uint32_t om_zeros = 0, om_nz = 0;
   for (int q = tid; q < BM * C8; q += NT) {
     const int r = q / C8, c = (q % C8) * 8;
@@ -926,12 +935,26 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
       }
     }
   }
-  if (om) om_commit(om_zeros, om_nz, a.om_counts);
+  return make_uint2(om_zeros, om_nz);
+  };
+  if constexpr (PT) {
+    uint32_t om_zeros = 0, om_nz = 0;
+    for (int64_t vid = blockIdx.x; vid < ntiles; vid += gridDim.x) {
+      const uint2 t = tile_body(vid);
+      om_zeros += t.x;
+      om_nz += t.y;
+      __syncthreads();  // the next tile reuses the LDS
+    }
+    if (om) om_commit(om_zeros, om_nz, a.om_counts);
+  } else {
+    const uint2 t = tile_body(blockIdx.x);
+    if (om) om_commit(t.x, t.y, a.om_counts);
+  }
 }
 
-template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
+template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP, bool PT = false>
 void launch_ig(dim3 grid, hipStream_t st, const GemmArgs &a) {
-  hipLaunchKernelGGL((igemm_kernel<DT, WGM, WGN, WTM, WTN, PF, KS, SKIP>), grid,
+  hipLaunchKernelGGL((igemm_kernel<DT, WGM, WGN, WTM, WTN, PF, KS, SKIP, PT>), grid,
                      dim3(64 * WGM * WGN), 0, st, a);
 }
 
@@ -941,9 +964,21 @@ enum IgCfg { kIg128x64 = 1, kIg64x64, kIg128x128 };
 
 // 64-channel chunks: two MFMA k-steps per barrier (four measured slower:
 // more LDS and registers per work-group for the same latency per step).
+// Persistent launches (pt) serve the output-measuring (routed, so skip-form)
+// calls with more tiles than two work-groups per CU; only tiles with 64 rows
+// per work-group column of 128 get there.
 template <int DT, bool SKIP>
-bool dispatch_ig(int cfg, int kchunk, dim3 grid, hipStream_t st, const GemmArgs &a) {
+bool dispatch_ig(int cfg, int kchunk, dim3 grid, hipStream_t st, const GemmArgs &a, bool pt) {
   if (kchunk != kBK2) return false;
+  if (pt) {
+    if constexpr (SKIP) {
+      switch (cfg) {
+        case kIg128x64: launch_ig<DT, 2, 2, 4, 2, 4, 2, SKIP, true>(grid, st, a); return true;
+        case kIg128x128: launch_ig<DT, 2, 2, 4, 4, 2, 2, SKIP, true>(grid, st, a); return true;
+      }
+    }
+    return false;
+  }
   switch (cfg) {
     case kIg128x64: launch_ig<DT, 2, 2, 4, 2, 4, 2, SKIP>(grid, st, a); return true;
     case kIg64x64: launch_ig<DT, 2, 2, 2, 2, 4, 2, SKIP>(grid, st, a); return true;
@@ -1054,6 +1089,19 @@ sparoa_status launch_split_reduce(const SplitReduceJob &job, hipStream_t stream)
 }
 
 namespace {
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static std::atomic<int> cus[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  int v = cus[dev].load(std::memory_order_relaxed);
+  if (v == 0) {
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) v = 0;
+    cus[dev].store(v, std::memory_order_relaxed);
+  }
+  return v;
+}
+
 // The second-generation kernel takes 16-bit convs whose channel count is a
 // multiple of its 64-wide K chunk.
 bool ig_eligible(const sparoa_conv_desc &d) {
@@ -1201,17 +1249,29 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
     SPAROA_LAUNCH_CHECK("set_u64");
   }
   dim3 grid((unsigned)cdiv(s.M, t.bm), (unsigned)cdiv(s.N, t.bn), (unsigned)gz);
-  if (t.cfg) grid = dim3((unsigned)(cdiv(s.M, t.bm) * cdiv(s.N, t.bn) * gz));
+  bool persistent = false;
+  if (t.cfg) {
+    int64_t g = cdiv(s.M, t.bm) * cdiv(s.N, t.bn) * gz;
+    // measuring its output, the kernel walks the tiles with two work-groups
+    // per CU (one count commit per work-group; a multiple of 8 keeps each
+    // work-group's tiles on its XCD)
+    const int64_t slots = 2 * (int64_t)device_cus() / 8 * 8;
+    if (a.om_counts && skip && t.cfg != kIg64x64 && slots >= 8 && g > slots) {
+      g = slots;
+      persistent = true;
+    }
+    grid = dim3((unsigned)g);
+  }
   bool ok = false;
   if (t.cfg) {
     switch (d.dtype) {
       case SPAROA_BF16:
-        ok = skip ? dispatch_ig<SPAROA_BF16, true>(t.cfg, t.kchunk, grid, stream, a)
-                  : dispatch_ig<SPAROA_BF16, false>(t.cfg, t.kchunk, grid, stream, a);
+        ok = skip ? dispatch_ig<SPAROA_BF16, true>(t.cfg, t.kchunk, grid, stream, a, persistent)
+                  : dispatch_ig<SPAROA_BF16, false>(t.cfg, t.kchunk, grid, stream, a, persistent);
         break;
       case SPAROA_F16:
-        ok = skip ? dispatch_ig<SPAROA_F16, true>(t.cfg, t.kchunk, grid, stream, a)
-                  : dispatch_ig<SPAROA_F16, false>(t.cfg, t.kchunk, grid, stream, a);
+        ok = skip ? dispatch_ig<SPAROA_F16, true>(t.cfg, t.kchunk, grid, stream, a, persistent)
+                  : dispatch_ig<SPAROA_F16, false>(t.cfg, t.kchunk, grid, stream, a, persistent);
         break;
       default: break;
     }
