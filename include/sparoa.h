@@ -197,9 +197,14 @@ sparoa_status sparoa_route(const sparoa_counts *counts, const sparoa_intensity *
  *   bias [c_out] (if desc->has_bias), residual (NHWC, output shape) nullable.
  *   executed_blocks_dev (nullable, skip paths): receives the number of
  *   executed (row tile, tap, channel block) triples.
+ *   Workspace: sparoa_conv2d_workspace_size bytes -- the split-K partial
+ *   sums, and for shapes whose GEMM can measure its output (see
+ *   sparoa_conv2d_routed_measured) 2048 more bytes of count-commit words
+ *   after them, which must be zero before the first call that uses them and
+ *   are zero again after every call.  Only the partial sums are required.
  * Errors: INVALID_ARG for bad shapes, null x/w/y, a null mask on a skip path;
  * UNSUPPORTED for grouped non-depthwise convs, unsupported dtype/path;
- * WORKSPACE if ws_bytes is below sparoa_conv2d_workspace_size.
+ * WORKSPACE if ws_bytes is below the partial-sum bytes.
  * ---------------------------------------------------------------------- */
 sparoa_status sparoa_conv2d_workspace_size(const sparoa_conv_desc *desc, sparoa_path path,
                                            size_t *bytes);
@@ -329,7 +334,11 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
  *   Fused into the GEMM epilogue (or its split-K reduction) when the 16-bit
  *   64-channel-chunk implicit GEMM serves the layer and cols % 64 == 0: no
  *   launch of its own and no second read of y; otherwise the standalone
- *   measurement of y runs after the layer (and overwrites y_counts).
+ *   measurement of y runs after the layer (and overwrites y_counts).  The
+ *   fused form commits its counts through the count-commit words of a
+ *   workspace of the queried size (zero on entry, left zero; 8 ticketed
+ *   words per counter instead of one atomic per work-group on y_counts),
+ *   and directly into y_counts with a smaller workspace.
  *   Other arguments as for sparoa_conv2d_routed / sparoa_fc_routed.
  * Errors: theirs, and INVALID_ARG for a null y_counts or y_mask.
  * ---------------------------------------------------------------------- */

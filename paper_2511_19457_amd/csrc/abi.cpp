@@ -325,7 +325,7 @@ sparoa_status sparoa_conv2d(const sparoa_conv_desc *d, sparoa_path path, const v
     return launch_depthwise(*d, x, w, d->has_bias ? bias : nullptr, residual, act, y, stream);
   }
   if (d->groups != 1) return fail(SPAROA_ERR_UNSUPPORTED, "grouped (non-depthwise) conv");
-  if (ws_bytes < gemm_workspace(*d, path))
+  if (ws_bytes < gemm_workspace_required(*d, path))
     return fail(SPAROA_ERR_WORKSPACE, "conv2d: workspace too small");
   return launch_gemm_conv(*d, path, x, w, d->has_bias ? bias : nullptr, residual, act,
                           skip ? mask : nullptr, y, workspace, ws_bytes, executed, stream);
@@ -445,7 +445,7 @@ sparoa_status sparoa_fc(const sparoa_fc_desc *d, sparoa_path path, const void *x
                         skip ? mask : nullptr, y, workspace, ws_bytes, executed, stream);
   }
   const sparoa_conv_desc c = fc_as_conv(*d);
-  if (ws_bytes < gemm_workspace(c, path)) return fail(SPAROA_ERR_WORKSPACE, "fc: workspace too small");
+  if (ws_bytes < gemm_workspace_required(c, path)) return fail(SPAROA_ERR_WORKSPACE, "fc: workspace too small");
   return launch_gemm_conv(c, path, x, w, d->has_bias ? bias : nullptr, residual, act,
                           skip ? mask : nullptr, y, workspace, ws_bytes, executed, stream);
 }
@@ -522,7 +522,7 @@ sparoa_status conv_routed_impl(const sparoa_conv_desc *d, const sparoa_threshold
   }
   if (d->groups != 1) return fail(SPAROA_ERR_UNSUPPORTED, "grouped (non-depthwise) conv");
   const sparoa_path p = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
-  if (ws_bytes < gemm_workspace(*d, p)) return fail(SPAROA_ERR_WORKSPACE, "conv2d_routed: workspace too small");
+  if (ws_bytes < gemm_workspace_required(*d, p)) return fail(SPAROA_ERR_WORKSPACE, "conv2d_routed: workspace too small");
   // without a skip kernel for this shape the dense kernel runs and records a dense path
   const bool can_skip = gemm_skip_supported(*d);
   if (measure_y && gemm_fuses_out_measure(*d, p)) {   // y_counts arrives initialised
@@ -608,7 +608,7 @@ sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *t
   }
   const sparoa_conv_desc c = fc_as_conv(*d);
   const sparoa_path p = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
-  if (ws_bytes < gemm_workspace(c, p)) return fail(SPAROA_ERR_WORKSPACE, "fc_routed: workspace too small");
+  if (ws_bytes < gemm_workspace_required(c, p)) return fail(SPAROA_ERR_WORKSPACE, "fc_routed: workspace too small");
   const bool can_skip = gemm_skip_supported(c);
   if (measure_y && gemm_fuses_out_measure(c, p)) {   // y_counts arrives initialised
     const OutMeasure om{y_counts, y_mask};
@@ -731,7 +731,7 @@ sparoa_status split_impl(const sparoa_conv_desc &c, double sparsity_thr,
   if (is_depthwise(c) || c.groups != 1 || gemm_choose(c, SPAROA_PATH_SKIP_MFMA).cfg == 0)
     return fail(SPAROA_ERR_UNSUPPORTED,
                 "split: needs the 16-bit, C_in % 64 == 0 implicit GEMM (groups 1)");
-  if (ws_bytes < gemm_workspace(c, SPAROA_PATH_SKIP_MFMA))
+  if (ws_bytes < gemm_workspace_required(c, SPAROA_PATH_SKIP_MFMA))
     return fail(SPAROA_ERR_WORKSPACE, "split: workspace too small");
   DeviceRoute r{nullptr, sparsity_thr, SPAROA_ROUTE_ELEMENT, 0, nullptr};
   r.sample_zeros = reinterpret_cast<const unsigned long long *>(sample_zeros);

@@ -109,6 +109,7 @@ struct SplitReduceJob {
   void *y;
   sparoa_counts *om_counts;  // non-null: measure y (see OutMeasure)
   uint32_t *om_mask;
+  unsigned long long *om_words;  // non-null: grouped count commit (gemm_workspace)
 };
 sparoa_status launch_split_reduce(const SplitReduceJob &job, hipStream_t stream);
 // Several reductions of one dtype in one launch (n <= kGroupMax).
@@ -133,6 +134,11 @@ struct GemmTileChoice {
 };
 GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path path);
 bool gemm_skip_supported(const sparoa_conv_desc &d);
+// Workspace bytes a GEMM call needs (split-K partials) ...
+size_t gemm_workspace_required(const sparoa_conv_desc &d, sparoa_path path);
+// ... and the size the workspace queries report: the required bytes plus,
+// for shapes whose epilogue or reduction measures the output, the words of
+// the grouped count commit (zero on entry, left zero by every call).
 size_t gemm_workspace(const sparoa_conv_desc &d, sparoa_path path);
 sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, const void *x,
                                const void *w, const void *bias, const void *residual,

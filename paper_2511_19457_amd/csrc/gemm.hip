@@ -65,6 +65,7 @@ struct GemmArgs {
   DeviceRoute route;
   sparoa_counts *om_counts;  // non-null: the epilogue measures y (OutMeasure)
   uint32_t *om_mask;
+  unsigned long long *om_words;  // grouped count commit words, or null
 };
 
 template <int DT>
@@ -366,9 +367,22 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
       }
 }
 
-// Adds a work-group's zero count and nonzero-block count into counts (one
-// atomic per counter per work-group; zero_blocks starts at nb).
-__device__ __forceinline__ void om_commit(uint32_t zeros, uint32_t nz, sparoa_counts *counts) {
+// Workspace words of the grouped count commit: kOmGroups groups x 2
+// counters, one 128-byte line each.
+constexpr int kOmGroups = 8;
+constexpr size_t kOmWordsBytes = 2 * kOmGroups * 128;
+
+// Adds a work-group's zero count and nonzero-block count into counts
+// (zero_blocks starts at nb).  Same-address atomics serialise device-wide
+// (13-17 ns per work-group measured with one atomic per counter), so with
+// `words` (kOmWordsBytes of workspace, zero on entry) work-group b of nwg is
+// a member of group b % kOmGroups: each member adds (1 << 40) + its count to
+// its group's word with one returning atomic, and the member whose add
+// completes the group adds the group's total to counts and clears the word
+// for the next call.  Without `words`: one atomic per counter per
+// work-group.
+__device__ __forceinline__ void om_commit(uint32_t zeros, uint32_t nz, sparoa_counts *counts,
+                                          unsigned long long *words, int64_t b, int64_t nwg) {
   __shared__ uint32_t part[2][16];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
@@ -387,8 +401,28 @@ __device__ __forceinline__ void om_commit(uint32_t zeros, uint32_t nz, sparoa_co
       z += part[0][i];
       n += part[1][i];
     }
-    if (z) atomicAdd((unsigned long long *)&counts->zeros, z);
-    if (n) atomicAdd((unsigned long long *)&counts->zero_blocks, 0ull - n);
+    if (!words) {
+      if (z) atomicAdd((unsigned long long *)&counts->zeros, z);
+      if (n) atomicAdd((unsigned long long *)&counts->zero_blocks, 0ull - n);
+      return;
+    }
+    constexpr unsigned long long kTicket = 1ull << 40;  // sums < 2^40, members < 2^24
+    const int64_t g = b % kOmGroups;
+    const unsigned long long members =
+        (unsigned long long)(nwg / kOmGroups + (g < nwg % kOmGroups ? 1 : 0));
+    unsigned long long *wz = words + g * 32, *wn = words + g * 32 + 16;
+    const unsigned long long oz = atomicAdd(wz, kTicket + z);
+    const unsigned long long on = atomicAdd(wn, kTicket + n);
+    if ((oz >> 40) == members - 1) {
+      const unsigned long long tz = (oz & (kTicket - 1)) + z;
+      if (tz) atomicAdd((unsigned long long *)&counts->zeros, tz);
+      atomicExch(wz, 0ull);
+    }
+    if ((on >> 40) == members - 1) {
+      const unsigned long long tn = (on & (kTicket - 1)) + n;
+      if (tn) atomicAdd((unsigned long long *)&counts->zero_blocks, 0ull - tn);
+      atomicExch(wn, 0ull);
+    }
   }
 }
 
@@ -408,6 +442,7 @@ struct ReduceGroup {
   char *y[kGroupMax];
   sparoa_counts *om_counts[kGroupMax];  // non-null: measure y (16-bit, N % 8 == 0)
   uint32_t *om_mask[kGroupMax];
+  unsigned long long *om_words[kGroupMax];
 };
 
 template <int DT>
@@ -485,7 +520,7 @@ __global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
         for (int e = 0; e < 8; ++e) y[i + e] = t[e];
       }
     }
-    if (om) om_commit(om_zeros, om_nz, om);
+    if (om) om_commit(om_zeros, om_nz, om, g.om_words[j], b0, nb);
   } else {
     for (int64_t i = b0 * 256 + threadIdx.x; i < total; i += nb * 256) {
       float o = 0.f;
@@ -945,10 +980,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
       om_nz += t.y;
       __syncthreads();  // the next tile reuses the LDS
     }
-    if (om) om_commit(om_zeros, om_nz, a.om_counts);
+    if (om) om_commit(om_zeros, om_nz, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
   } else {
     const uint2 t = tile_body(blockIdx.x);
-    if (om) om_commit(t.x, t.y, a.om_counts);
+    if (om) om_commit(t.x, t.y, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
   }
 }
 
@@ -1064,6 +1099,7 @@ sparoa_status launch_split_reduce_group(const SplitReduceJob *jobs, int n, hipSt
     g.y[j] = static_cast<char *>(r.y);
     g.om_counts[j] = r.om_counts;
     g.om_mask[j] = r.om_mask;
+    g.om_words[j] = r.om_words;
     if (r.om_counts && (elem_size(r.dt) != 2 || r.N % 8 != 0))
       return fail(SPAROA_ERR_UNSUPPORTED, "split reduce: output measurement needs 16-bit, N % 8 == 0");
     wg += blocks;
@@ -1188,11 +1224,22 @@ bool gemm_fuses_out_measure(const sparoa_conv_desc &d, sparoa_path path) {
   return gemm_choose(d, path).cfg != 0 && d.c_out % 64 == 0 && elem_size(d.dtype) == 2;
 }
 
-size_t gemm_workspace(const sparoa_conv_desc &d, sparoa_path path) {
+size_t gemm_workspace_required(const sparoa_conv_desc &d, sparoa_path path) {
   const GemmTileChoice t = gemm_choose(d, path);
   if (t.split_k <= 1) return 0;
   const Shape s = shape_of(d);
   return (size_t)t.split_k * (size_t)s.M * (size_t)s.N * sizeof(float);
+}
+
+namespace {
+size_t om_words_offset(const sparoa_conv_desc &d, sparoa_path path) {
+  return (gemm_workspace_required(d, path) + 255) / 256 * 256;
+}
+}  // namespace
+
+size_t gemm_workspace(const sparoa_conv_desc &d, sparoa_path path) {
+  if (!gemm_fuses_out_measure(d, path)) return gemm_workspace_required(d, path);
+  return om_words_offset(d, path) + kOmWordsBytes;
 }
 
 sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, const void *x,
@@ -1240,6 +1287,12 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   // the epilogue measures y when it writes y; with split-K the reduction does
   a.om_counts = om && gz == 1 ? om->counts : nullptr;
   a.om_mask = om && gz == 1 ? om->mask : nullptr;
+  // grouped count commit when the workspace holds its words
+  unsigned long long *om_words = nullptr;
+  if (om && ws && ws_bytes >= om_words_offset(d, path) + kOmWordsBytes)
+    om_words = reinterpret_cast<unsigned long long *>(static_cast<char *>(ws) +
+                                                      om_words_offset(d, path));
+  a.om_words = gz == 1 ? om_words : nullptr;
   if (gz > 1 && ws_bytes < (size_t)gz * s.M * s.N * sizeof(float))
     return fail(SPAROA_ERR_WORKSPACE, "GEMM split-K workspace too small");
 
@@ -1284,7 +1337,7 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   SPAROA_LAUNCH_CHECK("gemm_kernel");
   const SplitReduceJob job{d.dtype, a.partial, gz > 1 ? (int)gz : 0, s.M, s.N, bias, residual,
                            act, y, om && gz > 1 ? om->counts : nullptr,
-                           om && gz > 1 ? om->mask : nullptr};
+                           om && gz > 1 ? om->mask : nullptr, gz > 1 ? om_words : nullptr};
   if (defer) {
     *defer = job;
     return SPAROA_OK;

@@ -66,6 +66,8 @@ def test_conv_routed_measured(case):
     ws = torch.zeros(max(16, max(abi.sparoa_conv2d_workspace_size(d, q) for q in range(4))),
                      dtype=torch.uint8, device=dev)
     rows, cols = n * ho * wo, cout
+    # the GEMM measures y itself (count-commit words at the workspace's end)
+    fused = dt != "f32" and cin % 64 == 0 and cout % 64 == 0
     for s_thr in (0.0, 2.0):       # skip and dense routes
         y = torch.full((n, ho, wo, cout), float("nan"), dtype=tdt, device=dev)
         y_counts = _fresh_counts(rows, cols, dev)
@@ -82,6 +84,18 @@ def test_conv_routed_measured(case):
         assert int(path.item()) == int(p2.item())
         assert torch.equal(y, y2), f"{case} s_thr {s_thr}"
         _check_y_measurement(abi, y, rows, cols, y_counts, y_mask, f"{case} s_thr {s_thr}")
+        if fused:   # the count-commit words are left zero for the next call
+            assert int(ws[-2048:].count_nonzero().item()) == 0
+    if fused:       # a workspace without the commit words: direct commits, same counts
+        small = ws[:ws.numel() - 2048] if ws.numel() > 2048 else None
+        y = torch.full((n, ho, wo, cout), float("nan"), dtype=tdt, device=dev)
+        y_counts = _fresh_counts(rows, cols, dev)
+        y_mask = torch.full((abi.sparoa_mask_words(rows, cols, 1, 8),), -1, dtype=torch.int32,
+                            device=dev)
+        abi.sparoa_conv2d_routed_measured(d, 0.0, 0.0, abi.ROUTE_BLOCK, counts, x, wt, b, r,
+                                          abi.ACT_RELU, mask, y, y_counts, y_mask, small)
+        torch.cuda.synchronize()
+        _check_y_measurement(abi, y, rows, cols, y_counts, y_mask, f"{case} small workspace")
 
 
 FC_CASES = [
@@ -125,6 +139,14 @@ def test_fc_routed_measured(case):
     torch.cuda.synchronize()
     assert torch.equal(y, y2)
     _check_y_measurement(abi, y, m, n, y_counts, y_mask, str(case))
+    if c_thr == 0.0 and n % 64 == 0:   # fused: commit words left zero; direct commits
+        assert int(ws[-2048:].count_nonzero().item()) == 0
+        small = ws[:ws.numel() - 2048] if ws.numel() > 2048 else None
+        y_counts = _fresh_counts(m, n, dev)
+        abi.sparoa_fc_routed_measured(d, 0.5, c_thr, abi.ROUTE_BLOCK, counts, x, w, wp, None,
+                                      None, abi.ACT_RELU, mask, y, y_counts, y_mask, small)
+        torch.cuda.synchronize()
+        _check_y_measurement(abi, y, m, n, y_counts, y_mask, f"{case} small workspace")
 
 
 def test_measured_calls_reject_missing_outputs():
