@@ -28,8 +28,6 @@
 // are those of the dense variant, and a skipped chunk would only have added
 // exact zeros, the skip output equals the dense output bit for bit (for
 // finite weights).
-#include <atomic>
-
 #include "common.h"
 #include "dtype.h"
 
@@ -552,7 +550,7 @@ __global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
 constexpr int kBK2 = 64;
 constexpr int kMaxChunks2 = 1024;          // K <= 65536 on the skip path
 
-template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP, bool PT>
+template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
 __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   constexpr int NT = 64 * WGM * WGN;   // threads per work-group
   constexpr int BKC = 32 * KS;         // channels per chunk (KS MFMA k-steps)
@@ -590,13 +588,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   // XCDs, so XCD i gets the i-th contiguous range of tile ids, and a tile id
   // walks (split, row tile, column tile) with the column tiles innermost: the
   // tiles that gather the same input rows run together in one XCD's L2.
-  // PT: a grid smaller than the tile count (a multiple of 8, so a
-  // work-group's virtual ids keep its XCD) walks the tiles persistently, and
-  // a launch that measures its output commits its counts once per work-group
-  // instead of once per tile (same-address atomics serialise device-wide).
-  // Otherwise the grid has one work-group per tile.
   const int64_t ntm = cdiv_dev(a.M, BM), ntn = cdiv_dev(a.N, BN);
-  const int64_t ntiles = ntm * ntn * a.split;
+  const int64_t ntiles = ntm * ntn * a.split;   // == gridDim.x
   const bool om = BN % 64 == 0 && a.om_counts != nullptr;
   // one tile; returns its output's zero count and nonzero-block count
   auto tile_body = [&](const int64_t vid) __attribute__((always_inline)) -> uint2 {
@@ -972,24 +965,15 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   }
   return make_uint2(om_zeros, om_nz);
   };
-  if constexpr (PT) {
-    uint32_t om_zeros = 0, om_nz = 0;
-    for (int64_t vid = blockIdx.x; vid < ntiles; vid += gridDim.x) {
-      const uint2 t = tile_body(vid);
-      om_zeros += t.x;
-      om_nz += t.y;
-      __syncthreads();  // the next tile reuses the LDS
-    }
-    if (om) om_commit(om_zeros, om_nz, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
-  } else {
-    const uint2 t = tile_body(blockIdx.x);
-    if (om) om_commit(t.x, t.y, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
-  }
+  // (one tile per work-group; the lambda form measured fewer scalar-register
+  // spills than straight-line code)
+  const uint2 t = tile_body(blockIdx.x);
+  if (om) om_commit(t.x, t.y, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
 }
 
-template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP, bool PT = false>
+template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
 void launch_ig(dim3 grid, hipStream_t st, const GemmArgs &a) {
-  hipLaunchKernelGGL((igemm_kernel<DT, WGM, WGN, WTM, WTN, PF, KS, SKIP, PT>), grid,
+  hipLaunchKernelGGL((igemm_kernel<DT, WGM, WGN, WTM, WTN, PF, KS, SKIP>), grid,
                      dim3(64 * WGM * WGN), 0, st, a);
 }
 
@@ -999,21 +983,9 @@ enum IgCfg { kIg128x64 = 1, kIg64x64, kIg128x128 };
 
 // 64-channel chunks: two MFMA k-steps per barrier (four measured slower:
 // more LDS and registers per work-group for the same latency per step).
-// Persistent launches (pt) serve the output-measuring (routed, so skip-form)
-// calls with more tiles than two work-groups per CU; only tiles with 64 rows
-// per work-group column of 128 get there.
 template <int DT, bool SKIP>
-bool dispatch_ig(int cfg, int kchunk, dim3 grid, hipStream_t st, const GemmArgs &a, bool pt) {
+bool dispatch_ig(int cfg, int kchunk, dim3 grid, hipStream_t st, const GemmArgs &a) {
   if (kchunk != kBK2) return false;
-  if (pt) {
-    if constexpr (SKIP) {
-      switch (cfg) {
-        case kIg128x64: launch_ig<DT, 2, 2, 4, 2, 4, 2, SKIP, true>(grid, st, a); return true;
-        case kIg128x128: launch_ig<DT, 2, 2, 4, 4, 2, 2, SKIP, true>(grid, st, a); return true;
-      }
-    }
-    return false;
-  }
   switch (cfg) {
     case kIg128x64: launch_ig<DT, 2, 2, 4, 2, 4, 2, SKIP>(grid, st, a); return true;
     case kIg64x64: launch_ig<DT, 2, 2, 2, 2, 4, 2, SKIP>(grid, st, a); return true;
@@ -1125,19 +1097,6 @@ sparoa_status launch_split_reduce(const SplitReduceJob &job, hipStream_t stream)
 }
 
 namespace {
-// Compute units of the current device (cached per device).
-int device_cus() {
-  static std::atomic<int> cus[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-  int v = cus[dev].load(std::memory_order_relaxed);
-  if (v == 0) {
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) v = 0;
-    cus[dev].store(v, std::memory_order_relaxed);
-  }
-  return v;
-}
-
 // The second-generation kernel takes 16-bit convs whose channel count is a
 // multiple of its 64-wide K chunk.
 bool ig_eligible(const sparoa_conv_desc &d) {
@@ -1302,29 +1261,17 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
     SPAROA_LAUNCH_CHECK("set_u64");
   }
   dim3 grid((unsigned)cdiv(s.M, t.bm), (unsigned)cdiv(s.N, t.bn), (unsigned)gz);
-  bool persistent = false;
-  if (t.cfg) {
-    int64_t g = cdiv(s.M, t.bm) * cdiv(s.N, t.bn) * gz;
-    // measuring its output, the kernel walks the tiles with two work-groups
-    // per CU (one count commit per work-group; a multiple of 8 keeps each
-    // work-group's tiles on its XCD)
-    const int64_t slots = 2 * (int64_t)device_cus() / 8 * 8;
-    if (a.om_counts && skip && t.cfg != kIg64x64 && slots >= 8 && g > slots) {
-      g = slots;
-      persistent = true;
-    }
-    grid = dim3((unsigned)g);
-  }
+  if (t.cfg) grid = dim3((unsigned)(cdiv(s.M, t.bm) * cdiv(s.N, t.bn) * gz));
   bool ok = false;
   if (t.cfg) {
     switch (d.dtype) {
       case SPAROA_BF16:
-        ok = skip ? dispatch_ig<SPAROA_BF16, true>(t.cfg, t.kchunk, grid, stream, a, persistent)
-                  : dispatch_ig<SPAROA_BF16, false>(t.cfg, t.kchunk, grid, stream, a, persistent);
+        ok = skip ? dispatch_ig<SPAROA_BF16, true>(t.cfg, t.kchunk, grid, stream, a)
+                  : dispatch_ig<SPAROA_BF16, false>(t.cfg, t.kchunk, grid, stream, a);
         break;
       case SPAROA_F16:
-        ok = skip ? dispatch_ig<SPAROA_F16, true>(t.cfg, t.kchunk, grid, stream, a, persistent)
-                  : dispatch_ig<SPAROA_F16, false>(t.cfg, t.kchunk, grid, stream, a, persistent);
+        ok = skip ? dispatch_ig<SPAROA_F16, true>(t.cfg, t.kchunk, grid, stream, a)
+                  : dispatch_ig<SPAROA_F16, false>(t.cfg, t.kchunk, grid, stream, a);
         break;
       default: break;
     }
