@@ -801,8 +801,17 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   // ring stays in registers.
   static_assert(PF >= 2 && PF <= 4, "register ring depth");
   const int n = (int)count;
+  if constexpr (SKIP) {
+    // a dense-routed tile of the skip kernel walks the list too, filled in
+    // dense order: no branch on the route inside the main loop
+    if (!use_list) {
+      for (int i = tid; i < (int)count; i += NT) list[i] = (unsigned short)(c_begin + i);
+      __syncthreads();
+    }
+  }
   auto chunk_at = [&](int i) __attribute__((always_inline)) -> int {
-    return (SKIP && use_list) ? (int)list[i] : (int)c_begin + i;
+    if constexpr (SKIP) return (int)list[i];
+    else return (int)c_begin + i;
   };
   if (n > 0) {
     // chunk 0 alone first (every work-group starts at once: a deep prologue
@@ -823,9 +832,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
     constexpr int sn = ((D) + 1) % PF;                                             \
     const int i = i0 + (D);                                                        \
     if (!(GUARD) || i < n) {                                                       \
+      const int jn = chunk_at(min(i + 1 + PF, n - 1)); /* read before the MFMAs */ \
       compute(i & 1);                                                              \
       if (!(GUARD) || i + 1 < n) store_chunk((i + 1) & 1, ra[sn], rb[sn]); \
-      load_chunk(chunk_at(min(i + 1 + PF, n - 1)), ra[sn], rb[sn]);       \
+      load_chunk(jn, ra[sn], rb[sn]);                                              \
       __syncthreads();                                                             \
     }                                                                              \
   }
