@@ -196,7 +196,10 @@ sparoa_status sparoa_route(const sparoa_counts *counts, const sparoa_intensity *
  *   every input once and skips nothing.
  *   bias [c_out] (if desc->has_bias), residual (NHWC, output shape) nullable.
  *   executed_blocks_dev (nullable, skip paths): receives the number of
- *   executed (row tile, tap, channel block) triples.
+ *   executed (row tile, tap, channel block) triples; for 16-bit inputs of
+ *   at most 4 channels (image stems, served by a direct kernel with tiling
+ *   (16, 32)), the number of issued (16-pixel row block, 32-wide k-step)
+ *   MFMA steps.
  *   Workspace: sparoa_conv2d_workspace_size bytes -- the split-K partial
  *   sums, and for shapes whose GEMM can measure its output (see
  *   sparoa_conv2d_routed_measured) 2048 more bytes of count-commit words

@@ -131,6 +131,7 @@ struct GemmTileChoice {
   int bm, bn;       // output tile rows (pixels) x cols (channels)
   int kchunk;       // K elements per main-loop step == skip granularity (channels)
   int split_k;      // number of K splits (1 = none)
+  bool small_c = false;  // the direct kernel for C_in <= 4 (image stems), cfg 0
 };
 GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path path);
 bool gemm_skip_supported(const sparoa_conv_desc &d);

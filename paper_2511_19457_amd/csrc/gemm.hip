@@ -981,6 +981,244 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   if (om) om_commit(t.x, t.y, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
 }
 
+// ---------------------------------------------------------------------------
+// Direct MFMA conv for inputs with at most 4 channels (image stems: ResNet's
+// 7x7/2 and MobileNetV2's 3x3/2 over RGB), where the implicit GEMM's 8- or
+// 64-channel K chunks would be mostly padding and its gathers scalar.  A
+// work-group computes one output row (all Wo pixels, all C_out <= 64
+// channels).  It stages the kh input rows the row needs, zero-padded on both
+// sides, in LDS as [kh][PW][4] (channels padded to 4 with zeros), so K is
+// laid out as (kernel row r, tap pair j, tap parity, channel): an 8-element
+// block of K is two taps x 4 channels, contiguous and 8-byte aligned in the
+// patch.  K = kh * ceil(kw/2) blocks, four per v_mfma_f32_16x16x32 k-step;
+// a tap past kw (odd kw) and blocks past the last kernel row read zero.  The
+// B operands (weights, zero-padded the same way) stay in registers.  Waves
+// split C_out into 16-channel column blocks and the Wo pixels into 16-pixel
+// row blocks.  Skip form: an MFMA whose A operand is zero in all 64 lanes is
+// not issued (it would add exact zeros), so the skip output equals the dense
+// output bit for bit; executed_blocks counts the issued (row block, k-step)
+// pairs.  The fp32 tile goes through LDS to 16-byte stores with bias,
+// residual and activation.
+constexpr int kScMaxKSteps = 8;
+constexpr int kScMaxRB = 8;            // Wo <= 128
+constexpr int kScPatchBytes = 48 * 1024;  // LDS bound of the eligible shapes
+
+struct SmallCArgs {
+  const char *x, *w, *bias, *residual;
+  char *y;
+  unsigned long long *executed;
+  int N, H, W, C, Ho, Wo, Cout, kh, kw, sh, sw, ph, pw;
+  int PW, PWP, bpr, ksteps, act;   // PWP = PW + 1: patch row pitch in pixels
+  int raw_elems, w_elems;  // LDS elements of the raw rows and the weights (each % 8 == 0)
+  int c_w;                 // weight elements (Cout * kh * kw * C)
+  int region_off;          // LDS byte offset of the weights / raw rows / tile region
+  float inv_bpr, inv_rv, inv_rowe;   // 1 / bpr, 1 / (W*C/8), 1 / (W*C), rounded once
+  int vec;                 // rows and weights are whole 16-byte vectors
+  int mode;  // 0 dense, 1 skip, 2 device route
+  DeviceRoute route;
+};
+
+template <int DT, int KS>
+__global__ __launch_bounds__(256) void conv_small_c_kernel(SmallCArgs a) {
+  using E = Elem<DT>;
+  using raw = typename E::raw;
+  extern __shared__ __attribute__((aligned(16))) char smem[];   // small_c_lds_bytes
+  __shared__ unsigned long long exec_part[4];
+  __shared__ uint4 sink;   // target of the staging stores of out-of-range lanes
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nwn = a.Cout / 16, nwm = 4 / nwn;   // waves over column / row blocks
+  const int wn = wave % nwn, wm = wave / nwn;
+  const int g = lane >> 4, rl = lane & 15;
+  const int img = (int)(blockIdx.x / (unsigned)a.Ho), oh = (int)(blockIdx.x % (unsigned)a.Ho);
+  bool skip = a.mode == 1;
+  if (a.mode == 2) {
+    skip = device_route_skip(a.route);
+    if (a.route.path_out && blockIdx.x == 0 && tid == 0)
+      *a.route.path_out = (skip ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+  }
+  // LDS: patch [kh][PWP][4] | region: weights [Cout*kh*kw*C], raw input rows
+  // [kh][W*C] while the operands are built, then the fp32 output tile
+  raw *patch = reinterpret_cast<raw *>(smem);
+  char *region = smem + a.region_off;
+  raw *wl = reinterpret_cast<raw *>(region);
+  raw *rawx = wl + a.w_elems;
+  float *ct = reinterpret_cast<float *>(region);
+  const raw *x = reinterpret_cast<const raw *>(a.x);
+  const raw *w = reinterpret_cast<const raw *>(a.w);
+  const int rowe = a.W * a.C;
+  const int ih0 = oh * a.sh - a.ph;
+  const int64_t img_base = (int64_t)img * a.H * rowe;
+
+  // ---- weights and the kh input rows -> LDS: loads unconditional (clamped
+  // addresses; rows outside the image are zeroed by the patch below) and
+  // independent, stores unconditional (no branch to sink the loads into)
+  if (a.vec) {
+    const int wv = a.w_elems / 8, rv = rowe / 8, nv = a.kh * rv;
+    for (int v0 = tid; v0 < wv + nv; v0 += 256 * 4) {
+      uint4 q[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int v = min(v0 + 256 * u, wv + nv - 1);
+        int r, cv;
+        divmod_small(max(v - wv, 0), rv, a.inv_rv, r, cv);
+        const int ih = min(max(ih0 + r, 0), a.H - 1);
+        const raw *src = v < wv ? w + (int64_t)v * 8
+                                : x + img_base + (int64_t)ih * rowe + (int64_t)cv * 8;
+        q[u] = *reinterpret_cast<const uint4 *>(src);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int v = v0 + 256 * u;
+        *(v < wv + nv ? reinterpret_cast<uint4 *>(wl + (size_t)v * 8) : &sink) = q[u];
+      }
+    }
+  } else {
+    const int ne = a.kh * rowe;
+    for (int e0 = tid; e0 < a.c_w + ne; e0 += 256 * 8) {
+      raw q[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int e = min(e0 + 256 * u, a.c_w + ne - 1);
+        int r, ce;
+        divmod_small(max(e - a.c_w, 0), rowe, a.inv_rowe, r, ce);
+        const int ih = min(max(ih0 + r, 0), a.H - 1);
+        q[u] = e < a.c_w ? w[e] : x[img_base + (int64_t)ih * rowe + ce];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int e = e0 + 256 * u;
+        raw *dst = e < a.c_w ? wl + e : rawx + (e - a.c_w);
+        *(e < a.c_w + ne ? dst : reinterpret_cast<raw *>(&sink)) = q[u];
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- padded patch patch[r][q][c4] (q = input column + pw; zero outside
+  // the image and for channels >= C; one column past PW keeps every operand
+  // read in range): a thread owns columns, kernel rows inner
+  for (int q = tid; q < a.PWP; q += 256) {
+    const int iw = q - a.pw;
+    const bool col_in = iw >= 0 && iw < a.W;
+    const int iwc = min(max(iw, 0), a.W - 1) * a.C;
+    for (int r = 0; r < a.kh; ++r) {
+      const int ih = ih0 + r;
+      const bool in = col_in && ih >= 0 && ih < a.H;
+      const raw *src = rawx + r * rowe + iwc;
+      raw v[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {    // unconditional reads (clamped), then masked
+        const raw t = src[min(c, a.C - 1)];
+        v[c] = in && c < a.C ? t : (raw)0;
+      }
+      uint2 q2;
+      __builtin_memcpy(&q2, v, 8);
+      *reinterpret_cast<uint2 *>(patch + (size_t)(r * a.PWP + q) * 4) = q2;
+    }
+  }
+  // ---- B operands (registers): lane (column rl, group g) at k-step t holds
+  // K block b = 4t + g = (kernel row b / bpr, tap pair b % bpr); the A side
+  // keeps each block's patch offset and all-ones / zero masks of its taps
+  const int co = wn * 16 + rl;
+  int koff[KS];
+  uint32_t mlo[KS], mhi[KS];
+  u32x4 bop[KS];
+#pragma unroll
+  for (int t = 0; t < KS; ++t) {
+    int r, j;
+    divmod_small(4 * t + g, a.bpr, a.inv_bpr, r, j);
+    const int rc = min(r, a.kh - 1);
+    const bool lo_ok = r < a.kh, hi_ok = lo_ok && 2 * j + 1 < a.kw;
+    mlo[t] = lo_ok ? 0xFFFFFFFFu : 0u;
+    mhi[t] = hi_ok ? 0xFFFFFFFFu : 0u;
+    koff[t] = (rc * a.PWP + 2 * j) * 4;
+    const raw *wr = wl + ((co * a.kh + rc) * a.kw + 2 * j) * a.C;
+    const int s1 = min(2 * j + 1, a.kw - 1) - 2 * j;   // second tap (clamped)
+    raw v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int c = e & 3;
+      const raw wv = wr[(e >> 2) * s1 * a.C + min(c, a.C - 1)];
+      v[e] = (e < 4 ? lo_ok : hi_ok) && c < a.C ? wv : (raw)0;
+    }
+    __builtin_memcpy(&bop[t], v, 16);
+  }
+  __syncthreads();   // patch complete; weights and raw rows dead: the tile may reuse them
+
+  // ---- MFMAs, one 16-pixel row block at a time (this wave's rb = wm, wm +
+  // nwm, ...); each block's fp32 result goes straight to the tile
+  const int RB = (a.Wo + 15) / 16;
+  const int CS = a.Cout + 4;
+  unsigned long long executed = 0;
+  for (int rb = wm; rb < RB; rb += nwm) {
+    const int ow = min(rb * 16 + rl, a.Wo - 1);  // rows past Wo read a valid pixel, unused
+    const int pix = ow * a.sw * 4;
+    u32x4 aops[KS];
+#pragma unroll
+    for (int t = 0; t < KS; ++t) {   // all reads first
+      // two 8-byte reads: a block starts on an 8-byte (not 16-byte) boundary
+      const uint2 lo = *reinterpret_cast<const uint2 *>(patch + koff[t] + pix);
+      const uint2 hi = *reinterpret_cast<const uint2 *>(patch + koff[t] + pix + 4);
+      aops[t] = u32x4{lo.x & mlo[t], lo.y & mlo[t], hi.x & mhi[t], hi.y & mhi[t]};
+    }
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < KS; ++t) {
+      const u32x4 aop = aops[t];
+      if (skip && __ballot((aop[0] | aop[1] | aop[2] | aop[3]) != 0u) == 0ull) continue;  // exact
+      executed += 1;
+      if constexpr (DT == SPAROA_BF16)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, aop),
+                                                      __builtin_bit_cast(bf16x8, bop[t]), acc,
+                                                      0, 0, 0);
+      else
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, aop),
+                                                     __builtin_bit_cast(f16x8, bop[t]), acc,
+                                                     0, 0, 0);
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) ct[(rb * 16 + 4 * g + v) * CS + wn * 16 + rl] = acc[v];
+  }
+  if (a.executed && skip && wn == 0 && lane == 0) exec_part[wm] = executed;
+  __syncthreads();
+
+  // ---- epilogue: 8 channels per thread, 16-byte stores
+  const int C8 = a.Cout / 8, lc8 = C8 == 8 ? 3 : (C8 == 4 ? 2 : 1);   // Cout in {16, 32, 64}
+  const raw *bias = reinterpret_cast<const raw *>(a.bias);
+  const int64_t row0 = (int64_t)blockIdx.x * a.Wo;
+  for (int q = tid; q < a.Wo * C8; q += 256) {
+    const int ow = q >> lc8, c = (q & (C8 - 1)) * 8;
+    const int64_t orow = row0 + ow;
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = ct[ow * CS + c + e];
+    raw t8[8];
+    if (bias) {
+      const uint4 q4 = *reinterpret_cast<const uint4 *>(bias + c);
+      __builtin_memcpy(t8, &q4, 16);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] += E::to_f32(t8[e]);
+    }
+    if (a.residual) {
+      const uint4 q4 = *reinterpret_cast<const uint4 *>(
+          reinterpret_cast<const raw *>(a.residual) + orow * a.Cout + c);
+      __builtin_memcpy(t8, &q4, 16);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] += E::to_f32(t8[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t8[e] = E::from_f32(apply_act(o[e], a.act));
+    uint4 q4;
+    __builtin_memcpy(&q4, t8, 16);
+    *reinterpret_cast<uint4 *>(reinterpret_cast<raw *>(a.y) + orow * a.Cout + c) = q4;
+  }
+  if (a.executed && skip && tid == 0) {
+    unsigned long long tot = 0;
+    for (int i = 0; i < nwm; ++i) tot += exec_part[i];
+    if (tot) atomicAdd(a.executed, tot);
+  }
+}
+
 template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
 void launch_ig(dim3 grid, hipStream_t st, const GemmArgs &a) {
   hipLaunchKernelGGL((igemm_kernel<DT, WGM, WGN, WTM, WTN, PF, KS, SKIP>), grid,
@@ -1107,6 +1345,87 @@ sparoa_status launch_split_reduce(const SplitReduceJob &job, hipStream_t stream)
 }
 
 namespace {
+// LDS of the direct small-channel kernel: raw input rows, weights (each
+// rounded up to whole 16-byte vectors) and the padded patch.
+int64_t small_c_raw_elems(const sparoa_conv_desc &d) { return cdiv(d.kh * d.w * d.c_in, 8) * 8; }
+int64_t small_c_w_elems(const sparoa_conv_desc &d) {
+  return cdiv(d.c_out * d.kh * d.kw * d.c_in, 8) * 8;
+}
+// LDS layout: patch [kh][PW + 1][4] | region: weights and raw rows, later the
+// fp32 output tile [16 * ceil(Wo / 16)][Cout + 4]
+int64_t small_c_region_off(const sparoa_conv_desc &d) {
+  const Shape s = shape_of(d);
+  return cdiv(d.kh * (d.sw * (s.wo - 1) + d.kw + 1) * 8, 16) * 16;
+}
+int64_t small_c_lds_bytes(const sparoa_conv_desc &d) {
+  const Shape s = shape_of(d);
+  const int64_t staged = 2 * (small_c_raw_elems(d) + small_c_w_elems(d));
+  const int64_t tile = 16 * cdiv(s.wo, 16) * (d.c_out + 4) * 4;
+  return small_c_region_off(d) + (staged > tile ? staged : tile);
+}
+
+// Shapes the direct small-channel kernel serves (image stems).
+bool small_c_eligible(const sparoa_conv_desc &d) {
+  if (d.dtype == SPAROA_F32 || d.groups != 1 || d.dh != 1 || d.dw != 1) return false;
+  if (d.c_in > 4 || d.kw > 8 || d.kh > 32) return false;
+  if (!(d.c_out == 16 || d.c_out == 32 || d.c_out == 64)) return false;
+  const Shape s = shape_of(d);
+  if (s.wo > 16 * kScMaxRB || d.n * s.ho >= ((int64_t)1 << 31)) return false;
+  if (cdiv(d.kh * ((d.kw + 1) / 2), 4) > kScMaxKSteps) return false;
+  return small_c_lds_bytes(d) <= kScPatchBytes;
+}
+
+sparoa_status launch_small_c(const sparoa_conv_desc &d, const void *x, const void *w,
+                             const void *bias, const void *residual, sparoa_act act, void *y,
+                             bool skip, uint64_t *executed, hipStream_t stream,
+                             const DeviceRoute *route) {
+  const Shape s = shape_of(d);
+  SmallCArgs a;
+  a.x = static_cast<const char *>(x);
+  a.w = static_cast<const char *>(w);
+  a.bias = static_cast<const char *>(bias);
+  a.residual = static_cast<const char *>(residual);
+  a.y = static_cast<char *>(y);
+  a.executed = reinterpret_cast<unsigned long long *>(skip ? executed : nullptr);
+  a.N = (int)d.n; a.H = (int)d.h; a.W = (int)d.w; a.C = (int)d.c_in;
+  a.Ho = (int)s.ho; a.Wo = (int)s.wo; a.Cout = (int)d.c_out;
+  a.kh = (int)d.kh; a.kw = (int)d.kw; a.sh = (int)d.sh; a.sw = (int)d.sw;
+  a.ph = (int)d.ph; a.pw = (int)d.pw;
+  a.PW = (int)(d.sw * (s.wo - 1) + d.kw);
+  a.PWP = a.PW + 1;
+  a.bpr = (int)((d.kw + 1) / 2);
+  a.ksteps = (int)cdiv(d.kh * a.bpr, 4);
+  a.raw_elems = (int)small_c_raw_elems(d);
+  a.w_elems = (int)small_c_w_elems(d);
+  a.c_w = (int)(d.c_out * d.kh * d.kw * d.c_in);
+  // whole vectors: each input row and the weight tensor a multiple of 8 elements
+  a.vec = (d.w * d.c_in) % 8 == 0 && (d.c_out * d.kh * d.kw * d.c_in) % 8 == 0;
+  a.inv_bpr = 1.0f / (float)a.bpr;
+  a.inv_rv = a.vec ? 1.0f / (float)(d.w * d.c_in / 8) : 0.0f;
+  a.inv_rowe = 1.0f / (float)(d.w * d.c_in);
+  a.region_off = (int)small_c_region_off(d);
+  a.act = act;
+  a.mode = route && route->counts ? 2 : (skip ? 1 : 0);
+  a.route = route ? *route : DeviceRoute{nullptr, 0.0, 0, 0, nullptr};
+  const dim3 grid((unsigned)(d.n * s.ho));
+  const unsigned lds = (unsigned)small_c_lds_bytes(d);   // <= kScPatchBytes (eligibility)
+  switch (a.ksteps) {
+#define SPAROA_SC(K)                                                                         \
+  case K:                                                                                  \
+    if (d.dtype == SPAROA_BF16)                                                            \
+      hipLaunchKernelGGL((conv_small_c_kernel<SPAROA_BF16, K>), grid, dim3(256), lds, stream, a); \
+    else                                                                                   \
+      hipLaunchKernelGGL((conv_small_c_kernel<SPAROA_F16, K>), grid, dim3(256), lds, stream, a);  \
+    break;
+    SPAROA_SC(1) SPAROA_SC(2) SPAROA_SC(3) SPAROA_SC(4)
+    SPAROA_SC(5) SPAROA_SC(6) SPAROA_SC(7) SPAROA_SC(8)
+#undef SPAROA_SC
+    default: return fail(SPAROA_ERR_UNSUPPORTED, "small-channel conv: k-steps");
+  }
+  SPAROA_LAUNCH_CHECK("conv_small_c_kernel");
+  return SPAROA_OK;
+}
+
 // The second-generation kernel takes 16-bit convs whose channel count is a
 // multiple of its 64-wide K chunk.
 bool ig_eligible(const sparoa_conv_desc &d) {
@@ -1153,7 +1472,7 @@ GemmTileChoice ig_choose(const Shape &s, int64_t c_in) {
 
 bool gemm_skip_supported(const sparoa_conv_desc &d) {
   const Shape s = shape_of(d);
-  if (ig_eligible(d)) return true;
+  if (ig_eligible(d) || small_c_eligible(d)) return true;
   const int64_t bits = d.kh * d.kw * cdiv(d.c_in, 8);
   return cdiv(s.K, kBK) <= kMaxChunks && bits <= (int64_t)kMaxVecWords * 32;
 }
@@ -1163,6 +1482,15 @@ GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path) {
   const Shape s = shape_of(d);
   if (ig_eligible(d)) return ig_choose(s, d.c_in);
   GemmTileChoice t;
+  if (small_c_eligible(d)) {   // one output row per work-group, 16-pixel row blocks
+    t.cfg = 0;
+    t.bm = 16;
+    t.bn = 16;
+    t.kchunk = 32;
+    t.split_k = 1;
+    t.small_c = true;
+    return t;
+  }
   t.cfg = 0;
   t.kchunk = kBK;
   if (d.dtype == SPAROA_F32) {
@@ -1269,6 +1597,11 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
     hipLaunchKernelGGL(set_u64, dim3(1), dim3(1), 0, stream,
                        reinterpret_cast<unsigned long long *>(executed), 0ull);
     SPAROA_LAUNCH_CHECK("set_u64");
+  }
+  if (t.small_c) {
+    if (defer) *defer = SplitReduceJob{d.dtype, nullptr, 0, s.M, s.N, bias, residual, act, y,
+                                       nullptr, nullptr, nullptr};
+    return launch_small_c(d, x, w, bias, residual, act, y, skip, executed, stream, route);
   }
   dim3 grid((unsigned)cdiv(s.M, t.bm), (unsigned)cdiv(s.N, t.bn), (unsigned)gz);
   if (t.cfg) grid = dim3((unsigned)(cdiv(s.M, t.bm) * cdiv(s.N, t.bn) * gz));

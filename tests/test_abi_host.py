@@ -180,6 +180,9 @@ def test_tiling_and_skip_block_queries():
     assert tr in (64, 128) and kc == 32               # general kernel: 32-wide chunks
     d32 = abi.conv_desc(1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, dtype=abi.F32)
     assert abi.sparoa_conv2d_tiling(d32, abi.PATH_DENSE_MFMA)[1] == 32
+    stem = abi.conv_desc(32, 3, 224, 224, 64, 7, 7, 2, 2, 3, 3)   # direct small-channel kernel
+    assert abi.sparoa_conv2d_tiling(stem, abi.PATH_SKIP_MFMA) == (16, 32)
+    assert abi.sparoa_conv2d_workspace_size(stem, abi.PATH_DENSE_MFMA) == 0
     f = abi.fc_desc(8, 4096, 4096)
     assert abi.sparoa_fc_skip_block(f, abi.PATH_SKIP_BW) == (8, 1)
     assert abi.sparoa_fc_tiling(f, abi.PATH_SKIP_BW) == (8, 1)

@@ -147,6 +147,64 @@ def test_depthwise_grid_stride_loop(stride):
         assert_close(y[sel], yr, ar, RTOL[torch.bfloat16], f"depthwise loop s{stride} {sel}")
 
 
+# Inputs of at most 4 channels (image stems) run the direct small-channel kernel.
+SMALL_C_SHAPES = [
+    (2, 3, 64, 64, 64, 7, 7, 2, 2, 3, 3, 1, 1, 1),     # ResNet stem, Wo 32
+    (2, 3, 50, 50, 32, 3, 3, 2, 2, 1, 1, 1, 1, 1),     # MobileNetV2 stem, ragged row block
+    (1, 1, 20, 37, 16, 4, 4, 1, 1, 1, 2, 1, 1, 1),     # one channel, even kw, stride 1
+    (1, 4, 9, 256, 64, 5, 5, 2, 2, 2, 2, 1, 1, 1),     # four channels, Wo 128 (8 row blocks)
+]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+@pytest.mark.parametrize("shape", SMALL_C_SHAPES)
+def test_small_c_conv_vs_oracle_and_skip(dt, shape):
+    """Dense output against the oracle (bias, residual, ReLU); the skip path
+    equal to the dense path bit for bit on an input whose top half is zero
+    (some k-steps skipped), and executing nothing on an all-zero input."""
+    abi = _abi()
+    n, cin, h, wd, cout, kh, kw, sh, sw, ph, pw, dh, dw, g = shape
+    d = abi.conv_desc(*shape, DT[dt])
+    assert abi.sparoa_conv2d_tiling(d, 1) == (16, 32)
+    ho = (h + 2 * ph - kh) // sh + 1
+    wo = (wd + 2 * pw - kw) // sw + 1
+    seed = 1500 + SMALL_C_SHAPES.index(shape)
+    x = synth.relu_normal((n, h, wd, cin), dt, seed)
+    x[:, : h // 2] = 0
+    w = synth.he_normal((cout, kh, kw, cin), kh * kw * cin, dt, seed + 1)
+    b = synth.normal((cout,), dt, seed + 2)
+    r = synth.normal((n, ho, wo, cout), dt, seed + 3)
+    yd, _, _ = run_conv(x, w, shape, 0, bias=b, residual=r, act=1)
+    ys, ex, _ = run_conv(x, w, shape, 1, bias=b, residual=r, act=1)
+    assert torch.equal(yd, ys)
+    total = n * ho * -(-wo // 16) * -(-(kh * -(-kw // 2)) // 4)   # (row block, k-step) pairs
+    assert 0 < ex < total
+    yr, ar = oracle_conv(x, w, shape, bias=b, residual=r, act=1)
+    assert_close(yd, yr, ar, RTOL[DT[dt]], f"small-c conv {shape} {dt}")
+    z = torch.zeros_like(x)
+    yz, exz, _ = run_conv(z, w, shape, 1, bias=b, act=1)
+    yzd, _, _ = run_conv(z, w, shape, 0, bias=b, act=1)
+    assert exz == 0 and torch.equal(yz, yzd)
+
+
+def test_resnet50_stem_full_size():
+    """The ResNet-50 stem at batch 32 (224 x 224 x 3 -> 112 x 112 x 64, 7x7/2),
+    bf16: sampled outputs against the oracle, skip path equal to dense."""
+    shape = (32, 3, 224, 224, 64, 7, 7, 2, 2, 3, 3, 1, 1, 1)
+    x = synth.normal((32, 224, 224, 3), "bf16", synth.seed_for(3, 1))
+    w = synth.he_normal((64, 7, 7, 3), 147, "bf16", synth.seed_for(3, 2))
+    yd, _, _ = run_conv(x, w, shape, 0, act=1)
+    ys, _, _ = run_conv(x, w, shape, 1, act=1)
+    assert torch.equal(yd, ys)
+    total = yd.numel()
+    rng = np.random.default_rng(77)
+    idx = np.unique(np.concatenate([rng.integers(0, total, size=4096), [0, total - 1]]))
+    yr, ar = oracle.conv2d_at(x, w, idx, *shape, act=1)
+    yg = yd.reshape(-1)[idx].float().numpy().astype(np.float64)
+    bound = RTOL[torch.bfloat16] * ar + SUBNORMAL_STEP[torch.bfloat16]
+    assert np.all(np.abs(yg - yr) <= bound), float(np.max(np.abs(yg - yr) - bound))
+
+
 def test_config1_full():
     """Single 3x3 conv 64 -> 64 at 56 x 56, fp32, ReLU(N(0,1)) input."""
     shape = (1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, 1, 1, 1)

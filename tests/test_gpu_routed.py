@@ -71,7 +71,8 @@ def test_fc_routed_matches_host_route_and_fixed_path(case, thr_kind):
 
 
 CONV_CASES = [(2, 64, 14, 14, 64, 3, 3, 1, 1, 1, 1, 1), (1, 32, 20, 20, 192, 1, 1, 1, 1, 0, 0, 1),
-              (2, 96, 12, 12, 96, 3, 3, 2, 2, 1, 1, 96)]
+              (2, 96, 12, 12, 96, 3, 3, 2, 2, 1, 1, 96),
+              (2, 3, 30, 30, 64, 7, 7, 2, 2, 3, 3, 1)]    # 3-channel stem (direct kernel)
 
 
 @pytest.mark.parametrize("case", CONV_CASES)
