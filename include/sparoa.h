@@ -337,7 +337,8 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
  *   Fused into the GEMM epilogue (or its split-K reduction) when the 16-bit
  *   64-channel-chunk implicit GEMM serves the layer and cols % 64 == 0: no
  *   launch of its own and no second read of y; otherwise the standalone
- *   measurement of y runs after the layer (and overwrites y_counts).  The
+ *   measurement of y runs after the layer (as sparoa_measure_sparsity_preset:
+ *   one launch for the block shapes whose bitmap needs no clearing).  The
  *   fused form commits its counts through the count-commit words of a
  *   workspace of the queried size (zero on entry, left zero; 8 ticketed
  *   words per counter instead of one atomic per work-group on y_counts),

@@ -510,8 +510,10 @@ sparoa_status conv_routed_impl(const sparoa_conv_desc *d, const sparoa_threshold
   if ((st = check_conv(d, &ho, &wo)) != SPAROA_OK) return st;
   const int64_t rows = d->n * ho * wo, cols = d->c_out;
   auto measure_after = [&]() {
+    // y_counts arrive preset ({0, numel, nb, nb}): no init launch where the
+    // bitmap needs no clearing
     return measure_y ? launch_measure(y, d->dtype, rows, cols, 1, 8, 0, y_counts, y_mask, nullptr,
-                                      stream)
+                                      stream, true)
                      : SPAROA_OK;
   };
   if (dw) {
@@ -596,7 +598,7 @@ sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *t
     return fail(SPAROA_ERR_INVALID_ARG, "fc_routed_measured: null y_counts or y_mask");
   auto measure_after = [&]() {
     return measure_y ? launch_measure(y, d->dtype, d->m, d->n, 1, 8, 0, y_counts, y_mask, nullptr,
-                                      stream)
+                                      stream, true)   // y_counts arrive preset
                      : SPAROA_OK;
   };
   const DeviceRoute r{counts_dev, thr->sparsity_thr, thr->mode, bw, path_dev};
