@@ -816,12 +816,14 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   if (n > 0) {
     // chunk 0 alone first (every work-group starts at once: a deep prologue
     // would queue each one's first chunk behind all the others' prefetch)
+    // (chunks past the last are not loaded: short K -- a 1x1 conv over 64
+    // channels is one chunk -- would otherwise re-read its chunks PF times)
     load_chunk(chunk_at(0), ra[0], rb[0]);
     store_chunk(0, ra[0], rb[0]);
-    load_chunk(chunk_at(min(1, n - 1)), ra[1], rb[1]);
-    if constexpr (PF > 2) load_chunk(chunk_at(min(2, n - 1)), ra[PF > 2 ? 2 : 0], rb[PF > 2 ? 2 : 0]);
-    if constexpr (PF > 3) load_chunk(chunk_at(min(3, n - 1)), ra[PF > 3 ? 3 : 0], rb[PF > 3 ? 3 : 0]);
-    load_chunk(chunk_at(min(PF, n - 1)), ra[0], rb[0]);
+    if (1 < n) load_chunk(chunk_at(1), ra[1], rb[1]);
+    if constexpr (PF > 2) if (2 < n) load_chunk(chunk_at(2), ra[PF > 2 ? 2 : 0], rb[PF > 2 ? 2 : 0]);
+    if constexpr (PF > 3) if (3 < n) load_chunk(chunk_at(3), ra[PF > 3 ? 3 : 0], rb[PF > 3 ? 3 : 0]);
+    if (PF < n) load_chunk(chunk_at(PF), ra[0], rb[0]);
     __syncthreads();
   // Steady state: groups of PF straight-line steps (no branch inside a step,
   // so the compiler's load counters stay exact and PF chunks stay in flight);
@@ -835,7 +837,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
       const int jn = chunk_at(min(i + 1 + PF, n - 1)); /* read before the MFMAs */ \
       compute(i & 1);                                                              \
       if (!(GUARD) || i + 1 < n) store_chunk((i + 1) & 1, ra[sn], rb[sn]); \
-      load_chunk(jn, ra[sn], rb[sn]);                                              \
+      if (!(GUARD) || i + 1 + PF < n) load_chunk(jn, ra[sn], rb[sn]);            \
       __syncthreads();                                                             \
     }                                                                              \
   }
