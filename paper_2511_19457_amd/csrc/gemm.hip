@@ -581,6 +581,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   __shared__ unsigned short list[SKIP ? kMaxChunks2 : 1];
   __shared__ uint32_t nzvec[SKIP ? kMaxVecWords : 1];
   __shared__ int list_len;
+  __shared__ uint8_t ombytes[BM * (BN / 64 > 0 ? BN / 64 : 1)];   // output bitmap bytes of the tile
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
@@ -918,12 +919,9 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
       }
       om_nz += nzb;
       const uint64_t bal = __ballot(nzb != 0u);
-      // rows past M still clear their byte when it lies inside the bitmap's
-      // last word (bits past the last block are 0)
-      const int64_t byte = row * (a.N / 64) + col / 64;
-      const int64_t mbytes = 4 * ((a.M * (a.N / 8) + 31) / 32);
-      if ((lane & 7) == 0 && (valid || byte < mbytes))
-        reinterpret_cast<uint8_t *>(a.om_mask)[byte] = valid ? (uint8_t)(bal >> (lane & ~7)) : 0;
+      // the tile's bitmap bytes (8 channel blocks of 8 per byte) meet in LDS
+      // and each row's BN / 64 bytes leave as one store below
+      if ((lane & 7) == 0) ombytes[r * (BN / 64) + c / 64] = valid ? (uint8_t)(bal >> (lane & ~7)) : 0;
       continue;
     }
     if (row >= a.M || col >= a.N) continue;
@@ -972,6 +970,22 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
         if (a.bias) v += E::to_f32(reinterpret_cast<const raw *>(a.bias)[col + e]);
         if (a.residual) v += E::to_f32(reinterpret_cast<const raw *>(a.residual)[row * a.N + col + e]);
         dst[e] = E::from_f32(apply_act(v, a.act));
+      }
+    }
+  }
+  if (om) {
+    __syncthreads();
+    // rows past M still clear their bytes when they lie inside the bitmap's
+    // last word (bits past the last block are 0)
+    const int64_t mbytes = 4 * ((a.M * (a.N / 8) + 31) / 32);
+    for (int r = tid; r < BM; r += NT) {
+      const int64_t row = m0 + r, byte = row * (a.N / 64) + n0 / 64;
+      if (byte >= mbytes) continue;   // (BN / 64 bytes of a row lie in one word)
+      if constexpr (BN == 128) {      // n0 / 64 and N / 64 even: 2-byte aligned
+        const uint16_t v = (uint16_t)(ombytes[2 * r] | (ombytes[2 * r + 1] << 8));
+        *reinterpret_cast<uint16_t *>(reinterpret_cast<uint8_t *>(a.om_mask) + byte) = v;
+      } else {
+        reinterpret_cast<uint8_t *>(a.om_mask)[byte] = ombytes[r];
       }
     }
   }
