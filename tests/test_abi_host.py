@@ -183,6 +183,15 @@ def test_tiling_and_skip_block_queries():
     stem = abi.conv_desc(32, 3, 224, 224, 64, 7, 7, 2, 2, 3, 3)   # direct small-channel kernel
     assert abi.sparoa_conv2d_tiling(stem, abi.PATH_SKIP_MFMA) == (16, 32)
     assert abi.sparoa_conv2d_workspace_size(stem, abi.PATH_DENSE_MFMA) == 0
+    # its limits: 16-bit, C_in <= 4, C_out in {16, 32, 64}, dilation 1 (else the general kernel)
+    for desc in (abi.conv_desc(2, 4, 40, 40, 32, 3, 3, 1, 1, 1, 1),
+                 abi.conv_desc(2, 1, 40, 40, 16, 5, 5, 2, 2, 2, 2, dtype=abi.F16)):
+        assert abi.sparoa_conv2d_tiling(desc, abi.PATH_DENSE_MFMA) == (16, 32)
+    for desc in (abi.conv_desc(2, 5, 40, 40, 32, 3, 3, 1, 1, 1, 1),
+                 abi.conv_desc(2, 3, 40, 40, 48, 3, 3, 1, 1, 1, 1),
+                 abi.conv_desc(2, 3, 40, 40, 32, 3, 3, 1, 1, 1, 1, dtype=abi.F32),
+                 abi.conv_desc(2, 3, 40, 40, 32, 3, 3, 1, 1, 2, 2, 2, 2)):
+        assert abi.sparoa_conv2d_tiling(desc, abi.PATH_DENSE_MFMA)[0] != 16
     f = abi.fc_desc(8, 4096, 4096)
     assert abi.sparoa_fc_skip_block(f, abi.PATH_SKIP_BW) == (8, 1)
     assert abi.sparoa_fc_tiling(f, abi.PATH_SKIP_BW) == (8, 1)
