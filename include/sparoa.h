@@ -38,7 +38,10 @@
 extern "C" {
 #endif
 
-#define SPAROA_ABI_VERSION 1u
+/* 2: the GEMM workspace queries include count-commit words (zero on entry,
+ *    left zero) used by the output-measuring calls; smaller workspaces keep
+ *    the version-1 behaviour. */
+#define SPAROA_ABI_VERSION 2u
 
 typedef enum {
   SPAROA_OK = 0,

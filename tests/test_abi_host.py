@@ -28,7 +28,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert abi.sparoa_abi_version() == 1
+    assert abi.sparoa_abi_version() == 2
     assert abi.sparoa_status_string(0) == "ok"
     assert abi.sparoa_status_string(3) == "workspace too small"
 
