@@ -1,13 +1,15 @@
 """Split execution of one operator over the zero-skip and dense paths (each
 row tile of the implicit GEMM routed by the zero fraction of the samples its
 rows come from): the executed work must equal the oracle's count under the
-same per-tile rule, bit for bit, and the output must equal the dense path's
-bit for bit."""
+same per-tile rule, bit for bit, the output must equal the dense path's bit
+for bit, and it must lie within the dtype's tolerance of the oracle's direct
+conv / FC element by element."""
 import pytest
 import torch
 
 import oracle
 import synth
+from tests._util import RTOL, assert_close
 
 pytestmark = pytest.mark.gpu
 
@@ -64,6 +66,7 @@ def test_conv2d_split(case):
                      dtype=torch.uint8, device=dev)
     y_dense = torch.empty(n, ho, wo, cout, dtype=tdt, device=dev)
     abi.sparoa_conv2d(d, abi.PATH_DENSE_MFMA, xd, wd, None, None, abi.ACT_RELU, None, y_dense, ws)
+    yr, ar, _ = oracle.conv2d(x, wt, n, cin, h, w, cout, k, k, s, s, p, p, act=oracle.ACT_RELU)
     rows, kc = abi.sparoa_conv2d_tiling(d, abi.PATH_SKIP_MFMA)
     assert kc == 64
     for thr in (0.0, 0.3, 0.5, 0.9, 2.0):
@@ -71,6 +74,7 @@ def test_conv2d_split(case):
         ex = torch.full((1,), -1, dtype=torch.int64, device=dev)
         abi.sparoa_conv2d_split(d, thr, zs, xd, wd, None, None, abi.ACT_RELU, mask, y, ws, ex)
         torch.cuda.synchronize()
+        assert_close(y, yr, ar, RTOL[tdt], f"split conv {case} thr {thr} vs oracle")
         assert torch.equal(y, y_dense), f"{case} thr {thr}"
         want = oracle.conv_split_executed_blocks(x, n, cin, h, w, k, k, s, s, p, p, 1, 1, rows,
                                                  64, thr)
@@ -95,12 +99,14 @@ def test_fc_split(m, k, n):
                      dtype=torch.uint8, device=dev)
     y_dense = torch.empty(m, n, dtype=torch.bfloat16, device=dev)
     abi.sparoa_fc(d, abi.PATH_DENSE_MFMA, xd, wd, None, None, abi.ACT_NONE, None, y_dense, ws)
+    yr, ar = oracle.fc(x, w, m, k, n)
     rows, kc = abi.sparoa_fc_tiling(d, abi.PATH_SKIP_MFMA)
     for thr in (0.0, 0.45, 0.85, 2.0):
         y = torch.full_like(y_dense, float("nan"))
         ex = torch.full((1,), -1, dtype=torch.int64, device=dev)
         abi.sparoa_fc_split(d, thr, zs, xd, wd, None, None, abi.ACT_NONE, mask, y, ws, ex)
         torch.cuda.synchronize()
+        assert_close(y, yr, ar, RTOL[torch.bfloat16], f"split fc {m}x{k}x{n} thr {thr} vs oracle")
         assert torch.equal(y, y_dense), f"thr {thr}"
         want = oracle.conv_split_executed_blocks(x.reshape(m, 1, 1, k), m, k, 1, 1, 1, 1, 1, 1,
                                                  0, 0, 1, 1, rows, kc, thr)
