@@ -38,10 +38,13 @@
 extern "C" {
 #endif
 
-/* 2: the GEMM workspace queries include count-commit words (zero on entry,
- *    left zero) used by the output-measuring calls; smaller workspaces keep
- *    the version-1 behaviour. */
-#define SPAROA_ABI_VERSION 2u
+/* 3: the output-measuring calls take their count-commit words as an explicit
+ *    argument (y_commit); the workspace queries report the split-K partial
+ *    sums only. */
+#define SPAROA_ABI_VERSION 3u
+
+/* Bytes of the count-commit words of the output-measuring calls (y_commit). */
+#define SPAROA_COMMIT_WORDS_BYTES 2048
 
 typedef enum {
   SPAROA_OK = 0,
@@ -204,10 +207,8 @@ sparoa_status sparoa_route(const sparoa_counts *counts, const sparoa_intensity *
  *   (16, 32)), the number of issued (16-pixel row block, 32-wide k-step)
  *   MFMA steps.
  *   Workspace: sparoa_conv2d_workspace_size bytes -- the split-K partial
- *   sums, and for shapes whose GEMM can measure its output (see
- *   sparoa_conv2d_routed_measured) 2048 more bytes of count-commit words
- *   after them, which must be zero before the first call that uses them and
- *   are zero again after every call.  Only the partial sums are required.
+ *   sums (0 when the GEMM needs no K split); its contents on entry do not
+ *   matter and several calls may share one workspace in stream order.
  * Errors: INVALID_ARG for bad shapes, null x/w/y, a null mask on a skip path;
  * UNSUPPORTED for grouped non-depthwise convs, unsupported dtype/path;
  * WORKSPACE if ws_bytes is below the partial-sum bytes.
@@ -341,11 +342,15 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
  *   64-channel-chunk implicit GEMM serves the layer and cols % 64 == 0: no
  *   launch of its own and no second read of y; otherwise the standalone
  *   measurement of y runs after the layer (as sparoa_measure_sparsity_preset:
- *   one launch for the block shapes whose bitmap needs no clearing).  The
- *   fused form commits its counts through the count-commit words of a
- *   workspace of the queried size (zero on entry, left zero; 8 ticketed
- *   words per counter instead of one atomic per work-group on y_counts),
- *   and directly into y_counts with a smaller workspace.
+ *   one launch for the block shapes whose bitmap needs no clearing).
+ *   y_commit (nullable): SPAROA_COMMIT_WORDS_BYTES of device memory that
+ *   must be all zero on entry and is all zero again when the call's kernels
+ *   finish (a caller resets it with y_counts).  The fused form then commits
+ *   its counts through 8 ticketed words per counter (one atomic per
+ *   work-group on a word of its group; the work-group completing a group
+ *   adds the group's total to y_counts and clears the word) instead of one
+ *   same-address atomic per work-group on y_counts.  NULL: direct commits,
+ *   same counts.  Calls that overlap in time must not share y_commit.
  *   Other arguments as for sparoa_conv2d_routed / sparoa_fc_routed.
  * Errors: theirs, and INVALID_ARG for a null y_counts or y_mask.
  * ---------------------------------------------------------------------- */
@@ -356,7 +361,7 @@ sparoa_status sparoa_conv2d_routed_measured(const sparoa_conv_desc *desc,
                                             sparoa_act act, const uint32_t *mask, void *y,
                                             void *workspace, size_t ws_bytes, uint32_t *path_dev,
                                             sparoa_counts *y_counts, uint32_t *y_mask,
-                                            hipStream_t stream);
+                                            uint64_t *y_commit, hipStream_t stream);
 sparoa_status sparoa_fc_routed_measured(const sparoa_fc_desc *desc, const sparoa_thresholds *thr,
                                         const sparoa_counts *counts_dev, const void *x,
                                         const void *w_nk, const void *w_packed, const void *bias,
@@ -364,7 +369,7 @@ sparoa_status sparoa_fc_routed_measured(const sparoa_fc_desc *desc, const sparoa
                                         const uint32_t *mask, void *y, void *workspace,
                                         size_t ws_bytes, uint32_t *path_dev,
                                         sparoa_counts *y_counts, uint32_t *y_mask,
-                                        hipStream_t stream);
+                                        uint64_t *y_commit, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Split execution of one operator over the zero-skip and dense paths: the
@@ -441,10 +446,13 @@ sparoa_status sparoa_fc_measured(const sparoa_fc_desc *desc, const sparoa_thresh
  * of their own are measured together (two launches per 16 ops), then their
  * FC kernels run in op order, then their split-K reductions run together
  * (one launch per 16 ops of a dtype); results are those of op-by-op calls,
- * bit for bit.  Ops whose inputs (x, residual) overlap another op's
- * output run op by op instead.
- * Stops at the first failing op and returns its status (a batch that fails
- * validation launches nothing).
+ * bit for bit.  A batch in which memory one op writes (y, counts, mask,
+ * workspace, path) overlaps memory another op reads or writes runs op by
+ * op instead, in order.
+ * Every op is validated (as sparoa_fc_measured validates) before the first
+ * launch: a batch with an invalid op launches nothing and returns that op's
+ * status, with "op <i>: " leading the message.  A HIP failure during the
+ * launches returns SPAROA_ERR_HIP at once.
  * ---------------------------------------------------------------------- */
 typedef struct {
   sparoa_fc_desc desc;

@@ -19,6 +19,7 @@ ACT_NONE, ACT_RELU, ACT_RELU6 = 0, 1, 2
 PATH_DENSE_MFMA, PATH_SKIP_MFMA, PATH_DENSE_BW, PATH_SKIP_BW = 0, 1, 2, 3
 ROUTE_BLOCK, ROUTE_ELEMENT = 0, 1
 PATH_NAMES = {0: "dense_mfma", 1: "skip_mfma", 2: "dense_bw", 3: "skip_bw"}
+COMMIT_WORDS_BYTES = 2048   # SPAROA_COMMIT_WORDS_BYTES
 
 _TORCH_DT = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
 
@@ -142,10 +143,10 @@ def _load():
                                            ctypes.c_int, vp, vp, vp, sz, vp, vp]),
         "sparoa_conv2d_routed_measured": (ctypes.c_int, [P(ConvDesc), P(Thresholds), vp, vp, vp,
                                                          vp, vp, ctypes.c_int, vp, vp, vp, sz, vp,
-                                                         vp, vp, vp]),
+                                                         vp, vp, vp, vp]),
         "sparoa_fc_routed_measured": (ctypes.c_int, [P(FcDesc), P(Thresholds), vp, vp, vp, vp, vp,
                                                      vp, ctypes.c_int, vp, vp, vp, sz, vp, vp, vp,
-                                                     vp]),
+                                                     vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -387,26 +388,28 @@ def sparoa_fc_routed(desc, sparsity_thr, intensity_thr, mode, counts, x, w_nk, w
 
 def sparoa_conv2d_routed_measured(desc, sparsity_thr, intensity_thr, mode, counts, x, w, bias,
                                   residual, act, mask, y, y_counts, y_mask, workspace=None,
-                                  path=None, stream=None):
-    """sparoa_conv2d_routed that also measures y into y_counts / y_mask."""
+                                  path=None, y_commit=None, stream=None):
+    """sparoa_conv2d_routed that also measures y into y_counts / y_mask
+    (y_commit: zeroed count-commit words, or None)."""
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     t = Thresholds(sparsity_thr, intensity_thr, mode)
     _check(_L.sparoa_conv2d_routed_measured(
         ctypes.byref(desc), ctypes.byref(t), _ptr(counts), _ptr(x), _ptr(w), _ptr(bias),
         _ptr(residual), act, _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes, _ptr(path),
-        _ptr(y_counts), _ptr(y_mask), _stream(stream)))
+        _ptr(y_counts), _ptr(y_mask), _ptr(y_commit), _stream(stream)))
 
 
 def sparoa_fc_routed_measured(desc, sparsity_thr, intensity_thr, mode, counts, x, w_nk, w_packed,
                               bias, residual, act, mask, y, y_counts, y_mask, workspace=None,
-                              path=None, stream=None):
-    """sparoa_fc_routed that also measures y into y_counts / y_mask."""
+                              path=None, y_commit=None, stream=None):
+    """sparoa_fc_routed that also measures y into y_counts / y_mask
+    (y_commit: zeroed count-commit words, or None)."""
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     t = Thresholds(sparsity_thr, intensity_thr, mode)
     _check(_L.sparoa_fc_routed_measured(
         ctypes.byref(desc), ctypes.byref(t), _ptr(counts), _ptr(x), _ptr(w_nk), _ptr(w_packed),
         _ptr(bias), _ptr(residual), act, _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes,
-        _ptr(path), _ptr(y_counts), _ptr(y_mask), _stream(stream)))
+        _ptr(path), _ptr(y_counts), _ptr(y_mask), _ptr(y_commit), _stream(stream)))
 
 
 def sparoa_conv2d_split(desc, sparsity_thr, sample_zeros, x, w, bias, residual, act, mask, y,

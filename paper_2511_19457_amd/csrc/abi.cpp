@@ -263,7 +263,7 @@ sparoa_status sparoa_conv2d_workspace_size(const sparoa_conv_desc *d, sparoa_pat
   sparoa_status st = check_conv(d, &ho, &wo);
   if (st != SPAROA_OK) return st;
   if (!bytes || !path_ok(path)) return fail(SPAROA_ERR_INVALID_ARG, "workspace_size: bad argument");
-  *bytes = is_depthwise(*d) ? 0 : gemm_workspace(*d, path);
+  *bytes = is_depthwise(*d) ? 0 : gemm_workspace_required(*d, path);
   return SPAROA_OK;
 }
 
@@ -395,7 +395,7 @@ sparoa_status sparoa_fc_workspace_size(const sparoa_fc_desc *d, sparoa_path path
   if (st != SPAROA_OK) return st;
   if (!bytes || !path_ok(path)) return fail(SPAROA_ERR_INVALID_ARG, "workspace_size: bad argument");
   *bytes = ((path & 2) && fc_bw_streams(*d)) ? fc_bw_workspace(*d, path)
-                                              : gemm_workspace(fc_as_conv(*d), path);
+                                              : gemm_workspace_required(fc_as_conv(*d), path);
   return SPAROA_OK;
 }
 
@@ -490,7 +490,7 @@ sparoa_status conv_routed_impl(const sparoa_conv_desc *d, const sparoa_threshold
                                const void *bias, const void *residual, sparoa_act act,
                                const uint32_t *mask, void *y, void *workspace, size_t ws_bytes,
                                uint32_t *path_dev, sparoa_counts *y_counts, uint32_t *y_mask,
-                               hipStream_t stream) {
+                               uint64_t *y_commit, hipStream_t stream) {
   sparoa_intensity in;
   sparoa_status st = sparoa_op_intensity_conv(d, &in);
   if (st != SPAROA_OK) return st;
@@ -498,7 +498,8 @@ sparoa_status conv_routed_impl(const sparoa_conv_desc *d, const sparoa_threshold
   if (!counts_dev || !x || !w || !y || !mask || !act_ok(act))
     return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed: null counts/x/w/mask/y or bad act");
   if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed: has_bias without bias");
-  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace, y_counts, y_mask})) != SPAROA_OK)
+  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace, y_counts, y_mask,
+                          y_commit})) != SPAROA_OK)
     return st;
   const bool measure_y = y_counts != nullptr;
   if (measure_y != (y_mask != nullptr))
@@ -528,7 +529,7 @@ sparoa_status conv_routed_impl(const sparoa_conv_desc *d, const sparoa_threshold
   // without a skip kernel for this shape the dense kernel runs and records a dense path
   const bool can_skip = gemm_skip_supported(*d);
   if (measure_y && gemm_fuses_out_measure(*d, p)) {   // y_counts arrives initialised
-    const OutMeasure om{y_counts, y_mask};
+    const OutMeasure om{y_counts, y_mask, reinterpret_cast<unsigned long long *>(y_commit)};
     return launch_gemm_conv(*d, p, x, w, d->has_bias ? bias : nullptr, residual, act,
                             can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r,
                             nullptr, &om);
@@ -550,7 +551,7 @@ sparoa_status sparoa_conv2d_routed(const sparoa_conv_desc *d, const sparoa_thres
                                    size_t ws_bytes, uint32_t *path_dev, hipStream_t stream) {
   g_last_error.clear();
   return conv_routed_impl(d, thr, counts_dev, x, w, bias, residual, act, mask, y, workspace,
-                          ws_bytes, path_dev, nullptr, nullptr, stream);
+                          ws_bytes, path_dev, nullptr, nullptr, nullptr, stream);
 }
 
 sparoa_status sparoa_conv2d_routed_measured(const sparoa_conv_desc *d,
@@ -560,27 +561,26 @@ sparoa_status sparoa_conv2d_routed_measured(const sparoa_conv_desc *d,
                                             sparoa_act act, const uint32_t *mask, void *y,
                                             void *workspace, size_t ws_bytes, uint32_t *path_dev,
                                             sparoa_counts *y_counts, uint32_t *y_mask,
-                                            hipStream_t stream) {
+                                            uint64_t *y_commit, hipStream_t stream) {
   g_last_error.clear();
   if (!y_counts || !y_mask)
     return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed_measured: null y_counts or y_mask");
   return conv_routed_impl(d, thr, counts_dev, x, w, bias, residual, act, mask, y, workspace,
-                          ws_bytes, path_dev, y_counts, y_mask, stream);
+                          ws_bytes, path_dev, y_counts, y_mask, y_commit, stream);
 }
 
 
 }  // extern "C"
 
 namespace {
-// The routed FC (see sparoa_fc_routed); defer as for launch_gemm_conv.
-sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
-                             const sparoa_counts *counts_dev, const void *x, const void *w_nk,
-                             const void *w_packed, const void *bias, const void *residual,
-                             sparoa_act act, const uint32_t *mask, void *y, void *workspace,
-                             size_t ws_bytes, uint32_t *path_dev, hipStream_t stream,
-                             SplitReduceJob *defer, sparoa_counts *y_counts = nullptr,
-                             uint32_t *y_mask = nullptr) {
-  if (defer) defer->split = 0;
+// Every check of the routed FC, with no device work: the executor runs it on
+// a whole batch before its first launch.
+sparoa_status fc_routed_check(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
+                              const sparoa_counts *counts_dev, const void *x, const void *w_nk,
+                              const void *w_packed, const void *bias, const void *residual,
+                              sparoa_act act, const uint32_t *mask, void *y, void *workspace,
+                              size_t ws_bytes, const sparoa_counts *y_counts,
+                              const uint32_t *y_mask, const uint64_t *y_commit) {
   sparoa_intensity in;
   sparoa_status st = sparoa_op_intensity_fc(d, &in);
   if (st != SPAROA_OK) return st;
@@ -591,11 +591,37 @@ sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *t
   if (!counts_dev || !x || !w || !y || !mask || !act_ok(act))
     return fail(SPAROA_ERR_INVALID_ARG, "fc_routed: null counts/x/weights/mask/y or bad act");
   if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "fc_routed: has_bias without bias");
-  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace, y_counts, y_mask})) != SPAROA_OK)
+  if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace, y_counts, y_mask,
+                          y_commit})) != SPAROA_OK)
     return st;
-  const bool measure_y = y_counts != nullptr;
-  if (measure_y != (y_mask != nullptr))
+  if ((y_counts != nullptr) != (y_mask != nullptr))
     return fail(SPAROA_ERR_INVALID_ARG, "fc_routed_measured: null y_counts or y_mask");
+  if (!streams) {
+    const sparoa_path p = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
+    if (ws_bytes < gemm_workspace_required(fc_as_conv(*d), p))
+      return fail(SPAROA_ERR_WORKSPACE, "fc_routed: workspace too small");
+  }
+  return SPAROA_OK;
+}
+
+// The routed FC (see sparoa_fc_routed); defer as for launch_gemm_conv.
+sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
+                             const sparoa_counts *counts_dev, const void *x, const void *w_nk,
+                             const void *w_packed, const void *bias, const void *residual,
+                             sparoa_act act, const uint32_t *mask, void *y, void *workspace,
+                             size_t ws_bytes, uint32_t *path_dev, hipStream_t stream,
+                             SplitReduceJob *defer, sparoa_counts *y_counts = nullptr,
+                             uint32_t *y_mask = nullptr, uint64_t *y_commit = nullptr) {
+  if (defer) defer->split = 0;
+  sparoa_status st = fc_routed_check(d, thr, counts_dev, x, w_nk, w_packed, bias, residual, act,
+                                     mask, y, workspace, ws_bytes, y_counts, y_mask, y_commit);
+  if (st != SPAROA_OK) return st;
+  sparoa_intensity in;
+  sparoa_op_intensity_fc(d, &in);
+  const int bw = in.intensity < thr->intensity_thr ? 1 : 0;
+  const bool streams = bw && fc_bw_streams(*d);
+  const void *w = streams ? w_packed : w_nk;
+  const bool measure_y = y_counts != nullptr;
   auto measure_after = [&]() {
     return measure_y ? launch_measure(y, d->dtype, d->m, d->n, 1, 8, 0, y_counts, y_mask, nullptr,
                                       stream, true)   // y_counts arrive preset
@@ -610,10 +636,9 @@ sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *t
   }
   const sparoa_conv_desc c = fc_as_conv(*d);
   const sparoa_path p = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
-  if (ws_bytes < gemm_workspace_required(c, p)) return fail(SPAROA_ERR_WORKSPACE, "fc_routed: workspace too small");
   const bool can_skip = gemm_skip_supported(c);
   if (measure_y && gemm_fuses_out_measure(c, p)) {   // y_counts arrives initialised
-    const OutMeasure om{y_counts, y_mask};
+    const OutMeasure om{y_counts, y_mask, reinterpret_cast<unsigned long long *>(y_commit)};
     return launch_gemm_conv(c, p, x, w, d->has_bias ? bias : nullptr, residual, act,
                             can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r,
                             defer, &om);
@@ -635,10 +660,12 @@ struct FcPlan {
   MeasureJob measure;
 };
 
+// Validates the whole call (measurement and routed FC) before any launch.
 sparoa_status fc_measured_plan(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
-                               const void *x, const void *w_packed, const void *bias,
-                               const void *residual, sparoa_act act, sparoa_counts *counts_dev,
-                               uint32_t *mask_dev, void *y, FcPlan *p) {
+                               const void *x, const void *w_nk, const void *w_packed,
+                               const void *bias, const void *residual, sparoa_act act,
+                               sparoa_counts *counts_dev, uint32_t *mask_dev, void *y,
+                               void *workspace, size_t ws_bytes, FcPlan *p) {
   sparoa_intensity in;
   sparoa_status st = sparoa_op_intensity_fc(d, &in);
   if (st != SPAROA_OK) return st;
@@ -655,7 +682,11 @@ sparoa_status fc_measured_plan(const sparoa_fc_desc *d, const sparoa_thresholds 
   const sparoa_path fam = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
   if ((st = sparoa_fc_skip_block(d, fam, &br, &bc)) != SPAROA_OK) return st;
   p->measure = MeasureJob{x, d->dtype, d->m, d->k, br, bc, counts_dev, mask_dev};
-  return check_measure(x, d->dtype, d->m, d->k, br, bc, 0, counts_dev, mask_dev, nullptr);
+  if ((st = check_measure(x, d->dtype, d->m, d->k, br, bc, 0, counts_dev, mask_dev, nullptr)) !=
+      SPAROA_OK)
+    return st;
+  return fc_routed_check(d, thr, counts_dev, x, w_nk, w_packed, bias, residual, act, mask_dev, y,
+                         workspace, ws_bytes, nullptr, nullptr, nullptr);
 }
 }  // namespace
 
@@ -678,12 +709,13 @@ sparoa_status sparoa_fc_routed_measured(const sparoa_fc_desc *d, const sparoa_th
                                         const uint32_t *mask, void *y, void *workspace,
                                         size_t ws_bytes, uint32_t *path_dev,
                                         sparoa_counts *y_counts, uint32_t *y_mask,
-                                        hipStream_t stream) {
+                                        uint64_t *y_commit, hipStream_t stream) {
   g_last_error.clear();
   if (!y_counts || !y_mask)
     return fail(SPAROA_ERR_INVALID_ARG, "fc_routed_measured: null y_counts or y_mask");
   return fc_routed_impl(d, thr, counts_dev, x, w_nk, w_packed, bias, residual, act, mask, y,
-                        workspace, ws_bytes, path_dev, stream, nullptr, y_counts, y_mask);
+                        workspace, ws_bytes, path_dev, stream, nullptr, y_counts, y_mask,
+                        y_commit);
 }
 
 sparoa_status sparoa_fc_measured(const sparoa_fc_desc *d, const sparoa_thresholds *thr,
@@ -694,8 +726,8 @@ sparoa_status sparoa_fc_measured(const sparoa_fc_desc *d, const sparoa_threshold
                                  hipStream_t stream) {
   g_last_error.clear();
   FcPlan p;
-  sparoa_status st = fc_measured_plan(d, thr, x, w_packed, bias, residual, act, counts_dev,
-                                      mask_dev, y, &p);
+  sparoa_status st = fc_measured_plan(d, thr, x, w_nk, w_packed, bias, residual, act, counts_dev,
+                                      mask_dev, y, workspace, ws_bytes, &p);
   if (st != SPAROA_OK) return st;
   if (p.self_measures) {
     const int bw = 1;
@@ -772,27 +804,51 @@ sparoa_status sparoa_fc_split(const sparoa_fc_desc *d, double sparsity_thr,
 // ---------------------------------------------------------------- executor
 
 namespace {
-// True when some op reads memory that some op writes (an output feeding
-// another op's input): then the ops must run strictly one after another.
-bool ops_chained(const sparoa_fc_op *ops, int64_t n) {
+// True when some op writes memory that another op reads or writes (an
+// output feeding another op's input, or counts, masks, workspaces or path
+// words shared between ops -- valid one op after another, but a batch
+// measures every op before any op routes and reduces split-K partials after
+// later GEMMs): then the ops must run strictly one after another.  Called on
+// validated ops.
+bool ops_chained(const sparoa_fc_op *ops, int64_t n, const sparoa_thresholds *thr) {
+  typedef std::pair<uintptr_t, uintptr_t> Range;
   auto range = [](const void *p, int64_t bytes) {
     const uintptr_t b = reinterpret_cast<uintptr_t>(p);
-    return std::make_pair(b, b + (uintptr_t)(p ? bytes : 0));
+    return Range(b, b + (uintptr_t)(p ? bytes : 0));
   };
-  auto overlap = [](std::pair<uintptr_t, uintptr_t> a, std::pair<uintptr_t, uintptr_t> b) {
-    return a.first < b.second && b.first < a.second;
-  };
-  for (int64_t j = 0; j < n; ++j) {
-    const sparoa_fc_desc &dj = ops[j].desc;
-    const int64_t e = elem_size(dj.dtype);
-    const auto xj = range(ops[j].x, dj.m * dj.k * e), rj = range(ops[j].residual, dj.m * dj.n * e);
-    for (int64_t i = 0; i < n; ++i) {
-      if (i == j) continue;
-      const sparoa_fc_desc &di = ops[i].desc;
-      const auto yi = range(ops[i].y, di.m * di.n * elem_size(di.dtype));
-      if (overlap(xj, yi) || overlap(rj, yi)) return true;
-    }
+  auto overlap = [](Range a, Range b) { return a.first < b.second && b.first < a.second; };
+  std::vector<std::vector<Range>> rd((size_t)n), wr((size_t)n);
+  for (int64_t i = 0; i < n; ++i) {
+    const sparoa_fc_op &o = ops[i];
+    const sparoa_fc_desc &d = o.desc;
+    const int64_t e = elem_size(d.dtype);
+    const sparoa_thresholds *t = thr ? thr : &o.thr;
+    sparoa_intensity in;
+    sparoa_op_intensity_fc(&d, &in);
+    const sparoa_path fam =
+        in.intensity < t->intensity_thr ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
+    int64_t br = 1, bc = 1, words = 0;
+    sparoa_fc_skip_block(&d, fam, &br, &bc);
+    sparoa_mask_words(d.m, d.k, br, bc, &words);
+    size_t packed = 0;
+    sparoa_fc_packed_bytes(&d, &packed);
+    rd[i] = {range(o.x, d.m * d.k * e), range(o.residual, d.m * d.n * e),
+             range(o.w_nk, d.n * d.k * e), range(o.w_packed, (int64_t)packed),
+             range(o.bias, d.n * e)};
+    wr[i] = {range(o.y, d.m * d.n * e), range(o.counts, (int64_t)sizeof(sparoa_counts)),
+             range(o.mask, words * 4), range(o.workspace, (int64_t)o.ws_bytes),
+             range(o.path, 4)};
   }
+  for (int64_t i = 0; i < n; ++i)
+    for (int64_t j = 0; j < n; ++j) {
+      if (i == j) continue;
+      for (const Range &w : wr[i]) {
+        for (const Range &r : rd[j])
+          if (overlap(w, r)) return true;
+        for (const Range &r : wr[j])
+          if (overlap(w, r)) return true;
+      }
+    }
   return false;
 }
 
@@ -812,7 +868,19 @@ sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa
   g_last_error.clear();
   sparoa_status st = check_ops(ops, n, thr);
   if (st != SPAROA_OK) return st;
-  if (events || ops_chained(ops, n)) {  // op by op (each bracketed by its events, if given)
+  // Every op is validated before the first launch (a batch that fails
+  // validation launches nothing), whichever way it then runs.
+  std::vector<FcPlan> plan((size_t)n);
+  for (int64_t i = 0; i < n; ++i) {
+    const sparoa_fc_op &o = ops[i];
+    if ((st = fc_measured_plan(&o.desc, thr ? thr : &o.thr, o.x, o.w_nk, o.w_packed, o.bias,
+                               o.residual, o.act, o.counts, o.mask, o.y, o.workspace, o.ws_bytes,
+                               &plan[i])) != SPAROA_OK) {
+      g_last_error = "op " + std::to_string(i) + ": " + g_last_error;
+      return st;
+    }
+  }
+  if (events || ops_chained(ops, n, thr)) {  // op by op (each bracketed by its events, if given)
     for (int64_t i = 0; i < n; ++i) {
       const sparoa_fc_op &o = ops[i];
       if (events) SPAROA_HIP_CHECK(hipEventRecord(events[2 * i], stream));
@@ -831,13 +899,6 @@ sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa
   // one dtype and row-tile count); then each other op's FC kernel in op
   // order; then the split-K reductions, grouped per dtype.  Same arithmetic
   // as op-by-op calls, fewer launches.
-  std::vector<FcPlan> plan((size_t)n);
-  for (int64_t i = 0; i < n; ++i) {
-    const sparoa_fc_op &o = ops[i];
-    if ((st = fc_measured_plan(&o.desc, thr ? thr : &o.thr, o.x, o.w_packed, o.bias, o.residual,
-                               o.act, o.counts, o.mask, o.y, &plan[i])) != SPAROA_OK)
-      return st;
-  }
   for (int esz : {2, 4}) {
     std::vector<MeasureJob> group;
     for (int64_t i = 0; i < n; ++i) {

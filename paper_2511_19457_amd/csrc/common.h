@@ -109,7 +109,7 @@ struct SplitReduceJob {
   void *y;
   sparoa_counts *om_counts;  // non-null: measure y (see OutMeasure)
   uint32_t *om_mask;
-  unsigned long long *om_words;  // non-null: grouped count commit (gemm_workspace)
+  unsigned long long *om_words;  // non-null: grouped count commit (OutMeasure::words)
 };
 sparoa_status launch_split_reduce(const SplitReduceJob &job, hipStream_t stream);
 // Several reductions of one dtype in one launch (n <= kGroupMax).
@@ -120,9 +120,12 @@ sparoa_status launch_split_reduce_group(const SplitReduceJob *jobs, int n, hipSt
 // [M = N*Ho*Wo, C_out] -- exactly what launch_measure gives for that view.
 // counts must hold {0, numel, nb, nb} before the producer runs (the caller
 // resets them); the bitmap needs no clearing.
+// words: SPAROA_COMMIT_WORDS_BYTES of zeroed count-commit words (ticketed
+// commit, left zero), or null for one atomic per work-group on counts.
 struct OutMeasure {
   sparoa_counts *counts;
   uint32_t *mask;
+  unsigned long long *words = nullptr;
 };
 
 // Implicit-GEMM MFMA conv (groups == 1); FC runs through it as a 1x1 conv.
@@ -135,12 +138,8 @@ struct GemmTileChoice {
 };
 GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path path);
 bool gemm_skip_supported(const sparoa_conv_desc &d);
-// Workspace bytes a GEMM call needs (split-K partials) ...
+// Workspace bytes a GEMM call needs (split-K partials).
 size_t gemm_workspace_required(const sparoa_conv_desc &d, sparoa_path path);
-// ... and the size the workspace queries report: the required bytes plus,
-// for shapes whose epilogue or reduction measures the output, the words of
-// the grouped count commit (zero on entry, left zero by every call).
-size_t gemm_workspace(const sparoa_conv_desc &d, sparoa_path path);
 sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, const void *x,
                                const void *w, const void *bias, const void *residual,
                                sparoa_act act, const uint32_t *mask, void *y, void *ws,

@@ -365,15 +365,15 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
       }
 }
 
-// Workspace words of the grouped count commit: kOmGroups groups x 2
-// counters, one 128-byte line each.
+// Words of the grouped count commit: kOmGroups groups x 2 counters, one
+// 128-byte line each.
 constexpr int kOmGroups = 8;
-constexpr size_t kOmWordsBytes = 2 * kOmGroups * 128;
+static_assert(2 * kOmGroups * 128 == SPAROA_COMMIT_WORDS_BYTES, "commit word layout");
 
 // Adds a work-group's zero count and nonzero-block count into counts
 // (zero_blocks starts at nb).  Same-address atomics serialise device-wide
 // (13-17 ns per work-group measured with one atomic per counter), so with
-// `words` (kOmWordsBytes of workspace, zero on entry) work-group b of nwg is
+// `words` (the caller's zeroed count-commit words) work-group b of nwg is
 // a member of group b % kOmGroups: each member adds (1 << 40) + its count to
 // its group's word with one returning atomic, and the member whose add
 // completes the group adds the group's total to counts and clears the word
@@ -1544,16 +1544,6 @@ size_t gemm_workspace_required(const sparoa_conv_desc &d, sparoa_path path) {
   return (size_t)t.split_k * (size_t)s.M * (size_t)s.N * sizeof(float);
 }
 
-namespace {
-size_t om_words_offset(const sparoa_conv_desc &d, sparoa_path path) {
-  return (gemm_workspace_required(d, path) + 255) / 256 * 256;
-}
-}  // namespace
-
-size_t gemm_workspace(const sparoa_conv_desc &d, sparoa_path path) {
-  if (!gemm_fuses_out_measure(d, path)) return gemm_workspace_required(d, path);
-  return om_words_offset(d, path) + kOmWordsBytes;
-}
 
 sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, const void *x,
                                const void *w, const void *bias, const void *residual,
@@ -1600,11 +1590,8 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   // the epilogue measures y when it writes y; with split-K the reduction does
   a.om_counts = om && gz == 1 ? om->counts : nullptr;
   a.om_mask = om && gz == 1 ? om->mask : nullptr;
-  // grouped count commit when the workspace holds its words
-  unsigned long long *om_words = nullptr;
-  if (om && ws && ws_bytes >= om_words_offset(d, path) + kOmWordsBytes)
-    om_words = reinterpret_cast<unsigned long long *>(static_cast<char *>(ws) +
-                                                      om_words_offset(d, path));
+  // grouped count commit when the caller gives the words
+  unsigned long long *om_words = om ? om->words : nullptr;
   a.om_words = gz == 1 ? om_words : nullptr;
   if (gz > 1 && ws_bytes < (size_t)gz * s.M * s.N * sizeof(float))
     return fail(SPAROA_ERR_WORKSPACE, "GEMM split-K workspace too small");

@@ -96,10 +96,17 @@ class Engine:
                 st["mask"] = torch.zeros(
                     abi.sparoa_mask_words(st["rows"], st["cols"], st["br"], st["bc"]),
                     dtype=torch.int32, device=self.dev)
-                st["ws"] = torch.zeros(max(16, ws), dtype=torch.uint8, device=self.dev)
+                st["ws_bytes"] = ws
                 st["path"] = torch.zeros(1, dtype=torch.int32, device=self.dev)
             self.acts[i + 1] = torch.empty(output_shape(L), dtype=dtype, device=self.dev)
             self.st.append(st)
+        # one split-K workspace serves every layer (they run in stream order;
+        # its contents on entry do not matter)
+        self.ws = torch.empty(max([16] + [st.get("ws_bytes", 0) for st in self.st]),
+                              dtype=torch.uint8, device=self.dev)
+        for st in self.st:
+            if "ws_bytes" in st:
+                st["ws"] = self.ws
         # Activations a conv/FC produces and some consumer measures at block
         # (1, 8): in routed mode the producer measures them in its epilogue
         # (sparoa_*_routed_measured) and those consumers skip their own pass.
@@ -136,14 +143,20 @@ class Engine:
         # counters never share a line with the input counters other
         # work-groups of the same kernel read
         pad = [row + [0] * 12 for row in tmpl]
+        # then the zeroed count-commit words of every fused output
+        # measurement (16 lines each), reset with the counters
+        cw_rows = abi.COMMIT_WORDS_BYTES // 128
+        pad += [[0] * 16] * (cw_rows * len(meas))
         self.ctr_template = torch.tensor(pad, dtype=torch.int64, device=self.dev)
         self.ctr = torch.zeros_like(self.ctr_template)
         for i, L in enumerate(layers):
             if L.kind != "maxpool":
                 self.st[i]["counts"] = self.ctr[i, :4]
+        cw0 = len(layers) + len(meas)
         for j, (t, _, words) in enumerate(meas):
             self.tmeas[t] = dict(counts=self.ctr[len(layers) + j, :4],
-                                 mask=torch.zeros(words, dtype=torch.int32, device=self.dev))
+                                 mask=torch.zeros(words, dtype=torch.int32, device=self.dev),
+                                 commit=self.ctr[cw0 + cw_rows * j:cw0 + cw_rows * (j + 1)])
         torch.cuda.synchronize(self.dev)
 
     def reset_counters(self):
@@ -211,14 +224,16 @@ class Engine:
             if out is not None:
                 abi.sparoa_conv2d_routed_measured(st["desc"], self.s_thr, self.c_thr, self.mode,
                                                   counts, x, st["w"], None, res, L.act, mask, y,
-                                                  out["counts"], out["mask"], st["ws"], st["path"])
+                                                  out["counts"], out["mask"], st["ws"], st["path"],
+                                                  out["commit"])
             else:
                 abi.sparoa_conv2d_routed(st["desc"], self.s_thr, self.c_thr, self.mode, counts, x,
                                          st["w"], None, res, L.act, mask, y, st["ws"], st["path"])
         elif out is not None:
             abi.sparoa_fc_routed_measured(st["desc"], self.s_thr, self.c_thr, self.mode, counts, x,
                                           st["w"], st.get("wp"), None, res, L.act, mask, y,
-                                          out["counts"], out["mask"], st["ws"], st["path"])
+                                          out["counts"], out["mask"], st["ws"], st["path"],
+                                          out["commit"])
         else:
             abi.sparoa_fc_routed(st["desc"], self.s_thr, self.c_thr, self.mode, counts, x,
                                  st["w"], st.get("wp"), None, res, L.act, mask, y, st["ws"],

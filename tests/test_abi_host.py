@@ -4,6 +4,8 @@ bit, and argument validation rejects bad calls before any device work."""
 import os
 import re
 
+import ctypes
+
 import numpy as np
 import pytest
 
@@ -28,7 +30,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert abi.sparoa_abi_version() == 2
+    assert abi.sparoa_abi_version() == 3
     assert abi.sparoa_status_string(0) == "ok"
     assert abi.sparoa_status_string(3) == "workspace too small"
 
@@ -216,3 +218,44 @@ def test_executor_chained_batch_without_events_fails_cleanly_without_a_gpu():
     arr = (abi.FcOp * 2)(*ops)
     st = abi._L.sparoa_fc_ops_run(arr, 2, None, None, None)
     assert st == 4, abi._L.sparoa_last_error()
+
+
+def _fake_op(d, base, t, ws_bytes=1 << 26, w_nk=True):
+    """An FC op whose device pointers are distinct fake addresses."""
+    a = [base + (i << 28) for i in range(9)]
+    return abi.FcOp(d, a[0], a[1] if w_nk else None, a[2], None, None, abi.ACT_RELU, a[3], a[4],
+                    a[5], a[6], ws_bytes, a[7], t)
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"),
+                    reason="host-only check: the fake device pointers must never reach a GPU")
+@pytest.mark.parametrize("bad", ["workspace", "w_nk"])
+def test_executor_validates_every_op_before_any_launch(bad):
+    """A batch whose second op fails validation launches nothing: the call
+    reports that op's validation error (with no GPU present, any launch
+    before it would have reported a HIP error instead)."""
+    d = abi.fc_desc(64, 4096, 4096, abi.BF16)
+    t = abi.Thresholds(0.5, 0.0, abi.ROUTE_BLOCK)            # MFMA family: split-K workspace
+    need = abi.sparoa_fc_workspace_size(d, abi.PATH_SKIP_MFMA)
+    assert need > 0
+    op1 = _fake_op(d, 0x2000000000, t, ws_bytes=need - 16) if bad == "workspace" else \
+        _fake_op(d, 0x2000000000, t, w_nk=False)
+    arr = (abi.FcOp * 2)(_fake_op(d, 0x1000000000, t), op1)
+    st = abi._L.sparoa_fc_ops_run(arr, 2, None, None, None)
+    assert st == (3 if bad == "workspace" else 1), abi._L.sparoa_last_error()
+    assert b"op 1" in abi._L.sparoa_last_error()
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"),
+                    reason="host-only check: the fake device pointers must never reach a GPU")
+def test_measured_fc_validates_before_measuring():
+    """sparoa_fc_measured checks the routed FC's workspace before it launches
+    the measurement of x."""
+    d = abi.fc_desc(64, 4096, 4096, abi.BF16)
+    need = abi.sparoa_fc_workspace_size(d, abi.PATH_SKIP_MFMA)
+    with pytest.raises(abi.SparoaError) as e:
+        abi._check(abi._L.sparoa_fc_measured(
+            ctypes.byref(d), ctypes.byref(abi.Thresholds(0.5, 0.0, abi.ROUTE_BLOCK)),
+            0x1000000000, 0x1100000000, None, None, None, abi.ACT_NONE, 0x1200000000,
+            0x1300000000, 0x1400000000, 0x1500000000, need - 16, None, None))
+    assert e.value.status == 3

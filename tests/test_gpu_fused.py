@@ -63,10 +63,12 @@ def test_conv_routed_measured(case):
     counts = torch.zeros(4, dtype=torch.int64, device=dev)
     mask = torch.zeros(abi.sparoa_mask_words(n * h * w, cin, 1, 8), dtype=torch.int32, device=dev)
     abi.sparoa_measure_sparsity(x, n * h * w, cin, 1, 8, 0, counts, mask)
-    ws = torch.zeros(max(16, max(abi.sparoa_conv2d_workspace_size(d, q) for q in range(4))),
-                     dtype=torch.uint8, device=dev)
+    # workspace contents on entry do not matter
+    ws = torch.full((max(16, max(abi.sparoa_conv2d_workspace_size(d, q) for q in range(4))),),
+                    0xA5, dtype=torch.uint8, device=dev)
+    commit = torch.zeros(abi.COMMIT_WORDS_BYTES // 8, dtype=torch.int64, device=dev)
     rows, cols = n * ho * wo, cout
-    # the GEMM measures y itself (count-commit words at the workspace's end)
+    # the GEMM measures y itself (ticketed commits through `commit`)
     fused = dt != "f32" and cin % 64 == 0 and cout % 64 == 0
     for s_thr in (0.0, 2.0):       # skip and dense routes
         y = torch.full((n, ho, wo, cout), float("nan"), dtype=tdt, device=dev)
@@ -75,7 +77,8 @@ def test_conv_routed_measured(case):
                             device=dev)
         path = torch.full((1,), -1, dtype=torch.int32, device=dev)
         abi.sparoa_conv2d_routed_measured(d, s_thr, 0.0, abi.ROUTE_BLOCK, counts, x, wt, b, r,
-                                          abi.ACT_RELU, mask, y, y_counts, y_mask, ws, path)
+                                          abi.ACT_RELU, mask, y, y_counts, y_mask, ws, path,
+                                          commit)
         y2 = torch.full_like(y, float("nan"))
         p2 = torch.full((1,), -1, dtype=torch.int32, device=dev)
         abi.sparoa_conv2d_routed(d, s_thr, 0.0, abi.ROUTE_BLOCK, counts, x, wt, b, r,
@@ -84,18 +87,17 @@ def test_conv_routed_measured(case):
         assert int(path.item()) == int(p2.item())
         assert torch.equal(y, y2), f"{case} s_thr {s_thr}"
         _check_y_measurement(abi, y, rows, cols, y_counts, y_mask, f"{case} s_thr {s_thr}")
-        if fused:   # the count-commit words are left zero for the next call
-            assert int(ws[-2048:].count_nonzero().item()) == 0
-    if fused:       # a workspace without the commit words: direct commits, same counts
-        small = ws[:ws.numel() - 2048] if ws.numel() > 2048 else None
+        # the count-commit words are left zero for the next call
+        assert int(commit.count_nonzero().item()) == 0
+    if fused:       # no commit words: direct commits, same counts
         y = torch.full((n, ho, wo, cout), float("nan"), dtype=tdt, device=dev)
         y_counts = _fresh_counts(rows, cols, dev)
         y_mask = torch.full((abi.sparoa_mask_words(rows, cols, 1, 8),), -1, dtype=torch.int32,
                             device=dev)
         abi.sparoa_conv2d_routed_measured(d, 0.0, 0.0, abi.ROUTE_BLOCK, counts, x, wt, b, r,
-                                          abi.ACT_RELU, mask, y, y_counts, y_mask, small)
+                                          abi.ACT_RELU, mask, y, y_counts, y_mask, ws)
         torch.cuda.synchronize()
-        _check_y_measurement(abi, y, rows, cols, y_counts, y_mask, f"{case} small workspace")
+        _check_y_measurement(abi, y, rows, cols, y_counts, y_mask, f"{case} direct commits")
 
 
 FC_CASES = [
@@ -126,27 +128,73 @@ def test_fc_routed_measured(case):
     counts = torch.zeros(4, dtype=torch.int64, device=dev)
     mask = torch.zeros(abi.sparoa_mask_words(m, k, br, bc), dtype=torch.int32, device=dev)
     abi.sparoa_measure_sparsity(x, m, k, br, bc, 0, counts, mask)
-    ws = torch.zeros(max(16, max(abi.sparoa_fc_workspace_size(d, q) for q in range(4))),
-                     dtype=torch.uint8, device=dev)
+    ws = torch.full((max(16, max(abi.sparoa_fc_workspace_size(d, q) for q in range(4))),),
+                    0x5A, dtype=torch.uint8, device=dev)
+    commit = torch.zeros(abi.COMMIT_WORDS_BYTES // 8, dtype=torch.int64, device=dev)
     y = torch.full((m, n), float("nan"), dtype=tdt, device=dev)
     y_counts = _fresh_counts(m, n, dev)
     y_mask = torch.full((abi.sparoa_mask_words(m, n, 1, 8),), -1, dtype=torch.int32, device=dev)
     abi.sparoa_fc_routed_measured(d, 0.5, c_thr, abi.ROUTE_BLOCK, counts, x, w, wp, None, None,
-                                  abi.ACT_RELU, mask, y, y_counts, y_mask, ws)
+                                  abi.ACT_RELU, mask, y, y_counts, y_mask, ws, None, commit)
     y2 = torch.full_like(y, float("nan"))
     abi.sparoa_fc_routed(d, 0.5, c_thr, abi.ROUTE_BLOCK, counts, x, w, wp, None, None,
                          abi.ACT_RELU, mask, y2, ws)
     torch.cuda.synchronize()
     assert torch.equal(y, y2)
     _check_y_measurement(abi, y, m, n, y_counts, y_mask, str(case))
-    if c_thr == 0.0 and n % 64 == 0:   # fused: commit words left zero; direct commits
-        assert int(ws[-2048:].count_nonzero().item()) == 0
-        small = ws[:ws.numel() - 2048] if ws.numel() > 2048 else None
+    assert int(commit.count_nonzero().item()) == 0     # commit words left zero
+    if c_thr == 0.0 and n % 64 == 0:   # fused, no commit words: direct commits
         y_counts = _fresh_counts(m, n, dev)
         abi.sparoa_fc_routed_measured(d, 0.5, c_thr, abi.ROUTE_BLOCK, counts, x, w, wp, None,
-                                      None, abi.ACT_RELU, mask, y, y_counts, y_mask, small)
+                                      None, abi.ACT_RELU, mask, y, y_counts, y_mask, ws)
         torch.cuda.synchronize()
-        _check_y_measurement(abi, y, m, n, y_counts, y_mask, f"{case} small workspace")
+        _check_y_measurement(abi, y, m, n, y_counts, y_mask, f"{case} direct commits")
+
+
+def test_shared_workspace_split_k_then_fused():
+    """One workspace serves a split-K layer (its partial sums fill the
+    workspace) and then a layer whose epilogue measures its output with
+    ticketed commits: the second layer's counts and bitmap still equal the
+    oracle's measurement of its output (the commit words are an argument of
+    their own, never workspace bytes)."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    d1 = abi.fc_desc(64, 4096, 4096, abi.BF16)        # split-K
+    d2 = abi.conv_desc(8, 64, 32, 32, 128, 3, 3, 1, 1, 1, 1, 1, 1, 1, torch.bfloat16)
+    assert abi.sparoa_fc_workspace_size(d1, abi.PATH_SKIP_MFMA) > 0
+    ws = torch.full((max(abi.sparoa_fc_workspace_size(d1, abi.PATH_SKIP_MFMA),
+                         abi.sparoa_conv2d_workspace_size(d2, abi.PATH_SKIP_MFMA), 16),),
+                    0xFF, dtype=torch.uint8, device=dev)
+    commit = torch.zeros(abi.COMMIT_WORDS_BYTES // 8, dtype=torch.int64, device=dev)
+    x1 = synth.sparse_matrix(64, 4096, 0.5, "block", "bf16", 1290).to(dev)
+    w1 = synth.normal((4096, 4096), "bf16", 1291, std=1 / 64).to(dev)
+    c1 = torch.zeros(4, dtype=torch.int64, device=dev)
+    m1 = torch.zeros(abi.sparoa_mask_words(64, 4096, 1, 8), dtype=torch.int32, device=dev)
+    abi.sparoa_measure_sparsity(x1, 64, 4096, 1, 8, 0, c1, m1)
+    y1 = torch.empty(64, 4096, dtype=torch.bfloat16, device=dev)
+    y1_counts = _fresh_counts(64, 4096, dev)
+    y1_mask = torch.zeros(abi.sparoa_mask_words(64, 4096, 1, 8), dtype=torch.int32, device=dev)
+    x2 = synth.relu_normal((8, 32, 32, 64), "bf16", 1292).to(dev)
+    w2 = synth.he_normal((128, 3, 3, 64), 576, "bf16", 1293).to(dev)
+    c2 = torch.zeros(4, dtype=torch.int64, device=dev)
+    m2 = torch.zeros(abi.sparoa_mask_words(8 * 32 * 32, 64, 1, 8), dtype=torch.int32, device=dev)
+    abi.sparoa_measure_sparsity(x2, 8 * 32 * 32, 64, 1, 8, 0, c2, m2)
+    y2 = torch.empty(8, 32, 32, 128, dtype=torch.bfloat16, device=dev)
+    for rep in range(2):
+        y1_counts.copy_(_fresh_counts(64, 4096, dev))
+        y2_counts = _fresh_counts(8 * 32 * 32, 128, dev)
+        y2_mask = torch.full((abi.sparoa_mask_words(8 * 32 * 32, 128, 1, 8),), -1,
+                             dtype=torch.int32, device=dev)
+        abi.sparoa_fc_routed_measured(d1, 0.5, 0.0, abi.ROUTE_BLOCK, c1, x1, w1, None, None, None,
+                                      abi.ACT_RELU, m1, y1, y1_counts, y1_mask, ws, None, commit)
+        abi.sparoa_conv2d_routed_measured(d2, 0.5, 0.0, abi.ROUTE_BLOCK, c2, x2, w2, None, None,
+                                          abi.ACT_RELU, m2, y2, y2_counts, y2_mask, ws, None,
+                                          commit)
+        torch.cuda.synchronize()
+        _check_y_measurement(abi, y1, 64, 4096, y1_counts, y1_mask, f"split-K layer, rep {rep}")
+        _check_y_measurement(abi, y2, 8 * 32 * 32, 128, y2_counts, y2_mask,
+                             f"fused layer after it, rep {rep}")
+        assert int(commit.count_nonzero().item()) == 0
 
 
 def test_measured_calls_reject_missing_outputs():

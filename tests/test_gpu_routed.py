@@ -342,6 +342,36 @@ def test_fc_ops_run_batched_equals_op_by_op():
     assert torch.equal(y2, y_chain)
 
 
+def test_fc_ops_run_shared_scratch_runs_in_order():
+    """Ops that share their counts, mask and split-K workspace (valid one op
+    after another) are detected and run in order: each output equals a
+    private op-by-op call's, and the shared counts hold the last op's."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    d = abi.fc_desc(64, 4096, 1024, abi.BF16)
+    thr = (0.5, 0.0, abi.ROUTE_BLOCK)              # MFMA family: split-K partials
+    assert abi.sparoa_fc_workspace_size(d, abi.PATH_SKIP_MFMA) > 0
+    shared = _batch_op(abi, dev, d, synth.sparse_matrix(64, 4096, 0.3, "block", "bf16", 640).to(dev),
+                       740, thr=thr[:2])
+    bufs = []
+    for i in range(3):
+        x = synth.sparse_matrix(64, 4096, 0.2 + 0.3 * i, "block", "bf16", 641 + i).to(dev)
+        bufs.append(_batch_op(abi, dev, d, x, 741 + i, thr=thr[:2]))
+    ops = [abi.fc_op(b["d"], b["x"], b["w"], b["wp"], None, None, abi.ACT_RELU, shared["counts"],
+                     shared["mask"], b["y"], shared["ws"], b["path"], thr) for b in bufs]
+    abi.sparoa_fc_ops_run(abi.fc_op_array(ops))
+    torch.cuda.synchronize()
+    for i, b in enumerate(bufs):
+        c2 = torch.zeros_like(b["counts"])
+        y2 = torch.full_like(b["y"], float("nan"))
+        abi.sparoa_fc_measured(b["d"], thr[0], thr[1], abi.ROUTE_BLOCK, b["x"], b["w"], b["wp"],
+                               None, None, abi.ACT_RELU, c2, b["mask"], y2, b["ws"])
+        torch.cuda.synchronize()
+        assert torch.equal(y2, b["y"]), f"op {i}"
+        if i == len(bufs) - 1:
+            assert torch.equal(c2, shared["counts"])
+
+
 def test_fc_ops_run_grouped_streaming_equals_op_by_op():
     """Self-measuring streaming FCs run as grouped launches (one per dtype,
     at most 16 ops each): 22 ops in 3 launches, m from 1 to 64 (ragged, up to
