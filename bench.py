@@ -42,6 +42,7 @@ PATTERNS = ("iid", "block")
 K = N = 4096
 INTENSITY_THR = 315.0   # bf16 ridge point of MI355X: 2.5 PFLOP/s / 8 TB/s (datasheet)
 SKIP_MARGIN = 0.97      # calibration: a skip path must beat dense by 3 % to count as a win
+THRESHOLDS_FILE = os.path.join(ROOT, "calibration", "fc_sweep_thresholds.json")
 
 
 def parse():
@@ -53,8 +54,16 @@ def parse():
                    help="bound on the oracle CPU-baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--thresholds", default=None,
-                   help='JSON {m: [sparsity_thr, intensity_thr]}; default: calibrated from the '
-                        'cold forced-path timings')
+                   help='JSON {m: [sparsity_thr, intensity_thr]}, or a file holding it (or a '
+                        'calibration record with "thresholds_per_m"); default: the committed '
+                        'calibration/fc_sweep_thresholds.json')
+    p.add_argument("--calibrate", action="store_true",
+                   help="calibrate the thresholds from this run's forced-path timings instead "
+                        "of reading them")
+    p.add_argument("--calibrate-out", default=None, metavar="FILE",
+                   help="with --calibrate: write the thresholds and the timings they come from")
+    p.add_argument("--no-layers", action="store_true",
+                   help="skip the per-layer tables of the model stacks")
     p.add_argument("--cases-out", default=None, help="write the per-case table (JSON) here")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only run 5 plain device-to-device copies of MIB MiB and exit (the "
@@ -546,6 +555,18 @@ def model_latencies(abi, torch, synth, reps=10):
     return out
 
 
+def load_thresholds(arg):
+    """Thresholds per operator class {m: (sparsity_thr, intensity_thr)} from a
+    JSON object, or from a file holding one or a calibration record."""
+    text = arg
+    if not arg.lstrip().startswith("{"):
+        with open(arg) as f:
+            text = f.read()
+    obj = json.loads(text)
+    obj = obj.get("thresholds_per_m", obj)
+    return {int(k): (float(v[0]), float(v[1])) for k, v in obj.items()}
+
+
 def calibrate(abi, cases, batch=None):
     """Thresholds per operator class (m): the kernel family whose dense path
     is faster -- over the class's operators issued as one executor batch when
@@ -602,6 +623,296 @@ def cpu_baseline_timed(cases, budget_s):
     return flops, elapsed, done
 
 
+# ---------------------------------------------------------------------------
+# Single 3x3 conv workload, per-layer tables of the model stacks, and the
+# oracle's CPU timings beside them.
+
+FP32_PEAK_TFLOPS = 157.3
+MFMA16_PEAK_TFLOPS = 2500.0
+
+
+def _roof_us(flops, nbytes, dtype_bits):
+    """Roofline time (us) of an operator: max of its flops at the dtype's
+    dense peak and its compulsory bytes at the HBM peak."""
+    peak = FP32_PEAK_TFLOPS if dtype_bits == 32 else MFMA16_PEAK_TFLOPS
+    return max(flops / (peak * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)) * 1e6
+
+
+def _graph_us(torch, fn, reps):
+    """Median duration (us) of `fn` captured once in a HIP graph and replayed
+    `reps` times, HIP events around every replay."""
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g):
+            fn()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e3)
+    del g
+    return sorted(ts)[len(ts) // 2]
+
+
+def _queued_us(torch, fn, reps, cyc):
+    """Median GPU time (us) of the kernels `fn` enqueues: a spin kernel first,
+    so the host has enqueued all of them before the GPU reaches the first of
+    the two HIP events around them."""
+    ts = []
+    for _ in range(reps):
+        torch.cuda._sleep(cyc)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e3)
+    return sorted(ts)[len(ts) // 2]
+
+
+def config1_single_conv(abi, torch, synth, reps=50):
+    """The single 3x3 conv workload: x = ReLU(N(0,1)) fp32 [1,56,56,64]
+    (NHWC), w ~ N(0, 2/576) [64,3,3,64], bias 0.  Timed: the whole path
+    (zero count and bitmap of x, device-side route, routed conv) and its
+    parts, each as a HIP graph replayed `reps` times (median).  Launch-latency
+    bound at this size: reported in us, with the fp32 roofline for context."""
+    dev = torch.device("cuda")
+    d = abi.conv_desc(1, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, dtype=abi.F32)
+    x = synth.relu_normal((1, 56, 56, 64), "f32", synth.seed_for(1, 0)).to(dev)
+    w = synth.he_normal((64, 3, 3, 64), 576, "f32", synth.seed_for(1, 1)).to(dev)
+    inten = abi.sparoa_op_intensity_conv(d)
+    counts = torch.zeros(4, dtype=torch.int64, device=dev)
+    mask = torch.zeros(abi.sparoa_mask_words(56 * 56, 64, 1, 8), dtype=torch.int32, device=dev)
+    ws = torch.empty(max(16, max(abi.sparoa_conv2d_workspace_size(d, p) for p in range(4))),
+                     dtype=torch.uint8, device=dev)
+    y = torch.empty(1, 56, 56, 64, dtype=torch.float32, device=dev)
+    path = torch.zeros(1, dtype=torch.int32, device=dev)
+    s_thr, c_thr = 0.5, 20.0          # fp32 ridge point: 157.3 TFLOP/s / 8 TB/s
+
+    def measure():
+        abi.sparoa_measure_sparsity(x, 56 * 56, 64, 1, 8, 0, counts, mask)
+
+    def whole():
+        measure()
+        abi.sparoa_conv2d_routed(d, s_thr, c_thr, abi.ROUTE_BLOCK, counts, x, w, None, None,
+                                 abi.ACT_NONE, mask, y, ws, path)
+
+    def conv_dense():
+        abi.sparoa_conv2d(d, abi.PATH_DENSE_MFMA, x, w, None, None, abi.ACT_NONE, None, y, ws)
+
+    cyc = _sleep_cycles(torch)
+    whole_us = _queued_us(torch, whole, reps, cyc)
+    meas_us = _queued_us(torch, measure, reps, cyc)
+    conv_us = _queued_us(torch, conv_dense, reps, cyc)
+    graph_us = _graph_us(torch, whole, reps)
+    c = dict(zip(("zeros", "numel", "zero_blocks", "num_blocks"), counts.cpu().tolist()))
+    roof = _roof_us(inten["flops"], inten["bytes"], 32)
+    return dict(workload="single 3x3 conv, x ReLU(N(0,1)) fp32 [1,56,56,64] NHWC, w N(0,2/576) "
+                         "[64,3,3,64], bias 0; measure + device route + conv",
+                path=abi.PATH_NAMES[int(path.item())], zeros=c["zeros"], numel=c["numel"],
+                macs=inten["macs"], bytes=inten["bytes"], intensity=round(inten["intensity"], 3),
+                whole_path_us=round(whole_us, 2), measure_us=round(meas_us, 2),
+                conv_dense_us=round(conv_us, 2),
+                conv_tflops=round(inten["flops"] / conv_us / 1e6, 2),
+                fp32_roofline_us=round(roof, 3), conv_roofline_frac=round(roof / conv_us, 4),
+                whole_path_graph_replay_us=round(graph_us, 2),
+                timing=f"each piece queued behind a spin kernel, HIP events around it, median of "
+                       f"{reps} (warm); whole_path_graph_replay_us: the whole path as one HIP "
+                       f"graph, events around each replay (includes the graph launch)")
+
+
+def _sleep_cycles(torch):
+    """A torch.cuda._sleep argument that keeps the GPU busy for about 300 us
+    (long enough for the host to enqueue a whole layer behind it)."""
+    n = 100000
+    for _ in range(12):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        torch.cuda._sleep(n)
+        e1.record()
+        e1.synchronize()
+        us = e0.elapsed_time(e1) * 1e3
+        if us >= 300.0:
+            return n
+        n = int(n * max(2.0, 330.0 / max(us, 1.0)))
+    return n
+
+
+def layer_table(abi, torch, synth, name, layers, dtype, reps=5):
+    """Per layer of one model stack: its routed path alone (input measurement
+    where not fused in its producer, device route, kernel, output
+    measurement where fused), timed after a full routed pass has left every
+    activation and counter in place.  Each rep restores the counters the
+    layer reads and writes to their values before the layer, then (cold
+    mode) overwrites a 512 MiB buffer to evict the Infinity Cache, queues a
+    spin kernel so the host has enqueued the whole layer before the GPU
+    reaches the first event, and brackets the layer with HIP events.  Median
+    of `reps` per mode.  Algorithmic bytes and flops are the layer's Eq. 2
+    figures (compulsory traffic of input, weights and output; 2 * MACs)."""
+    from paper_2511_19457_amd.driver import Engine
+    from paper_2511_19457_amd.stacks import input_shape, output_shape
+    eng = Engine(layers, dtype, "cuda", seed=synth.seed_for(3, 0), sparsity_thr=0.5)
+    x = synth.normal(input_shape(layers), dtype, synth.seed_for(3, 1)).cuda()
+    eng.forward_routed(x)
+    torch.cuda.synchronize()
+    recs = eng.records_from_device()
+    final = eng.ctr.clone()
+    tmpl = eng.ctr_template
+    base = eng.ctr.data_ptr()
+    bits = 32 if dtype == torch.float32 else 16
+    esz = bits // 8
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    cyc = _sleep_cycles(torch)
+    rows = []
+    for i, L in enumerate(layers):
+        pre = final.clone()
+        if L.kind != "maxpool":
+            pre[i] = tmpl[i]                       # the layer's own input-measurement counters
+        out = eng.tmeas.get(i + 1)
+        if out is not None:                        # its fused / standalone output counters
+            r = (out["counts"].data_ptr() - base) // (16 * 8)
+            pre[r] = tmpl[r]
+        times = {}
+        for mode in ("warm", "cold"):
+            ts = []
+            for _ in range(reps):
+                eng.ctr.copy_(pre)
+                if mode == "cold":
+                    scrub.fill_(len(ts) & 255)
+                torch.cuda._sleep(cyc)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                eng.run_layer_routed(i)
+                e1.record()
+                e1.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e3)
+            times[mode] = sorted(ts)[len(ts) // 2]
+        rec = recs[i]
+        if L.kind == "maxpool":
+            s = L.shape
+            n_in = s["n"] * s["h"] * s["w"] * s["c"]
+            oshape = output_shape(L)
+            n_out = oshape[0] * oshape[1] * oshape[2] * oshape[3]
+            flops, nbytes, path, inten = 0, (n_in + n_out) * esz, "glue", 0.0
+        else:
+            assert int(eng.st[i]["path"].item()) == rec.path, (name, L.name, "path changed")
+            flops, nbytes = 2 * rec.macs, rec.bytes
+            path, inten = abi.PATH_NAMES[rec.path], rec.intensity
+        roof = _roof_us(flops, nbytes, bits)
+        bound = "mfma" if flops and inten >= (315.0 if bits == 16 else 20.0) else "hbm"
+        t = times["warm"] if bound == "mfma" else times["cold"]
+        rows.append(dict(layer=L.name, kind=L.kind, rho_e=round(rec.rho_e, 4),
+                         rho_b=round(rec.rho_b, 4), intensity=round(inten, 2), path=path,
+                         us_warm=round(times["warm"], 2), us_cold=round(times["cold"], 2),
+                         gbps=round(nbytes / t / 1e3, 1), tflops=round(flops / t / 1e6, 2),
+                         bound=bound, roofline_frac=round(roof / t, 4)))
+    del eng, x, scrub
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    tot_w = sum(r["us_warm"] for r in rows)
+    return dict(rows=rows, sum_us_warm=round(tot_w, 1),
+                sum_us_cold=round(sum(r["us_cold"] for r in rows), 1),
+                timing=("each layer alone after a full routed pass, HIP events after a spin "
+                        "kernel; median of %d reps; warm = back to back, cold = after a 512 MiB "
+                        "overwrite; roofline_frac and rates use the warm time for layers at or "
+                        "above the ridge point (mfma) and the cold time otherwise (hbm)" % reps))
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_timings(torch, synth, budget_s=8.0):
+    """The oracle (plain C, double precision) on the host cores, one core and
+    all cores: the single 3x3 conv in full, and sampled outputs of
+    representative layers of the three stacks (conv2d_at on seeded output
+    offsets), scaled to each stack's whole pass by its MAC count.  A baseline
+    only (no BLAS, no vectorisation)."""
+    import oracle
+    from paper_2511_19457_amd import stacks
+    all_cores = oracle.set_threads(0)
+    out = dict(cpu_model=cpu_model(), nproc=os.cpu_count(), threads_all_cores=all_cores)
+    x1 = synth.relu_normal((1, 56, 56, 64), "f32", synth.seed_for(1, 0))
+    w1 = synth.he_normal((64, 3, 3, 64), 576, "f32", synth.seed_for(1, 1))
+    cfg1 = {}
+    for label, nt in (("one_core", 1), ("all_cores", all_cores)):
+        oracle.set_threads(nt)
+        t0 = time.perf_counter()
+        _, _, macs = oracle.conv2d(x1, w1, 1, 64, 56, 56, 64, 3, 3, ph=1, pw=1)
+        cfg1[label + "_s"] = round(time.perf_counter() - t0, 3)
+    cfg1["macs"] = macs
+    out["single_conv"] = cfg1
+    specs = [("resnet50_b32_bf16", stacks.resnet50(32), torch.bfloat16,
+              ("s2b1.c2", "s3b2.c1", "s4b1.c3")),
+             ("mobilenet_v2_b32_fp16", stacks.mobilenet_v2(32), torch.float16,
+              ("b2.1.expand", "b2.1.dw", "b4.2.project")),
+             ("ffn12_2048x768_fp16", stacks.ffn(), torch.float16, ("ffn1.fc1", "ffn1.fc2"))]
+    for name, layers, dt, picks in specs:
+        pass_macs = 0
+        for L in layers:
+            s = L.shape
+            if L.kind == "conv":
+                ho = (s["h"] + 2 * s["ph"] - s["kh"]) // s["sh"] + 1
+                wo = (s["w"] + 2 * s["pw"] - s["kw"]) // s["sw"] + 1
+                pass_macs += s["n"] * ho * wo * s["cout"] * (s["cin"] // s["groups"]) * \
+                    s["kh"] * s["kw"]
+            elif L.kind == "fc":
+                pass_macs += s["m"] * s["k"] * s["n"]
+        res = dict(pass_macs=pass_macs, sampled_layers=list(picks))
+        for label, nt in (("one_core", 1), ("all_cores", all_cores)):
+            oracle.set_threads(nt)
+            macs_done, secs = 0, 0.0
+            for L in layers:
+                if L.name not in picks:
+                    continue
+                s = L.shape
+                if L.kind == "conv":    # one image: the MAC rate does not depend on the batch
+                    n, cin, h, w, cout, k = 1, s["cin"], s["h"], s["w"], s["cout"], s["kh"]
+                    ho = (h + 2 * s["ph"] - k) // s["sh"] + 1
+                    wo = (w + 2 * s["pw"] - k) // s["sw"] + 1
+                    cin_g = cin // s["groups"]
+                    x = synth.relu_normal((n, h, w, cin), dt, 77)
+                    wt = synth.he_normal((cout, k, k, cin_g), k * k * cin_g, dt, 78)
+                    total, per = n * ho * wo * cout, cin_g * k * k
+                    args = (n, cin, h, w, cout, k, k, s["sh"], s["sw"], s["ph"], s["pw"], 1, 1,
+                            s["groups"])
+                else:
+                    x = synth.relu_normal((s["m"], s["k"]), dt, 77)
+                    wt = synth.normal((s["n"], 1, 1, s["k"]), dt, 78)
+                    total, per = s["m"] * s["n"], s["k"]
+                    args = (s["m"], s["k"], 1, 1, s["n"], 1, 1)
+                count = max(256, min(total, int(4e7 / per / (8 if nt == 1 else 1))))
+                idx = synth.rng(79).integers(0, total, size=count)
+                t0 = time.perf_counter()
+                oracle.conv2d_at(x, wt, idx, *args)
+                secs += time.perf_counter() - t0
+                macs_done += count * per
+                if secs > budget_s:
+                    break
+            rate = macs_done / secs
+            res[label] = dict(mmac_per_s=round(rate / 1e6, 1),
+                              est_pass_s=round(pass_macs / rate, 1),
+                              sampled_macs=macs_done, seconds=round(secs, 2))
+        out[name] = res
+    oracle.set_threads(all_cores)
+    return out
+
+
 def main():
     args = parse()
     if args.profile_summary:
@@ -640,8 +951,15 @@ def main():
     # Forced-path timings per case (untimed phase, cold weights): the sparsity
     # sweep of the metric, and the data the thresholds are calibrated from.
     paths_swept = (abi.PATH_DENSE_BW, abi.PATH_SKIP_BW, abi.PATH_DENSE_MFMA, abi.PATH_SKIP_MFMA)
-    if args.thresholds is None and args.no_sweep:
-        print("bench.py: --no-sweep needs --thresholds", file=sys.stderr)
+    thr_source = args.thresholds
+    if thr_source is None and not args.calibrate:
+        if os.path.exists(THRESHOLDS_FILE):
+            thr_source = THRESHOLDS_FILE
+        else:
+            print(f"bench: {THRESHOLDS_FILE} missing: calibrating from this run", file=sys.stderr)
+    if thr_source is None and args.no_sweep:
+        print("bench.py: --no-sweep needs thresholds (--thresholds or the committed file)",
+              file=sys.stderr)
         sys.exit(2)
     batch_times = None
     if args.no_sweep:
@@ -651,8 +969,28 @@ def main():
         print("bench: forced-path sweep", file=sys.stderr, flush=True)
         forced_times(abi, torch, cases, paths_swept)
         batch_times = family_batch_times(abi, torch, cases)
-    thresholds = calibrate(abi, cases, batch_times) if args.thresholds is None else \
-        {int(k): tuple(v) for k, v in json.loads(args.thresholds).items()}
+    calibrated = calibrate(abi, cases, batch_times) if not args.no_sweep else None
+    thresholds = calibrated if thr_source is None else load_thresholds(thr_source)
+    if args.calibrate_out and calibrated is not None:
+        rec = dict(thresholds_per_m={str(k): list(v) for k, v in calibrated.items()},
+                   rule="per operator class m: kernel family by the faster dense path of the "
+                        "class's operators issued as one executor batch (intensity threshold = "
+                        "the class's intensity when the MFMA family wins, else the bf16 ridge "
+                        "point 315); sparsity threshold = the smallest block sparsity from "
+                        "which the family's skip path beats its dense path by more than 3 % "
+                        "in every case of the class (1.0 when it never does)",
+                   family_batch_us={f"m={m} {abi.PATH_NAMES[f]}": round(t, 2)
+                                    for (m, f), t in batch_times.items()},
+                   forced_path_us=[dict(m=c.m, rho=c.rho, pattern=c.pattern,
+                                        rho_b_bw=round(c.rho_b[abi.PATH_DENSE_BW], 4),
+                                        rho_b_mfma=round(c.rho_b[abi.PATH_DENSE_MFMA], 4),
+                                        **{abi.PATH_NAMES[p]: round(c.forced[p], 2)
+                                           for p in paths_swept}) for c in cases],
+                   source_digest=source_digest(),
+                   workload="FC sweep: x [m,4096] bf16, w [4096,4096] bf16, cold weights; whole "
+                            "path (sparoa_fc_measured) forced onto each path, best of 5")
+        with open(args.calibrate_out, "w") as f:
+            json.dump(rec, f, indent=1)
     for c in cases:
         c.s_thr, c.c_thr = thresholds[c.m]
     print(f"bench: warmup {args.warmup} steps, thresholds per m (sparsity, intensity): "
@@ -810,6 +1148,9 @@ def main():
                              "one weight matrix per operator; measure+route+execute each",
                     global_batch=sum(M_LIST) * len(RHO_LIST) * len(PATTERNS),
                     thresholds_per_m={str(k): v for k, v in thresholds.items()},
+                    thresholds_source=(os.path.relpath(thr_source, ROOT)
+                                       if thr_source and os.path.exists(thr_source) else
+                                       "command line" if thr_source else "calibrated in this run"),
                     route_mode="block", issue=args.mode),
         hbm_gbps_step=round(tot_bytes / step_s / 1e9, 1),
         step_gpu_us=round(step_gpu_us, 2),
@@ -821,15 +1162,35 @@ def main():
     )
     if not args.no_models:
         line["models"] = model_latencies(abi, torch, synth)
+        print("bench: single 3x3 conv", file=sys.stderr, flush=True)
+        line["single_conv"] = config1_single_conv(abi, torch, synth)
+    if not args.no_models and not args.no_layers:
+        from paper_2511_19457_amd import stacks
+        line["layers"] = {}
+        for name, layers, dt in (("resnet50_b32_bf16", stacks.resnet50(32), torch.bfloat16),
+                                 ("mobilenet_v2_b32_fp16", stacks.mobilenet_v2(32), torch.float16),
+                                 ("ffn12_2048x768_fp16", stacks.ffn(), torch.float16)):
+            print(f"bench: per-layer table {name}", file=sys.stderr, flush=True)
+            line["layers"][name] = layer_table(abi, torch, synth, name, layers, dt)
     if not args.no_cpu_baseline:
+        import oracle
         print("bench: oracle CPU baseline", file=sys.stderr, flush=True)
+        cores = oracle.set_threads(0)
         flops, elapsed, done = cpu_baseline_timed(cases, args.cpu_seconds)
-        cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        oracle.set_threads(1)
+        flops1, elapsed1, done1 = cpu_baseline_timed(cases, args.cpu_seconds / 4)
+        oracle.set_threads(cores)
         line["cpu_baseline"] = dict(
             value=round(flops / elapsed / 1e12, 6), unit="TFLOP/s", cores=cores, kind="oracle",
             sample=f"first {len(done)} of 24 sweep operators in case order "
                    f"({done[0]} .. {done[-1]}): oracle measure + route + FC in double, "
-                   f"{elapsed:.1f} s")
+                   f"{elapsed:.1f} s",
+            one_core=dict(value=round(flops1 / elapsed1 / 1e12, 6), unit="TFLOP/s",
+                          sample=f"first {len(done1)} sweep operators, {elapsed1:.1f} s"),
+            cpu_model=cpu_model(), nproc=os.cpu_count())
+        if not args.no_models:
+            print("bench: oracle timings of the other workloads", file=sys.stderr, flush=True)
+            line["oracle_timings"] = oracle_timings(torch, synth)
     else:
         line["cpu_baseline"] = None
     if args.cases_out:

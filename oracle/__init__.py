@@ -72,6 +72,8 @@ def lib():
         L.or_conv_split_executed_blocks.argtypes = ([_vp, ctypes.c_int] + [_i64] * 14 +
                                                     [ctypes.c_double, _u64p])
         L.or_maxpool2d.argtypes = [_i64] * 7 + [ctypes.c_int, _vp, _dp]
+        L.or_set_threads.restype = ctypes.c_int
+        L.or_set_threads.argtypes = [ctypes.c_int]
         _lib = L
     return _lib
 
@@ -265,6 +267,12 @@ def conv_split_executed_blocks(x, n, cin, h, w, kh, kw, sh, sw, ph, pw, dh, dw, 
                                                pw, dh, dw, tile_rows, block_c, sparsity_thr,
                                                ctypes.byref(out)), "conv_split_executed_blocks")
     return out.value
+
+
+def set_threads(n=0):
+    """Threads of the oracle's OpenMP loops (n <= 0: unchanged); returns the
+    count in effect."""
+    return lib().or_set_threads(int(n))
 
 
 def maxpool2d(x, n, c, h, w, k=3, s=2, p=1):

@@ -36,6 +36,7 @@
  * is not available).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -598,4 +599,14 @@ int or_maxpool2d(int64_t n, int64_t c, int64_t h, int64_t w, int64_t k, int64_t 
           y_out[((in * ho_n + oh) * wo_n + ow) * c + ch] = best;
         }
   return OR_OK;
+}
+
+/*
+ * Threads of the OpenMP loops above (the CPU-baseline columns time the same
+ * loops on one core and on every core).  n <= 0 leaves the setting alone.
+ * Returns the thread count now in effect.
+ */
+int or_set_threads(int n) {
+  if (n > 0) omp_set_num_threads(n);
+  return omp_get_max_threads();
 }
