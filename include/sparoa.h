@@ -472,6 +472,26 @@ sparoa_status sparoa_fc_ops_run(const sparoa_fc_op *ops, int64_t n, const sparoa
 
 
 /* ------------------------------------------------------------------------
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: the same
+ * convolution as sparoa_conv2d (same validation, kernels and output, bit for
+ * bit) with no workspace argument.  The split-K partial sums live in a
+ * library-owned device array of SPAROA_NOALLOC_SCRATCH_BYTES per GPU,
+ * allocated when the library's code object loads and held until the process
+ * ends; the call allocates nothing (no hipMalloc, hipFree or allocating
+ * library routine).  The array's contents on entry do not matter.
+ * Calls that overlap in time on one GPU (other streams, other host threads)
+ * share that GPU's array and race; calls ordered on one stream do not.
+ * Errors: those of sparoa_conv2d; SPAROA_ERR_WORKSPACE when the shape's
+ * split-K partial sums (sparoa_conv2d_workspace_size) exceed the array.
+ * ---------------------------------------------------------------------- */
+#define SPAROA_NOALLOC_SCRATCH_BYTES (8u << 20)
+sparoa_status sparoa_conv2d_noalloc(const sparoa_conv_desc *desc, sparoa_path path, const void *x,
+                                    const void *w, const void *bias, const void *residual,
+                                    sparoa_act act, const uint32_t *mask, void *y,
+                                    uint64_t *executed_blocks_dev, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Network glue (not routed): NHWC max pooling, window k, stride s, padding p.
  * ---------------------------------------------------------------------- */
 sparoa_status sparoa_maxpool2d(const void *x, sparoa_dtype dtype, int64_t n, int64_t c,

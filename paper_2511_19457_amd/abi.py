@@ -34,6 +34,7 @@ EXPORTS = [
     "sparoa_fc_routed", "sparoa_fc_uses_packed", "sparoa_fc_ops_run",
     "sparoa_fc_measured", "sparoa_conv2d_routed_measured", "sparoa_fc_routed_measured",
     "sparoa_conv2d_split", "sparoa_fc_split", "sparoa_measure_sparsity_preset",
+    "sparoa_conv2d_noalloc",
 ]
 
 
@@ -112,6 +113,8 @@ def _load():
                                          vp, vp, vp, sz, vp, vp]),
         "sparoa_conv2d_dense": (ctypes.c_int, [P(ConvDesc), vp, vp, vp, vp, ctypes.c_int, vp, vp,
                                                sz, vp]),
+        "sparoa_conv2d_noalloc": (ctypes.c_int, [P(ConvDesc), ctypes.c_int, vp, vp, vp, vp,
+                                                 ctypes.c_int, vp, vp, vp, vp]),
         "sparoa_conv2d_zero_skip": (ctypes.c_int, [P(ConvDesc), vp, vp, vp, vp, ctypes.c_int, vp,
                                                    vp, vp, sz, vp, vp]),
         "sparoa_fc_packed_bytes": (ctypes.c_int, [P(FcDesc), P(sz)]),
@@ -298,6 +301,14 @@ def sparoa_conv2d(desc, path, x, w, bias, residual, act, mask, y, workspace=None
     _check(_L.sparoa_conv2d(ctypes.byref(desc), path, _ptr(x), _ptr(w), _ptr(bias),
                             _ptr(residual), act, _ptr(mask), _ptr(y), _ptr(workspace), ws_bytes,
                             _ptr(executed), _stream(stream)))
+
+
+def sparoa_conv2d_noalloc(desc, path, x, w, bias, residual, act, mask, y, executed=None,
+                          stream=None):
+    """sparoa_conv2d with its split-K scratch in the library's own device array."""
+    _check(_L.sparoa_conv2d_noalloc(ctypes.byref(desc), path, _ptr(x), _ptr(w), _ptr(bias),
+                                    _ptr(residual), act, _ptr(mask), _ptr(y), _ptr(executed),
+                                    _stream(stream)))
 
 
 def sparoa_conv2d_dense(desc, x, w, bias, residual, act, y, workspace=None, stream=None):

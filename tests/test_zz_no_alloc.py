@@ -1,0 +1,88 @@
+"""sparoa_conv2d_noalloc: the convolution for callers that cannot allocate,
+with its split-K partial sums in the library's own device array.  Its output
+must equal sparoa_conv2d's (given a workspace) bit for bit and lie within the
+dtype's tolerance of the oracle, on consecutive calls whose inputs shrink
+(the array keeps the previous call's partials); a shape whose partial sums do
+not fit the array is rejected before any device work."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests._util import RTOL, assert_close
+
+SCRATCH = 8 << 20      # SPAROA_NOALLOC_SCRATCH_BYTES
+
+
+def _abi():
+    from paper_2511_19457_amd import abi
+    return abi
+
+
+# n, cin, h, w, cout, k, stride, dtype, skip: largest first, every one split-K
+CALLS = [
+    (1, 64, 56, 56, 64, 3, 1, "f32", False),     # the single 3x3 conv workload
+    (1, 128, 14, 14, 128, 3, 1, "bf16", True),
+    (1, 64, 8, 8, 64, 3, 1, "bf16", False),
+]
+
+
+@pytest.mark.gpu
+def test_noalloc_equals_workspace_call_on_shrinking_inputs():
+    abi = _abi()
+    dev = torch.device("cuda")
+    for rep in range(2):
+        for i, (n, cin, h, w, cout, k, s, dt, skip) in enumerate(CALLS):
+            what = f"call {i} rep {rep}: {n}x{cin}x{h}x{w} -> {cout}, {k}x{k}, {dt}, skip {skip}"
+            print(what, flush=True)
+            tdt = {"f32": torch.float32, "bf16": torch.bfloat16}[dt]
+            p = k // 2
+            d = abi.conv_desc(n, cin, h, w, cout, k, k, s, s, p, p, 1, 1, 1, tdt)
+            path = abi.PATH_SKIP_MFMA if skip else abi.PATH_DENSE_MFMA
+            need = abi.sparoa_conv2d_workspace_size(d, path)
+            assert 0 < need <= SCRATCH, what           # the scratch array is in use
+            seed = 1900 + 10 * i
+            x = synth.relu_normal((n, h, w, cin), dt, seed)
+            wt = synth.he_normal((cout, k, k, cin), k * k * cin, dt, seed + 1)
+            xd, wd = x.to(dev), wt.to(dev)
+            mask = None
+            if skip:
+                counts = torch.zeros(4, dtype=torch.int64, device=dev)
+                mask = torch.zeros(abi.sparoa_mask_words(n * h * w, cin, 1, 8),
+                                   dtype=torch.int32, device=dev)
+                abi.sparoa_measure_sparsity(xd, n * h * w, cin, 1, 8, 0, counts, mask)
+            ho, wo = (h + 2 * p - k) // s + 1, (w + 2 * p - k) // s + 1
+            y = torch.full((n, ho, wo, cout), float("nan"), dtype=tdt, device=dev)
+            ex = torch.full((1,), -1, dtype=torch.int64, device=dev)
+            abi.sparoa_conv2d_noalloc(d, path, xd, wd, None, None, abi.ACT_RELU, mask, y,
+                                      ex if skip else None)
+            ws = torch.full((need,), 0x7F, dtype=torch.uint8, device=dev)
+            y_ref = torch.full_like(y, float("nan"))
+            ex_ref = torch.full((1,), -1, dtype=torch.int64, device=dev)
+            abi.sparoa_conv2d(d, path, xd, wd, None, None, abi.ACT_RELU, mask, y_ref, ws,
+                              ex_ref if skip else None)
+            torch.cuda.synchronize()
+            assert torch.equal(y, y_ref), what
+            if skip:
+                assert int(ex.item()) == int(ex_ref.item()), what
+            yr, ar, _ = oracle.conv2d(x, wt, n, cin, h, w, cout, k, k, s, s, p, p,
+                                      act=oracle.ACT_RELU)
+            assert_close(y, yr, ar, RTOL[tdt], what)
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"),
+                    reason="host-only check: the fake device pointers must never reach a GPU")
+def test_noalloc_rejects_shapes_beyond_the_scratch_array():
+    abi = _abi()
+    # fp32, 191 tiles of 64 x 64, split 3: 3 * 12224 * 64 * 4 bytes of partial sums
+    d = abi.conv_desc(1, 1024, 191, 64, 64, 1, 1, dtype=abi.F32)
+    assert abi.sparoa_conv2d_workspace_size(d, abi.PATH_DENSE_MFMA) > SCRATCH
+    fake = 0x100000000
+    with pytest.raises(abi.SparoaError) as e:
+        abi.sparoa_conv2d_noalloc(d, abi.PATH_DENSE_MFMA, fake, fake, None, None, abi.ACT_NONE,
+                                  None, fake)
+    assert e.value.status == 3
+    assert b"scratch" in abi._L.sparoa_last_error()
