@@ -190,9 +190,18 @@ sparoa_status sparoa_route(const sparoa_counts *counts, const sparoa_intensity *
  * residual joins before the activation, as in a ResNet bottleneck).
  *   Paths: DENSE_MFMA / SKIP_MFMA : implicit-GEMM on MFMA (groups == 1);
  *          DENSE_BW / SKIP_BW     : depthwise (groups == c_in == c_out) direct
- *                                   kernel, or, for groups == 1, the
- *                                   implicit GEMM with a tile shape that reads
- *                                   each activation once.
+ *                                   kernel; for groups == 1 1x1 convs
+ *                                   (16-bit, no padding, c_in <= 256 and
+ *                                   % 8 == 0, c_out % 8 == 0, the weights in
+ *                                   at most four 48 KB slices, several slices
+ *                                   only over >= 32768 output pixels, and not
+ *                                   c_in >= 192 with c_in % 64 == 0 and
+ *                                   c_out >= 64) the pointwise kernel: the
+ *                                   weights stay in LDS and each activation is
+ *                                   read once per slice
+ *                                   (sparoa_conv2d_tiling gives (16, 32));
+ *                                   any other groups == 1 conv runs the
+ *                                   implicit GEMM.
  *   Skip paths need `mask`: the bitmap of x written by
  *   sparoa_measure_sparsity over the [n*h*w, c_in] view with the block shape
  *   returned by sparoa_conv2d_skip_block (one pixel x 8 channels); a
@@ -205,7 +214,8 @@ sparoa_status sparoa_route(const sparoa_counts *counts, const sparoa_intensity *
  *   executed (row tile, tap, channel block) triples; for 16-bit inputs of
  *   at most 4 channels (image stems, served by a direct kernel with tiling
  *   (16, 32)), the number of issued (16-pixel row block, 32-wide k-step)
- *   MFMA steps.
+ *   MFMA steps; on the pointwise kernel, the (16-pixel, 32-channel) blocks
+ *   of x holding a nonzero (its skip form skips the others).
  *   Workspace: sparoa_conv2d_workspace_size bytes -- the split-K partial
  *   sums (0 when the GEMM needs no K split); its contents on entry do not
  *   matter and several calls may share one workspace in stream order.
@@ -246,9 +256,11 @@ sparoa_status sparoa_conv2d_zero_skip(const sparoa_conv_desc *desc, const void *
  *                                   the packed layout of
  *                                   sparoa_fc_pack_weights, each weight byte
  *                                   read at most once, no workspace; any
- *                                   other FC on a BW path runs the implicit
- *                                   GEMM on w[n][k] (sparoa_fc_uses_packed
- *                                   tells which layout a call takes).
+ *                                   other FC on a BW path is the 1x1 conv
+ *                                   over m pixels (pointwise kernel where it
+ *                                   applies, else the implicit GEMM) on
+ *                                   w[n][k] (sparoa_fc_uses_packed tells
+ *                                   which layout a call takes).
  *   Skip paths need `mask` of x measured over [m, k] with the block shape of
  *   sparoa_fc_skip_block ((1, 8) for the implicit GEMM, (m, 1) for the
  *   weight-streaming kernel):

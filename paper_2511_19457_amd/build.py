@@ -9,7 +9,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsparoa.so")
-SOURCES = ["abi.cpp", "measure.hip", "gemm.hip", "fc_bw.hip", "direct.hip", "noalloc.hip"]
+SOURCES = ["abi.cpp", "measure.hip", "gemm.hip", "fc_bw.hip", "direct.hip", "noalloc.hip", "pointwise.hip"]
 OBJDIR = os.path.join(PKG, "_build")
 
 FLAGS = [

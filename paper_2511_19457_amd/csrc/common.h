@@ -135,6 +135,7 @@ struct GemmTileChoice {
   int kchunk;       // K elements per main-loop step == skip granularity (channels)
   int split_k;      // number of K splits (1 = none)
   bool small_c = false;  // the direct kernel for C_in <= 4 (image stems), cfg 0
+  bool pointwise = false;  // the bandwidth-path 1x1 kernel (weights in LDS), cfg 0
 };
 GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path path);
 bool gemm_skip_supported(const sparoa_conv_desc &d);
@@ -152,6 +153,18 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
 // om: measure y in the epilogue (or in the split-K reduction); only when
 // gemm_fuses_out_measure(d, path) -- otherwise the call fails.
 bool gemm_fuses_out_measure(const sparoa_conv_desc &d, sparoa_path path);
+
+// Pointwise (1x1) kernel of the bandwidth path: 16-bit, groups 1, no
+// padding, C_in <= 256 and % 8 == 0, C_out % 8 == 0, the weights in at most
+// four LDS slices.  Skip form: MFMAs over all-zero 16-pixel x 32-channel
+// activation blocks are not issued.  om: fused output measurement (only when
+// pw_fuses_out_measure).
+bool pw_eligible(const sparoa_conv_desc &d);
+bool pw_fuses_out_measure(const sparoa_conv_desc &d);
+sparoa_status launch_pointwise(const sparoa_conv_desc &d, const void *x, const void *w,
+                               const void *bias, const void *residual, sparoa_act act, void *y,
+                               bool skip, uint64_t *executed, hipStream_t stream,
+                               const DeviceRoute *route, const OutMeasure *om);
 
 // Writes v to *p on the stream with a one-lane kernel (no memset node).
 sparoa_status launch_set_u64(uint64_t *p, uint64_t v, hipStream_t stream);

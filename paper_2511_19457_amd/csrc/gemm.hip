@@ -28,6 +28,7 @@
 // are those of the dense variant, and a skipped chunk would only have added
 // exact zeros, the skip output equals the dense output bit for bit (for
 // finite weights).
+#include "commit.h"
 #include "common.h"
 #include "dtype.h"
 
@@ -363,65 +364,6 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
           reinterpret_cast<typename E::raw *>(a.y)[row * a.N + col] = E::from_f32(apply_act(o, a.act));
         }
       }
-}
-
-// Words of the grouped count commit: kOmGroups groups x 2 counters, one
-// 128-byte line each.
-constexpr int kOmGroups = 8;
-static_assert(2 * kOmGroups * 128 == SPAROA_COMMIT_WORDS_BYTES, "commit word layout");
-
-// Adds a work-group's zero count and nonzero-block count into counts
-// (zero_blocks starts at nb).  Same-address atomics serialise device-wide
-// (13-17 ns per work-group measured with one atomic per counter), so with
-// `words` (the caller's zeroed count-commit words) work-group b of nwg is
-// a member of group b % kOmGroups: each member adds (1 << 40) + its count to
-// its group's word with one returning atomic, and the member whose add
-// completes the group adds the group's total to counts and clears the word
-// for the next call.  Without `words`: one atomic per counter per
-// work-group.
-__device__ __forceinline__ void om_commit(uint32_t zeros, uint32_t nz, sparoa_counts *counts,
-                                          unsigned long long *words, int64_t b, int64_t nwg) {
-  __shared__ uint32_t part[2][16];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    zeros += __shfl_xor(zeros, o, 64);
-    nz += __shfl_xor(nz, o, 64);
-  }
-  if (lane == 0) {
-    part[0][wave] = zeros;
-    part[1][wave] = nz;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    unsigned long long z = 0, n = 0;
-    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) {
-      z += part[0][i];
-      n += part[1][i];
-    }
-    if (!words) {
-      if (z) atomicAdd((unsigned long long *)&counts->zeros, z);
-      if (n) atomicAdd((unsigned long long *)&counts->zero_blocks, 0ull - n);
-      return;
-    }
-    constexpr unsigned long long kTicket = 1ull << 40;  // sums < 2^40, members < 2^24
-    const int64_t g = b % kOmGroups;
-    const unsigned long long members =
-        (unsigned long long)(nwg / kOmGroups + (g < nwg % kOmGroups ? 1 : 0));
-    unsigned long long *wz = words + g * 32, *wn = words + g * 32 + 16;
-    const unsigned long long oz = atomicAdd(wz, kTicket + z);
-    const unsigned long long on = atomicAdd(wn, kTicket + n);
-    if ((oz >> 40) == members - 1) {
-      const unsigned long long tz = (oz & (kTicket - 1)) + z;
-      if (tz) atomicAdd((unsigned long long *)&counts->zeros, tz);
-      atomicExch(wz, 0ull);
-    }
-    if ((on >> 40) == members - 1) {
-      const unsigned long long tn = (on & (kTicket - 1)) + n;
-      if (tn) atomicAdd((unsigned long long *)&counts->zero_blocks, 0ull - tn);
-      atomicExch(wn, 0ull);
-    }
-  }
 }
 
 // Sums the K-split partials in split order, adds bias and residual, then
@@ -1494,10 +1436,19 @@ bool gemm_skip_supported(const sparoa_conv_desc &d) {
 }
 
 
-GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path) {
+GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path path) {
   const Shape s = shape_of(d);
-  if (ig_eligible(d)) return ig_choose(s, d.c_in);
   GemmTileChoice t;
+  if ((path & 2) && pw_eligible(d)) {   // bandwidth path, 1x1: weights in LDS, x read once
+    t.cfg = 0;
+    t.bm = 16;      // skip unit: 16-pixel x 32-channel activation blocks
+    t.bn = 16;
+    t.kchunk = 32;
+    t.split_k = 1;
+    t.pointwise = true;
+    return t;
+  }
+  if (ig_eligible(d)) return ig_choose(s, d.c_in);
   if (small_c_eligible(d)) {   // one output row per work-group, 16-pixel row blocks
     t.cfg = 0;
     t.bm = 16;
@@ -1532,9 +1483,12 @@ GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path) {
 }
 
 bool gemm_fuses_out_measure(const sparoa_conv_desc &d, sparoa_path path) {
+  const GemmTileChoice t = gemm_choose(d, path);
+  // the pointwise kernel measures whole tiles of one weight slice
+  if (t.pointwise) return pw_fuses_out_measure(d);
   // the second-generation kernel (64-column tiles) writes whole bitmap bytes
   // when C_out % 64 == 0; its split-K reduction measures 16-byte vectors
-  return gemm_choose(d, path).cfg != 0 && d.c_out % 64 == 0 && elem_size(d.dtype) == 2;
+  return t.cfg != 0 && d.c_out % 64 == 0 && elem_size(d.dtype) == 2;
 }
 
 size_t gemm_workspace_required(const sparoa_conv_desc &d, sparoa_path path) {
@@ -1605,6 +1559,11 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
     if (defer) *defer = SplitReduceJob{d.dtype, nullptr, 0, s.M, s.N, bias, residual, act, y,
                                        nullptr, nullptr, nullptr};
     return launch_small_c(d, x, w, bias, residual, act, y, skip, executed, stream, route);
+  }
+  if (t.pointwise) {
+    if (defer) *defer = SplitReduceJob{d.dtype, nullptr, 0, s.M, s.N, bias, residual, act, y,
+                                       nullptr, nullptr, nullptr};
+    return launch_pointwise(d, x, w, bias, residual, act, y, skip, executed, stream, route, om);
   }
   dim3 grid((unsigned)cdiv(s.M, t.bm), (unsigned)cdiv(s.N, t.bn), (unsigned)gz);
   if (t.cfg) grid = dim3((unsigned)(cdiv(s.M, t.bm) * cdiv(s.N, t.bn) * gz));
