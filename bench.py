@@ -43,6 +43,10 @@ K = N = 4096
 INTENSITY_THR = 315.0   # bf16 ridge point of MI355X: 2.5 PFLOP/s / 8 TB/s (datasheet)
 SKIP_MARGIN = 0.97      # calibration: a skip path must beat dense by 3 % to count as a win
 THRESHOLDS_FILE = os.path.join(ROOT, "calibration", "fc_sweep_thresholds.json")
+# model stacks: name -> (layer table builder (stacks module), dtype name)
+STACKS = {"resnet50_b32_bf16": ("resnet50", 32, "bf16"),
+          "mobilenet_v2_b32_fp16": ("mobilenet_v2", 32, "f16"),
+          "ffn12_2048x768_fp16": ("ffn", None, "f16")}
 
 
 def parse():
@@ -64,6 +68,12 @@ def parse():
                    help="with --calibrate: write the thresholds and the timings they come from")
     p.add_argument("--no-layers", action="store_true",
                    help="skip the per-layer tables of the model stacks")
+    p.add_argument("--stack", default=None, choices=sorted(STACKS),
+                   help="only replay one model stack's routed pass as a HIP graph (--steps "
+                        "times) and print its layer table: the program rocprofv3 profiles")
+    p.add_argument("--stack-summary", default=None, metavar="DIR",
+                   help="no GPU: turn the rocprofv3 outputs of the --stack runs under DIR into "
+                        "profiles/<stack>_layers.md")
     p.add_argument("--cases-out", default=None, help="write the per-case table (JSON) here")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only run 5 plain device-to-device copies of MIB MiB and exit (the "
@@ -142,10 +152,10 @@ PROFILE_COMMANDS = {
 }
 
 
-def _bench_line(log_path):
+def _bench_line(log_path, key="metric"):
     with open(log_path) as f:
         for line in reversed(f.read().splitlines()):
-            if line.startswith("{") and '"metric"' in line:
+            if line.startswith("{") and f'"{key}"' in line:
                 return json.loads(line)
     raise ValueError(f"no bench JSON line in {log_path}")
 
@@ -913,10 +923,212 @@ def oracle_timings(torch, synth, budget_s=8.0):
     return out
 
 
+
+# ---------------------------------------------------------------------------
+# Model-stack profiles: the program rocprofv3 runs (--stack) and the summary
+# of its outputs (--stack-summary).
+
+STACK_COMMANDS = {
+    "trace": "rocprofv3 --kernel-trace --output-format csv -d $REPO/gpurun_out/stk_trace_{S} "
+             "-o trace -- python3 $REPO/bench.py --stack {S} --steps 10",
+    "pmc": "rocprofv3 --pmc {C} --output-format csv -d $REPO/gpurun_out/stk_pmc_{S}_{T} -o pmc "
+           "-- python3 $REPO/bench.py --stack {S} --steps 3",
+    "copy": "rocprofv3 --pmc {C} --output-format csv -d $REPO/gpurun_out/pmc_copy_{C} -o pmc "
+            "-- python3 $REPO/bench.py --copy-probe 256",
+}
+STACK_PMC = {"fetch": "FETCH_SIZE", "write": "WRITE_SIZE",
+             "mfma": "SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 "
+                     "SQ_INSTS_VALU_MFMA_MOPS_F16 GRBM_GUI_ACTIVE"}
+
+
+def _stack_layers(torch, name):
+    from paper_2511_19457_amd import stacks
+    fn, n, dt = STACKS[name]
+    layers = getattr(stacks, fn)(n) if n is not None else getattr(stacks, fn)()
+    return layers, {"bf16": torch.bfloat16, "f16": torch.float16}[dt]
+
+
+def _graph_nodes(torch, fn):
+    """Kernels `fn` enqueues: nodes of a HIP graph it is captured into."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so")
+    g = torch.cuda.CUDAGraph(keep_graph=True)
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g):
+            fn()
+    torch.cuda.synchronize()
+    n = ctypes.c_size_t(0)
+    rc = hip.hipGraphGetNodes(ctypes.c_void_p(g.raw_cuda_graph()), None, ctypes.byref(n))
+    assert rc == 0, f"hipGraphGetNodes: {rc}"
+    del g
+    return int(n.value)
+
+
+def stack_profile_run(abi, torch, synth, name, reps):
+    """One model stack's routed pass (counter reset, then measure + device
+    route + execute per layer) captured once as a HIP graph and replayed
+    `reps` times, after counting the kernels of each layer (its routed call
+    captured alone).  Prints the layer table the summary needs."""
+    from paper_2511_19457_amd.driver import Engine
+    from paper_2511_19457_amd.stacks import input_shape
+    layers, dt = _stack_layers(torch, name)
+    eng = Engine(layers, dt, "cuda", seed=synth.seed_for(3, 0), sparsity_thr=0.5)
+    x = synth.normal(input_shape(layers), dt, synth.seed_for(3, 1)).cuda()
+    eng.forward_routed(x)
+    torch.cuda.synchronize()
+    recs = eng.records_from_device()
+    counts = [_graph_nodes(torch, lambda i=i: eng.run_layer_routed(i)) for i in range(len(layers))]
+    reset = _graph_nodes(torch, eng.reset_counters)
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g):
+            eng.forward_routed(x)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    rows = []
+    for L, rec, k in zip(layers, recs, counts):
+        if L.kind == "maxpool":      # glue: input + output bytes
+            from paper_2511_19457_amd.stacks import output_shape
+            sh, o = L.shape, output_shape(L)
+            rec.bytes = (sh["n"] * sh["h"] * sh["w"] * sh["c"] + o[0] * o[1] * o[2] * o[3]) * \
+                torch.tensor([], dtype=dt).element_size()
+        rows.append(dict(layer=L.name, kind=L.kind, kernels=k,
+                         path=abi.PATH_NAMES.get(rec.path, "glue") if L.kind != "maxpool" else "glue",
+                         macs=rec.macs, bytes=rec.bytes, rho_e=round(rec.rho_e, 4),
+                         rho_b=round(rec.rho_b, 4), intensity=round(rec.intensity, 2)))
+    print(json.dumps(dict(stack=name, reps=reps, reset_kernels=reset,
+                          kernels_per_pass=reset + sum(counts), ms=sorted(ts)[len(ts) // 2],
+                          layers=rows)), flush=True)
+
+
+def _csv_rows(d, pattern):
+    import csv
+    import glob
+    files = sorted(glob.glob(os.path.join(d, "**", pattern), recursive=True))
+    if not files:
+        raise FileNotFoundError(f"no {pattern} under {d}")
+    with open(files[0]) as f:
+        return list(csv.DictReader(f))
+
+
+def stack_summary(d):
+    """profiles/<stack>_layers.md from the --stack runs under d: per layer
+    its kernels' average duration per pass (kernel trace of 10 replays), its
+    HBM bytes per pass (FETCH_SIZE and WRITE_SIZE, each scaled by what it
+    reads for a plain 256 MiB copy), and its MFMA busy fraction
+    (SQ_VALU_MFMA_BUSY_CYCLES over GRBM_GUI_ACTIVE x 4 SIMDs x 256 CUs)."""
+    from collections import defaultdict
+    scale = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        rows = _csv_rows(os.path.join(d, f"pmc_copy_{c}"), "*counter_collection.csv")
+        vals = sorted(float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"])
+        vals = vals[-5:]
+        scale[c] = 256 * 1024.0 / (sum(vals) / len(vals))
+    for name in STACKS:
+        try:
+            line = _bench_line(os.path.join(d, f"stk_{name}.log"), key="stack")
+        except (OSError, ValueError):
+            continue
+        per = line["kernels_per_pass"]
+        # kernel trace: the last reps passes, dispatch order
+        tr = _csv_rows(os.path.join(d, f"stk_trace_{name}"), "*kernel_trace.csv")
+        tr.sort(key=lambda r: int(r["Dispatch_Id"]))
+        tr = tr[-line["reps"] * per:]
+        dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in tr]
+        names = [r["Kernel_Name"] for r in tr]
+        # counters per dispatch: the last passes of each run
+        def pmc(tag):
+            rows = _csv_rows(os.path.join(d, f"stk_pmc_{name}_{tag}"), "*counter_collection.csv")
+            by = defaultdict(dict)
+            for r in rows:
+                by[int(r["Dispatch_Id"])][r["Counter_Name"]] = \
+                    by[int(r["Dispatch_Id"])].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+            ids = sorted(by)
+            reps_c = len(ids) // per
+            ids = ids[-per * min(reps_c, 3):]
+            return [by[i] for i in ids], min(reps_c, 3)
+        fetch, nf = pmc("fetch")
+        write, nw = pmc("write")
+        mf, nm = pmc("mfma")
+        out = [f"# {name}: per-layer kernel time, HBM traffic and MFMA use", "",
+               f"One routed pass (counter reset, then per layer: input measurement where not "
+               f"fused in its producer, device-side route, the layer's kernel with fused output "
+               f"measurement where available) captured as a HIP graph; {per} kernels per pass; "
+               f"graph replay median {line['ms']:.3f} ms in the traced run (profiler attached).",
+               "", "Commands (from /tmp on the GPU machine, REPO = repository root):", "", "```",
+               STACK_COMMANDS["trace"].format(S=name)]
+        for tag, c in STACK_PMC.items():
+            out.append(STACK_COMMANDS["pmc"].format(S=name, T=tag, C=c))
+        for c in ("FETCH_SIZE", "WRITE_SIZE"):
+            out.append(STACK_COMMANDS["copy"].format(C=c))
+        out += ["```", "",
+                f"Counter scale (plain 256 MiB copy): FETCH_SIZE x {scale['FETCH_SIZE']:.4f}, "
+                f"WRITE_SIZE x {scale['WRITE_SIZE']:.4f}.  Algorithmic bytes: the layer's Eq. 2 "
+                "compulsory traffic (input, weights, output); a residual read adds to the counted "
+                "bytes only (max pool: input + output).  Rates use the traced kernel time; "
+                "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES (summed over SIMDs) / (one XCD's "
+                "GRBM_GUI_ACTIVE x 1024 SIMDs), over the layer's kernels.", "",
+                "| layer | path | kernels | us | alg MB | counted MB | counted/alg | GB/s (counted) "
+                "| TFLOP/s | MFMA busy % | roofline % | kernels (avg us) |",
+                "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+        tot_us = tot_alg = tot_cnt = 0.0
+        pos = line["reset_kernels"]
+        bits = 32 if name.endswith("fp32") else 16
+        for L in line["layers"]:
+            k = L["kernels"]
+            us = sum(dur[p * per + pos + j] for p in range(line["reps"]) for j in range(k)) / \
+                line["reps"]
+            def cnt(rows, n_rep, c):
+                return sum(rows[p * per + pos + j].get(c, 0.0) for p in range(n_rep)
+                           for j in range(k)) / max(n_rep, 1)
+            counted = (cnt(fetch, nf, "FETCH_SIZE") * scale["FETCH_SIZE"] +
+                       cnt(write, nw, "WRITE_SIZE") * scale["WRITE_SIZE"]) * 1024
+            busy = cnt(mf, nm, "SQ_VALU_MFMA_BUSY_CYCLES")
+            # GRBM_GUI_ACTIVE arrives summed over the 8 XCDs: one XCD's
+            # active cycles is the sum / 8
+            gui = sum(max(mf[p * per + pos + j].get("GRBM_GUI_ACTIVE", 0.0), 1.0) / 8
+                      for p in range(nm) for j in range(k)) / max(nm, 1)
+            kn = defaultdict(list)
+            for j in range(k):
+                kn[_short(names[pos + j])].append(
+                    sum(dur[p * per + pos + j] for p in range(line["reps"])) / line["reps"])
+            flops = 2 * L["macs"]
+            roof = _roof_us(flops, L["bytes"], bits) if L["kind"] != "maxpool" else \
+                L.get("bytes", 0) / (HBM_PEAK_GBS * 1e3)
+            frac = roof / us if us else 0.0
+            out.append(f"| {L['layer']} | {L['path']} | {k} | {us:.2f} | {L['bytes'] / 1e6:.1f} | "
+                       f"{counted / 1e6:.1f} | {counted / max(L['bytes'], 1):.2f} | "
+                       f"{counted / us / 1e3:.0f} | {flops / us / 1e6:.1f} | "
+                       f"{100 * busy / (gui * 1024):.1f} | {100 * frac:.1f} | " +
+                       ", ".join(f"`{kk}` {sum(v) / len(v):.1f}" for kk, v in kn.items()) + " |")
+            tot_us += us
+            tot_alg += L["bytes"]
+            tot_cnt += counted
+            pos += k
+        out += ["", f"Sum of kernel time per pass: {tot_us:.1f} us; algorithmic {tot_alg / 1e6:.1f} "
+                f"MB, counted {tot_cnt / 1e6:.1f} MB."]
+        with open(os.path.join(ROOT, "profiles", f"{name}_layers.md"), "w") as f:
+            f.write("\n".join(out) + "\n")
+        print(f"wrote profiles/{name}_layers.md", file=sys.stderr)
+
 def main():
     args = parse()
     if args.profile_summary:
         profile_summary(args.profile_summary, args.copy_probe or 256)
+        return
+    if args.stack_summary:
+        stack_summary(args.stack_summary)
         return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
@@ -940,6 +1152,9 @@ def main():
         return
     import synth
     from paper_2511_19457_amd import abi
+    if args.stack:
+        stack_profile_run(abi, torch, synth, args.stack, args.steps)
+        return
     if args.crossover:
         print(json.dumps(dict(sweep="f2 crossover", workload="x [m,4096] x w [4096,4096] bf16, "
                               "whole path forced per path", data="synthetic",

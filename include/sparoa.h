@@ -142,11 +142,16 @@ sparoa_status sparoa_measure_sparsity(const void *x_dev, sparoa_dtype dtype, int
  * vector, 1 row x block_cols >= cols for rows narrower than 16 bytes, or
  * whole columns (block_rows >= rows, block_cols == 1) -- the call is then
  * one launch instead of two.  Other block shapes initialise everything as
- * sparoa_measure_sparsity does.  Errors as there. */
+ * sparoa_measure_sparsity does.  commit_dev (nullable): zeroed count-commit
+ * words (SPAROA_COMMIT_WORDS_BYTES, zero on entry, zero again when the call's
+ * kernel finishes; see sparoa_conv2d_routed_measured) through which the
+ * one-vector and narrow-row layouts commit their counts instead of one
+ * same-address atomic per counter per work-group.  Errors as there. */
 sparoa_status sparoa_measure_sparsity_preset(const void *x_dev, sparoa_dtype dtype, int64_t rows,
                                              int64_t cols, int64_t block_rows,
                                              int64_t block_cols, sparoa_counts *counts_dev,
-                                             uint32_t *mask_dev, hipStream_t stream);
+                                             uint32_t *mask_dev, uint64_t *commit_dev,
+                                             hipStream_t stream);
 /* Same as sparoa_measure_sparsity, then copies the counts into *counts_host
  * and waits for the stream.  counts_dev is caller-provided device scratch of
  * one sparoa_counts. */
@@ -350,10 +355,11 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
  *   y_counts must hold {0, rows*cols, nb, nb} on entry, nb = rows*ceil(cols/8):
  *   the fused form adds into it (a caller resets all of a network's counters
  *   with one copy from a template before each pass).
- *   Fused into the GEMM epilogue (or its split-K reduction) when the 16-bit
- *   64-channel-chunk implicit GEMM serves the layer and cols % 64 == 0: no
- *   launch of its own and no second read of y; otherwise the standalone
- *   measurement of y runs after the layer (as sparoa_measure_sparsity_preset:
+ *   Fused into the producer's epilogue (or its split-K reduction) where the
+ *   kernel that serves the layer can (the 64-channel-chunk implicit GEMM with
+ *   cols % 64 == 0; the pointwise kernel with one weight slice): no launch of
+ *   its own and no second read of y; otherwise the standalone measurement of
+ *   y runs after the layer (as sparoa_measure_sparsity_preset with y_commit:
  *   one launch for the block shapes whose bitmap needs no clearing).
  *   y_commit (nullable): SPAROA_COMMIT_WORDS_BYTES of device memory that
  *   must be all zero on entry and is all zero again when the call's kernels

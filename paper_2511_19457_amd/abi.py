@@ -139,7 +139,7 @@ def _load():
         "sparoa_fc_routed": (ctypes.c_int, [P(FcDesc), P(Thresholds), vp, vp, vp, vp, vp, vp,
                                             ctypes.c_int, vp, vp, vp, sz, vp, vp]),
         "sparoa_measure_sparsity_preset": (ctypes.c_int, [vp, ctypes.c_int, i64, i64, i64, i64,
-                                                          vp, vp, vp]),
+                                                          vp, vp, vp, vp]),
         "sparoa_conv2d_split": (ctypes.c_int, [P(ConvDesc), ctypes.c_double, vp, vp, vp, vp, vp,
                                                ctypes.c_int, vp, vp, vp, sz, vp, vp]),
         "sparoa_fc_split": (ctypes.c_int, [P(FcDesc), ctypes.c_double, vp, vp, vp, vp, vp,
@@ -235,11 +235,12 @@ def sparoa_measure_sparsity(x, rows, cols, block_rows, block_cols, samples, coun
 
 
 def sparoa_measure_sparsity_preset(x, rows, cols, block_rows, block_cols, counts, mask,
-                                   stream=None, dtype=None):
-    """Measurement into counters already set to {0, numel, nb, nb} (see sparoa.h)."""
+                                   stream=None, dtype=None, commit=None):
+    """Measurement into counters already set to {0, numel, nb, nb} (see sparoa.h);
+    commit: zeroed count-commit words, or None."""
     _check(_L.sparoa_measure_sparsity_preset(
         _ptr(x), dtype_code(x) if dtype is None else dtype, rows, cols, block_rows, block_cols,
-        _ptr(counts), _ptr(mask), _stream(stream)))
+        _ptr(counts), _ptr(mask), _ptr(commit), _stream(stream)))
 
 
 def sparoa_measure_sparsity_sync(x, rows, cols, block_rows, block_cols, samples, counts,

@@ -153,13 +153,15 @@ sparoa_status sparoa_measure_sparsity(const void *x_dev, sparoa_dtype dtype, int
 sparoa_status sparoa_measure_sparsity_preset(const void *x_dev, sparoa_dtype dtype, int64_t rows,
                                              int64_t cols, int64_t block_rows,
                                              int64_t block_cols, sparoa_counts *counts_dev,
-                                             uint32_t *mask_dev, hipStream_t stream) {
+                                             uint32_t *mask_dev, uint64_t *commit_dev,
+                                             hipStream_t stream) {
   g_last_error.clear();
   sparoa_status st = check_measure(x_dev, dtype, rows, cols, block_rows, block_cols, 0,
                                    counts_dev, mask_dev, nullptr);
   if (st != SPAROA_OK) return st;
+  if ((st = check_ptrs16({commit_dev})) != SPAROA_OK) return st;
   return launch_measure(x_dev, dtype, rows, cols, block_rows, block_cols, 0, counts_dev,
-                        mask_dev, nullptr, stream, true);
+                        mask_dev, nullptr, stream, true, commit_dev);
 }
 
 sparoa_status sparoa_measure_sparsity_sync(const void *x_dev, sparoa_dtype dtype, int64_t rows,
@@ -514,7 +516,7 @@ sparoa_status conv_routed_impl(const sparoa_conv_desc *d, const sparoa_threshold
     // y_counts arrive preset ({0, numel, nb, nb}): no init launch where the
     // bitmap needs no clearing
     return measure_y ? launch_measure(y, d->dtype, rows, cols, 1, 8, 0, y_counts, y_mask, nullptr,
-                                      stream, true)
+                                      stream, true, y_commit)
                      : SPAROA_OK;
   };
   if (dw) {
@@ -624,7 +626,7 @@ sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *t
   const bool measure_y = y_counts != nullptr;
   auto measure_after = [&]() {
     return measure_y ? launch_measure(y, d->dtype, d->m, d->n, 1, 8, 0, y_counts, y_mask, nullptr,
-                                      stream, true)   // y_counts arrive preset
+                                      stream, true, y_commit)   // y_counts arrive preset
                      : SPAROA_OK;
   };
   const DeviceRoute r{counts_dev, thr->sparsity_thr, thr->mode, bw, path_dev};

@@ -77,10 +77,13 @@ __device__ __forceinline__ bool device_route_skip(const DeviceRoute &r) {
 // preset: counts already hold {0, numel, nb, nb}; layouts whose bitmap needs
 // no clearing (block 1 x one 16-byte vector, one block per row narrower than
 // 16 bytes, whole-column strips) then skip the init launch.
+// commit_words (preset only, nullable): zeroed count-commit words for the
+// layouts that commit per work-group (lanebit, rowbit), left zero.
 sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64_t cols,
                              int64_t block_rows, int64_t block_cols, int64_t samples,
                              sparoa_counts *counts, uint32_t *mask, uint64_t *per_sample,
-                             hipStream_t stream, bool preset = false);
+                             hipStream_t stream, bool preset = false,
+                             uint64_t *commit_words = nullptr);
 
 constexpr int kGroupMax = 16;  // jobs per grouped launch
 

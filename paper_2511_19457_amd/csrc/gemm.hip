@@ -520,7 +520,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   auto stage = [&](int buf) __attribute__((always_inline)) -> char * {
     return smem_raw + buf * ((BM + BN) * ROW);
   };
-  __shared__ unsigned short list[SKIP ? kMaxChunks2 : 1];
+  // the chunks this tile walks, in order, each packed as
+  // j | cb << 10 | r << 20 | s << 25 (chunk id, channel block within the
+  // tap, kernel row and column): the walk needs no division per chunk
+  __shared__ int list[kMaxChunks2];
   __shared__ uint32_t nzvec[SKIP ? kMaxVecWords : 1];
   __shared__ int list_len;
   __shared__ uint8_t ombytes[BM * (BN / 64 > 0 ? BN / 64 : 1)];   // output bitmap bytes of the tile
@@ -549,6 +552,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   const int64_t c_begin = zsplit * a.chunks_per_split;
   const int64_t c_end = min(c_begin + a.chunks_per_split, a.nchunks);
   const int cpt = (int)(a.Cin / BKC);   // chunks per tap
+  auto pack_chunk = [&](int j) __attribute__((always_inline)) -> int {
+    const int t = j / cpt, cb = j - t * cpt;
+    const int r = t / (int)a.Kw, sx = t - r * (int)a.Kw;
+    return j | (cb << 10) | (r << 20) | (sx << 25);
+  };
   const int cg = tid % VPR;             // this thread's 16-byte column of a chunk row
   const int rr = tid / VPR;             // this thread's first chunk row
 
@@ -624,16 +632,21 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
     const int kv_words = (int)((a.taps * cpg + 31) / 32);
     for (int i = tid; i < kv_words; i += NT) nzvec[i] = 0u;
     __syncthreads();
-    for (int64_t p = tid; p < (int64_t)BM * a.taps; p += NT) {
-      const int r_in = (int)(p / a.taps);
-      const int tap = (int)(p - (int64_t)r_in * a.taps);
-      const int64_t m = m0 + r_in;
-      if (m >= a.M) continue;
-      const int64_t ow = m % a.Wo, oh = (m / a.Wo) % a.Ho, nn = m / (a.Wo * a.Ho);
-      const int64_t r = tap / a.Kw, sx = tap - r * a.Kw;
-      const int64_t ih = oh * a.sh - a.ph + r * a.dh, iw = ow * a.sw - a.pw + sx * a.dw;
-      if (ih < 0 || ih >= a.H || iw < 0 || iw >= a.W) continue;
-      const int64_t pix = (nn * a.H + ih) * a.W + iw;
+    // (32-bit index arithmetic with float-reciprocal division: pixel
+    // indices are below 2^24 on this kernel)
+    const int taps = (int)a.taps, ntp = BM * taps;
+    const float inv_taps = 1.0f / (float)taps, inv_kw = 1.0f / (float)kw;
+    for (int p = tid; p < ntp; p += NT) {
+      int r_in, tap, t1, ow, nn, oh, r, sx;
+      divmod_small(p, taps, inv_taps, r_in, tap);
+      const int m = (int)m0 + r_in;
+      if (m >= (int)a.M) continue;
+      divmod_small(m, Wo, inv_wo, t1, ow);
+      divmod_small(t1, Ho, inv_ho, nn, oh);
+      divmod_small(tap, kw, inv_kw, r, sx);
+      const int ih = oh * (int)a.sh - (int)a.ph + r * dh, iw = ow * (int)a.sw - (int)a.pw + sx * dw;
+      if (ih < 0 || ih >= H || iw < 0 || iw >= W) continue;
+      const int64_t pix = ((int64_t)nn * H + ih) * W + iw;
       for (int b = 0; b < cpg; b += 32) {
         const int nb = min(32, cpg - b);
         lds_or_bits(nzvec, tap * cpg + b, read_bits(a.mask, pix * cpg + b, nb), nb);
@@ -656,7 +669,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
         }
         const uint64_t bal = __ballot(nz);
         const int before = __popcll(bal & ((1ull << lane) - 1ull));
-        if (nz) list[total + before] = (unsigned short)j;
+        if (nz) list[total + before] = pack_chunk((int)j);
         total += __popcll(bal);
       }
       if (lane == 0) {
@@ -671,20 +684,25 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
 
   // ---- staging: a ring of PF chunks in registers, two chunks in LDS --------
   u32x4 ra[PF][AV], rb[PF][BV];  // native vectors: no struct copies, stays in VGPRs
-  auto load_chunk = [&](int j, u32x4 (&ra_s)[AV], u32x4 (&rb_s)[BV])
+  // valid == false: every offset out of range, the loads return zeros without
+  // touching memory -- the prologue issues its PF + 1 loads unconditionally,
+  // so the compiler can count the loads in flight at the loop head (a
+  // conditional prologue load made it wait for the whole ring there)
+  auto load_chunk = [&](int info, u32x4 (&ra_s)[AV], u32x4 (&rb_s)[BV], bool valid)
                         __attribute__((always_inline)) {
-    const int t = j / cpt, cb = j - t * cpt;
-    const int r = t / kw, sx = t - r * kw;
+    const int j = info & 1023, cb = (info >> 10) & 1023;
+    const int r = (info >> 20) & 31, sx = (info >> 25) & 31;
     const int tap_offb = ((r * dh * W + sx * dw) * Cin + cb * BKC) * 2;
 #pragma unroll
     for (int u = 0; u < AV; ++u) {
-      const bool in_img = (vrow[u] >> r) & (vcol[u] >> sx) & 1u;
+      const bool in_img = valid && ((vrow[u] >> r) & (vcol[u] >> sx) & 1u);
       const int off = in_img ? a_offb[u] + tap_offb : (int)0x80000000;
       ra_s[u] = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
     }
 #pragma unroll
     for (int u = 0; u < BV; ++u)
-      rb_s[u] = __builtin_amdgcn_raw_buffer_load_b128(wr, b_offb[u], j * (BKC * 2), 0);
+      rb_s[u] = __builtin_amdgcn_raw_buffer_load_b128(wr, valid ? b_offb[u] : (int)0x80000000,
+                                                      valid ? j * (BKC * 2) : 0, 0);
   };
   // every row a thread stores is rr mod 8 (RPU and BM are multiples of 8)
   const int st_col = 16 * (cg ^ (rr & 7));
@@ -744,29 +762,33 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   // ring stays in registers.
   static_assert(PF >= 2 && PF <= 4, "register ring depth");
   const int n = (int)count;
-  if constexpr (SKIP) {
-    // a dense-routed tile of the skip kernel walks the list too, filled in
-    // dense order: no branch on the route inside the main loop
-    if (!use_list) {
-      for (int i = tid; i < (int)count; i += NT) list[i] = (unsigned short)(c_begin + i);
-      __syncthreads();
-    }
+  // dense walks (the dense kernel, and a dense-routed tile of the skip
+  // kernel) fill the list in dense order: no branch on the route inside the
+  // main loop
+  if (!SKIP || !use_list) {
+    for (int i = tid; i < (int)count; i += NT) list[i] = pack_chunk((int)c_begin + i);
+    __syncthreads();
   }
+  // (the list entry is the same in every lane: read it as a scalar, so the
+  // weight loads take it as their scalar offset -- an LDS value the
+  // compiler must treat as divergent made it wrap every weight load in a
+  // readfirstlane loop)
   auto chunk_at = [&](int i) __attribute__((always_inline)) -> int {
-    if constexpr (SKIP) return (int)list[i];
-    else return (int)c_begin + i;
+    return __builtin_amdgcn_readfirstlane(list[i]);
   };
   if (n > 0) {
     // chunk 0 alone first (every work-group starts at once: a deep prologue
     // would queue each one's first chunk behind all the others' prefetch)
     // (chunks past the last are not loaded: short K -- a 1x1 conv over 64
     // channels is one chunk -- would otherwise re-read its chunks PF times)
-    load_chunk(chunk_at(0), ra[0], rb[0]);
+    load_chunk(chunk_at(0), ra[0], rb[0], true);
     store_chunk(0, ra[0], rb[0]);
-    if (1 < n) load_chunk(chunk_at(1), ra[1], rb[1]);
-    if constexpr (PF > 2) if (2 < n) load_chunk(chunk_at(2), ra[PF > 2 ? 2 : 0], rb[PF > 2 ? 2 : 0]);
-    if constexpr (PF > 3) if (3 < n) load_chunk(chunk_at(3), ra[PF > 3 ? 3 : 0], rb[PF > 3 ? 3 : 0]);
-    if (PF < n) load_chunk(chunk_at(PF), ra[0], rb[0]);
+    load_chunk(chunk_at(min(1, n - 1)), ra[1], rb[1], 1 < n);
+    if constexpr (PF > 2)
+      load_chunk(chunk_at(min(2, n - 1)), ra[PF > 2 ? 2 : 0], rb[PF > 2 ? 2 : 0], 2 < n);
+    if constexpr (PF > 3)
+      load_chunk(chunk_at(min(3, n - 1)), ra[PF > 3 ? 3 : 0], rb[PF > 3 ? 3 : 0], 3 < n);
+    load_chunk(chunk_at(min(PF, n - 1)), ra[0], rb[0], PF < n);
     __syncthreads();
   // Steady state: groups of PF straight-line steps (no branch inside a step,
   // so the compiler's load counters stay exact and PF chunks stay in flight);
@@ -780,7 +802,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
       const int jn = chunk_at(min(i + 1 + PF, n - 1)); /* read before the MFMAs */ \
       compute(i & 1);                                                              \
       if (!(GUARD) || i + 1 < n) store_chunk((i + 1) & 1, ra[sn], rb[sn]); \
-      if (!(GUARD) || i + 1 + PF < n) load_chunk(jn, ra[sn], rb[sn]);            \
+      if (!(GUARD) || i + 1 + PF < n) load_chunk(jn, ra[sn], rb[sn], true);      \
       __syncthreads();                                                             \
     }                                                                              \
   }

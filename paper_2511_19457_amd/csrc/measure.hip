@@ -17,6 +17,7 @@
 // Counts leave a work-group through one atomic per counter: atomics on one
 // address serialise device-wide (~10 ns each on MI355X), so grids stay at a
 // few hundred work-groups that loop over the tensor.
+#include "commit.h"
 #include "common.h"
 
 namespace sparoa {
@@ -221,7 +222,8 @@ constexpr int kLanebitUnroll = 4;
 template <int ESZ, int V>
 __device__ __forceinline__ void lanebit_pass(const char *__restrict__ x, int64_t items,
                                              int64_t words, uint32_t *__restrict__ mask,
-                                             sparoa_counts *counts, int64_t bid, int64_t nblk) {
+                                             sparoa_counts *counts, int64_t bid, int64_t nblk,
+                                             unsigned long long *commit = nullptr) {
   constexpr int NT = kLanebitThreads;
   const int lane = threadIdx.x & 63;
   const int64_t slot = nblk * NT;
@@ -250,15 +252,19 @@ __device__ __forceinline__ void lanebit_pass(const char *__restrict__ x, int64_t
       nonzero += lane == 0 ? (uint64_t)__popcll(bal) : 0ull;
     }
   }
-  wg_commit<NT>(zeros, nonzero, counts, nullptr);
+  // with commit words: ticketed commits over 16 addresses instead of one
+  // same-address atomic per counter per work-group
+  if (commit) om_commit((uint32_t)zeros, (uint32_t)nonzero, counts, commit, bid, nblk);
+  else wg_commit<NT>(zeros, nonzero, counts, nullptr);
 }
 
 template <int ESZ, int V>
 __global__ __launch_bounds__(kLanebitThreads) void measure_lanebit(const char *__restrict__ x,
                                                                    int64_t items, int64_t words,
                                                                    uint32_t *__restrict__ mask,
-                                                                   sparoa_counts *counts) {
-  lanebit_pass<ESZ, V>(x, items, words, mask, counts, blockIdx.x, gridDim.x);
+                                                                   sparoa_counts *counts,
+                                                                   unsigned long long *commit) {
+  lanebit_pass<ESZ, V>(x, items, words, mask, counts, blockIdx.x, gridDim.x, commit);
 }
 
 // One bitmap bit per row (block = 1 row x block_cols >= cols) for rows
@@ -273,7 +279,8 @@ __global__ __launch_bounds__(kLanebitThreads) void measure_rowbit(const char *__
                                                                   int64_t rows, int cols,
                                                                   int64_t words,
                                                                   uint32_t *__restrict__ mask,
-                                                                  sparoa_counts *counts) {
+                                                                  sparoa_counts *counts,
+                                                                  unsigned long long *commit) {
   constexpr int EPV = 16 / ESZ;  // elements per 16-byte vector
   const int lane = threadIdx.x & 63;
   const int nv = cols * ESZ / 2;  // vectors per 8 rows
@@ -317,7 +324,8 @@ __global__ __launch_bounds__(kLanebitThreads) void measure_rowbit(const char *__
     const int64_t w = base / 4 + lane / 4;
     if ((lane & 3) == 0 && w < words) mask[w] = word;
   }
-  wg_commit<kLanebitThreads>(zeros, nonzero, counts, nullptr);
+  if (commit) om_commit((uint32_t)zeros, (uint32_t)nonzero, counts, commit, blockIdx.x, gridDim.x);
+  else wg_commit<kLanebitThreads>(zeros, nonzero, counts, nullptr);
 }
 
 // Several tensors of one element size in the lanebit layout, one launch:
@@ -584,7 +592,10 @@ sparoa_status launch_measure_group(const MeasureJob *jobs, int n, hipStream_t st
 sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64_t cols,
                              int64_t block_rows, int64_t block_cols, int64_t samples,
                              sparoa_counts *counts, uint32_t *mask, uint64_t *per_sample,
-                             hipStream_t stream, bool preset) {
+                             hipStream_t stream, bool preset, uint64_t *commit_words) {
+  // commit words serve the layouts whose counts arrive preset
+  unsigned long long *commit =
+      preset ? reinterpret_cast<unsigned long long *>(commit_words) : nullptr;
   const int esz = (int)elem_size(dt);
   const int vw = 16 / esz;
   const bool want_mask = mask != nullptr;
@@ -638,14 +649,16 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
 
   if (lanebit) {
     const int64_t items = rows * (cols / vw);
-    int64_t gx = cdiv(items, (int64_t)kLanebitThreads);
+    // each lane's kLanebitUnroll loads in flight cover the tensor once where
+    // it is small (fewer work-groups to commit), at most one per CU
+    int64_t gx = cdiv(items, (int64_t)kLanebitThreads * kLanebitUnroll);
     if (gx > 256) gx = 256;
     if (esz == 2)
       hipLaunchKernelGGL((measure_lanebit<2, 8>), dim3((unsigned)gx), dim3(kLanebitThreads), 0,
-                         stream, static_cast<const char *>(x), items, words, mask, counts);
+                         stream, static_cast<const char *>(x), items, words, mask, counts, commit);
     else
       hipLaunchKernelGGL((measure_lanebit<4, 4>), dim3((unsigned)gx), dim3(kLanebitThreads), 0,
-                         stream, static_cast<const char *>(x), items, words, mask, counts);
+                         stream, static_cast<const char *>(x), items, words, mask, counts, commit);
     SPAROA_LAUNCH_CHECK("measure_lanebit");
     return SPAROA_OK;
   }
@@ -654,10 +667,12 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
     if (gx > 256) gx = 256;
     if (esz == 2)
       hipLaunchKernelGGL(measure_rowbit<2>, dim3((unsigned)gx), dim3(kLanebitThreads), 0, stream,
-                         static_cast<const char *>(x), rows, (int)cols, words, mask, counts);
+                         static_cast<const char *>(x), rows, (int)cols, words, mask, counts,
+                         commit);
     else
       hipLaunchKernelGGL(measure_rowbit<4>, dim3((unsigned)gx), dim3(kLanebitThreads), 0, stream,
-                         static_cast<const char *>(x), rows, (int)cols, words, mask, counts);
+                         static_cast<const char *>(x), rows, (int)cols, words, mask, counts,
+                         commit);
     SPAROA_LAUNCH_CHECK("measure_rowbit");
     return SPAROA_OK;
   }

@@ -146,13 +146,16 @@ class Engine:
         # then the zeroed count-commit words of every fused output
         # measurement (16 lines each), reset with the counters
         cw_rows = abi.COMMIT_WORDS_BYTES // 128
-        pad += [[0] * 16] * (cw_rows * len(meas))
+        pad += [[0] * 16] * (cw_rows * (len(meas) + 1))
         self.ctr_template = torch.tensor(pad, dtype=torch.int64, device=self.dev)
         self.ctr = torch.zeros_like(self.ctr_template)
         for i, L in enumerate(layers):
             if L.kind != "maxpool":
                 self.st[i]["counts"] = self.ctr[i, :4]
         cw0 = len(layers) + len(meas)
+        # commit words of the standalone input measurements (one call at a
+        # time, each leaves them zero): after the fused outputs' words
+        self.commit_in = self.ctr[cw0 + cw_rows * len(meas):cw0 + cw_rows * (len(meas) + 1)]
         for j, (t, _, words) in enumerate(meas):
             self.tmeas[t] = dict(counts=self.ctr[len(layers) + j, :4],
                                  mask=torch.zeros(words, dtype=torch.int32, device=self.dev),
@@ -216,7 +219,7 @@ class Engine:
         else:
             counts, mask = st["counts"], st["mask"]
             abi.sparoa_measure_sparsity_preset(x, st["rows"], st["cols"], st["br"], st["bc"],
-                                               counts, mask)
+                                               counts, mask, commit=self.commit_in)
         st["used"] = (counts, mask)
         res = self.acts[L.res] if L.res is not None else None
         out = self.tmeas.get(i + 1)

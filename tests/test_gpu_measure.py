@@ -118,6 +118,7 @@ def test_measure_full_size(shape, dt, blk):
 @pytest.mark.parametrize("rows,cols,br,bc,dt", [
     (3136, 64, 1, 8, "bf16"),         # 1 x one 16-byte vector: one launch
     (100352, 96, 1, 8, "f16"),        # same, grid-stride over many work-groups
+    (262144, 64, 1, 8, "bf16"),       # 33.5 MB: 256 work-groups, two passes each
     (40, 2048, 1, 4, "f32"),          # fp32 vector
     (8, 4096, 8, 1, "bf16"),          # whole-column strips
     (37, 100, 2, 4, "bf16"),          # other blocks: initialises everything itself
@@ -137,12 +138,17 @@ def test_measure_preset_counters(rows, cols, br, bc, dt):
     owns_words = (br == 1 and bc * esz == 16) or (bc == 1 and br >= rows) or \
         (br == 1 and bc >= cols and cols * esz < 16)
     preset = [0, rows * cols, nb, nb] if owns_words else [7, 7, 7, 7]
-    for _ in range(2):    # twice: the second call starts from the preset again
+    commit = torch.zeros(abi.COMMIT_WORDS_BYTES // 8, dtype=torch.int64, device=dev)
+    # twice without and twice with commit words: each call starts from the
+    # preset again, and the commit words are left zero for the next call
+    for use_commit in (False, False, True, True):
         counts = torch.tensor(preset, dtype=torch.int64, device=dev)
         mask = torch.full((abi.sparoa_mask_words(rows, cols, br, bc),), -1, dtype=torch.int32,
                           device=dev)
-        abi.sparoa_measure_sparsity_preset(x.to(dev), rows, cols, br, bc, counts, mask)
+        abi.sparoa_measure_sparsity_preset(x.to(dev), rows, cols, br, bc, counts, mask,
+                                           commit=commit if use_commit else None)
         torch.cuda.synchronize()
         assert counts.cpu().tolist() == [ref["zeros"], ref["numel"], ref["zero_blocks"],
-                                         ref["num_blocks"]]
+                                         ref["num_blocks"]], use_commit
         assert np.array_equal(mask_np(mask), ref["mask"])
+        assert int(commit.count_nonzero().item()) == 0
