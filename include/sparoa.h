@@ -40,8 +40,11 @@ extern "C" {
 
 /* 3: the output-measuring calls take their count-commit words as an explicit
  *    argument (y_commit); the workspace queries report the split-K partial
- *    sums only. */
-#define SPAROA_ABI_VERSION 3u
+ *    sums only.
+ * 4: counts-only output measurement (y_mask NULL in *_routed_measured); a
+ *    conv's x bitmap is needed only where its skip kernel reads one
+ *    (sparoa_conv2d_reads_mask / sparoa_conv2d_routed_reads_mask). */
+#define SPAROA_ABI_VERSION 4u
 
 /* Bytes of the count-commit words of the output-measuring calls (y_commit). */
 #define SPAROA_COMMIT_WORDS_BYTES 2048
@@ -207,13 +210,15 @@ sparoa_status sparoa_route(const sparoa_counts *counts, const sparoa_intensity *
  *                                   (sparoa_conv2d_tiling gives (16, 32));
  *                                   any other groups == 1 conv runs the
  *                                   implicit GEMM.
- *   Skip paths need `mask`: the bitmap of x written by
+ *   Skip paths of the implicit GEMM need `mask`: the bitmap of x written by
  *   sparoa_measure_sparsity over the [n*h*w, c_in] view with the block shape
  *   returned by sparoa_conv2d_skip_block (one pixel x 8 channels); a
  *   work-group skips every (tile, K chunk) whose gathered input is zero:
  *   those blocks are never loaded nor multiplied.  UNSUPPORTED above
- *   K = 65536 (the routed form then runs dense).  Dense paths ignore mask.  The depthwise kernel reads
- *   every input once and skips nothing.
+ *   K = 65536 (the routed form then runs dense).  The pointwise and
+ *   small-channel kernels test x themselves and take mask == NULL
+ *   (sparoa_conv2d_reads_mask tells which).  Dense paths ignore mask.  The
+ *   depthwise kernel reads every input once and skips nothing.
  *   bias [c_out] (if desc->has_bias), residual (NHWC, output shape) nullable.
  *   executed_blocks_dev (nullable, skip paths): receives the number of
  *   executed (row tile, tap, channel block) triples; for 16-bit inputs of
@@ -224,7 +229,8 @@ sparoa_status sparoa_route(const sparoa_counts *counts, const sparoa_intensity *
  *   Workspace: sparoa_conv2d_workspace_size bytes -- the split-K partial
  *   sums (0 when the GEMM needs no K split); its contents on entry do not
  *   matter and several calls may share one workspace in stream order.
- * Errors: INVALID_ARG for bad shapes, null x/w/y, a null mask on a skip path;
+ * Errors: INVALID_ARG for bad shapes, null x/w/y, a null mask on a skip path
+ * whose kernel reads it;
  * UNSUPPORTED for grouped non-depthwise convs, unsupported dtype/path;
  * WORKSPACE if ws_bytes is below the partial-sum bytes.
  * ---------------------------------------------------------------------- */
@@ -232,6 +238,11 @@ sparoa_status sparoa_conv2d_workspace_size(const sparoa_conv_desc *desc, sparoa_
                                            size_t *bytes);
 sparoa_status sparoa_conv2d_skip_block(const sparoa_conv_desc *desc, sparoa_path path,
                                        int64_t *block_rows, int64_t *block_cols);
+/* *reads = 1 when the kernel serving `path` reads x's bitmap (the skip
+ * paths of the implicit GEMM), 0 otherwise (dense paths; the depthwise,
+ * pointwise and small-channel kernels, which test x themselves). */
+sparoa_status sparoa_conv2d_reads_mask(const sparoa_conv_desc *desc, sparoa_path path,
+                                       int *reads);
 /* Work tiling of the implicit-GEMM kernel: rows (output pixels) per tile and
  * K values per chunk, the units executed_blocks_dev counts.  UNSUPPORTED for
  * depthwise convs (not tiled). */
@@ -322,7 +333,10 @@ sparoa_status sparoa_fc_zero_skip(const sparoa_fc_desc *desc, const void *x, con
  * sparoa_route, so the path equals sparoa_route's on the same counts.  No
  * host synchronisation between measurement and execution.
  *   mask: bitmap of x at the block shape of the family's skip path
- *         (sparoa_*_skip_block with SKIP_MFMA or SKIP_BW); required.
+ *         (sparoa_*_skip_block with SKIP_MFMA or SKIP_BW).  FC: required.
+ *         Conv: required where the family's skip kernel reads it
+ *         (sparoa_conv2d_routed_reads_mask); the depthwise, pointwise and
+ *         small-channel kernels test x themselves and take NULL.
  *   FC: w_nk is used on the MFMA family, w_packed on the BW family; the
  *       other may be NULL.
  *   path_dev (nullable): receives the path taken (a uint32 sparoa_path).
@@ -337,6 +351,12 @@ sparoa_status sparoa_conv2d_routed(const sparoa_conv_desc *desc, const sparoa_th
                                    const void *bias, const void *residual, sparoa_act act,
                                    const uint32_t *mask, void *y, void *workspace,
                                    size_t ws_bytes, uint32_t *path_dev, hipStream_t stream);
+/* *reads = 1 when the kernel that serves the routed conv's skip path (the
+ * family its intensity and thr->intensity_thr select) reads x's bitmap, 0
+ * when it tests x itself (depthwise, pointwise and small-channel kernels)
+ * and the call takes mask == NULL. */
+sparoa_status sparoa_conv2d_routed_reads_mask(const sparoa_conv_desc *desc,
+                                              const sparoa_thresholds *thr, int *reads);
 sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_thresholds *thr,
                                const sparoa_counts *counts_dev, const void *x, const void *w_nk,
                                const void *w_packed, const void *bias, const void *residual,
@@ -347,11 +367,16 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
  * Routed conv / FC that also measures its own output, the next layer's input
  * (the sparsity feature of Eq. 1 is taken on a layer's output activation,
  * SparOA Section 3.1; here the producer emits it instead of a separate pass).
- *   y_counts, y_mask (device, required): afterwards they hold exactly what
- *   sparoa_measure_sparsity(y, dtype, rows, cols, 1, 8, 0, ...) gives, with
- *   rows = n*Ho*Wo, cols = c_out (FC: rows = m, cols = n) -- the block shape
- *   every conv and MFMA-family FC consumer skips at.  y_mask holds
- *   sparoa_mask_words(rows, cols, 1, 8) words and needs no clearing.
+ *   y_counts (device, required), y_mask (device, nullable): afterwards they
+ *   hold exactly what sparoa_measure_sparsity(y, dtype, rows, cols, 1, 8, 0,
+ *   ...) gives, with rows = n*Ho*Wo, cols = c_out (FC: rows = m, cols = n)
+ *   -- the block shape every conv and MFMA-family FC consumer skips at.
+ *   y_mask holds sparoa_mask_words(rows, cols, 1, 8) words and needs no
+ *   clearing.  y_mask NULL: counts only -- all four counts, no bitmap (for a
+ *   consumer that routes on the counts and reads no bitmap); 16-bit y with
+ *   cols % 8 == 0.  The depthwise kernel's counts-only form is its plain
+ *   kernel with per-lane counting; with y_mask it runs one output vector
+ *   per lane so that a wave's bits are two whole bitmap words.
  *   y_counts must hold {0, rows*cols, nb, nb} on entry, nb = rows*ceil(cols/8):
  *   the fused form adds into it (a caller resets all of a network's counters
  *   with one copy from a template before each pass).
@@ -370,7 +395,8 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
  *   same-address atomic per work-group on y_counts.  NULL: direct commits,
  *   same counts.  Calls that overlap in time must not share y_commit.
  *   Other arguments as for sparoa_conv2d_routed / sparoa_fc_routed.
- * Errors: theirs, and INVALID_ARG for a null y_counts or y_mask.
+ * Errors: theirs, and INVALID_ARG for a null y_counts, or a NULL y_mask
+ * where y is not 16-bit or cols % 8 != 0.
  * ---------------------------------------------------------------------- */
 sparoa_status sparoa_conv2d_routed_measured(const sparoa_conv_desc *desc,
                                             const sparoa_thresholds *thr,

@@ -34,7 +34,7 @@ EXPORTS = [
     "sparoa_fc_routed", "sparoa_fc_uses_packed", "sparoa_fc_ops_run",
     "sparoa_fc_measured", "sparoa_conv2d_routed_measured", "sparoa_fc_routed_measured",
     "sparoa_conv2d_split", "sparoa_fc_split", "sparoa_measure_sparsity_preset",
-    "sparoa_conv2d_noalloc",
+    "sparoa_conv2d_noalloc", "sparoa_conv2d_reads_mask", "sparoa_conv2d_routed_reads_mask",
 ]
 
 
@@ -109,6 +109,9 @@ def _load():
         "sparoa_conv2d_workspace_size": (ctypes.c_int, [P(ConvDesc), ctypes.c_int, P(sz)]),
         "sparoa_conv2d_skip_block": (ctypes.c_int, [P(ConvDesc), ctypes.c_int, P(i64), P(i64)]),
         "sparoa_conv2d_tiling": (ctypes.c_int, [P(ConvDesc), ctypes.c_int, P(i64), P(i64)]),
+        "sparoa_conv2d_reads_mask": (ctypes.c_int, [P(ConvDesc), ctypes.c_int, P(ctypes.c_int)]),
+        "sparoa_conv2d_routed_reads_mask": (ctypes.c_int, [P(ConvDesc), P(Thresholds),
+                                                           P(ctypes.c_int)]),
         "sparoa_conv2d": (ctypes.c_int, [P(ConvDesc), ctypes.c_int, vp, vp, vp, vp, ctypes.c_int,
                                          vp, vp, vp, sz, vp, vp]),
         "sparoa_conv2d_dense": (ctypes.c_int, [P(ConvDesc), vp, vp, vp, vp, ctypes.c_int, vp, vp,
@@ -292,6 +295,22 @@ def sparoa_conv2d_skip_block(desc, path):
     return _pair(_L.sparoa_conv2d_skip_block, desc, path)
 
 
+def sparoa_conv2d_reads_mask(desc, path):
+    """Whether the kernel serving `path` reads x's bitmap."""
+    v = ctypes.c_int()
+    _check(_L.sparoa_conv2d_reads_mask(ctypes.byref(desc), path, ctypes.byref(v)))
+    return bool(v.value)
+
+
+def sparoa_conv2d_routed_reads_mask(desc, sparsity_thr, intensity_thr, mode):
+    """Whether the routed conv's skip kernel reads x's bitmap (else mask may be None)."""
+    v = ctypes.c_int()
+    t = Thresholds(sparsity_thr, intensity_thr, mode)
+    _check(_L.sparoa_conv2d_routed_reads_mask(ctypes.byref(desc), ctypes.byref(t),
+                                              ctypes.byref(v)))
+    return bool(v.value)
+
+
 def sparoa_conv2d_tiling(desc, path):
     return _pair(_L.sparoa_conv2d_tiling, desc, path)
 
@@ -402,7 +421,7 @@ def sparoa_conv2d_routed_measured(desc, sparsity_thr, intensity_thr, mode, count
                                   residual, act, mask, y, y_counts, y_mask, workspace=None,
                                   path=None, y_commit=None, stream=None):
     """sparoa_conv2d_routed that also measures y into y_counts / y_mask
-    (y_commit: zeroed count-commit words, or None)."""
+    (y_mask None: counts only; y_commit: zeroed count-commit words, or None)."""
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     t = Thresholds(sparsity_thr, intensity_thr, mode)
     _check(_L.sparoa_conv2d_routed_measured(

@@ -319,7 +319,8 @@ sparoa_status sparoa_conv2d(const sparoa_conv_desc *d, sparoa_path path, const v
     return fail(SPAROA_ERR_INVALID_ARG, "conv2d: null x/w/y or bad path/act");
   if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "conv2d: has_bias without bias");
   const bool skip = (path & 1) != 0;
-  if (skip && !mask) return fail(SPAROA_ERR_INVALID_ARG, "conv2d: skip path needs a mask");
+  if (skip && !mask && !is_depthwise(*d) && conv_skip_reads_mask(*d, path))
+    return fail(SPAROA_ERR_INVALID_ARG, "conv2d: this skip path's kernel needs x's bitmap");
   if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace})) != SPAROA_OK) return st;
   if (is_depthwise(*d)) {
     if (!(path & 2)) return fail(SPAROA_ERR_UNSUPPORTED, "depthwise conv runs on the BW path");
@@ -331,6 +332,16 @@ sparoa_status sparoa_conv2d(const sparoa_conv_desc *d, sparoa_path path, const v
     return fail(SPAROA_ERR_WORKSPACE, "conv2d: workspace too small");
   return launch_gemm_conv(*d, path, x, w, d->has_bias ? bias : nullptr, residual, act,
                           skip ? mask : nullptr, y, workspace, ws_bytes, executed, stream);
+}
+
+sparoa_status sparoa_conv2d_reads_mask(const sparoa_conv_desc *d, sparoa_path path, int *reads) {
+  g_last_error.clear();
+  int64_t ho, wo;
+  sparoa_status st = check_conv(d, &ho, &wo);
+  if (st != SPAROA_OK) return st;
+  if (!reads || !path_ok(path)) return fail(SPAROA_ERR_INVALID_ARG, "reads_mask: bad argument");
+  *reads = (!is_depthwise(*d) && conv_skip_reads_mask(*d, path)) ? 1 : 0;
+  return SPAROA_OK;
 }
 
 sparoa_status sparoa_conv2d_dense(const sparoa_conv_desc *d, const void *x, const void *w,
@@ -484,6 +495,21 @@ sparoa_status check_thr(const sparoa_thresholds *thr) {
 }  // extern "C"
 
 namespace {
+// The output measurement of a *_routed_measured call: y_counts with y_mask
+// (counts and bitmap), y_counts alone (counts only: 16-bit y, cols % 8 == 0),
+// or neither.
+sparoa_status check_out_measure(const sparoa_counts *y_counts, const uint32_t *y_mask,
+                                sparoa_dtype dt, int64_t cols) {
+  if (y_mask && !y_counts)
+    return fail(SPAROA_ERR_INVALID_ARG, "routed_measured: y_mask without y_counts");
+  if (y_counts && !y_mask && (elem_size(dt) != 2 || cols % 8 != 0))
+    return fail(SPAROA_ERR_INVALID_ARG,
+                "routed_measured: counts-only measurement needs 16-bit y with cols % 8 == 0");
+  return SPAROA_OK;
+}
+}  // namespace
+
+namespace {
 // The routed conv (see sparoa_conv2d_routed).  With y_counts / y_mask
 // non-null it also measures y at block (1, 8) over [N*Ho*Wo, C_out]: in the
 // GEMM's epilogue where that is fused, else by a standalone pass after it.
@@ -497,29 +523,37 @@ sparoa_status conv_routed_impl(const sparoa_conv_desc *d, const sparoa_threshold
   sparoa_status st = sparoa_op_intensity_conv(d, &in);
   if (st != SPAROA_OK) return st;
   if ((st = check_thr(thr)) != SPAROA_OK) return st;
-  if (!counts_dev || !x || !w || !y || !mask || !act_ok(act))
-    return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed: null counts/x/w/mask/y or bad act");
+  if (!counts_dev || !x || !w || !y || !act_ok(act))
+    return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed: null counts/x/w/y or bad act");
   if (d->has_bias && !bias) return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed: has_bias without bias");
   if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace, y_counts, y_mask,
                           y_commit})) != SPAROA_OK)
     return st;
-  const bool measure_y = y_counts != nullptr;
-  if (measure_y != (y_mask != nullptr))
-    return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed_measured: null y_counts or y_mask");
   const bool dw = is_depthwise(*d);
   const int bw = (dw || in.intensity < thr->intensity_thr) ? 1 : 0;
+  if (!mask && !dw && d->groups == 1 &&
+      conv_skip_reads_mask(*d, bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA))
+    return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed: this layer's skip kernel needs x's bitmap");
   const DeviceRoute r{counts_dev, thr->sparsity_thr, thr->mode, bw, path_dev};
   int64_t ho = 0, wo = 0;
   if ((st = check_conv(d, &ho, &wo)) != SPAROA_OK) return st;
   const int64_t rows = d->n * ho * wo, cols = d->c_out;
+  const bool measure_y = y_counts != nullptr;
+  if ((st = check_out_measure(y_counts, y_mask, d->dtype, cols)) != SPAROA_OK) return st;
   auto measure_after = [&]() {
     // y_counts arrive preset ({0, numel, nb, nb}): no init launch where the
     // bitmap needs no clearing
-    return measure_y ? launch_measure(y, d->dtype, rows, cols, 1, 8, 0, y_counts, y_mask, nullptr,
-                                      stream, true, y_commit)
-                     : SPAROA_OK;
+    if (!measure_y) return SPAROA_OK;
+    return y_mask ? launch_measure(y, d->dtype, rows, cols, 1, 8, 0, y_counts, y_mask, nullptr,
+                                   stream, true, y_commit)
+                  : launch_measure_counts8(y, d->dtype, rows, cols, y_counts, y_commit, stream);
   };
   if (dw) {
+    if (measure_y && dw_fuses_out_measure(*d)) {   // y_counts arrives initialised
+      const OutMeasure om{y_counts, y_mask, reinterpret_cast<unsigned long long *>(y_commit)};
+      return launch_depthwise(*d, x, w, d->has_bias ? bias : nullptr, residual, act, y, stream,
+                              &r, &om);
+    }
     if ((st = launch_depthwise(*d, x, w, d->has_bias ? bias : nullptr, residual, act, y, stream,
                                &r)) != SPAROA_OK)
       return st;
@@ -556,6 +590,22 @@ sparoa_status sparoa_conv2d_routed(const sparoa_conv_desc *d, const sparoa_thres
                           ws_bytes, path_dev, nullptr, nullptr, nullptr, stream);
 }
 
+sparoa_status sparoa_conv2d_routed_reads_mask(const sparoa_conv_desc *d,
+                                              const sparoa_thresholds *thr, int *reads) {
+  g_last_error.clear();
+  sparoa_intensity in;
+  sparoa_status st = sparoa_op_intensity_conv(d, &in);
+  if (st != SPAROA_OK) return st;
+  if ((st = check_thr(thr)) != SPAROA_OK) return st;
+  if (!reads) return fail(SPAROA_ERR_INVALID_ARG, "routed_reads_mask: null reads");
+  const bool dw = is_depthwise(*d);
+  const int bw = (dw || in.intensity < thr->intensity_thr) ? 1 : 0;
+  *reads = (!dw && d->groups == 1 &&
+            conv_skip_reads_mask(*d, bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA))
+               ? 1 : 0;
+  return SPAROA_OK;
+}
+
 sparoa_status sparoa_conv2d_routed_measured(const sparoa_conv_desc *d,
                                             const sparoa_thresholds *thr,
                                             const sparoa_counts *counts_dev, const void *x,
@@ -565,8 +615,7 @@ sparoa_status sparoa_conv2d_routed_measured(const sparoa_conv_desc *d,
                                             sparoa_counts *y_counts, uint32_t *y_mask,
                                             uint64_t *y_commit, hipStream_t stream) {
   g_last_error.clear();
-  if (!y_counts || !y_mask)
-    return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed_measured: null y_counts or y_mask");
+  if (!y_counts) return fail(SPAROA_ERR_INVALID_ARG, "conv2d_routed_measured: null y_counts");
   return conv_routed_impl(d, thr, counts_dev, x, w, bias, residual, act, mask, y, workspace,
                           ws_bytes, path_dev, y_counts, y_mask, y_commit, stream);
 }
@@ -596,8 +645,7 @@ sparoa_status fc_routed_check(const sparoa_fc_desc *d, const sparoa_thresholds *
   if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace, y_counts, y_mask,
                           y_commit})) != SPAROA_OK)
     return st;
-  if ((y_counts != nullptr) != (y_mask != nullptr))
-    return fail(SPAROA_ERR_INVALID_ARG, "fc_routed_measured: null y_counts or y_mask");
+  if ((st = check_out_measure(y_counts, y_mask, d->dtype, d->n)) != SPAROA_OK) return st;
   if (!streams) {
     const sparoa_path p = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
     if (ws_bytes < gemm_workspace_required(fc_as_conv(*d), p))
@@ -624,10 +672,11 @@ sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *t
   const bool streams = bw && fc_bw_streams(*d);
   const void *w = streams ? w_packed : w_nk;
   const bool measure_y = y_counts != nullptr;
-  auto measure_after = [&]() {
-    return measure_y ? launch_measure(y, d->dtype, d->m, d->n, 1, 8, 0, y_counts, y_mask, nullptr,
-                                      stream, true, y_commit)   // y_counts arrive preset
-                     : SPAROA_OK;
+  auto measure_after = [&]() {   // y_counts arrive preset
+    if (!measure_y) return SPAROA_OK;
+    return y_mask ? launch_measure(y, d->dtype, d->m, d->n, 1, 8, 0, y_counts, y_mask, nullptr,
+                                   stream, true, y_commit)
+                  : launch_measure_counts8(y, d->dtype, d->m, d->n, y_counts, y_commit, stream);
   };
   const DeviceRoute r{counts_dev, thr->sparsity_thr, thr->mode, bw, path_dev};
   if (streams) {
@@ -713,8 +762,7 @@ sparoa_status sparoa_fc_routed_measured(const sparoa_fc_desc *d, const sparoa_th
                                         sparoa_counts *y_counts, uint32_t *y_mask,
                                         uint64_t *y_commit, hipStream_t stream) {
   g_last_error.clear();
-  if (!y_counts || !y_mask)
-    return fail(SPAROA_ERR_INVALID_ARG, "fc_routed_measured: null y_counts or y_mask");
+  if (!y_counts) return fail(SPAROA_ERR_INVALID_ARG, "fc_routed_measured: null y_counts");
   return fc_routed_impl(d, thr, counts_dev, x, w_nk, w_packed, bias, residual, act, mask, y,
                         workspace, ws_bytes, path_dev, stream, nullptr, y_counts, y_mask,
                         y_commit);

@@ -4,7 +4,10 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <map>
+#include <mutex>
 #include <string>
+#include <tuple>
 
 #include "sparoa.h"
 
@@ -30,6 +33,28 @@ sparoa_status hip_fail(hipError_t e, const char *what);
 inline int64_t elem_size(sparoa_dtype d) { return d == SPAROA_F32 ? 4 : 2; }
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Work-groups of kernel `fn` (`threads` threads, `lds` bytes of dynamic LDS)
+// resident on the whole current device at once: the occupancy query times the
+// compute-unit count, cached per (device, kernel, threads, LDS).  Sizes the
+// grids of persistent kernels.
+inline sparoa_status resident_blocks(const void *fn, int threads, unsigned lds, int *out) {
+  static std::mutex mu;
+  static std::map<std::tuple<int, const void *, int, unsigned>, int> cache;
+  int dev = 0;
+  SPAROA_HIP_CHECK(hipGetDevice(&dev));
+  const auto key = std::make_tuple(dev, fn, threads, lds);
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find(key);
+  if (it == cache.end()) {
+    int per_cu = 0, cus = 0;
+    SPAROA_HIP_CHECK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, lds));
+    SPAROA_HIP_CHECK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    it = cache.emplace(key, (per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1)).first;
+  }
+  *out = it->second;
+  return SPAROA_OK;
+}
 
 // Word 3 of a raw buffer descriptor on gfx9-family GPUs (32-bit data format;
 // untyped loads ignore the rest).  Buffer loads at an offset past the
@@ -84,6 +109,12 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
                              sparoa_counts *counts, uint32_t *mask, uint64_t *per_sample,
                              hipStream_t stream, bool preset = false,
                              uint64_t *commit_words = nullptr);
+// Counts only, at block (1, 8) over [rows, cols] (16-bit, cols % 8 == 0):
+// all four counts, no bitmap.  counts arrive preset {0, numel, nb, nb}
+// (commit_words as for the preset measurement).
+sparoa_status launch_measure_counts8(const void *x, sparoa_dtype dt, int64_t rows, int64_t cols,
+                                    sparoa_counts *counts, uint64_t *commit_words,
+                                    hipStream_t stream);
 
 constexpr int kGroupMax = 16;  // jobs per grouped launch
 
@@ -140,6 +171,10 @@ struct GemmTileChoice {
   bool small_c = false;  // the direct kernel for C_in <= 4 (image stems), cfg 0
   bool pointwise = false;  // the bandwidth-path 1x1 kernel (weights in LDS), cfg 0
 };
+// Whether the kernel of a groups == 1 conv's skip path reads x's bitmap
+// (false for dense paths, the pointwise and small-channel kernels, which test
+// x themselves, and shapes without a skip kernel).
+bool conv_skip_reads_mask(const sparoa_conv_desc &d, sparoa_path path);
 GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path path);
 bool gemm_skip_supported(const sparoa_conv_desc &d);
 // Workspace bytes a GEMM call needs (split-K partials).
@@ -172,10 +207,13 @@ sparoa_status launch_pointwise(const sparoa_conv_desc &d, const void *x, const v
 // Writes v to *p on the stream with a one-lane kernel (no memset node).
 sparoa_status launch_set_u64(uint64_t *p, uint64_t v, hipStream_t stream);
 
-// Depthwise direct conv (groups == c_in == c_out).
+// Depthwise direct conv (groups == c_in == c_out); om: measure y in the
+// kernel (only when dw_fuses_out_measure).
+bool dw_fuses_out_measure(const sparoa_conv_desc &d);
 sparoa_status launch_depthwise(const sparoa_conv_desc &d, const void *x, const void *w,
                                const void *bias, const void *residual, sparoa_act act, void *y,
-                               hipStream_t stream, const DeviceRoute *route = nullptr);
+                               hipStream_t stream, const DeviceRoute *route = nullptr,
+                               const OutMeasure *om = nullptr);
 
 // FC weight-streaming (bandwidth) kernel over k-major packed weights.
 size_t fc_packed_bytes(const sparoa_fc_desc &d);

@@ -10,6 +10,7 @@
 // wave cover consecutive channel vectors, then consecutive pixels, so every
 // load and store is a coalesced 16-byte access; HBM sees each input and
 // output byte about once.
+#include "commit.h"
 #include "common.h"
 #include "dtype.h"
 
@@ -27,6 +28,9 @@ struct DwArgs {
   int kh, kw, sh, sw, ph, pw, dh, dw;
   int act;
   DeviceRoute route;
+  sparoa_counts *om_counts = nullptr;   // non-null: measure y (fused; see dw3x3_kernel)
+  uint32_t *om_mask = nullptr;
+  unsigned long long *om_words = nullptr;
 };
 
 template <int DT, int V>
@@ -154,120 +158,243 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv &f) {
 }
 
 // 3x3 depthwise, padding 1, stride S in both directions, 16-byte channel
-// vectors.  An item is (n, oh, run of run3<S>() output pixels, channel vector);
-// the grid stride is a multiple of the channel-vector count, so a thread
-// keeps one channel vector for its whole life and loads its 9 x V weights
-// once (nine 16-byte loads: w[c][3][3] is contiguous over the V channels).
-// Per item, the 3 x NC input vectors the run needs are loaded unconditionally
-// (clamped addresses, zeroed outside the image) so they are all in flight
-// at once; each is decoded once and feeds every (output, tap) pair that
-// uses it.  Run length: 4 outputs over 6 input columns at stride 1; 2 outputs
-// over 5 columns at stride 2 (more lanes in flight, measured faster there).
-template <int S>
-constexpr int run3() { return S == 1 ? 4 : 2; }
-
-template <int DT, int S>
-__global__ __launch_bounds__(kThreads) void dw3x3_kernel(DwArgs a, FastDiv fcv, FastDiv fruns, FastDiv fho) {
-  using E = Elem<DT>;
-  using raw = typename E::raw;
-  constexpr int ESZ = E::size;
-  constexpr int V = 16 / ESZ;
-  constexpr int R = run3<S>();
-  constexpr int NC = (R - 1) * S + 3;  // input columns per kernel row
-  const int64_t cv = a.C / V;
-  const int64_t runs = (a.Wo + R - 1) / R;
-  const int64_t total = a.N * a.Ho * runs * cv;
-  const int64_t stride = (int64_t)gridDim.x * kThreads;
-  if (a.route.counts && a.route.path_out && blockIdx.x == 0 && threadIdx.x == 0)
-    *a.route.path_out = (device_route_skip(a.route) ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
-  int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x;
-  if (i >= total) return;
-  const int64_t c0 = (int64_t)((uint32_t)i - fdiv((uint32_t)i, fcv) * (uint32_t)cv) * V;
-  float wv[9][V];
-  {
+// vectors.  An item is (n, oh, run of R output pixels, channel vector), R
+// dividing Wo so runs never cross a row (pixel-run pr = item / cv covers
+// pixels pr * R .. pr * R + R - 1); a thread keeps one channel vector for its
+// whole life and loads its 9 x V weights once (nine 16-byte loads: w[c][3][3]
+// is contiguous over the V channels).  Per item, the 3 x NC input vectors the
+// run needs are loaded unconditionally (clamped addresses, zeroed outside the
+// image) so they are all in flight at once; each is decoded once and feeds
+// every (output, tap) pair that uses it.
+template <int DT>
+struct Dw3Lane {
+  static constexpr int V = 16 / Elem<DT>::size;
+  // weights stay in their 16-bit form (half the registers of fp32 copies);
+  // fp16 products then map to mixed-precision FMAs with no conversions
+  typename Elem<DT>::raw wv[9][V];
+  float bv[V];
+  __device__ __forceinline__ void load(const DwArgs &a, int64_t c0) {
+    using E = Elem<DT>;
+    using raw = typename E::raw;
     raw we[9 * V];
 #pragma unroll
     for (int t = 0; t < 9; ++t) {
-      const uint4 q = *reinterpret_cast<const uint4 *>(a.w + (c0 * 9 + t * V) * ESZ);
+      const uint4 q = *reinterpret_cast<const uint4 *>(a.w + (c0 * 9 + t * V) * E::size);
       __builtin_memcpy(&we[t * V], &q, 16);
     }
 #pragma unroll
     for (int j = 0; j < V; ++j)
 #pragma unroll
-      for (int t = 0; t < 9; ++t) wv[t][j] = E::to_f32(we[j * 9 + t]);
-  }
-  float bv[V];
-  if (a.bias) {
-    load_vec<DT, V>(a.bias + c0 * ESZ, bv);
-  } else {
+      for (int t = 0; t < 9; ++t) wv[t][j] = we[j * 9 + t];
+    if (a.bias) {
+      load_vec<DT, V>(a.bias + c0 * E::size, bv);
+    } else {
 #pragma unroll
-    for (int j = 0; j < V; ++j) bv[j] = 0.f;
+      for (int j = 0; j < V; ++j) bv[j] = 0.f;
+    }
   }
+};
+
+// One item in flight: its output position and its 3 x NC input vectors.
+template <int S, int R>
+struct Dw3Item {
+  static constexpr int NC = (R - 1) * S + 3;  // input columns per kernel row
+  int64_t o;            // element offset of the run's first output vector
+  uint4 xin[3][NC];
+};
+
+// Issues the input loads of item i (buffer loads: a tap outside the image
+// takes an offset past the descriptor's range and reads zero without a
+// memory access -- no branch, no select; x is under 2^31 bytes).
+template <int DT, int S, int R>
+__device__ __forceinline__ void dw3_fetch(const DwArgs &a, __amdgpu_buffer_rsrc_t xrs, uint32_t i,
+                                          int64_t c0, const FastDiv &fcv, const FastDiv &fruns,
+                                          const FastDiv &fho, Dw3Item<S, R> &it) {
+  constexpr int ESZ = Elem<DT>::size;
+  constexpr int NC = Dw3Item<S, R>::NC;
   const int H = (int)a.H, W = (int)a.W;
-  for (; i < total; i += stride) {
-    const uint32_t rest = fdiv((uint32_t)i, fcv);
-    const uint32_t rest2 = fdiv(rest, fruns);
-    const int run = (int)(rest - rest2 * (uint32_t)runs);
-    const uint32_t n32 = fdiv(rest2, fho);
-    const int oh = (int)(rest2 - n32 * (uint32_t)a.Ho);
-    const int64_t n = n32;
-    const int ow0 = run * R;
-    const int ih0 = oh * S - 1, iw0 = ow0 * S - 1;
-    uint4 xin[3][NC];
+  const uint32_t runs = (uint32_t)(a.Wo / R);
+  const uint32_t rest = fdiv(i, fcv);   // pixel-run
+  const uint32_t rest2 = fdiv(rest, fruns);
+  const int run = (int)(rest - rest2 * runs);
+  const uint32_t n32 = fdiv(rest2, fho);
+  const int oh = (int)(rest2 - n32 * (uint32_t)a.Ho);
+  const int64_t n = n32;
+  const int ow0 = run * R;
+  const int ih0 = oh * S - 1, iw0 = ow0 * S - 1;
+  it.o = ((n * a.Ho + oh) * a.Wo + ow0) * a.C + c0;
+  const uint32_t pix_bytes = (uint32_t)(a.C * ESZ);
 #pragma unroll
-    for (int r = 0; r < 3; ++r) {
-      const int ih = ih0 + r;
-      const bool rv = ih >= 0 && ih < H;
-      const int ihc = min(max(ih, 0), H - 1);
-      const char *rowp = a.x + (((n * H + ihc) * W) * a.C + c0) * ESZ;
+  for (int r = 0; r < 3; ++r) {
+    const int ih = ih0 + r;
+    const bool rv = ih >= 0 && ih < H;
+    const uint32_t row_off = (uint32_t)((n * H + ih) * W) * pix_bytes + (uint32_t)(c0 * ESZ);
 #pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        const int iw = iw0 + c;
-        const bool v = rv && iw >= 0 && iw < W;
-        const int iwc = min(max(iw, 0), W - 1);
-        const uint4 q = *reinterpret_cast<const uint4 *>(rowp + (int64_t)iwc * a.C * ESZ);
-        xin[r][c] = v ? q : make_uint4(0u, 0u, 0u, 0u);
-      }
-    }
-    float acc[R][V];
-#pragma unroll
-    for (int q = 0; q < R; ++q)
-#pragma unroll
-      for (int j = 0; j < V; ++j) acc[q][j] = bv[j];
-#pragma unroll
-    for (int r = 0; r < 3; ++r)
-#pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        raw e[V];
-        __builtin_memcpy(e, &xin[r][c], 16);
-        float xv[V];
-#pragma unroll
-        for (int j = 0; j < V; ++j) xv[j] = E::to_f32(e[j]);
-#pragma unroll
-        for (int q = 0; q < R; ++q) {
-          const int s = c - q * S;  // tap column that reads input column c for output q
-          if (s < 0 || s > 2) continue;
-#pragma unroll
-          for (int j = 0; j < V; ++j) acc[q][j] = fmaf(xv[j], wv[r * 3 + s][j], acc[q][j]);
-        }
-      }
-#pragma unroll
-    for (int q = 0; q < R; ++q) {
-      const int ow = ow0 + q;
-      if (ow >= a.Wo) continue;
-      const int64_t o = ((n * a.Ho + oh) * a.Wo + ow) * a.C + c0;
-      if (a.residual) {
-        float rv[V];
-        load_vec<DT, V>(a.residual + o * ESZ, rv);
-#pragma unroll
-        for (int j = 0; j < V; ++j) acc[q][j] += rv[j];
-      }
-      float v[V];
-#pragma unroll
-      for (int j = 0; j < V; ++j) v[j] = apply_act(acc[q][j], a.act);
-      store_vec<DT, V>(a.y + o * ESZ, v);
+    for (int c = 0; c < NC; ++c) {
+      const int iw = iw0 + c;
+      const bool v = rv && iw >= 0 && iw < W;
+      const uint32_t off = v ? row_off + (uint32_t)iw * pix_bytes : 0x80000000u;
+      it.xin[r][c] =
+          __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xrs, off, 0, 0));
     }
   }
+}
+
+// Computes and stores the item's R output vectors.  Returns bit q set iff
+// output vector q has a nonzero element; adds its zero elements to *zeros.
+template <int DT, int S, int R, bool COUNT>
+__device__ __forceinline__ uint32_t dw3_finish(const DwArgs &a, const Dw3Lane<DT> &l,
+                                               const Dw3Item<S, R> &it, uint32_t *zeros) {
+  using E = Elem<DT>;
+  using raw = typename E::raw;
+  constexpr int ESZ = E::size;
+  constexpr int V = Dw3Lane<DT>::V;
+  constexpr int NC = Dw3Item<S, R>::NC;
+  float acc[R][V];
+#pragma unroll
+  for (int q = 0; q < R; ++q)
+#pragma unroll
+    for (int j = 0; j < V; ++j) acc[q][j] = l.bv[j];
+#pragma unroll
+  for (int r = 0; r < 3; ++r)
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      raw e[V];
+      __builtin_memcpy(e, &it.xin[r][c], 16);
+      float xv[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) xv[j] = E::to_f32(e[j]);
+#pragma unroll
+      for (int q = 0; q < R; ++q) {
+        const int s = c - q * S;  // tap column that reads input column c for output q
+        if (s < 0 || s > 2) continue;
+#pragma unroll
+        for (int j = 0; j < V; ++j)
+          acc[q][j] = fmaf(xv[j], E::to_f32(l.wv[r * 3 + s][j]), acc[q][j]);
+      }
+    }
+  uint32_t nzbits = 0;
+#pragma unroll
+  for (int q = 0; q < R; ++q) {
+    const int64_t o = it.o + q * a.C;
+    if (a.residual) {
+      float rv[V];
+      load_vec<DT, V>(a.residual + o * ESZ, rv);
+#pragma unroll
+      for (int j = 0; j < V; ++j) acc[q][j] += rv[j];
+    }
+    raw t[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      t[j] = E::from_f32(apply_act(acc[q][j], a.act));
+      if (COUNT) {
+        const bool z = (t[j] & E::mag_mask) == 0u;   // +0 or -0
+        *zeros += z ? 1u : 0u;
+        nzbits |= z ? 0u : (1u << q);
+      }
+    }
+    uint4 qv;
+    __builtin_memcpy(&qv, t, 16);
+    *reinterpret_cast<uint4 *>(a.y + o * ESZ) = qv;
+  }
+  return nzbits;
+}
+
+template <int DT>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t dw3_x_rsrc(const DwArgs &a) {
+  return __builtin_amdgcn_make_buffer_rsrc((void *)a.x, (short)0,
+                                           (int)(a.N * a.H * a.W * a.C * Elem<DT>::size),
+                                           kBufDword3);
+}
+
+// Work-groups are dispatched to the 8 XCDs round robin (b -> XCD b % 8), each
+// XCD with its own L2.  With nb % 8 == 0 this maps them to logical blocks so
+// that each XCD walks one contiguous eighth of the items: adjacent output
+// rows, which read two of their three input rows in common, then share an L2
+// (consecutive ids would put them on different XCDs and fetch every input
+// row three times from HBM).  A bijection on [0, nb) either way.
+__device__ __forceinline__ int64_t xcd_block(int64_t b, int64_t nb) {
+  return (nb & 7) ? b : (b & 7) * (nb >> 3) + (b >> 3);
+}
+
+// Plain walk: a grid of up to 4096 work-groups (most lanes get a single
+// item) striding over items by a multiple of cv, so a thread's channel
+// vector never changes.  The first item's inputs are requested before the
+// lane's weights, so both arrive in one round trip.  COUNT: the counts-only
+// output measurement (Section 3.1, Eq. 1, at block (1 pixel, 8 channels) =
+// one output vector, no bitmap): zeros and nonzero vectors per lane, one
+// ticketed commit per work-group.
+template <int DT, int S, int R, bool COUNT>
+__global__ __launch_bounds__(kThreads) void dw3x3_kernel(DwArgs a, FastDiv fcv, FastDiv fruns,
+                                                        FastDiv fho) {
+  const int64_t cv = a.C / Dw3Lane<DT>::V;
+  const int64_t total = a.N * a.Ho * (a.Wo / R) * cv;
+  if (a.route.counts && a.route.path_out && blockIdx.x == 0 && threadIdx.x == 0)
+    *a.route.path_out = (device_route_skip(a.route) ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+  int64_t i = xcd_block(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
+  if (!COUNT && i >= total) return;   // (COUNT: every thread reaches the commit)
+  uint32_t zeros = 0, nz = 0;
+  if (i < total) {
+    const int64_t c0 = (int64_t)((uint32_t)i - fdiv((uint32_t)i, fcv) * (uint32_t)cv) *
+                       Dw3Lane<DT>::V;
+    const __amdgpu_buffer_rsrc_t xrs = dw3_x_rsrc<DT>(a);
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    Dw3Item<S, R> it;
+    dw3_fetch<DT, S, R>(a, xrs, (uint32_t)i, c0, fcv, fruns, fho, it);
+    Dw3Lane<DT> l;
+    l.load(a, c0);
+    for (;;) {
+      const uint32_t bits = dw3_finish<DT, S, R, COUNT>(a, l, it, &zeros);
+      if (COUNT) nz += (uint32_t)__popc(bits);
+      i += stride;
+      if (i >= total) break;
+      dw3_fetch<DT, S, R>(a, xrs, (uint32_t)i, c0, fcv, fruns, fho, it);
+    }
+  }
+  if (COUNT) om_commit(zeros, nz, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
+}
+
+// Measured walk: the same convolution with the output measurement of
+// Section 3.1 (Eq. 1) on y, bitmap at block (1 pixel, 8 channels) = one
+// output vector.  One output vector per lane (runs of 1), so the item index
+// is the block index and a wave's 64 items, starting at a multiple of 64,
+// are two whole bitmap words: the wave ballots them and two lanes store them
+// (no atomics, no clearing).  The grid stride is a multiple of 64 and of cv.
+// A persistent grid: each work-group ends in a returning count commit, paid
+// once per resident work-group rather than once per 256 items.
+template <int DT, int S>
+__global__ __launch_bounds__(kThreads) void dw3x3_measured_kernel(DwArgs a, FastDiv fcv,
+                                                                 FastDiv fwo, FastDiv fho,
+                                                                 int64_t om_words) {
+  const int lane = threadIdx.x & 63;
+  const int64_t cv = a.C / Dw3Lane<DT>::V;
+  const int64_t total = a.N * a.Ho * a.Wo * cv;
+  if (a.route.counts && a.route.path_out && blockIdx.x == 0 && threadIdx.x == 0)
+    *a.route.path_out = (device_route_skip(a.route) ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+  const int64_t first = xcd_block(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
+  const int64_t c0 = (int64_t)((uint32_t)first - fdiv((uint32_t)first, fcv) * (uint32_t)cv) *
+                     Dw3Lane<DT>::V;
+  const __amdgpu_buffer_rsrc_t xrs = dw3_x_rsrc<DT>(a);
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  uint32_t zeros = 0, nz = 0;
+  Dw3Item<S, 1> it;
+  if (first < total) dw3_fetch<DT, S, 1>(a, xrs, (uint32_t)first, c0, fcv, fwo, fho, it);
+  Dw3Lane<DT> l;
+  l.load(a, c0);
+  for (int64_t base = first - lane; base < total; base += stride) {   // wave-uniform
+    const int64_t i = base + lane, next = i + stride;
+    Dw3Item<S, 1> nx;
+    if (next < total) dw3_fetch<DT, S, 1>(a, xrs, (uint32_t)next, c0, fcv, fwo, fho, nx);
+    uint32_t bits = 0;
+    if (i < total) bits = dw3_finish<DT, S, 1, true>(a, l, it, &zeros);
+    const uint64_t bal = __ballot(bits != 0u);
+    const int64_t w0 = base >> 5;
+    if (lane == 0 && w0 < om_words) a.om_mask[w0] = (uint32_t)bal;
+    if (lane == 32 && w0 + 1 < om_words) a.om_mask[w0 + 1] = (uint32_t)(bal >> 32);
+    nz += lane == 0 ? (uint32_t)__popcll(bal) : 0u;
+    it = nx;
+  }
+  om_commit(zeros, nz, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
 }
 
 template <int DT, int V>
@@ -302,6 +429,76 @@ __global__ __launch_bounds__(kThreads) void maxpool_kernel(const char *x, char *
   }
 }
 
+// Run length of the 3x3 kernel: 4 outputs along w at stride 1 where 4
+// divides Wo, else 2 where Wo is even, else 1 (a run never crosses a row).
+// Longer runs re-read fewer input columns per output.
+int dw_run(int64_t wo, int64_t s) {
+  if (s == 1 && wo % 4 == 0) return 4;
+  return wo % 2 == 0 ? 2 : 1;
+}
+
+bool dw_fast3(const DwArgs &a, int esz) {
+  return a.C % (16 / esz) == 0 && a.kh == 3 && a.kw == 3 && a.ph == 1 && a.pw == 1 &&
+         a.dh == 1 && a.dw == 1 && a.sh == a.sw && (a.sh == 1 || a.sh == 2);
+}
+
+int64_t gcd64(int64_t a, int64_t b) {
+  while (b) { const int64_t t = a % b; a = b; b = t; }
+  return a;
+}
+
+// Work-group count of a walk over `items` whose stride (nb x 256 items) must
+// be a multiple of cv: a multiple of q = cv / gcd(256, cv) and of 8 (XCD
+// mapping), at most `cap` unless one multiple is more.
+int64_t dw_grid(int64_t items, int64_t cv, int64_t cap) {
+  const int64_t q = cv / gcd64(kThreads, cv);
+  const int64_t unit = q * 8 / gcd64(q, 8);
+  int64_t nb = cdiv(items, kThreads);
+  if (nb > cap) nb = cap;
+  nb = cdiv(nb, unit) * unit;
+  return nb;
+}
+
+template <int DT, int S, int R>
+sparoa_status launch_dw3(const DwArgs &a, hipStream_t st, const FastDiv &fcv, int64_t cv) {
+  const int64_t runs = a.Wo / R;
+  const int64_t items = a.N * a.Ho * runs * cv;
+  const FastDiv fruns = make_fastdiv((uint32_t)runs), fho = make_fastdiv((uint32_t)a.Ho);
+  const int64_t nb = dw_grid(items, cv, 4096);
+  if (a.om_counts)   // counts only (no bitmap)
+    hipLaunchKernelGGL((dw3x3_kernel<DT, S, R, true>), dim3((unsigned)nb), dim3(kThreads), 0, st,
+                       a, fcv, fruns, fho);
+  else
+    hipLaunchKernelGGL((dw3x3_kernel<DT, S, R, false>), dim3((unsigned)nb), dim3(kThreads), 0,
+                       st, a, fcv, fruns, fho);
+  SPAROA_LAUNCH_CHECK("dw3x3_kernel");
+  return SPAROA_OK;
+}
+
+template <int DT, int S>
+sparoa_status launch_dw3_measured(const DwArgs &a, hipStream_t st, const FastDiv &fcv,
+                                  int64_t cv) {
+  const int64_t items = a.N * a.Ho * a.Wo * cv;
+  const void *fn = reinterpret_cast<const void *>(&dw3x3_measured_kernel<DT, S>);
+  int resident = 0;
+  if (sparoa_status st2 = resident_blocks(fn, kThreads, 0, &resident); st2 != SPAROA_OK)
+    return st2;
+  const int64_t nb = dw_grid(items, cv, resident);
+  const int64_t om_words = cdiv(items, 32);
+  hipLaunchKernelGGL((dw3x3_measured_kernel<DT, S>), dim3((unsigned)nb), dim3(kThreads), 0, st,
+                     a, fcv, make_fastdiv((uint32_t)a.Wo), make_fastdiv((uint32_t)a.Ho),
+                     om_words);
+  SPAROA_LAUNCH_CHECK("dw3x3_measured_kernel");
+  return SPAROA_OK;
+}
+
+// The 3x3 fast path's limits: item indices and the grid stride stay below
+// 2^31 (32-bit divisions), x below 2^31 bytes (32-bit buffer offsets).
+bool dw3_fits(const DwArgs &a, int esz) {
+  return dw_fast3(a, esz) && a.N * a.Ho * a.Wo * (a.C / (16 / esz)) < (1ll << 30) &&
+         a.N * a.H * a.W * a.C * esz < (1ll << 31);
+}
+
 template <int DT>
 sparoa_status dw_dispatch(const DwArgs &a, hipStream_t st) {
   constexpr int VV = 16 / Elem<DT>::size;
@@ -311,29 +508,28 @@ sparoa_status dw_dispatch(const DwArgs &a, hipStream_t st) {
   int64_t blocks = cdiv(total, kThreads);
   if (blocks > 65536) blocks = 65536;
   const bool k3 = a.kh == 3 && a.kw == 3;
-  const bool fast3 = vec && k3 && a.ph == 1 && a.pw == 1 && a.dh == 1 && a.dw == 1 &&
-                     a.sh == a.sw && (a.sh == 1 || a.sh == 2);
-  const int64_t cv = a.C / VV;
-  const int64_t runs = cdiv(a.Wo, a.sh == 1 ? run3<1>() : run3<2>());
-  const int64_t items = a.N * a.Ho * runs * cv;
-  // item indices and the grid stride stay below 2^31 (32-bit divisions)
-  if (fast3 && items < (1ll << 30)) {
-    // the grid stride must be a multiple of the channel-vector count
-    int64_t g = 256, c = cv;
-    while (c) { const int64_t t = g % c; g = c; c = t; }  // gcd(256, cv)
-    const int64_t q = cv / g;
-    int64_t nb = cdiv(items, kThreads);
-    if (nb > 4096) nb = 4096;
-    nb = cdiv(nb, q) * q;
-    const FastDiv fcv = make_fastdiv((uint32_t)cv), fruns = make_fastdiv((uint32_t)runs),
-                  fho = make_fastdiv((uint32_t)a.Ho);
-    if (a.sh == 1)
-      hipLaunchKernelGGL((dw3x3_kernel<DT, 1>), dim3((unsigned)nb), dim3(kThreads), 0, st, a, fcv, fruns, fho);
-    else
-      hipLaunchKernelGGL((dw3x3_kernel<DT, 2>), dim3((unsigned)nb), dim3(kThreads), 0, st, a, fcv, fruns, fho);
-    SPAROA_LAUNCH_CHECK("dw3x3_kernel");
-    return SPAROA_OK;
+  if (dw3_fits(a, Elem<DT>::size)) {
+    const int64_t cv = a.C / VV;
+    const FastDiv fcv = make_fastdiv((uint32_t)cv);
+    if (a.om_counts) {
+      if constexpr (Elem<DT>::size == 2) {
+        if (a.om_mask)   // the bitmap too: one output vector per lane
+          return a.sh == 1 ? launch_dw3_measured<DT, 1>(a, st, fcv, cv)
+                           : launch_dw3_measured<DT, 2>(a, st, fcv, cv);
+      } else {
+        return fail(SPAROA_ERR_UNSUPPORTED, "depthwise: no fused output measurement");
+      }
+    }
+    const int R = dw_run(a.Wo, a.sh);
+    if (a.sh == 1) {
+      if (R == 4) return launch_dw3<DT, 1, 4>(a, st, fcv, cv);
+      if (R == 2) return launch_dw3<DT, 1, 2>(a, st, fcv, cv);
+      return launch_dw3<DT, 1, 1>(a, st, fcv, cv);
+    }
+    if (R == 2) return launch_dw3<DT, 2, 2>(a, st, fcv, cv);
+    return launch_dw3<DT, 2, 1>(a, st, fcv, cv);
   }
+  if (a.om_counts) return fail(SPAROA_ERR_UNSUPPORTED, "depthwise: no fused output measurement");
   if (vec && k3)
     hipLaunchKernelGGL((depthwise_kernel<DT, VV, 3, 3>), dim3((unsigned)blocks), dim3(kThreads), 0, st, a);
   else if (vec)
@@ -366,23 +562,42 @@ sparoa_status mp_dispatch(const void *x, void *y, int64_t n, int64_t c, int64_t 
 
 }  // namespace
 
-sparoa_status launch_depthwise(const sparoa_conv_desc &d, const void *x, const void *w,
-                               const void *bias, const void *residual, sparoa_act act, void *y,
-                               hipStream_t stream, const DeviceRoute *route) {
-  if (d.kh * d.kw > kMaxTaps) return fail(SPAROA_ERR_UNSUPPORTED, "depthwise window above 5x5");
+namespace {
+DwArgs dw_args(const sparoa_conv_desc &d) {
   DwArgs a;
-  a.x = static_cast<const char *>(x);
-  a.w = static_cast<const char *>(w);
-  a.bias = static_cast<const char *>(bias);
-  a.residual = static_cast<const char *>(residual);
-  a.y = static_cast<char *>(y);
   a.N = d.n; a.H = d.h; a.W = d.w; a.C = d.c_in;
   a.Ho = (d.h + 2 * d.ph - d.dh * (d.kh - 1) - 1) / d.sh + 1;
   a.Wo = (d.w + 2 * d.pw - d.dw * (d.kw - 1) - 1) / d.sw + 1;
   a.kh = (int)d.kh; a.kw = (int)d.kw; a.sh = (int)d.sh; a.sw = (int)d.sw;
   a.ph = (int)d.ph; a.pw = (int)d.pw; a.dh = (int)d.dh; a.dw = (int)d.dw;
+  return a;
+}
+}  // namespace
+
+bool dw_fuses_out_measure(const sparoa_conv_desc &d) {
+  return elem_size(d.dtype) == 2 && dw3_fits(dw_args(d), 2);   // one output vector = one block
+}
+
+sparoa_status launch_depthwise(const sparoa_conv_desc &d, const void *x, const void *w,
+                               const void *bias, const void *residual, sparoa_act act, void *y,
+                               hipStream_t stream, const DeviceRoute *route,
+                               const OutMeasure *om) {
+  if (om && !dw_fuses_out_measure(d))
+    return fail(SPAROA_ERR_UNSUPPORTED, "depthwise: no fused output measurement for this shape");
+  if (d.kh * d.kw > kMaxTaps) return fail(SPAROA_ERR_UNSUPPORTED, "depthwise window above 5x5");
+  DwArgs a = dw_args(d);
+  a.x = static_cast<const char *>(x);
+  a.w = static_cast<const char *>(w);
+  a.bias = static_cast<const char *>(bias);
+  a.residual = static_cast<const char *>(residual);
+  a.y = static_cast<char *>(y);
   a.act = act;
   a.route = route ? *route : DeviceRoute{nullptr, 0.0, 0, 0, nullptr};
+  if (om) {
+    a.om_counts = om->counts;
+    a.om_mask = om->mask;
+    a.om_words = om->words;
+  }
   switch (d.dtype) {
     case SPAROA_BF16: return dw_dispatch<SPAROA_BF16>(a, stream);
     case SPAROA_F16: return dw_dispatch<SPAROA_F16>(a, stream);

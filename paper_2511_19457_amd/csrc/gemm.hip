@@ -401,9 +401,9 @@ __global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
   // output measurement: vector v = block v at (1 row, 8 channels); a wave's
   // 64 consecutive vectors are two whole bitmap words (as in measure_lanebit)
   sparoa_counts *om = E::size == 2 ? g.om_counts[j] : nullptr;
-  uint32_t *om_mask = g.om_mask[j];
+  uint32_t *om_mask = g.om_mask[j];   // null: counts only
   const int lane = threadIdx.x & 63;
-  const int64_t om_words = (total / 8 + 31) / 32;
+  const int64_t om_words = om_mask ? (total / 8 + 31) / 32 : 0;
   uint32_t om_zeros = 0, om_nz = 0;
   if (N % 8 == 0) {
     for (int64_t v = b0 * 256 + threadIdx.x; v < total / 8; v += nb * 256) {
@@ -941,7 +941,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
     __syncthreads();
     // rows past M still clear their bytes when they lie inside the bitmap's
     // last word (bits past the last block are 0)
-    const int64_t mbytes = 4 * ((a.M * (a.N / 8) + 31) / 32);
+    const int64_t mbytes = a.om_mask ? 4 * ((a.M * (a.N / 8) + 31) / 32) : 0;   // null: counts only
     for (int r = tid; r < BM; r += NT) {
       const int64_t row = m0 + r, byte = row * (a.N / 64) + n0 / 64;
       if (byte >= mbytes) continue;   // (BN / 64 bytes of a row lie in one word)
@@ -1458,6 +1458,12 @@ bool gemm_skip_supported(const sparoa_conv_desc &d) {
 }
 
 
+bool conv_skip_reads_mask(const sparoa_conv_desc &d, sparoa_path path) {
+  if (!(path & 1) || d.groups != 1 || !gemm_skip_supported(d)) return false;
+  const GemmTileChoice t = gemm_choose(d, path);
+  return !(t.pointwise || t.small_c);
+}
+
 GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path path) {
   const Shape s = shape_of(d);
   GemmTileChoice t;
@@ -1533,7 +1539,9 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
     return fail(SPAROA_ERR_UNSUPPORTED, "GEMM: no fused output measurement for this shape");
   const int epv = d.dtype == SPAROA_F32 ? 4 : 8;
   const bool vec = d.c_in % epv == 0;
-  const bool skip = mask != nullptr;
+  // the skip form: x's bitmap given, or a skip path on a kernel that tests x
+  // itself (the pointwise and small-channel kernels read no bitmap)
+  const bool skip = mask != nullptr || ((path & 1) && (t.pointwise || t.small_c));
   const int64_t nchunks = cdiv(s.K, t.kchunk);
   if (skip && !gemm_skip_supported(d))
     return fail(SPAROA_ERR_UNSUPPORTED, "zero-skip conv: K above the skip kernel's 65536");

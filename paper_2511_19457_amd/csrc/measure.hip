@@ -589,6 +589,29 @@ sparoa_status launch_measure_group(const MeasureJob *jobs, int n, hipStream_t st
   return SPAROA_OK;
 }
 
+sparoa_status launch_measure_counts8(const void *x, sparoa_dtype dt, int64_t rows, int64_t cols,
+                                    sparoa_counts *counts, uint64_t *commit_words,
+                                    hipStream_t stream) {
+  if (elem_size(dt) != 2 || cols % 8 != 0)
+    return fail(SPAROA_ERR_INVALID_ARG, "counts-only measurement: 16-bit data, cols % 8 == 0");
+  // the lanebit layout with no bitmap words: item = block = one 16-byte vector
+  const int64_t items = rows * (cols / 8);
+  const char *xc = static_cast<const char *>(x);
+  if (items <= 4096) {   // one work-group writes all four counts
+    hipLaunchKernelGGL((measure_lanebit_wg<2, 8>), dim3(1), dim3(1024), 0, stream, xc, items,
+                       (int64_t)0, (uint32_t *)nullptr, counts);
+    SPAROA_LAUNCH_CHECK("measure_lanebit_wg");
+    return SPAROA_OK;
+  }
+  int64_t gx = cdiv(items, (int64_t)kLanebitThreads);
+  if (gx > 256) gx = 256;
+  hipLaunchKernelGGL((measure_lanebit<2, 8>), dim3((unsigned)gx), dim3(kLanebitThreads), 0, stream,
+                     xc, items, (int64_t)0, (uint32_t *)nullptr, counts,
+                     reinterpret_cast<unsigned long long *>(commit_words));
+  SPAROA_LAUNCH_CHECK("measure_lanebit");
+  return SPAROA_OK;
+}
+
 sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64_t cols,
                              int64_t block_rows, int64_t block_cols, int64_t samples,
                              sparoa_counts *counts, uint32_t *mask, uint64_t *per_sample,
@@ -649,9 +672,11 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
 
   if (lanebit) {
     const int64_t items = rows * (cols / vw);
-    // each lane's kLanebitUnroll loads in flight cover the tensor once where
-    // it is small (fewer work-groups to commit), at most one per CU
-    int64_t gx = cdiv(items, (int64_t)kLanebitThreads * kLanebitUnroll);
+    // one work-group per CU where the tensor fills them (one item per lane
+    // at the least); with commit words a work-group's commit costs two
+    // returning atomics spread over 16 addresses, so a small tensor is spread
+    // over as many compute units as it has 1024-item slots
+    int64_t gx = cdiv(items, (int64_t)kLanebitThreads);
     if (gx > 256) gx = 256;
     if (esz == 2)
       hipLaunchKernelGGL((measure_lanebit<2, 8>), dim3((unsigned)gx), dim3(kLanebitThreads), 0,

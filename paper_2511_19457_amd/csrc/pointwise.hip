@@ -30,10 +30,6 @@
 // one slice the epilogue also counts the zeros of y and builds its bitmap at
 // block (1 pixel, 8 channels); a tile's bitmap words meet in LDS (tiles start
 // on 32-bit word boundaries) and leave as whole-word stores.
-#include <map>
-#include <mutex>
-#include <tuple>
-
 #include "commit.h"
 #include "common.h"
 #include "dtype.h"
@@ -403,24 +399,6 @@ const void *pw_kernel(int nb, int r, int ks) {
 
 // Work-groups of `fn` that fit on the current device at once (occupancy
 // query, cached per device, kernel and LDS size).
-sparoa_status pw_resident(const void *fn, unsigned lds, int *out) {
-  static std::mutex mu;
-  static std::map<std::tuple<int, const void *, unsigned>, int> cache;
-  int dev = 0;
-  SPAROA_HIP_CHECK(hipGetDevice(&dev));
-  const auto key = std::make_tuple(dev, fn, lds);
-  std::lock_guard<std::mutex> lock(mu);
-  auto it = cache.find(key);
-  if (it == cache.end()) {
-    int per_cu = 0, cus = 0;
-    SPAROA_HIP_CHECK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kPwThreads, lds));
-    SPAROA_HIP_CHECK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-    it = cache.emplace(key, (per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1)).first;
-  }
-  *out = it->second;
-  return SPAROA_OK;
-}
-
 }  // namespace
 
 bool pw_eligible(const sparoa_conv_desc &d) {
@@ -469,7 +447,7 @@ sparoa_status launch_pointwise(const sparoa_conv_desc &d, const void *x, const v
   a.om_counts = om ? om->counts : nullptr;
   a.om_mask = om ? om->mask : nullptr;
   a.om_words = om ? om->words : nullptr;
-  a.om_mask_words = (a.M * (int64_t)(d.c_out / 8) + 31) / 32;
+  a.om_mask_words = a.om_mask ? (a.M * (int64_t)(d.c_out / 8) + 31) / 32 : 0;   // null: counts only
   const unsigned lds = (unsigned)(c.nb * 16 * c.row_bytes);
   const void *fn = d.dtype == SPAROA_BF16 ? pw_kernel<SPAROA_BF16>(c.nb, c.r, c.ksi)
                                           : pw_kernel<SPAROA_F16>(c.nb, c.r, c.ksi);
@@ -477,7 +455,8 @@ sparoa_status launch_pointwise(const sparoa_conv_desc &d, const void *x, const v
   // persistent work-groups, as many as are resident at once, each bound to
   // one slice: every work-group stages its weights once for many tiles
   int resident = 0;
-  if (sparoa_status st = pw_resident(fn, lds, &resident); st != SPAROA_OK) return st;
+  if (sparoa_status st = resident_blocks(fn, kPwThreads, lds, &resident); st != SPAROA_OK)
+    return st;
   int64_t per_slice = resident / c.slices;
   if (per_slice < 1) per_slice = 1;
   if (per_slice > a.tiles) per_slice = a.tiles;

@@ -157,10 +157,22 @@ class Engine:
         # time, each leaves them zero): after the fused outputs' words
         self.commit_in = self.ctr[cw0 + cw_rows * len(meas):cw0 + cw_rows * (len(meas) + 1)]
         for j, (t, _, words) in enumerate(meas):
-            self.tmeas[t] = dict(counts=self.ctr[len(layers) + j, :4],
-                                 mask=torch.zeros(words, dtype=torch.int32, device=self.dev),
+            # the bitmap only where a consumer's skip kernel reads it (FC
+            # consumers, implicit-GEMM convs); the others route on the counts
+            # and the producer measures counts only
+            need_mask = any(layers[k].src == t and layers[k].kind != "maxpool" and
+                            self._reads_mask(k) for k in range(len(layers)))
+            mask = torch.zeros(words, dtype=torch.int32, device=self.dev) if need_mask else None
+            self.tmeas[t] = dict(counts=self.ctr[len(layers) + j, :4], mask=mask,
                                  commit=self.ctr[cw0 + cw_rows * j:cw0 + cw_rows * (j + 1)])
         torch.cuda.synchronize(self.dev)
+
+    def _reads_mask(self, k):
+        """Whether layer k's routed call needs its input's bitmap."""
+        if self.layers[k].kind != "conv":
+            return True
+        return abi.sparoa_conv2d_routed_reads_mask(self.st[k]["desc"], self.s_thr, self.c_thr,
+                                                   self.mode)
 
     def reset_counters(self):
         """Preset values of every counter of a routed pass (a kernel, not a

@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert abi.sparoa_abi_version() == 3
+    assert abi.sparoa_abi_version() == 4
     assert abi.sparoa_status_string(0) == "ok"
     assert abi.sparoa_status_string(3) == "workspace too small"
 
@@ -200,6 +200,53 @@ def test_tiling_and_skip_block_queries():
     # two layouts of 16-column panels: k-major, then 32-k chunks (k rounded up)
     assert abi.sparoa_fc_packed_bytes(f) == 2 * 4096 * 4096 * 2
     assert abi.sparoa_fc_packed_bytes(abi.fc_desc(1, 100, 65)) == 80 * 100 * 2 + 80 * 128 * 2
+
+
+def test_reads_mask_queries():
+    """Which conv kernels read x's bitmap: the implicit GEMM's skip forms;
+    not the dense paths, nor the kernels that test x themselves."""
+    c3 = abi.conv_desc(2, 64, 14, 14, 64, 3, 3, 1, 1, 1, 1)
+    assert abi.sparoa_conv2d_reads_mask(c3, abi.PATH_SKIP_MFMA)
+    assert not abi.sparoa_conv2d_reads_mask(c3, abi.PATH_DENSE_MFMA)
+    pw = abi.conv_desc(2, 64, 56, 56, 96, 1, 1)          # the pointwise kernel on the BW path
+    assert abi.sparoa_conv2d_tiling(pw, abi.PATH_SKIP_BW) == (16, 32)
+    assert not abi.sparoa_conv2d_reads_mask(pw, abi.PATH_SKIP_BW)
+    assert abi.sparoa_conv2d_reads_mask(pw, abi.PATH_SKIP_MFMA)
+    dw = abi.conv_desc(2, 32, 16, 16, 32, 3, 3, 1, 1, 1, 1, groups=32)
+    assert not abi.sparoa_conv2d_reads_mask(dw, abi.PATH_SKIP_BW)
+    stem = abi.conv_desc(32, 3, 224, 224, 64, 7, 7, 2, 2, 3, 3)
+    assert not abi.sparoa_conv2d_reads_mask(stem, abi.PATH_SKIP_MFMA)
+    # the routed form: the family the intensity threshold selects
+    inten = abi.sparoa_op_intensity_conv(pw)["intensity"]
+    assert not abi.sparoa_conv2d_routed_reads_mask(pw, 0.5, inten * 2, abi.ROUTE_BLOCK)
+    assert abi.sparoa_conv2d_routed_reads_mask(pw, 0.5, 0.0, abi.ROUTE_BLOCK)
+    assert not abi.sparoa_conv2d_routed_reads_mask(dw, 0.5, 0.0, abi.ROUTE_BLOCK)
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"),
+                    reason="host-only check: the fake device pointers must never reach a GPU")
+def test_counts_only_and_null_mask_validation():
+    """Rejected before any device work: a counts-only output measurement of
+    fp32 or cols % 8 != 0, y_mask without y_counts, and a null x bitmap for a
+    routed conv whose skip kernel reads one."""
+    c3 = abi.conv_desc(2, 64, 14, 14, 64, 3, 3, 1, 1, 1, 1)
+    for desc, y_counts, y_mask in ((abi.conv_desc(2, 64, 14, 14, 64, 3, 3, 1, 1, 1, 1,
+                                                  dtype=abi.F32), FAKE, None),
+                                   (abi.conv_desc(2, 64, 14, 14, 60, 3, 3, 1, 1, 1, 1), FAKE,
+                                    None),
+                                   (c3, None, FAKE)):
+        with pytest.raises(abi.SparoaError) as e:
+            abi.sparoa_conv2d_routed_measured(desc, 0.5, 0.0, abi.ROUTE_BLOCK, FAKE, FAKE, FAKE,
+                                              None, None, 0, FAKE, FAKE, y_counts, y_mask, None)
+        assert e.value.status == 1
+    with pytest.raises(abi.SparoaError) as e:
+        abi.sparoa_conv2d_routed(c3, 0.5, 0.0, abi.ROUTE_BLOCK, FAKE, FAKE, FAKE, None, None, 0,
+                                 None, FAKE)
+    assert e.value.status == 1
+    with pytest.raises(abi.SparoaError) as e:
+        abi.sparoa_fc_routed_measured(abi.fc_desc(64, 256, 100), 0.5, 0.0, abi.ROUTE_BLOCK, FAKE,
+                                      FAKE, FAKE, None, None, None, 0, FAKE, FAKE, FAKE, None)
+    assert e.value.status == 1
 
 
 @pytest.mark.skipif(os.path.exists("/dev/kfd"),

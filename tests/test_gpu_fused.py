@@ -25,10 +25,12 @@ def _fresh_counts(rows, cols, dev):
 
 
 def _check_y_measurement(abi, y, rows, cols, y_counts, y_mask, what):
+    """y_mask None: a counts-only measurement (the four counts, no bitmap)."""
     ref = oracle.measure(y.cpu(), rows, cols, 1, 8)
     assert y_counts.cpu().tolist() == [ref["zeros"], ref["numel"], ref["zero_blocks"],
                                        ref["num_blocks"]], what
-    assert np.array_equal(y_mask.cpu().numpy().view(np.uint32), ref["mask"]), what
+    if y_mask is not None:
+        assert np.array_equal(y_mask.cpu().numpy().view(np.uint32), ref["mask"]), what
 
 
 CONV_CASES = [
@@ -98,6 +100,97 @@ def test_conv_routed_measured(case):
                                           abi.ACT_RELU, mask, y, y_counts, y_mask, ws)
         torch.cuda.synchronize()
         _check_y_measurement(abi, y, rows, cols, y_counts, y_mask, f"{case} direct commits")
+    if dt != "f32":   # counts only (no bitmap): fused or standalone, same counts
+        for s_thr in (0.0, 2.0):
+            y = torch.full((n, ho, wo, cout), float("nan"), dtype=tdt, device=dev)
+            y_counts = _fresh_counts(rows, cols, dev)
+            abi.sparoa_conv2d_routed_measured(d, s_thr, 0.0, abi.ROUTE_BLOCK, counts, x, wt, b, r,
+                                              abi.ACT_RELU, mask, y, y_counts, None, ws, None,
+                                              commit)
+            y2 = torch.full_like(y, float("nan"))
+            abi.sparoa_conv2d_routed(d, s_thr, 0.0, abi.ROUTE_BLOCK, counts, x, wt, b, r,
+                                     abi.ACT_RELU, mask, y2, ws)
+            torch.cuda.synchronize()
+            assert torch.equal(y, y2), f"{case} counts only s_thr {s_thr}"
+            _check_y_measurement(abi, y, rows, cols, y_counts, None,
+                                 f"{case} counts only s_thr {s_thr}")
+            assert int(commit.count_nonzero().item()) == 0
+
+
+DW_CASES = [
+    # n, c, h, w, stride, dtype: MobileNetV2 depthwise shapes and ragged ones;
+    # the 16-bit 3x3 cases measure in the kernel, fp32 in a standalone pass
+    (2, 144, 56, 56, 1, "f16"),    # 18 channel vectors per pixel
+    (2, 96, 112, 112, 2, "bf16"),  # stride 2
+    (3, 384, 14, 14, 1, "bf16"),
+    (3, 576, 14, 14, 2, "f16"),    # stride 2, Wo 7
+    (2, 24, 13, 15, 1, "bf16"),    # odd Wo, 3 channel vectors per pixel
+    (2, 960, 7, 7, 1, "bf16"),     # 120 vectors per pixel
+    (1, 8, 5, 3, 1, "f16"),        # fewer items than one wave
+    (2, 32, 9, 9, 1, "f32"),       # fp32: standalone pass
+]
+
+
+@pytest.mark.parametrize("case", DW_CASES)
+def test_depthwise_routed_measured(case):
+    """The depthwise kernel measuring its own output: counts and bitmap equal
+    the oracle's measurement, y equals the unmeasured call's bit for bit and
+    the oracle's conv within tolerance; with and without commit words.  The
+    bias drives whole 8-channel groups below zero so zero blocks occur."""
+    from tests._util import RTOL, assert_close
+    abi = _abi()
+    dev = torch.device("cuda")
+    n, c, h, w, s, dt = case
+    tdt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[dt]
+    d = abi.conv_desc(n, c, h, w, c, 3, 3, s, s, 1, 1, 1, 1, c, tdt, has_bias=True)
+    ho, wo = (h + 2 - 3) // s + 1, (w + 2 - 3) // s + 1
+    seed = 1500 + DW_CASES.index(case) * 5
+    x = synth.relu_normal((n, h, w, c), dt, seed)
+    wt = synth.he_normal((c, 3, 3, 1), 9, dt, seed + 1)
+    b = synth.normal((c,), dt, seed + 2).float()
+    b[(torch.arange(c) // 8) % 3 == 0] = -20.0
+    b = b.to(tdt)
+    r = synth.normal((n, ho, wo, c), dt, seed + 3)
+    xd, wd, bd, rd = x.to(dev), wt.to(dev), b.to(dev), r.to(dev)
+    counts = torch.zeros(4, dtype=torch.int64, device=dev)
+    mask = torch.zeros(abi.sparoa_mask_words(n * h * w, c, 1, 8), dtype=torch.int32, device=dev)
+    abi.sparoa_measure_sparsity(xd, n * h * w, c, 1, 8, 0, counts, mask)
+    ws = torch.zeros(16, dtype=torch.uint8, device=dev)
+    commit = torch.zeros(abi.COMMIT_WORDS_BYTES // 8, dtype=torch.int64, device=dev)
+    rows = n * ho * wo
+    y2 = torch.full((n, ho, wo, c), float("nan"), dtype=tdt, device=dev)
+    abi.sparoa_conv2d_routed(d, 0.5, 0.0, abi.ROUTE_BLOCK, counts, xd, wd, bd, rd,
+                             abi.ACT_RELU, mask, y2, ws)
+    torch.cuda.synchronize()
+    yr, ar, _ = oracle.conv2d(x, wt, n, c, h, w, c, 3, 3, s, s, 1, 1, 1, 1, c, bias=b,
+                              residual=r, act=abi.ACT_RELU)
+    assert_close(y2.cpu(), yr, ar, RTOL[tdt], f"depthwise {case}")
+    for words in (commit, None):
+        for rep in range(2):
+            y = torch.full_like(y2, float("nan"))
+            y_counts = _fresh_counts(rows, c, dev)
+            y_mask = torch.full((abi.sparoa_mask_words(rows, c, 1, 8),), -1, dtype=torch.int32,
+                                device=dev)
+            abi.sparoa_conv2d_routed_measured(d, 0.5, 0.0, abi.ROUTE_BLOCK, counts, xd, wd, bd, rd,
+                                              abi.ACT_RELU, mask, y, y_counts, y_mask, ws, None,
+                                              words)
+            torch.cuda.synchronize()
+            what = f"{case} commit words {words is not None} rep {rep}"
+            assert torch.equal(y, y2), what
+            _check_y_measurement(abi, y, rows, c, y_counts, y_mask, what)
+            assert int(commit.count_nonzero().item()) == 0
+    if dt != "f32":   # counts only: the plain kernel counting per lane
+        for words in (commit, None):
+            y = torch.full_like(y2, float("nan"))
+            y_counts = _fresh_counts(rows, c, dev)
+            abi.sparoa_conv2d_routed_measured(d, 0.5, 0.0, abi.ROUTE_BLOCK, counts, xd, wd, bd, rd,
+                                              abi.ACT_RELU, mask, y, y_counts, None, ws, None,
+                                              words)
+            torch.cuda.synchronize()
+            what = f"{case} counts only, commit words {words is not None}"
+            assert torch.equal(y, y2), what
+            _check_y_measurement(abi, y, rows, c, y_counts, None, what)
+            assert int(commit.count_nonzero().item()) == 0
 
 
 FC_CASES = [
@@ -149,6 +242,60 @@ def test_fc_routed_measured(case):
                                       None, abi.ACT_RELU, mask, y, y_counts, y_mask, ws)
         torch.cuda.synchronize()
         _check_y_measurement(abi, y, m, n, y_counts, y_mask, f"{case} direct commits")
+    if n % 8 == 0:   # counts only (no bitmap)
+        y_counts = _fresh_counts(m, n, dev)
+        y = torch.full_like(y2, float("nan"))
+        abi.sparoa_fc_routed_measured(d, 0.5, c_thr, abi.ROUTE_BLOCK, counts, x, w, wp, None,
+                                      None, abi.ACT_RELU, mask, y, y_counts, None, ws, None,
+                                      commit)
+        torch.cuda.synchronize()
+        assert torch.equal(y, y2)
+        _check_y_measurement(abi, y, m, n, y_counts, None, f"{case} counts only")
+        assert int(commit.count_nonzero().item()) == 0
+
+
+POINTWISE_NO_MASK = [
+    # n, cin, h, w, cout, dtype: 1x1 convs the pointwise kernel serves on the BW path
+    (4, 64, 28, 28, 96, "f16"),
+    (2, 32, 56, 56, 144, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", POINTWISE_NO_MASK)
+def test_pointwise_consumer_without_bitmap(case):
+    """A routed 1x1 conv on the pointwise kernel routes on x's counts and
+    tests x itself: it takes no bitmap, and its output equals the call's
+    with one, on the skip and the dense route."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    n, cin, h, w, cout, dt = case
+    tdt = torch.float16 if dt == "f16" else torch.bfloat16
+    d = abi.conv_desc(n, cin, h, w, cout, 1, 1, 1, 1, 0, 0, 1, 1, 1, tdt)
+    c_thr = abi.sparoa_op_intensity_conv(d)["intensity"] * 2   # the BW family
+    assert not abi.sparoa_conv2d_routed_reads_mask(d, 0.5, c_thr, abi.ROUTE_BLOCK)
+    seed = 1600 + POINTWISE_NO_MASK.index(case) * 3
+    x = synth.sparse_matrix(n * h * w, cin, 0.6, "block", dt, seed).reshape(n, h, w, cin).to(dev)
+    wt = synth.he_normal((cout, 1, 1, cin), cin, dt, seed + 1).to(dev)
+    counts = torch.zeros(4, dtype=torch.int64, device=dev)
+    mask = torch.zeros(abi.sparoa_mask_words(n * h * w, cin, 1, 8), dtype=torch.int32, device=dev)
+    abi.sparoa_measure_sparsity(x, n * h * w, cin, 1, 8, 0, counts, mask)
+    ws = torch.zeros(16, dtype=torch.uint8, device=dev)
+    for s_thr in (0.0, 2.0):
+        y = torch.full((n, h, w, cout), float("nan"), dtype=tdt, device=dev)
+        y2 = torch.full_like(y, float("nan"))
+        p1 = torch.full((1,), -1, dtype=torch.int32, device=dev)
+        p2 = torch.full((1,), -1, dtype=torch.int32, device=dev)
+        abi.sparoa_conv2d_routed(d, s_thr, c_thr, abi.ROUTE_BLOCK, counts, x, wt, None, None,
+                                 abi.ACT_RELU, None, y, ws, p1)
+        abi.sparoa_conv2d_routed(d, s_thr, c_thr, abi.ROUTE_BLOCK, counts, x, wt, None, None,
+                                 abi.ACT_RELU, mask, y2, ws, p2)
+        torch.cuda.synchronize()
+        assert int(p1.item()) == int(p2.item()) == (abi.PATH_SKIP_BW if s_thr == 0.0
+                                                    else abi.PATH_DENSE_BW)
+        assert torch.equal(y, y2), f"{case} s_thr {s_thr}"
+        yr, ar, _ = oracle.conv2d(x.cpu(), wt.cpu(), n, cin, h, w, cout, 1, 1, act=abi.ACT_RELU)
+        from tests._util import RTOL, assert_close
+        assert_close(y.cpu(), yr, ar, RTOL[tdt], f"{case} s_thr {s_thr}")
 
 
 def test_shared_workspace_split_k_then_fused():
