@@ -354,14 +354,13 @@ __global__ __launch_bounds__(kThreads) void dw3x3_kernel(DwArgs a, FastDiv fcv, 
   if (COUNT) om_commit(zeros, nz, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
 }
 
-// Measured walk: the same convolution with the output measurement of
-// Section 3.1 (Eq. 1) on y, bitmap at block (1 pixel, 8 channels) = one
-// output vector.  One output vector per lane (runs of 1), so the item index
-// is the block index and a wave's 64 items, starting at a multiple of 64,
-// are two whole bitmap words: the wave ballots them and two lanes store them
-// (no atomics, no clearing).  The grid stride is a multiple of 64 and of cv.
-// A persistent grid: each work-group ends in a returning count commit, paid
-// once per resident work-group rather than once per 256 items.
+// Measured walk with the bitmap: the same convolution with the output
+// measurement of Section 3.1 (Eq. 1) on y, bitmap at block (1 pixel, 8
+// channels) = one output vector.  One output vector per lane (runs of 1), so
+// the item index is the block index and a wave's 64 items, starting at a
+// multiple of 64, are two whole bitmap words: the wave ballots them and two
+// lanes store them (no atomics, no clearing).  The grid stride (as in the
+// plain walk, up to 4096 work-groups) is a multiple of 64 and of cv.
 template <int DT, int S>
 __global__ __launch_bounds__(kThreads) void dw3x3_measured_kernel(DwArgs a, FastDiv fcv,
                                                                  FastDiv fwo, FastDiv fho,
@@ -382,9 +381,7 @@ __global__ __launch_bounds__(kThreads) void dw3x3_measured_kernel(DwArgs a, Fast
   Dw3Lane<DT> l;
   l.load(a, c0);
   for (int64_t base = first - lane; base < total; base += stride) {   // wave-uniform
-    const int64_t i = base + lane, next = i + stride;
-    Dw3Item<S, 1> nx;
-    if (next < total) dw3_fetch<DT, S, 1>(a, xrs, (uint32_t)next, c0, fcv, fwo, fho, nx);
+    const int64_t i = base + lane;
     uint32_t bits = 0;
     if (i < total) bits = dw3_finish<DT, S, 1, true>(a, l, it, &zeros);
     const uint64_t bal = __ballot(bits != 0u);
@@ -392,7 +389,7 @@ __global__ __launch_bounds__(kThreads) void dw3x3_measured_kernel(DwArgs a, Fast
     if (lane == 0 && w0 < om_words) a.om_mask[w0] = (uint32_t)bal;
     if (lane == 32 && w0 + 1 < om_words) a.om_mask[w0 + 1] = (uint32_t)(bal >> 32);
     nz += lane == 0 ? (uint32_t)__popcll(bal) : 0u;
-    it = nx;
+    if (i + stride < total) dw3_fetch<DT, S, 1>(a, xrs, (uint32_t)(i + stride), c0, fcv, fwo, fho, it);
   }
   om_commit(zeros, nz, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
 }
@@ -479,11 +476,7 @@ template <int DT, int S>
 sparoa_status launch_dw3_measured(const DwArgs &a, hipStream_t st, const FastDiv &fcv,
                                   int64_t cv) {
   const int64_t items = a.N * a.Ho * a.Wo * cv;
-  const void *fn = reinterpret_cast<const void *>(&dw3x3_measured_kernel<DT, S>);
-  int resident = 0;
-  if (sparoa_status st2 = resident_blocks(fn, kThreads, 0, &resident); st2 != SPAROA_OK)
-    return st2;
-  const int64_t nb = dw_grid(items, cv, resident);
+  const int64_t nb = dw_grid(items, cv, 4096);
   const int64_t om_words = cdiv(items, 32);
   hipLaunchKernelGGL((dw3x3_measured_kernel<DT, S>), dim3((unsigned)nb), dim3(kThreads), 0, st,
                      a, fcv, make_fastdiv((uint32_t)a.Wo), make_fastdiv((uint32_t)a.Ho),
