@@ -142,8 +142,9 @@ sparoa_status sparoa_measure_sparsity(const void *x_dev, sparoa_dtype dtype, int
  * already set to {0, rows*cols, nb, nb} (nb = ceil(rows/block_rows) *
  * ceil(cols/block_cols); a caller resets many counters with one copy): for
  * the block shapes whose bitmap needs no clearing -- 1 row x one 16-byte
- * vector, 1 row x block_cols >= cols for rows narrower than 16 bytes, or
- * whole columns (block_rows >= rows, block_cols == 1) -- the call is then
+ * vector, 1 row x 8 fp32 columns (cols % 8 == 0), 1 row x block_cols >= cols
+ * for rows narrower than 16 bytes, or whole columns (block_rows >= rows,
+ * block_cols == 1) -- the call is then
  * one launch instead of two.  Other block shapes initialise everything as
  * sparoa_measure_sparsity does.  commit_dev (nullable): zeroed count-commit
  * words (SPAROA_COMMIT_WORDS_BYTES, zero on entry, zero again when the call's
@@ -373,8 +374,7 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
  *   -- the block shape every conv and MFMA-family FC consumer skips at.
  *   y_mask holds sparoa_mask_words(rows, cols, 1, 8) words and needs no
  *   clearing.  y_mask NULL: counts only -- all four counts, no bitmap (for a
- *   consumer that routes on the counts and reads no bitmap); 16-bit y with
- *   cols % 8 == 0.  The depthwise kernel's counts-only form is its plain
+ *   consumer that routes on the counts and reads no bitmap); cols % 8 == 0.  The depthwise kernel's counts-only form is its plain
  *   kernel with per-lane counting; with y_mask it runs one output vector
  *   per lane so that a wave's bits are two whole bitmap words.
  *   y_counts must hold {0, rows*cols, nb, nb} on entry, nb = rows*ceil(cols/8):
@@ -396,7 +396,7 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
  *   same counts.  Calls that overlap in time must not share y_commit.
  *   Other arguments as for sparoa_conv2d_routed / sparoa_fc_routed.
  * Errors: theirs, and INVALID_ARG for a null y_counts, or a NULL y_mask
- * where y is not 16-bit or cols % 8 != 0.
+ * where cols % 8 != 0.
  * ---------------------------------------------------------------------- */
 sparoa_status sparoa_conv2d_routed_measured(const sparoa_conv_desc *desc,
                                             const sparoa_thresholds *thr,

@@ -496,15 +496,15 @@ sparoa_status check_thr(const sparoa_thresholds *thr) {
 
 namespace {
 // The output measurement of a *_routed_measured call: y_counts with y_mask
-// (counts and bitmap), y_counts alone (counts only: 16-bit y, cols % 8 == 0),
-// or neither.
+// (counts and bitmap), y_counts alone (counts only: cols % 8 == 0), or
+// neither.
 sparoa_status check_out_measure(const sparoa_counts *y_counts, const uint32_t *y_mask,
-                                sparoa_dtype dt, int64_t cols) {
+                                int64_t cols) {
   if (y_mask && !y_counts)
     return fail(SPAROA_ERR_INVALID_ARG, "routed_measured: y_mask without y_counts");
-  if (y_counts && !y_mask && (elem_size(dt) != 2 || cols % 8 != 0))
+  if (y_counts && !y_mask && cols % 8 != 0)
     return fail(SPAROA_ERR_INVALID_ARG,
-                "routed_measured: counts-only measurement needs 16-bit y with cols % 8 == 0");
+                "routed_measured: counts-only measurement needs cols % 8 == 0");
   return SPAROA_OK;
 }
 }  // namespace
@@ -539,7 +539,7 @@ sparoa_status conv_routed_impl(const sparoa_conv_desc *d, const sparoa_threshold
   if ((st = check_conv(d, &ho, &wo)) != SPAROA_OK) return st;
   const int64_t rows = d->n * ho * wo, cols = d->c_out;
   const bool measure_y = y_counts != nullptr;
-  if ((st = check_out_measure(y_counts, y_mask, d->dtype, cols)) != SPAROA_OK) return st;
+  if ((st = check_out_measure(y_counts, y_mask, cols)) != SPAROA_OK) return st;
   auto measure_after = [&]() {
     // y_counts arrive preset ({0, numel, nb, nb}): no init launch where the
     // bitmap needs no clearing
@@ -645,7 +645,7 @@ sparoa_status fc_routed_check(const sparoa_fc_desc *d, const sparoa_thresholds *
   if ((st = check_ptrs16({x, w, bias, residual, y, mask, workspace, y_counts, y_mask,
                           y_commit})) != SPAROA_OK)
     return st;
-  if ((st = check_out_measure(y_counts, y_mask, d->dtype, d->n)) != SPAROA_OK) return st;
+  if ((st = check_out_measure(y_counts, y_mask, d->n)) != SPAROA_OK) return st;
   if (!streams) {
     const sparoa_path p = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
     if (ws_bytes < gemm_workspace_required(fc_as_conv(*d), p))

@@ -140,6 +140,16 @@ __device__ __forceinline__ uint32_t nonzero_bits(const char *p) {
   return nz;
 }
 
+// The V elements of one lanebit item (one block of 1 x V): a 16-byte vector,
+// or two of them for fp32 blocks of 8 (32 contiguous bytes per lane).
+template <int ESZ, int V>
+__device__ __forceinline__ uint32_t item_nonzero_bits(const char *p) {
+  if constexpr (V * ESZ == 32)
+    return nonzero_bits<ESZ, V / 2>(p) | (nonzero_bits<ESZ, V / 2>(p + 16) << (V / 2));
+  else
+    return nonzero_bits<ESZ, V>(p);
+}
+
 // grid = (x: work-groups per sample, y: samples).  Sample s covers rows
 // [s*rs, s*rs + rs); its block rows are numbered s*nbr_s + local index.
 // Work item = (block row, chunk of kRowChunk rows inside it, column group):
@@ -235,7 +245,7 @@ __device__ __forceinline__ void lanebit_pass(const char *__restrict__ x, int64_t
 #pragma unroll
     for (int u = 0; u < kLanebitUnroll; ++u) {
       const int64_t item = base + u * slot + threadIdx.x;
-      nz[u] = nonzero_bits<ESZ, V>(x + min(item, items - 1) * 16);
+      nz[u] = item_nonzero_bits<ESZ, V>(x + min(item, items - 1) * (V * ESZ));
     }
 #pragma unroll
     for (int u = 0; u < kLanebitUnroll; ++u) {
@@ -376,7 +386,7 @@ __global__ __launch_bounds__(1024) void measure_lanebit_wg(const char *__restric
 #pragma unroll
     for (int u = 0; u < U; ++u) {  // unconditional loads, masked past the end
       const int64_t item = base + u * NT + threadIdx.x;
-      nz[u] = nonzero_bits<ESZ, V>(x + min(item, items - 1) * 16);
+      nz[u] = item_nonzero_bits<ESZ, V>(x + min(item, items - 1) * (V * ESZ));
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -592,22 +602,31 @@ sparoa_status launch_measure_group(const MeasureJob *jobs, int n, hipStream_t st
 sparoa_status launch_measure_counts8(const void *x, sparoa_dtype dt, int64_t rows, int64_t cols,
                                     sparoa_counts *counts, uint64_t *commit_words,
                                     hipStream_t stream) {
-  if (elem_size(dt) != 2 || cols % 8 != 0)
-    return fail(SPAROA_ERR_INVALID_ARG, "counts-only measurement: 16-bit data, cols % 8 == 0");
-  // the lanebit layout with no bitmap words: item = block = one 16-byte vector
+  if (cols % 8 != 0)
+    return fail(SPAROA_ERR_INVALID_ARG, "counts-only measurement: cols % 8 == 0");
+  // the lanebit layout with no bitmap words: item = block = 8 elements
   const int64_t items = rows * (cols / 8);
   const char *xc = static_cast<const char *>(x);
+  const bool h = elem_size(dt) == 2;
   if (items <= 4096) {   // one work-group writes all four counts
-    hipLaunchKernelGGL((measure_lanebit_wg<2, 8>), dim3(1), dim3(1024), 0, stream, xc, items,
-                       (int64_t)0, (uint32_t *)nullptr, counts);
+    if (h)
+      hipLaunchKernelGGL((measure_lanebit_wg<2, 8>), dim3(1), dim3(1024), 0, stream, xc, items,
+                         (int64_t)0, (uint32_t *)nullptr, counts);
+    else
+      hipLaunchKernelGGL((measure_lanebit_wg<4, 8>), dim3(1), dim3(1024), 0, stream, xc, items,
+                         (int64_t)0, (uint32_t *)nullptr, counts);
     SPAROA_LAUNCH_CHECK("measure_lanebit_wg");
     return SPAROA_OK;
   }
   int64_t gx = cdiv(items, (int64_t)kLanebitThreads);
   if (gx > 256) gx = 256;
-  hipLaunchKernelGGL((measure_lanebit<2, 8>), dim3((unsigned)gx), dim3(kLanebitThreads), 0, stream,
-                     xc, items, (int64_t)0, (uint32_t *)nullptr, counts,
-                     reinterpret_cast<unsigned long long *>(commit_words));
+  unsigned long long *cw = reinterpret_cast<unsigned long long *>(commit_words);
+  if (h)
+    hipLaunchKernelGGL((measure_lanebit<2, 8>), dim3((unsigned)gx), dim3(kLanebitThreads), 0,
+                       stream, xc, items, (int64_t)0, (uint32_t *)nullptr, counts, cw);
+  else
+    hipLaunchKernelGGL((measure_lanebit<4, 8>), dim3((unsigned)gx), dim3(kLanebitThreads), 0,
+                       stream, xc, items, (int64_t)0, (uint32_t *)nullptr, counts, cw);
   SPAROA_LAUNCH_CHECK("measure_lanebit");
   return SPAROA_OK;
 }
@@ -633,14 +652,19 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
 
   const bool vec = cols % vw == 0 && (!want_mask || bc % vw == 0 || vw % bc == 0);
   // fast paths that own whole bitmap words (no atomics, no clearing)
-  const bool lanebit = want_mask && vec && br == 1 && bc == vw && !per_sample;
+  // lanebit items: one 16-byte vector, or two for fp32 blocks of 8
+  const int lv = (esz == 4 && bc == 8 && cols % 8 == 0) ? 8 : vw;
+  const bool lanebit = want_mask && vec && br == 1 && bc == lv && !per_sample;
   const bool strips = want_mask && vec && bc == 1 && !per_sample && br >= rows;
   const bool rowbit = want_mask && br == 1 && bc >= cols && cols * esz < 16 && !per_sample;
 
-  if (lanebit && rows * (cols / vw) <= 4096) {  // one work-group measures it all
-    const int64_t items = rows * (cols / vw);
+  if (lanebit && rows * (cols / lv) <= 4096) {  // one work-group measures it all
+    const int64_t items = rows * (cols / lv);
     if (esz == 2)
       hipLaunchKernelGGL((measure_lanebit_wg<2, 8>), dim3(1), dim3(1024), 0, stream,
+                         static_cast<const char *>(x), items, words, mask, counts);
+    else if (lv == 8)
+      hipLaunchKernelGGL((measure_lanebit_wg<4, 8>), dim3(1), dim3(1024), 0, stream,
                          static_cast<const char *>(x), items, words, mask, counts);
     else
       hipLaunchKernelGGL((measure_lanebit_wg<4, 4>), dim3(1), dim3(1024), 0, stream,
@@ -671,7 +695,7 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
   }
 
   if (lanebit) {
-    const int64_t items = rows * (cols / vw);
+    const int64_t items = rows * (cols / lv);
     // one work-group per CU where the tensor fills them (one item per lane
     // at the least); with commit words a work-group's commit costs two
     // returning atomics spread over 16 addresses, so a small tensor is spread
@@ -680,6 +704,9 @@ sparoa_status launch_measure(const void *x, sparoa_dtype dt, int64_t rows, int64
     if (gx > 256) gx = 256;
     if (esz == 2)
       hipLaunchKernelGGL((measure_lanebit<2, 8>), dim3((unsigned)gx), dim3(kLanebitThreads), 0,
+                         stream, static_cast<const char *>(x), items, words, mask, counts, commit);
+    else if (lv == 8)
+      hipLaunchKernelGGL((measure_lanebit<4, 8>), dim3((unsigned)gx), dim3(kLanebitThreads), 0,
                          stream, static_cast<const char *>(x), items, words, mask, counts, commit);
     else
       hipLaunchKernelGGL((measure_lanebit<4, 4>), dim3((unsigned)gx), dim3(kLanebitThreads), 0,

@@ -226,11 +226,11 @@ def test_reads_mask_queries():
 @pytest.mark.skipif(os.path.exists("/dev/kfd"),
                     reason="host-only check: the fake device pointers must never reach a GPU")
 def test_counts_only_and_null_mask_validation():
-    """Rejected before any device work: a counts-only output measurement of
-    fp32 or cols % 8 != 0, y_mask without y_counts, and a null x bitmap for a
-    routed conv whose skip kernel reads one."""
+    """Rejected before any device work: a counts-only output measurement with
+    cols % 8 != 0, y_mask without y_counts, and a null x bitmap for a routed
+    conv whose skip kernel reads one."""
     c3 = abi.conv_desc(2, 64, 14, 14, 64, 3, 3, 1, 1, 1, 1)
-    for desc, y_counts, y_mask in ((abi.conv_desc(2, 64, 14, 14, 64, 3, 3, 1, 1, 1, 1,
+    for desc, y_counts, y_mask in ((abi.conv_desc(2, 64, 14, 14, 60, 3, 3, 1, 1, 1, 1,
                                                   dtype=abi.F32), FAKE, None),
                                    (abi.conv_desc(2, 64, 14, 14, 60, 3, 3, 1, 1, 1, 1), FAKE,
                                     None),

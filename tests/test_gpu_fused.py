@@ -100,7 +100,7 @@ def test_conv_routed_measured(case):
                                           abi.ACT_RELU, mask, y, y_counts, y_mask, ws)
         torch.cuda.synchronize()
         _check_y_measurement(abi, y, rows, cols, y_counts, y_mask, f"{case} direct commits")
-    if dt != "f32":   # counts only (no bitmap): fused or standalone, same counts
+    if cout % 8 == 0:   # counts only (no bitmap): fused or standalone, same counts
         for s_thr in (0.0, 2.0):
             y = torch.full((n, ho, wo, cout), float("nan"), dtype=tdt, device=dev)
             y_counts = _fresh_counts(rows, cols, dev)
@@ -179,7 +179,7 @@ def test_depthwise_routed_measured(case):
             assert torch.equal(y, y2), what
             _check_y_measurement(abi, y, rows, c, y_counts, y_mask, what)
             assert int(commit.count_nonzero().item()) == 0
-    if dt != "f32":   # counts only: the plain kernel counting per lane
+    if c % 8 == 0:   # counts only: the plain kernel counting per lane (fp32: standalone)
         for words in (commit, None):
             y = torch.full_like(y2, float("nan"))
             y_counts = _fresh_counts(rows, c, dev)

@@ -54,6 +54,8 @@ CASES = [
     # rows narrower than 16 bytes, one block per row (one bit per row)
     (1001, 3, 1, 8, 0), (777, 1, 1, 4, 0), (3000, 7, 1, 8, 0), (4099, 3, 1, 3, 0),
     (2100001, 3, 1, 8, 0),
+    # 1 x 8 blocks of fewer than 4096 vectors (one work-group; fp32: two vectors per block)
+    (37, 64, 1, 8, 0),
 ]
 
 
@@ -120,6 +122,8 @@ def test_measure_full_size(shape, dt, blk):
     (100352, 96, 1, 8, "f16"),        # same, grid-stride over many work-groups
     (262144, 64, 1, 8, "bf16"),       # 33.5 MB: 256 work-groups, two passes each
     (40, 2048, 1, 4, "f32"),          # fp32 vector
+    (40, 2048, 1, 8, "f32"),          # fp32 blocks of 8: two vectors per lane
+    (3136, 64, 1, 8, "f32"),
     (8, 4096, 8, 1, "bf16"),          # whole-column strips
     (37, 100, 2, 4, "bf16"),          # other blocks: initialises everything itself
     (1001, 3, 1, 8, "bf16"),          # rows narrower than 16 bytes, one bit per row
@@ -136,7 +140,8 @@ def test_measure_preset_counters(rows, cols, br, bc, dt):
     nb = -(-rows // br) * -(-cols // bc)
     esz = torch.tensor([], dtype=DT[dt]).element_size()
     owns_words = (br == 1 and bc * esz == 16) or (bc == 1 and br >= rows) or \
-        (br == 1 and bc >= cols and cols * esz < 16)
+        (br == 1 and bc >= cols and cols * esz < 16) or \
+        (br == 1 and bc == 8 and esz == 4 and cols % 8 == 0)
     preset = [0, rows * cols, nb, nb] if owns_words else [7, 7, 7, 7]
     commit = torch.zeros(abi.COMMIT_WORDS_BYTES // 8, dtype=torch.int64, device=dev)
     # twice without and twice with commit words: each call starts from the
