@@ -74,6 +74,13 @@ def parse():
     p.add_argument("--stack-summary", default=None, metavar="DIR",
                    help="no GPU: turn the rocprofv3 outputs of the --stack runs under DIR into "
                         "profiles/<stack>_layers.md")
+    p.add_argument("--bw-kernels", action="store_true",
+                   help="only run the bandwidth-bound kernels on large model tensors (standalone "
+                        "measurement, depthwise with fused measurement, pointwise), --steps "
+                        "calls each: the program rocprofv3 profiles for --bw-summary")
+    p.add_argument("--bw-summary", default=None, metavar="DIR",
+                   help="no GPU: turn the rocprofv3 outputs of the --bw-kernels runs under DIR "
+                        "into profiles/bandwidth_kernels.md")
     p.add_argument("--cases-out", default=None, help="write the per-case table (JSON) here")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only run 5 plain device-to-device copies of MIB MiB and exit (the "
@@ -1122,6 +1129,176 @@ def stack_summary(d):
             f.write("\n".join(out) + "\n")
         print(f"wrote profiles/{name}_layers.md", file=sys.stderr)
 
+# ---------------------------------------------------------------------------
+# Bandwidth-bound kernels on large model tensors: the program rocprofv3 runs
+# (--bw-kernels) and the summary of its outputs (--bw-summary).
+
+BW_COMMANDS = {
+    "trace": "rocprofv3 --kernel-trace --output-format csv -d $REPO/gpurun_out/bw_trace -o trace "
+             "-- python3 $REPO/bench.py --bw-kernels --steps 20",
+    "pmc": "rocprofv3 --pmc {C} --output-format csv -d $REPO/gpurun_out/bw_pmc_{C} -o pmc -- "
+           "python3 $REPO/bench.py --bw-kernels --steps 3",
+}
+
+
+def bw_workloads(abi, torch, synth):
+    """(name, kernel-name substrings of one call, algorithmic bytes, callable) of
+    each bandwidth-bound workload, on MobileNetV2 / ResNet-50 N = 32 tensors."""
+    dev = torch.device("cuda")
+    out = []
+
+    def measure(shape, dt):
+        x = synth.relu_normal(shape, dt, synth.seed_for(4, len(out))).to(dev)
+        rows, cols = x.numel() // shape[-1], shape[-1]
+        nb = rows * cols // 8
+        preset = torch.tensor([0, rows * cols, nb, nb], dtype=torch.int64, device=dev)
+        c = preset.clone()
+        m = torch.zeros(abi.sparoa_mask_words(rows, cols, 1, 8), dtype=torch.int32, device=dev)
+        cw = torch.zeros(abi.COMMIT_WORDS_BYTES // 8, dtype=torch.int64, device=dev)
+
+        def f():
+            abi.sparoa_measure_sparsity_preset(x, rows, cols, 1, 8, c, m, commit=cw)
+        name = f"measurement {list(shape)} {dt} at (1, 8), preset counters, commit words"
+        out.append((name, ["measure_lanebit"], x.numel() * x.element_size() + m.numel() * 4, f))
+
+    def depthwise(n, c, h, s, dt):
+        tdt = torch.float16 if dt == "f16" else torch.bfloat16
+        d = abi.conv_desc(n, c, h, h, c, 3, 3, s, s, 1, 1, 1, 1, c, tdt, has_bias=True)
+        ho = (h - 1) // s + 1
+        seed = synth.seed_for(4, 10 + len(out))
+        x = synth.relu_normal((n, h, h, c), dt, seed).to(dev)
+        w = synth.he_normal((c, 3, 3, 1), 9, dt, seed + 1).to(dev)
+        b = synth.normal((c,), dt, seed + 2).to(dev)
+        y = torch.empty(n, ho, ho, c, dtype=tdt, device=dev)
+        cnt = torch.zeros(4, dtype=torch.int64, device=dev)
+        rows = n * ho * ho
+        yc = torch.tensor([0, rows * c, rows * c // 8, rows * c // 8], dtype=torch.int64,
+                          device=dev)
+        cw = torch.zeros(abi.COMMIT_WORDS_BYTES // 8, dtype=torch.int64, device=dev)
+        ws = torch.zeros(16, dtype=torch.uint8, device=dev)
+
+        def f():
+            abi.sparoa_conv2d_routed_measured(d, 2.0, 0.0, abi.ROUTE_BLOCK, cnt, x, w, b, None,
+                                              abi.ACT_RELU6, None, y, yc, None, ws, None, cw)
+        name = (f"depthwise 3x3/{s} [{n},{h},{h},{c}] {dt}, ReLU6, counts-only output "
+                "measurement fused")
+        out.append((name, ["dw3x3_kernel"], (x.numel() + y.numel() + w.numel() + c) * 2, f))
+
+    def pointwise(n, cin, h, cout, dt, residual):
+        tdt = torch.float16 if dt == "f16" else torch.bfloat16
+        d = abi.conv_desc(n, cin, h, h, cout, 1, 1, 1, 1, 0, 0, 1, 1, 1, tdt)
+        seed = synth.seed_for(4, 20 + len(out))
+        x = synth.relu_normal((n, h, h, cin), dt, seed).to(dev)
+        w = synth.he_normal((cout, 1, 1, cin), cin, dt, seed + 1).to(dev)
+        r = synth.normal((n, h, h, cout), dt, seed + 2).to(dev) if residual else None
+        y = torch.empty(n, h, h, cout, dtype=tdt, device=dev)
+        ws = torch.zeros(16, dtype=torch.uint8, device=dev)
+        assert abi.sparoa_conv2d_tiling(d, abi.PATH_DENSE_BW) == (16, 32)   # the pointwise kernel
+
+        def f():
+            abi.sparoa_conv2d(d, abi.PATH_DENSE_BW, x, w, None, r, abi.ACT_RELU, None, y, ws)
+        alg = (x.numel() + y.numel() + w.numel() + (r.numel() if residual else 0)) * 2
+        name = (f"pointwise 1x1 [{n},{h},{h},{cin}] -> {cout} {dt}"
+                + (", residual" if residual else ""))
+        out.append((name, ["pointwise_kernel"], alg, f))
+
+    measure((32, 56, 56, 256), "bf16")
+    measure((32, 112, 112, 96), "f16")
+    depthwise(32, 32, 112, 1, "f16")
+    depthwise(32, 96, 112, 2, "f16")
+    depthwise(32, 144, 56, 1, "f16")
+    pointwise(32, 16, 112, 96, "f16", False)
+    pointwise(32, 64, 56, 256, "bf16", True)
+    return out
+
+
+def bw_kernels_run(abi, torch, synth, reps):
+    """Each workload: 2 warm-up calls, then `reps` calls; prints the JSON line
+    the summary reads (workload order, kernel names, algorithmic bytes)."""
+    work = bw_workloads(abi, torch, synth)
+    torch.cuda.synchronize()
+    rows = []
+    for name, kern, alg, f in work:
+        for _ in range(2 + reps):
+            f()
+        torch.cuda.synchronize()
+        rows.append(dict(name=name, kernels=kern, alg_bytes=alg, calls=2 + reps))
+    print(json.dumps(dict(bw_kernels=rows, reps=reps)), flush=True)
+
+
+def bw_summary(d):
+    """profiles/bandwidth_kernels.md from the --bw-kernels runs under d: per
+    workload the kernel's average duration over its timed calls (kernel
+    trace) and its HBM bytes per call (FETCH_SIZE and WRITE_SIZE, each scaled
+    by what it reads for a plain 256 MiB copy)."""
+    from collections import defaultdict
+    scale = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        rows = _csv_rows(os.path.join(d, f"pmc_copy_{c}"), "*counter_collection.csv")
+        vals = sorted(float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"])
+        vals = vals[-5:]
+        scale[c] = 256 * 1024.0 / (sum(vals) / len(vals))
+
+    def walk(dispatches, line):
+        """Dispatches (dispatch order) of each workload's calls, by kernel name."""
+        res, i = [], 0
+        for w in line["bw_kernels"]:
+            got = []
+            while i < len(dispatches) and len(got) < w["calls"]:
+                if any(k in dispatches[i][0] for k in w["kernels"]):
+                    got.append(dispatches[i])
+                i += 1
+            res.append(got[2:])   # the timed calls
+        return res
+
+    line_t = _bench_line(os.path.join(d, "bw_trace.log"), key="bw_kernels")
+    tr = _csv_rows(os.path.join(d, "bw_trace"), "*kernel_trace.csv")
+    tr.sort(key=lambda r: int(r["Dispatch_Id"]))
+    disp = [(r["Kernel_Name"], (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+            for r in tr]
+    times = walk(disp, line_t)
+    cnt = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        line_c = _bench_line(os.path.join(d, f"bw_pmc_{c}.log"), key="bw_kernels")
+        rows = _csv_rows(os.path.join(d, f"bw_pmc_{c}"), "*counter_collection.csv")
+        by = defaultdict(float)
+        names = {}
+        for r in rows:
+            by[int(r["Dispatch_Id"])] += float(r["Counter_Value"])
+            names[int(r["Dispatch_Id"])] = r["Kernel_Name"]
+        disp_c = [(names[k], by[k]) for k in sorted(by)]
+        cnt[c] = walk(disp_c, line_c)
+    out = ["# Bandwidth-bound kernels on large model tensors: kernel time and HBM traffic", "",
+           "Each workload runs 2 warm-up calls and then the timed calls back to back on one "
+           "stream (warm: the tensors stay in the 256 MB Infinity Cache where they fit).",
+           "", "Commands (from /tmp on the GPU machine, REPO = repository root):", "", "```",
+           BW_COMMANDS["trace"]]
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        out.append(BW_COMMANDS["pmc"].format(C=c))
+        out.append(STACK_COMMANDS["copy"].format(C=c))
+    out += ["```", "",
+            f"Counter scale (plain 256 MiB copy): FETCH_SIZE x {scale['FETCH_SIZE']:.4f}, "
+            f"WRITE_SIZE x {scale['WRITE_SIZE']:.4f}.  Algorithmic bytes: input + output (+ "
+            "weights, residual, bitmap) once.  Rates use the traced kernel time; the roofline "
+            f"fraction is against {HBM_PEAK_GBS / 1000:.0f} TB/s.", "",
+            "| workload | kernel | calls | avg us | alg MB | counted MB | GB/s (alg) | "
+            "fraction of HBM peak |", "|---|---|---|---|---|---|---|---|"]
+    for w, ts, fe, wr in zip(line_t["bw_kernels"], times, cnt["FETCH_SIZE"], cnt["WRITE_SIZE"]):
+        if not ts:
+            continue
+        us = sum(t for _, t in ts) / len(ts)
+        kb = {c: (sum(v for _, v in cc) / len(cc) if cc else 0.0)
+              for c, cc in (("FETCH_SIZE", fe), ("WRITE_SIZE", wr))}
+        counted = sum(kb[c] * 1024 * scale[c] for c in kb)
+        gbs = w["alg_bytes"] / us / 1e3
+        out.append(f"| {w['name']} | `{_short(ts[0][0])}` | {len(ts)} | {us:.2f} | "
+                   f"{w['alg_bytes'] / 1e6:.1f} | {counted / 1e6:.1f} | {gbs:.0f} | "
+                   f"{gbs / HBM_PEAK_GBS:.3f} |")
+    with open(os.path.join(ROOT, "profiles", "bandwidth_kernels.md"), "w") as f:
+        f.write("\n".join(out) + "\n")
+    print("wrote profiles/bandwidth_kernels.md", file=sys.stderr)
+
+
 def main():
     args = parse()
     if args.profile_summary:
@@ -1129,6 +1306,9 @@ def main():
         return
     if args.stack_summary:
         stack_summary(args.stack_summary)
+        return
+    if args.bw_summary:
+        bw_summary(args.bw_summary)
         return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
@@ -1154,6 +1334,9 @@ def main():
     from paper_2511_19457_amd import abi
     if args.stack:
         stack_profile_run(abi, torch, synth, args.stack, args.steps)
+        return
+    if args.bw_kernels:
+        bw_kernels_run(abi, torch, synth, args.steps)
         return
     if args.crossover:
         print(json.dumps(dict(sweep="f2 crossover", workload="x [m,4096] x w [4096,4096] bf16, "
