@@ -537,6 +537,18 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   const int64_t ntm = cdiv_dev(a.M, BM), ntn = cdiv_dev(a.N, BN);
   const int64_t ntiles = ntm * ntn * a.split;   // == gridDim.x
   const bool om = BN % 64 == 0 && a.om_counts != nullptr;
+  // the device route's counts, requested first as vector loads (in-order
+  // counters: waiting for them later does not wait for the loads behind
+  // them; a scalar load would make the first kernel-argument use wait for
+  // it): their latency overlaps the tile's offset arithmetic and the dense
+  // walk's list writes
+  u32x4 rcq[2] = {u32x4{0u, 0u, 0u, 0u}, u32x4{0u, 0u, 0u, 0u}};
+  if (SKIP && !a.route.sample_zeros && a.route.counts) {
+    const __amdgpu_buffer_rsrc_t cr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.route.counts, (short)0, (int)sizeof(sparoa_counts), kBufDword3);
+    rcq[0] = __builtin_amdgcn_raw_buffer_load_b128(cr, 0, 0, 0);
+    rcq[1] = __builtin_amdgcn_raw_buffer_load_b128(cr, 16, 0, 0);
+  }
   // one tile; returns its output's zero count and nonzero-block count
   auto tile_body = [&](const int64_t vid) __attribute__((always_inline)) -> uint2 {
   int64_t tile;
@@ -604,6 +616,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   // ---- skip list ---------------------------------------------------------
   int64_t count = c_end - c_begin;
   bool use_list = SKIP;
+  bool prefilled = false;   // the list already holds the dense walk
   if constexpr (SKIP) {
     if (a.route.sample_zeros) {
       // split execution: this tile's own route, from the zero counts of the
@@ -618,7 +631,17 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
       if (!use_list && a.executed && first_col && tid == 0 && count)
         atomicAdd(a.executed, (unsigned long long)count);  // a dense tile runs every chunk
     } else if (a.route.counts) {
-      use_list = device_route_skip(a.route);
+      // the dense walk is written while the route's counts are in flight
+      // (a dense-routed tile then waits for them only once); a skip-routed
+      // tile overwrites it with its list
+      for (int i = tid; i < (int)count; i += NT) list[i] = pack_chunk((int)c_begin + i);
+      prefilled = true;
+      uint32_t rw[8];   // the same in every lane: scalars, so the route is uniform
+#pragma unroll
+      for (int q = 0; q < 8; ++q) rw[q] = __builtin_amdgcn_readfirstlane(rcq[q >> 2][q & 3]);
+      sparoa_counts rc;
+      __builtin_memcpy(&rc, rw, sizeof(rc));
+      use_list = route_skip_counts(rc, a.route.sparsity_thr, a.route.mode);
       if (a.route.path_out && first_tile && tid == 0)
         *a.route.path_out = (use_list ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
     }
@@ -766,7 +789,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   // kernel) fill the list in dense order: no branch on the route inside the
   // main loop
   if (!SKIP || !use_list) {
-    for (int i = tid; i < (int)count; i += NT) list[i] = pack_chunk((int)c_begin + i);
+    if (!prefilled)
+      for (int i = tid; i < (int)count; i += NT) list[i] = pack_chunk((int)c_begin + i);
     __syncthreads();
   }
   // (the list entry is the same in every lane: read it as a scalar, so the
