@@ -195,37 +195,42 @@ struct Dw3Lane {
   }
 };
 
-// One item in flight: its output position and its 3 x NC input vectors.
-template <int S, int R>
+// One item in flight: its output position and its NR x NC input vectors.  An
+// item is RH output rows x a run of R output pixels of one channel vector;
+// with RH = 2 at stride 1 the two rows share two of their four input rows,
+// so an output takes 3 instead of 4.5 loads at R = 4.
+template <int S, int R, int RH>
 struct Dw3Item {
-  static constexpr int NC = (R - 1) * S + 3;  // input columns per kernel row
-  int64_t o;            // element offset of the run's first output vector
-  uint4 xin[3][NC];
+  static constexpr int NC = (R - 1) * S + 3;   // input columns per kernel row
+  static constexpr int NR = (RH - 1) * S + 3;  // input rows
+  int64_t o;            // element offset of the item's first output vector
+  uint4 xin[NR][NC];
 };
 
 // Issues the input loads of item i (buffer loads: a tap outside the image
 // takes an offset past the descriptor's range and reads zero without a
 // memory access -- no branch, no select; x is under 2^31 bytes).
-template <int DT, int S, int R>
+// fho divides by Ho / RH (row groups per image).
+template <int DT, int S, int R, int RH>
 __device__ __forceinline__ void dw3_fetch(const DwArgs &a, __amdgpu_buffer_rsrc_t xrs, uint32_t i,
                                           int64_t c0, const FastDiv &fcv, const FastDiv &fruns,
-                                          const FastDiv &fho, Dw3Item<S, R> &it) {
+                                          const FastDiv &fho, Dw3Item<S, R, RH> &it) {
   constexpr int ESZ = Elem<DT>::size;
-  constexpr int NC = Dw3Item<S, R>::NC;
+  constexpr int NC = Dw3Item<S, R, RH>::NC, NR = Dw3Item<S, R, RH>::NR;
   const int H = (int)a.H, W = (int)a.W;
-  const uint32_t runs = (uint32_t)(a.Wo / R);
+  const uint32_t runs = (uint32_t)(a.Wo / R), groups = (uint32_t)(a.Ho / RH);
   const uint32_t rest = fdiv(i, fcv);   // pixel-run
   const uint32_t rest2 = fdiv(rest, fruns);
   const int run = (int)(rest - rest2 * runs);
   const uint32_t n32 = fdiv(rest2, fho);
-  const int oh = (int)(rest2 - n32 * (uint32_t)a.Ho);
+  const int oh = (int)(rest2 - n32 * groups) * RH;
   const int64_t n = n32;
   const int ow0 = run * R;
   const int ih0 = oh * S - 1, iw0 = ow0 * S - 1;
   it.o = ((n * a.Ho + oh) * a.Wo + ow0) * a.C + c0;
   const uint32_t pix_bytes = (uint32_t)(a.C * ESZ);
 #pragma unroll
-  for (int r = 0; r < 3; ++r) {
+  for (int r = 0; r < NR; ++r) {
     const int ih = ih0 + r;
     const bool rv = ih >= 0 && ih < H;
     const uint32_t row_off = (uint32_t)((n * H + ih) * W) * pix_bytes + (uint32_t)(c0 * ESZ);
@@ -240,62 +245,81 @@ __device__ __forceinline__ void dw3_fetch(const DwArgs &a, __amdgpu_buffer_rsrc_
   }
 }
 
-// Computes and stores the item's R output vectors.  Returns bit q set iff
-// output vector q has a nonzero element; adds its zero elements to *zeros.
-template <int DT, int S, int R, bool COUNT>
+// Computes and stores the item's RH x R output vectors.  Returns bit
+// rh R + q set iff output vector (rh, q) has a nonzero element; adds its
+// zero elements to *zeros.
+template <int DT, int S, int R, int RH, bool COUNT>
 __device__ __forceinline__ uint32_t dw3_finish(const DwArgs &a, const Dw3Lane<DT> &l,
-                                               const Dw3Item<S, R> &it, uint32_t *zeros) {
+                                               const Dw3Item<S, R, RH> &it, uint32_t *zeros) {
   using E = Elem<DT>;
   using raw = typename E::raw;
   constexpr int ESZ = E::size;
   constexpr int V = Dw3Lane<DT>::V;
-  constexpr int NC = Dw3Item<S, R>::NC;
-  float acc[R][V];
+  constexpr int NC = Dw3Item<S, R, RH>::NC, NR = Dw3Item<S, R, RH>::NR;
+  float acc[RH][R][V];
 #pragma unroll
-  for (int q = 0; q < R; ++q)
+  for (int h = 0; h < RH; ++h)
 #pragma unroll
-    for (int j = 0; j < V; ++j) acc[q][j] = l.bv[j];
+    for (int q = 0; q < R; ++q)
 #pragma unroll
-  for (int r = 0; r < 3; ++r)
+      for (int j = 0; j < V; ++j) acc[h][q][j] = l.bv[j];
+  uint32_t nzbits = 0;
+  // Input rows in order; output row h is complete after input row h S + 2
+  // and is stored there, so its accumulators die before the next rows.
+#pragma unroll
+  for (int rr = 0; rr < NR; ++rr) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       raw e[V];
-      __builtin_memcpy(e, &it.xin[r][c], 16);
+      __builtin_memcpy(e, &it.xin[rr][c], 16);
       float xv[V];
 #pragma unroll
       for (int j = 0; j < V; ++j) xv[j] = E::to_f32(e[j]);
 #pragma unroll
+      for (int h = 0; h < RH; ++h) {
+        const int r = rr - h * S;   // kernel row that reads input row rr for output row h
+        if (r < 0 || r > 2) continue;
+#pragma unroll
+        for (int q = 0; q < R; ++q) {
+          const int s = c - q * S;  // kernel column that reads input column c for output q
+          if (s < 0 || s > 2) continue;
+#pragma unroll
+          for (int j = 0; j < V; ++j)
+            acc[h][q][j] = fmaf(xv[j], E::to_f32(l.wv[r * 3 + s][j]), acc[h][q][j]);
+        }
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < RH; ++h) {
+      if (h * S + 2 != rr) continue;
+#pragma unroll
       for (int q = 0; q < R; ++q) {
-        const int s = c - q * S;  // tap column that reads input column c for output q
-        if (s < 0 || s > 2) continue;
+        const int64_t o = it.o + (h * a.Wo + q) * a.C;
+        if (a.residual) {
+          float rv[V];
+          load_vec<DT, V>(a.residual + o * ESZ, rv);
 #pragma unroll
-        for (int j = 0; j < V; ++j)
-          acc[q][j] = fmaf(xv[j], E::to_f32(l.wv[r * 3 + s][j]), acc[q][j]);
+          for (int j = 0; j < V; ++j) acc[h][q][j] += rv[j];
+        }
+        raw t[V];
+        uint32_t any = 0;   // OR of the magnitudes
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          t[j] = E::from_f32(apply_act(acc[h][q][j], a.act));
+          if (COUNT) {
+            // zero test in plain integer arithmetic (m - 1 wraps to bit 31 iff
+            // m == 0; m < 2^31), so no compare masks occupy scalar registers
+            const uint32_t m = (uint32_t)t[j] & E::mag_mask;   // 0 for +0 and -0
+            *zeros += (m - 1u) >> 31;
+            any |= m;
+          }
+        }
+        if (COUNT) nzbits |= (((any - 1u) >> 31) ^ 1u) << (h * R + q);
+        uint4 qv;
+        __builtin_memcpy(&qv, t, 16);
+        *reinterpret_cast<uint4 *>(a.y + o * ESZ) = qv;
       }
     }
-  uint32_t nzbits = 0;
-#pragma unroll
-  for (int q = 0; q < R; ++q) {
-    const int64_t o = it.o + q * a.C;
-    if (a.residual) {
-      float rv[V];
-      load_vec<DT, V>(a.residual + o * ESZ, rv);
-#pragma unroll
-      for (int j = 0; j < V; ++j) acc[q][j] += rv[j];
-    }
-    raw t[V];
-#pragma unroll
-    for (int j = 0; j < V; ++j) {
-      t[j] = E::from_f32(apply_act(acc[q][j], a.act));
-      if (COUNT) {
-        const bool z = (t[j] & E::mag_mask) == 0u;   // +0 or -0
-        *zeros += z ? 1u : 0u;
-        nzbits |= z ? 0u : (1u << q);
-      }
-    }
-    uint4 qv;
-    __builtin_memcpy(&qv, t, 16);
-    *reinterpret_cast<uint4 *>(a.y + o * ESZ) = qv;
   }
   return nzbits;
 }
@@ -323,12 +347,15 @@ __device__ __forceinline__ int64_t xcd_block(int64_t b, int64_t nb) {
 // lane's weights, so both arrive in one round trip.  COUNT: the counts-only
 // output measurement (Section 3.1, Eq. 1, at block (1 pixel, 8 channels) =
 // one output vector, no bitmap): zeros and nonzero vectors per lane, one
-// ticketed commit per work-group.
-template <int DT, int S, int R, bool COUNT>
-__global__ __launch_bounds__(kThreads) void dw3x3_kernel(DwArgs a, FastDiv fcv, FastDiv fruns,
+// ticketed commit per work-group.  Two waves per SIMD at least: the
+// counting form of the 2 x 4 item would otherwise take 258 registers and one
+// wave; capped at 256 it spills a few bytes per lane and is still 10-15%
+// faster than 1 x 4 items on the stride-1 MobileNetV2 layers.
+template <int DT, int S, int R, int RH, bool COUNT>
+__global__ __launch_bounds__(kThreads, 2) void dw3x3_kernel(DwArgs a, FastDiv fcv, FastDiv fruns,
                                                         FastDiv fho) {
   const int64_t cv = a.C / Dw3Lane<DT>::V;
-  const int64_t total = a.N * a.Ho * (a.Wo / R) * cv;
+  const int64_t total = a.N * (a.Ho / RH) * (a.Wo / R) * cv;
   if (a.route.counts && a.route.path_out && blockIdx.x == 0 && threadIdx.x == 0)
     *a.route.path_out = (device_route_skip(a.route) ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
   int64_t i = xcd_block(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
@@ -339,16 +366,16 @@ __global__ __launch_bounds__(kThreads) void dw3x3_kernel(DwArgs a, FastDiv fcv, 
                        Dw3Lane<DT>::V;
     const __amdgpu_buffer_rsrc_t xrs = dw3_x_rsrc<DT>(a);
     const int64_t stride = (int64_t)gridDim.x * kThreads;
-    Dw3Item<S, R> it;
-    dw3_fetch<DT, S, R>(a, xrs, (uint32_t)i, c0, fcv, fruns, fho, it);
+    Dw3Item<S, R, RH> it;
+    dw3_fetch<DT, S, R, RH>(a, xrs, (uint32_t)i, c0, fcv, fruns, fho, it);
     Dw3Lane<DT> l;
     l.load(a, c0);
     for (;;) {
-      const uint32_t bits = dw3_finish<DT, S, R, COUNT>(a, l, it, &zeros);
+      const uint32_t bits = dw3_finish<DT, S, R, RH, COUNT>(a, l, it, &zeros);
       if (COUNT) nz += (uint32_t)__popc(bits);
       i += stride;
       if (i >= total) break;
-      dw3_fetch<DT, S, R>(a, xrs, (uint32_t)i, c0, fcv, fruns, fho, it);
+      dw3_fetch<DT, S, R, RH>(a, xrs, (uint32_t)i, c0, fcv, fruns, fho, it);
     }
   }
   if (COUNT) om_commit(zeros, nz, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
@@ -376,20 +403,21 @@ __global__ __launch_bounds__(kThreads) void dw3x3_measured_kernel(DwArgs a, Fast
   const __amdgpu_buffer_rsrc_t xrs = dw3_x_rsrc<DT>(a);
   const int64_t stride = (int64_t)gridDim.x * kThreads;
   uint32_t zeros = 0, nz = 0;
-  Dw3Item<S, 1> it;
-  if (first < total) dw3_fetch<DT, S, 1>(a, xrs, (uint32_t)first, c0, fcv, fwo, fho, it);
+  Dw3Item<S, 1, 1> it;
+  if (first < total) dw3_fetch<DT, S, 1, 1>(a, xrs, (uint32_t)first, c0, fcv, fwo, fho, it);
   Dw3Lane<DT> l;
   l.load(a, c0);
   for (int64_t base = first - lane; base < total; base += stride) {   // wave-uniform
     const int64_t i = base + lane;
     uint32_t bits = 0;
-    if (i < total) bits = dw3_finish<DT, S, 1, true>(a, l, it, &zeros);
+    if (i < total) bits = dw3_finish<DT, S, 1, 1, true>(a, l, it, &zeros);
     const uint64_t bal = __ballot(bits != 0u);
     const int64_t w0 = base >> 5;
     if (lane == 0 && w0 < om_words) a.om_mask[w0] = (uint32_t)bal;
     if (lane == 32 && w0 + 1 < om_words) a.om_mask[w0 + 1] = (uint32_t)(bal >> 32);
     nz += lane == 0 ? (uint32_t)__popcll(bal) : 0u;
-    if (i + stride < total) dw3_fetch<DT, S, 1>(a, xrs, (uint32_t)(i + stride), c0, fcv, fwo, fho, it);
+    if (i + stride < total)
+      dw3_fetch<DT, S, 1, 1>(a, xrs, (uint32_t)(i + stride), c0, fcv, fwo, fho, it);
   }
   om_commit(zeros, nz, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
 }
@@ -456,18 +484,18 @@ int64_t dw_grid(int64_t items, int64_t cv, int64_t cap) {
   return nb;
 }
 
-template <int DT, int S, int R>
+template <int DT, int S, int R, int RH>
 sparoa_status launch_dw3(const DwArgs &a, hipStream_t st, const FastDiv &fcv, int64_t cv) {
   const int64_t runs = a.Wo / R;
-  const int64_t items = a.N * a.Ho * runs * cv;
-  const FastDiv fruns = make_fastdiv((uint32_t)runs), fho = make_fastdiv((uint32_t)a.Ho);
+  const int64_t items = a.N * (a.Ho / RH) * runs * cv;
+  const FastDiv fruns = make_fastdiv((uint32_t)runs), fho = make_fastdiv((uint32_t)(a.Ho / RH));
   const int64_t nb = dw_grid(items, cv, 4096);
   if (a.om_counts)   // counts only (no bitmap)
-    hipLaunchKernelGGL((dw3x3_kernel<DT, S, R, true>), dim3((unsigned)nb), dim3(kThreads), 0, st,
-                       a, fcv, fruns, fho);
-  else
-    hipLaunchKernelGGL((dw3x3_kernel<DT, S, R, false>), dim3((unsigned)nb), dim3(kThreads), 0,
+    hipLaunchKernelGGL((dw3x3_kernel<DT, S, R, RH, true>), dim3((unsigned)nb), dim3(kThreads), 0,
                        st, a, fcv, fruns, fho);
+  else
+    hipLaunchKernelGGL((dw3x3_kernel<DT, S, R, RH, false>), dim3((unsigned)nb), dim3(kThreads),
+                       0, st, a, fcv, fruns, fho);
   SPAROA_LAUNCH_CHECK("dw3x3_kernel");
   return SPAROA_OK;
 }
@@ -515,12 +543,17 @@ sparoa_status dw_dispatch(const DwArgs &a, hipStream_t st) {
     }
     const int R = dw_run(a.Wo, a.sh);
     if (a.sh == 1) {
-      if (R == 4) return launch_dw3<DT, 1, 4>(a, st, fcv, cv);
-      if (R == 2) return launch_dw3<DT, 1, 2>(a, st, fcv, cv);
-      return launch_dw3<DT, 1, 1>(a, st, fcv, cv);
+      // two output rows per item where Ho is even (stride 1: 3 loads per
+      // output at runs of 4 instead of 4.5)
+      const bool rows2 = a.Ho % 2 == 0;
+      if (R == 4)
+        return rows2 ? launch_dw3<DT, 1, 4, 2>(a, st, fcv, cv) : launch_dw3<DT, 1, 4, 1>(a, st, fcv, cv);
+      if (R == 2)
+        return rows2 ? launch_dw3<DT, 1, 2, 2>(a, st, fcv, cv) : launch_dw3<DT, 1, 2, 1>(a, st, fcv, cv);
+      return rows2 ? launch_dw3<DT, 1, 1, 2>(a, st, fcv, cv) : launch_dw3<DT, 1, 1, 1>(a, st, fcv, cv);
     }
-    if (R == 2) return launch_dw3<DT, 2, 2>(a, st, fcv, cv);
-    return launch_dw3<DT, 2, 1>(a, st, fcv, cv);
+    if (R == 2) return launch_dw3<DT, 2, 2, 1>(a, st, fcv, cv);
+    return launch_dw3<DT, 2, 1, 1>(a, st, fcv, cv);
   }
   if (a.om_counts) return fail(SPAROA_ERR_UNSUPPORTED, "depthwise: no fused output measurement");
   if (vec && k3)

@@ -106,7 +106,8 @@ def test_conv_skip_equals_dense_and_oracle(dt, rho, shape):
 DW_SHAPES = [
     (2, 32, 12, 12, 32, 3, 3, 1, 1, 1, 1, 1, 1, 32),
     (1, 96, 15, 15, 96, 3, 3, 2, 2, 1, 1, 1, 1, 96),
-    (1, 144, 8, 9, 144, 3, 3, 1, 1, 1, 1, 1, 1, 144),
+    (1, 144, 8, 9, 144, 3, 3, 1, 1, 1, 1, 1, 1, 144),  # even Ho, odd Wo: 2 x 1 items
+    (2, 48, 6, 10, 48, 3, 3, 1, 1, 1, 1, 1, 1, 48),    # even Ho, Wo 10: 2 x 2 items
     (1, 12, 7, 7, 12, 5, 5, 1, 1, 2, 2, 1, 1, 12),     # runtime-window kernel
     (1, 5, 6, 6, 5, 3, 3, 1, 1, 1, 1, 1, 1, 5),        # channels % 8 != 0
     (3, 24, 14, 13, 24, 3, 3, 2, 2, 1, 1, 1, 1, 24),   # stride 2, ragged pixel runs
