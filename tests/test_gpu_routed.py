@@ -420,6 +420,57 @@ def test_fc_ops_run_grouped_streaming_equals_op_by_op():
     assert seen == {abi.PATH_DENSE_BW, abi.PATH_SKIP_BW}
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+def test_fc_ops_run_grouped_streaming_edge_cases(dt):
+    """One grouped streaming launch over ten FCs with m <= 16: K up to 4096
+    (full slices) and ragged (a partial last slice), N from one panel to 32
+    and ragged, an all-zero input (skip route, every slice list empty), a
+    dense input routed to the skip path (threshold 0: lists of every
+    column), bias and residual on some -- counts, bitmap, path and output
+    bits equal op-by-op calls and the oracle's measurement."""
+    abi = _abi()
+    dev = torch.device("cuda")
+    tdt = abi.F16 if dt == "f16" else abi.BF16
+    specs = [  # m, k, n, rho, pattern, sparsity threshold
+        (1, 4096, 512, 0.0, "iid", 0.8), (8, 4096, 512, 0.95, "block", 0.8),
+        (1, 4096, 16, 0.95, "iid", 0.8), (16, 4096, 100, 0.5, "iid", 0.8),
+        (3, 2048, 256, 1.0, "iid", 0.8), (8, 4096, 64, 0.3, "iid", 0.0),
+        (15, 1000, 200, 0.8, "block", 0.6), (8, 4096, 512, 0.8, "block", 0.8),
+        (1, 64, 48, 0.5, "iid", 0.4), (12, 4096, 512, 0.0, "block", 0.9),
+    ]
+    bufs = []
+    for i, (m, k, n, rho, pat, st) in enumerate(specs):
+        d = abi.fc_desc(m, k, n, tdt, has_bias=(i % 3 == 1))
+        x = synth.sparse_matrix(m, k, rho, pat, dt, 1200 + i).to(dev)
+        res = synth.normal((m, n), dt, 1250 + i).to(dev) if i % 4 == 3 else None
+        b = _batch_op(abi, dev, d, x, 1300 + i, thr=(st, 315.0), residual=res)
+        b["bias"] = synth.normal((n,), dt, 1350 + i).to(dev) if d.has_bias else None
+        bufs.append(b)
+    ops = [abi.fc_op(b["d"], b["x"], b["w"], b["wp"], b["bias"], b["res"], abi.ACT_NONE,
+                     b["counts"], b["mask"], b["y"], b["ws"], b["path"],
+                     (b["thr"][0], b["thr"][1], abi.ROUTE_BLOCK)) for b in bufs]
+    abi.sparoa_fc_ops_run(abi.fc_op_array(ops))
+    torch.cuda.synchronize()
+    seen = set()
+    for i, b in enumerate(bufs):
+        m, k = b["x"].shape
+        ref = oracle.measure(b["x"].cpu(), m, k, b["br"], b["bc"])
+        assert b["counts"].cpu().tolist() == [ref["zeros"], ref["numel"], ref["zero_blocks"],
+                                              ref["num_blocks"]], f"op {i}"
+        assert np.array_equal(b["mask"].cpu().numpy().view(np.uint32), ref["mask"]), f"op {i}"
+        c2 = torch.zeros_like(b["counts"])
+        k2 = torch.zeros_like(b["mask"])
+        y2 = torch.full_like(b["y"], float("nan"))
+        p2 = torch.full((1,), -1, dtype=torch.int32, device=dev)
+        abi.sparoa_fc_measured(b["d"], b["thr"][0], b["thr"][1], abi.ROUTE_BLOCK, b["x"], b["w"],
+                               b["wp"], b["bias"], b["res"], abi.ACT_NONE, c2, k2, y2, b["ws"], p2)
+        torch.cuda.synchronize()
+        assert int(p2.item()) == int(b["path"].item()), f"op {i}"
+        assert torch.equal(y2, b["y"]), f"op {i}"
+        seen.add(int(p2.item()))
+    assert seen == {abi.PATH_DENSE_BW, abi.PATH_SKIP_BW}
+
+
 def test_fc_ops_run_in_a_hip_graph_equals_eager():
     """The executor captured in a HIP graph: every replay (with eager work and
     synchronisations in between) gives the eager run's counts, paths and
