@@ -7,15 +7,18 @@ bf16 ~ N(0, 1/4096), m in {1, 8, 64}, activation sparsity rho in
 |N(0, 1)|.  Every operator has its own weight matrix (24 x 32 MiB, more than
 the 256 MB Infinity Cache holds), so weights stream from HBM.  Per operator
 the step runs the whole path: intensity from the shape (host), sparsity
-measurement (GPU), routing, and the routed FC kernel.  Default (--mode graph):
-the 24 operators are issued by one native executor call (sparoa_fc_ops_run),
-captured once in a HIP graph.  The weight-streaming FCs measure their own
-input and take the route decision themselves, all of them in one grouped
-launch; the implicit-GEMM FCs run a grouped measurement, one GEMM each
-(device-side route) and a grouped split-K reduction.
---mode eager issues the same executor call every step; --mode host reads the
-counts back and routes on the host, one Python call per kernel.  Inputs are
-resident in HBM before timing starts.
+measurement (GPU), routing, and the routed FC kernel.  Default (--mode eager):
+the 24 operators are issued by one native executor call (sparoa_fc_ops_run)
+per step.  The weight-streaming FCs measure their own input and take the
+route decision themselves, in grouped launches (one per row-tile count);
+the implicit-GEMM FCs run a grouped measurement, one GEMM each (device-side
+route) and a grouped split-K reduction.  --mode graph replays the same call
+captured once in a HIP graph (on this stack a replay leaves the GPU idle for
+about 18 us between steps, where back-to-back executor calls leave none);
+--mode host reads the counts back and routes on the host, one Python call
+per kernel.  Inputs are resident in HBM before timing starts; one pair of
+HIP events brackets the timed steps (an event pair per step costs 8-9 us per
+step).
 
 value = dense-equivalent TFLOP/s of the step: sum over operators of
 2 m k n divided by the step time (skipped work counts as done).
@@ -98,7 +101,7 @@ def parse():
                    help="f2 sweep instead of the benchmark: whole-path time of every forced "
                         "path at block sparsity 0 .. 0.99 (step 0.05) for each m and zero "
                         "pattern; prints one JSON line with the skip/dense crossovers")
-    p.add_argument("--mode", choices=("graph", "eager", "host"), default="graph",
+    p.add_argument("--mode", choices=("graph", "eager", "host"), default="eager",
                    help="graph: the executor call captured in a HIP graph, one replay per step; "
                         "eager: the executor call every step; host: counts read back, "
                         "sparoa_route on the host, then the fixed-path call")
@@ -191,12 +194,13 @@ def profile_summary(d, copy_mib):
            "Command (from /tmp on the GPU machine, REPO = repository root):", "", "```",
            "THR='" + thr + "'", PROFILE_COMMANDS["trace"], "```", "",
            f"Kernel dispatches: {len(rows)}; total kernel time {tot / 1e3:.2f} ms (all phases "
-           "of the run: eager reference, warm-up, timed steps, per-family replays).", "",
+           "of the run: eager reference, warm-up, timed steps, per-family calls).", "",
            "| kernel | calls | total ms | avg us | min us | max us | % |", "|---|---|---|---|---|---|---|"]
     for k, v in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
         out.append(f"| `{k}` | {len(v)} | {sum(v) / 1e3:.3f} | {sum(v) / len(v):.2f} | "
                    f"{min(v):.2f} | {max(v):.2f} | {100 * sum(v) / tot:.1f} |")
-    out += ["", "bench.py's own figures in the same run (HIP events, per-family graph replays):", ""]
+    out += ["", "bench.py's own figures in the same run (HIP events around back-to-back "
+            "executor calls per family):", ""]
     for fam, r in [("dominant", line["roofline"])] + list(line.get("roofline_other_families", {}).items()):
         out.append(f"- {fam}: `{r['kernel']}`, {r['operators']} operators in {r['launches']} "
                    f"launches, avg {r['avg_launch_us']} us per launch, {r['achieved']} GB/s "
@@ -1404,7 +1408,7 @@ def main():
     def executor_step():
         abi.sparoa_fc_ops_run(op_array)
 
-    # eager reference outputs: the graph replays must reproduce them
+    # reference outputs: the timed steps must reproduce them
     executor_step()
     torch.cuda.synchronize()
     y_ref = [c.y.clone() for c in cases]
@@ -1434,15 +1438,14 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # one pair of HIP events brackets every step on the stream it runs on
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
+    # one pair of HIP events brackets the timed steps on the stream they run on
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    ev0.record()
     for s in range(args.steps):
-        ev[s][0].record()
         step()
-        ev[s][1].record()
+    ev1.record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     paths = [int(c.path_dev.item()) for c in cases] if args.mode != "host" else \
@@ -1462,7 +1465,7 @@ def main():
 
     flops_step = sum(2 * c.m * K * N for c in cases)
     value = flops_step / step_s / 1e12
-    step_gpu_us = sum(a.elapsed_time(b) for a, b in ev) * 1e3 / args.steps
+    step_gpu_us = ev0.elapsed_time(ev1) * 1e3 / args.steps
     if args.no_sweep:
         for c in cases:
             c.path_us = None
@@ -1485,25 +1488,24 @@ def main():
     tot_bytes = sum(c.alg for c in cases)
 
     # Roofline of each kernel family's launches: the step's operators of one
-    # family replayed as their own HIP graph, events around every replay.
+    # family issued by back-to-back executor calls on the current stream, one
+    # pair of HIP events around all of them (the launches run back to back).
     fam_rows = {}
     for fam in (abi.PATH_DENSE_BW, abi.PATH_DENSE_MFMA):
         sel = [c for c in cases if family(c) == fam]
         if not sel:
             continue
         arr = batch(sel)
-        g = capture(lambda: abi.sparoa_fc_ops_run(arr))
-        g.replay()
+        abi.sparoa_fc_ops_run(arr)
         torch.cuda.synchronize()
         reps = max(10, args.steps)
-        evf = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(reps)]
-        for e0, e1 in evf:
-            e0.record()
-            g.replay()
-            e1.record()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            abi.sparoa_fc_ops_run(arr)
+        e1.record()
         torch.cuda.synchronize()
-        us = sum(a.elapsed_time(b) for a, b in evf) * 1e3 / reps
+        us = e0.elapsed_time(e1) * 1e3 / reps
         fam_rows[fam] = (sel, us)
     dominant = max(fam_rows, key=lambda f: fam_rows[f][1])
     digest = source_digest()
@@ -1530,8 +1532,9 @@ def main():
                     frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic, kernel=kernel,
                     operators=len(sel), launches=launches, alg_bytes_per_launch=per_launch,
                     avg_launch_us=round(us / launches, 3),
-                    timing="this family's operators of the step replayed as one HIP graph, HIP "
-                           "events around every replay (gaps between launches included)",
+                    timing="this family's operators of the step issued by back-to-back "
+                           "executor calls, one pair of HIP events around them all (gaps "
+                           "between launches included)",
                     source_digest=digest)
 
     roofline = roofline_of(dominant)
