@@ -233,7 +233,9 @@ def test_maxpool_vs_oracle(dt):
 # Shapes that make the tile chooser pick each tile of the 64-channel-chunk
 # kernel (expected tile rows in the last field).
 IG_SHAPES = [
-    ((2, 64, 64, 64, 1024, 1, 1, 1, 1, 0, 0, 1, 1, 1), 128),   # 128 x 128, wide N
+    ((2, 64, 64, 64, 1024, 1, 1, 1, 1, 0, 0, 1, 1, 1), 128),   # 128 x 256, 1x1, wide N
+    ((4, 128, 57, 55, 512, 1, 1, 1, 1, 0, 0, 1, 1, 1), 128),   # 128 x 256, 1x1, ragged M
+    ((2, 64, 80, 64, 640, 1, 1, 1, 1, 0, 0, 1, 1, 1), 128),    # 128 x 128, 1x1, N % 256 != 0
     ((6, 64, 61, 67, 256, 3, 3, 1, 1, 1, 1, 1, 1, 1), 128),    # 128 x 128, 3x3, ragged M
     ((1, 64, 64, 64, 1000, 1, 1, 1, 1, 0, 0, 1, 1, 1), 128),   # 128 x 64, ragged N
     ((4, 64, 128, 128, 64, 3, 3, 1, 1, 1, 1, 1, 1, 1), 128),   # 128 x 64, N = 64

@@ -41,6 +41,7 @@ CONV_CASES = [
     (3, 64, 15, 13, 64, 3, 2, "f16"),      # ragged rows, split-K
     (15, 64, 29, 31, 64, 3, 1, "bf16"),    # ragged rows in the last tile, no split
     (13, 64, 59, 61, 256, 3, 1, "bf16"),   # 128 x 128 tiles, ragged rows (732 tiles)
+    (4, 128, 57, 55, 512, 1, 1, "bf16"),   # 128 x 256 tiles (1x1), ragged rows (196 tiles)
     (5, 64, 120, 120, 64, 3, 1, "f16"),    # 128 x 64 tiles (563 tiles)
     (2, 64, 16, 16, 96, 1, 1, "bf16"),     # c_out % 64 != 0: standalone pass
     (2, 32, 16, 16, 64, 3, 1, "bf16"),     # c_in % 64 != 0 (first-generation GEMM): standalone
