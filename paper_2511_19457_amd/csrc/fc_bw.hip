@@ -687,16 +687,27 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
     // Column of entry e of chunk i (-1 past the slice's entries or the walk).
     // Everything is computed unconditionally and selected (a short-circuit
     // here becomes a branch inside the ring, which drains it).
+    // column_at: the same for chunk c of slice sl (sl >= nslices: past the
+    // walk), which the ring's look-ahead tracks with counters instead of a
+    // division per step.
+    auto column_at = [&](int sl, int c, int e) __attribute__((always_inline)) -> int {
+      const int slc = min(sl, nslices - 1);
+      const int ee = c * kCh + e;
+      int k, cnt;
+      if constexpr (LIST) {
+        cnt = slice_count[slc];
+        k = slc * slice + (int)lists[slc][max(0, min(ee, cnt - 1))];
+      } else {  // every column of the slice (no LDS read: no wait in the ring)
+        cnt = min(slice, Ki - slc * slice);
+        k = slc * slice + ee;
+      }
+      const bool ok = (sl < nslices) & (ee < cnt);
+      return ok ? k : -1;
+    };
     auto column = [&](int i, int e) __attribute__((always_inline)) -> int {
       const int ic = min(i, total - 1);
       const int sl = ic / nchu, c = ic - sl * nchu;
-      const int cnt = slice_count[sl];
-      const int ee = c * kCh + e;
-      int k;
-      if constexpr (LIST) k = sl * slice + (int)lists[sl][max(0, min(ee, cnt - 1))];
-      else k = sl * slice + ee;
-      const bool ok = (i < total) & (ee < cnt);
-      return ok ? k : -1;
+      return column_at(i < total ? sl : nslices, c, e);
     };
     // x stage t -> registers: dense, NXVEC 16-byte vectors (row, 8 entries)
     // per thread; skip order, NXV 2-byte gathers per thread.
@@ -747,13 +758,13 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
     // weight ring: chunk i's 32 entries; skip layout: lane = (entry lane / 2,
     // half lane % 2); dense layout: the B operand (column lane % 16, entries
     // 8 (lane / 16) + 0..7) of the slice's k chunk
-    auto wload = [&](uint4 &w, int i) __attribute__((always_inline)) {
+    auto wload = [&](uint4 &w, int sl, int c) __attribute__((always_inline)) {
       int off;
       if constexpr (LIST) {
-        const int k = column(i, lane >> 1);
+        const int k = column_at(sl, c, lane >> 1);
         off = pvalid && k >= 0 ? (k * kPanel + 8 * (lane & 1)) * 2 : kOob;
       } else {
-        const int k = column(i, 0);  // the chunk's first column, -1 past the walk
+        const int k = column_at(sl, c, 0);  // the chunk's first column, -1 past the walk
         off = pvalid && k >= 0 ? ((k >> 5) * 16 + (lane & 15)) * 64 + 16 * (lane >> 4) : kOob;
       }
       w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wrs, off, 0, 0));
@@ -805,10 +816,13 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
     stage_store(0);
 #pragma unroll
     for (int q = 0; q < D; ++q) {
-      wload(ring[q], q);
+      const int qc = min(q, total - 1);
+      wload(ring[q], q < total ? qc / nchu : nslices, qc % nchu);
       __builtin_amdgcn_sched_barrier(0);  // slot order, as in the loop
     }
     __syncthreads();
+    // (slice, chunk) of the look-ahead chunk i + D, advanced one per step
+    int la_sl = D / nchu, la_c = D % nchu;
     const int iters = (total + U - 1) / U;  // loop iterations of U steps
     for (int it = 0; it < iters; ++it) {
 #pragma unroll
@@ -816,7 +830,11 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
         const int i = it * U + q;
         if (q % SC == 0) stage_load(i / SC + 1);  // the next stage, during this one
         step(ring[q % D], i);
-        wload(ring[q % D], i + D);
+        wload(ring[q % D], la_sl, la_c);
+        ++la_c;
+        const bool wrap = la_c == nchu;
+        la_c = wrap ? 0 : la_c;
+        la_sl += wrap ? 1 : 0;
         if (q % SC == SC - 1) {
           stage_store(i / SC + 1);
           __syncthreads();  // next stage staged; this stage's readers done
