@@ -674,8 +674,11 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
 #pragma unroll
   for (int i = 0; i < MT; ++i) acc[i] = sum[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto run = [&](auto list_tag) __attribute__((always_inline)) {
+  // ALIGNED: nchu % U == 0 (dense slices of 8 or 16 chunks), so a slice ends
+  // only at an iteration's last step and the partial's selects run there
+  auto run = [&](auto list_tag, auto aligned_tag) __attribute__((always_inline)) {
     constexpr bool LIST = decltype(list_tag)::value;
+    constexpr bool ALIGNED = decltype(aligned_tag)::value;
     using GS = GroupShape<MT, LIST>;
     constexpr int SC = GS::SC, D = GS::D, U = GS::U, XROW = GS::XROW;
     const __amdgpu_buffer_rsrc_t wrs = fc_panel_rsrc<LIST>(a, pvalid ? p : 0);
@@ -770,7 +773,7 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
       w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wrs, off, 0, 0));
     };
     int cc = 0;  // chunks done in the current slice
-    auto step = [&](const uint4 &w, int i) __attribute__((always_inline)) {
+    auto step = [&](const uint4 &w, int i, bool last) __attribute__((always_inline)) {
       // weights transposed into the wave's tile, then MT MFMAs whose A
       // operands come straight from the staged x
       const int g = lane >> 4, rl = lane & 15;
@@ -801,8 +804,9 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
                                                            acc[mt], 0, 0, 0);
       }
       // at a slice's end its partial joins the sum (selects, no branch)
-      const bool end = ++cc == nchu;
-      cc = end ? 0 : cc;
+      if (ALIGNED && !last) return;
+      const bool end = ALIGNED ? (i + 1) % nchu == 0 : ++cc == nchu;
+      if (!ALIGNED) cc = end ? 0 : cc;
 #pragma unroll
       for (int r = 0; r < MT; ++r) {
         const f32x4 t = sum[r] + acc[r];
@@ -829,7 +833,7 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
       for (int q = 0; q < U; ++q) {
         const int i = it * U + q;
         if (q % SC == 0) stage_load(i / SC + 1);  // the next stage, during this one
-        step(ring[q % D], i);
+        step(ring[q % D], i, q == U - 1);
         wload(ring[q % D], la_sl, la_c);
         ++la_c;
         const bool wrap = la_c == nchu;
@@ -843,8 +847,9 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
       }
     }
   };
-  if (use_list) run(std::true_type{});
-  else run(std::false_type{});
+  if (use_list) run(std::true_type{}, std::false_type{});
+  else if (nchu % GroupShape<MT>::U == 0) run(std::false_type{}, std::true_type{});
+  else run(std::false_type{}, std::false_type{});
 
   if (!pvalid) return;
   const int g = lane >> 4, rl = lane & 15;
