@@ -708,6 +708,12 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
       return ok ? k : -1;
     };
     auto column = [&](int i, int e) __attribute__((always_inline)) -> int {
+      if constexpr (!LIST) {
+        // dense: the chunks tile K in order (a slice is nchu whole chunks, or
+        // the only slice), so chunk i starts at column 32 i
+        const int k = i * kCh + e;
+        return (i < total) & (k < Ki) ? k : -1;
+      }
       const int ic = min(i, total - 1);
       const int sl = ic / nchu, c = ic - sl * nchu;
       return column_at(i < total ? sl : nslices, c, e);
@@ -761,13 +767,13 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
     // weight ring: chunk i's 32 entries; skip layout: lane = (entry lane / 2,
     // half lane % 2); dense layout: the B operand (column lane % 16, entries
     // 8 (lane / 16) + 0..7) of the slice's k chunk
-    auto wload = [&](uint4 &w, int sl, int c) __attribute__((always_inline)) {
+    auto wload = [&](uint4 &w, int i, int sl, int c) __attribute__((always_inline)) {
       int off;
       if constexpr (LIST) {
         const int k = column_at(sl, c, lane >> 1);
         off = pvalid && k >= 0 ? (k * kPanel + 8 * (lane & 1)) * 2 : kOob;
       } else {
-        const int k = column_at(sl, c, 0);  // the chunk's first column, -1 past the walk
+        const int k = column(i, 0);  // the chunk's first column, -1 past the walk
         off = pvalid && k >= 0 ? ((k >> 5) * 16 + (lane & 15)) * 64 + 16 * (lane >> 4) : kOob;
       }
       w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wrs, off, 0, 0));
@@ -821,11 +827,12 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
 #pragma unroll
     for (int q = 0; q < D; ++q) {
       const int qc = min(q, total - 1);
-      wload(ring[q], q < total ? qc / nchu : nslices, qc % nchu);
+      wload(ring[q], q, q < total ? qc / nchu : nslices, qc % nchu);
       __builtin_amdgcn_sched_barrier(0);  // slot order, as in the loop
     }
     __syncthreads();
-    // (slice, chunk) of the look-ahead chunk i + D, advanced one per step
+    // (slice, chunk) of the look-ahead chunk i + D in skip order, advanced
+    // one per step (the dense order computes its columns directly)
     int la_sl = D / nchu, la_c = D % nchu;
     const int iters = (total + U - 1) / U;  // loop iterations of U steps
     for (int it = 0; it < iters; ++it) {
@@ -834,11 +841,13 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
         const int i = it * U + q;
         if (q % SC == 0) stage_load(i / SC + 1);  // the next stage, during this one
         step(ring[q % D], i, q == U - 1);
-        wload(ring[q % D], la_sl, la_c);
-        ++la_c;
-        const bool wrap = la_c == nchu;
-        la_c = wrap ? 0 : la_c;
-        la_sl += wrap ? 1 : 0;
+        wload(ring[q % D], i + D, la_sl, la_c);
+        if constexpr (LIST) {
+          ++la_c;
+          const bool wrap = la_c == nchu;
+          la_c = wrap ? 0 : la_c;
+          la_sl += wrap ? 1 : 0;
+        }
         if (q % SC == SC - 1) {
           stage_store(i / SC + 1);
           __syncthreads();  // next stage staged; this stage's readers done
