@@ -564,7 +564,7 @@ sparoa_status conv_routed_impl(const sparoa_conv_desc *d, const sparoa_threshold
   if (ws_bytes < gemm_workspace_required(*d, p)) return fail(SPAROA_ERR_WORKSPACE, "conv2d_routed: workspace too small");
   // without a skip kernel for this shape the dense kernel runs and records a dense path
   const bool can_skip = gemm_skip_supported(*d);
-  if (measure_y && gemm_fuses_out_measure(*d, p)) {   // y_counts arrives initialised
+  if (measure_y && gemm_fuses_out_measure(*d, p, y_mask != nullptr)) {   // y_counts initialised
     const OutMeasure om{y_counts, y_mask, reinterpret_cast<unsigned long long *>(y_commit)};
     return launch_gemm_conv(*d, p, x, w, d->has_bias ? bias : nullptr, residual, act,
                             can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r,
@@ -688,7 +688,7 @@ sparoa_status fc_routed_impl(const sparoa_fc_desc *d, const sparoa_thresholds *t
   const sparoa_conv_desc c = fc_as_conv(*d);
   const sparoa_path p = bw ? SPAROA_PATH_SKIP_BW : SPAROA_PATH_SKIP_MFMA;
   const bool can_skip = gemm_skip_supported(c);
-  if (measure_y && gemm_fuses_out_measure(c, p)) {   // y_counts arrives initialised
+  if (measure_y && gemm_fuses_out_measure(c, p, y_mask != nullptr)) {   // y_counts initialised
     const OutMeasure om{y_counts, y_mask, reinterpret_cast<unsigned long long *>(y_commit)};
     return launch_gemm_conv(c, p, x, w, d->has_bias ? bias : nullptr, residual, act,
                             can_skip ? mask : nullptr, y, workspace, ws_bytes, nullptr, stream, &r,

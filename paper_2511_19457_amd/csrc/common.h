@@ -189,8 +189,10 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
 // defer: when non-null, a split-K reduction is described there (split > 1)
 // instead of launched; split = 0 when the GEMM needs none.
 // om: measure y in the epilogue (or in the split-K reduction); only when
-// gemm_fuses_out_measure(d, path) -- otherwise the call fails.
-bool gemm_fuses_out_measure(const sparoa_conv_desc &d, sparoa_path path);
+// gemm_fuses_out_measure(d, path, om->mask != nullptr) -- otherwise the call
+// fails.  bitmap: the measurement also writes y's bitmap (the small-channel
+// kernel only counts).
+bool gemm_fuses_out_measure(const sparoa_conv_desc &d, sparoa_path path, bool bitmap);
 
 // Pointwise (1x1) kernel of the bandwidth path: 16-bit, groups 1, no
 // padding, C_in <= 256 and % 8 == 0, C_out % 8 == 0, the weights in at most

@@ -1007,7 +1007,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
 // not issued (it would add exact zeros), so the skip output equals the dense
 // output bit for bit; executed_blocks counts the issued (row block, k-step)
 // pairs.  The fp32 tile goes through LDS to 16-byte stores with bias,
-// residual and activation.
+// residual and activation; each thread's 8 output channels of a pixel are one
+// (1, 8) block of the output, so the epilogue also counts zeros and nonzero
+// blocks when asked (counts-only measurement of y, one ticketed commit per
+// work-group).
 constexpr int kScMaxKSteps = 8;
 constexpr int kScMaxRB = 8;            // Wo <= 128
 constexpr int kScPatchBytes = 48 * 1024;  // LDS bound of the eligible shapes
@@ -1025,6 +1028,10 @@ struct SmallCArgs {
   int vec;                 // rows and weights are whole 16-byte vectors
   int mode;  // 0 dense, 1 skip, 2 device route
   DeviceRoute route;
+  // counts-only output measurement at block (1 pixel, 8 channels): non-null
+  // om_counts holds {0, numel, nb, nb} on entry; om_words: count-commit words
+  sparoa_counts *om_counts;
+  unsigned long long *om_words;
 };
 
 template <int DT, int KS>
@@ -1194,6 +1201,7 @@ __global__ __launch_bounds__(256) void conv_small_c_kernel(SmallCArgs a) {
   // ---- epilogue: 8 channels per thread, 16-byte stores
   const int C8 = a.Cout / 8, lc8 = C8 == 8 ? 3 : (C8 == 4 ? 2 : 1);   // Cout in {16, 32, 64}
   const raw *bias = reinterpret_cast<const raw *>(a.bias);
+  uint32_t om_zeros = 0, om_nz = 0;
   const int64_t row0 = (int64_t)blockIdx.x * a.Wo;
   for (int q = tid; q < a.Wo * C8; q += 256) {
     const int ow = q >> lc8, c = (q & (C8 - 1)) * 8;
@@ -1215,8 +1223,16 @@ __global__ __launch_bounds__(256) void conv_small_c_kernel(SmallCArgs a) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[e] += E::to_f32(t8[e]);
     }
+    uint32_t any = 0;   // OR of the magnitudes
 #pragma unroll
-    for (int e = 0; e < 8; ++e) t8[e] = E::from_f32(apply_act(o[e], a.act));
+    for (int e = 0; e < 8; ++e) {
+      t8[e] = E::from_f32(apply_act(o[e], a.act));
+      // zero test in integer arithmetic (m - 1 wraps to bit 31 iff m == 0)
+      const uint32_t m = (uint32_t)t8[e] & E::mag_mask;
+      om_zeros += (m - 1u) >> 31;
+      any |= m;
+    }
+    om_nz += ((any - 1u) >> 31) ^ 1u;
     uint4 q4;
     __builtin_memcpy(&q4, t8, 16);
     *reinterpret_cast<uint4 *>(reinterpret_cast<raw *>(a.y) + orow * a.Cout + c) = q4;
@@ -1226,6 +1242,7 @@ __global__ __launch_bounds__(256) void conv_small_c_kernel(SmallCArgs a) {
     for (int i = 0; i < nwm; ++i) tot += exec_part[i];
     if (tot) atomicAdd(a.executed, tot);
   }
+  if (a.om_counts) om_commit(om_zeros, om_nz, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
 }
 
 template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
@@ -1388,7 +1405,9 @@ bool small_c_eligible(const sparoa_conv_desc &d) {
 sparoa_status launch_small_c(const sparoa_conv_desc &d, const void *x, const void *w,
                              const void *bias, const void *residual, sparoa_act act, void *y,
                              bool skip, uint64_t *executed, hipStream_t stream,
-                             const DeviceRoute *route) {
+                             const DeviceRoute *route, const OutMeasure *om) {
+  if (om && om->mask)
+    return fail(SPAROA_ERR_UNSUPPORTED, "small-channel conv: fused measurement is counts-only");
   const Shape s = shape_of(d);
   SmallCArgs a;
   a.x = static_cast<const char *>(x);
@@ -1417,6 +1436,8 @@ sparoa_status launch_small_c(const sparoa_conv_desc &d, const void *x, const voi
   a.act = act;
   a.mode = route && route->counts ? 2 : (skip ? 1 : 0);
   a.route = route ? *route : DeviceRoute{nullptr, 0.0, 0, 0, nullptr};
+  a.om_counts = om ? om->counts : nullptr;
+  a.om_words = om ? om->words : nullptr;
   const dim3 grid((unsigned)(d.n * s.ho));
   const unsigned lds = (unsigned)small_c_lds_bytes(d);   // <= kScPatchBytes (eligibility)
   switch (a.ksteps) {
@@ -1551,10 +1572,12 @@ GemmTileChoice gemm_choose(const sparoa_conv_desc &d, sparoa_path path) {
   return t;
 }
 
-bool gemm_fuses_out_measure(const sparoa_conv_desc &d, sparoa_path path) {
+bool gemm_fuses_out_measure(const sparoa_conv_desc &d, sparoa_path path, bool bitmap) {
   const GemmTileChoice t = gemm_choose(d, path);
   // the pointwise kernel measures whole tiles of one weight slice
   if (t.pointwise) return pw_fuses_out_measure(d);
+  // the small-channel kernel counts (no bitmap)
+  if (t.small_c) return !bitmap;
   // the second-generation kernel (64-column tiles) writes whole bitmap bytes
   // when C_out % 64 == 0; its split-K reduction measures 16-byte vectors
   return t.cfg != 0 && d.c_out % 64 == 0 && elem_size(d.dtype) == 2;
@@ -1576,7 +1599,7 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
                                const OutMeasure *om) {
   const Shape s = shape_of(d);
   const GemmTileChoice t = gemm_choose(d, path);
-  if (om && !gemm_fuses_out_measure(d, path))
+  if (om && !gemm_fuses_out_measure(d, path, om->mask != nullptr))
     return fail(SPAROA_ERR_UNSUPPORTED, "GEMM: no fused output measurement for this shape");
   const int epv = d.dtype == SPAROA_F32 ? 4 : 8;
   const bool vec = d.c_in % epv == 0;
@@ -1629,7 +1652,7 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   if (t.small_c) {
     if (defer) *defer = SplitReduceJob{d.dtype, nullptr, 0, s.M, s.N, bias, residual, act, y,
                                        nullptr, nullptr, nullptr};
-    return launch_small_c(d, x, w, bias, residual, act, y, skip, executed, stream, route);
+    return launch_small_c(d, x, w, bias, residual, act, y, skip, executed, stream, route, om);
   }
   if (t.pointwise) {
     if (defer) *defer = SplitReduceJob{d.dtype, nullptr, 0, s.M, s.N, bias, residual, act, y,

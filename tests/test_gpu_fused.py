@@ -44,6 +44,8 @@ CONV_CASES = [
     (4, 128, 57, 55, 512, 1, 1, "bf16"),   # 128 x 256 tiles (1x1), ragged rows (196 tiles)
     (5, 64, 120, 120, 64, 3, 1, "f16"),    # 128 x 64 tiles (563 tiles)
     (2, 64, 16, 16, 96, 1, 1, "bf16"),     # c_out % 64 != 0: standalone pass
+    (2, 3, 40, 40, 64, 7, 2, "bf16"),      # image stem (small-channel kernel): counts fused
+    (3, 3, 30, 34, 32, 3, 2, "f16"),       # MobileNetV2-like stem, ragged rows: counts fused
     (2, 32, 16, 16, 64, 3, 1, "bf16"),     # c_in % 64 != 0 (first-generation GEMM): standalone
     (2, 64, 16, 16, 64, 3, 1, "f32"),      # fp32: standalone pass
 ]
