@@ -59,6 +59,12 @@ struct GemmArgs {
   int64_t nchunks, chunks_per_split;
   int64_t x_bytes, w_bytes;  // buffer-descriptor ranges (second-generation kernel)
   float inv_wo, inv_ho;      // 1 / Wo, 1 / Ho rounded once on the host (float divmod)
+  // 32-bit tile walk of the second-generation kernel (every value below
+  // 2^24; the host checks the tile count): column tiles, row x column tiles
+  // per split, chunks per tap, kernel rows, and the reciprocals of the
+  // divisors rounded once (float divmod)
+  int ntn32, ntmn32, cpt32, kh32;
+  float inv_ntn, inv_ntmn, inv_cpt, inv_kw, inv_dh, inv_dw;
   int act;
   int split;
   DeviceRoute route;
@@ -95,19 +101,32 @@ __device__ __forceinline__ f32x4 mfma_chunk(const char *a_row, const char *b_row
 __device__ __forceinline__ int64_t cdiv_dev(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // q = n / d, r = n % d for 0 <= n < 2^24 and 0 < d < 2^24: the float
-// quotient is within one of the true one, then one integer correction.
+// quotient is within one of the true one, then one integer correction,
+// written as selects (no branch: a kernel's start keeps one basic block, so
+// its kernel-argument loads are issued together rather than one round trip
+// per block)
 __device__ __forceinline__ void divmod_small(int n, int d, float inv_d, int &q, int &r) {
-  q = (int)((float)n * inv_d);
-  r = n - q * d;
-  if (r < 0) {
-    --q;
-    r += d;
-  } else if (r >= d) {
-    ++q;
-    r -= d;
-  }
+  const int q0 = (int)((float)n * inv_d);
+  const int r0 = n - q0 * d;
+  const bool lo = r0 < 0, hi = r0 >= d;
+  q = lo ? q0 - 1 : (hi ? q0 + 1 : q0);
+  r = lo ? r0 + d : (hi ? r0 - d : r0);
 }
 
+
+// Bit t set for the taps t of [0, k) whose input coordinate o + t d lies in
+// [0, n): t from ceil(-o / d) to ceil((n - o) / d), clipped to [0, k <= 32)
+// (no branch; inv_d = 1 / d rounded once).
+__device__ __forceinline__ uint32_t taps_inside(int o, int n, int k, int d, float inv_d) {
+  int lo, hi, rem;
+  divmod_small(max(-o, 0) + d - 1, d, inv_d, lo, rem);
+  divmod_small(max(n - o, 0) + d - 1, d, inv_d, hi, rem);
+  lo = min(lo, k);
+  hi = min(hi, k);
+  const uint32_t mhi = hi >= 32 ? ~0u : (1u << hi) - 1u;
+  const uint32_t mlo = lo >= 32 ? ~0u : (1u << lo) - 1u;
+  return hi > lo ? mhi & ~mlo : 0u;
+}
 
 // Reads n <= 32 bits starting at bit `pos` of a bitmap.
 __device__ __forceinline__ uint32_t read_bits(const uint32_t *m, int64_t pos, int n) {
@@ -534,8 +553,16 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   // XCDs, so XCD i gets the i-th contiguous range of tile ids, and a tile id
   // walks (split, row tile, column tile) with the column tiles innermost: the
   // tiles that gather the same input rows run together in one XCD's L2.
-  const int64_t ntm = cdiv_dev(a.M, BM), ntn = cdiv_dev(a.N, BN);
-  const int64_t ntiles = ntm * ntn * a.split;   // == gridDim.x
+  // (tile arithmetic in 32 bits with float-reciprocal division: a 64-bit
+  // division by a runtime value is a long scalar sequence on the critical
+  // path of every work-group's start)
+  // The set-up's kernel arguments are requested in one round trip: this
+  // empty statement needs them at the top (the compiler otherwise loads each
+  // group just before its first use, behind branches, one round trip each).
+  asm volatile("" ::"s"(a.M), "s"(a.N), "s"(a.H), "s"(a.W), "s"(a.Cin), "s"(a.Ho), "s"(a.Wo),
+               "s"(a.Kw), "s"(a.sh), "s"(a.sw), "s"(a.ph), "s"(a.pw), "s"(gridDim.x),
+               "s"(a.route.counts), "s"(a.route.path_out), "s"(a.om_counts));
+  const int ntiles = (int)gridDim.x;   // row tiles x column tiles x splits
   const bool om = BN % 64 == 0 && a.om_counts != nullptr;
   // the device route's counts, requested first as vector loads (in-order
   // counters: waiting for them later does not wait for the loads behind
@@ -550,23 +577,25 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
     rcq[1] = __builtin_amdgcn_raw_buffer_load_b128(cr, 16, 0, 0);
   }
   // one tile; returns its output's zero count and nonzero-block count
-  auto tile_body = [&](const int64_t vid) __attribute__((always_inline)) -> uint2 {
-  int64_t tile;
-  {
-    const int64_t q = ntiles >> 3, r = ntiles & 7, xcd = vid & 7, k = vid >> 3;
-    tile = xcd < r ? xcd * (q + 1) + k : r * (q + 1) + (xcd - r) * q + k;
-  }
-  const int64_t zsplit = tile / (ntm * ntn);
-  const int64_t rest = tile - zsplit * ntm * ntn;
-  const int64_t m0 = (rest / ntn) * BM, n0 = (rest % ntn) * BN;
+  auto tile_body = [&](const int vid) __attribute__((always_inline)) -> uint2 {
+  // (XCD i holds the i-th range: q + 1 tiles for the first r XCDs, q after)
+  const int tile = (vid & 7) * (ntiles >> 3) + min(vid & 7, ntiles & 7) + (vid >> 3);
+  int zsplit_, rest, mt, nt;
+  divmod_small(tile, a.ntmn32, a.inv_ntmn, zsplit_, rest);
+  divmod_small(rest, a.ntn32, a.inv_ntn, mt, nt);
+  const int64_t zsplit = zsplit_;
+  const int64_t m0 = (int64_t)mt * BM, n0 = (int64_t)nt * BN;
   const bool first_tile = tile == 0;
-  const bool first_col = rest % ntn == 0;
-  const int64_t c_begin = zsplit * a.chunks_per_split;
-  const int64_t c_end = min(c_begin + a.chunks_per_split, a.nchunks);
-  const int cpt = (int)(a.Cin / BKC);   // chunks per tap
+  const bool first_col = nt == 0;
+  const int cps = (int)a.chunks_per_split;
+  const int c_begin = zsplit_ * cps;
+  const int c_end = min(c_begin + cps, (int)a.nchunks);
+  const int cpt = a.cpt32;   // chunks per tap
+  const float inv_cpt = a.inv_cpt, inv_kw_ = a.inv_kw;
   auto pack_chunk = [&](int j) __attribute__((always_inline)) -> int {
-    const int t = j / cpt, cb = j - t * cpt;
-    const int r = t / (int)a.Kw, sx = t - r * (int)a.Kw;
+    int t, cb, r, sx;
+    divmod_small(j, cpt, inv_cpt, t, cb);
+    divmod_small(t, (int)a.Kw, inv_kw_, r, sx);
     return j | (cb << 10) | (r << 20) | (sx << 25);
   };
   const int cg = tid % VPR;             // this thread's 16-byte column of a chunk row
@@ -594,17 +623,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
     divmod_small(t1, Ho, inv_ho, nn, oh);
     const int h0 = oh * (int)a.sh - (int)a.ph, w0 = ow * (int)a.sw - (int)a.pw;
     a_offb[u] = (((nn * H + h0) * W + w0) * Cin + cg * 8) * 2;
-    uint32_t rb_ = 0, cb_ = 0;
-    for (int r = 0; r < (int)a.taps / kw; ++r) {
-      const int ih = h0 + r * dh;
-      rb_ |= (ih >= 0 && ih < H ? 1u : 0u) << r;
-    }
-    for (int sx = 0; sx < kw; ++sx) {
-      const int iw = w0 + sx * dw;
-      cb_ |= (iw >= 0 && iw < W ? 1u : 0u) << sx;
-    }
-    vrow[u] = rb_;
-    vcol[u] = cb_;
+    vrow[u] = taps_inside(h0, H, a.kh32, dh, a.inv_dh);
+    vcol[u] = taps_inside(w0, W, kw, dw, a.inv_dw);
   }
   int b_offb[BV];
 #pragma unroll
@@ -614,7 +634,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   }
 
   // ---- skip list ---------------------------------------------------------
-  int64_t count = c_end - c_begin;
+  int count = c_end - c_begin;
   bool use_list = SKIP;
   bool prefilled = false;   // the list already holds the dense walk
   if constexpr (SKIP) {
@@ -678,21 +698,22 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
     __syncthreads();
     if (wave == 0) {
       int total = 0;
-      for (int64_t base = c_begin; base < c_end; base += 64) {
-        const int64_t j = base + lane;
+      for (int base = c_begin; base < c_end; base += 64) {
+        const int j = base + lane;
         bool nz = false;
         if (j < c_end) {
           // chunk j = channels [BKC cb, BKC cb + BKC) of tap t: BKC / 8
           // bitmap bits starting at a multiple of BKC / 8 (cpg is one too),
           // so they lie inside one 32-bit word
-          const int t = (int)(j / cpt), cb = (int)(j - (int64_t)t * cpt);
+          int t, cb;
+          divmod_small(j, cpt, inv_cpt, t, cb);
           const int pos = t * cpg + (BKC / 8) * cb;
           constexpr uint32_t kBits = BKC / 8 >= 32 ? 0xFFFFFFFFu : ((1u << (BKC / 8)) - 1u);
           nz = ((nzvec[pos >> 5] >> (pos & 31)) & kBits) != 0u;
         }
         const uint64_t bal = __ballot(nz);
         const int before = __popcll(bal & ((1ull << lane) - 1ull));
-        if (nz) list[total + before] = pack_chunk((int)j);
+        if (nz) list[total + before] = pack_chunk(j);
         total += __popcll(bal);
       }
       if (lane == 0) {
@@ -863,12 +884,35 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
             acc[tm][tn][v];
   __syncthreads();
   constexpr int C8 = BN / 8;
+  constexpr int EIT = BM * C8 / NT;   // epilogue rows per thread
+  static_assert(BM * C8 % NT == 0 && NT % C8 == 0, "epilogue mapping");
   const bool vec_n = a.N % 8 == 0;
+  // A thread's 8 columns are the same in every epilogue row (NT is a
+  // multiple of C8): its bias vector is loaded once, and the residual
+  // vectors of all its rows are requested before its first store (a load
+  // issued behind stores waits for them here, which serialised the rows).
+  const int c_t = (tid % C8) * 8;
+  const bool vec_t = vec_n && a.split == 1 && n0 + c_t < a.N;
+  using raw_t = typename E::raw;
+  uint4 bias_q = {0u, 0u, 0u, 0u};
+  if (a.bias && vec_t)
+    bias_q = *reinterpret_cast<const uint4 *>(reinterpret_cast<const raw_t *>(a.bias) + n0 + c_t);
+  uint4 res_q[EIT];
+#pragma unroll
+  for (int it = 0; it < EIT; ++it) {
+    const int64_t row = m0 + (tid + it * NT) / C8;
+    res_q[it] = uint4{0u, 0u, 0u, 0u};
+    if (a.residual && vec_t && row < a.M)
+      res_q[it] = *reinterpret_cast<const uint4 *>(reinterpret_cast<const raw_t *>(a.residual) +
+                                                   row * a.N + n0 + c_t);
+  }
   // Output measurement (host: no split, N % 64 == 0, and N % BN == 0 for
   // wider tiles): each 8 consecutive lanes of a tile row hold one bitmap byte
   // (8 channel blocks of 8); every lane stays in the loop for the ballot.
   uint32_t om_zeros = 0, om_nz = 0;
-  for (int q = tid; q < BM * C8; q += NT) {
+#pragma unroll
+  for (int it = 0; it < EIT; ++it) {
+    const int q = tid + it * NT;
     const int r = q / C8, c = (q % C8) * 8;
     const int64_t row = m0 + r, col = n0 + c;
     if (om) {
@@ -882,15 +926,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
         o[4] = hi.x; o[5] = hi.y; o[6] = hi.z; o[7] = hi.w;
         raw t[8], out[8];
         if (a.bias) {
-          const uint4 q4 = *reinterpret_cast<const uint4 *>(reinterpret_cast<const raw *>(a.bias) + col);
-          __builtin_memcpy(t, &q4, 16);
+          __builtin_memcpy(t, &bias_q, 16);
 #pragma unroll
           for (int e = 0; e < 8; ++e) o[e] += E::to_f32(t[e]);
         }
         if (a.residual) {
-          const uint4 q4 = *reinterpret_cast<const uint4 *>(
-              reinterpret_cast<const raw *>(a.residual) + row * a.N + col);
-          __builtin_memcpy(t, &q4, 16);
+          __builtin_memcpy(t, &res_q[it], 16);
 #pragma unroll
           for (int e = 0; e < 8; ++e) o[e] += E::to_f32(t[e]);
         }
@@ -935,15 +976,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
     if (vec_n) {
       raw bv[8], rv[8], out[8];
       if (a.bias) {
-        const uint4 q4 = *reinterpret_cast<const uint4 *>(reinterpret_cast<const raw *>(a.bias) + col);
-        __builtin_memcpy(bv, &q4, 16);
+        __builtin_memcpy(bv, &bias_q, 16);
 #pragma unroll
         for (int e = 0; e < 8; ++e) o[e] += E::to_f32(bv[e]);
       }
       if (a.residual) {
-        const uint4 q4 = *reinterpret_cast<const uint4 *>(
-            reinterpret_cast<const raw *>(a.residual) + row * a.N + col);
-        __builtin_memcpy(rv, &q4, 16);
+        __builtin_memcpy(rv, &res_q[it], 16);
 #pragma unroll
         for (int e = 0; e < 8; ++e) o[e] += E::to_f32(rv[e]);
       }
@@ -986,7 +1024,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   };
   // (one tile per work-group; the lambda form measured fewer scalar-register
   // spills than straight-line code)
-  const uint2 t = tile_body(blockIdx.x);
+  const uint2 t = tile_body((int)blockIdx.x);
   if (om) om_commit(t.x, t.y, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
 }
 
@@ -1629,6 +1667,10 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   a.inv_wo = 1.0f / (float)s.wo;
   a.inv_ho = 1.0f / (float)s.ho;
   a.nchunks = nchunks;
+  a.kh32 = (int)d.kh;
+  a.inv_kw = 1.0f / (float)d.kw;
+  a.inv_dh = 1.0f / (float)d.dh;
+  a.inv_dw = 1.0f / (float)d.dw;
   a.split = t.split_k;
   a.chunks_per_split = cdiv(nchunks, t.split_k);
   a.act = act;
@@ -1660,7 +1702,18 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
     return launch_pointwise(d, x, w, bias, residual, act, y, skip, executed, stream, route, om);
   }
   dim3 grid((unsigned)cdiv(s.M, t.bm), (unsigned)cdiv(s.N, t.bn), (unsigned)gz);
-  if (t.cfg) grid = dim3((unsigned)(cdiv(s.M, t.bm) * cdiv(s.N, t.bn) * gz));
+  if (t.cfg) {
+    const int64_t ntn = cdiv(s.N, t.bn), ntmn = cdiv(s.M, t.bm) * ntn;
+    if (ntmn * gz >= (int64_t)1 << 24)
+      return fail(SPAROA_ERR_UNSUPPORTED, "GEMM: 2^24 tiles or more");
+    grid = dim3((unsigned)(ntmn * gz));
+    a.ntn32 = (int)ntn;
+    a.ntmn32 = (int)ntmn;
+    a.inv_ntn = 1.0f / (float)ntn;
+    a.inv_ntmn = 1.0f / (float)ntmn;
+    a.cpt32 = (int)(d.c_in / t.kchunk);
+    a.inv_cpt = 1.0f / (float)a.cpt32;
+  }
   bool ok = false;
   if (t.cfg) {
     switch (d.dtype) {
