@@ -95,7 +95,41 @@ __device__ __forceinline__ bool route_skip_counts(const sparoa_counts &c, double
 __device__ __forceinline__ bool device_route_skip(const DeviceRoute &r) {
   return route_skip_counts(*r.counts, r.sparsity_thr, r.mode);
 }
+
+// The route's counts as two 16-byte vector loads, requested at a kernel's top
+// and decided on later (their memory round trip then overlaps the kernel's
+// own start).  Vector loads, not scalar ones: the scalar-load counter
+// completes in order, so a scalar load of the counts would make every later
+// kernel-argument use wait for it.  Null counts read zeros (a descriptor of
+// size 0) and route dense.
+struct RouteCountsReq {
+  __attribute__((ext_vector_type(4))) unsigned int q[2];
+};
+__device__ __forceinline__ RouteCountsReq route_counts_request(const DeviceRoute &r) {
+  const __amdgpu_buffer_rsrc_t cr = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)r.counts, (short)0, r.counts ? (int)sizeof(sparoa_counts) : 0, kBufDword3);
+  RouteCountsReq q;
+  q.q[0] = __builtin_amdgcn_raw_buffer_load_b128(cr, 0, 0, 0);
+  q.q[1] = __builtin_amdgcn_raw_buffer_load_b128(cr, 16, 0, 0);
+  return q;
+}
+__device__ __forceinline__ bool route_counts_skip(const RouteCountsReq &q, const DeviceRoute &r) {
+  uint32_t w[8];   // the same in every lane: scalars, so the decision is uniform
+#pragma unroll
+  for (int i = 0; i < 8; ++i) w[i] = __builtin_amdgcn_readfirstlane(q.q[i >> 2][i & 3]);
+  sparoa_counts c;
+  __builtin_memcpy(&c, w, sizeof(c));
+  return r.counts != nullptr && route_skip_counts(c, r.sparsity_thr, r.mode);
+}
 #endif
+
+// Kernel arguments a kernel's start needs, requested together: an empty asm
+// statement that reads them from scalar registers makes the compiler issue
+// their loads at the kernel's top in one memory round trip.  Left alone, it
+// loads each group just before its first use, and a group behind a branch
+// costs a round trip of its own (about 0.5 us at the start of every
+// work-group, measured on the implicit GEMM).
+#define SPAROA_ARGS_UP_FRONT(...) asm volatile("" ::__VA_ARGS__)
 
 // ---- launchers (validated arguments; defined in the .hip files) ---------
 

@@ -356,8 +356,13 @@ __global__ __launch_bounds__(kThreads, 2) void dw3x3_kernel(DwArgs a, FastDiv fc
                                                         FastDiv fho) {
   const int64_t cv = a.C / Dw3Lane<DT>::V;
   const int64_t total = a.N * (a.Ho / RH) * (a.Wo / R) * cv;
-  if (a.route.counts && a.route.path_out && blockIdx.x == 0 && threadIdx.x == 0)
-    *a.route.path_out = (device_route_skip(a.route) ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+  SPAROA_ARGS_UP_FRONT("s"(a.x), "s"(a.w), "s"(a.bias), "s"(a.residual), "s"(a.y), "s"(a.N),
+                       "s"(a.H), "s"(a.W), "s"(a.C), "s"(a.Ho), "s"(a.Wo), "s"(a.act),
+                       "s"(a.om_counts), "s"(a.route.counts), "s"(gridDim.x), "s"(fcv.m),
+                       "s"(fcv.l), "s"(fruns.m), "s"(fruns.l), "s"(fho.m), "s"(fho.l));
+  // the route's counts are requested with the first item's loads; work-group
+  // 0 records the path once they are in (behind no other work-group's start)
+  const RouteCountsReq rq = route_counts_request(a.route);
   int64_t i = xcd_block(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
   if (!COUNT && i >= total) return;   // (COUNT: every thread reaches the commit)
   uint32_t zeros = 0, nz = 0;
@@ -370,6 +375,8 @@ __global__ __launch_bounds__(kThreads, 2) void dw3x3_kernel(DwArgs a, FastDiv fc
     dw3_fetch<DT, S, R, RH>(a, xrs, (uint32_t)i, c0, fcv, fruns, fho, it);
     Dw3Lane<DT> l;
     l.load(a, c0);
+    if (a.route.counts && a.route.path_out && blockIdx.x == 0 && threadIdx.x == 0)
+      *a.route.path_out = (route_counts_skip(rq, a.route) ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
     for (;;) {
       const uint32_t bits = dw3_finish<DT, S, R, RH, COUNT>(a, l, it, &zeros);
       if (COUNT) nz += (uint32_t)__popc(bits);
@@ -395,8 +402,13 @@ __global__ __launch_bounds__(kThreads) void dw3x3_measured_kernel(DwArgs a, Fast
   const int lane = threadIdx.x & 63;
   const int64_t cv = a.C / Dw3Lane<DT>::V;
   const int64_t total = a.N * a.Ho * a.Wo * cv;
-  if (a.route.counts && a.route.path_out && blockIdx.x == 0 && threadIdx.x == 0)
-    *a.route.path_out = (device_route_skip(a.route) ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+  SPAROA_ARGS_UP_FRONT("s"(a.x), "s"(a.w), "s"(a.bias), "s"(a.residual), "s"(a.y), "s"(a.N),
+                       "s"(a.H), "s"(a.W), "s"(a.C), "s"(a.Ho), "s"(a.Wo), "s"(a.act),
+                       "s"(a.om_counts), "s"(a.route.counts), "s"(gridDim.x), "s"(fcv.m),
+                       "s"(fcv.l), "s"(fwo.m), "s"(fwo.l), "s"(fho.m), "s"(fho.l));
+  // the route's counts are requested with the first item's loads; work-group
+  // 0 records the path once they are in (behind no other work-group's start)
+  const RouteCountsReq rq = route_counts_request(a.route);
   const int64_t first = xcd_block(blockIdx.x, gridDim.x) * kThreads + threadIdx.x;
   const int64_t c0 = (int64_t)((uint32_t)first - fdiv((uint32_t)first, fcv) * (uint32_t)cv) *
                      Dw3Lane<DT>::V;
@@ -407,6 +419,8 @@ __global__ __launch_bounds__(kThreads) void dw3x3_measured_kernel(DwArgs a, Fast
   if (first < total) dw3_fetch<DT, S, 1, 1>(a, xrs, (uint32_t)first, c0, fcv, fwo, fho, it);
   Dw3Lane<DT> l;
   l.load(a, c0);
+  if (a.route.counts && a.route.path_out && blockIdx.x == 0 && threadIdx.x == 0)
+    *a.route.path_out = (route_counts_skip(rq, a.route) ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
   for (int64_t base = first - lane; base < total; base += stride) {   // wave-uniform
     const int64_t i = base + lane;
     uint32_t bits = 0;

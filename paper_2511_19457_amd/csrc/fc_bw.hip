@@ -637,8 +637,11 @@ __global__ __launch_bounds__(64 * GroupShape<MT>::NW, MT == 4 ? 2 : 4) void fc_b
                     (MT <= 2 ? 80 : 160) * 1024,
                 "LDS budget");
 
+  // this work-group's operator: the starts at or below blockIdx.x, counted
+  // over fixed indices (their loads are issued together, not one per step)
   int j = 0;
-  while (j + 1 < grp.n && (int)blockIdx.x >= grp.start[j + 1]) ++j;
+#pragma unroll
+  for (int q = 1; q < kGroupMax; ++q) j += (q < grp.n && (int)blockIdx.x >= grp.start[q]) ? 1 : 0;
   const FcBwArgs a = uniform_copy(grp.op[j]);
   const int wg = (int)blockIdx.x - grp.start[j];
   const int tid = threadIdx.x, lane = tid & 63;

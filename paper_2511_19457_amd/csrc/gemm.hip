@@ -408,8 +408,11 @@ template <int DT>
 __global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
   using E = Elem<DT>;
   using raw = typename E::raw;
+  // this work-group's job: the starts at or below blockIdx.x, counted over
+  // fixed indices (their loads are issued together, not one per step)
   int j = 0;
-  while (j + 1 < g.n && (int)blockIdx.x >= g.wg_begin[j + 1]) ++j;
+#pragma unroll
+  for (int q = 1; q < kGroupMax; ++q) j += (q < g.n && (int)blockIdx.x >= g.wg_begin[q]) ? 1 : 0;
   const int64_t b0 = blockIdx.x - g.wg_begin[j], nb = g.wg_begin[j + 1] - g.wg_begin[j];
   const int64_t M = g.M[j], N = g.N[j], total = M * N;
   const float *partial = g.partial[j];
@@ -425,10 +428,31 @@ __global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
   const int64_t om_words = om_mask ? (total / 8 + 31) / 32 : 0;
   uint32_t om_zeros = 0, om_nz = 0;
   if (N % 8 == 0) {
-    for (int64_t v = b0 * 256 + threadIdx.x; v < total / 8; v += nb * 256) {
-      const int64_t i = v * 8, col = i % N;
+    // the column advances by a fixed step mod N (one division per thread)
+    const int64_t step = nb * 256;
+    int64_t col = ((b0 * 256 + threadIdx.x) * 8) % N;
+    const int64_t col_step = (step * 8) % N;
+    for (int64_t v = b0 * 256 + threadIdx.x; v < total / 8;
+         v += step, col = col + col_step >= N ? col + col_step - N : col + col_step) {
+      const int64_t i = v * 8;
       float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      for (int z = 0; z < split; ++z) {
+      // the slices' partial sums added in slice order (the rounding of the
+      // reduction is fixed), four slices' loads in flight at a time
+      int z = 0;
+      for (; z + 4 <= split; z += 4) {
+        float4 lo[4], hi[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          lo[u] = *reinterpret_cast<const float4 *>(partial + (z + u) * total + i);
+          hi[u] = *reinterpret_cast<const float4 *>(partial + (z + u) * total + i + 4);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          o[0] += lo[u].x; o[1] += lo[u].y; o[2] += lo[u].z; o[3] += lo[u].w;
+          o[4] += hi[u].x; o[5] += hi[u].y; o[6] += hi[u].z; o[7] += hi[u].w;
+        }
+      }
+      for (; z < split; ++z) {
         const float4 lo = *reinterpret_cast<const float4 *>(partial + z * total + i);
         const float4 hi = *reinterpret_cast<const float4 *>(partial + z * total + i + 4);
         o[0] += lo.x; o[1] += lo.y; o[2] += lo.z; o[3] += lo.w;
@@ -1083,13 +1107,14 @@ __global__ __launch_bounds__(256) void conv_small_c_kernel(SmallCArgs a) {
   const int nwn = a.Cout / 16, nwm = 4 / nwn;   // waves over column / row blocks
   const int wn = wave % nwn, wm = wave / nwn;
   const int g = lane >> 4, rl = lane & 15;
+  SPAROA_ARGS_UP_FRONT("s"(a.x), "s"(a.w), "s"(a.H), "s"(a.W), "s"(a.C), "s"(a.Ho), "s"(a.Cout),
+                       "s"(a.kh), "s"(a.sh), "s"(a.ph), "s"(a.w_elems), "s"(a.c_w),
+                       "s"(a.region_off), "s"(a.inv_rv), "s"(a.vec), "s"(a.mode),
+                       "s"(a.route.counts));
   const int img = (int)(blockIdx.x / (unsigned)a.Ho), oh = (int)(blockIdx.x % (unsigned)a.Ho);
-  bool skip = a.mode == 1;
-  if (a.mode == 2) {
-    skip = device_route_skip(a.route);
-    if (a.route.path_out && blockIdx.x == 0 && tid == 0)
-      *a.route.path_out = (skip ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
-  }
+  // the device route's counts are requested now and decided on once the
+  // weights and input rows are staged (nothing before needs the decision)
+  const RouteCountsReq rq = route_counts_request(a.route);
   // LDS: patch [kh][PWP][4] | region: weights [Cout*kh*kw*C], raw input rows
   // [kh][W*C] while the operands are built, then the fp32 output tile
   raw *patch = reinterpret_cast<raw *>(smem);
@@ -1147,6 +1172,12 @@ __global__ __launch_bounds__(256) void conv_small_c_kernel(SmallCArgs a) {
     }
   }
   __syncthreads();
+  bool skip = a.mode == 1;
+  if (a.mode == 2) {
+    skip = route_counts_skip(rq, a.route);
+    if (a.route.path_out && blockIdx.x == 0 && tid == 0)
+      *a.route.path_out = (skip ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+  }
 
   // ---- padded patch patch[r][q][c4] (q = input column + pw; zero outside
   // the image and for channels >= C; one column past PW keeps every operand

@@ -274,6 +274,8 @@ __global__ __launch_bounds__(kLanebitThreads) void measure_lanebit(const char *_
                                                                    uint32_t *__restrict__ mask,
                                                                    sparoa_counts *counts,
                                                                    unsigned long long *commit) {
+  SPAROA_ARGS_UP_FRONT("s"(x), "s"(items), "s"(words), "s"(mask), "s"(counts), "s"(commit),
+                       "s"(gridDim.x));
   lanebit_pass<ESZ, V>(x, items, words, mask, counts, blockIdx.x, gridDim.x, commit);
 }
 
@@ -291,6 +293,8 @@ __global__ __launch_bounds__(kLanebitThreads) void measure_rowbit(const char *__
                                                                   uint32_t *__restrict__ mask,
                                                                   sparoa_counts *counts,
                                                                   unsigned long long *commit) {
+  SPAROA_ARGS_UP_FRONT("s"(x), "s"(rows), "s"(cols), "s"(words), "s"(mask), "s"(counts),
+                       "s"(commit), "s"(gridDim.x));
   constexpr int EPV = 16 / ESZ;  // elements per 16-byte vector
   const int lane = threadIdx.x & 63;
   const int nv = cols * ESZ / 2;  // vectors per 8 rows
@@ -362,8 +366,11 @@ __global__ void measure_init_group(LanebitGroup g) {
 
 template <int ESZ, int V>
 __global__ __launch_bounds__(kLanebitThreads) void measure_lanebit_group(LanebitGroup g) {
+  // this work-group's tensor: the starts at or below blockIdx.x, counted
+  // over fixed indices (their loads are issued together, not one per step)
   int j = 0;
-  while (j + 1 < g.n && (int)blockIdx.x >= g.wg_begin[j + 1]) ++j;
+#pragma unroll
+  for (int q = 1; q < kGroupMax; ++q) j += (q < g.n && (int)blockIdx.x >= g.wg_begin[q]) ? 1 : 0;
   lanebit_pass<ESZ, V>(g.x[j], g.items[j], (g.items[j] + 31) / 32, g.mask[j], g.counts[j],
                        blockIdx.x - g.wg_begin[j], g.wg_begin[j + 1] - g.wg_begin[j]);
 }

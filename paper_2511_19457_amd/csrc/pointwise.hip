@@ -69,15 +69,11 @@ struct PwArgs {
 };
 
 __device__ __forceinline__ void divmod_f(int n, int d, float inv_d, int &q, int &r) {
-  q = (int)((float)n * inv_d);
-  r = n - q * d;
-  if (r < 0) {
-    --q;
-    r += d;
-  } else if (r >= d) {
-    ++q;
-    r -= d;
-  }
+  const int q0 = (int)((float)n * inv_d);
+  const int r0 = n - q0 * d;
+  const bool lo = r0 < 0, hi = r0 >= d;   // one correction, as selects
+  q = lo ? q0 - 1 : (hi ? q0 + 1 : q0);
+  r = lo ? r0 + d : (hi ? r0 - d : r0);
 }
 
 template <int DT, int NB, int R, int KS>
@@ -96,12 +92,12 @@ __global__ __launch_bounds__(kPwThreads) void pointwise_kernel(PwArgs a) {
   const int wgs_per_slice = (int)(gridDim.x / (unsigned)a.slices);
   const int c0 = slice * a.bn;
 
-  bool skip = a.mode == 1;
-  if (a.mode == 2) {
-    skip = device_route_skip(a.route);
-    if (a.route.path_out && blockIdx.x == 0 && tid == 0)
-      *a.route.path_out = (skip ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
-  }
+  SPAROA_ARGS_UP_FRONT("s"(a.x), "s"(a.w), "s"(a.y), "s"(a.M), "s"(a.K), "s"(a.Cout),
+                       "s"(a.bn), "s"(a.slices), "s"(a.row_bytes), "s"(a.x_bytes), "s"(a.mode),
+                       "s"(a.route.counts));
+  // the device route's counts are requested now and decided on once the
+  // weight slice is staged (nothing before needs the decision)
+  const RouteCountsReq rq = route_counts_request(a.route);
 
   // ---- weight slice -> LDS, zero past C_out and past K (16-byte vectors;
   // K % 8 == 0, so a vector never straddles two rows).  Eight independent
@@ -129,6 +125,12 @@ __global__ __launch_bounds__(kPwThreads) void pointwise_kernel(PwArgs a) {
     }
   }
   __syncthreads();
+  bool skip = a.mode == 1;
+  if (a.mode == 2) {
+    skip = route_counts_skip(rq, a.route);
+    if (a.route.path_out && blockIdx.x == 0 && tid == 0)
+      *a.route.path_out = (skip ? 1u : 0u) | ((uint32_t)a.route.bw_bit << 1);
+  }
 
   const __amdgpu_buffer_rsrc_t xr =
       __builtin_amdgcn_make_buffer_rsrc((void *)a.x, (short)0, a.x_bytes, kBufDword3);
