@@ -468,6 +468,42 @@ __global__ __launch_bounds__(kThreads) void maxpool_kernel(const char *x, char *
   }
 }
 
+// The same pooling with 32-bit indices (items and x below 2^31 elements):
+// the item decomposes by multiply-shift divisions (a 64-bit division per
+// item made the general kernel ALU-bound at about 3.4 TB/s), one item per
+// lane.
+template <int DT, int V>
+__global__ __launch_bounds__(kThreads) void maxpool32_kernel(const char *x, char *y, int C, int H,
+                                                             int W, int Ho, int Wo, int k, int s,
+                                                             int p, uint32_t total, FastDiv fcv,
+                                                             FastDiv fwo, FastDiv fho) {
+  SPAROA_ARGS_UP_FRONT("s"(x), "s"(y), "s"(C), "s"(H), "s"(W), "s"(total), "s"(fcv.m),
+                       "s"(fcv.l), "s"(fwo.m), "s"(fwo.l), "s"(fho.m), "s"(fho.l));
+  using E = Elem<DT>;
+  constexpr int ESZ = E::size;
+  const uint32_t i = blockIdx.x * (uint32_t)kThreads + threadIdx.x;
+  if (i >= total) return;
+  const uint32_t pix = fdiv(i, fcv), t = fdiv(pix, fwo), n = fdiv(t, fho);
+  const int c0 = (int)(i - pix * fcv.d) * V;
+  const int ow = (int)(pix - t * fwo.d), oh = (int)(t - n * fho.d);
+  float best[V];
+#pragma unroll
+  for (int j = 0; j < V; ++j) best[j] = -INFINITY;
+  for (int r = 0; r < k; ++r) {
+    const int ih = oh * s - p + r;
+    if (ih < 0 || ih >= H) continue;
+    for (int q = 0; q < k; ++q) {
+      const int iw = ow * s - p + q;
+      if (iw < 0 || iw >= W) continue;
+      float v[V];
+      load_vec<DT, V>(x + (size_t)((((int)n * H + ih) * W + iw) * C + c0) * ESZ, v);
+#pragma unroll
+      for (int j = 0; j < V; ++j) best[j] = v[j] > best[j] ? v[j] : best[j];
+    }
+  }
+  store_vec<DT, V>(y + (size_t)((int)pix * C + c0) * ESZ, best);
+}
+
 // Run length of the 3x3 kernel: 4 outputs along w at stride 1 where 4
 // divides Wo, else 2 where Wo is even, else 1 (a run never crosses a row).
 // Longer runs re-read fewer input columns per output.
@@ -590,6 +626,15 @@ sparoa_status mp_dispatch(const void *x, void *y, int64_t n, int64_t c, int64_t 
   if (blocks > 65536) blocks = 65536;
   const char *xp = static_cast<const char *>(x);
   char *yp = static_cast<char *>(y);
+  if (vec && total < (1ll << 31) && n * h * w * c < (1ll << 31) && n * ho * wo * c < (1ll << 31)) {
+    const uint32_t cv = (uint32_t)(c / VV);
+    hipLaunchKernelGGL((maxpool32_kernel<DT, VV>), dim3((unsigned)cdiv(total, kThreads)),
+                       dim3(kThreads), 0, st, xp, yp, (int)c, (int)h, (int)w, (int)ho, (int)wo, k,
+                       s, p, (uint32_t)total, make_fastdiv(cv), make_fastdiv((uint32_t)wo),
+                       make_fastdiv((uint32_t)ho));
+    SPAROA_LAUNCH_CHECK("maxpool32_kernel");
+    return SPAROA_OK;
+  }
   if (vec)
     hipLaunchKernelGGL((maxpool_kernel<DT, VV>), dim3((unsigned)blocks), dim3(kThreads), 0, st, xp,
                        yp, n, c, h, w, ho, wo, k, s, p);

@@ -220,13 +220,19 @@ def test_config1_full():
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
-def test_maxpool_vs_oracle(dt):
+@pytest.mark.parametrize("shape", [(2, 17, 18, 64), (3, 29, 23, 24), (2, 9, 7, 12), (1, 4, 4, 8)],
+                         ids=["c64", "c24-odd-hw", "c12-general", "tiny"])
+def test_maxpool_vs_oracle(dt, shape):
+    # whole 16-byte channel vectors: the 32-bit multiply-shift kernel; C = 12
+    # in a 16-bit type: the general one
     abi = _abi()
-    x = synth.normal((2, 17, 18, 64), dt, 123)
-    y = torch.empty(2, 9, 9, 64, dtype=DT[dt], device="cuda")
-    abi.sparoa_maxpool2d(x.cuda(), 2, 64, 17, 18, 3, 2, 1, y)
+    n, h, w, c = shape
+    x = synth.normal((n, h, w, c), dt, 123 + c)
+    ho, wo = (h - 1) // 2 + 1, (w - 1) // 2 + 1
+    y = torch.empty(n, ho, wo, c, dtype=DT[dt], device="cuda")
+    abi.sparoa_maxpool2d(x.cuda(), n, c, h, w, 3, 2, 1, y)
     torch.cuda.synchronize()
-    ref = oracle.maxpool2d(x, 2, 64, 17, 18)
+    ref = oracle.maxpool2d(x, n, c, h, w)
     assert np.array_equal(y.float().cpu().numpy().astype(np.float64), ref)
 
 
