@@ -381,8 +381,10 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
  *   the fused form adds into it (a caller resets all of a network's counters
  *   with one copy from a template before each pass).
  *   Fused into the producer's epilogue (or its split-K reduction) where the
- *   kernel that serves the layer can (the 64-channel-chunk implicit GEMM with
- *   cols % 64 == 0; the pointwise kernel with one weight slice): no launch of
+ *   kernel that serves the layer can (the 64-channel-chunk implicit GEMM --
+ *   16-bit, C_in % 64 == 0 or C_in % 8 == 0 with C_in >= 48 -- with
+ *   cols % 64 == 0; the pointwise kernel with one weight slice; the depthwise
+ *   and image-stem kernels, counts only for the stem): no launch of
  *   its own and no second read of y; otherwise the standalone measurement of
  *   y runs after the layer (as sparoa_measure_sparsity_preset with y_commit:
  *   one launch for the block shapes whose bitmap needs no clearing).
@@ -432,9 +434,10 @@ sparoa_status sparoa_fc_routed_measured(const sparoa_fc_desc *desc, const sparoa
  *     (sparoa_measure_sparsity with samples = n, or = m for an FC).
  *   mask: bitmap of x at block (1, 8).
  *   executed_blocks_dev (nullable): executed (row tile, tap, 64-channel
- *     chunk) triples, every chunk counting on a dense tile.
- * Errors: UNSUPPORTED unless the 16-bit, C_in % 64 == 0, groups 1 implicit
- * GEMM serves the layer; INVALID_ARG for null pointers or a NaN / negative
+ *     chunk) triples, every chunk counting on a dense tile (a tap's last
+ *     chunk holds C_in mod 64 channels when C_in % 64 != 0).
+ * Errors: UNSUPPORTED unless the 16-bit, groups 1 implicit GEMM serves the
+ * layer (C_in % 64 == 0, or C_in % 8 == 0 and C_in >= 48); INVALID_ARG for null pointers or a NaN / negative
  * threshold; WORKSPACE as for sparoa_conv2d.
  * ---------------------------------------------------------------------- */
 sparoa_status sparoa_conv2d_split(const sparoa_conv_desc *desc, double sparsity_thr,

@@ -535,7 +535,10 @@ __global__ __launch_bounds__(256) void split_reduce_group(ReduceGroup g) {
 constexpr int kBK2 = 64;
 constexpr int kMaxChunks2 = 1024;          // K <= 65536 on the skip path
 
-template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
+// PART: C_in % 64 != 0, a tap's last chunk is partial (a separate
+// instantiation: the per-lane channel test and the per-chunk weight offset
+// cost the whole-chunk kernels up to 10 %).
+template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP, bool PART>
 __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   constexpr int NT = 64 * WGM * WGN;   // threads per work-group
   constexpr int BKC = 32 * KS;         // channels per chunk (KS MFMA k-steps)
@@ -567,7 +570,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   // j | cb << 10 | r << 20 | s << 25 (chunk id, channel block within the
   // tap, kernel row and column): the walk needs no division per chunk
   __shared__ int list[kMaxChunks2];
-  __shared__ uint32_t nzvec[SKIP ? kMaxVecWords : 1];
+  __shared__ uint32_t nzvec[SKIP ? kMaxVecWords + 1 : 1];
   __shared__ int list_len;
   __shared__ uint8_t ombytes[BM * (BN / 64 > 0 ? BN / 64 : 1)];   // output bitmap bytes of the tile
 
@@ -696,7 +699,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
   }
   if (SKIP && use_list) {
     const int cpg = (int)(a.Cin / 8);  // bitmap blocks per pixel
-    const int kv_words = (int)((a.taps * cpg + 31) / 32);
+    const int kv_words = (int)((a.taps * cpg + 31) / 32) + 1;   // + the window's spare word
     for (int i = tid; i < kv_words; i += NT) nzvec[i] = 0u;
     __syncthreads();
     // (32-bit index arithmetic with float-reciprocal division: pixel
@@ -726,14 +729,25 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
         const int j = base + lane;
         bool nz = false;
         if (j < c_end) {
-          // chunk j = channels [BKC cb, BKC cb + BKC) of tap t: BKC / 8
-          // bitmap bits starting at a multiple of BKC / 8 (cpg is one too),
-          // so they lie inside one 32-bit word
+          // chunk j = channels [BKC cb, min(BKC cb + BKC, Cin)) of tap t:
+          // up to BKC / 8 bitmap bits from bit t cpg + (BKC / 8) cb, read
+          // through a 64-bit window (with cpg % 8 != 0 they may straddle a
+          // word; the word past the last is cleared)
+          // (whole chunks: BKC / 8 bits at a multiple of BKC / 8, inside
+          // one word)
+          static_assert(BKC / 8 <= 32, "chunk bits in a 64-bit window");
           int t, cb;
           divmod_small(j, cpt, inv_cpt, t, cb);
           const int pos = t * cpg + (BKC / 8) * cb;
-          constexpr uint32_t kBits = BKC / 8 >= 32 ? 0xFFFFFFFFu : ((1u << (BKC / 8)) - 1u);
-          nz = ((nzvec[pos >> 5] >> (pos & 31)) & kBits) != 0u;
+          if constexpr (PART) {
+            const int nb = min(BKC / 8, cpg - (BKC / 8) * cb);
+            const uint64_t win =
+                (uint64_t)nzvec[pos >> 5] | ((uint64_t)nzvec[(pos >> 5) + 1] << 32);
+            nz = ((win >> (pos & 31)) & ((1ull << nb) - 1ull)) != 0ull;
+          } else {
+            constexpr uint32_t kBits = BKC / 8 >= 32 ? 0xFFFFFFFFu : ((1u << (BKC / 8)) - 1u);
+            nz = ((nzvec[pos >> 5] >> (pos & 31)) & kBits) != 0u;
+          }
         }
         const uint64_t bal = __ballot(nz);
         const int before = __popcll(bal & ((1ull << lane) - 1ull));
@@ -761,16 +775,22 @@ __global__ __launch_bounds__(64 * WGM * WGN, 2) void igemm_kernel(GemmArgs a) {
     const int j = info & 1023, cb = (info >> 10) & 1023;
     const int r = (info >> 20) & 31, sx = (info >> 25) & 31;
     const int tap_offb = ((r * dh * W + sx * dw) * Cin + cb * BKC) * 2;
+    // PART: this lane's 8 channels of the chunk exist (channels past C_in in
+    // the last chunk of a tap read zero on both sides), and the chunk starts
+    // at K index (r kw + sx) C_in + BKC cb of a weight row (whole chunks:
+    // at BKC j)
+    const bool col = PART ? valid && cb * BKC + cg * 8 < Cin : valid;
+    const int kofs = PART ? ((r * kw + sx) * Cin + cb * BKC) * 2 : j * (BKC * 2);
 #pragma unroll
     for (int u = 0; u < AV; ++u) {
-      const bool in_img = valid && ((vrow[u] >> r) & (vcol[u] >> sx) & 1u);
+      const bool in_img = col && ((vrow[u] >> r) & (vcol[u] >> sx) & 1u);
       const int off = in_img ? a_offb[u] + tap_offb : (int)0x80000000;
       ra_s[u] = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
     }
 #pragma unroll
     for (int u = 0; u < BV; ++u)
-      rb_s[u] = __builtin_amdgcn_raw_buffer_load_b128(wr, valid ? b_offb[u] : (int)0x80000000,
-                                                      valid ? j * (BKC * 2) : 0, 0);
+      rb_s[u] = __builtin_amdgcn_raw_buffer_load_b128(wr, col ? b_offb[u] : (int)0x80000000,
+                                                      valid ? kofs : 0, 0);
   };
   // every row a thread stores is rr mod 8 (RPU and BM are multiples of 8)
   const int st_col = 16 * (cg ^ (rr & 7));
@@ -1314,9 +1334,9 @@ __global__ __launch_bounds__(256) void conv_small_c_kernel(SmallCArgs a) {
   if (a.om_counts) om_commit(om_zeros, om_nz, a.om_counts, a.om_words, blockIdx.x, gridDim.x);
 }
 
-template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP>
+template <int DT, int WGM, int WGN, int WTM, int WTN, int PF, int KS, bool SKIP, bool PART>
 void launch_ig(dim3 grid, hipStream_t st, const GemmArgs &a) {
-  hipLaunchKernelGGL((igemm_kernel<DT, WGM, WGN, WTM, WTN, PF, KS, SKIP>), grid,
+  hipLaunchKernelGGL((igemm_kernel<DT, WGM, WGN, WTM, WTN, PF, KS, SKIP, PART>), grid,
                      dim3(64 * WGM * WGN), 0, st, a);
 }
 
@@ -1327,13 +1347,20 @@ enum IgCfg { kIg128x64 = 1, kIg64x64, kIg128x128, kIg128x256 };
 // 64-channel chunks: two MFMA k-steps per barrier (four measured slower:
 // more LDS and registers per work-group for the same latency per step).
 template <int DT, bool SKIP>
-bool dispatch_ig(int cfg, int kchunk, dim3 grid, hipStream_t st, const GemmArgs &a) {
+bool dispatch_ig(int cfg, int kchunk, bool part, dim3 grid, hipStream_t st, const GemmArgs &a) {
   if (kchunk != kBK2) return false;
+  if (part) {   // partial chunks: the two tiles the chooser takes for them
+    switch (cfg) {
+      case kIg128x64: launch_ig<DT, 2, 2, 4, 2, 4, 2, SKIP, true>(grid, st, a); return true;
+      case kIg64x64: launch_ig<DT, 2, 2, 2, 2, 4, 2, SKIP, true>(grid, st, a); return true;
+    }
+    return false;
+  }
   switch (cfg) {
-    case kIg128x64: launch_ig<DT, 2, 2, 4, 2, 4, 2, SKIP>(grid, st, a); return true;
-    case kIg64x64: launch_ig<DT, 2, 2, 2, 2, 4, 2, SKIP>(grid, st, a); return true;
-    case kIg128x128: launch_ig<DT, 2, 2, 4, 4, 3, 2, SKIP>(grid, st, a); return true;
-    case kIg128x256: launch_ig<DT, 2, 4, 4, 4, 3, 2, SKIP>(grid, st, a); return true;
+    case kIg128x64: launch_ig<DT, 2, 2, 4, 2, 4, 2, SKIP, false>(grid, st, a); return true;
+    case kIg64x64: launch_ig<DT, 2, 2, 2, 2, 4, 2, SKIP, false>(grid, st, a); return true;
+    case kIg128x128: launch_ig<DT, 2, 2, 4, 4, 3, 2, SKIP, false>(grid, st, a); return true;
+    case kIg128x256: launch_ig<DT, 2, 4, 4, 4, 3, 2, SKIP, false>(grid, st, a); return true;
   }
   return false;
 }
@@ -1533,8 +1560,12 @@ bool ig_eligible(const sparoa_conv_desc &d) {
   if (d.n * d.h * d.w * d.c_in >= ((int64_t)1 << 30)) return false;
   if (shape_of(d).M >= ((int64_t)1 << 24) || d.kw > 32 || d.kh > 32) return false;
   if (d.c_out * d.kh * d.kw * d.c_in >= ((int64_t)1 << 30)) return false;
-  return d.dtype != SPAROA_F32 && d.groups == 1 && d.c_in % kBK2 == 0 &&
-         cdiv(d.kh * d.kw * d.c_in, kBK2) <= kMaxChunks2 &&
+  // C_in a multiple of 8 (16-byte vectors); a tap's last chunk may be
+  // partial (its channels past C_in read zero), from 48 channels up (below,
+  // most of a chunk would be padding)
+  return d.dtype != SPAROA_F32 && d.groups == 1 &&
+         (d.c_in % kBK2 == 0 || (d.c_in % 8 == 0 && d.c_in >= 48)) &&
+         d.kh * d.kw * cdiv(d.c_in, kBK2) <= kMaxChunks2 &&
          d.kh * d.kw * (d.c_in / 8) <= (int64_t)kMaxVecWords * 32;
 }
 
@@ -1557,16 +1588,19 @@ GemmTileChoice ig_choose(const Shape &s, int64_t c_in) {
   // channels instead of 128; 7 - 13 % faster on 1 x 1 convs and GEMMs with
   // N >= 1024 (FFN 2048 x 768 -> 3072: 28.2 -> 25.8 us), 2 - 9 % slower on
   // 3 x 3 convs with 256-512 channels, which keep 128 x 128
-  if (one_tap && s.N % 256 == 0 && tiles(128, 256) >= 192) {
+  // (partial chunks, C_in % 64 != 0: 128 x 64 or 64 x 64 only)
+  const bool whole = c_in % t.kchunk == 0;
+  if (whole && one_tap && s.N % 256 == 0 && tiles(128, 256) >= 192) {
     t.cfg = kIg128x256; t.bm = 128; t.bn = 256;
-  } else if (s.N % 128 == 0 && tiles(128, 128) >= 384) {
+  } else if (whole && s.N % 128 == 0 && tiles(128, 128) >= 384) {
     t.cfg = kIg128x128; t.bm = 128; t.bn = 128;
   } else if (tiles(128, 64) >= 240) {
     t.cfg = kIg128x64; t.bm = 128; t.bn = 64;
   } else {
     t.cfg = kIg64x64; t.bm = 64; t.bn = 64;
   }
-  const int64_t tl = tiles(t.bm, t.bn), nchunks = cdiv(s.K, t.kchunk);
+  // chunks: whole or partial 64-channel blocks of each tap
+  const int64_t tl = tiles(t.bm, t.bn), nchunks = (s.K / c_in) * cdiv(c_in, t.kchunk);
   int64_t split = 1;
   if (tl < 192) {
     // about one work-group per CU: more splits cost more partial traffic than
@@ -1675,7 +1709,10 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
   // the skip form: x's bitmap given, or a skip path on a kernel that tests x
   // itself (the pointwise and small-channel kernels read no bitmap)
   const bool skip = mask != nullptr || ((path & 1) && (t.pointwise || t.small_c));
-  const int64_t nchunks = cdiv(s.K, t.kchunk);
+  // (the second-generation kernel's chunks are per tap: whole or partial
+  // 64-channel blocks)
+  const int64_t nchunks =
+      t.cfg ? d.kh * d.kw * cdiv(d.c_in, t.kchunk) : cdiv(s.K, t.kchunk);
   if (skip && !gemm_skip_supported(d))
     return fail(SPAROA_ERR_UNSUPPORTED, "zero-skip conv: K above the skip kernel's 65536");
   if (s.M > INT32_MAX || s.N > INT32_MAX) return fail(SPAROA_ERR_UNSUPPORTED, "GEMM too large");
@@ -1742,19 +1779,20 @@ sparoa_status launch_gemm_conv(const sparoa_conv_desc &d, sparoa_path path, cons
     a.ntmn32 = (int)ntmn;
     a.inv_ntn = 1.0f / (float)ntn;
     a.inv_ntmn = 1.0f / (float)ntmn;
-    a.cpt32 = (int)(d.c_in / t.kchunk);
+    a.cpt32 = (int)cdiv(d.c_in, t.kchunk);
     a.inv_cpt = 1.0f / (float)a.cpt32;
   }
   bool ok = false;
+  const bool part = d.c_in % kBK2 != 0;   // a tap's last chunk is partial
   if (t.cfg) {
     switch (d.dtype) {
       case SPAROA_BF16:
-        ok = skip ? dispatch_ig<SPAROA_BF16, true>(t.cfg, t.kchunk, grid, stream, a)
-                  : dispatch_ig<SPAROA_BF16, false>(t.cfg, t.kchunk, grid, stream, a);
+        ok = skip ? dispatch_ig<SPAROA_BF16, true>(t.cfg, t.kchunk, part, grid, stream, a)
+                  : dispatch_ig<SPAROA_BF16, false>(t.cfg, t.kchunk, part, grid, stream, a);
         break;
       case SPAROA_F16:
-        ok = skip ? dispatch_ig<SPAROA_F16, true>(t.cfg, t.kchunk, grid, stream, a)
-                  : dispatch_ig<SPAROA_F16, false>(t.cfg, t.kchunk, grid, stream, a);
+        ok = skip ? dispatch_ig<SPAROA_F16, true>(t.cfg, t.kchunk, part, grid, stream, a)
+                  : dispatch_ig<SPAROA_F16, false>(t.cfg, t.kchunk, part, grid, stream, a);
         break;
       default: break;
     }

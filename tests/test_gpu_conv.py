@@ -249,6 +249,12 @@ IG_SHAPES = [
     ((1, 128, 32, 64, 1024, 1, 1, 1, 1, 0, 0, 1, 1, 1), 128),  # 128 x 64, wide N
     ((2, 128, 9, 9, 96, 3, 3, 2, 2, 1, 1, 1, 1, 1), 64),       # 64 x 64, split-K
     ((1, 192, 7, 7, 36, 3, 3, 1, 1, 1, 1, 1, 1, 1), 64),       # 64 x 64, N % 8 != 0
+    # C_in % 64 != 0: a tap's last chunk is partial
+    ((2, 96, 14, 14, 576, 1, 1, 1, 1, 0, 0, 1, 1, 1), 64),     # 1x1, 96 = 64 + 32
+    ((1, 160, 7, 7, 960, 1, 1, 1, 1, 0, 0, 1, 1, 1), 64),      # 1x1, 160 = 2 x 64 + 32
+    ((32, 96, 28, 28, 128, 1, 1, 1, 1, 0, 0, 1, 1, 1), 128),   # 128 x 64, 1x1
+    ((2, 56, 19, 21, 72, 3, 3, 1, 1, 1, 1, 1, 1, 1), 64),      # 3x3, 56 < 64: one partial chunk per tap
+    ((1, 200, 9, 11, 64, 3, 3, 2, 2, 1, 1, 1, 1, 1), 64),      # 3x3 stride 2, 200 = 3 x 64 + 8, split-K
 ]
 
 

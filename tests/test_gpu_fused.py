@@ -46,7 +46,11 @@ CONV_CASES = [
     (2, 64, 16, 16, 96, 1, 1, "bf16"),     # c_out % 64 != 0: standalone pass
     (2, 3, 40, 40, 64, 7, 2, "bf16"),      # image stem (small-channel kernel): counts fused
     (3, 3, 30, 34, 32, 3, 2, "f16"),       # MobileNetV2-like stem, ragged rows: counts fused
-    (2, 32, 16, 16, 64, 3, 1, "bf16"),     # c_in % 64 != 0 (first-generation GEMM): standalone
+    (2, 32, 16, 16, 64, 3, 1, "bf16"),     # c_in < 48, not a multiple of 64 (first-generation GEMM): standalone
+    (4, 96, 14, 14, 576, 1, 1, "f16"),     # c_in % 64 != 0 (partial chunks): fused epilogue
+    (2, 160, 7, 7, 960, 1, 1, "f16"),      # partial chunks, 160 = 2 x 64 + 32
+    (1, 160, 7, 7, 192, 3, 1, "bf16"),     # partial chunks, split-K: fused reduction
+    (3, 72, 17, 15, 128, 3, 1, "bf16"),    # partial chunks per tap of a 3x3 kernel
     (2, 64, 16, 16, 64, 3, 1, "f32"),      # fp32: standalone pass
 ]
 
@@ -74,7 +78,7 @@ def test_conv_routed_measured(case):
     commit = torch.zeros(abi.COMMIT_WORDS_BYTES // 8, dtype=torch.int64, device=dev)
     rows, cols = n * ho * wo, cout
     # the GEMM measures y itself (ticketed commits through `commit`)
-    fused = dt != "f32" and cin % 64 == 0 and cout % 64 == 0
+    fused = dt != "f32" and (cin % 64 == 0 or (cin % 8 == 0 and cin >= 48)) and cout % 64 == 0
     for s_thr in (0.0, 2.0):       # skip and dense routes
         y = torch.full((n, ho, wo, cout), float("nan"), dtype=tdt, device=dev)
         y_counts = _fresh_counts(rows, cols, dev)
