@@ -383,7 +383,8 @@ sparoa_status sparoa_fc_routed(const sparoa_fc_desc *desc, const sparoa_threshol
  *   Fused into the producer's epilogue (or its split-K reduction) where the
  *   kernel that serves the layer can (the 64-channel-chunk implicit GEMM --
  *   16-bit, C_in % 64 == 0 or C_in % 8 == 0 with C_in >= 48 -- with
- *   cols % 64 == 0; the pointwise kernel with one weight slice; the depthwise
+ *   cols % 64 == 0, or cols % 8 == 0 where it splits K and its reduction
+ *   writes y; the pointwise kernel with one weight slice; the depthwise
  *   and image-stem kernels, counts only for the stem): no launch of
  *   its own and no second read of y; otherwise the standalone measurement of
  *   y runs after the layer (as sparoa_measure_sparsity_preset with y_commit:

@@ -1682,8 +1682,14 @@ bool gemm_fuses_out_measure(const sparoa_conv_desc &d, sparoa_path path, bool bi
   // the small-channel kernel counts (no bitmap)
   if (t.small_c) return !bitmap;
   // the second-generation kernel (64-column tiles) writes whole bitmap bytes
-  // when C_out % 64 == 0; its split-K reduction measures 16-byte vectors
-  return t.cfg != 0 && d.c_out % 64 == 0 && elem_size(d.dtype) == 2;
+  // when C_out % 64 == 0; its split-K reduction measures 16-byte vectors (a
+  // wave's 64 vectors are two whole bitmap words), any C_out % 8 == 0
+  if (t.cfg == 0 || elem_size(d.dtype) != 2) return false;
+  if (d.c_out % 64 == 0) return true;
+  // the K splits the launch will take (as launch_gemm_conv counts them)
+  const int64_t nchunks = d.kh * d.kw * cdiv(d.c_in, t.kchunk);
+  const int64_t gz = cdiv(nchunks, cdiv(nchunks, t.split_k));
+  return gz > 1 && d.c_out % 8 == 0;
 }
 
 size_t gemm_workspace_required(const sparoa_conv_desc &d, sparoa_path path) {

@@ -50,6 +50,8 @@ CONV_CASES = [
     (4, 96, 14, 14, 576, 1, 1, "f16"),     # c_in % 64 != 0 (partial chunks): fused epilogue
     (2, 160, 7, 7, 960, 1, 1, "f16"),      # partial chunks, 160 = 2 x 64 + 32
     (1, 160, 7, 7, 192, 3, 1, "bf16"),     # partial chunks, split-K: fused reduction
+    (1, 160, 7, 7, 96, 3, 1, "bf16"),      # c_out % 64 != 0, split-K: the reduction measures
+    (32, 960, 7, 7, 160, 1, 1, "f16"),     # MobileNetV2 project-like: split-K, c_out = 160
     (3, 72, 17, 15, 128, 3, 1, "bf16"),    # partial chunks per tap of a 3x3 kernel
     (2, 64, 16, 16, 64, 3, 1, "f32"),      # fp32: standalone pass
 ]
