@@ -47,7 +47,8 @@ INTENSITY_THR = 315.0   # bf16 ridge point of MI355X: 2.5 PFLOP/s / 8 TB/s (data
 SKIP_MARGIN = 0.97      # calibration: a skip path must beat dense by 3 % to count as a win
 THRESHOLDS_FILE = os.path.join(ROOT, "calibration", "fc_sweep_thresholds.json")
 # model stacks: name -> (layer table builder (stacks module), dtype name)
-STACKS = {"resnet50_b32_bf16": ("resnet50", 32, "bf16"),
+STACKS = {"resnet50_b1_bf16": ("resnet50", 1, "bf16"),
+          "resnet50_b32_bf16": ("resnet50", 32, "bf16"),
           "mobilenet_v2_b32_fp16": ("mobilenet_v2", 32, "f16"),
           "ffn12_2048x768_fp16": ("ffn", None, "f16")}
 

@@ -12,6 +12,7 @@ namespace sparoa {
 // Words of the grouped count commit: kOmGroups groups x 2 counters, one
 // 128-byte line each.
 constexpr int kOmGroups = 8;
+constexpr int kOmDirectMax = 64;   // grids up to this many work-groups commit directly
 static_assert(2 * kOmGroups * 128 == SPAROA_COMMIT_WORDS_BYTES, "commit word layout");
 
 // Adds a work-group's zero count and nonzero-block count into counts
@@ -21,8 +22,9 @@ static_assert(2 * kOmGroups * 128 == SPAROA_COMMIT_WORDS_BYTES, "commit word lay
 // a member of group b % kOmGroups: each member adds (1 << 40) + its count to
 // its group's word with one returning atomic, and the member whose add
 // completes the group adds the group's total to counts and clears the word
-// for the next call.  Without `words`: one atomic per counter per
-// work-group.
+// for the next call.  Without `words`, or for a grid of at most
+// kOmDirectMax work-groups: one atomic per counter per work-group (the words
+// are left untouched).
 __device__ __forceinline__ void om_commit(uint32_t zeros, uint32_t nz, sparoa_counts *counts,
                                           unsigned long long *words, int64_t b, int64_t nwg) {
   __shared__ uint32_t part[2][16];
@@ -43,7 +45,11 @@ __device__ __forceinline__ void om_commit(uint32_t zeros, uint32_t nz, sparoa_co
       z += part[0][i];
       n += part[1][i];
     }
-    if (!words) {
+    // small grids commit directly: the ticket's returning atomic is a memory
+    // round trip on every work-group's path (about 1 us), more than up to 64
+    // work-groups' serialised same-address atomics (measured: 64 work-groups
+    // 1 us faster direct, 98 work-groups 0.25 us slower)
+    if (!words || nwg <= kOmDirectMax) {
       if (z) atomicAdd((unsigned long long *)&counts->zeros, z);
       if (n) atomicAdd((unsigned long long *)&counts->zero_blocks, 0ull - n);
       return;
