@@ -1609,6 +1609,10 @@ GemmTileChoice ig_choose(const Shape &s, int64_t c_in) {
     if (split > 8) split = 8;
     if (split > nchunks / 4) split = nchunks / 4;
     if (split < 1) split = 1;
+    // the reduction is a launch of its own (about 6 us on small outputs):
+    // split only where the chunks it takes off a tile's walk (about 0.3 us
+    // each on these under-filled grids) are worth more
+    if (split > 1 && nchunks * (split - 1) < 20 * split) split = 1;
   }
   t.split_k = (int)split;
   return t;

@@ -247,7 +247,8 @@ IG_SHAPES = [
     ((4, 64, 128, 128, 64, 3, 3, 1, 1, 1, 1, 1, 1, 1), 128),   # 128 x 64, N = 64
     ((2, 64, 127, 129, 64, 3, 3, 1, 1, 1, 1, 1, 1, 1), 128),   # 128 x 64, ragged M
     ((1, 128, 32, 64, 1024, 1, 1, 1, 1, 0, 0, 1, 1, 1), 128),  # 128 x 64, wide N
-    ((2, 128, 9, 9, 96, 3, 3, 2, 2, 1, 1, 1, 1, 1), 64),       # 64 x 64, split-K
+    ((2, 256, 9, 9, 96, 3, 3, 2, 2, 1, 1, 1, 1, 1), 64),       # 64 x 64, split-K
+    ((2, 128, 9, 9, 96, 3, 3, 2, 2, 1, 1, 1, 1, 1), 64),       # 64 x 64, too few chunks to split
     ((1, 192, 7, 7, 36, 3, 3, 1, 1, 1, 1, 1, 1, 1), 64),       # 64 x 64, N % 8 != 0
     # C_in % 64 != 0: a tap's last chunk is partial
     ((2, 96, 14, 14, 576, 1, 1, 1, 1, 0, 0, 1, 1, 1), 64),     # 1x1, 96 = 64 + 32

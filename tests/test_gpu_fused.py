@@ -37,8 +37,9 @@ CONV_CASES = [
     # n, cin, h, w, cout, k, s, dtype; comment: which form runs
     (8, 64, 32, 32, 128, 3, 1, "bf16"),    # fused epilogue, 64 x 64 tiles, no split
     (4, 64, 32, 32, 64, 1, 1, "f16"),      # fused epilogue, 128 x 64 tiles
-    (1, 128, 14, 14, 128, 3, 1, "bf16"),   # split-K: fused reduction
-    (3, 64, 15, 13, 64, 3, 2, "f16"),      # ragged rows, split-K
+    (1, 256, 14, 14, 128, 3, 1, "bf16"),   # split-K: fused reduction
+    (1, 128, 14, 14, 128, 3, 1, "bf16"),   # too few chunks to split: fused epilogue
+    (3, 192, 15, 13, 64, 3, 2, "f16"),     # ragged rows, split-K
     (15, 64, 29, 31, 64, 3, 1, "bf16"),    # ragged rows in the last tile, no split
     (13, 64, 59, 61, 256, 3, 1, "bf16"),   # 128 x 128 tiles, ragged rows (732 tiles)
     (4, 128, 57, 55, 512, 1, 1, "bf16"),   # 128 x 256 tiles (1x1), ragged rows (196 tiles)
@@ -51,7 +52,8 @@ CONV_CASES = [
     (2, 160, 7, 7, 960, 1, 1, "f16"),      # partial chunks, 160 = 2 x 64 + 32
     (1, 160, 7, 7, 192, 3, 1, "bf16"),     # partial chunks, split-K: fused reduction
     (1, 160, 7, 7, 96, 3, 1, "bf16"),      # c_out % 64 != 0, split-K: the reduction measures
-    (32, 960, 7, 7, 160, 1, 1, "f16"),     # MobileNetV2 project-like: split-K, c_out = 160
+    (8, 1920, 7, 7, 160, 1, 1, "f16"),     # c_out = 160, split-K: the reduction measures
+    (32, 960, 7, 7, 160, 1, 1, "f16"),     # MobileNetV2 project (c_out = 160, no split): standalone
     (3, 72, 17, 15, 128, 3, 1, "bf16"),    # partial chunks per tap of a 3x3 kernel
     (2, 64, 16, 16, 64, 3, 1, "f32"),      # fp32: standalone pass
 ]

@@ -25,8 +25,8 @@ def _abi():
 # n, cin, h, w, cout, k, stride, dtype, skip: largest first, every one split-K
 CALLS = [
     (1, 64, 56, 56, 64, 3, 1, "f32", False),     # the single 3x3 conv workload
-    (1, 128, 14, 14, 128, 3, 1, "bf16", True),
-    (1, 64, 8, 8, 64, 3, 1, "bf16", False),
+    (1, 256, 14, 14, 128, 3, 1, "bf16", True),
+    (1, 256, 7, 7, 64, 3, 1, "bf16", False),
 ]
 
 
