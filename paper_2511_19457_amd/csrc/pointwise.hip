@@ -330,6 +330,12 @@ bool pw_choose(const sparoa_conv_desc &d, PwChoice *c) {
   const int64_t ho = (d.h - 1) / d.sh + 1, wo = (d.w - 1) / d.sw + 1;
   const int64_t M = d.n * ho * wo;
   if (M >= ((int64_t)1 << 24) || d.n * d.h * d.w * d.c_in * 2 >= ((int64_t)1 << 31)) return false;
+  // below 32768 pixels the layer is latency-bound and the implicit GEMM's
+  // tiles finish sooner wherever it takes the channel count and there are
+  // 64 output channels or more (ResNet-50 stage 1 at N = 1, 64 -> 256: 4.8
+  // vs 8.8 us; N = 8, 64 -> 64: 5.7 vs 7.6 us); from 100352 pixels the
+  // pointwise kernel wins (N = 32, 64 -> 256: 26 vs 36 us)
+  if (M < 32768 && d.c_out >= 64 && (d.c_in % 64 == 0 || d.c_in >= 48)) return false;
   const int ks = (int)cdiv(d.c_in, 32);
   // instantiated k-step counts; LDS rows hold all of them (zero past K)
   const int ksi = ks <= 2 ? ks : (ks <= 4 ? 4 : 8);

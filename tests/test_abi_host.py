@@ -208,7 +208,7 @@ def test_reads_mask_queries():
     c3 = abi.conv_desc(2, 64, 14, 14, 64, 3, 3, 1, 1, 1, 1)
     assert abi.sparoa_conv2d_reads_mask(c3, abi.PATH_SKIP_MFMA)
     assert not abi.sparoa_conv2d_reads_mask(c3, abi.PATH_DENSE_MFMA)
-    pw = abi.conv_desc(2, 64, 56, 56, 96, 1, 1)          # the pointwise kernel on the BW path
+    pw = abi.conv_desc(11, 64, 56, 56, 96, 1, 1)         # the pointwise kernel on the BW path
     assert abi.sparoa_conv2d_tiling(pw, abi.PATH_SKIP_BW) == (16, 32)
     assert not abi.sparoa_conv2d_reads_mask(pw, abi.PATH_SKIP_BW)
     assert abi.sparoa_conv2d_reads_mask(pw, abi.PATH_SKIP_MFMA)

@@ -27,17 +27,29 @@ def _abi():
 MBV2 = [(32, 16, 112, 1, False), (16, 96, 112, 1, False), (96, 24, 56, 1, False),
         (24, 144, 56, 1, False), (144, 24, 56, 1, True), (144, 32, 28, 1, False),
         (32, 192, 28, 1, False), (192, 32, 28, 1, True)]
-# 1x1 convs of ResNet-50 widths it serves (bandwidth-routed at the bf16 ridge)
+# 1x1 convs of ResNet-50 widths it serves (bandwidth-routed at the bf16 ridge;
+# with 64 output channels or more only from 32768 pixels: below, the implicit
+# GEMM serves them)
 R50 = [(64, 64, 56, 1, False), (64, 256, 56, 1, True), (128, 32, 56, 1, False)]
+
+
+def _batch(cin, cout, h, s, small):
+    """A batch the pointwise kernel serves: `small` images, or enough for
+    32768 output pixels where the implicit GEMM would take fewer."""
+    ho = (h - 1) // s + 1
+    if cout >= 64 and (cin % 64 == 0 or cin >= 48):
+        return max(small, -(-32768 // (ho * ho)))
+    return small
 
 
 def test_shapes_beyond_the_kernel_run_the_implicit_gemm():
     abi = _abi()
-    # (weights beyond four LDS slices, K > 256, or several slices over few
-    # pixels)
+    # (weights beyond four LDS slices, K > 256, several slices over few
+    # pixels, or fewer than 32768 pixels with 64 output channels or more)
     for cin, cout, h, s in ((160, 960, 7, 1), (256, 512, 56, 2), (384, 64, 14, 1),
                             (96, 576, 14, 1), (64, 384, 14, 1), (128, 512, 28, 1),
-                            (192, 64, 14, 1), (256, 64, 56, 1)):
+                            (192, 64, 14, 1), (256, 64, 56, 1), (64, 256, 56, 1),
+                            (64, 64, 56, 1), (128, 128, 28, 1)):
         d = abi.conv_desc(2, cin, h, h, cout, 1, 1, s, s, 0, 0, 1, 1, 1, torch.bfloat16)
         assert abi.sparoa_conv2d_tiling(d, abi.PATH_DENSE_BW) != (16, 32)
 
@@ -60,7 +72,7 @@ def test_pointwise_vs_oracle(shape):
     dev = torch.device("cuda")
     cin, cout, h, s, with_res = shape
     dt = "f16" if shape in MBV2 else "bf16"
-    n = 2 if h >= 56 else 3
+    n = _batch(cin, cout, h, s, 2 if h >= 56 else 3)
     seed = 2100 + 10 * (MBV2 + R50).index(shape)
     act = abi.ACT_RELU6 if dt == "f16" else abi.ACT_RELU
     d, tdt, ho, x, w, r, yr, ar = _case(abi, dev, cin, cout, h, s, with_res, dt, n, seed, act)
@@ -101,6 +113,7 @@ def test_pointwise_routed_measured(shape, n):
     abi = _abi()
     dev = torch.device("cuda")
     cin, cout, h, s, with_res = shape
+    n = _batch(cin, cout, h, s, n)
     seed = 2400 + 10 * cin + cout
     d, tdt, ho, x, w, r, yr, ar = _case(abi, dev, cin, cout, h, s, with_res, "bf16", n, seed,
                                         abi.ACT_RELU)
@@ -136,11 +149,13 @@ def test_pointwise_routed_measured(shape, n):
 
 
 def test_fc_over_many_rows_on_the_bandwidth_path():
-    """An FC with m > 64 on the bandwidth path is the 1x1 conv over m pixels
-    and runs the pointwise kernel (w in [n][k])."""
+    """An FC with many rows (32768 or more: below, the implicit GEMM serves
+    it) on the bandwidth path is the 1x1 conv over m pixels and runs the
+    pointwise kernel (w in [n][k])."""
     abi = _abi()
     dev = torch.device("cuda")
-    m, k, n = 1000, 128, 96
+    m, k, n = 33000, 128, 96
+    assert abi.sparoa_fc_tiling(abi.fc_desc(1000, k, n, abi.BF16), abi.PATH_DENSE_BW) != (16, 32)
     d = abi.fc_desc(m, k, n, abi.BF16)
     assert not abi.sparoa_fc_uses_packed(d, abi.PATH_DENSE_BW)
     assert abi.sparoa_fc_tiling(d, abi.PATH_DENSE_BW) == (16, 32)
