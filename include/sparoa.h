@@ -205,7 +205,10 @@ sparoa_status sparoa_route(const sparoa_counts *counts, const sparoa_intensity *
  *                                   at most four 48 KB slices, several slices
  *                                   only over >= 32768 output pixels, and not
  *                                   c_in >= 192 with c_in % 64 == 0 and
- *                                   c_out >= 64) the pointwise kernel: the
+ *                                   c_out >= 64, nor below 32768 output
+ *                                   pixels with c_out >= 64 where the
+ *                                   implicit GEMM takes c_in: those are
+ *                                   latency-bound) the pointwise kernel: the
  *                                   weights stay in LDS and each activation is
  *                                   read once per slice
  *                                   (sparoa_conv2d_tiling gives (16, 32));
