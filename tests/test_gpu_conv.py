@@ -113,6 +113,8 @@ DW_SHAPES = [
     (3, 24, 14, 13, 24, 3, 3, 2, 2, 1, 1, 1, 1, 24),   # stride 2, ragged pixel runs
     (2, 16, 5, 3, 16, 3, 3, 1, 1, 1, 1, 1, 1, 16),     # row narrower than a run
     (1, 40, 9, 9, 40, 3, 3, 1, 1, 1, 1, 2, 2, 40),     # dilation 2: general kernel
+    (2, 32, 37, 21, 32, 3, 3, 1, 1, 1, 1, 1, 1, 32),   # stride 1: ragged row and column tiles
+    (1, 88, 13, 11, 88, 3, 3, 1, 1, 1, 1, 1, 1, 88),   # 11 vectors per pixel: 1-vector tiles
 ]
 
 
